@@ -1,0 +1,243 @@
+"""Verify rounds, commit, strict truncation, AR decoding and the image driver
+(oracle, test infrastructure).
+
+Paper: Sec. 3.3 "Verification as Auto Correction".  A drafted block goes
+through the backbone in one pass; every drafted position is corrected
+independently by rule (A), (B) or (C) (see ``oracle.select``); the procedure
+repeats for a fixed number of rounds, rejected positions take the previous
+round's backbone distribution as their reference; after the last round one
+more forward pass commits the corrected block and updates the KV cache.
+Strict verification that truncates at the first mismatch is the standard
+speculative scheme the paper contrasts with; it is kept here as a mode because
+it is exact (it reproduces greedy AR decoding), which pins the forward pass.
+
+Scoring alignment (reading): block position k is scored by the backbone's
+prediction for position f+k, i.e. the logits output at block position k-1;
+position 0 is scored by the carry -- the last logits of the previous commit
+(or of the prefill).  A block may start with one fixed position (n_fixed = 1):
+a token already chosen but not yet in the cache, which is not verified.
+
+Pins: tests/test_oracle_decode.py -- truncation decoding and Jacobi-style
+greedy rounds (r >= K) both reproduce greedy AR decoding (Eq. 1 with argmax)
+token for token; the verify pass leaves the frontier unchanged and the commit
+pass advances it by K; the pass count of a decoded image equals the plan's.
+"""
+
+import numpy as np
+
+from . import model as M
+from . import schedule as S
+from . import select as R
+
+
+class Session:
+    def __init__(self, model, B, P, max_ctx):
+        self.model = model
+        self.cfg = model.cfg
+        self.B, self.P = B, P
+        self.cache = M.Cache(model.cfg, B, max_ctx)
+        self.f = np.zeros(B, dtype=np.int64)
+        self.carry = None  # (B, V_img) float64
+        self.passes = 0
+
+
+def prefill(model, prefix, max_ctx):
+    """Forward the text prefix (B, P) from position 0; the carry is the last
+    position's logits (they score the first image token)."""
+    prefix = np.asarray(prefix)
+    B, P = prefix.shape
+    s = Session(model, B, P, max_ctx)
+    logits, _ = M.forward(model, s.cache, prefix, s.f)
+    s.f[:] = P
+    s.carry = logits[:, P - 1, :].copy()
+    s.passes = 1
+    return s
+
+
+def scoring_logits(sess, logits, b, k):
+    return sess.carry[b] if k == 0 else logits[b, k - 1]
+
+
+def verify_round(sess, block, n_fixed, rule, rnd, seed=0, temperature=1.0, top_k=0, ref=None):
+    """One verify-and-correct round.
+
+    block -- (B, K) image-code indices (0-based within the image range)
+    ref   -- list over b of lists over k of reference logits (None = point mass);
+             updated in place for rule (C) rejections
+    Returns (new_block, accept (B,K) bool, count (B,), logits (B,K,V_img)).
+    The frontier does not move; the block's KV slots are overwritten.
+    """
+    cfg = sess.cfg
+    block = np.asarray(block, dtype=np.int64)
+    B, K = block.shape
+    logits, _ = M.forward(sess.model, sess.cache, block + cfg.img_lo, sess.f)
+    sess.passes += 1
+    new = block.copy()
+    acc = np.zeros((B, K), dtype=bool)
+    for b in range(B):
+        for k in range(n_fixed, K):
+            pos = int(sess.f[b]) + k
+            u0 = R.uniform(seed, b, pos, rnd, 0)
+            u1 = R.uniform(seed, b, pos, rnd, 1)
+            L = scoring_logits(sess, logits, b, k)
+            rk = None if ref is None else ref[b][k]
+            t, a, replaced = R.select_position(rule, L, int(block[b, k]), rk, u0, u1, temperature, top_k)
+            new[b, k] = t
+            acc[b, k] = a
+            if replaced and ref is not None:
+                ref[b][k] = np.array(L, dtype=np.float64)
+    return new, acc, acc[:, n_fixed:].sum(axis=1), logits
+
+
+def commit(sess, block):
+    """Commit pass: forward the final block, keep its KV, advance the frontier
+    by K and take the last position's logits as the new carry."""
+    cfg = sess.cfg
+    block = np.asarray(block, dtype=np.int64)
+    K = block.shape[1]
+    logits, h_pre = M.forward(sess.model, sess.cache, block + cfg.img_lo, sess.f)
+    sess.passes += 1
+    sess.f += K
+    sess.carry = logits[:, K - 1, :].copy()
+    return logits, h_pre
+
+
+def truncate_step(sess, block, n_fixed):
+    """Strict greedy verification (single sequence or uniform frontier per row):
+    accept the leading run of drafts equal to the argmax, then take the argmax
+    at the first mismatch (or after the block) as the pending token.
+    Returns (n_accepted (B,), pending (B,)).  The frontier advances by
+    n_fixed + n_accepted; the KV of those positions is already final."""
+    cfg = sess.cfg
+    block = np.asarray(block, dtype=np.int64)
+    B, K = block.shape
+    logits, _ = M.forward(sess.model, sess.cache, block + cfg.img_lo, sess.f)
+    sess.passes += 1
+    n_acc = np.zeros(B, dtype=np.int64)
+    pending = np.zeros(B, dtype=np.int64)
+    for b in range(B):
+        n = 0
+        k = n_fixed
+        while k < K:
+            a = R.argmax_lowest(scoring_logits(sess, logits, b, k))
+            if a != block[b, k]:
+                break
+            n += 1
+            k += 1
+        # k is the first unaccepted block position (or K)
+        pending[b] = R.argmax_lowest(logits[b, k - 1]) if k >= 1 else R.argmax_lowest(sess.carry[b])
+        n_acc[b] = n
+        sess.f[b] += n_fixed + n
+    return n_acc, pending
+
+
+def ar_decode(model, prefix, n_tokens):
+    """Greedy autoregressive decoding (Eq. 1 with argmax): one forward pass per
+    image token.  Returns (B, n_tokens) image-code indices."""
+    prefix = np.asarray(prefix)
+    B, P = prefix.shape
+    s = prefill(model, prefix, P + n_tokens)
+    out = np.zeros((B, n_tokens), dtype=np.int64)
+    for j in range(n_tokens):
+        for b in range(B):
+            out[b, j] = R.argmax_lowest(s.carry[b])
+        if j + 1 < n_tokens:
+            commit(s, out[:, j:j + 1])
+    return out
+
+
+def decode_truncate(model, prefix, drafts, K):
+    """Exact greedy speculative decoding of len(drafts[b]) image tokens per
+    sequence with blocks of K positions ([pending, K-1 drafts]); sequences are
+    decoded one at a time.  Returns (tokens (B, N), passes)."""
+    prefix = np.asarray(prefix)
+    drafts = np.asarray(drafts, dtype=np.int64)
+    B, N = drafts.shape
+    P = prefix.shape[1]
+    out = np.zeros((B, N), dtype=np.int64)
+    passes = 0
+    for b in range(B):
+        s = prefill(model, prefix[b:b + 1], P + N + K)
+        pending = R.argmax_lowest(s.carry[0])
+        done = 0  # tokens final (in cache)
+        while True:
+            out[b, done] = pending
+            if done + 1 == N:
+                break
+            k_blk = min(K, N - done)
+            blk = np.concatenate([[pending], drafts[b, done + 1:done + k_blk]])[None, :]
+            n_acc, pend = truncate_step(s, blk, 1)
+            n = int(n_acc[0])
+            out[b, done + 1:done + 1 + n] = blk[0, 1:1 + n]
+            done += 1 + n
+            pending = int(pend[0])
+            if done >= N:
+                break
+        passes += s.passes
+    return out, passes
+
+
+def decode_image(model, prefix, H, W, drafts, rule=R.RULE_GREEDY, seed=0, temperature=1.0, top_k=0,
+                 k_h=5, h_rounds=1, k_v=1, b=2, i=0, q_table=None, trace=None):
+    """Decode one image per sequence under the SSD schedule with planted drafts.
+
+    drafts  -- (B, H, W) image-code indices used as the draft of every position
+    q_table -- optional (B, H, W, V_img) draft logits (rule C reference for the
+               first round of each position); None = point masses at the drafts
+    trace   -- optional list collecting (op, accept, count, logits) per verify
+    Returns (tokens (B, H, W), stats dict).
+    """
+    cfg = model.cfg
+    prefix = np.asarray(prefix)
+    B, P = prefix.shape
+    N = H * W
+    drafts = np.asarray(drafts, dtype=np.int64).reshape(B, N)
+    ops = S.plan(H, W, k_h=k_h, h_rounds=h_rounds, k_v=k_v, b=b, i=i)
+    sess = None
+    work = drafts.copy()
+    refs = [dict() for _ in range(B)]  # image index -> reference logits
+    stats = {"accepted": 0, "proposed": 0, "verify_rounds": 0}
+    for op in ops:
+        if op[0] == "prefill":
+            sess = prefill(model, prefix, P + N)
+        elif op[0] == "first":
+            for bb in range(B):
+                u1 = R.uniform(seed, bb, P, 0, 2)
+                work[bb, 0] = R.sample_first(rule, sess.carry[bb], u1, temperature, top_k)
+        elif op[0] == "verify":
+            _, start, K, nf, rnd = op
+            assert int(sess.f[0]) == P + start
+            ref = None
+            if rule == R.RULE_ACCEPT_REJECT:
+                ref = []
+                for bb in range(B):
+                    row = []
+                    for k in range(K):
+                        idx = start + k
+                        if idx not in refs[bb]:
+                            refs[bb][idx] = None if q_table is None else \
+                                np.asarray(q_table[bb].reshape(N, -1)[idx], np.float64)
+                        row.append(refs[bb][idx])
+                    ref.append(row)
+            blk = work[:, start:start + K]
+            new, acc, cnt, logits = verify_round(sess, blk, nf, rule, rnd, seed, temperature, top_k, ref)
+            if ref is not None:
+                for bb in range(B):
+                    for k in range(K):
+                        refs[bb][start + k] = ref[bb][k]
+            work[:, start:start + K] = new
+            stats["accepted"] += int(cnt.sum())
+            stats["proposed"] += B * (K - nf)
+            stats["verify_rounds"] += 1
+            if trace is not None:
+                trace.append((op, acc, cnt, logits, new))
+        elif op[0] == "commit":
+            _, start, K = op
+            assert int(sess.f[0]) == P + start
+            commit(sess, work[:, start:start + K])
+            for bb in range(B):
+                for k in range(K):
+                    refs[bb].pop(start + k, None)
+    stats["passes"] = sess.passes
+    assert sess.passes == S.n_passes(ops)
+    return work.reshape(B, H, W), stats
