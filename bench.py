@@ -1,0 +1,207 @@
+#!/usr/bin/env python3
+"""Image tokens/s of SSD decoding on one MI355X (gfx950).
+
+A step is one ssd_decode_image call: the whole SSD schedule of one batch of
+images (prefix prefill, horizontal runs of 5 tokens with one verify round
+each, then every row verified r times and committed), i.e. every verify
+pass of the image through the library's HIP kernels.  Inputs (prompt ids and
+planted drafts) are resident in device memory before the timed region.
+
+Workload (default): the 1B-class bf16 decoder (24 layers, d=2048, 16x128
+heads, MLP 5632, 16384 image codes), 64-token random prompt, 24x24 grid,
+batch 1, greedy rule, r = 2, drafts planted from the backbone's own greedy
+AR image with keep-probability 0.6.  Weights N(0, 0.02) from seed 0.
+
+Prints one JSON line (rank 0).  Extra keys: `roofline` (the weight-streaming
+GEMM kernel, HIP events around every launch in the timed region),
+`attention` (the same for the attention kernel), `cpu_baseline` (the oracle
+on the host cores on a bounded sample), AR tokens/s on the same kernels.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def cfg_of(ssd, shape):
+    c = ssd.ssd_model_config()
+    c.n_layers, c.d_model, c.n_heads, c.n_kv_heads = shape.n_layers, shape.d_model, shape.n_heads, shape.n_kv_heads
+    c.head_dim, c.d_ff, c.vocab = shape.head_dim, shape.d_ff, shape.vocab
+    c.img_lo, c.img_hi = shape.img_lo, shape.img_hi
+    c.dtype = ssd.SSD_BF16 if shape.dtype == "bf16" else ssd.SSD_F32
+    c.rms_eps, c.rope_theta = 1e-5, 10000.0
+    return c
+
+
+def gpu_greedy_ar(ssd, model, shape, prefix, n):
+    """Greedy AR decoding through the ABI: one commit pass per token."""
+    B, P = prefix.shape
+    sess = ssd.ssd_prefill(model, B, P, prefix, P + n + 1, 1)
+    out = np.zeros((B, n), np.int64)
+    carry = np.zeros((B, shape.v_img), np.float32)
+    prm = ssd.ssd_verify_params()
+    prm.rule, prm.temperature, prm.commit = ssd.SSD_GREEDY, 1.0, 1
+    tok = np.zeros((B, 1), np.int32)
+    t0 = time.perf_counter()
+    for j in range(n):
+        ssd.ssd_get_carry(sess, carry)
+        out[:, j] = carry.argmax(axis=1)
+        if j + 1 < n:
+            tok[:, 0] = out[:, j] + shape.img_lo
+            ssd.ssd_verify_step(sess, 1, tok, prm)
+    dt = time.perf_counter() - t0
+    ssd.ssd_free_session(sess)
+    return out, dt
+
+
+def cpu_baseline(wl, w, prefix, drafts):
+    """The oracle (numpy float64) on the host cores, on prefix + the first two rows."""
+    from oracle import decode as Dc
+    from oracle import model as M
+    shape = wl.model
+    om = M.Model(M.Config(shape.n_layers, shape.d_model, shape.n_heads, shape.n_kv_heads, shape.head_dim,
+                          shape.d_ff, shape.vocab, shape.img_lo, shape.img_hi, shape.dtype), w)
+    rows = 2
+    t0 = time.perf_counter()
+    tok, st = Dc.decode_image(om, prefix, rows, wl.grid, drafts[:, :rows, :], rule=wl.rule, seed=3,
+                              top_k=wl.top_k, b=wl.rounds)
+    dt = time.perf_counter() - t0
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        cores = os.cpu_count()
+    n_tok = prefix.shape[0] * rows * wl.grid
+    return {"value": n_tok / dt, "unit": "image tokens/s", "cores": int(cores), "kind": "oracle",
+            "sample": f"prefill + rows 0-{rows - 1} of the {wl.grid}x{wl.grid} image ({st['passes']} passes, "
+                      f"batch {prefix.shape[0]}, {n_tok} tokens) in {dt:.1f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", default="1b-24x24")
+    ap.add_argument("--accept-p", type=float, default=None)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-ar", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py: this build runs on exactly one GPU (asked for {args.gpus}); the verify path "
+              "shards by independent images, see DESIGN.md", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2606_20543_amd as ssd
+    import synth
+
+    wl = synth.WORKLOADS[args.workload]
+    shape = wl.model
+    B, P, H = wl.batch, wl.prefix, wl.grid
+    W = H
+    p_keep = args.accept_p if args.accept_p is not None else wl.accept_p[len(wl.accept_p) // 2]
+    log(f"[bench] workload {wl.name}: generating weights")
+    w = synth.weights(shape)
+    cfg = cfg_of(ssd, shape)
+    model = ssd.ssd_init_model(cfg, w)
+    prefix = synth.prompt(shape, B, P)
+
+    ar_rate = None
+    if not args.no_ar:
+        log("[bench] greedy AR on the GPU (plants the drafts)")
+        ar, ar_dt = gpu_greedy_ar(ssd, model, shape, prefix, H * W)
+        ar_rate = B * H * W / ar_dt
+        target = ar.reshape(B, H, W)
+    else:
+        target = synth.random_codes(shape, (B, H, W))
+    drafts = synth.plant(target, p_keep, shape.v_img)
+
+    dev = torch.device("cuda:0")
+    d_prefix = torch.from_numpy(prefix.astype(np.int32)).to(dev)
+    d_drafts = torch.from_numpy((drafts + shape.img_lo).astype(np.int32)).to(dev)
+    d_out = torch.zeros((B, H, W), dtype=torch.int32, device=dev)
+    sc = ssd.ssd_schedule()
+    sc.grid_h, sc.grid_w, sc.k_h, sc.h_rounds, sc.k_v, sc.b_rounds, sc.i_rounds = H, W, 5, 1, 1, wl.rounds, 0
+    sc.rule, sc.top_k, sc.temperature, sc.seed = wl.rule, wl.top_k, wl.temperature, synth.SEED_SAMPLING
+
+    for i in range(args.warmup):
+        ssd.ssd_decode_image(model, sc, B, P, d_prefix, d_drafts, d_out)
+        log(f"[bench] warmup {i + 1}/{args.warmup} done")
+    torch.cuda.synchronize()
+    ssd.ssd_profile(model, 1)
+    ssd.ssd_profile_read(model, reset=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    stats = None
+    for i in range(args.steps):
+        stats = ssd.ssd_decode_image(model, sc, B, P, d_prefix, d_drafts, d_out)
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    prof = ssd.ssd_profile_read(model, reset=True)
+    ssd.ssd_profile(model, 0)
+    log(f"[bench] timed {args.steps} steps in {dt:.3f} s")
+
+    ms_step = dt * 1000.0 / args.steps
+    value = B * H * W / (dt / args.steps)
+    gemm = [prof[c] for c in ("qkv", "o_proj", "gate_up", "down", "lm_head")]
+    g_ms = sum(x[0] for x in gemm)
+    g_n = sum(x[1] for x in gemm)
+    g_bytes = sum(x[2] for x in gemm)
+    g_gbs = g_bytes / (g_ms / 1000.0) / 1e9
+    a_ms, a_n, a_bytes = prof["attention"]
+    a_gbs = a_bytes / (a_ms / 1000.0) / 1e9 if a_ms > 0 else 0.0
+    per_class = {c: {"ms_per_launch": prof[c][0] / max(prof[c][1], 1), "launches": prof[c][1],
+                     "GB_per_s": prof[c][2] / (prof[c][0] / 1000.0) / 1e9 if prof[c][0] > 0 else None}
+                 for c in prof}
+    acc = stats.accepted / max(stats.proposed, 1)
+
+    result = {
+        "metric": "image tokens/sec (1 GPU) at fixed acceptance; verify-step HBM GB/s % of peak",
+        "value": value,
+        "unit": "image tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": shape.dtype,
+        "data": "synthetic (random N(0,0.02) weights, random prompt ids, planted drafts)",
+        "config": {"workload": wl.name, "batch": B, "prefix": P, "grid": f"{H}x{W}", "rule": wl.rule,
+                   "rounds": wl.rounds, "k_h": 5, "k_v": 1, "top_k": wl.top_k, "planted_keep_p": p_keep,
+                   "passes_per_image": stats.passes, "parallelism": "single GPU"},
+        "roofline": {"bound": "hbm", "kernel": "gemm_bf16_kernel (QKV/O/gate-up/down/LM-head weight streaming)",
+                     "achieved": g_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": g_gbs / HBM_PEAK_GBS,
+                     "traffic": None, "launches": g_n, "ms_per_launch": g_ms / max(g_n, 1),
+                     "bytes_per_launch": g_bytes / max(g_n, 1)},
+        "attention": {"bound": "hbm", "achieved": a_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                      "frac": a_gbs / HBM_PEAK_GBS, "launches": a_n, "ms_per_launch": a_ms / max(a_n, 1)},
+        "kernel_classes": per_class,
+        "acceptance": acc,
+        "verify_ms_per_pass": ms_step / stats.passes,
+        "ar_tokens_per_s_same_kernels": ar_rate,
+        "speedup_vs_ar_same_kernels": (value / ar_rate) if ar_rate else None,
+    }
+    if not args.no_cpu_baseline:
+        log("[bench] timing the oracle on the host cores")
+        result["cpu_baseline"] = cpu_baseline(wl, w, prefix, drafts)
+    print(json.dumps(result), flush=True)
+    ssd.ssd_free_model(model)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,230 @@
+/*
+ * ssd.h -- C ABI of the MI355X (gfx950) implementation of the batched verify
+ * step of Spatially Speculative Decoding (SSD).
+ *
+ * The problem (paper Sec. 3.1, Eq. 1): a frozen decoder-only transformer
+ * generates an n x n grid of image-code tokens in raster order after a text
+ * prefix, one token per forward pass.  SSD (Sec. 3.3) drafts whole blocks of
+ * spatially adjacent tokens -- the rest of the current row in runs of k_h
+ * horizontal tokens, then k_v complete rows below -- and verifies a block in
+ * ONE backbone forward pass ("Verification as Auto Correction"): every drafted
+ * position is corrected independently by (A) greedy argmax, (B) sampling, or
+ * (C) acceptance-rejection with the residual distribution, for a fixed number
+ * of rounds; a final forward pass commits the corrected block to the KV cache.
+ *
+ * Conventions for every entry point:
+ *  - Return value: SSD_OK (0) or a negative ssd_status.  On error nothing has
+ *    been launched and the session/model is unchanged, except SSD_E_DEVICE,
+ *    which marks the object unusable.  ssd_last_error() returns a
+ *    thread-local message describing the last failure.
+ *  - Pointers to arrays may be host or device memory (HIP unified addressing
+ *    decides).  Work is enqueued on the object's HIP stream; when any output
+ *    array is host memory the call synchronizes the stream before returning,
+ *    otherwise it returns without synchronizing.
+ *  - The caller owns every array it passes; the library owns the device
+ *    weights, the KV cache and all workspaces of a model/session.
+ *  - Token ids are vocabulary ids.  Image codes occupy [img_lo, img_hi);
+ *    every block (draft) token must lie in that range.  Logits cover only the
+ *    image range, in code order.
+ *  - Sessions are not thread-safe; distinct sessions on distinct streams are.
+ *  - Nothing here allocates pinned host memory or changes stream priorities.
+ */
+#ifndef SSD_H
+#define SSD_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  SSD_OK = 0,
+  SSD_E_INVAL = -1,    /* bad argument (null pointer, shape, id out of range) */
+  SSD_E_STATE = -2,    /* call not allowed in the object's current state */
+  SSD_E_CAPACITY = -3, /* block would run past the session's max context */
+  SSD_E_OOM = -4,      /* device allocation failed */
+  SSD_E_DEVICE = -5    /* a HIP call failed; the object is poisoned */
+} ssd_status;
+
+typedef enum { SSD_F32 = 0, SSD_BF16 = 1 } ssd_dtype;
+
+/* Correction rules of Sec. 3.3 "Verification as Auto Correction". */
+typedef enum {
+  SSD_GREEDY = 0,        /* (A) argmax of p_k (ties: lowest id)                  */
+  SSD_SAMPLE = 1,        /* (B) a sample of p_k                                  */
+  SSD_ACCEPT_REJECT = 2  /* (C) keep t with prob min(p/q,1), else [p-q]_+ sample */
+} ssd_rule;
+
+/*
+ * Backbone shape.  A standard pre-norm decoder (the paper's backbones are
+ * used unmodified, Sec. 3.3): RMSNorm, grouped-query causal attention with
+ * rotary embedding over raster positions (rotate-half pairs, base rope_theta),
+ * SwiGLU MLP W2(silu(W1 z) * W3 z) (the form Eq. 2 writes out), final RMSNorm
+ * and an output layer ("GenHead") restricted to the image codes.
+ * n_heads must be a multiple of n_kv_heads; head_dim must be even.
+ * bf16 models: d_model, head_dim, d_ff and img_hi-img_lo must be multiples
+ * of 32 and head_dim a multiple of 16.
+ */
+typedef struct {
+  int32_t n_layers, d_model, n_heads, n_kv_heads, head_dim, d_ff, vocab;
+  int32_t img_lo, img_hi; /* image-code id range [img_lo, img_hi) */
+  int32_t dtype;          /* ssd_dtype of weights and KV cache */
+  float rms_eps;          /* RMSNorm epsilon (1e-5 in the synthetic models) */
+  float rope_theta;       /* rotary base (1e4 in the synthetic models) */
+} ssd_model_config;
+
+typedef struct ssd_model ssd_model;
+typedef struct ssd_session ssd_session;
+
+/*
+ * Upload a model.  `weights` is one packed buffer of elements of the model
+ * dtype (bf16 bit patterns as uint16, or float32) holding, in this order and
+ * row-major:
+ *   tok_emb [vocab][d]
+ *   for each layer: attn_norm [d], wq [Hq*D][d], wk [Hkv*D][d], wv [Hkv*D][d],
+ *                   wo [d][Hq*D], mlp_norm [d], w1 [d_ff][d] (gate),
+ *                   w3 [d_ff][d] (up), w2 [d][d_ff]
+ *   final_norm [d], lm_head [vocab][d]
+ * (a linear layer W maps y = W x).  The buffer may be host or device memory
+ * and is only read during the call; the library repacks the weights into its
+ * own device layout.  `stream` is a hipStream_t (NULL = default stream).
+ */
+ssd_status ssd_init_model(const ssd_model_config* cfg, const void* weights, void* stream, ssd_model** out);
+
+/* Number of elements the packed weight buffer of `cfg` must hold. */
+int64_t ssd_weights_numel(const ssd_model_config* cfg);
+
+void ssd_free_model(ssd_model* model);
+
+/*
+ * Create a session of B sequences and run the prefix ("prefill") pass
+ * (Eq. 1's condition c): prefix [B][P] vocabulary ids.  Afterwards every
+ * sequence's frontier is f = P and its carry (the logits that score the next
+ * position) is the prefix's last logits.  max_ctx bounds P + all committed
+ * and drafted positions; max_block bounds the block length K of later
+ * verify steps.  The KV cache of max_ctx positions is allocated here.
+ */
+ssd_status ssd_prefill(ssd_model* model, int32_t B, int32_t P, const int32_t* prefix, int32_t max_ctx,
+                       int32_t max_block, void* stream, ssd_session** out);
+
+void ssd_free_session(ssd_session* sess);
+
+typedef struct {
+  int32_t rule;        /* ssd_rule */
+  int32_t top_k;       /* keep the top_k codes of p and q (<= 0: all); boundary ties keep lower ids */
+  double temperature;  /* p = softmax(top_k(logits / temperature)); same warp for q */
+  uint64_t seed;       /* key of the counter-based uniforms */
+  uint32_t round;      /* verify-round index, part of the uniform's counter */
+  int32_t n_fixed;     /* 0 or 1: leading block positions that are already chosen (not verified) */
+  int32_t commit;      /* 0: verify-and-correct round; 1: commit pass */
+  int32_t truncate;    /* 1: strict greedy verification (exact speculative decoding) */
+} ssd_verify_params;
+
+/*
+ * One backbone forward pass over a block of K tokens per sequence at
+ * positions [f, f+K) of every sequence, under the ordinary causal mask over
+ * raster positions (position f+k sees the cache [0, f) and block positions
+ * 0..k), followed by the per-position correction (Sec. 3.3).
+ *
+ * tokens      [B][K] in: current block tokens (drafts or last round's result);
+ *             out (verify round): corrected tokens.  Image codes only.
+ * ref_logits  [B][K][V_img] or NULL.  Rule (C)'s reference distribution q
+ *             (as logits, warped like p).  Non-NULL replaces the stored
+ *             reference of every block position; NULL keeps the stored one,
+ *             and a position without one uses a point mass at its token.
+ * params      see ssd_verify_params.
+ * accept_mask [B][K] or NULL: 1 where the position kept its token.
+ * accept_count[B] or NULL: accepted positions per sequence.
+ * frontier    [B] or NULL: the frontier f after the call.
+ * logits_out  [B][K][V_img] or NULL: the pass's logits (position k predicts f+k+1).
+ * h_pre_out   [B][K][d] or NULL: last layer hidden state before the final norm.
+ *
+ * Scoring: block position k is scored by the logits of position k-1, and
+ * position 0 by the session's carry.  Positions k < n_fixed are not scored.
+ * Verify round (commit = 0): KV slots [f, f+K) are overwritten, f is
+ * unchanged; rule (C) rejections store this round's scoring logits as the
+ * position's new reference (Sec. 3.3: the previous-round backbone
+ * distribution becomes the reference).
+ * Commit pass (commit = 1): no correction; the KV slots become final,
+ * f += K, the carry becomes the logits of position K-1 and the stored
+ * references of the committed positions are dropped.
+ * Truncate (truncate = 1, rule (A)): the leading run of positions whose token
+ * equals the argmax is accepted, f advances past them (plus the n_fixed
+ * positions), and tokens[b][f_new - f_old] receives the argmax at the first
+ * mismatch (or after the block): the next block's fixed first token.
+ * Errors: SSD_E_INVAL for bad shapes/ids, SSD_E_CAPACITY if f+K > max_ctx,
+ * SSD_E_STATE after a device failure.
+ * The uniforms of position k are SplitMix64 outputs at the counter
+ * (b << 44) | ((f+k) << 20) | (round << 4) | stream, stream 0 = accept test,
+ * 1 = sample.
+ */
+ssd_status ssd_verify_step(ssd_session* sess, int32_t K, int32_t* tokens, const float* ref_logits,
+                           const ssd_verify_params* params, uint8_t* accept_mask, int32_t* accept_count,
+                           int32_t* frontier, float* logits_out, float* h_pre_out);
+
+/* Copy the current carry logits [B][V_img] (scores of position f). */
+ssd_status ssd_get_carry(ssd_session* sess, float* carry_out);
+
+/*
+ * SSD image schedule (Sec. 3.3; Sec. 4 "SSD Configuration"; Appendix
+ * "Multi-Row Anticipation Ablations"): the prefix prefill, the first image
+ * token from the prefill's carry (argmax for rule A, else a sample of the
+ * warped carry with uniform stream 2 at round 0), the rest of row 0 in runs
+ * of k_h tokens with h_rounds verify rounds each (the first run also carries
+ * the first token as a fixed position), then the remaining rows in groups of
+ * k_v: b_rounds joint rounds on the group, commit of its leading row, and for
+ * each later row of the group i_rounds rounds on the group's uncommitted rows
+ * followed by that row's commit.  The verify-round index grows over the whole
+ * image.  Passes = 1 + 2*ceil((W-1)/k_h) + sum over groups of m rows of
+ * (b + i*(m-1) + m) for h_rounds = 1.
+ */
+typedef struct {
+  int32_t grid_h, grid_w;
+  int32_t k_h, h_rounds, k_v, b_rounds, i_rounds;
+  int32_t rule, top_k;
+  double temperature;
+  uint64_t seed;
+} ssd_schedule;
+
+typedef struct {
+  int64_t passes;        /* backbone forward passes, prefill included */
+  int64_t verify_rounds; /* verify passes */
+  int64_t accepted;      /* accepted positions summed over verify rounds and sequences */
+  int64_t proposed;      /* verified positions summed over verify rounds and sequences */
+} ssd_stats;
+
+/*
+ * Decode B images: prefix [B][P]; drafts [B][H][W] image-code ids used as
+ * the draft of every position (planted drafts); draft_logits
+ * [B][H][W][V_img] or NULL (rule C reference for a position's first round,
+ * NULL = point masses); out_tokens [B][H][W].  stats may be NULL.
+ * The model keeps one decode workspace (KV cache for P + H*W positions)
+ * between calls with the same shape.
+ */
+ssd_status ssd_decode_image(ssd_model* model, const ssd_schedule* sched, int32_t B, int32_t P,
+                            const int32_t* prefix, const int32_t* drafts, const float* draft_logits,
+                            int32_t* out_tokens, ssd_stats* stats, void* stream);
+
+/*
+ * Measurement hook.  enable = 1 starts recording a HIP event pair around every
+ * projection-GEMM and attention launch of the model's forward passes (on the
+ * stream they run on); enable = 0 stops.  ssd_profile_read fills
+ * ms[c] = summed kernel time and launches[c] = launch count per class
+ * c = 0 QKV, 1 O-proj, 2 gate/up, 3 down, 4 LM head, 5 attention, and
+ * bytes[c] = algorithmic HBM bytes of those launches (weights + activations
+ * read + outputs written, KV read/written for attention); reset = 1 clears
+ * the totals afterwards.  Arrays have 6 entries; any may be NULL.
+ * Synchronizes the model's stream.
+ */
+ssd_status ssd_profile(ssd_model* model, int32_t enable);
+ssd_status ssd_profile_read(ssd_model* model, double* ms, int64_t* launches, double* bytes, int32_t reset);
+
+/* Thread-local description of the last error (empty string if none). */
+const char* ssd_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SSD_H */

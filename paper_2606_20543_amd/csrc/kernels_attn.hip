@@ -1,0 +1,368 @@
+// Block-causal multi-query attention of the verify pass over the KV cache.
+//
+// A block of K tokens at positions [f, f+K) attends under the backbone's
+// ordinary causal mask over raster positions: block token k (position f+k)
+// sees cache slots [0, f+k].  The paper's backbone is used unmodified
+// (Sec. 3.3), so no other mask exists; the drafted block simply occupies the
+// next raster positions.
+//
+// bf16 path: one wave per (key chunk, query group, sequence x KV head).  The
+// K*g query rows of a KV head (g = query heads per KV head) are tiled by 16;
+// S^T = K Q^T and O^T = V^T P^T run on v_mfma_f32_16x16x32_bf16 with queries
+// as the MFMA columns, so the softmax statistics of a query live in one lane
+// column and need only two cross-lane shuffles; the P^T operand is built in
+// registers straight from the S^T accumulators (its key order is matched by
+// reading the transposed V cache), so P never touches LDS.  Keys are streamed
+// 32 at a time with an online softmax; chunks of the context run on different
+// workgroups and the last one to finish merges the partial (max, sum, O)
+// triples in chunk order.
+#include "ssd_internal.h"
+
+namespace ssd {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ uint16_t f2bf_a(float f) {
+  uint32_t u = __float_as_uint(f);
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+
+struct AttnKArgs {
+  const uint16_t* q;   // [B][Hq][K][D]
+  const uint16_t* kc;  // [B][Hkv][Lmax][D]
+  const uint16_t* vc;  // [B][Hkv][D][Lmax]
+  uint16_t* o;         // [B*K][Hq*D]
+  float* part;         // [B*Hkv][nqg][nchunk][QPW*16][D+2]
+  unsigned* counters;  // [B*Hkv][nqg]
+  const int* f;
+  int K, Hq, Hkv, g, Lmax, rows, chunk, nchunk, nqg;
+  float scale_log2;
+};
+
+template <int D, int QPW>
+__global__ __launch_bounds__(64) void attn_bf16_kernel(AttnKArgs a) {
+  constexpr int KD = D / 32;   // 32-wide k steps over the head dimension
+  constexpr int DT = D / 16;   // 16-row d tiles of O^T
+  __shared__ int is_last;
+  const int c = blockIdx.x, qg = blockIdx.y, z = blockIdx.z;
+  const int b = z / a.Hkv, hkv = z - b * a.Hkv;
+  const int lane = threadIdx.x;
+  const int col = lane & 15, grp = lane >> 4;
+  const int fb = a.f[b];
+  const int ctx = fb + a.K;
+  const int nch = (ctx + a.chunk - 1) / a.chunk;
+  if (c >= nch) return;
+  const int kbeg = c * a.chunk;
+  const int kend = min(kbeg + a.chunk, ctx);
+  const int rbase = qg * QPW * 16;
+
+  // query fragments (B operand of S^T = K Q^T): lane holds row col of tile qt, d = 8*grp.. (+32 kd)
+  bf16x8 qf[QPW][KD];
+  int qpos[QPW];
+#pragma unroll
+  for (int qt = 0; qt < QPW; ++qt) {
+    const int r = rbase + qt * 16 + col;
+    const bool ok = r < a.rows;
+    const int j = ok ? r / a.K : 0, k = ok ? r - (r / a.K) * a.K : 0;
+    qpos[qt] = ok ? fb + k : -1;
+    const uint16_t* qp = a.q + (((size_t)b * a.Hq + hkv * a.g + j) * a.K + k) * D + grp * 8;
+#pragma unroll
+    for (int kd = 0; kd < KD; ++kd) {
+      uint4 v = ok ? *(const uint4*)(qp + kd * 32) : make_uint4(0, 0, 0, 0);
+      qf[qt][kd] = __builtin_bit_cast(bf16x8, v);
+    }
+  }
+
+  float m[QPW], l[QPW];
+  floatx4 O[QPW][DT];
+#pragma unroll
+  for (int qt = 0; qt < QPW; ++qt) {
+    m[qt] = -INFINITY;
+    l[qt] = 0.f;
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) O[qt][dt] = floatx4{0.f, 0.f, 0.f, 0.f};
+  }
+
+  const uint16_t* kbase = a.kc + ((size_t)b * a.Hkv + hkv) * a.Lmax * D;
+  const uint16_t* vbase = a.vc + ((size_t)b * a.Hkv + hkv) * (size_t)D * a.Lmax;
+
+  for (int key0 = kbeg; key0 < kend; key0 += 32) {
+    // S^T tiles for keys key0 + [0,16) and key0 + [16,32)
+    floatx4 s[2][QPW];
+#pragma unroll
+    for (int kt = 0; kt < 2; ++kt) {
+      int krow = key0 + kt * 16 + col;
+      krow = krow < a.Lmax ? krow : a.Lmax - 1;
+      const uint16_t* kp = kbase + (size_t)krow * D + grp * 8;
+      bf16x8 kf[KD];
+#pragma unroll
+      for (int kd = 0; kd < KD; ++kd) kf[kd] = __builtin_bit_cast(bf16x8, *(const uint4*)(kp + kd * 32));
+#pragma unroll
+      for (int qt = 0; qt < QPW; ++qt) {
+        floatx4 acc = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int kd = 0; kd < KD; ++kd) acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[kd], qf[qt][kd], acc, 0, 0, 0);
+        s[kt][qt] = acc;
+      }
+    }
+    // V^T fragments: lane row d = dt*16 + col, keys key0 + 4*grp + [0,4) and key0 + 16 + 4*grp + [0,4)
+    bf16x8 vf[DT];
+    {
+      int kA = key0 + 4 * grp, kB = key0 + 16 + 4 * grp;
+      kA = kA + 3 < a.Lmax ? kA : a.Lmax - 4;
+      kB = kB + 3 < a.Lmax ? kB : a.Lmax - 4;
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) {
+        const uint16_t* vp = vbase + (size_t)(dt * 16 + col) * a.Lmax;
+        uint2 lo = *(const uint2*)(vp + kA);
+        uint2 hi = *(const uint2*)(vp + kB);
+        uint4 v = make_uint4(lo.x, lo.y, hi.x, hi.y);
+        vf[dt] = __builtin_bit_cast(bf16x8, v);
+      }
+    }
+#pragma unroll
+    for (int qt = 0; qt < QPW; ++qt) {
+      float sv[8];
+      float mx = -INFINITY;
+#pragma unroll
+      for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int key = key0 + kt * 16 + 4 * grp + e;
+          float v = s[kt][qt][e] * a.scale_log2;
+          v = (key <= qpos[qt]) ? v : -INFINITY;
+          sv[kt * 4 + e] = v;
+          mx = fmaxf(mx, v);
+        }
+      mx = fmaxf(mx, __shfl_xor(mx, 16));
+      mx = fmaxf(mx, __shfl_xor(mx, 32));
+      const float mnew = fmaxf(m[qt], mx);
+      const bool none = (mnew == -INFINITY);
+      const float alpha = none ? 1.f : exp2f(m[qt] - mnew);
+      float ps = 0.f;
+      uint16_t pb[8];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        float p = none ? 0.f : exp2f(sv[i] - mnew);
+        ps += p;
+        pb[i] = f2bf_a(p);
+      }
+      l[qt] = l[qt] * alpha + ps;
+      m[qt] = mnew;
+      uint4 pv;
+      pv.x = (uint32_t)pb[0] | ((uint32_t)pb[1] << 16);
+      pv.y = (uint32_t)pb[2] | ((uint32_t)pb[3] << 16);
+      pv.z = (uint32_t)pb[4] | ((uint32_t)pb[5] << 16);
+      pv.w = (uint32_t)pb[6] | ((uint32_t)pb[7] << 16);
+      bf16x8 pf = __builtin_bit_cast(bf16x8, pv);
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) {
+        O[qt][dt] *= alpha;
+        O[qt][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf[dt], pf, O[qt][dt], 0, 0, 0);
+      }
+    }
+  }
+  // column sums of l
+#pragma unroll
+  for (int qt = 0; qt < QPW; ++qt) {
+    l[qt] += __shfl_xor(l[qt], 16);
+    l[qt] += __shfl_xor(l[qt], 32);
+  }
+
+  if (nch == 1) {
+#pragma unroll
+    for (int qt = 0; qt < QPW; ++qt) {
+      const int r = rbase + qt * 16 + col;
+      if (r >= a.rows) continue;
+      const int j = r / a.K, k = r - j * a.K;
+      const float inv = 1.f / l[qt];
+      uint16_t* op = a.o + ((size_t)b * a.K + k) * (a.Hq * D) + (hkv * a.g + j) * D;
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) {
+        const int d0 = dt * 16 + 4 * grp;
+        uint2 w;
+        w.x = (uint32_t)f2bf_a(O[qt][dt][0] * inv) | ((uint32_t)f2bf_a(O[qt][dt][1] * inv) << 16);
+        w.y = (uint32_t)f2bf_a(O[qt][dt][2] * inv) | ((uint32_t)f2bf_a(O[qt][dt][3] * inv) << 16);
+        *(uint2*)(op + d0) = w;
+      }
+    }
+    return;
+  }
+
+  // publish the partial (O unnormalised, m, l) of this chunk
+  constexpr int RS = D + 2;
+  const size_t grp_base = ((size_t)z * a.nqg + qg) * a.nchunk;
+  float* P = a.part + (grp_base + c) * (QPW * 16) * RS;
+#pragma unroll
+  for (int qt = 0; qt < QPW; ++qt) {
+    float* pr = P + (size_t)(qt * 16 + col) * RS;
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) {
+      const int d0 = dt * 16 + 4 * grp;
+      pr[d0 + 0] = O[qt][dt][0];
+      pr[d0 + 1] = O[qt][dt][1];
+      pr[d0 + 2] = O[qt][dt][2];
+      pr[d0 + 3] = O[qt][dt][3];
+    }
+    if (grp == 0) {
+      pr[D] = m[qt];
+      pr[D + 1] = l[qt];
+    }
+  }
+  __threadfence();
+  if (lane == 0) {
+    unsigned prev = atomicAdd(&a.counters[(size_t)z * a.nqg + qg], 1u);
+    is_last = (prev == (unsigned)(nch - 1));
+  }
+  __syncthreads();
+  if (!is_last) return;
+  __threadfence();
+  // merge chunks in order; lanes run over the head dimension
+  const float* G = a.part + grp_base * (QPW * 16) * RS;
+  for (int rr = 0; rr < QPW * 16; ++rr) {
+    const int r = rbase + rr;
+    if (r >= a.rows) break;
+    float M = -INFINITY;
+    for (int cc = 0; cc < nch; ++cc) M = fmaxf(M, __builtin_nontemporal_load(G + ((size_t)cc * QPW * 16 + rr) * RS + D));
+    float L = 0.f;
+    float acc[D / 64];
+#pragma unroll
+    for (int i = 0; i < D / 64; ++i) acc[i] = 0.f;
+    for (int cc = 0; cc < nch; ++cc) {
+      const float* pr = G + ((size_t)cc * QPW * 16 + rr) * RS;
+      const float mc = __builtin_nontemporal_load(pr + D);
+      const float lc = __builtin_nontemporal_load(pr + D + 1);
+      if (lc == 0.f) continue;
+      const float wgt = exp2f(mc - M);
+      L += lc * wgt;
+#pragma unroll
+      for (int i = 0; i < D / 64; ++i) acc[i] += __builtin_nontemporal_load(pr + lane + 64 * i) * wgt;
+    }
+    const int j = r / a.K, k = r - j * a.K;
+    uint16_t* op = a.o + ((size_t)b * a.K + k) * (a.Hq * D) + (hkv * a.g + j) * D;
+    const float inv = 1.f / L;
+#pragma unroll
+    for (int i = 0; i < D / 64; ++i) op[lane + 64 * i] = f2bf_a(acc[i] * inv);
+  }
+  if (lane == 0) a.counters[(size_t)z * a.nqg + qg] = 0u;
+}
+
+AttnPlan attn_plan(const Dims& dm, int B, int K, int max_ctx_now) {
+  AttnPlan p;
+  const int g = dm.Hq / dm.Hkv;
+  p.rows = K * g;
+  const int qt = (p.rows + 15) / 16;
+  p.qpw = qt >= 4 ? 4 : qt >= 2 ? 2 : 1;
+  p.nqg = (qt + p.qpw - 1) / p.qpw;
+  // chunk: enough workgroups to cover the chip, at least 64 keys
+  const int units = B * dm.Hkv * p.nqg;
+  int chunk = 64;
+  while (chunk < 2048 && (long)units * ((max_ctx_now + chunk - 1) / chunk) > 1024) chunk *= 2;
+  p.chunk = chunk;
+  p.nchunk = (max_ctx_now + chunk - 1) / chunk;
+  return p;
+}
+
+size_t attn_partials_floats(const Dims& dm, const AttnPlan& p, int B) {
+  return (size_t)B * dm.Hkv * p.nqg * p.nchunk * p.qpw * 16 * (dm.D + 2);
+}
+
+template <int D, int QPW>
+static void launch_attn(const AttnKArgs& a, int nchunk, int nqg, int z, hipStream_t st) {
+  hipLaunchKernelGGL((attn_bf16_kernel<D, QPW>), dim3(nchunk, nqg, z), dim3(64), 0, st, a);
+}
+
+void attention_bf16(const Dims& dm, const AttnPlan& p, int B, int K, const int* f, const void* q, const void* kc,
+                    const void* vc, int Lmax, void* o, float* partials, unsigned* counters, hipStream_t st) {
+  AttnKArgs a;
+  a.q = (const uint16_t*)q;
+  a.kc = (const uint16_t*)kc;
+  a.vc = (const uint16_t*)vc;
+  a.o = (uint16_t*)o;
+  a.part = partials;
+  a.counters = counters;
+  a.f = f;
+  a.K = K;
+  a.Hq = dm.Hq;
+  a.Hkv = dm.Hkv;
+  a.g = dm.Hq / dm.Hkv;
+  a.Lmax = Lmax;
+  a.rows = p.rows;
+  a.chunk = p.chunk;
+  a.nchunk = p.nchunk;
+  a.nqg = p.nqg;
+  a.scale_log2 = 1.4426950408889634f / sqrtf((float)dm.D);
+  const int z = B * dm.Hkv;
+  if (dm.D == 128) {
+    if (p.qpw == 4) launch_attn<128, 4>(a, p.nchunk, p.nqg, z, st);
+    else if (p.qpw == 2) launch_attn<128, 2>(a, p.nchunk, p.nqg, z, st);
+    else launch_attn<128, 1>(a, p.nchunk, p.nqg, z, st);
+  } else {
+    if (p.qpw == 4) launch_attn<64, 4>(a, p.nchunk, p.nqg, z, st);
+    else if (p.qpw == 2) launch_attn<64, 2>(a, p.nchunk, p.nqg, z, st);
+    else launch_attn<64, 1>(a, p.nchunk, p.nqg, z, st);
+  }
+}
+
+// ---------------- fp32 path ----------------
+// One workgroup per (query, head, sequence): scores in LDS, two-pass softmax.
+constexpr int F32_MAX_CTX = 4096;
+
+__global__ __launch_bounds__(256) void attn_f32_kernel(int K, int Hq, int Hkv, int D, int Lmax, const int* f,
+                                                       const float* q, const float* kc, const float* vc, float* o,
+                                                       float scale) {
+  __shared__ float sc[F32_MAX_CTX];
+  __shared__ float red[256];
+  const int k = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
+  const int g = Hq / Hkv, hkv = h / g;
+  const int pos = f[b] + k;
+  const int n = pos + 1;
+  const float* qp = q + (((size_t)b * Hq + h) * K + k) * D;
+  const float* kb = kc + ((size_t)b * Hkv + hkv) * (size_t)Lmax * D;
+  const float* vb = vc + ((size_t)b * Hkv + hkv) * (size_t)D * Lmax;
+  float mx = -INFINITY;
+  for (int j = threadIdx.x; j < n; j += blockDim.x) {
+    float s = 0.f;
+    for (int d = 0; d < D; ++d) s = fmaf(qp[d], kb[(size_t)j * D + d], s);
+    s *= scale;
+    sc[j] = s;
+    mx = fmaxf(mx, s);
+  }
+  red[threadIdx.x] = mx;
+  __syncthreads();
+  for (int w = 128; w > 0; w >>= 1) {
+    if (threadIdx.x < w) red[threadIdx.x] = fmaxf(red[threadIdx.x], red[threadIdx.x + w]);
+    __syncthreads();
+  }
+  mx = red[0];
+  __syncthreads();
+  float sum = 0.f;
+  for (int j = threadIdx.x; j < n; j += blockDim.x) {
+    float p = expf(sc[j] - mx);
+    sc[j] = p;
+    sum += p;
+  }
+  red[threadIdx.x] = sum;
+  __syncthreads();
+  for (int w = 128; w > 0; w >>= 1) {
+    if (threadIdx.x < w) red[threadIdx.x] += red[threadIdx.x + w];
+    __syncthreads();
+  }
+  const float inv = 1.f / red[0];
+  for (int d = threadIdx.x; d < D; d += blockDim.x) {
+    const float* vr = vb + (size_t)d * Lmax;
+    float acc = 0.f;
+    for (int j = 0; j < n; ++j) acc = fmaf(sc[j], vr[j], acc);
+    o[((size_t)b * K + k) * (Hq * D) + h * D + d] = acc * inv;
+  }
+}
+
+void attention_f32(const Dims& dm, int B, int K, const int* f, const float* q, const float* kc, const float* vc,
+                   int Lmax, float* o, hipStream_t st) {
+  hipLaunchKernelGGL(attn_f32_kernel, dim3(K, dm.Hq, B), dim3(256), 0, st, K, dm.Hq, dm.Hkv, dm.D, Lmax, f, q, kc, vc,
+                     o, 1.0f / sqrtf((float)dm.D));
+}
+
+}  // namespace ssd

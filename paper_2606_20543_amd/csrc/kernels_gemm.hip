@@ -1,0 +1,436 @@
+// Projection GEMMs of the backbone forward pass, y[t][n] = sum_k in[t][k] W[n][k],
+// with the epilogues the verify step needs fused into the final write:
+//   QKV    : 1/rms scale, rotary embedding at the token's raster position,
+//            q to the query buffer, k/v into the KV cache slots [f, f+K)
+//   RESID  : x += y; xn = bf16(g_next * x); per-block sums of x^2 for the next 1/rms
+//   SWIGLU : h = silu(gate / rms) * (up / rms)
+//   LOGITS : logits = y / rms  (fp32)
+//
+// bf16 path (gfx950 MFMA v_mfma_f32_16x16x32_bf16): the verify step runs at
+// small M (the draft count, 8..512 tokens), so the GEMMs stream the weights
+// from HBM once: each wave streams its own 16-feature tiles (prepacked so one
+// 16-byte load per lane fetches a whole A operand), the token rows of the
+// current K-chunk sit in LDS (B operand, shared by the four waves), and the
+// A loads of the next chunk are in flight while the current one is
+// multiplied.  When N/64 feature blocks cannot fill 256 CUs the K range is
+// split; the last workgroup of a feature block sums the partials in split
+// order (deterministic) and runs the epilogue.
+#include "ssd_internal.h"
+
+namespace ssd {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ uint16_t f2bf(float f) {
+  uint32_t u = __float_as_uint(f);
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+
+template <bool BF>
+__device__ __forceinline__ void st_act(void* base, size_t i, float v) {
+  if (BF)
+    ((uint16_t*)base)[i] = f2bf(v);
+  else
+    ((float*)base)[i] = v;
+}
+
+__device__ __forceinline__ float rms_scale(const EpiArgs& e, int t) {
+  if (!e.ssq) return 1.f;
+  float s = 0.f;
+  const size_t c = (size_t)e.ssq_off + (size_t)t * e.ssq_step;
+  for (int p = 0; p < e.ssq_parts; ++p) s += e.ssq[(size_t)p * e.ssq_ld + c];
+  return 1.0f / sqrtf(s * e.inv_d + e.eps);
+}
+
+// Epilogue of the output pair (n, n+1), n even, for token t with accumulators
+// (v0, v1) and rms scale r.  Returns the squared new residual values (RESID).
+template <bool BF>
+__device__ __forceinline__ float epi_pair(const EpiArgs& e, int t, int n, float v0, float v1, float r) {
+  switch (e.kind) {
+    case EPI_QKV: {
+      const int b = t / e.Kblk, k = t - b * e.Kblk;
+      const int pos = e.f[b] + k;
+      const int D = e.D, half = D >> 1;
+      const int qN = e.Hq * D, kN = e.Hkv * D;
+      v0 *= r;
+      v1 *= r;
+      if (n < qN + kN) {
+        const bool isq = n < qN;
+        const int nn = isq ? n : n - qN;
+        const int head = nn / D, j = (nn - head * D) >> 1;
+        const float2 cs = e.rope[(size_t)pos * half + j];
+        const float a = v0 * cs.x - v1 * cs.y;  // dim j
+        const float c = v1 * cs.x + v0 * cs.y;  // dim j + D/2
+        size_t base = isq ? (((size_t)b * e.Hq + head) * e.Kblk + k) * D
+                          : (((size_t)b * e.Hkv + head) * e.Lmax + pos) * D;
+        void* dst = isq ? e.q : e.kc;
+        st_act<BF>(dst, base + j, a);
+        st_act<BF>(dst, base + j + half, c);
+      } else {
+        const int nv = n - qN - kN;
+        const int head = nv / D, dd = nv - head * D;
+        size_t base = (((size_t)b * e.Hkv + head) * D + dd) * e.Lmax + pos;
+        st_act<BF>(e.vc, base, v0);
+        st_act<BF>(e.vc, base + e.Lmax, v1);
+      }
+      return 0.f;
+    }
+    case EPI_RESID: {
+      size_t i = (size_t)t * e.ld + n;
+      float2 xo = *(const float2*)(e.x + i);
+      float x0 = xo.x + v0, x1 = xo.y + v1;
+      *(float2*)(e.x + i) = make_float2(x0, x1);
+      st_act<BF>(e.xn, i, e.gnext[n] * x0);
+      st_act<BF>(e.xn, i + 1, e.gnext[n + 1] * x1);
+      return x0 * x0 + x1 * x1;
+    }
+    case EPI_SWIGLU: {
+      float g = v0 * r, u = v1 * r;
+      float s = g / (1.0f + expf(-g));
+      st_act<BF>(e.h, (size_t)t * e.ld + (n >> 1), s * u);
+      return 0.f;
+    }
+    default: {  // EPI_LOGITS
+      size_t i = (size_t)t * e.ld + n;
+      *(float2*)(e.logits + i) = make_float2(v0 * r, v1 * r);
+      return 0.f;
+    }
+  }
+}
+
+struct GemmKArgs {
+  const u32x4* W;
+  int N, K, KB;
+  int S, kchunks, n_fb;
+  const uint16_t* in;
+  int ld_in;
+  int M, t0;
+  float* part;
+  unsigned* counters;
+  EpiArgs epi;
+};
+
+template <int NT, int KCB>
+__device__ __forceinline__ void load_a(u32x4 (&ra)[NT][KCB], const u32x4* W, int KB, int nb0, int N, int kb0,
+                                       int lane) {
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) {
+    if ((nb0 + nt) * 16 < N) {
+      const u32x4* p = W + ((size_t)(nb0 + nt) * KB + kb0) * 64 + lane;
+#pragma unroll
+      for (int kb = 0; kb < KCB; ++kb) ra[nt][kb] = __builtin_nontemporal_load(p + kb * 64);
+    } else {
+#pragma unroll
+      for (int kb = 0; kb < KCB; ++kb) ra[nt][kb] = u32x4{0u, 0u, 0u, 0u};
+    }
+  }
+}
+
+template <int MT, int KCB>
+struct XStage {
+  static constexpr int MP = MT * 16;
+  static constexpr int KC = KCB * 32;
+  static constexpr int LD = KC + 8;          // bf16 per LDS row (16-byte pad)
+  static constexpr int CG = KC / 8;          // 16-byte column groups per row
+  static constexpr int RSTEP = 256 / CG;     // rows covered per pass
+  static constexpr int PASSES = (MP + RSTEP - 1) / RSTEP;
+};
+
+template <int MT, int KCB, int NP>
+__device__ __forceinline__ void load_x(u32x4 (&rx)[NP], const uint16_t* in, int ld_in, int M, int k0) {
+  using X = XStage<MT, KCB>;
+  const int cg = threadIdx.x % X::CG, r0 = threadIdx.x / X::CG;
+#pragma unroll
+  for (int p = 0; p < X::PASSES; ++p) {
+    int r = r0 + p * X::RSTEP;
+    if (r < M && r < X::MP)
+      rx[p] = *(const u32x4*)(in + (size_t)r * ld_in + k0 + cg * 8);
+    else
+      rx[p] = u32x4{0u, 0u, 0u, 0u};
+  }
+}
+
+template <int MT, int KCB, int NP>
+__device__ __forceinline__ void store_x(const u32x4 (&rx)[NP], uint16_t* xs) {
+  using X = XStage<MT, KCB>;
+  const int cg = threadIdx.x % X::CG, r0 = threadIdx.x / X::CG;
+#pragma unroll
+  for (int p = 0; p < X::PASSES; ++p) {
+    int r = r0 + p * X::RSTEP;
+    if (r < X::MP) *(u32x4*)(xs + r * X::LD + cg * 8) = rx[p];
+  }
+}
+
+template <int MT, int NT, int KCB>
+__device__ __forceinline__ void compute_chunk(floatx4 (&acc)[NT][MT], const u32x4 (&ra)[NT][KCB], const uint16_t* xs,
+                                              int lane) {
+  using X = XStage<MT, KCB>;
+  const int row = lane & 15, col = (lane >> 4) * 8;
+#pragma unroll
+  for (int kb = 0; kb < KCB; ++kb) {
+    bf16x8 bfr[MT];
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) {
+      u32x4 v = *(const u32x4*)(xs + (mt * 16 + row) * X::LD + kb * 32 + col);
+      bfr[mt] = __builtin_bit_cast(bf16x8, v);
+    }
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
+      bf16x8 a = __builtin_bit_cast(bf16x8, ra[nt][kb]);
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) acc[nt][mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, bfr[mt], acc[nt][mt], 0, 0, 0);
+    }
+  }
+}
+
+template <int MT, int NT, int KCB>
+__global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmKArgs a) {
+  using X = XStage<MT, KCB>;
+  __shared__ __attribute__((aligned(16))) uint16_t xs[2][X::MP * X::LD];
+  __shared__ float sq_red[4][X::MP];
+  __shared__ float rscale[X::MP];
+  __shared__ int is_last;
+
+  const int fb = blockIdx.x, s = blockIdx.y;
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int nb0 = (fb * 4 + w) * NT;
+  const int kb_split = s * a.kchunks * KCB;
+  const uint16_t* in = a.in;
+  const int nc = a.kchunks;
+
+  floatx4 acc[NT][MT];
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) acc[nt][mt] = floatx4{0.f, 0.f, 0.f, 0.f};
+
+  u32x4 ra[2][NT][KCB];
+  u32x4 rx[X::PASSES];
+
+  load_x<MT, KCB>(rx, in, a.ld_in, a.M, kb_split * 32);
+  load_a<NT, KCB>(ra[0], a.W, a.KB, nb0, a.N, kb_split, lane);
+  store_x<MT, KCB>(rx, xs[0]);
+  __syncthreads();
+  for (int c = 0; c < nc; c += 2) {
+    if (c + 1 < nc) {
+      load_x<MT, KCB>(rx, in, a.ld_in, a.M, (kb_split + (c + 1) * KCB) * 32);
+      load_a<NT, KCB>(ra[1], a.W, a.KB, nb0, a.N, kb_split + (c + 1) * KCB, lane);
+    }
+    compute_chunk<MT, NT, KCB>(acc, ra[0], xs[0], lane);
+    if (c + 1 < nc) store_x<MT, KCB>(rx, xs[1]);
+    __syncthreads();
+    if (c + 1 >= nc) break;
+    if (c + 2 < nc) {
+      load_x<MT, KCB>(rx, in, a.ld_in, a.M, (kb_split + (c + 2) * KCB) * 32);
+      load_a<NT, KCB>(ra[0], a.W, a.KB, nb0, a.N, kb_split + (c + 2) * KCB, lane);
+    }
+    compute_chunk<MT, NT, KCB>(acc, ra[1], xs[1], lane);
+    if (c + 2 < nc) store_x<MT, KCB>(rx, xs[0]);
+    __syncthreads();
+  }
+
+  if (a.S > 1) {
+    // split-K: publish partial fragments, the last workgroup of this feature block reduces
+    const size_t frag = (size_t)NT * MT * 64 * 4;
+    float* P = a.part + ((size_t)fb * 4 + w) * frag;
+    const size_t split_stride = (size_t)a.n_fb * 4 * frag;
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) *(floatx4*)(P + (size_t)s * split_stride + ((nt * MT + mt) * 64 + lane) * 4) = acc[nt][mt];
+    __threadfence();
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      unsigned prev = atomicAdd(&a.counters[fb], 1u);
+      is_last = (prev == (unsigned)(a.S - 1));
+    }
+    __syncthreads();
+    if (!is_last) return;
+    __threadfence();
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) {
+        floatx4 v = floatx4{0.f, 0.f, 0.f, 0.f};
+        for (int s2 = 0; s2 < a.S; ++s2) {
+          floatx4 pv = __builtin_nontemporal_load((const floatx4*)(P + (size_t)s2 * split_stride + ((nt * MT + mt) * 64 + lane) * 4));
+          v += pv;
+        }
+        acc[nt][mt] = v;
+      }
+    if (threadIdx.x == 0) a.counters[fb] = 0u;
+  }
+
+  // epilogue
+  const EpiArgs& e = a.epi;
+  if (threadIdx.x < X::MP) {
+    int t = threadIdx.x;
+    rscale[t] = (t < a.M) ? rms_scale(e, a.t0 + t) : 1.f;
+  }
+  __syncthreads();
+  float sq[MT];
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt) sq[mt] = 0.f;
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) {
+    const int n = (nb0 + nt) * 16 + 4 * (lane >> 4);
+    if ((nb0 + nt) * 16 >= a.N) continue;
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) {
+      const int tl = mt * 16 + (lane & 15);
+      if (tl < a.M) {
+        const int t = a.t0 + tl;
+        const float r = rscale[tl];
+        sq[mt] += epi_pair<true>(e, t, n, acc[nt][mt][0], acc[nt][mt][1], r);
+        sq[mt] += epi_pair<true>(e, t, n + 2, acc[nt][mt][2], acc[nt][mt][3], r);
+      }
+    }
+  }
+  if (e.kind == EPI_RESID) {
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) {
+      float v = sq[mt];
+      v += __shfl_xor(v, 16);
+      v += __shfl_xor(v, 32);
+      if (lane < 16) sq_red[w][mt * 16 + lane] = v;
+    }
+    __syncthreads();
+    if (threadIdx.x < X::MP && threadIdx.x < a.M) {
+      int tl = threadIdx.x;
+      float v = ((sq_red[0][tl] + sq_red[1][tl]) + sq_red[2][tl]) + sq_red[3][tl];
+      e.ssq_out[(size_t)fb * e.ssq_out_ld + a.t0 + tl] = v;
+    }
+  }
+}
+
+GemmPlan gemm_plan_bf16(int M, int N, int K) {
+  GemmPlan p;
+  int Mc = M < 128 ? M : 128;
+  p.MT = Mc <= 16 ? 1 : Mc <= 32 ? 2 : Mc <= 64 ? 4 : 8;
+  p.KCB = p.MT >= 8 ? 2 : p.MT == 4 ? 4 : 8;
+  p.NT = p.MT >= 4 ? 2 : 1;
+  p.bn = 4 * p.NT * 16;
+  p.n_fb = (N + p.bn - 1) / p.bn;
+  int kch = K / (p.KCB * 32);
+  p.S = 1;
+  if (p.n_fb < 480) {
+    int best = 1;
+    for (int s = 1; s <= kch && s <= 16; ++s) {
+      if (kch % s) continue;
+      best = s;
+      if (p.n_fb * s >= 480) break;
+    }
+    p.S = best;
+  }
+  p.kchunks = kch / p.S;
+  return p;
+}
+
+size_t gemm_partials_floats(const GemmPlan& p, int M) {
+  (void)M;
+  if (p.S <= 1) return 0;
+  return (size_t)p.S * p.n_fb * 4 * p.NT * p.MT * 64 * 4;
+}
+
+template <int MT, int NT, int KCB>
+static void launch_gemm(const GemmKArgs& a, int n_fb, int S, hipStream_t st) {
+  hipLaunchKernelGGL((gemm_bf16_kernel<MT, NT, KCB>), dim3(n_fb, S), dim3(256), 0, st, a);
+}
+
+void gemm_bf16(const GemmPlan& p, const void* Wpacked, int N, int K, const void* in, int ld_in, int M,
+               const EpiArgs& epi, float* partials, float* ssq_part, unsigned* counters, hipStream_t st) {
+  (void)ssq_part;
+  const int MP = p.MT * 16;
+  for (int t0 = 0; t0 < M; t0 += MP) {
+    GemmKArgs a;
+    a.W = (const u32x4*)Wpacked;
+    a.N = N;
+    a.K = K;
+    a.KB = K / 32;
+    a.S = p.S;
+    a.kchunks = p.kchunks;
+    a.n_fb = p.n_fb;
+    a.in = (const uint16_t*)in + (size_t)t0 * ld_in;
+    a.ld_in = ld_in;
+    a.M = (M - t0) < MP ? (M - t0) : MP;
+    a.t0 = t0;
+    a.part = partials;
+    a.counters = counters;
+    a.epi = epi;
+    switch (p.MT) {
+      case 1: launch_gemm<1, 1, 8>(a, p.n_fb, p.S, st); break;
+      case 2: launch_gemm<2, 1, 8>(a, p.n_fb, p.S, st); break;
+      case 4: launch_gemm<4, 2, 4>(a, p.n_fb, p.S, st); break;
+      default: launch_gemm<8, 2, 2>(a, p.n_fb, p.S, st); break;
+    }
+  }
+}
+
+// ---------------- fp32 path (small fp32 models) ----------------
+// One thread per (token, output pair); plain fp32 FMAs in k order.
+__global__ void gemm_f32_kernel(const float* W, int N, int K, const float* in, int ld_in, int M, EpiArgs e) {
+  const int pair = blockIdx.x * blockDim.x + threadIdx.x;
+  const int t = blockIdx.y;
+  const int n = pair * 2;
+  if (n >= N || t >= M) return;
+  const float* x = in + (size_t)t * ld_in;
+  const float* w0 = W + (size_t)n * K;
+  const float* w1 = w0 + K;
+  float a0 = 0.f, a1 = 0.f;
+  for (int k = 0; k < K; ++k) {
+    float xv = x[k];
+    a0 = fmaf(xv, w0[k], a0);
+    a1 = fmaf(xv, w1[k], a1);
+  }
+  float r = rms_scale(e, t);
+  epi_pair<false>(e, t, n, a0, a1, r);
+}
+
+void gemm_f32(const float* W, int N, int K, const float* in, int ld_in, int M, const EpiArgs& epi, hipStream_t st) {
+  int pairs = N / 2;
+  dim3 grid((pairs + 127) / 128, M);
+  hipLaunchKernelGGL(gemm_f32_kernel, grid, dim3(128), 0, st, W, N, K, in, ld_in, M, epi);
+}
+
+// ---------------- weight packing ----------------
+__global__ void pack_tiles_kernel(const uint16_t* src, const int* rowmap, int N, int K, u32x4* dst) {
+  const int KB = K / 32;
+  const size_t tiles = (size_t)(N / 16) * KB;
+  const size_t gid = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const size_t tile = gid >> 6;
+  const int lane = gid & 63;
+  if (tile >= tiles) return;
+  const int nb = (int)(tile / KB), kb = (int)(tile % KB);
+  const int row = rowmap[nb * 16 + (lane & 15)];
+  const uint16_t* p = src + (size_t)row * K + kb * 32 + (lane >> 4) * 8;
+  u32x4 v;
+  v.x = (uint32_t)p[0] | ((uint32_t)p[1] << 16);
+  v.y = (uint32_t)p[2] | ((uint32_t)p[3] << 16);
+  v.z = (uint32_t)p[4] | ((uint32_t)p[5] << 16);
+  v.w = (uint32_t)p[6] | ((uint32_t)p[7] << 16);
+  dst[tile * 64 + lane] = v;
+}
+
+void pack_bf16_tiles(const uint16_t* src, const int* rowmap, int N, int K, void* dst, hipStream_t st) {
+  size_t threads = (size_t)(N / 16) * (K / 32) * 64;
+  hipLaunchKernelGGL(pack_tiles_kernel, dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, st, src, rowmap, N, K,
+                     (u32x4*)dst);
+}
+
+__global__ void gather_rows_kernel(const float* src, const int* rowmap, int N, int K, float* dst) {
+  const size_t gid = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (gid >= (size_t)N * K) return;
+  const int n = (int)(gid / K), k = (int)(gid % K);
+  dst[gid] = src[(size_t)rowmap[n] * K + k];
+}
+
+void gather_rows_f32(const float* src, const int* rowmap, int N, int K, float* dst, hipStream_t st) {
+  size_t total = (size_t)N * K;
+  hipLaunchKernelGGL(gather_rows_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, st, src, rowmap, N, K,
+                     dst);
+}
+
+}  // namespace ssd

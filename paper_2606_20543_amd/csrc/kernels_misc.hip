@@ -1,0 +1,588 @@
+// Embedding gather, per-position correction rules and commit bookkeeping.
+//
+// Correction (paper Sec. 3.3, "Verification as Auto Correction"): every
+// drafted position k is decided independently and in parallel, one
+// workgroup per position:
+//   (A) greedy  : argmax of the scoring logits (ties -> lowest code)
+//   (B) sample  : inverse-CDF sample of p = softmax(top_k(logits / T))
+//   (C) accept/reject: keep the token t with probability min(p(t)/q(t), 1),
+//       else sample the residual [p - q]_+; a rejected position stores this
+//       round's logits as its next reference q (an accepted one keeps q).
+// q is the stored reference warped like p, or a point mass at t.
+// Probabilities, sums and the inverse CDF are float64; the top-k set is
+// found by an 8-bit radix select over order-preserving float keys, ties at
+// the boundary resolved towards lower codes.  Uniforms: 24-bit SplitMix64
+// outputs at a counter built from (sequence, position, round, stream)
+// (Steele, Lea & Flood, OOPSLA 2014).
+#include "ssd_internal.h"
+
+namespace ssd {
+
+__device__ __forceinline__ uint16_t f2bf_m(float f) {
+  uint32_t u = __float_as_uint(f);
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+
+// ---------------- embedding ----------------
+template <bool BF>
+__global__ __launch_bounds__(256) void embed_kernel(const void* emb, const int* tok, int d, int V, const float* g,
+                                                    float* x, void* xn, float* ssq) {
+  __shared__ float red[256];
+  const int t = blockIdx.x;
+  int id = tok[t];
+  id = id < 0 ? 0 : (id >= V ? V - 1 : id);
+  float s = 0.f;
+  for (int i = threadIdx.x; i < d; i += 256) {
+    float v = BF ? __uint_as_float(((uint32_t)((const uint16_t*)emb)[(size_t)id * d + i]) << 16)
+                 : ((const float*)emb)[(size_t)id * d + i];
+    x[(size_t)t * d + i] = v;
+    float gv = g[i] * v;
+    if (BF)
+      ((uint16_t*)xn)[(size_t)t * d + i] = f2bf_m(gv);
+    else
+      ((float*)xn)[(size_t)t * d + i] = gv;
+    s += v * v;
+  }
+  red[threadIdx.x] = s;
+  __syncthreads();
+  for (int w = 128; w > 0; w >>= 1) {
+    if (threadIdx.x < w) red[threadIdx.x] += red[threadIdx.x + w];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) ssq[t] = red[0];
+}
+
+void embed(const Dims& dm, const void* emb, const int* tok, int M, const float* g, float* x, void* xn, float* ssq,
+           hipStream_t st) {
+  if (dm.bf16)
+    hipLaunchKernelGGL(embed_kernel<true>, dim3(M), dim3(256), 0, st, emb, tok, dm.d, dm.V, g, x, xn, ssq);
+  else
+    hipLaunchKernelGGL(embed_kernel<false>, dim3(M), dim3(256), 0, st, emb, tok, dm.d, dm.V, g, x, xn, ssq);
+}
+
+__global__ __launch_bounds__(256) void ssq_kernel(const float* x, int d, float* ssq) {
+  __shared__ float red[256];
+  const int t = blockIdx.x;
+  float s = 0.f;
+  for (int i = threadIdx.x; i < d; i += 256) {
+    float v = x[(size_t)t * d + i];
+    s += v * v;
+  }
+  red[threadIdx.x] = s;
+  __syncthreads();
+  for (int w = 128; w > 0; w >>= 1) {
+    if (threadIdx.x < w) red[threadIdx.x] += red[threadIdx.x + w];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) ssq[t] = red[0];
+}
+
+void norm_rows_f32(const float* x, int M, int d, const float* g, float* xn, float* ssq, hipStream_t st) {
+  (void)g;
+  (void)xn;
+  hipLaunchKernelGGL(ssq_kernel, dim3(M), dim3(256), 0, st, x, d, ssq);
+}
+
+// ---------------- block helpers (256 threads) ----------------
+constexpr int NT_SEL = 256;
+
+__device__ __forceinline__ uint32_t fkey(float f) {
+  uint32_t u = __float_as_uint(f);
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+__device__ __forceinline__ uint64_t sm_mix(uint64_t z) {
+  z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+  z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+  return z ^ (z >> 31);
+}
+
+// output number c+1 of the SplitMix64 stream seeded with `seed`, top 24 bits in [0,1)
+__device__ __forceinline__ double uniform24(unsigned long long seed, int b, int pos, unsigned round, int stream) {
+  const uint64_t c = ((uint64_t)b << 44) | ((uint64_t)pos << 20) | ((uint64_t)(round & 0xFFFFu) << 4) | (uint64_t)stream;
+  const uint64_t z = sm_mix(seed + (c + 1ull) * 0x9E3779B97F4A7C15ull);
+  return (double)(z >> 40) * (1.0 / 16777216.0);
+}
+
+struct SelShared {
+  double dred[NT_SEL / 64];
+  float fred[NT_SEL / 64];
+  int ired[NT_SEL / 64];
+  int hist[256];
+  int tie_base[NT_SEL];
+  double pre[NT_SEL];
+  int bc_i[4];
+  double bc_d[4];
+  unsigned bc_u[2];
+};
+
+__device__ double block_sum_d(double v, SelShared& sh) {
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) sh.dred[threadIdx.x >> 6] = v;
+  __syncthreads();
+  double r = ((sh.dred[0] + sh.dred[1]) + sh.dred[2]) + sh.dred[3];
+  __syncthreads();
+  return r;
+}
+
+__device__ float block_max_f(float v, SelShared& sh) {
+  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) sh.fred[threadIdx.x >> 6] = v;
+  __syncthreads();
+  float r = fmaxf(fmaxf(sh.fred[0], sh.fred[1]), fmaxf(sh.fred[2], sh.fred[3]));
+  __syncthreads();
+  return r;
+}
+
+__device__ int block_min_i(int v, SelShared& sh) {
+  for (int o = 32; o > 0; o >>= 1) v = min(v, __shfl_xor(v, o));
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) sh.ired[threadIdx.x >> 6] = v;
+  __syncthreads();
+  int r = min(min(sh.ired[0], sh.ired[1]), min(sh.ired[2], sh.ired[3]));
+  __syncthreads();
+  return r;
+}
+
+__device__ int block_max_i(int v, SelShared& sh) {
+  for (int o = 32; o > 0; o >>= 1) v = max(v, __shfl_xor(v, o));
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) sh.ired[threadIdx.x >> 6] = v;
+  __syncthreads();
+  int r = max(max(sh.ired[0], sh.ired[1]), max(sh.ired[2], sh.ired[3]));
+  __syncthreads();
+  return r;
+}
+
+// argmax with ties to the lowest index over row[0..V)
+__device__ int block_argmax(const float* row, int V, SelShared& sh) {
+  const int VPT = (V + NT_SEL - 1) / NT_SEL;
+  const int lo = threadIdx.x * VPT, hi = min(lo + VPT, V);
+  float bv = -INFINITY;
+  int bi = 0x7fffffff;
+  for (int v = lo; v < hi; ++v) {
+    float x = row[v];
+    if (x > bv || bi == 0x7fffffff) {
+      bv = x;
+      bi = v;
+    }
+  }
+  for (int o = 32; o > 0; o >>= 1) {
+    float ov = __shfl_xor(bv, o);
+    int oi = __shfl_xor(bi, o);
+    if (ov > bv || (ov == bv && oi < bi)) {
+      bv = ov;
+      bi = oi;
+    }
+  }
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) {
+    sh.fred[threadIdx.x >> 6] = bv;
+    sh.ired[threadIdx.x >> 6] = bi;
+  }
+  __syncthreads();
+  float rv = sh.fred[0];
+  int ri = sh.ired[0];
+  for (int w = 1; w < NT_SEL / 64; ++w) {
+    if (sh.fred[w] > rv || (sh.fred[w] == rv && sh.ired[w] < ri)) {
+      rv = sh.fred[w];
+      ri = sh.ired[w];
+    }
+  }
+  __syncthreads();
+  return ri;
+}
+
+// The kept set of top_k(row): keys above `thr`, plus the first `need` keys equal to
+// `thr` in index order.  `all` when no truncation applies.
+struct TopK {
+  uint32_t thr;
+  int need;
+  bool all;
+};
+
+struct KeepIter {
+  uint32_t thr;
+  int need, rank;
+  bool all;
+  __device__ __forceinline__ bool next(uint32_t key) {
+    if (all || key > thr) return true;
+    if (key == thr) {
+      bool k = rank < need;
+      ++rank;
+      return k;
+    }
+    return false;
+  }
+};
+
+__device__ TopK topk_select(const float* row, int V, int top_k, SelShared& sh, int* tie_base_out) {
+  TopK tk;
+  tk.all = (top_k <= 0 || top_k >= V);
+  tk.thr = 0;
+  tk.need = 0;
+  const int VPT = (V + NT_SEL - 1) / NT_SEL;
+  const int lo = threadIdx.x * VPT, hi = min(lo + VPT, V);
+  if (tk.all) {
+    *tie_base_out = 0;
+    return tk;
+  }
+  uint32_t prefix = 0, mask = 0;
+  int remaining = top_k;
+  for (int shift = 24; shift >= 0; shift -= 8) {
+    sh.hist[threadIdx.x] = 0;
+    __syncthreads();
+    for (int v = lo; v < hi; ++v) {
+      uint32_t key = fkey(row[v]);
+      if ((key & mask) == prefix) atomicAdd(&sh.hist[(key >> shift) & 255u], 1);
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      int cum = 0, dgt = 255;
+      for (; dgt > 0; --dgt) {
+        if (cum + sh.hist[dgt] >= remaining) break;
+        cum += sh.hist[dgt];
+      }
+      sh.bc_i[0] = dgt;
+      sh.bc_i[1] = remaining - cum;
+    }
+    __syncthreads();
+    prefix |= (uint32_t)sh.bc_i[0] << shift;
+    mask |= 0xFFu << shift;
+    remaining = sh.bc_i[1];
+    __syncthreads();
+  }
+  tk.thr = prefix;
+  tk.need = remaining;
+  // exclusive prefix of ties per thread, in index order
+  int nt = 0;
+  for (int v = lo; v < hi; ++v) nt += (fkey(row[v]) == prefix);
+  sh.tie_base[threadIdx.x] = nt;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int acc = 0;
+    for (int i = 0; i < NT_SEL; ++i) {
+      int c = sh.tie_base[i];
+      sh.tie_base[i] = acc;
+      acc += c;
+    }
+  }
+  __syncthreads();
+  *tie_base_out = sh.tie_base[threadIdx.x];
+  __syncthreads();
+  return tk;
+}
+
+// A warped distribution p_v = [v kept] exp(z_v - mz) / Z, z = row / T.
+struct Warp {
+  const float* row;
+  TopK tk;
+  int tie_base;
+  double T, mz, Z;
+  __device__ __forceinline__ KeepIter iter() const { return KeepIter{tk.thr, tk.need, tie_base, tk.all}; }
+};
+
+__device__ Warp make_warp(const float* row, int V, int top_k, double T, SelShared& sh) {
+  Warp w;
+  w.row = row;
+  int tb;
+  w.tk = topk_select(row, V, top_k, sh, &tb);
+  w.tie_base = tb;
+  w.T = T;
+  const int VPT = (V + NT_SEL - 1) / NT_SEL;
+  const int lo = threadIdx.x * VPT, hi = min(lo + VPT, V);
+  float mx = -INFINITY;
+  for (int v = lo; v < hi; ++v) mx = fmaxf(mx, row[v]);
+  mx = block_max_f(mx, sh);
+  w.mz = (double)mx / T;
+  double s = 0.0;
+  KeepIter it = w.iter();
+  for (int v = lo; v < hi; ++v) {
+    float x = row[v];
+    if (it.next(fkey(x))) s += exp((double)x / T - w.mz);
+  }
+  w.Z = block_sum_d(s, sh);
+  return w;
+}
+
+// probability of one code under a warp (every thread returns the same value)
+__device__ double warp_prob(const Warp& w, int t, int V, SelShared& sh) {
+  const int VPT = (V + NT_SEL - 1) / NT_SEL;
+  const int lo = threadIdx.x * VPT, hi = min(lo + VPT, V);
+  if (t >= lo && t < hi) {
+    KeepIter it = w.iter();
+    double pv = 0.0;
+    for (int v = lo; v <= t; ++v) {
+      float x = w.row[v];
+      bool k = it.next(fkey(x));
+      if (v == t) pv = k ? exp((double)x / w.T - w.mz) / w.Z : 0.0;
+    }
+    sh.bc_d[0] = pv;
+  }
+  __syncthreads();
+  double r = sh.bc_d[0];
+  __syncthreads();
+  return r;
+}
+
+// inverse CDF over per-code weights produced by `wf(v, x_p, keep_p, x_q, keep_q)`;
+// smallest v with cumsum > u * total; fallback: last code of positive weight.
+template <typename WF>
+__device__ int block_invcdf(int V, double u, WF wf, SelShared& sh) {
+  const int VPT = (V + NT_SEL - 1) / NT_SEL;
+  const int lo = threadIdx.x * VPT, hi = min(lo + VPT, V);
+  double s = 0.0;
+  int lastpos = -1;
+  wf.begin();
+  for (int v = lo; v < hi; ++v) {
+    double w = wf(v);
+    s += w;
+    if (w > 0.0) lastpos = v;
+  }
+  sh.pre[threadIdx.x] = s;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    double acc = 0.0;
+    for (int i = 0; i < NT_SEL; ++i) {
+      double c = sh.pre[i];
+      sh.pre[i] = acc;
+      acc += c;
+    }
+    sh.bc_d[1] = acc;
+  }
+  __syncthreads();
+  const double total = sh.bc_d[1];
+  const double target = u * total;
+  double c = sh.pre[threadIdx.x];
+  int cand = 0x7fffffff;
+  wf.begin();
+  for (int v = lo; v < hi; ++v) {
+    c += wf(v);
+    if (c > target) {
+      cand = v;
+      break;
+    }
+  }
+  __syncthreads();
+  int best = block_min_i(cand, sh);
+  if (best == 0x7fffffff) best = block_max_i(lastpos, sh);
+  return best;
+}
+
+// weights of p (normalised)
+struct PW {
+  const Warp* p;
+  KeepIter ip;
+  __device__ void begin() { ip = p->iter(); }
+  __device__ double operator()(int v) {
+    float x = p->row[v];
+    return ip.next(fkey(x)) ? exp((double)x / p->T - p->mz) / p->Z : 0.0;
+  }
+};
+
+// residual [p - q]_+ with q a warp or a point mass at `pt`
+struct RW {
+  const Warp* p;
+  const Warp* q;  // nullptr -> point mass
+  int pt;
+  KeepIter ip, iq;
+  __device__ void begin() {
+    ip = p->iter();
+    if (q) iq = q->iter();
+  }
+  __device__ double operator()(int v) {
+    float x = p->row[v];
+    double pv = ip.next(fkey(x)) ? exp((double)x / p->T - p->mz) / p->Z : 0.0;
+    double qv;
+    if (q) {
+      float y = q->row[v];
+      qv = iq.next(fkey(y)) ? exp((double)y / q->T - q->mz) / q->Z : 0.0;
+    } else {
+      qv = (v == pt) ? 1.0 : 0.0;
+    }
+    double r = pv - qv;
+    return r > 0.0 ? r : 0.0;
+  }
+};
+
+__global__ __launch_bounds__(NT_SEL) void select_kernel(SelectArgs a) {
+  __shared__ SelShared sh;
+  const int k = blockIdx.x, b = blockIdx.y;
+  const int V = a.Vimg;
+  const size_t idx = (size_t)b * a.K + k;
+  if (k < a.n_fixed) {
+    if (threadIdx.x == 0) a.accept[idx] = 0;
+    return;
+  }
+  const float* L = (k == 0) ? a.carry + (size_t)b * V : a.logits + (idx - 1) * V;
+  int t = a.tokens[idx] - a.img_lo;
+  t = t < 0 ? 0 : (t >= V ? V - 1 : t);
+  const int pos = a.f[b] + k;
+  int newt = t;
+  bool acc = false;
+  if (a.rule == SSD_GREEDY || a.truncate) {
+    newt = block_argmax(L, V, sh);
+    acc = (newt == t);
+    if (a.truncate && threadIdx.x == 0) a.amax[idx] = newt;
+  } else {
+    Warp p = make_warp(L, V, a.top_k, a.temperature, sh);
+    if (a.rule == SSD_SAMPLE) {
+      const double u1 = uniform24(a.seed, b, pos, a.round, 1);
+      PW wf{&p, KeepIter{}};
+      newt = block_invcdf(V, u1, wf, sh);
+      acc = (newt == t);
+    } else {
+      const int slot = pos % a.ring;
+      const bool has_ref = a.ref_flag[(size_t)b * a.ring + slot] != 0;
+      float* refrow = a.ref + ((size_t)b * a.ring + slot) * V;
+      Warp q;
+      double qt = 1.0;
+      if (has_ref) {
+        q = make_warp(refrow, V, a.top_k, a.temperature, sh);
+        qt = warp_prob(q, t, V, sh);
+      }
+      const double pt = warp_prob(p, t, V, sh);
+      const double alpha = qt > 0.0 ? fmin(pt / qt, 1.0) : (pt > 0.0 ? 1.0 : 0.0);
+      const double u0 = uniform24(a.seed, b, pos, a.round, 0);
+      if (u0 < alpha) {
+        acc = true;
+      } else {
+        RW wf{&p, has_ref ? &q : nullptr, t, KeepIter{}, KeepIter{}};
+        // total residual mass (same association as the inverse CDF's)
+        const double u1 = uniform24(a.seed, b, pos, a.round, 1);
+        // zero residual (rounding only): keep the token
+        double s = 0.0;
+        {
+          const int VPT = (V + NT_SEL - 1) / NT_SEL;
+          const int lo = threadIdx.x * VPT, hi = min(lo + VPT, V);
+          wf.begin();
+          for (int v = lo; v < hi; ++v) s += wf(v);
+        }
+        const double tot = block_sum_d(s, sh);
+        if (!(tot > 0.0)) {
+          acc = true;
+        } else {
+          newt = block_invcdf(V, u1, wf, sh);
+          acc = false;
+          // the rejected position's reference becomes this round's backbone logits
+          for (int v = threadIdx.x; v < V; v += NT_SEL) refrow[v] = L[v];
+          if (threadIdx.x == 0) a.ref_flag[(size_t)b * a.ring + slot] = 1;
+        }
+      }
+    }
+  }
+  if (threadIdx.x == 0) {
+    a.tokens[idx] = newt + a.img_lo;
+    a.accept[idx] = acc ? 1 : 0;
+    if (acc) atomicAdd(&a.count[b], 1);
+  }
+}
+
+void select_tokens(const SelectArgs& a, hipStream_t st) {
+  hipLaunchKernelGGL(select_kernel, dim3(a.K, a.B), dim3(NT_SEL), 0, st, a);
+}
+
+// truncate mode: accepted run, new frontier and carry
+__global__ __launch_bounds__(256) void truncate_kernel(SelectArgs a, int* f, float* carry) {
+  __shared__ int kk_s;
+  const int b = blockIdx.x;
+  if (threadIdx.x == 0) {
+    int kk = a.n_fixed;
+    while (kk < a.K && a.accept[(size_t)b * a.K + kk]) ++kk;
+    kk_s = kk;
+    a.count[b] = kk - a.n_fixed;
+  }
+  __syncthreads();
+  const int kk = kk_s;
+  if (kk >= 1) {
+    const float* src = a.logits + ((size_t)b * a.K + kk - 1) * a.Vimg;
+    for (int v = threadIdx.x; v < a.Vimg; v += 256) carry[(size_t)b * a.Vimg + v] = src[v];
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) f[b] += kk;
+}
+
+void truncate_finalize(const SelectArgs& a, int* f, hipStream_t st) {
+  hipLaunchKernelGGL(truncate_kernel, dim3(a.B), dim3(256), 0, st, a, f, (float*)a.carry);
+}
+
+// commit: carry <- logits row (b * rps + last); f += f_inc; drop the references of the committed positions
+__global__ __launch_bounds__(256) void commit_kernel(int Vimg, const float* logits, int rps, int last, float* carry,
+                                                     int* f, int f_inc, int* ref_flag, int ring) {
+  const int b = blockIdx.x;
+  const float* src = logits + ((size_t)b * rps + last) * Vimg;
+  for (int v = threadIdx.x; v < Vimg; v += 256) carry[(size_t)b * Vimg + v] = src[v];
+  const int f0 = f[b];
+  if (ref_flag)
+    for (int k = threadIdx.x; k < f_inc && k < ring; k += 256) ref_flag[(size_t)b * ring + (f0 + k) % ring] = 0;
+  __syncthreads();
+  if (threadIdx.x == 0) f[b] = f0 + f_inc;
+}
+
+void commit_update(int B, int K, int Vimg, const float* logits, float* carry, int* f, int* ref_flag, int ring,
+                   hipStream_t st) {
+  // K > 0: logits rows are [B][K], carry from row K-1, f += K.
+  // K < 0: logits rows are [B][1] (last row only), f += -K.
+  int rps = K > 0 ? K : 1, last = K > 0 ? K - 1 : 0, inc = K > 0 ? K : -K;
+  hipLaunchKernelGGL(commit_kernel, dim3(B), dim3(256), 0, st, Vimg, logits, rps, last, carry, f, inc, ref_flag, ring);
+}
+
+__global__ void fill_u32_kernel(unsigned* p, size_t n, unsigned v) {
+  size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) p[i] = v;
+}
+
+void fill_u32(unsigned* p, size_t n, unsigned v, hipStream_t st) {
+  if (n == 0) return;
+  hipLaunchKernelGGL(fill_u32_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, p, n, v);
+}
+
+// rows of src [B][K][Vimg] become the references of positions f+k (only_new: keep existing ones)
+__global__ __launch_bounds__(256) void set_ref_kernel(int rows_per_b, int Vimg, const float* src, const int* f,
+                                                      float* ref, int* ref_flag, int ring, int only_new) {
+  const int k = blockIdx.x, b = blockIdx.y;
+  const int slot = (f[b] + k) % ring;
+  int* fl = ref_flag + (size_t)b * ring + slot;
+  if (only_new && *fl) return;
+  const float* s = src + ((size_t)b * rows_per_b + k) * Vimg;
+  float* d = ref + ((size_t)b * ring + slot) * Vimg;
+  for (int v = threadIdx.x; v < Vimg; v += 256) d[v] = s[v];
+  __syncthreads();
+  if (threadIdx.x == 0) *fl = 1;
+}
+
+void set_ref_rows(int B, int K, int rows_per_b, int Vimg, const float* src, const int* f, float* ref, int* ref_flag,
+                  int ring, int only_new, hipStream_t st) {
+  hipLaunchKernelGGL(set_ref_kernel, dim3(K, B), dim3(256), 0, st, rows_per_b, Vimg, src, f, ref, ref_flag, ring,
+                     only_new);
+}
+
+// first image token from the carry: argmax (rule A) or a sample of the warped carry (uniform stream 2, round 0)
+__global__ __launch_bounds__(NT_SEL) void first_token_kernel(int Vimg, int img_lo, const float* carry, int rule, int top_k,
+                                                              double T, unsigned long long seed, const int* f,
+                                                              int* out_abs, int out_stride) {
+  __shared__ SelShared sh;
+  const int b = blockIdx.x;
+  const float* L = carry + (size_t)b * Vimg;
+  int v;
+  if (rule == SSD_GREEDY) {
+    v = block_argmax(L, Vimg, sh);
+  } else {
+    Warp p = make_warp(L, Vimg, top_k, T, sh);
+    const double u1 = uniform24(seed, b, f[b], 0u, 2);
+    PW wf{&p, KeepIter{}};
+    v = block_invcdf(Vimg, u1, wf, sh);
+  }
+  if (threadIdx.x == 0) out_abs[(size_t)b * out_stride] = v + img_lo;
+}
+
+void first_token(int B, int Vimg, int img_lo, const float* carry, int rule, int top_k, double temperature,
+                 unsigned long long seed, const int* f, int* out_abs, int out_stride, hipStream_t st) {
+  hipLaunchKernelGGL(first_token_kernel, dim3(B), dim3(NT_SEL), 0, st, Vimg, img_lo, carry, rule, top_k, temperature,
+                     seed, f, out_abs, out_stride);
+}
+
+}  // namespace ssd

@@ -1,0 +1,1004 @@
+// C ABI of the SSD verify-step library: model upload, sessions, the verify
+// step and the image schedule driver.  See include/ssd.h for the contract.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "ssd_internal.h"
+
+using namespace ssd;
+
+namespace {
+
+thread_local std::string g_err;
+
+ssd_status fail(ssd_status st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return st;
+}
+
+struct HipError {
+  hipError_t e;
+  const char* what;
+};
+
+#define HIPCHK(x)                                 \
+  do {                                            \
+    hipError_t e_ = (x);                          \
+    if (e_ != hipSuccess) throw HipError{e_, #x}; \
+  } while (0)
+
+// host or device pointer?
+bool is_device_ptr(const void* p) {
+  if (!p) return false;
+  hipPointerAttribute_t attr;
+  hipError_t e = hipPointerGetAttributes(&attr, p);
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    return false;
+  }
+  return attr.type == hipMemoryTypeDevice || attr.type == hipMemoryTypeManaged;
+}
+
+struct Allocs {
+  std::vector<void*> ptrs;
+  ~Allocs() {
+    for (void* p : ptrs) (void)hipFree(p);
+  }
+  template <typename T>
+  T* get(size_t count) {
+    void* p = nullptr;
+    size_t bytes = count * sizeof(T);
+    if (bytes == 0) bytes = 16;
+    hipError_t e = hipMalloc(&p, bytes);
+    if (e != hipSuccess) {
+      (void)hipGetLastError();
+      throw HipError{e, "hipMalloc"};
+    }
+    ptrs.push_back(p);
+    return (T*)p;
+  }
+};
+
+int64_t numel_of(const ssd_model_config& c) {
+  const int64_t d = c.d_model, D = c.head_dim, f = c.d_ff;
+  int64_t per_layer = d + (int64_t)c.n_heads * D * d + 2LL * c.n_kv_heads * D * d + d * (int64_t)c.n_heads * D + d +
+                      2 * f * d + d * f;
+  return (int64_t)c.vocab * d * 2 + d + per_layer * c.n_layers;
+}
+
+ssd_status validate_config(const ssd_model_config* c) {
+  if (!c) return fail(SSD_E_INVAL, "config is NULL");
+  if (c->n_layers < 1 || c->d_model < 2 || c->n_heads < 1 || c->n_kv_heads < 1 || c->head_dim < 2 || c->d_ff < 1 ||
+      c->vocab < 1)
+    return fail(SSD_E_INVAL, "non-positive model dimension");
+  if (c->n_heads % c->n_kv_heads) return fail(SSD_E_INVAL, "n_heads must be a multiple of n_kv_heads");
+  if (c->head_dim % 2) return fail(SSD_E_INVAL, "head_dim must be even");
+  if (c->img_lo < 0 || c->img_hi > c->vocab || c->img_hi - c->img_lo < 2)
+    return fail(SSD_E_INVAL, "image range [%d,%d) invalid for vocab %d", c->img_lo, c->img_hi, c->vocab);
+  if (c->dtype != SSD_F32 && c->dtype != SSD_BF16) return fail(SSD_E_INVAL, "unknown dtype");
+  if (!(c->rms_eps > 0.f) || !(c->rope_theta > 0.f)) return fail(SSD_E_INVAL, "rms_eps and rope_theta must be > 0");
+  if (c->dtype == SSD_BF16) {
+    if (c->d_model % 256 || (c->n_heads * c->head_dim) % 256 || c->d_ff % 256)
+      return fail(SSD_E_INVAL, "bf16 models need d_model, n_heads*head_dim and d_ff multiples of 256");
+    if (c->head_dim != 128 && c->head_dim != 64) return fail(SSD_E_INVAL, "bf16 models need head_dim 64 or 128");
+    if ((c->img_hi - c->img_lo) % 16) return fail(SSD_E_INVAL, "bf16 models need an image range multiple of 16");
+  } else {
+    if ((c->img_hi - c->img_lo) % 2 || c->d_model % 2) return fail(SSD_E_INVAL, "fp32 models need even d_model and image range");
+  }
+  return SSD_OK;
+}
+
+}  // namespace
+
+struct ssd_session;
+
+namespace {
+// event timing of kernel classes (measurement hook)
+struct Prof {
+  bool on = false;
+  std::vector<hipEvent_t> pool;
+  size_t used = 0;
+  struct Mark {
+    int cls;
+    hipEvent_t a, b;
+    double bytes;
+  };
+  std::vector<Mark> marks;
+  double ms[6] = {0, 0, 0, 0, 0, 0}, bytes[6] = {0, 0, 0, 0, 0, 0};
+  int64_t n[6] = {0, 0, 0, 0, 0, 0};
+  hipEvent_t get() {
+    if (used == pool.size()) {
+      hipEvent_t e;
+      HIPCHK(hipEventCreate(&e));
+      pool.push_back(e);
+    }
+    return pool[used++];
+  }
+  // record around a launch sequence
+  template <typename F>
+  void run(int cls, double b, hipStream_t st, F&& f) {
+    if (!on) {
+      f();
+      return;
+    }
+    hipEvent_t e0 = get(), e1 = get();
+    HIPCHK(hipEventRecord(e0, st));
+    f();
+    HIPCHK(hipEventRecord(e1, st));
+    marks.push_back(Mark{cls, e0, e1, b});
+  }
+  // after the stream has drained
+  void flush() {
+    for (const Mark& m : marks) {
+      float t = 0.f;
+      HIPCHK(hipEventElapsedTime(&t, m.a, m.b));
+      ms[m.cls] += t;
+      bytes[m.cls] += m.bytes;
+      n[m.cls] += 1;
+    }
+    marks.clear();
+    used = 0;
+  }
+  ~Prof() {
+    for (hipEvent_t e : pool) (void)hipEventDestroy(e);
+  }
+};
+}  // namespace
+
+struct ssd_model {
+  ssd_model_config cfg;
+  Dims dm;
+  hipStream_t stream;
+  Allocs mem;
+  void* emb = nullptr;
+  std::vector<LayerW> layers;
+  float* gf = nullptr;
+  void* wlm = nullptr;
+  bool poisoned = false;
+  ssd_session* dec = nullptr;  // cached decode workspace
+  int dec_B = 0, dec_P = 0, dec_L = 0, dec_K = 0;
+  Prof prof;
+};
+
+struct ssd_session {
+  ssd_model* m;
+  Dims dm;
+  hipStream_t stream;
+  int B, P, Lmax, Kmax, Mmax, ring;
+  std::vector<int> f;  // host mirror of the frontier
+  bool poisoned = false;
+  Allocs mem;
+  int* d_f;
+  int* tok;         // [Mmax] working token ids
+  unsigned char* acc;
+  int* cnt;
+  int* amax;
+  float* x;
+  void* xn;
+  float* ssq;
+  int ssq_rows_ld;
+  void* q;
+  void* o;
+  void* h;
+  float* logits;
+  float* carry;
+  float* ref;
+  float* refstage;  // device copy of caller-provided reference logits [B][Kmax][V_img]
+  int* ref_flag;
+  void* kc;
+  void* vc;
+  size_t kv_layer_elems;
+  float2* rope;
+  float* gpart;
+  size_t gpart_cap;
+  unsigned* gcnt;
+  size_t gcnt_cap;
+  float* apart;
+  size_t apart_cap;
+  unsigned* acnt;
+  size_t acnt_cap;
+  // decode image buffers
+  int* img = nullptr;    // [B][H*W] working grid (absolute ids)
+  int img_cap = 0;
+  float* qtab = nullptr; // draft logits table for rule C references
+};
+
+namespace {
+
+size_t esize(const Dims& dm) { return dm.bf16 ? 2 : 4; }
+
+// ---------------- forward pass ----------------
+// lm_mode: 0 = logits for all B*K rows; 1 = logits for the last row of each sequence only
+void run_forward(ssd_session* s, int K, int lm_mode) {
+  const Dims& dm = s->dm;
+  ssd_model* m = s->m;
+  hipStream_t st = s->stream;
+  const int B = s->B, M = B * K;
+  const int d = dm.d, D = dm.D;
+  const int Nqkv = (dm.Hq + 2 * dm.Hkv) * D;
+  const size_t es = esize(dm);
+  int max_ctx_now = 0;
+  for (int b = 0; b < B; ++b) max_ctx_now = std::max(max_ctx_now, s->f[b] + K);
+
+  embed(dm, m->emb, s->tok, M, m->layers[0].g1, s->x, s->xn, s->ssq, st);
+  int ssq_parts = 1;
+
+  EpiArgs base{};
+  base.Kblk = K;
+  base.f = s->d_f;
+  base.ssq_ld = s->ssq_rows_ld;
+  base.ssq_off = 0;
+  base.ssq_step = 1;
+  base.inv_d = 1.0f / (float)d;
+  base.eps = dm.eps;
+  base.Lmax = s->Lmax;
+  base.Hq = dm.Hq;
+  base.Hkv = dm.Hkv;
+  base.D = D;
+  base.rope = s->rope;
+  base.x = s->x;
+  base.xn = s->xn;
+  base.ssq_out = s->ssq;
+  base.ssq_out_ld = s->ssq_rows_ld;
+
+  if (dm.bf16) {
+    GemmPlan pq = gemm_plan_bf16(M, Nqkv, d);
+    GemmPlan po = gemm_plan_bf16(M, d, dm.Hq * D);
+    GemmPlan p13 = gemm_plan_bf16(M, 2 * dm.dff, d);
+    GemmPlan p2 = gemm_plan_bf16(M, d, dm.dff);
+    AttnPlan pa = attn_plan(dm, B, K, max_ctx_now);
+    double attn_bytes = 2.0 * M * dm.Hq * D * es;  // q read + o written
+    for (int b = 0; b < B; ++b) attn_bytes += 2.0 * (s->f[b] + K) * dm.Hkv * D * es;
+    for (int l = 0; l < dm.L; ++l) {
+      const LayerW& W = m->layers[l];
+      char* kc = (char*)s->kc + (size_t)l * s->kv_layer_elems * es;
+      char* vc = (char*)s->vc + (size_t)l * s->kv_layer_elems * es;
+      EpiArgs e = base;
+      e.kind = EPI_QKV;
+      e.ssq = s->ssq;
+      e.ssq_parts = ssq_parts;
+      e.q = s->q;
+      e.kc = kc;
+      e.vc = vc;
+      m->prof.run(0, ((double)Nqkv * d + (double)M * d + (double)M * Nqkv) * es, st,
+                  [&] { gemm_bf16(pq, W.wqkv, Nqkv, d, s->xn, d, M, e, s->gpart, nullptr, s->gcnt, st); });
+      m->prof.run(5, attn_bytes, st, [&] {
+        attention_bf16(dm, pa, B, K, s->d_f, s->q, kc, vc, s->Lmax, s->o, s->apart, s->acnt, st);
+      });
+      e = base;
+      e.kind = EPI_RESID;
+      e.ssq = nullptr;
+      e.gnext = W.g2;
+      e.ld = d;
+      m->prof.run(1, ((double)d * dm.Hq * D + (double)M * dm.Hq * D) * es + (double)M * d * (8 + es), st,
+                  [&] { gemm_bf16(po, W.wo, d, dm.Hq * D, s->o, dm.Hq * D, M, e, s->gpart, nullptr, s->gcnt, st); });
+      ssq_parts = po.n_fb;
+      e = base;
+      e.kind = EPI_SWIGLU;
+      e.ssq = s->ssq;
+      e.ssq_parts = ssq_parts;
+      e.h = s->h;
+      e.ld = dm.dff;
+      m->prof.run(2, (2.0 * dm.dff * d + (double)M * d + (double)M * dm.dff) * es, st,
+                  [&] { gemm_bf16(p13, W.w13, 2 * dm.dff, d, s->xn, d, M, e, s->gpart, nullptr, s->gcnt, st); });
+      e = base;
+      e.kind = EPI_RESID;
+      e.ssq = nullptr;
+      e.gnext = (l + 1 < dm.L) ? m->layers[l + 1].g1 : m->gf;
+      e.ld = d;
+      m->prof.run(3, ((double)d * dm.dff + (double)M * dm.dff) * es + (double)M * d * (8 + es), st,
+                  [&] { gemm_bf16(p2, W.w2, d, dm.dff, s->h, dm.dff, M, e, s->gpart, nullptr, s->gcnt, st); });
+      ssq_parts = p2.n_fb;
+    }
+    EpiArgs e = base;
+    e.kind = EPI_LOGITS;
+    e.ssq = s->ssq;
+    e.ssq_parts = ssq_parts;
+    e.logits = s->logits;
+    e.ld = dm.Vimg;
+    if (lm_mode == 0) {
+      GemmPlan pl = gemm_plan_bf16(M, dm.Vimg, d);
+      m->prof.run(4, ((double)dm.Vimg * d + (double)M * d) * es + (double)M * dm.Vimg * 4, st,
+                  [&] { gemm_bf16(pl, m->wlm, dm.Vimg, d, s->xn, d, M, e, s->gpart, nullptr, s->gcnt, st); });
+    } else {
+      e.ssq_off = K - 1;
+      e.ssq_step = K;
+      GemmPlan pl = gemm_plan_bf16(B, dm.Vimg, d);
+      m->prof.run(4, ((double)dm.Vimg * d + (double)B * d) * es + (double)B * dm.Vimg * 4, st, [&] {
+        gemm_bf16(pl, m->wlm, dm.Vimg, d, (const char*)s->xn + (size_t)(K - 1) * d * es, K * d, B, e, s->gpart,
+                  nullptr, s->gcnt, st);
+      });
+    }
+  } else {
+    for (int l = 0; l < dm.L; ++l) {
+      const LayerW& W = m->layers[l];
+      float* kc = (float*)s->kc + (size_t)l * s->kv_layer_elems;
+      float* vc = (float*)s->vc + (size_t)l * s->kv_layer_elems;
+      EpiArgs e = base;
+      e.kind = EPI_QKV;
+      e.ssq = s->ssq;
+      e.ssq_parts = 1;
+      e.q = s->q;
+      e.kc = kc;
+      e.vc = vc;
+      gemm_f32((const float*)W.wqkv, Nqkv, d, (const float*)s->xn, d, M, e, st);
+      attention_f32(dm, B, K, s->d_f, (const float*)s->q, kc, vc, s->Lmax, (float*)s->o, st);
+      e = base;
+      e.kind = EPI_RESID;
+      e.ssq = nullptr;
+      e.gnext = W.g2;
+      e.ld = d;
+      gemm_f32((const float*)W.wo, d, dm.Hq * D, (const float*)s->o, dm.Hq * D, M, e, st);
+      norm_rows_f32(s->x, M, d, nullptr, nullptr, s->ssq, st);
+      e = base;
+      e.kind = EPI_SWIGLU;
+      e.ssq = s->ssq;
+      e.ssq_parts = 1;
+      e.h = s->h;
+      e.ld = dm.dff;
+      gemm_f32((const float*)W.w13, 2 * dm.dff, d, (const float*)s->xn, d, M, e, st);
+      e = base;
+      e.kind = EPI_RESID;
+      e.ssq = nullptr;
+      e.gnext = (l + 1 < dm.L) ? m->layers[l + 1].g1 : m->gf;
+      e.ld = d;
+      gemm_f32((const float*)W.w2, d, dm.dff, (const float*)s->h, dm.dff, M, e, st);
+      norm_rows_f32(s->x, M, d, nullptr, nullptr, s->ssq, st);
+    }
+    EpiArgs e = base;
+    e.kind = EPI_LOGITS;
+    e.ssq = s->ssq;
+    e.ssq_parts = 1;
+    e.logits = s->logits;
+    e.ld = dm.Vimg;
+    if (lm_mode == 0) {
+      gemm_f32((const float*)m->wlm, dm.Vimg, d, (const float*)s->xn, d, M, e, st);
+    } else {
+      e.ssq_off = K - 1;
+      e.ssq_step = K;
+      gemm_f32((const float*)m->wlm, dm.Vimg, d, (const float*)s->xn + (size_t)(K - 1) * d, K * d, B, e, st);
+    }
+  }
+  HIPCHK(hipGetLastError());
+}
+
+// workspace sizes for a session that runs blocks of up to Kmax tokens and a prefill of P
+void size_workspaces(const Dims& dm, int B, int P, int Kmax, int Lmax, size_t& gpart, size_t& gcnt, size_t& apart,
+                     size_t& acnt, int& ssq_parts_max) {
+  gpart = 0;
+  gcnt = 0;
+  apart = 0;
+  acnt = 0;
+  ssq_parts_max = 1;
+  if (!dm.bf16) return;
+  const int Nqkv = (dm.Hq + 2 * dm.Hkv) * dm.D;
+  // every token-tile class a launch chunk can fall in (plans depend on min(M, 128) only)
+  for (int Mc : {1, 16, 17, 32, 33, 64, 65, 128}) {
+    for (auto nk : {std::make_pair(Nqkv, dm.d), std::make_pair(dm.d, dm.Hq * dm.D), std::make_pair(2 * dm.dff, dm.d),
+                    std::make_pair(dm.d, dm.dff), std::make_pair(dm.Vimg, dm.d)}) {
+      GemmPlan p = gemm_plan_bf16(Mc, nk.first, nk.second);
+      gpart = std::max(gpart, gemm_partials_floats(p, Mc));
+      gcnt = std::max(gcnt, (size_t)p.n_fb);
+      if (nk.first == dm.d) ssq_parts_max = std::max(ssq_parts_max, p.n_fb);
+    }
+  }
+  // every block length the session can run, every context up to Lmax
+  std::vector<int> Ks;
+  for (int K = 1; K <= Kmax; ++K) Ks.push_back(K);
+  Ks.push_back(P);
+  for (int K : Ks) {
+    for (int ctx = 1; ctx <= Lmax + 63; ctx += 64) {
+      AttnPlan pc = attn_plan(dm, B, K, std::min(ctx, Lmax));
+      apart = std::max(apart, attn_partials_floats(dm, pc, B));
+      acnt = std::max(acnt, (size_t)B * dm.Hkv * pc.nqg);
+    }
+    AttnPlan pa = attn_plan(dm, B, K, Lmax);
+    apart = std::max(apart, attn_partials_floats(dm, pa, B));
+    acnt = std::max(acnt, (size_t)B * dm.Hkv * pa.nqg);
+  }
+}
+
+ssd_status create_session(ssd_model* m, int B, int P, int Lmax_req, int Kmax, ssd_session** out) {
+  const Dims& dm = m->dm;
+  auto* s = new ssd_session();
+  s->m = m;
+  s->dm = dm;
+  s->stream = m->stream;
+  s->B = B;
+  s->P = P;
+  s->Lmax = ((Lmax_req + 63) / 64) * 64;
+  s->Kmax = Kmax;
+  s->Mmax = B * std::max(P, Kmax);
+  s->ring = Kmax;
+  s->f.assign(B, 0);
+  const size_t es = esize(dm);
+  try {
+    size_t gpart, gcnt, apart, acnt;
+    int ssq_parts;
+    size_workspaces(dm, B, P, Kmax, s->Lmax, gpart, gcnt, apart, acnt, ssq_parts);
+    const size_t M = s->Mmax;
+    s->d_f = s->mem.get<int>(B);
+    s->tok = s->mem.get<int>(M);
+    s->acc = s->mem.get<unsigned char>(M);
+    s->cnt = s->mem.get<int>(B);
+    s->amax = s->mem.get<int>(M);
+    s->x = s->mem.get<float>(M * dm.d);
+    s->xn = s->mem.get<char>(M * dm.d * es);
+    s->ssq_rows_ld = (int)M;
+    s->ssq = s->mem.get<float>((size_t)ssq_parts * M);
+    s->q = s->mem.get<char>(M * dm.Hq * dm.D * es);
+    s->o = s->mem.get<char>(M * dm.Hq * dm.D * es);
+    s->h = s->mem.get<char>(M * dm.dff * es);
+    s->logits = s->mem.get<float>(M * dm.Vimg);
+    s->carry = s->mem.get<float>((size_t)B * dm.Vimg);
+    s->ref = s->mem.get<float>((size_t)B * s->ring * dm.Vimg);
+    s->refstage = s->mem.get<float>((size_t)B * Kmax * dm.Vimg);
+    s->ref_flag = s->mem.get<int>((size_t)B * s->ring);
+    s->kv_layer_elems = (size_t)B * dm.Hkv * s->Lmax * dm.D;
+    s->kc = s->mem.get<char>(s->kv_layer_elems * dm.L * es);
+    s->vc = s->mem.get<char>(s->kv_layer_elems * dm.L * es);
+    s->rope = s->mem.get<float2>((size_t)s->Lmax * (dm.D / 2));
+    s->gpart_cap = gpart;
+    s->gpart = s->mem.get<float>(gpart);
+    s->gcnt_cap = gcnt;
+    s->gcnt = s->mem.get<unsigned>(gcnt);
+    s->apart_cap = apart;
+    s->apart = s->mem.get<float>(apart);
+    s->acnt_cap = acnt;
+    s->acnt = s->mem.get<unsigned>(acnt);
+    hipStream_t st = s->stream;
+    // zero state that kernels read before writing (KV slots beyond the context are multiplied by 0)
+    fill_u32((unsigned*)s->kc, s->kv_layer_elems * dm.L * es / 4, 0u, st);
+    fill_u32((unsigned*)s->vc, s->kv_layer_elems * dm.L * es / 4, 0u, st);
+    fill_u32((unsigned*)s->ref_flag, (size_t)B * s->ring, 0u, st);
+    fill_u32(s->gcnt, gcnt, 0u, st);
+    fill_u32(s->acnt, acnt, 0u, st);
+    fill_u32((unsigned*)s->d_f, B, 0u, st);
+    // rotary table (host double precision, rounded to fp32)
+    std::vector<float2> rope((size_t)s->Lmax * (dm.D / 2));
+    for (int p = 0; p < s->Lmax; ++p)
+      for (int j = 0; j < dm.D / 2; ++j) {
+        double inv = std::pow((double)dm.theta, -2.0 * j / dm.D);
+        double ang = (double)p * inv;
+        rope[(size_t)p * (dm.D / 2) + j] = make_float2((float)std::cos(ang), (float)std::sin(ang));
+      }
+    HIPCHK(hipMemcpyAsync(s->rope, rope.data(), rope.size() * sizeof(float2), hipMemcpyHostToDevice, st));
+    HIPCHK(hipStreamSynchronize(st));
+    HIPCHK(hipGetLastError());
+  } catch (HipError& e) {
+    delete s;
+    if (e.e == hipErrorOutOfMemory || std::string(e.what) == "hipMalloc")
+      return fail(SSD_E_OOM, "device allocation failed (%s)", hipGetErrorString(e.e));
+    return fail(SSD_E_DEVICE, "%s: %s", e.what, hipGetErrorString(e.e));
+  }
+  *out = s;
+  return SSD_OK;
+}
+
+// prefix pass: tokens already in s->tok as [B][P]
+void prefill_pass(ssd_session* s) {
+  run_forward(s, s->P, 1);
+  commit_update(s->B, -s->P, s->dm.Vimg, s->logits, s->carry, s->d_f, s->ref_flag, s->ring, s->stream);
+  for (int b = 0; b < s->B; ++b) s->f[b] = s->P;
+}
+
+ssd_status check_tokens_host(const int32_t* t, size_t n, int lo, int hi, const char* what) {
+  for (size_t i = 0; i < n; ++i)
+    if (t[i] < lo || t[i] >= hi) return fail(SSD_E_INVAL, "%s[%zu] = %d outside [%d, %d)", what, i, t[i], lo, hi);
+  return SSD_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* ssd_last_error(void) { return g_err.c_str(); }
+
+int64_t ssd_weights_numel(const ssd_model_config* cfg) {
+  if (validate_config(cfg) != SSD_OK) return -1;
+  return numel_of(*cfg);
+}
+
+ssd_status ssd_init_model(const ssd_model_config* cfg, const void* weights, void* stream, ssd_model** out) {
+  g_err.clear();
+  if (!out) return fail(SSD_E_INVAL, "out is NULL");
+  *out = nullptr;
+  ssd_status vs = validate_config(cfg);
+  if (vs != SSD_OK) return vs;
+  if (!weights) return fail(SSD_E_INVAL, "weights is NULL");
+  auto* m = new ssd_model();
+  m->cfg = *cfg;
+  Dims& dm = m->dm;
+  dm.L = cfg->n_layers;
+  dm.d = cfg->d_model;
+  dm.Hq = cfg->n_heads;
+  dm.Hkv = cfg->n_kv_heads;
+  dm.D = cfg->head_dim;
+  dm.dff = cfg->d_ff;
+  dm.V = cfg->vocab;
+  dm.img_lo = cfg->img_lo;
+  dm.img_hi = cfg->img_hi;
+  dm.Vimg = cfg->img_hi - cfg->img_lo;
+  dm.bf16 = cfg->dtype == SSD_BF16;
+  dm.eps = cfg->rms_eps;
+  dm.theta = cfg->rope_theta;
+  m->stream = (hipStream_t)stream;
+  const size_t es = esize(dm);
+  const int d = dm.d, D = dm.D, f = dm.dff;
+  const int Nqkv = (dm.Hq + 2 * dm.Hkv) * D;
+  try {
+    hipStream_t st = m->stream;
+    // offsets (elements) of the packed layout
+    const size_t n_emb = (size_t)dm.V * d;
+    const size_t n_layer = d + (size_t)Nqkv * d + (size_t)d * dm.Hq * D + d + 2 * (size_t)f * d + (size_t)d * f;
+    size_t max_seg = std::max({(size_t)Nqkv * d, (size_t)d * dm.Hq * D, 2 * (size_t)f * d, (size_t)d * f,
+                               (size_t)dm.Vimg * d});
+    Allocs tmp;
+    char* stage = tmp.get<char>(max_seg * es);
+    float* gtmp = tmp.get<float>(d);
+    // row maps
+    std::vector<int> map_qkv(Nqkv), map_13(2 * f), map_id(std::max({d, dm.Vimg, 2 * f, Nqkv}));
+    for (int n = 0; n < Nqkv; ++n) {
+      if (n < (dm.Hq + dm.Hkv) * D) {
+        int head = n / D, r = n % D;
+        map_qkv[n] = head * D + ((r % 2 == 0) ? r / 2 : D / 2 + r / 2);
+      } else {
+        map_qkv[n] = n;
+      }
+    }
+    for (int n = 0; n < 2 * f; ++n) map_13[n] = (n % 2 == 0) ? n / 2 : f + n / 2;
+    for (size_t n = 0; n < map_id.size(); ++n) map_id[n] = (int)n;
+    int* d_map_qkv = tmp.get<int>(Nqkv);
+    int* d_map_13 = tmp.get<int>(2 * f);
+    int* d_map_id = tmp.get<int>(map_id.size());
+    HIPCHK(hipMemcpy(d_map_qkv, map_qkv.data(), Nqkv * sizeof(int), hipMemcpyHostToDevice));
+    HIPCHK(hipMemcpy(d_map_13, map_13.data(), 2 * f * sizeof(int), hipMemcpyHostToDevice));
+    HIPCHK(hipMemcpy(d_map_id, map_id.data(), map_id.size() * sizeof(int), hipMemcpyHostToDevice));
+
+    const char* src = (const char*)weights;
+    auto seg = [&](size_t off_elems) { return src + off_elems * es; };
+    auto gain = [&](size_t off) -> float* {
+      float* g = m->mem.get<float>(d);
+      if (dm.bf16) {
+        std::vector<uint16_t> hb(d);
+        HIPCHK(hipMemcpy(hb.data(), seg(off), d * 2, hipMemcpyDefault));
+        std::vector<float> hf(d);
+        for (int i = 0; i < d; ++i) {
+          uint32_t u = (uint32_t)hb[i] << 16;
+          std::memcpy(&hf[i], &u, 4);
+        }
+        HIPCHK(hipMemcpy(g, hf.data(), d * 4, hipMemcpyHostToDevice));
+      } else {
+        HIPCHK(hipMemcpy(g, seg(off), d * 4, hipMemcpyDefault));
+      }
+      return g;
+    };
+    (void)gtmp;
+    // packs the N x K matrix at element offset `off` with `map`
+    auto pack = [&](size_t off, int N, int K, const int* dmap) -> void* {
+      HIPCHK(hipMemcpy(stage, seg(off), (size_t)N * K * es, hipMemcpyDefault));
+      void* dst = m->mem.get<char>((size_t)N * K * es);
+      if (dm.bf16)
+        pack_bf16_tiles((const uint16_t*)stage, dmap, N, K, dst, st);
+      else
+        gather_rows_f32((const float*)stage, dmap, N, K, (float*)dst, st);
+      HIPCHK(hipGetLastError());
+      HIPCHK(hipStreamSynchronize(st));
+      return dst;
+    };
+    m->emb = m->mem.get<char>(n_emb * es);
+    HIPCHK(hipMemcpy(m->emb, seg(0), n_emb * es, hipMemcpyDefault));
+    size_t off = n_emb;
+    m->layers.resize(dm.L);
+    for (int l = 0; l < dm.L; ++l) {
+      LayerW& W = m->layers[l];
+      W.g1 = gain(off);
+      off += d;
+      W.wqkv = pack(off, Nqkv, d, d_map_qkv);
+      off += (size_t)Nqkv * d;
+      W.wo = pack(off, d, dm.Hq * D, d_map_id);
+      off += (size_t)d * dm.Hq * D;
+      W.g2 = gain(off);
+      off += d;
+      W.w13 = pack(off, 2 * f, d, d_map_13);
+      off += 2 * (size_t)f * d;
+      W.w2 = pack(off, d, f, d_map_id);
+      off += (size_t)d * f;
+    }
+    (void)n_layer;
+    m->gf = gain(off);
+    off += d;
+    m->wlm = pack(off + (size_t)dm.img_lo * d, dm.Vimg, d, d_map_id);
+    off += (size_t)dm.V * d;
+    if ((int64_t)off != numel_of(*cfg)) throw HipError{hipErrorInvalidValue, "layout size mismatch"};
+    HIPCHK(hipStreamSynchronize(st));
+  } catch (HipError& e) {
+    delete m;
+    if (e.e == hipErrorOutOfMemory || std::string(e.what) == "hipMalloc")
+      return fail(SSD_E_OOM, "device allocation failed (%s)", hipGetErrorString(e.e));
+    return fail(SSD_E_DEVICE, "%s: %s", e.what, hipGetErrorString(e.e));
+  }
+  *out = m;
+  return SSD_OK;
+}
+
+void ssd_free_session(ssd_session* s) {
+  if (!s) return;
+  if (s->m && s->m->dec == s) s->m->dec = nullptr;
+  (void)hipStreamSynchronize(s->stream);
+  delete s;
+}
+
+void ssd_free_model(ssd_model* m) {
+  if (!m) return;
+  (void)hipStreamSynchronize(m->stream);
+  if (m->dec) {
+    ssd_session* s = m->dec;
+    m->dec = nullptr;
+    delete s;
+  }
+  delete m;
+}
+
+ssd_status ssd_prefill(ssd_model* m, int32_t B, int32_t P, const int32_t* prefix, int32_t max_ctx, int32_t max_block,
+                       void* stream, ssd_session** out) {
+  g_err.clear();
+  if (!m || !prefix || !out) return fail(SSD_E_INVAL, "NULL argument");
+  *out = nullptr;
+  if (m->poisoned) return fail(SSD_E_STATE, "model is poisoned by an earlier device error");
+  if (B < 1 || B >= (1 << 20) || P < 1 || max_block < 1) return fail(SSD_E_INVAL, "bad B/P/max_block");
+  if (max_ctx < P + 1 || max_ctx >= (1 << 24)) return fail(SSD_E_INVAL, "max_ctx must be in [P+1, 2^24)");
+  if (!m->dm.bf16 && max_ctx > 4096) return fail(SSD_E_INVAL, "fp32 models support max_ctx <= 4096");
+  std::vector<int32_t> host((size_t)B * P);
+  if (hipMemcpy(host.data(), prefix, host.size() * 4, hipMemcpyDefault) != hipSuccess) {
+    (void)hipGetLastError();
+    return fail(SSD_E_INVAL, "prefix pointer not readable");
+  }
+  ssd_status cs = check_tokens_host(host.data(), host.size(), 0, m->dm.V, "prefix");
+  if (cs != SSD_OK) return cs;
+  if (stream) m->stream = (hipStream_t)stream;
+  ssd_session* s = nullptr;
+  ssd_status st = create_session(m, B, P, max_ctx, max_block, &s);
+  if (st != SSD_OK) return st;
+  try {
+    HIPCHK(hipMemcpyAsync(s->tok, host.data(), host.size() * 4, hipMemcpyHostToDevice, s->stream));
+    prefill_pass(s);
+    HIPCHK(hipStreamSynchronize(s->stream));
+  } catch (HipError& e) {
+    delete s;
+    m->poisoned = true;
+    return fail(SSD_E_DEVICE, "%s: %s", e.what, hipGetErrorString(e.e));
+  }
+  *out = s;
+  return SSD_OK;
+}
+
+ssd_status ssd_profile(ssd_model* m, int32_t enable) {
+  if (!m) return fail(SSD_E_INVAL, "NULL model");
+  try {
+    HIPCHK(hipStreamSynchronize(m->stream));
+    m->prof.flush();
+    m->prof.on = enable != 0;
+  } catch (HipError& e) {
+    return fail(SSD_E_DEVICE, "%s: %s", e.what, hipGetErrorString(e.e));
+  }
+  return SSD_OK;
+}
+
+ssd_status ssd_profile_read(ssd_model* m, double* ms, int64_t* launches, double* bytes, int32_t reset) {
+  if (!m) return fail(SSD_E_INVAL, "NULL model");
+  try {
+    HIPCHK(hipStreamSynchronize(m->stream));
+    m->prof.flush();
+  } catch (HipError& e) {
+    return fail(SSD_E_DEVICE, "%s: %s", e.what, hipGetErrorString(e.e));
+  }
+  for (int c = 0; c < 6; ++c) {
+    if (ms) ms[c] = m->prof.ms[c];
+    if (launches) launches[c] = m->prof.n[c];
+    if (bytes) bytes[c] = m->prof.bytes[c];
+    if (reset) {
+      m->prof.ms[c] = 0;
+      m->prof.n[c] = 0;
+      m->prof.bytes[c] = 0;
+    }
+  }
+  return SSD_OK;
+}
+
+ssd_status ssd_get_carry(ssd_session* s, float* carry_out) {
+  if (!s || !carry_out) return fail(SSD_E_INVAL, "NULL argument");
+  if (s->poisoned) return fail(SSD_E_STATE, "session is poisoned");
+  if (hipMemcpyAsync(carry_out, s->carry, (size_t)s->B * s->dm.Vimg * 4, hipMemcpyDefault, s->stream) != hipSuccess ||
+      hipStreamSynchronize(s->stream) != hipSuccess) {
+    s->poisoned = true;
+    return fail(SSD_E_DEVICE, "copy of the carry failed");
+  }
+  return SSD_OK;
+}
+
+ssd_status ssd_verify_step(ssd_session* s, int32_t K, int32_t* tokens, const float* ref_logits,
+                           const ssd_verify_params* prm, uint8_t* accept_mask, int32_t* accept_count,
+                           int32_t* frontier, float* logits_out, float* h_pre_out) {
+  g_err.clear();
+  if (!s || !tokens || !prm) return fail(SSD_E_INVAL, "NULL argument");
+  if (s->poisoned) return fail(SSD_E_STATE, "session is poisoned by an earlier device error");
+  const Dims& dm = s->dm;
+  const int B = s->B;
+  if (K < 1 || K > s->Kmax) return fail(SSD_E_INVAL, "K = %d outside [1, max_block = %d]", K, s->Kmax);
+  if (prm->rule < SSD_GREEDY || prm->rule > SSD_ACCEPT_REJECT) return fail(SSD_E_INVAL, "unknown rule");
+  if (!(prm->temperature > 0.0)) return fail(SSD_E_INVAL, "temperature must be > 0");
+  if (prm->n_fixed < 0 || prm->n_fixed > 1 || prm->n_fixed > K) return fail(SSD_E_INVAL, "n_fixed must be 0 or 1 (<= K)");
+  if (prm->round >= 65536u) return fail(SSD_E_INVAL, "round must be < 65536");
+  if (prm->truncate && (prm->commit || prm->rule != SSD_GREEDY))
+    return fail(SSD_E_INVAL, "truncate needs rule SSD_GREEDY and commit = 0");
+  for (int b = 0; b < B; ++b)
+    if (s->f[b] + K > s->Lmax || s->f[b] + K >= (1 << 24))
+      return fail(SSD_E_CAPACITY, "block [%d, %d) of sequence %d exceeds max_ctx", s->f[b], s->f[b] + K, b);
+  const bool tok_dev = is_device_ptr(tokens);
+  std::vector<int32_t> htok;
+  if (!tok_dev) {
+    ssd_status cs = check_tokens_host(tokens, (size_t)B * K, dm.img_lo, dm.img_hi, "tokens");
+    if (cs != SSD_OK) return cs;
+  }
+  const bool host_out = (!tok_dev && !prm->commit) || (accept_mask && !is_device_ptr(accept_mask)) ||
+                        (accept_count && !is_device_ptr(accept_count)) || (frontier && !is_device_ptr(frontier)) ||
+                        (logits_out && !is_device_ptr(logits_out)) || (h_pre_out && !is_device_ptr(h_pre_out));
+  hipStream_t st = s->stream;
+  try {
+    HIPCHK(hipMemcpyAsync(s->tok, tokens, (size_t)B * K * 4, hipMemcpyDefault, st));
+    if (ref_logits && !prm->commit)
+    {
+      // the caller's array may be host memory: stage it on the device first
+      HIPCHK(hipMemcpyAsync(s->refstage, ref_logits, (size_t)B * K * dm.Vimg * 4, hipMemcpyDefault, st));
+      set_ref_rows(B, K, K, dm.Vimg, s->refstage, s->d_f, s->ref, s->ref_flag, s->ring, 0, st);
+    }
+    const bool all_rows = !prm->commit || logits_out;
+    run_forward(s, K, all_rows ? 0 : 1);
+    if (logits_out)
+      HIPCHK(hipMemcpyAsync(logits_out, s->logits, (size_t)B * K * dm.Vimg * 4, hipMemcpyDefault, st));
+    if (h_pre_out) HIPCHK(hipMemcpyAsync(h_pre_out, s->x, (size_t)B * K * dm.d * 4, hipMemcpyDefault, st));
+    if (prm->commit) {
+      commit_update(B, all_rows ? K : -K, dm.Vimg, s->logits, s->carry, s->d_f, s->ref_flag, s->ring, st);
+      for (int b = 0; b < B; ++b) s->f[b] += K;
+    } else {
+      fill_u32((unsigned*)s->cnt, B, 0u, st);
+      SelectArgs a{};
+      a.rule = prm->rule;
+      a.top_k = prm->top_k;
+      a.temperature = prm->temperature;
+      a.seed = prm->seed;
+      a.round = prm->round;
+      a.n_fixed = prm->n_fixed;
+      a.K = K;
+      a.B = B;
+      a.Vimg = dm.Vimg;
+      a.img_lo = dm.img_lo;
+      a.truncate = prm->truncate;
+      a.f = s->d_f;
+      a.tokens = s->tok;
+      a.logits = s->logits;
+      a.carry = s->carry;
+      a.ref = s->ref;
+      a.ref_flag = s->ref_flag;
+      a.ring = s->ring;
+      a.accept = s->acc;
+      a.count = s->cnt;
+      a.amax = s->amax;
+      select_tokens(a, st);
+      if (prm->truncate) truncate_finalize(a, s->d_f, st);
+      HIPCHK(hipGetLastError());
+      HIPCHK(hipMemcpyAsync(tokens, s->tok, (size_t)B * K * 4, hipMemcpyDefault, st));
+      if (accept_mask) HIPCHK(hipMemcpyAsync(accept_mask, s->acc, (size_t)B * K, hipMemcpyDefault, st));
+      if (accept_count) HIPCHK(hipMemcpyAsync(accept_count, s->cnt, (size_t)B * 4, hipMemcpyDefault, st));
+      if (prm->truncate) {
+        HIPCHK(hipMemcpyAsync(s->f.data(), s->d_f, (size_t)B * 4, hipMemcpyDeviceToHost, st));
+        HIPCHK(hipStreamSynchronize(st));
+      }
+    }
+    if (frontier) HIPCHK(hipMemcpyAsync(frontier, s->d_f, (size_t)B * 4, hipMemcpyDefault, st));
+    if (host_out) {
+      HIPCHK(hipStreamSynchronize(st));
+      s->m->prof.flush();
+    }
+  } catch (HipError& e) {
+    s->poisoned = true;
+    return fail(SSD_E_DEVICE, "%s: %s", e.what, hipGetErrorString(e.e));
+  }
+  return SSD_OK;
+}
+
+// ---------------- image schedule driver ----------------
+namespace {
+
+struct Op {
+  int kind;  // 0 verify, 1 commit
+  int start, K, nf, rnd;
+};
+
+// pass plan of one image (mirrors the schedule documented in ssd.h)
+std::vector<Op> make_plan(int H, int W, int k_h, int h_rounds, int k_v, int b, int i) {
+  std::vector<Op> ops;
+  int rnd = 0;
+  auto verify = [&](int start, int K, int nf, int count) {
+    for (int c = 0; c < count; ++c) ops.push_back(Op{0, start, K, nf, rnd++});
+  };
+  bool first = true;
+  for (int s = 1; s < W;) {
+    int e = std::min(s + k_h, W);
+    if (first) {
+      verify(0, e, 1, h_rounds);
+      ops.push_back(Op{1, 0, e, 0, 0});
+      first = false;
+    } else {
+      verify(s, e - s, 0, h_rounds);
+      ops.push_back(Op{1, s, e - s, 0, 0});
+    }
+    s = e;
+  }
+  if (W == 1) ops.push_back(Op{1, 0, 1, 0, 0});
+  for (int y = 1; y < H;) {
+    int m = std::min(k_v, H - y);
+    verify(y * W, m * W, 0, b);
+    ops.push_back(Op{1, y * W, W, 0, 0});
+    for (int j = 1; j < m; ++j) {
+      verify((y + j) * W, (m - j) * W, 0, i);
+      ops.push_back(Op{1, (y + j) * W, W, 0, 0});
+    }
+    y += m;
+  }
+  return ops;
+}
+
+}  // namespace
+
+ssd_status ssd_decode_image(ssd_model* m, const ssd_schedule* sc, int32_t B, int32_t P, const int32_t* prefix,
+                            const int32_t* drafts, const float* draft_logits, int32_t* out_tokens, ssd_stats* stats,
+                            void* stream) {
+  g_err.clear();
+  if (!m || !sc || !prefix || !drafts || !out_tokens) return fail(SSD_E_INVAL, "NULL argument");
+  if (m->poisoned) return fail(SSD_E_STATE, "model is poisoned by an earlier device error");
+  const Dims& dm = m->dm;
+  const int H = sc->grid_h, W = sc->grid_w;
+  if (H < 1 || W < 1 || B < 1 || B >= (1 << 20) || P < 1) return fail(SSD_E_INVAL, "bad grid, batch or prefix size");
+  if (sc->k_h < 1 || sc->h_rounds < 0 || sc->k_v < 1 || sc->b_rounds < 0 || sc->i_rounds < 0)
+    return fail(SSD_E_INVAL, "bad schedule");
+  if (sc->rule < SSD_GREEDY || sc->rule > SSD_ACCEPT_REJECT || !(sc->temperature > 0.0))
+    return fail(SSD_E_INVAL, "bad rule or temperature");
+  const int N = H * W;
+  const int Lmax = P + N;
+  if (Lmax >= (1 << 24)) return fail(SSD_E_INVAL, "image too large");
+  if (!dm.bf16 && Lmax > 4096) return fail(SSD_E_INVAL, "fp32 models support P + H*W <= 4096");
+  std::vector<Op> ops = make_plan(H, W, sc->k_h, sc->h_rounds, sc->k_v, sc->b_rounds, sc->i_rounds);
+  int Kmax = 1;
+  int nverify = 0;
+  for (const Op& o : ops) {
+    Kmax = std::max(Kmax, o.K);
+    nverify += o.kind == 0;
+  }
+  if (nverify >= 65536) return fail(SSD_E_INVAL, "more than 65535 verify rounds");
+  std::vector<int32_t> hpre((size_t)B * P), hdr((size_t)B * N);
+  if (hipMemcpy(hpre.data(), prefix, hpre.size() * 4, hipMemcpyDefault) != hipSuccess ||
+      hipMemcpy(hdr.data(), drafts, hdr.size() * 4, hipMemcpyDefault) != hipSuccess) {
+    (void)hipGetLastError();
+    return fail(SSD_E_INVAL, "prefix or drafts not readable");
+  }
+  ssd_status cs = check_tokens_host(hpre.data(), hpre.size(), 0, dm.V, "prefix");
+  if (cs != SSD_OK) return cs;
+  cs = check_tokens_host(hdr.data(), hdr.size(), dm.img_lo, dm.img_hi, "drafts");
+  if (cs != SSD_OK) return cs;
+  if (stream) m->stream = (hipStream_t)stream;
+  // decode workspace, reused across calls of the same shape
+  if (!m->dec || m->dec_B != B || m->dec_P != P || m->dec_L != Lmax || m->dec_K != Kmax) {
+    if (m->dec) {
+      ssd_session* old = m->dec;
+      m->dec = nullptr;
+      delete old;
+    }
+    ssd_session* s = nullptr;
+    ssd_status st = create_session(m, B, P, Lmax, Kmax, &s);
+    if (st != SSD_OK) return st;
+    m->dec = s;
+    m->dec_B = B;
+    m->dec_P = P;
+    m->dec_L = Lmax;
+    m->dec_K = Kmax;
+  }
+  ssd_session* s = m->dec;
+  s->stream = m->stream;
+  hipStream_t st = s->stream;
+  int64_t passes = 0, nv = 0, proposed = 0;
+  try {
+    if (s->img_cap < B * N) {
+      s->img = s->mem.get<int>((size_t)B * N);
+      s->img_cap = B * N;
+    }
+    if (draft_logits && !s->qtab) s->qtab = s->mem.get<float>((size_t)B * N * dm.Vimg);
+    HIPCHK(hipMemcpyAsync(s->img, hdr.data(), hdr.size() * 4, hipMemcpyHostToDevice, st));
+    if (draft_logits)
+      HIPCHK(hipMemcpyAsync(s->qtab, draft_logits, (size_t)B * N * dm.Vimg * 4, hipMemcpyDefault, st));
+    fill_u32((unsigned*)s->d_f, B, 0u, st);
+    fill_u32((unsigned*)s->ref_flag, (size_t)B * s->ring, 0u, st);
+    fill_u32((unsigned*)s->cnt, B, 0u, st);
+    for (int b = 0; b < B; ++b) s->f[b] = 0;
+    HIPCHK(hipMemcpyAsync(s->tok, hpre.data(), hpre.size() * 4, hipMemcpyHostToDevice, st));
+    prefill_pass(s);
+    ++passes;
+    first_token(B, dm.Vimg, dm.img_lo, s->carry, sc->rule, sc->top_k, sc->temperature, sc->seed, s->d_f, s->img, N, st);
+    SelectArgs a{};
+    a.rule = sc->rule;
+    a.top_k = sc->top_k;
+    a.temperature = sc->temperature;
+    a.seed = sc->seed;
+    a.B = B;
+    a.Vimg = dm.Vimg;
+    a.img_lo = dm.img_lo;
+    a.f = s->d_f;
+    a.tokens = s->tok;
+    a.logits = s->logits;
+    a.carry = s->carry;
+    a.ref = s->ref;
+    a.ref_flag = s->ref_flag;
+    a.ring = s->ring;
+    a.accept = s->acc;
+    a.count = s->cnt;
+    a.amax = s->amax;
+    for (const Op& o : ops) {
+      HIPCHK(hipMemcpy2DAsync(s->tok, (size_t)o.K * 4, s->img + o.start, (size_t)N * 4, (size_t)o.K * 4, B,
+                              hipMemcpyDeviceToDevice, st));
+      if (o.kind == 0) {
+        if (sc->rule == SSD_ACCEPT_REJECT && draft_logits) {
+          // first round of a position: its reference is its draft distribution
+          // (positions that already hold a reference keep it)
+          set_ref_rows(B, o.K, N, dm.Vimg, s->qtab + (size_t)o.start * dm.Vimg, s->d_f, s->ref, s->ref_flag, s->ring,
+                       1, st);
+        }
+        run_forward(s, o.K, 0);
+        a.K = o.K;
+        a.n_fixed = o.nf;
+        a.round = (unsigned)o.rnd;
+        select_tokens(a, st);
+        HIPCHK(hipMemcpy2DAsync(s->img + o.start, (size_t)N * 4, s->tok, (size_t)o.K * 4, (size_t)o.K * 4, B,
+                                hipMemcpyDeviceToDevice, st));
+        ++nv;
+        proposed += (int64_t)B * (o.K - o.nf);
+      } else {
+        run_forward(s, o.K, 1);
+        commit_update(B, -o.K, dm.Vimg, s->logits, s->carry, s->d_f, s->ref_flag, s->ring, st);
+        for (int b = 0; b < B; ++b) s->f[b] += o.K;
+      }
+      ++passes;
+    }
+    HIPCHK(hipGetLastError());
+    HIPCHK(hipMemcpyAsync(out_tokens, s->img, (size_t)B * N * 4, hipMemcpyDefault, st));
+    std::vector<int> hc(B);
+    HIPCHK(hipMemcpyAsync(hc.data(), s->cnt, (size_t)B * 4, hipMemcpyDeviceToHost, st));
+    HIPCHK(hipStreamSynchronize(st));
+    m->prof.flush();
+    if (stats) {
+      stats->passes = passes;
+      stats->verify_rounds = nv;
+      stats->proposed = proposed;
+      int64_t acc = 0;
+      for (int v : hc) acc += v;
+      stats->accepted = acc;
+    }
+  } catch (HipError& e) {
+    m->poisoned = true;
+    return fail(SSD_E_DEVICE, "%s: %s", e.what, hipGetErrorString(e.e));
+  }
+  return SSD_OK;
+}
+
+}  // extern "C"

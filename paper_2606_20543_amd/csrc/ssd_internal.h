@@ -1,0 +1,150 @@
+// Internal declarations of the SSD verify-step library (gfx950).
+//
+// Data layout in HBM (all row-major unless stated):
+//   residual x        fp32 [M][d]
+//   xn                model dtype [M][d]      bf16(g * x): the GEMM input after an RMSNorm
+//   ssq               fp32 [parts][Mmax]      partial sums of x^2 per token (producer feature blocks)
+//   q                 model dtype [B][Hq][K][D]   (query row r = head_in_group * K + k)
+//   K cache           model dtype [L][B][Hkv][Lmax][D]
+//   V cache (transp.) model dtype [L][B][Hkv][D][Lmax]
+//   o                 model dtype [M][Hq*D]   attention output
+//   h                 model dtype [M][d_ff]   SwiGLU product
+//   logits            fp32 [M][V_img]
+// bf16 weight matrices W[N][K] are prepacked into 16x32 MFMA A-operand tiles:
+//   tile (nb, kb) = 64 lanes x 8 bf16, lane l holds W[nb*16 + l%16][kb*32 + 8*(l/16) + e]
+//   tiles ordered nb-major, so one wave reads 1 KiB contiguous per tile.
+// Row permutations applied at packing so that each lane's four consecutive
+// output features hold two (even, odd) pairs an epilogue needs together:
+//   q/k rows: within a head, packed row 2j <- dim j, 2j+1 <- dim j + D/2 (rotary pair)
+//   w1/w3:    packed row 2j <- gate row j, 2j+1 <- up row j (SwiGLU pair)
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/ssd.h"
+
+namespace ssd {
+
+struct Dims {
+  int L, d, Hq, Hkv, D, dff, V, img_lo, img_hi, Vimg;
+  bool bf16;
+  float eps, theta;
+};
+
+enum EpiKind { EPI_QKV = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_LOGITS = 3 };
+
+// Arguments of a GEMM epilogue.  Token index t (0..M-1 of the whole call)
+// maps to sequence b = t / Kblk and block position k = t % Kblk.
+struct EpiArgs {
+  int kind;
+  int Kblk;
+  const int* f;          // [B] block start positions (device)
+  // rms scale: r_t = 1/sqrt(sum_p ssq[p*ssq_ld + t] / d + eps); ssq == nullptr -> r = 1
+  const float* ssq;
+  int ssq_parts, ssq_ld;
+  int ssq_off, ssq_step;  // token t reads column ssq_off + t * ssq_step
+  float inv_d, eps;
+  // EPI_QKV
+  void* q;
+  void* kc;
+  void* vc;
+  int Lmax, Hq, Hkv, D;
+  const float2* rope;    // [Lmax][D/2] (cos, sin)
+  // EPI_RESID: x += v; xn = bf16(gnext * x); ssq_out[fb][t] = sum over the block's features of x^2
+  float* x;
+  void* xn;
+  const float* gnext;
+  float* ssq_out;
+  int ssq_out_ld;
+  // EPI_SWIGLU
+  void* h;
+  // EPI_LOGITS
+  float* logits;
+  // common leading dimensions (elements)
+  int ld;                // x / xn / h / logits row length
+};
+
+// Device model (owned by ssd_model)
+struct LayerW {
+  float* g1;
+  float* g2;
+  void* wqkv;  // N = (Hq + 2 Hkv) D, K = d   (packed)
+  void* wo;    // N = d, K = Hq D
+  void* w13;   // N = 2 dff, K = d
+  void* w2;    // N = d, K = dff
+};
+
+// GEMM launch plan for one (M, N, K) problem.
+struct GemmPlan {
+  int MT, NT, KCB;  // token tiles, feature tiles per wave, 32-k blocks per chunk
+  int S;            // K splits
+  int n_fb;         // feature blocks
+  int kchunks;      // chunks per split
+  int bn;           // features per workgroup
+};
+
+// ---- launchers (kernels_*.hip) ----
+GemmPlan gemm_plan_bf16(int M, int N, int K);
+size_t gemm_partials_floats(const GemmPlan& p, int M);
+// y = W x for bf16 inputs in[M][K] (row stride ld_in); epilogue per `epi`.
+void gemm_bf16(const GemmPlan& p, const void* Wpacked, int N, int K, const void* in, int ld_in, int M,
+               const EpiArgs& epi, float* partials, float* ssq_part, unsigned* counters, hipStream_t st);
+void gemm_f32(const float* W, int N, int K, const float* in, int ld_in, int M, const EpiArgs& epi, hipStream_t st);
+
+void pack_bf16_tiles(const uint16_t* src, const int* rowmap, int N, int K, void* dst, hipStream_t st);
+void gather_rows_f32(const float* src, const int* rowmap, int N, int K, float* dst, hipStream_t st);
+
+// x[t] = E[tok[t]]; xn = g * x (rounded to the model dtype); ssq[t] = sum x^2 (one part)
+void embed(const Dims& dm, const void* emb, const int* tok, int M, const float* g, float* x, void* xn, float* ssq,
+           hipStream_t st);
+// fp32 path: xn = g * x, ssq[t] = sum x^2 (one part)
+void norm_rows_f32(const float* x, int M, int d, const float* g, float* xn, float* ssq, hipStream_t st);
+
+struct AttnPlan {
+  int chunk;      // keys per workgroup
+  int nchunk;     // chunks covering max context
+  int qpw;        // query tiles per workgroup
+  int nqg;        // query groups
+  int rows;       // query rows per (b, kv head) = K * g
+};
+AttnPlan attn_plan(const Dims& dm, int B, int K, int max_ctx_now);
+size_t attn_partials_floats(const Dims& dm, const AttnPlan& p, int B);
+void attention_bf16(const Dims& dm, const AttnPlan& p, int B, int K, const int* f, const void* q, const void* kc,
+                    const void* vc, int Lmax, void* o, float* partials, unsigned* counters, hipStream_t st);
+void attention_f32(const Dims& dm, int B, int K, const int* f, const float* q, const float* kc, const float* vc,
+                   int Lmax, float* o, hipStream_t st);
+
+struct SelectArgs {
+  int rule, top_k;
+  double temperature;
+  unsigned long long seed;
+  unsigned round;
+  int n_fixed, K, B, Vimg, img_lo;
+  int truncate;
+  const int* f;
+  int* tokens;             // [B][K] absolute ids (in/out)
+  const float* logits;     // [B*K][Vimg]
+  const float* carry;      // [B][Vimg]
+  float* ref;              // ring [B][ring][Vimg]
+  int* ref_flag;           // ring [B][ring]
+  int ring;
+  unsigned char* accept;   // [B][K]
+  int* count;              // [B]
+  int* amax;               // [B][K] greedy argmax (truncate mode)
+};
+void select_tokens(const SelectArgs& a, hipStream_t st);
+// truncate mode: leading accepted run, f update, pending token
+void truncate_finalize(const SelectArgs& a, int* f, hipStream_t st);
+// commit bookkeeping: carry <- logits[b*K + K-1]; f += K; clear ring flags of committed positions
+void commit_update(int B, int K, int Vimg, const float* logits, float* carry, int* f, int* ref_flag, int ring,
+                   hipStream_t st);
+// fill helpers (graph-capture safe)
+void fill_u32(unsigned* p, size_t n, unsigned v, hipStream_t st);
+// references of block positions f+k <- src rows (b * rows_per_b + k); only_new keeps existing references
+void set_ref_rows(int B, int K, int rows_per_b, int Vimg, const float* src, const int* f, float* ref, int* ref_flag,
+                  int ring, int only_new, hipStream_t st);
+void first_token(int B, int Vimg, int img_lo, const float* carry, int rule, int top_k, double temperature,
+                 unsigned long long seed, const int* f, int* out_abs, int out_stride, hipStream_t st);
+
+}  // namespace ssd

@@ -1,0 +1,102 @@
+"""Helpers for GPU parity tests: build a model on the GPU through the C ABI and
+run the oracle beside it on the same seeded inputs.
+
+Parity protocol (decisions under bf16 logits):
+  1. logits: GPU vs oracle within the dtype's tolerance (2e-2 bf16, 1e-5 fp32);
+  2. decisions: the oracle's rule applied to the GPU's own logits (and the
+     same counter-based uniforms) reproduces the GPU's tokens, accept flags
+     and counts exactly;
+  3. end to end: where the oracle's rule on the oracle's logits disagrees with
+     the GPU, the disagreement must be one that the logit tolerance allows (a
+     greedy top-2 gap within twice the tolerance); both sides then continue
+     from the GPU's tokens (re-sync).
+"""
+import numpy as np
+
+import paper_2606_20543_amd as ssd
+import synth
+from oracle import decode as Dc
+from oracle import model as M
+from oracle import select as R
+
+TOL = {"f32": 1e-5, "bf16": 2e-2}
+
+
+def cfg_of(shape):
+    c = ssd.ssd_model_config()
+    c.n_layers, c.d_model, c.n_heads, c.n_kv_heads = shape.n_layers, shape.d_model, shape.n_heads, shape.n_kv_heads
+    c.head_dim, c.d_ff, c.vocab = shape.head_dim, shape.d_ff, shape.vocab
+    c.img_lo, c.img_hi = shape.img_lo, shape.img_hi
+    c.dtype = ssd.SSD_BF16 if shape.dtype == "bf16" else ssd.SSD_F32
+    c.rms_eps, c.rope_theta = 1e-5, 10000.0
+    return c
+
+
+def oracle_cfg(shape):
+    return M.Config(shape.n_layers, shape.d_model, shape.n_heads, shape.n_kv_heads, shape.head_dim, shape.d_ff,
+                    shape.vocab, shape.img_lo, shape.img_hi, shape.dtype)
+
+
+class Pair:
+    """A model loaded on the GPU and in the oracle from the same packed weights."""
+
+    def __init__(self, shape, seed=0, gain_std=0.0, oracle=True):
+        self.shape = shape
+        self.w = synth.weights(shape, seed=seed, gain_std=gain_std)
+        self.cfg = cfg_of(shape)
+        assert ssd.ssd_weights_numel(self.cfg) == self.w.size
+        self.model = ssd.ssd_init_model(self.cfg, self.w)
+        self.om = M.Model(oracle_cfg(shape), self.w) if oracle else None
+
+    def close(self):
+        if self.model:
+            ssd.ssd_free_model(self.model)
+            self.model = None
+
+
+def vparams(rule=R.RULE_GREEDY, top_k=0, T=1.0, seed=3, rnd=0, n_fixed=0, commit=0, truncate=0):
+    p = ssd.ssd_verify_params()
+    p.rule, p.top_k, p.temperature, p.seed = rule, top_k, T, seed
+    p.round, p.n_fixed, p.commit, p.truncate = rnd, n_fixed, commit, truncate
+    return p
+
+
+def gpu_verify(sess, shape, block_abs, prm, ref=None, want_h=False):
+    """One ssd_verify_step with host buffers; returns dict of outputs."""
+    B, K = block_abs.shape
+    tok = np.ascontiguousarray(block_abs.astype(np.int32))
+    acc = np.zeros((B, K), np.uint8)
+    cnt = np.zeros(B, np.int32)
+    fr = np.zeros(B, np.int32)
+    lg = np.zeros((B, K, shape.v_img), np.float32)
+    hp = np.zeros((B, K, shape.d_model), np.float32) if want_h else None
+    ssd.ssd_verify_step(sess, K, tok, prm, ref_logits=ref, accept_mask=acc, accept_count=cnt, frontier=fr,
+                        logits_out=lg, h_pre_out=hp)
+    return {"tokens": tok, "accept": acc.astype(bool), "count": cnt, "frontier": fr, "logits": lg, "h_pre": hp}
+
+
+def oracle_rule_on(logits_gpu, carry_gpu, block_codes, n_fixed, rule, rnd, seed, f, T=1.0, top_k=0, refs=None):
+    """Apply the oracle's rule to given (GPU) logits; returns (codes, accept, count, refs_after)."""
+    B, K = block_codes.shape
+    new = block_codes.copy()
+    acc = np.zeros((B, K), bool)
+    refs_after = None if refs is None else [list(r) for r in refs]
+    for b in range(B):
+        for k in range(n_fixed, K):
+            L = carry_gpu[b] if k == 0 else logits_gpu[b, k - 1]
+            L = L.astype(np.float64)
+            pos = int(f[b]) + k
+            u0 = R.uniform(seed, b, pos, rnd, 0)
+            u1 = R.uniform(seed, b, pos, rnd, 1)
+            rk = None if refs is None else refs[b][k]
+            t, a, repl = R.select_position(rule, L, int(block_codes[b, k]), rk, u0, u1, T, top_k)
+            new[b, k] = t
+            acc[b, k] = a
+            if repl and refs_after is not None:
+                refs_after[b][k] = L
+    return new, acc, acc[:, n_fixed:].sum(axis=1), refs_after
+
+
+def greedy_gap(L):
+    s = np.sort(np.asarray(L, np.float64))
+    return s[-1] - s[-2]

@@ -1,0 +1,143 @@
+"""GPU parity on the 1B-class bf16 decoder (24 layers, d=2048, 16x128 heads,
+MLP 5632, 16384 image codes, 64-token prompt): verify rounds and commits at
+the real shapes of the 24x24 batch-1 greedy workload and of the 32x32
+batch-4 top-k 2000 accept-reject workload, against the oracle under the
+parity protocol of tests/gpu_util.py (logits within 2e-2; decisions exact on
+the GPU's logits; end-to-end flips only where the logit tolerance allows)."""
+import numpy as np
+import pytest
+
+import paper_2606_20543_amd as ssd
+import synth
+from oracle import decode as Dc
+from oracle import select as R
+from tests import gpu_util as G
+
+pytestmark = pytest.mark.gpu
+
+SHAPE = synth.M1B
+TOL = G.TOL["bf16"]
+
+
+@pytest.fixture(scope="module")
+def pair():
+    print("building 1B model (GPU + oracle)", flush=True)
+    p = G.Pair(SHAPE)
+    yield p
+    p.close()
+
+
+def _check_round(sess, os_, blk, nf, rule, rnd, top_k, ref, stats, K):
+    B = blk.shape[0]
+    carry = np.zeros((B, SHAPE.v_img), np.float32)
+    ssd.ssd_get_carry(sess, carry)
+    f_before = os_.f.copy()
+    assert np.abs(carry - os_.carry).max() < TOL
+    out = G.gpu_verify(sess, SHAPE, blk + SHAPE.img_lo, G.vparams(rule, top_k=top_k, rnd=rnd, n_fixed=nf),
+                       ref=None if ref is None else np.ascontiguousarray(ref, np.float32))
+    refs = None
+    if ref is not None:
+        refs = [[ref[b, k].astype(np.float64) for k in range(K)] for b in range(B)]
+    gnew, gacc, gcnt, _ = G.oracle_rule_on(out["logits"], carry, blk, nf, rule, rnd, 3, f_before, 1.0, top_k, refs)
+    onew, oacc, _, ologits = Dc.verify_round(os_, blk, nf, rule, rnd, 3, 1.0, top_k,
+                                             None if refs is None else [list(r) for r in refs])
+    err = np.abs(out["logits"] - ologits).max()
+    stats["max_logit_err"] = max(stats.get("max_logit_err", 0.0), float(err))
+    assert err < TOL, f"logit error {err}"
+    assert np.array_equal(out["tokens"] - SHAPE.img_lo, gnew)
+    assert np.array_equal(out["accept"][:, nf:], gacc[:, nf:])
+    assert np.array_equal(out["count"], gcnt)
+    assert list(out["frontier"]) == list(f_before)
+    diff = np.argwhere(onew != gnew)
+    stats["flips"] = stats.get("flips", 0) + len(diff)
+    stats["positions"] = stats.get("positions", 0) + B * (K - nf)
+    if rule == R.RULE_GREEDY:
+        for b, k in diff:
+            L = os_.carry[b] if k == 0 else ologits[b, k - 1]
+            assert G.greedy_gap(L) < 2 * TOL, "greedy flip at a clear argmax"
+    return gnew, out
+
+
+def test_1b_greedy_rows(pair):
+    """24x24 batch-1 greedy workload: prompt, the first horizontal run (6 tokens,
+    first fixed), then two 24-token blocks with 2 rounds + commit each."""
+    B, P = 1, 64
+    pre = synth.prompt(SHAPE, B, P)
+    print("oracle greedy AR for planting", flush=True)
+    ar = Dc.ar_decode(pair.om, pre, 54)
+    drafts = synth.plant(ar, 0.6, SHAPE.v_img)
+    sess = ssd.ssd_prefill(pair.model, B, P, pre, P + 576, 24)
+    os_ = Dc.prefill(pair.om, pre, P + 576)
+    stats = {}
+    try:
+        work = drafts.copy()
+        work[:, 0] = [R.argmax_lowest(os_.carry[b]) for b in range(B)]
+        blocks = [(0, 6, 1, 1), (6, 24, 0, 2), (30, 24, 0, 2)]
+        rnd = 0
+        for start, K, nf, rounds in blocks:
+            for _ in range(rounds):
+                blk = work[:, start:start + K].copy()
+                gnew, _ = _check_round(sess, os_, blk, nf, R.RULE_GREEDY, rnd, 0, None, stats, K)
+                work[:, start:start + K] = gnew
+                rnd += 1
+            blk = work[:, start:start + K]
+            out = G.gpu_verify(sess, SHAPE, blk + SHAPE.img_lo, G.vparams(commit=1), want_h=True)
+            ol, oh = Dc.commit(os_, blk)
+            assert np.abs(out["logits"] - ol).max() < TOL
+            assert np.abs(out["h_pre"] - oh).max() < 0.05 * np.abs(oh).max()
+            assert list(out["frontier"]) == list(os_.f)
+        print("1b greedy parity stats", stats, flush=True)
+        assert stats["flips"] <= 0.02 * stats["positions"] + 1
+    finally:
+        ssd.ssd_free_session(sess)
+
+
+def test_1b_b4_accept_reject_topk(pair):
+    """32x32 batch-4 workload: top-k 2000, T = 1, rule (C) with draft
+    distributions q (random logits, draft = argmax q), two rounds (the second
+    uses the stored references) and a commit."""
+    B, P, K, top_k = 4, 64, 32, 2000
+    pre = synth.prompt(SHAPE, B, P)
+    q = synth.normal(synth.SEED_DRAFTS, 7, B * K * SHAPE.v_img, std=1.5).reshape(B, K, SHAPE.v_img)
+    drafts = q.argmax(axis=2).astype(np.int64)
+    sess = ssd.ssd_prefill(pair.model, B, P, pre, P + 1024, K)
+    os_ = Dc.prefill(pair.om, pre, P + 1024)
+    stats = {}
+    try:
+        blk = drafts.copy()
+        refs_state = q.astype(np.float64)
+        gnew, out = _check_round(sess, os_, blk, 0, R.RULE_ACCEPT_REJECT, 0, top_k, q, stats, K)
+        # second round: GPU uses its stored references; the oracle gets the same
+        # (accepted: the draft q; rejected: the first round's GPU scoring logits)
+        carry1 = None
+        blk2 = gnew.copy()
+        acc1 = out["accept"]
+        lg1 = out["logits"]
+        carry1 = np.zeros((B, SHAPE.v_img), np.float32)
+        ssd.ssd_get_carry(sess, carry1)
+        ref2 = np.empty_like(q)
+        for b in range(B):
+            for k in range(K):
+                if acc1[b, k]:
+                    ref2[b, k] = q[b, k]
+                else:
+                    ref2[b, k] = carry1[b] if k == 0 else lg1[b, k - 1]
+        f_before = os_.f.copy()
+        out2 = G.gpu_verify(sess, SHAPE, blk2 + SHAPE.img_lo, G.vparams(R.RULE_ACCEPT_REJECT, top_k=top_k, rnd=1))
+        refs2 = [[ref2[b, k].astype(np.float64) for k in range(K)] for b in range(B)]
+        g2, a2, c2, _ = G.oracle_rule_on(out2["logits"], carry1, blk2, 0, R.RULE_ACCEPT_REJECT, 1, 3, f_before, 1.0,
+                                         top_k, refs2)
+        assert np.array_equal(out2["tokens"] - SHAPE.img_lo, g2)
+        assert np.array_equal(out2["accept"], a2) and np.array_equal(out2["count"], c2)
+        ol2 = Dc.verify_round(os_, blk2, 0, R.RULE_ACCEPT_REJECT, 1, 3, 1.0, top_k, [list(r) for r in refs2])[3]
+        assert np.abs(out2["logits"] - ol2).max() < TOL
+        # commit
+        out3 = G.gpu_verify(sess, SHAPE, g2 + SHAPE.img_lo, G.vparams(commit=1))
+        ol3, _ = Dc.commit(os_, g2)
+        assert np.abs(out3["logits"] - ol3).max() < TOL
+        assert list(out3["frontier"]) == [P + K] * B
+        print("1b rule C parity stats", stats, "accepted r1", int(acc1.sum()), "r2", int(a2.sum()), flush=True)
+        assert stats["flips"] <= 0.05 * stats["positions"] + 1
+        del refs_state
+    finally:
+        ssd.ssd_free_session(sess)
