@@ -63,6 +63,7 @@ def splitmix64_stream(seed, n):
 
 
 def counter(b, pos, rnd, stream):
+    b, pos, rnd, stream = int(b), int(pos), int(rnd), int(stream)  # Python ints: no 64-bit overflow
     assert 0 <= b < (1 << 20) and 0 <= pos < (1 << 24)
     assert 0 <= rnd < (1 << 16) and 0 <= stream < 16
     return (b << 44) | (pos << 20) | (rnd << 4) | stream

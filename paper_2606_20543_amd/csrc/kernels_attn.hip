@@ -30,10 +30,11 @@ __device__ __forceinline__ uint16_t f2bf_a(float f) {
 }
 
 struct AttnKArgs {
-  const uint16_t* q;   // [B][Hq][K][D]
+  const uint16_t* q;   // [B][Hq][K][D], hi plane then lo plane (q_plane elements apart)
   const uint16_t* kc;  // [B][Hkv][Lmax][D]
   const uint16_t* vc;  // [B][Hkv][D][Lmax]
-  uint16_t* o;         // [B*K][Hq*D]
+  uint16_t* o;         // [B*K][Hq*D], hi plane then lo plane (o_plane elements apart)
+  size_t q_plane, o_plane;
   float* part;         // [B*Hkv][nqg][nchunk][QPW*16][D+2]
   unsigned* counters;  // [B*Hkv][nqg]
   const int* f;
@@ -58,8 +59,9 @@ __global__ __launch_bounds__(64) void attn_bf16_kernel(AttnKArgs a) {
   const int kend = min(kbeg + a.chunk, ctx);
   const int rbase = qg * QPW * 16;
 
-  // query fragments (B operand of S^T = K Q^T): lane holds row col of tile qt, d = 8*grp.. (+32 kd)
-  bf16x8 qf[QPW][KD];
+  // query fragments (B operand of S^T = K Q^T): lane holds row col of tile qt, d = 8*grp.. (+32 kd);
+  // q is fp32 carried as hi + lo bf16 operands
+  bf16x8 qh[QPW][KD], ql[QPW][KD];
   int qpos[QPW];
 #pragma unroll
   for (int qt = 0; qt < QPW; ++qt) {
@@ -70,8 +72,10 @@ __global__ __launch_bounds__(64) void attn_bf16_kernel(AttnKArgs a) {
     const uint16_t* qp = a.q + (((size_t)b * a.Hq + hkv * a.g + j) * a.K + k) * D + grp * 8;
 #pragma unroll
     for (int kd = 0; kd < KD; ++kd) {
-      uint4 v = ok ? *(const uint4*)(qp + kd * 32) : make_uint4(0, 0, 0, 0);
-      qf[qt][kd] = __builtin_bit_cast(bf16x8, v);
+      uint4 vh = ok ? *(const uint4*)(qp + kd * 32) : make_uint4(0, 0, 0, 0);
+      uint4 vl = ok ? *(const uint4*)(qp + a.q_plane + kd * 32) : make_uint4(0, 0, 0, 0);
+      qh[qt][kd] = __builtin_bit_cast(bf16x8, vh);
+      ql[qt][kd] = __builtin_bit_cast(bf16x8, vl);
     }
   }
 
@@ -103,7 +107,10 @@ __global__ __launch_bounds__(64) void attn_bf16_kernel(AttnKArgs a) {
       for (int qt = 0; qt < QPW; ++qt) {
         floatx4 acc = floatx4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int kd = 0; kd < KD; ++kd) acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[kd], qf[qt][kd], acc, 0, 0, 0);
+        for (int kd = 0; kd < KD; ++kd) {
+          acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[kd], qh[qt][kd], acc, 0, 0, 0);
+          acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[kd], ql[qt][kd], acc, 0, 0, 0);
+        }
         s[kt][qt] = acc;
       }
     }
@@ -142,25 +149,32 @@ __global__ __launch_bounds__(64) void attn_bf16_kernel(AttnKArgs a) {
       const bool none = (mnew == -INFINITY);
       const float alpha = none ? 1.f : exp2f(m[qt] - mnew);
       float ps = 0.f;
-      uint16_t pb[8];
+      uint16_t pb[8], pl[8];
 #pragma unroll
       for (int i = 0; i < 8; ++i) {
         float p = none ? 0.f : exp2f(sv[i] - mnew);
         ps += p;
         pb[i] = f2bf_a(p);
+        pl[i] = f2bf_a(p - __uint_as_float((uint32_t)pb[i] << 16));
       }
       l[qt] = l[qt] * alpha + ps;
       m[qt] = mnew;
-      uint4 pv;
+      uint4 pv, pw;
       pv.x = (uint32_t)pb[0] | ((uint32_t)pb[1] << 16);
       pv.y = (uint32_t)pb[2] | ((uint32_t)pb[3] << 16);
       pv.z = (uint32_t)pb[4] | ((uint32_t)pb[5] << 16);
       pv.w = (uint32_t)pb[6] | ((uint32_t)pb[7] << 16);
+      pw.x = (uint32_t)pl[0] | ((uint32_t)pl[1] << 16);
+      pw.y = (uint32_t)pl[2] | ((uint32_t)pl[3] << 16);
+      pw.z = (uint32_t)pl[4] | ((uint32_t)pl[5] << 16);
+      pw.w = (uint32_t)pl[6] | ((uint32_t)pl[7] << 16);
       bf16x8 pf = __builtin_bit_cast(bf16x8, pv);
+      bf16x8 pg = __builtin_bit_cast(bf16x8, pw);
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt) {
         O[qt][dt] *= alpha;
         O[qt][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf[dt], pf, O[qt][dt], 0, 0, 0);
+        O[qt][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf[dt], pg, O[qt][dt], 0, 0, 0);
       }
     }
   }
@@ -182,10 +196,20 @@ __global__ __launch_bounds__(64) void attn_bf16_kernel(AttnKArgs a) {
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt) {
         const int d0 = dt * 16 + 4 * grp;
-        uint2 w;
-        w.x = (uint32_t)f2bf_a(O[qt][dt][0] * inv) | ((uint32_t)f2bf_a(O[qt][dt][1] * inv) << 16);
-        w.y = (uint32_t)f2bf_a(O[qt][dt][2] * inv) | ((uint32_t)f2bf_a(O[qt][dt][3] * inv) << 16);
+        uint16_t hi[4], lo[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const float v = O[qt][dt][e] * inv;
+          hi[e] = f2bf_a(v);
+          lo[e] = f2bf_a(v - __uint_as_float((uint32_t)hi[e] << 16));
+        }
+        uint2 w, x;
+        w.x = (uint32_t)hi[0] | ((uint32_t)hi[1] << 16);
+        w.y = (uint32_t)hi[2] | ((uint32_t)hi[3] << 16);
+        x.x = (uint32_t)lo[0] | ((uint32_t)lo[1] << 16);
+        x.y = (uint32_t)lo[2] | ((uint32_t)lo[3] << 16);
         *(uint2*)(op + d0) = w;
+        *(uint2*)(op + a.o_plane + d0) = x;
       }
     }
     return;
@@ -244,7 +268,12 @@ __global__ __launch_bounds__(64) void attn_bf16_kernel(AttnKArgs a) {
     uint16_t* op = a.o + ((size_t)b * a.K + k) * (a.Hq * D) + (hkv * a.g + j) * D;
     const float inv = 1.f / L;
 #pragma unroll
-    for (int i = 0; i < D / 64; ++i) op[lane + 64 * i] = f2bf_a(acc[i] * inv);
+    for (int i = 0; i < D / 64; ++i) {
+      const float v = acc[i] * inv;
+      const uint16_t hi = f2bf_a(v);
+      op[lane + 64 * i] = hi;
+      op[a.o_plane + lane + 64 * i] = f2bf_a(v - __uint_as_float((uint32_t)hi << 16));
+    }
   }
   if (lane == 0) a.counters[(size_t)z * a.nqg + qg] = 0u;
 }
@@ -254,7 +283,7 @@ AttnPlan attn_plan(const Dims& dm, int B, int K, int max_ctx_now) {
   const int g = dm.Hq / dm.Hkv;
   p.rows = K * g;
   const int qt = (p.rows + 15) / 16;
-  p.qpw = qt >= 4 ? 4 : qt >= 2 ? 2 : 1;
+  p.qpw = qt >= 2 ? 2 : 1;
   p.nqg = (qt + p.qpw - 1) / p.qpw;
   // chunk: enough workgroups to cover the chip, at least 64 keys
   const int units = B * dm.Hkv * p.nqg;
@@ -274,13 +303,16 @@ static void launch_attn(const AttnKArgs& a, int nchunk, int nqg, int z, hipStrea
   hipLaunchKernelGGL((attn_bf16_kernel<D, QPW>), dim3(nchunk, nqg, z), dim3(64), 0, st, a);
 }
 
-void attention_bf16(const Dims& dm, const AttnPlan& p, int B, int K, const int* f, const void* q, const void* kc,
-                    const void* vc, int Lmax, void* o, float* partials, unsigned* counters, hipStream_t st) {
+void attention_bf16(const Dims& dm, const AttnPlan& p, int B, int K, const int* f, const void* q, size_t q_plane,
+                    const void* kc, const void* vc, int Lmax, void* o, size_t o_plane, float* partials,
+                    unsigned* counters, hipStream_t st) {
   AttnKArgs a;
   a.q = (const uint16_t*)q;
   a.kc = (const uint16_t*)kc;
   a.vc = (const uint16_t*)vc;
   a.o = (uint16_t*)o;
+  a.q_plane = q_plane;
+  a.o_plane = o_plane;
   a.part = partials;
   a.counters = counters;
   a.f = f;
@@ -296,12 +328,10 @@ void attention_bf16(const Dims& dm, const AttnPlan& p, int B, int K, const int* 
   a.scale_log2 = 1.4426950408889634f / sqrtf((float)dm.D);
   const int z = B * dm.Hkv;
   if (dm.D == 128) {
-    if (p.qpw == 4) launch_attn<128, 4>(a, p.nchunk, p.nqg, z, st);
-    else if (p.qpw == 2) launch_attn<128, 2>(a, p.nchunk, p.nqg, z, st);
+    if (p.qpw == 2) launch_attn<128, 2>(a, p.nchunk, p.nqg, z, st);
     else launch_attn<128, 1>(a, p.nchunk, p.nqg, z, st);
   } else {
-    if (p.qpw == 4) launch_attn<64, 4>(a, p.nchunk, p.nqg, z, st);
-    else if (p.qpw == 2) launch_attn<64, 2>(a, p.nchunk, p.nqg, z, st);
+    if (p.qpw == 2) launch_attn<64, 2>(a, p.nchunk, p.nqg, z, st);
     else launch_attn<64, 1>(a, p.nchunk, p.nqg, z, st);
   }
 }

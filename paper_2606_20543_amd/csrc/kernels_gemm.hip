@@ -1,8 +1,8 @@
 // Projection GEMMs of the backbone forward pass, y[t][n] = sum_k in[t][k] W[n][k],
 // with the epilogues the verify step needs fused into the final write:
 //   QKV    : 1/rms scale, rotary embedding at the token's raster position,
-//            q to the query buffer, k/v into the KV cache slots [f, f+K)
-//   RESID  : x += y; xn = bf16(g_next * x); per-block sums of x^2 for the next 1/rms
+//            q to the query buffer, k/v (bf16) into the KV cache slots [f, f+K)
+//   RESID  : x += y; xn = g_next * x; per-block sums of x^2 for the next 1/rms
 //   SWIGLU : h = silu(gate / rms) * (up / rms)
 //   LOGITS : logits = y / rms  (fp32)
 //
@@ -12,9 +12,10 @@
 // 16-byte load per lane fetches a whole A operand), the token rows of the
 // current K-chunk sit in LDS (B operand, shared by the four waves), and the
 // A loads of the next chunk are in flight while the current one is
-// multiplied.  When N/64 feature blocks cannot fill 256 CUs the K range is
-// split; the last workgroup of a feature block sums the partials in split
-// order (deterministic) and runs the epilogue.
+// multiplied.  Activations arrive as hi/lo bf16 planes (fp32 precision), so
+// each A tile meets two B operands.  When N/64 feature blocks cannot fill
+// 256 CUs the K range is split; the last workgroup of a feature block sums
+// the partials in split order (deterministic) and runs the epilogue.
 #include "ssd_internal.h"
 
 namespace ssd {
@@ -29,12 +30,27 @@ __device__ __forceinline__ uint16_t f2bf(float f) {
   return (uint16_t)(u >> 16);
 }
 
+__device__ __forceinline__ float bf2f(uint16_t h) { return __uint_as_float(((uint32_t)h) << 16); }
+
+// stored state: bf16 for bf16 models (KV cache)
 template <bool BF>
-__device__ __forceinline__ void st_act(void* base, size_t i, float v) {
+__device__ __forceinline__ void st_state(void* base, size_t i, float v) {
   if (BF)
     ((uint16_t*)base)[i] = f2bf(v);
   else
     ((float*)base)[i] = v;
+}
+
+// activation: hi/lo bf16 planes for bf16 models, fp32 otherwise
+template <bool BF>
+__device__ __forceinline__ void st_split(void* base, size_t plane, size_t i, float v) {
+  if (BF) {
+    uint16_t hi = f2bf(v);
+    ((uint16_t*)base)[i] = hi;
+    ((uint16_t*)base)[plane + i] = f2bf(v - bf2f(hi));
+  } else {
+    ((float*)base)[i] = v;
+  }
 }
 
 __device__ __forceinline__ float rms_scale(const EpiArgs& e, int t) {
@@ -64,17 +80,21 @@ __device__ __forceinline__ float epi_pair(const EpiArgs& e, int t, int n, float 
         const float2 cs = e.rope[(size_t)pos * half + j];
         const float a = v0 * cs.x - v1 * cs.y;  // dim j
         const float c = v1 * cs.x + v0 * cs.y;  // dim j + D/2
-        size_t base = isq ? (((size_t)b * e.Hq + head) * e.Kblk + k) * D
-                          : (((size_t)b * e.Hkv + head) * e.Lmax + pos) * D;
-        void* dst = isq ? e.q : e.kc;
-        st_act<BF>(dst, base + j, a);
-        st_act<BF>(dst, base + j + half, c);
+        if (isq) {
+          size_t base = (((size_t)b * e.Hq + head) * e.Kblk + k) * D;
+          st_split<BF>(e.q, e.q_plane, base + j, a);
+          st_split<BF>(e.q, e.q_plane, base + j + half, c);
+        } else {
+          size_t base = (((size_t)b * e.Hkv + head) * e.Lmax + pos) * D;
+          st_state<BF>(e.kc, base + j, a);
+          st_state<BF>(e.kc, base + j + half, c);
+        }
       } else {
         const int nv = n - qN - kN;
         const int head = nv / D, dd = nv - head * D;
         size_t base = (((size_t)b * e.Hkv + head) * D + dd) * e.Lmax + pos;
-        st_act<BF>(e.vc, base, v0);
-        st_act<BF>(e.vc, base + e.Lmax, v1);
+        st_state<BF>(e.vc, base, v0);
+        st_state<BF>(e.vc, base + e.Lmax, v1);
       }
       return 0.f;
     }
@@ -83,14 +103,14 @@ __device__ __forceinline__ float epi_pair(const EpiArgs& e, int t, int n, float 
       float2 xo = *(const float2*)(e.x + i);
       float x0 = xo.x + v0, x1 = xo.y + v1;
       *(float2*)(e.x + i) = make_float2(x0, x1);
-      st_act<BF>(e.xn, i, e.gnext[n] * x0);
-      st_act<BF>(e.xn, i + 1, e.gnext[n + 1] * x1);
+      st_split<BF>(e.xn, e.xn_plane, i, e.gnext[n] * x0);
+      st_split<BF>(e.xn, e.xn_plane, i + 1, e.gnext[n + 1] * x1);
       return x0 * x0 + x1 * x1;
     }
     case EPI_SWIGLU: {
       float g = v0 * r, u = v1 * r;
       float s = g / (1.0f + expf(-g));
-      st_act<BF>(e.h, (size_t)t * e.ld + (n >> 1), s * u);
+      st_split<BF>(e.h, e.h_plane, (size_t)t * e.ld + (n >> 1), s * u);
       return 0.f;
     }
     default: {  // EPI_LOGITS
@@ -106,6 +126,7 @@ struct GemmKArgs {
   int N, K, KB;
   int S, kchunks, n_fb;
   const uint16_t* in;
+  size_t in_plane;
   int ld_in;
   int M, t0;
   float* part;
@@ -134,33 +155,43 @@ struct XStage {
   static constexpr int MP = MT * 16;
   static constexpr int KC = KCB * 32;
   static constexpr int LD = KC + 8;          // bf16 per LDS row (16-byte pad)
+  static constexpr int PL = MP * LD;         // one plane
   static constexpr int CG = KC / 8;          // 16-byte column groups per row
   static constexpr int RSTEP = 256 / CG;     // rows covered per pass
   static constexpr int PASSES = (MP + RSTEP - 1) / RSTEP;
 };
 
+// x chunk (both planes) -> registers
 template <int MT, int KCB, int NP>
-__device__ __forceinline__ void load_x(u32x4 (&rx)[NP], const uint16_t* in, int ld_in, int M, int k0) {
+__device__ __forceinline__ void load_x(u32x4 (&rx)[2][NP], const uint16_t* in, size_t plane, int ld_in, int M,
+                                       int k0) {
   using X = XStage<MT, KCB>;
   const int cg = threadIdx.x % X::CG, r0 = threadIdx.x / X::CG;
 #pragma unroll
-  for (int p = 0; p < X::PASSES; ++p) {
+  for (int p = 0; p < NP; ++p) {
     int r = r0 + p * X::RSTEP;
-    if (r < M && r < X::MP)
-      rx[p] = *(const u32x4*)(in + (size_t)r * ld_in + k0 + cg * 8);
-    else
-      rx[p] = u32x4{0u, 0u, 0u, 0u};
+    if (r < M && r < X::MP) {
+      const uint16_t* src = in + (size_t)r * ld_in + k0 + cg * 8;
+      rx[0][p] = *(const u32x4*)src;
+      rx[1][p] = *(const u32x4*)(src + plane);
+    } else {
+      rx[0][p] = u32x4{0u, 0u, 0u, 0u};
+      rx[1][p] = u32x4{0u, 0u, 0u, 0u};
+    }
   }
 }
 
 template <int MT, int KCB, int NP>
-__device__ __forceinline__ void store_x(const u32x4 (&rx)[NP], uint16_t* xs) {
+__device__ __forceinline__ void store_x(const u32x4 (&rx)[2][NP], uint16_t* xs) {
   using X = XStage<MT, KCB>;
   const int cg = threadIdx.x % X::CG, r0 = threadIdx.x / X::CG;
 #pragma unroll
-  for (int p = 0; p < X::PASSES; ++p) {
+  for (int p = 0; p < NP; ++p) {
     int r = r0 + p * X::RSTEP;
-    if (r < X::MP) *(u32x4*)(xs + r * X::LD + cg * 8) = rx[p];
+    if (r < X::MP) {
+      *(u32x4*)(xs + r * X::LD + cg * 8) = rx[0][p];
+      *(u32x4*)(xs + X::PL + r * X::LD + cg * 8) = rx[1][p];
+    }
   }
 }
 
@@ -171,17 +202,21 @@ __device__ __forceinline__ void compute_chunk(floatx4 (&acc)[NT][MT], const u32x
   const int row = lane & 15, col = (lane >> 4) * 8;
 #pragma unroll
   for (int kb = 0; kb < KCB; ++kb) {
-    bf16x8 bfr[MT];
+    bf16x8 bhi[MT], blo[MT];
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
-      u32x4 v = *(const u32x4*)(xs + (mt * 16 + row) * X::LD + kb * 32 + col);
-      bfr[mt] = __builtin_bit_cast(bf16x8, v);
+      const uint16_t* p = xs + (mt * 16 + row) * X::LD + kb * 32 + col;
+      bhi[mt] = __builtin_bit_cast(bf16x8, *(const u32x4*)p);
+      blo[mt] = __builtin_bit_cast(bf16x8, *(const u32x4*)(p + X::PL));
     }
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
       bf16x8 a = __builtin_bit_cast(bf16x8, ra[nt][kb]);
 #pragma unroll
-      for (int mt = 0; mt < MT; ++mt) acc[nt][mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, bfr[mt], acc[nt][mt], 0, 0, 0);
+      for (int mt = 0; mt < MT; ++mt) {
+        acc[nt][mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, bhi[mt], acc[nt][mt], 0, 0, 0);
+        acc[nt][mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, blo[mt], acc[nt][mt], 0, 0, 0);
+      }
     }
   }
 }
@@ -189,7 +224,7 @@ __device__ __forceinline__ void compute_chunk(floatx4 (&acc)[NT][MT], const u32x
 template <int MT, int NT, int KCB>
 __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmKArgs a) {
   using X = XStage<MT, KCB>;
-  __shared__ __attribute__((aligned(16))) uint16_t xs[2][X::MP * X::LD];
+  __shared__ __attribute__((aligned(16))) uint16_t xs[2][2 * X::PL];
   __shared__ float sq_red[4][X::MP];
   __shared__ float rscale[X::MP];
   __shared__ int is_last;
@@ -208,15 +243,15 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmKArgs a) {
     for (int mt = 0; mt < MT; ++mt) acc[nt][mt] = floatx4{0.f, 0.f, 0.f, 0.f};
 
   u32x4 ra[2][NT][KCB];
-  u32x4 rx[X::PASSES];
+  u32x4 rx[2][X::PASSES];
 
-  load_x<MT, KCB>(rx, in, a.ld_in, a.M, kb_split * 32);
+  load_x<MT, KCB>(rx, in, a.in_plane, a.ld_in, a.M, kb_split * 32);
   load_a<NT, KCB>(ra[0], a.W, a.KB, nb0, a.N, kb_split, lane);
   store_x<MT, KCB>(rx, xs[0]);
   __syncthreads();
   for (int c = 0; c < nc; c += 2) {
     if (c + 1 < nc) {
-      load_x<MT, KCB>(rx, in, a.ld_in, a.M, (kb_split + (c + 1) * KCB) * 32);
+      load_x<MT, KCB>(rx, in, a.in_plane, a.ld_in, a.M, (kb_split + (c + 1) * KCB) * 32);
       load_a<NT, KCB>(ra[1], a.W, a.KB, nb0, a.N, kb_split + (c + 1) * KCB, lane);
     }
     compute_chunk<MT, NT, KCB>(acc, ra[0], xs[0], lane);
@@ -224,7 +259,7 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmKArgs a) {
     __syncthreads();
     if (c + 1 >= nc) break;
     if (c + 2 < nc) {
-      load_x<MT, KCB>(rx, in, a.ld_in, a.M, (kb_split + (c + 2) * KCB) * 32);
+      load_x<MT, KCB>(rx, in, a.in_plane, a.ld_in, a.M, (kb_split + (c + 2) * KCB) * 32);
       load_a<NT, KCB>(ra[0], a.W, a.KB, nb0, a.N, kb_split + (c + 2) * KCB, lane);
     }
     compute_chunk<MT, NT, KCB>(acc, ra[1], xs[1], lane);
@@ -240,7 +275,8 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmKArgs a) {
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt)
 #pragma unroll
-      for (int mt = 0; mt < MT; ++mt) *(floatx4*)(P + (size_t)s * split_stride + ((nt * MT + mt) * 64 + lane) * 4) = acc[nt][mt];
+      for (int mt = 0; mt < MT; ++mt)
+        *(floatx4*)(P + (size_t)s * split_stride + ((nt * MT + mt) * 64 + lane) * 4) = acc[nt][mt];
     __threadfence();
     __syncthreads();
     if (threadIdx.x == 0) {
@@ -256,7 +292,8 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmKArgs a) {
       for (int mt = 0; mt < MT; ++mt) {
         floatx4 v = floatx4{0.f, 0.f, 0.f, 0.f};
         for (int s2 = 0; s2 < a.S; ++s2) {
-          floatx4 pv = __builtin_nontemporal_load((const floatx4*)(P + (size_t)s2 * split_stride + ((nt * MT + mt) * 64 + lane) * 4));
+          floatx4 pv = __builtin_nontemporal_load(
+              (const floatx4*)(P + (size_t)s2 * split_stride + ((nt * MT + mt) * 64 + lane) * 4));
           v += pv;
         }
         acc[nt][mt] = v;
@@ -310,7 +347,7 @@ GemmPlan gemm_plan_bf16(int M, int N, int K) {
   GemmPlan p;
   int Mc = M < 128 ? M : 128;
   p.MT = Mc <= 16 ? 1 : Mc <= 32 ? 2 : Mc <= 64 ? 4 : 8;
-  p.KCB = p.MT >= 8 ? 2 : p.MT == 4 ? 4 : 8;
+  p.KCB = p.MT == 1 ? 8 : p.MT == 2 ? 4 : p.MT == 4 ? 2 : 1;
   p.NT = p.MT >= 4 ? 2 : 1;
   p.bn = 4 * p.NT * 16;
   p.n_fb = (N + p.bn - 1) / p.bn;
@@ -340,9 +377,8 @@ static void launch_gemm(const GemmKArgs& a, int n_fb, int S, hipStream_t st) {
   hipLaunchKernelGGL((gemm_bf16_kernel<MT, NT, KCB>), dim3(n_fb, S), dim3(256), 0, st, a);
 }
 
-void gemm_bf16(const GemmPlan& p, const void* Wpacked, int N, int K, const void* in, int ld_in, int M,
-               const EpiArgs& epi, float* partials, float* ssq_part, unsigned* counters, hipStream_t st) {
-  (void)ssq_part;
+void gemm_bf16(const GemmPlan& p, const void* Wpacked, int N, int K, const void* in, size_t in_plane, int ld_in,
+               int M, const EpiArgs& epi, float* partials, unsigned* counters, hipStream_t st) {
   const int MP = p.MT * 16;
   for (int t0 = 0; t0 < M; t0 += MP) {
     GemmKArgs a;
@@ -354,6 +390,7 @@ void gemm_bf16(const GemmPlan& p, const void* Wpacked, int N, int K, const void*
     a.kchunks = p.kchunks;
     a.n_fb = p.n_fb;
     a.in = (const uint16_t*)in + (size_t)t0 * ld_in;
+    a.in_plane = in_plane;
     a.ld_in = ld_in;
     a.M = (M - t0) < MP ? (M - t0) : MP;
     a.t0 = t0;
@@ -362,9 +399,9 @@ void gemm_bf16(const GemmPlan& p, const void* Wpacked, int N, int K, const void*
     a.epi = epi;
     switch (p.MT) {
       case 1: launch_gemm<1, 1, 8>(a, p.n_fb, p.S, st); break;
-      case 2: launch_gemm<2, 1, 8>(a, p.n_fb, p.S, st); break;
-      case 4: launch_gemm<4, 2, 4>(a, p.n_fb, p.S, st); break;
-      default: launch_gemm<8, 2, 2>(a, p.n_fb, p.S, st); break;
+      case 2: launch_gemm<2, 1, 4>(a, p.n_fb, p.S, st); break;
+      case 4: launch_gemm<4, 2, 2>(a, p.n_fb, p.S, st); break;
+      default: launch_gemm<8, 2, 1>(a, p.n_fb, p.S, st); break;
     }
   }
 }

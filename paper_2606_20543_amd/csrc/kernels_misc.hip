@@ -27,7 +27,7 @@ __device__ __forceinline__ uint16_t f2bf_m(float f) {
 // ---------------- embedding ----------------
 template <bool BF>
 __global__ __launch_bounds__(256) void embed_kernel(const void* emb, const int* tok, int d, int V, const float* g,
-                                                    float* x, void* xn, float* ssq) {
+                                                    float* x, void* xn, size_t xn_plane, float* ssq) {
   __shared__ float red[256];
   const int t = blockIdx.x;
   int id = tok[t];
@@ -38,10 +38,14 @@ __global__ __launch_bounds__(256) void embed_kernel(const void* emb, const int* 
                  : ((const float*)emb)[(size_t)id * d + i];
     x[(size_t)t * d + i] = v;
     float gv = g[i] * v;
-    if (BF)
-      ((uint16_t*)xn)[(size_t)t * d + i] = f2bf_m(gv);
-    else
+    if (BF) {
+      // fp32 activation as hi + lo bf16 planes
+      const uint16_t hi = f2bf_m(gv);
+      ((uint16_t*)xn)[(size_t)t * d + i] = hi;
+      ((uint16_t*)xn)[xn_plane + (size_t)t * d + i] = f2bf_m(gv - __uint_as_float((uint32_t)hi << 16));
+    } else {
       ((float*)xn)[(size_t)t * d + i] = gv;
+    }
     s += v * v;
   }
   red[threadIdx.x] = s;
@@ -53,12 +57,12 @@ __global__ __launch_bounds__(256) void embed_kernel(const void* emb, const int* 
   if (threadIdx.x == 0) ssq[t] = red[0];
 }
 
-void embed(const Dims& dm, const void* emb, const int* tok, int M, const float* g, float* x, void* xn, float* ssq,
-           hipStream_t st) {
+void embed(const Dims& dm, const void* emb, const int* tok, int M, const float* g, float* x, void* xn,
+           size_t xn_plane, float* ssq, hipStream_t st) {
   if (dm.bf16)
-    hipLaunchKernelGGL(embed_kernel<true>, dim3(M), dim3(256), 0, st, emb, tok, dm.d, dm.V, g, x, xn, ssq);
+    hipLaunchKernelGGL(embed_kernel<true>, dim3(M), dim3(256), 0, st, emb, tok, dm.d, dm.V, g, x, xn, xn_plane, ssq);
   else
-    hipLaunchKernelGGL(embed_kernel<false>, dim3(M), dim3(256), 0, st, emb, tok, dm.d, dm.V, g, x, xn, ssq);
+    hipLaunchKernelGGL(embed_kernel<false>, dim3(M), dim3(256), 0, st, emb, tok, dm.d, dm.V, g, x, xn, xn_plane, ssq);
 }
 
 __global__ __launch_bounds__(256) void ssq_kernel(const float* x, int d, float* ssq) {

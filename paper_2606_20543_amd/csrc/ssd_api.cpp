@@ -188,6 +188,7 @@ struct ssd_session {
   void* xn;
   float* ssq;
   int ssq_rows_ld;
+  size_t xn_plane, q_plane, o_plane, h_plane;  // lo-plane offsets (elements) of the split activations
   void* q;
   void* o;
   void* h;
@@ -231,7 +232,7 @@ void run_forward(ssd_session* s, int K, int lm_mode) {
   int max_ctx_now = 0;
   for (int b = 0; b < B; ++b) max_ctx_now = std::max(max_ctx_now, s->f[b] + K);
 
-  embed(dm, m->emb, s->tok, M, m->layers[0].g1, s->x, s->xn, s->ssq, st);
+  embed(dm, m->emb, s->tok, M, m->layers[0].g1, s->x, s->xn, s->xn_plane, s->ssq, st);
   int ssq_parts = 1;
 
   EpiArgs base{};
@@ -251,15 +252,25 @@ void run_forward(ssd_session* s, int K, int lm_mode) {
   base.xn = s->xn;
   base.ssq_out = s->ssq;
   base.ssq_out_ld = s->ssq_rows_ld;
+  base.q_plane = s->q_plane;
+  base.xn_plane = s->xn_plane;
+  base.h_plane = s->h_plane;
 
   if (dm.bf16) {
+    // algorithmic bytes: bf16 weights and KV, 4-byte activations (two bf16 planes), fp32 residual
+    const double A = 4.0;
     GemmPlan pq = gemm_plan_bf16(M, Nqkv, d);
     GemmPlan po = gemm_plan_bf16(M, d, dm.Hq * D);
     GemmPlan p13 = gemm_plan_bf16(M, 2 * dm.dff, d);
     GemmPlan p2 = gemm_plan_bf16(M, d, dm.dff);
     AttnPlan pa = attn_plan(dm, B, K, max_ctx_now);
-    double attn_bytes = 2.0 * M * dm.Hq * D * es;  // q read + o written
+    double attn_bytes = 2.0 * M * dm.Hq * D * A;  // q read + o written
     for (int b = 0; b < B; ++b) attn_bytes += 2.0 * (s->f[b] + K) * dm.Hkv * D * es;
+    const double qkv_bytes = (double)Nqkv * d * es + (double)M * d * A + (double)M * dm.Hq * D * A +
+                             2.0 * M * dm.Hkv * D * es;
+    const double o_bytes = (double)d * dm.Hq * D * es + (double)M * dm.Hq * D * A + (double)M * d * (8 + A);
+    const double gu_bytes = 2.0 * dm.dff * d * es + (double)M * d * A + (double)M * dm.dff * A;
+    const double dn_bytes = (double)d * dm.dff * es + (double)M * dm.dff * A + (double)M * d * (8 + A);
     for (int l = 0; l < dm.L; ++l) {
       const LayerW& W = m->layers[l];
       char* kc = (char*)s->kc + (size_t)l * s->kv_layer_elems * es;
@@ -271,18 +282,21 @@ void run_forward(ssd_session* s, int K, int lm_mode) {
       e.q = s->q;
       e.kc = kc;
       e.vc = vc;
-      m->prof.run(0, ((double)Nqkv * d + (double)M * d + (double)M * Nqkv) * es, st,
-                  [&] { gemm_bf16(pq, W.wqkv, Nqkv, d, s->xn, d, M, e, s->gpart, nullptr, s->gcnt, st); });
+      m->prof.run(0, qkv_bytes, st, [&] {
+        gemm_bf16(pq, W.wqkv, Nqkv, d, s->xn, s->xn_plane, d, M, e, s->gpart, s->gcnt, st);
+      });
       m->prof.run(5, attn_bytes, st, [&] {
-        attention_bf16(dm, pa, B, K, s->d_f, s->q, kc, vc, s->Lmax, s->o, s->apart, s->acnt, st);
+        attention_bf16(dm, pa, B, K, s->d_f, s->q, s->q_plane, kc, vc, s->Lmax, s->o, s->o_plane, s->apart, s->acnt,
+                       st);
       });
       e = base;
       e.kind = EPI_RESID;
       e.ssq = nullptr;
       e.gnext = W.g2;
       e.ld = d;
-      m->prof.run(1, ((double)d * dm.Hq * D + (double)M * dm.Hq * D) * es + (double)M * d * (8 + es), st,
-                  [&] { gemm_bf16(po, W.wo, d, dm.Hq * D, s->o, dm.Hq * D, M, e, s->gpart, nullptr, s->gcnt, st); });
+      m->prof.run(1, o_bytes, st, [&] {
+        gemm_bf16(po, W.wo, d, dm.Hq * D, s->o, s->o_plane, dm.Hq * D, M, e, s->gpart, s->gcnt, st);
+      });
       ssq_parts = po.n_fb;
       e = base;
       e.kind = EPI_SWIGLU;
@@ -290,15 +304,17 @@ void run_forward(ssd_session* s, int K, int lm_mode) {
       e.ssq_parts = ssq_parts;
       e.h = s->h;
       e.ld = dm.dff;
-      m->prof.run(2, (2.0 * dm.dff * d + (double)M * d + (double)M * dm.dff) * es, st,
-                  [&] { gemm_bf16(p13, W.w13, 2 * dm.dff, d, s->xn, d, M, e, s->gpart, nullptr, s->gcnt, st); });
+      m->prof.run(2, gu_bytes, st, [&] {
+        gemm_bf16(p13, W.w13, 2 * dm.dff, d, s->xn, s->xn_plane, d, M, e, s->gpart, s->gcnt, st);
+      });
       e = base;
       e.kind = EPI_RESID;
       e.ssq = nullptr;
       e.gnext = (l + 1 < dm.L) ? m->layers[l + 1].g1 : m->gf;
       e.ld = d;
-      m->prof.run(3, ((double)d * dm.dff + (double)M * dm.dff) * es + (double)M * d * (8 + es), st,
-                  [&] { gemm_bf16(p2, W.w2, d, dm.dff, s->h, dm.dff, M, e, s->gpart, nullptr, s->gcnt, st); });
+      m->prof.run(3, dn_bytes, st, [&] {
+        gemm_bf16(p2, W.w2, d, dm.dff, s->h, s->h_plane, dm.dff, M, e, s->gpart, s->gcnt, st);
+      });
       ssq_parts = p2.n_fb;
     }
     EpiArgs e = base;
@@ -309,15 +325,16 @@ void run_forward(ssd_session* s, int K, int lm_mode) {
     e.ld = dm.Vimg;
     if (lm_mode == 0) {
       GemmPlan pl = gemm_plan_bf16(M, dm.Vimg, d);
-      m->prof.run(4, ((double)dm.Vimg * d + (double)M * d) * es + (double)M * dm.Vimg * 4, st,
-                  [&] { gemm_bf16(pl, m->wlm, dm.Vimg, d, s->xn, d, M, e, s->gpart, nullptr, s->gcnt, st); });
+      m->prof.run(4, (double)dm.Vimg * d * es + (double)M * d * A + (double)M * dm.Vimg * 4, st, [&] {
+        gemm_bf16(pl, m->wlm, dm.Vimg, d, s->xn, s->xn_plane, d, M, e, s->gpart, s->gcnt, st);
+      });
     } else {
       e.ssq_off = K - 1;
       e.ssq_step = K;
       GemmPlan pl = gemm_plan_bf16(B, dm.Vimg, d);
-      m->prof.run(4, ((double)dm.Vimg * d + (double)B * d) * es + (double)B * dm.Vimg * 4, st, [&] {
-        gemm_bf16(pl, m->wlm, dm.Vimg, d, (const char*)s->xn + (size_t)(K - 1) * d * es, K * d, B, e, s->gpart,
-                  nullptr, s->gcnt, st);
+      m->prof.run(4, (double)dm.Vimg * d * es + (double)B * d * A + (double)B * dm.Vimg * 4, st, [&] {
+        gemm_bf16(pl, m->wlm, dm.Vimg, d, (const uint16_t*)s->xn + (size_t)(K - 1) * d, s->xn_plane, K * d, B, e,
+                  s->gpart, s->gcnt, st);
       });
     }
   } else {
@@ -434,12 +451,17 @@ ssd_status create_session(ssd_model* m, int B, int P, int Lmax_req, int Kmax, ss
     s->cnt = s->mem.get<int>(B);
     s->amax = s->mem.get<int>(M);
     s->x = s->mem.get<float>(M * dm.d);
-    s->xn = s->mem.get<char>(M * dm.d * es);
+    // activations: 4 bytes per element (fp32, or hi + lo bf16 planes)
+    s->xn_plane = M * dm.d;
+    s->q_plane = M * dm.Hq * dm.D;
+    s->o_plane = M * dm.Hq * dm.D;
+    s->h_plane = M * dm.dff;
+    s->xn = s->mem.get<char>(M * dm.d * 4);
     s->ssq_rows_ld = (int)M;
     s->ssq = s->mem.get<float>((size_t)ssq_parts * M);
-    s->q = s->mem.get<char>(M * dm.Hq * dm.D * es);
-    s->o = s->mem.get<char>(M * dm.Hq * dm.D * es);
-    s->h = s->mem.get<char>(M * dm.dff * es);
+    s->q = s->mem.get<char>(M * dm.Hq * dm.D * 4);
+    s->o = s->mem.get<char>(M * dm.Hq * dm.D * 4);
+    s->h = s->mem.get<char>(M * dm.dff * 4);
     s->logits = s->mem.get<float>(M * dm.Vimg);
     s->carry = s->mem.get<float>((size_t)B * dm.Vimg);
     s->ref = s->mem.get<float>((size_t)B * s->ring * dm.Vimg);

@@ -2,14 +2,18 @@
 //
 // Data layout in HBM (all row-major unless stated):
 //   residual x        fp32 [M][d]
-//   xn                model dtype [M][d]      bf16(g * x): the GEMM input after an RMSNorm
+//   xn                act [M][d]              g * x: the GEMM input after an RMSNorm
 //   ssq               fp32 [parts][Mmax]      partial sums of x^2 per token (producer feature blocks)
-//   q                 model dtype [B][Hq][K][D]   (query row r = head_in_group * K + k)
+//   q                 act [B][Hq][K][D]       (query row r = head_in_group * K + k)
 //   K cache           model dtype [L][B][Hkv][Lmax][D]
 //   V cache (transp.) model dtype [L][B][Hkv][D][Lmax]
-//   o                 model dtype [M][Hq*D]   attention output
-//   h                 model dtype [M][d_ff]   SwiGLU product
+//   o                 act [M][Hq*D]           attention output
+//   h                 act [M][d_ff]           SwiGLU product
 //   logits            fp32 [M][V_img]
+// "act" buffers of bf16 models are two bf16 planes, hi = bf16(v) and
+// lo = bf16(v - hi), `plane` elements apart: an fp32 activation as a pair of
+// MFMA operands (hi + lo carries v to 2^-17 relative).  fp32 models store
+// fp32 in the first plane only.
 // bf16 weight matrices W[N][K] are prepacked into 16x32 MFMA A-operand tiles:
 //   tile (nb, kb) = 64 lanes x 8 bf16, lane l holds W[nb*16 + l%16][kb*32 + 8*(l/16) + e]
 //   tiles ordered nb-major, so one wave reads 1 KiB contiguous per tile.
@@ -63,6 +67,8 @@ struct EpiArgs {
   float* logits;
   // common leading dimensions (elements)
   int ld;                // x / xn / h / logits row length
+  // plane strides (elements) of the split activation buffers
+  size_t q_plane, xn_plane, h_plane;
 };
 
 // Device model (owned by ssd_model)
@@ -87,17 +93,17 @@ struct GemmPlan {
 // ---- launchers (kernels_*.hip) ----
 GemmPlan gemm_plan_bf16(int M, int N, int K);
 size_t gemm_partials_floats(const GemmPlan& p, int M);
-// y = W x for bf16 inputs in[M][K] (row stride ld_in); epilogue per `epi`.
-void gemm_bf16(const GemmPlan& p, const void* Wpacked, int N, int K, const void* in, int ld_in, int M,
-               const EpiArgs& epi, float* partials, float* ssq_part, unsigned* counters, hipStream_t st);
+// y = W x for split inputs in[M][K] (row stride ld_in, lo plane in_plane elements after hi); epilogue per `epi`.
+void gemm_bf16(const GemmPlan& p, const void* Wpacked, int N, int K, const void* in, size_t in_plane, int ld_in,
+               int M, const EpiArgs& epi, float* partials, unsigned* counters, hipStream_t st);
 void gemm_f32(const float* W, int N, int K, const float* in, int ld_in, int M, const EpiArgs& epi, hipStream_t st);
 
 void pack_bf16_tiles(const uint16_t* src, const int* rowmap, int N, int K, void* dst, hipStream_t st);
 void gather_rows_f32(const float* src, const int* rowmap, int N, int K, float* dst, hipStream_t st);
 
-// x[t] = E[tok[t]]; xn = g * x (rounded to the model dtype); ssq[t] = sum x^2 (one part)
-void embed(const Dims& dm, const void* emb, const int* tok, int M, const float* g, float* x, void* xn, float* ssq,
-           hipStream_t st);
+// x[t] = E[tok[t]]; xn = g * x (split planes for bf16 models); ssq[t] = sum x^2 (one part)
+void embed(const Dims& dm, const void* emb, const int* tok, int M, const float* g, float* x, void* xn,
+           size_t xn_plane, float* ssq, hipStream_t st);
 // fp32 path: xn = g * x, ssq[t] = sum x^2 (one part)
 void norm_rows_f32(const float* x, int M, int d, const float* g, float* xn, float* ssq, hipStream_t st);
 
@@ -110,8 +116,9 @@ struct AttnPlan {
 };
 AttnPlan attn_plan(const Dims& dm, int B, int K, int max_ctx_now);
 size_t attn_partials_floats(const Dims& dm, const AttnPlan& p, int B);
-void attention_bf16(const Dims& dm, const AttnPlan& p, int B, int K, const int* f, const void* q, const void* kc,
-                    const void* vc, int Lmax, void* o, float* partials, unsigned* counters, hipStream_t st);
+void attention_bf16(const Dims& dm, const AttnPlan& p, int B, int K, const int* f, const void* q, size_t q_plane,
+                    const void* kc, const void* vc, int Lmax, void* o, size_t o_plane, float* partials,
+                    unsigned* counters, hipStream_t st);
 void attention_f32(const Dims& dm, int B, int K, const int* f, const float* q, const float* kc, const float* vc,
                    int Lmax, float* o, hipStream_t st);
 

@@ -100,3 +100,34 @@ def oracle_rule_on(logits_gpu, carry_gpu, block_codes, n_fixed, rule, rnd, seed,
 def greedy_gap(L):
     s = np.sort(np.asarray(L, np.float64))
     return s[-1] - s[-2]
+
+
+def flip_within_tolerance(rule, L_oracle, ref_oracle, t, u0, u1, new_gpu, acc_gpu, delta, T=1.0, top_k=0):
+    """Whether a GPU decision that differs from the oracle's is one the logit
+    error `delta` (max |GPU - oracle| on the rows involved) can cause.
+
+    A logit error of at most delta changes every warped probability by a
+    factor within exp(+-2 delta), so: alpha by a factor within exp(+-4 delta);
+    the cumulative residual (or p) mass at any code by at most
+    2 (exp(2 delta) - 1) per distribution involved.  The GPU's outcome is
+    accepted when the oracle's own numbers put the uniform inside that band.
+    """
+    if rule == R.RULE_GREEDY:
+        return greedy_gap(L_oracle) < 2 * delta
+    p = R.warp(L_oracle, T, top_k)
+    if rule == R.RULE_SAMPLE:
+        w, eps_a, accept_ok = p, 2 * (np.exp(2 * delta) - 1), None
+    else:
+        q = R.point_mass(p.shape[0], t) if ref_oracle is None else R.warp(ref_oracle, T, top_k)
+        alpha = R.accept_prob(p, q, t)
+        band = alpha * (np.exp(4 * delta) - 1) + 1e-12
+        if acc_gpu:
+            return new_gpu == t and u0 < alpha + band
+        if u0 < alpha - band:
+            return False
+        w, eps_a = R.residual(p, q), 4 * (np.exp(2 * delta) - 1)
+    c = np.cumsum(w)
+    target = u1 * c[-1]
+    lo = c[new_gpu - 1] if new_gpu > 0 else 0.0
+    hi = c[new_gpu]
+    return lo - eps_a <= target <= hi + eps_a
