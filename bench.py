@@ -98,6 +98,7 @@ def main():
     ap.add_argument("--accept-p", type=float, default=None)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-ar", action="store_true")
+    ap.add_argument("--no-events", action="store_true", help="time without the per-launch event hook")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this build runs on exactly one GPU (asked for {args.gpus}); the verify path "
@@ -141,7 +142,7 @@ def main():
         ssd.ssd_decode_image(model, sc, B, P, d_prefix, d_drafts, d_out)
         log(f"[bench] warmup {i + 1}/{args.warmup} done")
     torch.cuda.synchronize()
-    ssd.ssd_profile(model, 1)
+    ssd.ssd_profile(model, 0 if args.no_events else 1)
     ssd.ssd_profile_read(model, reset=True)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -160,7 +161,7 @@ def main():
     g_ms = sum(x[0] for x in gemm)
     g_n = sum(x[1] for x in gemm)
     g_bytes = sum(x[2] for x in gemm)
-    g_gbs = g_bytes / (g_ms / 1000.0) / 1e9
+    g_gbs = g_bytes / (g_ms / 1000.0) / 1e9 if g_ms > 0 else 0.0
     a_ms, a_n, a_bytes = prof["attention"]
     a_gbs = a_bytes / (a_ms / 1000.0) / 1e9 if a_ms > 0 else 0.0
     per_class = {c: {"ms_per_launch": prof[c][0] / max(prof[c][1], 1), "launches": prof[c][1],

@@ -38,7 +38,7 @@ struct AttnKArgs {
   float* part;         // [B*Hkv][nqg][nchunk][QPW*16][D+2]
   unsigned* counters;  // [B*Hkv][nqg]
   const int* f;
-  int K, Hq, Hkv, g, Lmax, rows, chunk, nchunk, nqg;
+  int K, Hq, Hkv, g, Lmax, rows, chunk, nchunk, nqg, groups, xcd;
   float scale_log2;
 };
 
@@ -47,7 +47,11 @@ __global__ __launch_bounds__(64) void attn_bf16_kernel(AttnKArgs a) {
   constexpr int KD = D / 32;   // 32-wide k steps over the head dimension
   constexpr int DT = D / 16;   // 16-row d tiles of O^T
   __shared__ int is_last;
-  const int c = blockIdx.x, qg = blockIdx.y, z = blockIdx.z;
+  // reduction group = (sequence x KV head, query group); members = key chunks, all on one XCD
+  int grp_id, c;
+  xcd_unmap(blockIdx.x, a.nchunk, a.xcd, grp_id, c);
+  if (grp_id >= a.groups) return;
+  const int qg = grp_id % a.nqg, z = grp_id / a.nqg;
   const int b = z / a.Hkv, hkv = z - b * a.Hkv;
   const int lane = threadIdx.x;
   const int col = lane & 15, grp = lane >> 4;
@@ -217,7 +221,7 @@ __global__ __launch_bounds__(64) void attn_bf16_kernel(AttnKArgs a) {
 
   // publish the partial (O unnormalised, m, l) of this chunk
   constexpr int RS = D + 2;
-  const size_t grp_base = ((size_t)z * a.nqg + qg) * a.nchunk;
+  const size_t grp_base = (size_t)grp_id * a.nchunk;
   float* P = a.part + (grp_base + c) * (QPW * 16) * RS;
 #pragma unroll
   for (int qt = 0; qt < QPW; ++qt) {
@@ -235,34 +239,43 @@ __global__ __launch_bounds__(64) void attn_bf16_kernel(AttnKArgs a) {
       pr[D + 1] = l[qt];
     }
   }
-  __threadfence();
+  // partial stores acknowledged by this XCD's L2, then count the arrival
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
   if (lane == 0) {
-    unsigned prev = atomicAdd(&a.counters[(size_t)z * a.nqg + qg], 1u);
+    if (!a.xcd) __threadfence();  // chunks on different XCDs: write back through L2
+    unsigned prev = atomicAdd(&a.counters[grp_id], 1u);
     is_last = (prev == (unsigned)(nch - 1));
+    if (is_last && !a.xcd) __threadfence();
   }
   __syncthreads();
   if (!is_last) return;
-  __threadfence();
-  // merge chunks in order; lanes run over the head dimension
+  // merge the chunks: per query row, lane c holds chunk c's statistics; the
+  // O rows are summed in chunk order with lanes over the head dimension
   const float* G = a.part + grp_base * (QPW * 16) * RS;
   for (int rr = 0; rr < QPW * 16; ++rr) {
     const int r = rbase + rr;
     if (r >= a.rows) break;
-    float M = -INFINITY;
-    for (int cc = 0; cc < nch; ++cc) M = fmaxf(M, __builtin_nontemporal_load(G + ((size_t)cc * QPW * 16 + rr) * RS + D));
-    float L = 0.f;
+    float mc = -INFINITY, lc = 0.f;
+    if (lane < nch) {
+      const float* pr = G + ((size_t)lane * QPW * 16 + rr) * RS;
+      mc = pr[D];
+      lc = pr[D + 1];
+    }
+    float M = mc;
+    for (int o = 32; o > 0; o >>= 1) M = fmaxf(M, __shfl_xor(M, o));
+    const float wv = (lc > 0.f) ? exp2f(mc - M) : 0.f;
+    float L = lc * wv;
+    for (int o = 32; o > 0; o >>= 1) L += __shfl_xor(L, o);
     float acc[D / 64];
 #pragma unroll
     for (int i = 0; i < D / 64; ++i) acc[i] = 0.f;
     for (int cc = 0; cc < nch; ++cc) {
+      const float wgt = __shfl(wv, cc);
+      if (wgt == 0.f) continue;
       const float* pr = G + ((size_t)cc * QPW * 16 + rr) * RS;
-      const float mc = __builtin_nontemporal_load(pr + D);
-      const float lc = __builtin_nontemporal_load(pr + D + 1);
-      if (lc == 0.f) continue;
-      const float wgt = exp2f(mc - M);
-      L += lc * wgt;
 #pragma unroll
-      for (int i = 0; i < D / 64; ++i) acc[i] += __builtin_nontemporal_load(pr + lane + 64 * i) * wgt;
+      for (int i = 0; i < D / 64; ++i) acc[i] += pr[lane + 64 * i] * wgt;
     }
     const int j = r / a.K, k = r - j * a.K;
     uint16_t* op = a.o + ((size_t)b * a.K + k) * (a.Hq * D) + (hkv * a.g + j) * D;
@@ -275,11 +288,12 @@ __global__ __launch_bounds__(64) void attn_bf16_kernel(AttnKArgs a) {
       op[a.o_plane + lane + 64 * i] = f2bf_a(v - __uint_as_float((uint32_t)hi << 16));
     }
   }
-  if (lane == 0) a.counters[(size_t)z * a.nqg + qg] = 0u;
+  if (lane == 0) a.counters[grp_id] = 0u;
 }
 
-AttnPlan attn_plan(const Dims& dm, int B, int K, int max_ctx_now) {
+AttnPlan attn_plan(const Dims& dm, int B, int K, int max_ctx_now, int xcd) {
   AttnPlan p;
+  p.xcd = xcd;
   const int g = dm.Hq / dm.Hkv;
   p.rows = K * g;
   const int qt = (p.rows + 15) / 16;
@@ -288,7 +302,10 @@ AttnPlan attn_plan(const Dims& dm, int B, int K, int max_ctx_now) {
   // chunk: enough workgroups to cover the chip, at least 64 keys
   const int units = B * dm.Hkv * p.nqg;
   int chunk = 64;
-  while (chunk < 2048 && (long)units * ((max_ctx_now + chunk - 1) / chunk) > 1024) chunk *= 2;
+  // at most 64 chunks (the merge holds one chunk per lane)
+  while ((chunk < 2048 && (long)units * ((max_ctx_now + chunk - 1) / chunk) > 1024) ||
+         (max_ctx_now + chunk - 1) / chunk > 64)
+    chunk *= 2;
   p.chunk = chunk;
   p.nchunk = (max_ctx_now + chunk - 1) / chunk;
   return p;
@@ -299,8 +316,8 @@ size_t attn_partials_floats(const Dims& dm, const AttnPlan& p, int B) {
 }
 
 template <int D, int QPW>
-static void launch_attn(const AttnKArgs& a, int nchunk, int nqg, int z, hipStream_t st) {
-  hipLaunchKernelGGL((attn_bf16_kernel<D, QPW>), dim3(nchunk, nqg, z), dim3(64), 0, st, a);
+static void launch_attn(const AttnKArgs& a, hipStream_t st) {
+  hipLaunchKernelGGL((attn_bf16_kernel<D, QPW>), dim3(xcd_grid(a.groups, a.nchunk, a.xcd)), dim3(64), 0, st, a);
 }
 
 void attention_bf16(const Dims& dm, const AttnPlan& p, int B, int K, const int* f, const void* q, size_t q_plane,
@@ -325,14 +342,15 @@ void attention_bf16(const Dims& dm, const AttnPlan& p, int B, int K, const int* 
   a.chunk = p.chunk;
   a.nchunk = p.nchunk;
   a.nqg = p.nqg;
+  a.groups = B * dm.Hkv * p.nqg;
+  a.xcd = p.nchunk > 1 ? p.xcd : 0;
   a.scale_log2 = 1.4426950408889634f / sqrtf((float)dm.D);
-  const int z = B * dm.Hkv;
   if (dm.D == 128) {
-    if (p.qpw == 2) launch_attn<128, 2>(a, p.nchunk, p.nqg, z, st);
-    else launch_attn<128, 1>(a, p.nchunk, p.nqg, z, st);
+    if (p.qpw == 2) launch_attn<128, 2>(a, st);
+    else launch_attn<128, 1>(a, st);
   } else {
-    if (p.qpw == 2) launch_attn<64, 2>(a, p.nchunk, p.nqg, z, st);
-    else launch_attn<64, 1>(a, p.nchunk, p.nqg, z, st);
+    if (p.qpw == 2) launch_attn<64, 2>(a, st);
+    else launch_attn<64, 1>(a, st);
   }
 }
 

@@ -129,6 +129,7 @@ struct GemmKArgs {
   size_t in_plane;
   int ld_in;
   int M, t0;
+  int xcd;
   float* part;
   unsigned* counters;
   EpiArgs epi;
@@ -221,20 +222,46 @@ __device__ __forceinline__ void compute_chunk(floatx4 (&acc)[NT][MT], const u32x
   }
 }
 
-template <int MT, int NT, int KCB>
+// per-token 1/rms(x) from the producer's partial sums, loaded in parallel
+// (parts in blocks of 16 through LDS, summed in part order)
+template <int MP>
+__device__ __forceinline__ void rms_prologue(const EpiArgs& e, int M, int t0, float (*red)[MP], float* rscale) {
+  float s = 0.f;
+  for (int p0 = 0; p0 < e.ssq_parts; p0 += 16) {
+    for (int i = threadIdx.x; i < 16 * MP; i += 256) {
+      const int p = p0 + i / MP, t = i % MP;
+      red[i / MP][t] = (p < e.ssq_parts && t < M)
+                           ? e.ssq[(size_t)p * e.ssq_ld + (size_t)e.ssq_off + (size_t)(t0 + t) * e.ssq_step]
+                           : 0.f;
+    }
+    __syncthreads();
+    if (threadIdx.x < MP)
+      for (int p = 0; p < 16; ++p) s += red[p][threadIdx.x];
+    __syncthreads();
+  }
+  if (threadIdx.x < MP) rscale[threadIdx.x] = 1.0f / sqrtf(s * e.inv_d + e.eps);
+}
+
+// NBUF = 1: the workgroup's whole K-slice is one chunk, loaded in one burst
+// (weights to registers, tokens to LDS); NBUF = 2: chunks double-buffered.
+template <int MT, int NT, int KCB, int NBUF>
 __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmKArgs a) {
   using X = XStage<MT, KCB>;
-  __shared__ __attribute__((aligned(16))) uint16_t xs[2][2 * X::PL];
+  __shared__ __attribute__((aligned(16))) uint16_t xs[NBUF][2 * X::PL];
   __shared__ float sq_red[4][X::MP];
   __shared__ float rscale[X::MP];
+  __shared__ float rms_red[16][X::MP];
   __shared__ int is_last;
 
-  const int fb = blockIdx.x, s = blockIdx.y;
+  int fb, s;
+  xcd_unmap(blockIdx.x, a.S, a.xcd, fb, s);
+  if (fb >= a.n_fb) return;
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int nb0 = (fb * 4 + w) * NT;
   const int kb_split = s * a.kchunks * KCB;
   const uint16_t* in = a.in;
   const int nc = a.kchunks;
+  const EpiArgs& e = a.epi;
 
   floatx4 acc[NT][MT];
 #pragma unroll
@@ -242,13 +269,21 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmKArgs a) {
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) acc[nt][mt] = floatx4{0.f, 0.f, 0.f, 0.f};
 
-  u32x4 ra[2][NT][KCB];
+  u32x4 ra[NBUF][NT][KCB];
   u32x4 rx[2][X::PASSES];
 
-  load_x<MT, KCB>(rx, in, a.in_plane, a.ld_in, a.M, kb_split * 32);
   load_a<NT, KCB>(ra[0], a.W, a.KB, nb0, a.N, kb_split, lane);
+  load_x<MT, KCB>(rx, in, a.in_plane, a.ld_in, a.M, kb_split * 32);
+  // the per-token rms scale is fetched while the weights are in flight
+  if (e.ssq)
+    rms_prologue<X::MP>(e, a.M, a.t0, rms_red, rscale);
+  else if (threadIdx.x < X::MP)
+    rscale[threadIdx.x] = 1.f;
   store_x<MT, KCB>(rx, xs[0]);
   __syncthreads();
+  if constexpr (NBUF == 1) {
+    compute_chunk<MT, NT, KCB>(acc, ra[0], xs[0], lane);
+  } else {
   for (int c = 0; c < nc; c += 2) {
     if (c + 1 < nc) {
       load_x<MT, KCB>(rx, in, a.in_plane, a.ld_in, a.M, (kb_split + (c + 1) * KCB) * 32);
@@ -266,6 +301,7 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmKArgs a) {
     if (c + 2 < nc) store_x<MT, KCB>(rx, xs[0]);
     __syncthreads();
   }
+  }
 
   if (a.S > 1) {
     // split-K: publish partial fragments, the last workgroup of this feature block reduces
@@ -277,23 +313,24 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmKArgs a) {
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt)
         *(floatx4*)(P + (size_t)s * split_stride + ((nt * MT + mt) * 64 + lane) * 4) = acc[nt][mt];
-    __threadfence();
+    // every wave's partial stores acknowledged (they sit in this XCD's L2)
+    __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
     if (threadIdx.x == 0) {
+      if (!a.xcd) __threadfence();  // splits on different XCDs: write back through L2
       unsigned prev = atomicAdd(&a.counters[fb], 1u);
       is_last = (prev == (unsigned)(a.S - 1));
+      if (is_last && !a.xcd) __threadfence();
     }
     __syncthreads();
     if (!is_last) return;
-    __threadfence();
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt)
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt) {
         floatx4 v = floatx4{0.f, 0.f, 0.f, 0.f};
         for (int s2 = 0; s2 < a.S; ++s2) {
-          floatx4 pv = __builtin_nontemporal_load(
-              (const floatx4*)(P + (size_t)s2 * split_stride + ((nt * MT + mt) * 64 + lane) * 4));
+          floatx4 pv = *(const floatx4*)(P + (size_t)s2 * split_stride + ((nt * MT + mt) * 64 + lane) * 4);
           v += pv;
         }
         acc[nt][mt] = v;
@@ -301,13 +338,7 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmKArgs a) {
     if (threadIdx.x == 0) a.counters[fb] = 0u;
   }
 
-  // epilogue
-  const EpiArgs& e = a.epi;
-  if (threadIdx.x < X::MP) {
-    int t = threadIdx.x;
-    rscale[t] = (t < a.M) ? rms_scale(e, a.t0 + t) : 1.f;
-  }
-  __syncthreads();
+  // epilogue (rscale was filled before the first barrier)
   float sq[MT];
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt) sq[mt] = 0.f;
@@ -343,14 +374,37 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmKArgs a) {
   }
 }
 
-GemmPlan gemm_plan_bf16(int M, int N, int K) {
+GemmPlan gemm_plan_bf16(int M, int N, int K, int xcd) {
   GemmPlan p;
+  p.xcd = xcd;
   int Mc = M < 128 ? M : 128;
   p.MT = Mc <= 16 ? 1 : Mc <= 32 ? 2 : Mc <= 64 ? 4 : 8;
-  p.KCB = p.MT == 1 ? 8 : p.MT == 2 ? 4 : p.MT == 4 ? 2 : 1;
   p.NT = p.MT >= 4 ? 2 : 1;
   p.bn = 4 * p.NT * 16;
   p.n_fb = (N + p.bn - 1) / p.bn;
+  const int kb = K / 32;
+  if (p.MT <= 2) {
+    // one burst per workgroup: the smallest split count whose K-slice (8 or 16
+    // k-blocks) fits registers and LDS, preferring >= 256 workgroups
+    p.S = 0;
+    for (int s = 1; s <= kb; ++s) {
+      if (kb % s) continue;
+      const int kcb = kb / s;
+      if (kcb != 16 && kcb != 8) continue;
+      if (p.S == 0) p.S = s;
+      if (p.n_fb * s >= 256) {
+        p.S = s;
+        break;
+      }
+    }
+    if (p.S) {
+      p.KCB = kb / p.S;
+      p.kchunks = 1;
+      return p;
+    }
+  }
+  // double-buffered chunks
+  p.KCB = p.MT == 1 ? 8 : p.MT == 2 ? 4 : p.MT == 4 ? 2 : 1;
   int kch = K / (p.KCB * 32);
   p.S = 1;
   if (p.n_fb < 480) {
@@ -372,9 +426,9 @@ size_t gemm_partials_floats(const GemmPlan& p, int M) {
   return (size_t)p.S * p.n_fb * 4 * p.NT * p.MT * 64 * 4;
 }
 
-template <int MT, int NT, int KCB>
+template <int MT, int NT, int KCB, int NBUF>
 static void launch_gemm(const GemmKArgs& a, int n_fb, int S, hipStream_t st) {
-  hipLaunchKernelGGL((gemm_bf16_kernel<MT, NT, KCB>), dim3(n_fb, S), dim3(256), 0, st, a);
+  hipLaunchKernelGGL((gemm_bf16_kernel<MT, NT, KCB, NBUF>), dim3(xcd_grid(n_fb, S, a.xcd)), dim3(256), 0, st, a);
 }
 
 void gemm_bf16(const GemmPlan& p, const void* Wpacked, int N, int K, const void* in, size_t in_plane, int ld_in,
@@ -394,14 +448,23 @@ void gemm_bf16(const GemmPlan& p, const void* Wpacked, int N, int K, const void*
     a.ld_in = ld_in;
     a.M = (M - t0) < MP ? (M - t0) : MP;
     a.t0 = t0;
+    a.xcd = p.S > 1 ? p.xcd : 0;
     a.part = partials;
     a.counters = counters;
     a.epi = epi;
     switch (p.MT) {
-      case 1: launch_gemm<1, 1, 8>(a, p.n_fb, p.S, st); break;
-      case 2: launch_gemm<2, 1, 4>(a, p.n_fb, p.S, st); break;
-      case 4: launch_gemm<4, 2, 2>(a, p.n_fb, p.S, st); break;
-      default: launch_gemm<8, 2, 1>(a, p.n_fb, p.S, st); break;
+      case 1:
+        if (p.kchunks == 1 && p.KCB == 16) launch_gemm<1, 1, 16, 1>(a, p.n_fb, p.S, st);
+        else if (p.kchunks == 1 && p.KCB == 8) launch_gemm<1, 1, 8, 1>(a, p.n_fb, p.S, st);
+        else launch_gemm<1, 1, 8, 2>(a, p.n_fb, p.S, st);
+        break;
+      case 2:
+        if (p.kchunks == 1 && p.KCB == 16) launch_gemm<2, 1, 16, 1>(a, p.n_fb, p.S, st);
+        else if (p.kchunks == 1 && p.KCB == 8) launch_gemm<2, 1, 8, 1>(a, p.n_fb, p.S, st);
+        else launch_gemm<2, 1, 4, 2>(a, p.n_fb, p.S, st);
+        break;
+      case 4: launch_gemm<4, 2, 2, 2>(a, p.n_fb, p.S, st); break;
+      default: launch_gemm<8, 2, 1, 2>(a, p.n_fb, p.S, st); break;
     }
   }
 }

@@ -534,6 +534,17 @@ void commit_update(int B, int K, int Vimg, const float* logits, float* carry, in
   hipLaunchKernelGGL(commit_kernel, dim3(B), dim3(256), 0, st, Vimg, logits, rps, last, carry, f, inc, ref_flag, ring);
 }
 
+// Which XCD (accelerator complex die) each workgroup runs on: the XCC_ID
+// hardware register (bits [3:0]).  Used once at start-up to verify the
+// round-robin workgroup-to-XCD dispatch the split-K reductions rely on.
+__global__ void xcc_probe_kernel(int* out) {
+  if (threadIdx.x == 0) out[blockIdx.x] = (int)(__builtin_amdgcn_s_getreg(20 | (0 << 6) | ((4 - 1) << 11)) & 0xF);
+}
+
+void xcc_probe(int* out, int n_wg, hipStream_t st) {
+  hipLaunchKernelGGL(xcc_probe_kernel, dim3(n_wg), dim3(64), 0, st, out);
+}
+
 __global__ void fill_u32_kernel(unsigned* p, size_t n, unsigned v) {
   size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i < n) p[i] = v;

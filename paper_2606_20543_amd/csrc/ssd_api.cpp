@@ -5,6 +5,7 @@
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
+#include <cstdlib>
 #include <cstring>
 #include <string>
 #include <vector>
@@ -168,6 +169,7 @@ struct ssd_model {
   bool poisoned = false;
   ssd_session* dec = nullptr;  // cached decode workspace
   int dec_B = 0, dec_P = 0, dec_L = 0, dec_K = 0;
+  int xcd = 0;  // XCD count when workgroups are dispatched round-robin over XCDs (see xcd_grid), else 0
   Prof prof;
 };
 
@@ -259,11 +261,12 @@ void run_forward(ssd_session* s, int K, int lm_mode) {
   if (dm.bf16) {
     // algorithmic bytes: bf16 weights and KV, 4-byte activations (two bf16 planes), fp32 residual
     const double A = 4.0;
-    GemmPlan pq = gemm_plan_bf16(M, Nqkv, d);
-    GemmPlan po = gemm_plan_bf16(M, d, dm.Hq * D);
-    GemmPlan p13 = gemm_plan_bf16(M, 2 * dm.dff, d);
-    GemmPlan p2 = gemm_plan_bf16(M, d, dm.dff);
-    AttnPlan pa = attn_plan(dm, B, K, max_ctx_now);
+    const int X = m->xcd;
+    GemmPlan pq = gemm_plan_bf16(M, Nqkv, d, X);
+    GemmPlan po = gemm_plan_bf16(M, d, dm.Hq * D, X);
+    GemmPlan p13 = gemm_plan_bf16(M, 2 * dm.dff, d, X);
+    GemmPlan p2 = gemm_plan_bf16(M, d, dm.dff, X);
+    AttnPlan pa = attn_plan(dm, B, K, max_ctx_now, X);
     double attn_bytes = 2.0 * M * dm.Hq * D * A;  // q read + o written
     for (int b = 0; b < B; ++b) attn_bytes += 2.0 * (s->f[b] + K) * dm.Hkv * D * es;
     const double qkv_bytes = (double)Nqkv * d * es + (double)M * d * A + (double)M * dm.Hq * D * A +
@@ -324,14 +327,14 @@ void run_forward(ssd_session* s, int K, int lm_mode) {
     e.logits = s->logits;
     e.ld = dm.Vimg;
     if (lm_mode == 0) {
-      GemmPlan pl = gemm_plan_bf16(M, dm.Vimg, d);
+      GemmPlan pl = gemm_plan_bf16(M, dm.Vimg, d, X);
       m->prof.run(4, (double)dm.Vimg * d * es + (double)M * d * A + (double)M * dm.Vimg * 4, st, [&] {
         gemm_bf16(pl, m->wlm, dm.Vimg, d, s->xn, s->xn_plane, d, M, e, s->gpart, s->gcnt, st);
       });
     } else {
       e.ssq_off = K - 1;
       e.ssq_step = K;
-      GemmPlan pl = gemm_plan_bf16(B, dm.Vimg, d);
+      GemmPlan pl = gemm_plan_bf16(B, dm.Vimg, d, X);
       m->prof.run(4, (double)dm.Vimg * d * es + (double)B * d * A + (double)B * dm.Vimg * 4, st, [&] {
         gemm_bf16(pl, m->wlm, dm.Vimg, d, (const uint16_t*)s->xn + (size_t)(K - 1) * d, s->xn_plane, K * d, B, e,
                   s->gpart, s->gcnt, st);
@@ -390,6 +393,37 @@ void run_forward(ssd_session* s, int K, int lm_mode) {
   HIPCHK(hipGetLastError());
 }
 
+// Number of XCDs if workgroup w always runs on XCD w % X (checked on 4096
+// workgroups through the XCC_ID register), else 0 -- the cross-workgroup
+// reductions then fall back to device-scope fences.  SSD_NO_XCD_LOCAL=1 forces
+// the fallback.
+int detect_xcd(hipStream_t st) {
+  const char* env = std::getenv("SSD_NO_XCD_LOCAL");
+  if (env && env[0] == '1') return 0;
+  const int n = 4096;
+  int* d = nullptr;
+  if (hipMalloc(&d, n * sizeof(int)) != hipSuccess) {
+    (void)hipGetLastError();
+    return 0;
+  }
+  xcc_probe(d, n, st);
+  std::vector<int> h(n, -1);
+  bool ok = hipGetLastError() == hipSuccess &&
+            hipMemcpyAsync(h.data(), d, n * sizeof(int), hipMemcpyDeviceToHost, st) == hipSuccess &&
+            hipStreamSynchronize(st) == hipSuccess;
+  (void)hipFree(d);
+  if (!ok) {
+    (void)hipGetLastError();
+    return 0;
+  }
+  int X = 0;
+  for (int v : h) X = std::max(X, v + 1);
+  if (X < 1) return 0;
+  for (int w = 0; w < n; ++w)
+    if (h[w] != w % X) return 0;
+  return X;
+}
+
 // workspace sizes for a session that runs blocks of up to Kmax tokens and a prefill of P
 void size_workspaces(const Dims& dm, int B, int P, int Kmax, int Lmax, size_t& gpart, size_t& gcnt, size_t& apart,
                      size_t& acnt, int& ssq_parts_max) {
@@ -404,7 +438,7 @@ void size_workspaces(const Dims& dm, int B, int P, int Kmax, int Lmax, size_t& g
   for (int Mc : {1, 16, 17, 32, 33, 64, 65, 128}) {
     for (auto nk : {std::make_pair(Nqkv, dm.d), std::make_pair(dm.d, dm.Hq * dm.D), std::make_pair(2 * dm.dff, dm.d),
                     std::make_pair(dm.d, dm.dff), std::make_pair(dm.Vimg, dm.d)}) {
-      GemmPlan p = gemm_plan_bf16(Mc, nk.first, nk.second);
+      GemmPlan p = gemm_plan_bf16(Mc, nk.first, nk.second, 0);  // sizes do not depend on the XCD mapping
       gpart = std::max(gpart, gemm_partials_floats(p, Mc));
       gcnt = std::max(gcnt, (size_t)p.n_fb);
       if (nk.first == dm.d) ssq_parts_max = std::max(ssq_parts_max, p.n_fb);
@@ -416,11 +450,11 @@ void size_workspaces(const Dims& dm, int B, int P, int Kmax, int Lmax, size_t& g
   Ks.push_back(P);
   for (int K : Ks) {
     for (int ctx = 1; ctx <= Lmax + 63; ctx += 64) {
-      AttnPlan pc = attn_plan(dm, B, K, std::min(ctx, Lmax));
+      AttnPlan pc = attn_plan(dm, B, K, std::min(ctx, Lmax), 0);
       apart = std::max(apart, attn_partials_floats(dm, pc, B));
       acnt = std::max(acnt, (size_t)B * dm.Hkv * pc.nqg);
     }
-    AttnPlan pa = attn_plan(dm, B, K, Lmax);
+    AttnPlan pa = attn_plan(dm, B, K, Lmax, 0);
     apart = std::max(apart, attn_partials_floats(dm, pa, B));
     acnt = std::max(acnt, (size_t)B * dm.Hkv * pa.nqg);
   }
@@ -642,6 +676,7 @@ ssd_status ssd_init_model(const ssd_model_config* cfg, const void* weights, void
     m->gf = gain(off);
     off += d;
     m->wlm = pack(off + (size_t)dm.img_lo * d, dm.Vimg, d, d_map_id);
+    if (dm.bf16) m->xcd = detect_xcd(st);
     off += (size_t)dm.V * d;
     if ((int64_t)off != numel_of(*cfg)) throw HipError{hipErrorInvalidValue, "layout size mismatch"};
     HIPCHK(hipStreamSynchronize(st));

@@ -88,10 +88,31 @@ struct GemmPlan {
   int n_fb;         // feature blocks
   int kchunks;      // chunks per split
   int bn;           // features per workgroup
+  int xcd;          // >0: workgroups that reduce together share one XCD (n XCDs); 0: fenced reduction
 };
 
+// Cross-workgroup reductions (split-K partials, attention key chunks).  The
+// workgroups of one reduction group are mapped onto one XCD, so their
+// partials meet in that XCD's L2 and the last arrival needs no device-scope
+// fence (no L2 write-back/invalidate).  Workgroup w runs on XCD w % X; group g
+// lives on XCD g % X as its (g / X)-th group there.
+__host__ __device__ inline int xcd_grid(int groups, int per_group, int X) {
+  return X > 0 ? ((groups + X - 1) / X) * X * per_group : groups * per_group;
+}
+// -> (group, member) of workgroup w; group >= groups means idle
+__host__ __device__ inline void xcd_unmap(int w, int per_group, int X, int& group, int& member) {
+  if (X > 0) {
+    const int x = w % X, slot = w / X;
+    group = (slot / per_group) * X + x;
+    member = slot % per_group;
+  } else {
+    group = w / per_group;
+    member = w % per_group;
+  }
+}
+
 // ---- launchers (kernels_*.hip) ----
-GemmPlan gemm_plan_bf16(int M, int N, int K);
+GemmPlan gemm_plan_bf16(int M, int N, int K, int xcd);
 size_t gemm_partials_floats(const GemmPlan& p, int M);
 // y = W x for split inputs in[M][K] (row stride ld_in, lo plane in_plane elements after hi); epilogue per `epi`.
 void gemm_bf16(const GemmPlan& p, const void* Wpacked, int N, int K, const void* in, size_t in_plane, int ld_in,
@@ -113,8 +134,9 @@ struct AttnPlan {
   int qpw;        // query tiles per workgroup
   int nqg;        // query groups
   int rows;       // query rows per (b, kv head) = K * g
+  int xcd;        // see xcd_grid
 };
-AttnPlan attn_plan(const Dims& dm, int B, int K, int max_ctx_now);
+AttnPlan attn_plan(const Dims& dm, int B, int K, int max_ctx_now, int xcd);
 size_t attn_partials_floats(const Dims& dm, const AttnPlan& p, int B);
 void attention_bf16(const Dims& dm, const AttnPlan& p, int B, int K, const int* f, const void* q, size_t q_plane,
                     const void* kc, const void* vc, int Lmax, void* o, size_t o_plane, float* partials,
@@ -148,6 +170,8 @@ void commit_update(int B, int K, int Vimg, const float* logits, float* carry, in
                    hipStream_t st);
 // fill helpers (graph-capture safe)
 void fill_u32(unsigned* p, size_t n, unsigned v, hipStream_t st);
+// out[w] = XCD index workgroup w ran on
+void xcc_probe(int* out, int n_wg, hipStream_t st);
 // references of block positions f+k <- src rows (b * rows_per_b + k); only_new keeps existing references
 void set_ref_rows(int B, int K, int rows_per_b, int Vimg, const float* src, const int* f, float* ref, int* ref_flag,
                   int ring, int only_new, hipStream_t st);
