@@ -63,8 +63,9 @@ typedef enum {
  * SwiGLU MLP W2(silu(W1 z) * W3 z) (the form Eq. 2 writes out), final RMSNorm
  * and an output layer ("GenHead") restricted to the image codes.
  * n_heads must be a multiple of n_kv_heads; head_dim must be even.
- * bf16 models: d_model, head_dim, d_ff and img_hi-img_lo must be multiples
- * of 32 and head_dim a multiple of 16.
+ * bf16 models: d_model, n_heads*head_dim and d_ff must be multiples of 256,
+ * d_model at most 8192, head_dim 64 or 128, img_hi-img_lo a multiple of 16.
+ * fp32 models: d_model and img_hi-img_lo even.  Other shapes: SSD_E_INVAL.
  */
 typedef struct {
   int32_t n_layers, d_model, n_heads, n_kv_heads, head_dim, d_ff, vocab;

@@ -6,16 +6,18 @@
 // (Sec. 3.3), so no other mask exists; the drafted block simply occupies the
 // next raster positions.
 //
-// bf16 path: one wave per (key chunk, query group, sequence x KV head).  The
-// K*g query rows of a KV head (g = query heads per KV head) are tiled by 16;
-// S^T = K Q^T and O^T = V^T P^T run on v_mfma_f32_16x16x32_bf16 with queries
-// as the MFMA columns, so the softmax statistics of a query live in one lane
-// column and need only two cross-lane shuffles; the P^T operand is built in
-// registers straight from the S^T accumulators (its key order is matched by
-// reading the transposed V cache), so P never touches LDS.  Keys are streamed
-// 32 at a time with an online softmax; chunks of the context run on different
-// workgroups and the last one to finish merges the partial (max, sum, O)
-// triples in chunk order.
+// bf16 path: a workgroup of four waves owns one key chunk of one query group
+// (up to 32 query rows of one sequence x KV head; the K*g rows of a KV head,
+// g = query heads per KV head, are tiled by 16).  Wave w streams the chunk's
+// 32-key blocks w, w+4, ... : S^T = K Q^T and O^T = V^T P^T run on
+// v_mfma_f32_16x16x32_bf16 with queries as the MFMA columns, so the softmax
+// statistics of a query live in one lane column and need two cross-lane
+// shuffles; the P^T operand is built in registers straight from the S^T
+// accumulators (its key order is matched by reading the transposed V cache),
+// so P never touches LDS.  The four waves' (max, sum, O) triples are merged
+// through LDS.  Chunks of one query group run on workgroups of one XCD; each
+// publishes its merged triple and the last to arrive combines them in chunk
+// order, all threads loading in parallel.
 #include "ssd_internal.h"
 
 namespace ssd {
@@ -29,39 +31,70 @@ __device__ __forceinline__ uint16_t f2bf_a(float f) {
   return (uint16_t)(u >> 16);
 }
 
+constexpr int ATTN_WAVES = 4;
+constexpr int ATTN_KEYS = 32;                           // keys per wave step
+constexpr int ATTN_MIN_CHUNK = ATTN_WAVES * ATTN_KEYS;  // keys per workgroup step
+constexpr int ATTN_MAX_CHUNKS = 64;
+
 struct AttnKArgs {
   const uint16_t* q;   // [B][Hq][K][D], hi plane then lo plane (q_plane elements apart)
   const uint16_t* kc;  // [B][Hkv][Lmax][D]
   const uint16_t* vc;  // [B][Hkv][D][Lmax]
   uint16_t* o;         // [B*K][Hq*D], hi plane then lo plane (o_plane elements apart)
   size_t q_plane, o_plane;
-  float* part;         // [B*Hkv][nqg][nchunk][QPW*16][D+2]
-  unsigned* counters;  // [B*Hkv][nqg]
+  float* opart;        // [groups][nchunk][QPW*16][D]   chunk partial O (relative to the chunk max)
+  float2* spart;       // [groups][nchunk][QPW*16]      chunk (max, sum), log2 domain
+  unsigned* counters;  // [groups]
   const int* f;
   int K, Hq, Hkv, g, Lmax, rows, chunk, nchunk, nqg, groups, xcd;
   float scale_log2;
 };
 
+// hi/lo bf16 planes of four consecutive fp32 values
+__device__ __forceinline__ void store_split4(uint16_t* p, size_t plane, floatx4 v) {
+  uint16_t hi[4], lo[4];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    hi[e] = f2bf_a(v[e]);
+    lo[e] = f2bf_a(v[e] - __uint_as_float((uint32_t)hi[e] << 16));
+  }
+  uint2 w, x;
+  w.x = (uint32_t)hi[0] | ((uint32_t)hi[1] << 16);
+  w.y = (uint32_t)hi[2] | ((uint32_t)hi[3] << 16);
+  x.x = (uint32_t)lo[0] | ((uint32_t)lo[1] << 16);
+  x.y = (uint32_t)lo[2] | ((uint32_t)lo[3] << 16);
+  *(uint2*)p = w;
+  *(uint2*)(p + plane) = x;
+}
+
 template <int D, int QPW>
-__global__ __launch_bounds__(64) void attn_bf16_kernel(AttnKArgs a) {
+__global__ __launch_bounds__(256) void attn_bf16_kernel(AttnKArgs a) {
   constexpr int KD = D / 32;   // 32-wide k steps over the head dimension
   constexpr int DT = D / 16;   // 16-row d tiles of O^T
+  constexpr int ROWS = QPW * 16;
+  constexpr int RS = D + 4;    // LDS row stride (floats): rows of one wave fall on different banks
+  constexpr int NV = ROWS * D / 4 / 256;  // float4 outputs per thread
+  static_assert(NV >= 1 && ROWS * D / 4 == NV * 256, "thread map");
+  static_assert(3 * ATTN_MAX_CHUNKS * ROWS <= ATTN_WAVES * ROWS * RS, "chunk statistics fit the O stage");
+  __shared__ __align__(16) float sm_o[ATTN_WAVES * ROWS * RS];
+  __shared__ float sm_m[ATTN_WAVES * ROWS], sm_l[ATTN_WAVES * ROWS];
   __shared__ int is_last;
+
   // reduction group = (sequence x KV head, query group); members = key chunks, all on one XCD
   int grp_id, c;
   xcd_unmap(blockIdx.x, a.nchunk, a.xcd, grp_id, c);
   if (grp_id >= a.groups) return;
   const int qg = grp_id % a.nqg, z = grp_id / a.nqg;
   const int b = z / a.Hkv, hkv = z - b * a.Hkv;
-  const int lane = threadIdx.x;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int col = lane & 15, grp = lane >> 4;
   const int fb = a.f[b];
   const int ctx = fb + a.K;
   const int nch = (ctx + a.chunk - 1) / a.chunk;
-  if (c >= nch) return;
+  if (c >= nch) return;  // whole workgroup, before any barrier
   const int kbeg = c * a.chunk;
   const int kend = min(kbeg + a.chunk, ctx);
-  const int rbase = qg * QPW * 16;
+  const int rbase = qg * ROWS;
 
   // query fragments (B operand of S^T = K Q^T): lane holds row col of tile qt, d = 8*grp.. (+32 kd);
   // q is fp32 carried as hi + lo bf16 operands
@@ -96,7 +129,7 @@ __global__ __launch_bounds__(64) void attn_bf16_kernel(AttnKArgs a) {
   const uint16_t* kbase = a.kc + ((size_t)b * a.Hkv + hkv) * a.Lmax * D;
   const uint16_t* vbase = a.vc + ((size_t)b * a.Hkv + hkv) * (size_t)D * a.Lmax;
 
-  for (int key0 = kbeg; key0 < kend; key0 += 32) {
+  for (int key0 = kbeg + wave * ATTN_KEYS; key0 < kend; key0 += ATTN_MIN_CHUNK) {
     // S^T tiles for keys key0 + [0,16) and key0 + [16,32)
     floatx4 s[2][QPW];
 #pragma unroll
@@ -182,67 +215,77 @@ __global__ __launch_bounds__(64) void attn_bf16_kernel(AttnKArgs a) {
       }
     }
   }
-  // column sums of l
+
+  // stage this wave's triple: O^T accumulator element e of tile (qt, dt) is row
+  // qt*16 + col, dims dt*16 + 4*grp + e
 #pragma unroll
   for (int qt = 0; qt < QPW; ++qt) {
     l[qt] += __shfl_xor(l[qt], 16);
     l[qt] += __shfl_xor(l[qt], 32);
+    float* row = sm_o + (size_t)(wave * ROWS + qt * 16 + col) * RS;
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) *(floatx4*)(row + dt * 16 + 4 * grp) = O[qt][dt];
+    if (grp == 0) {
+      sm_m[wave * ROWS + qt * 16 + col] = m[qt];
+      sm_l[wave * ROWS + qt * 16 + col] = l[qt];
+    }
+  }
+  __syncthreads();
+
+  // merge the four waves: thread owns NV float4 slots (row r, dims 4*d4..)
+  floatx4 acc[NV];
+  float Lr[NV], Mr[NV];
+#pragma unroll
+  for (int i = 0; i < NV; ++i) {
+    const int idx = threadIdx.x + 256 * i;
+    const int r = idx / (D / 4), d4 = idx - r * (D / 4);
+    float M = -INFINITY;
+#pragma unroll
+    for (int w = 0; w < ATTN_WAVES; ++w) M = fmaxf(M, sm_m[w * ROWS + r]);
+    float L = 0.f;
+    floatx4 v = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int w = 0; w < ATTN_WAVES; ++w) {
+      const float mw = sm_m[w * ROWS + r];
+      const float ew = (mw == -INFINITY) ? 0.f : exp2f(mw - M);
+      L += sm_l[w * ROWS + r] * ew;
+      v += *(const floatx4*)(sm_o + (size_t)(w * ROWS + r) * RS + 4 * d4) * ew;
+    }
+    acc[i] = v;
+    Lr[i] = L;
+    Mr[i] = M;
   }
 
   if (nch == 1) {
 #pragma unroll
-    for (int qt = 0; qt < QPW; ++qt) {
-      const int r = rbase + qt * 16 + col;
-      if (r >= a.rows) continue;
-      const int j = r / a.K, k = r - j * a.K;
-      const float inv = 1.f / l[qt];
-      uint16_t* op = a.o + ((size_t)b * a.K + k) * (a.Hq * D) + (hkv * a.g + j) * D;
-#pragma unroll
-      for (int dt = 0; dt < DT; ++dt) {
-        const int d0 = dt * 16 + 4 * grp;
-        uint16_t hi[4], lo[4];
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const float v = O[qt][dt][e] * inv;
-          hi[e] = f2bf_a(v);
-          lo[e] = f2bf_a(v - __uint_as_float((uint32_t)hi[e] << 16));
-        }
-        uint2 w, x;
-        w.x = (uint32_t)hi[0] | ((uint32_t)hi[1] << 16);
-        w.y = (uint32_t)hi[2] | ((uint32_t)hi[3] << 16);
-        x.x = (uint32_t)lo[0] | ((uint32_t)lo[1] << 16);
-        x.y = (uint32_t)lo[2] | ((uint32_t)lo[3] << 16);
-        *(uint2*)(op + d0) = w;
-        *(uint2*)(op + a.o_plane + d0) = x;
-      }
+    for (int i = 0; i < NV; ++i) {
+      const int idx = threadIdx.x + 256 * i;
+      const int r = idx / (D / 4), d4 = idx - r * (D / 4);
+      const int rg = rbase + r;
+      if (rg >= a.rows) continue;
+      const int j = rg / a.K, k = rg - j * a.K;
+      uint16_t* op = a.o + ((size_t)b * a.K + k) * (a.Hq * D) + (hkv * a.g + j) * D + 4 * d4;
+      store_split4(op, a.o_plane, acc[i] * (1.f / Lr[i]));
     }
     return;
   }
 
-  // publish the partial (O unnormalised, m, l) of this chunk
-  constexpr int RS = D + 2;
-  const size_t grp_base = (size_t)grp_id * a.nchunk;
-  float* P = a.part + (grp_base + c) * (QPW * 16) * RS;
+  // publish the chunk's triple
+  const size_t gbase = (size_t)grp_id * a.nchunk;
+  {
+    floatx4* Op = (floatx4*)(a.opart + (gbase + c) * ROWS * D);
 #pragma unroll
-  for (int qt = 0; qt < QPW; ++qt) {
-    float* pr = P + (size_t)(qt * 16 + col) * RS;
-#pragma unroll
-    for (int dt = 0; dt < DT; ++dt) {
-      const int d0 = dt * 16 + 4 * grp;
-      pr[d0 + 0] = O[qt][dt][0];
-      pr[d0 + 1] = O[qt][dt][1];
-      pr[d0 + 2] = O[qt][dt][2];
-      pr[d0 + 3] = O[qt][dt][3];
-    }
-    if (grp == 0) {
-      pr[D] = m[qt];
-      pr[D + 1] = l[qt];
+    for (int i = 0; i < NV; ++i) {
+      const int idx = threadIdx.x + 256 * i;
+      Op[idx] = acc[i];
+      const int r = idx / (D / 4), d4 = idx - r * (D / 4);
+      if (d4 == 0) a.spart[(gbase + c) * ROWS + r] = make_float2(Mr[i], Lr[i]);
     }
   }
   // partial stores acknowledged by this XCD's L2, then count the arrival
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
-  if (lane == 0) {
+  if (threadIdx.x == 0) {
     if (!a.xcd) __threadfence();  // chunks on different XCDs: write back through L2
     unsigned prev = atomicAdd(&a.counters[grp_id], 1u);
     is_last = (prev == (unsigned)(nch - 1));
@@ -250,45 +293,45 @@ __global__ __launch_bounds__(64) void attn_bf16_kernel(AttnKArgs a) {
   }
   __syncthreads();
   if (!is_last) return;
-  // merge the chunks: per query row, lane c holds chunk c's statistics; the
-  // O rows are summed in chunk order with lanes over the head dimension
-  const float* G = a.part + grp_base * (QPW * 16) * RS;
-  for (int rr = 0; rr < QPW * 16; ++rr) {
-    const int r = rbase + rr;
-    if (r >= a.rows) break;
-    float mc = -INFINITY, lc = 0.f;
-    if (lane < nch) {
-      const float* pr = G + ((size_t)lane * QPW * 16 + rr) * RS;
-      mc = pr[D];
-      lc = pr[D + 1];
-    }
-    float M = mc;
-    for (int o = 32; o > 0; o >>= 1) M = fmaxf(M, __shfl_xor(M, o));
-    const float wv = (lc > 0.f) ? exp2f(mc - M) : 0.f;
-    float L = lc * wv;
-    for (int o = 32; o > 0; o >>= 1) L += __shfl_xor(L, o);
-    float acc[D / 64];
-#pragma unroll
-    for (int i = 0; i < D / 64; ++i) acc[i] = 0.f;
-    for (int cc = 0; cc < nch; ++cc) {
-      const float wgt = __shfl(wv, cc);
-      if (wgt == 0.f) continue;
-      const float* pr = G + ((size_t)cc * QPW * 16 + rr) * RS;
-#pragma unroll
-      for (int i = 0; i < D / 64; ++i) acc[i] += pr[lane + 64 * i] * wgt;
-    }
-    const int j = r / a.K, k = r - j * a.K;
-    uint16_t* op = a.o + ((size_t)b * a.K + k) * (a.Hq * D) + (hkv * a.g + j) * D;
-    const float inv = 1.f / L;
-#pragma unroll
-    for (int i = 0; i < D / 64; ++i) {
-      const float v = acc[i] * inv;
-      const uint16_t hi = f2bf_a(v);
-      op[lane + 64 * i] = hi;
-      op[a.o_plane + lane + 64 * i] = f2bf_a(v - __uint_as_float((uint32_t)hi << 16));
-    }
+
+  // last chunk: statistics of every (chunk, row) into LDS (parallel loads)
+  float* cm = sm_o;                          // [nch][ROWS] chunk max
+  float* cl = sm_o + ATTN_MAX_CHUNKS * ROWS; // [nch][ROWS] chunk sum, then weight
+  for (int i = threadIdx.x; i < nch * ROWS; i += 256) {
+    const float2 st = a.spart[gbase * ROWS + i];
+    cm[i] = st.x;
+    cl[i] = st.y;
   }
-  if (lane == 0) a.counters[grp_id] = 0u;
+  __syncthreads();
+  if (threadIdx.x < ROWS) {
+    const int r = threadIdx.x;
+    float M = -INFINITY;
+    for (int cc = 0; cc < nch; ++cc) M = fmaxf(M, cm[cc * ROWS + r]);
+    float L = 0.f;
+    for (int cc = 0; cc < nch; ++cc) {
+      const float lc = cl[cc * ROWS + r];
+      const float w = (lc > 0.f) ? exp2f(cm[cc * ROWS + r] - M) : 0.f;
+      L += lc * w;
+      cl[cc * ROWS + r] = w;
+    }
+    sm_l[r] = L;
+  }
+  __syncthreads();
+  const floatx4* G = (const floatx4*)(a.opart + gbase * ROWS * D);
+#pragma unroll
+  for (int i = 0; i < NV; ++i) {
+    const int idx = threadIdx.x + 256 * i;
+    const int r = idx / (D / 4), d4 = idx - r * (D / 4);
+    floatx4 v = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll 4
+    for (int cc = 0; cc < nch; ++cc) v += G[(size_t)cc * (ROWS * D / 4) + idx] * cl[cc * ROWS + r];
+    const int rg = rbase + r;
+    if (rg >= a.rows) continue;
+    const int j = rg / a.K, k = rg - j * a.K;
+    uint16_t* op = a.o + ((size_t)b * a.K + k) * (a.Hq * D) + (hkv * a.g + j) * D + 4 * d4;
+    store_split4(op, a.o_plane, v * (1.f / sm_l[r]));
+  }
+  if (threadIdx.x == 0) a.counters[grp_id] = 0u;
 }
 
 AttnPlan attn_plan(const Dims& dm, int B, int K, int max_ctx_now, int xcd) {
@@ -299,15 +342,14 @@ AttnPlan attn_plan(const Dims& dm, int B, int K, int max_ctx_now, int xcd) {
   const int qt = (p.rows + 15) / 16;
   p.qpw = qt >= 2 ? 2 : 1;
   p.nqg = (qt + p.qpw - 1) / p.qpw;
-  // chunk: enough workgroups to cover the chip, at least 64 keys
-  const int units = B * dm.Hkv * p.nqg;
-  int chunk = 64;
-  // at most 64 chunks (the merge holds one chunk per lane)
-  while ((chunk < 2048 && (long)units * ((max_ctx_now + chunk - 1) / chunk) > 1024) ||
-         (max_ctx_now + chunk - 1) / chunk > 64)
-    chunk *= 2;
+  // chunk (multiple of one workgroup step): enough workgroups to cover the
+  // chip, at most ATTN_MAX_CHUNKS chunks per query group
+  const long units = (long)B * dm.Hkv * p.nqg;
+  int chunk = ATTN_MIN_CHUNK;
+  auto nchunks = [&](int ch) { return (max_ctx_now + ch - 1) / ch; };
+  while ((chunk < 4096 && units * nchunks(chunk) > 1024) || nchunks(chunk) > ATTN_MAX_CHUNKS) chunk *= 2;
   p.chunk = chunk;
-  p.nchunk = (max_ctx_now + chunk - 1) / chunk;
+  p.nchunk = nchunks(chunk);
   return p;
 }
 
@@ -317,7 +359,7 @@ size_t attn_partials_floats(const Dims& dm, const AttnPlan& p, int B) {
 
 template <int D, int QPW>
 static void launch_attn(const AttnKArgs& a, hipStream_t st) {
-  hipLaunchKernelGGL((attn_bf16_kernel<D, QPW>), dim3(xcd_grid(a.groups, a.nchunk, a.xcd)), dim3(64), 0, st, a);
+  hipLaunchKernelGGL((attn_bf16_kernel<D, QPW>), dim3(xcd_grid(a.groups, a.nchunk, a.xcd)), dim3(256), 0, st, a);
 }
 
 void attention_bf16(const Dims& dm, const AttnPlan& p, int B, int K, const int* f, const void* q, size_t q_plane,
@@ -330,7 +372,10 @@ void attention_bf16(const Dims& dm, const AttnPlan& p, int B, int K, const int* 
   a.o = (uint16_t*)o;
   a.q_plane = q_plane;
   a.o_plane = o_plane;
-  a.part = partials;
+  a.groups = B * dm.Hkv * p.nqg;
+  // partial O block first, then the (max, sum) pairs (offset is a multiple of D floats: 8-byte aligned)
+  a.opart = partials;
+  a.spart = (float2*)(partials + (size_t)a.groups * p.nchunk * p.qpw * 16 * dm.D);
   a.counters = counters;
   a.f = f;
   a.K = K;
@@ -342,7 +387,6 @@ void attention_bf16(const Dims& dm, const AttnPlan& p, int B, int K, const int* 
   a.chunk = p.chunk;
   a.nchunk = p.nchunk;
   a.nqg = p.nqg;
-  a.groups = B * dm.Hkv * p.nqg;
   a.xcd = p.nchunk > 1 ? p.xcd : 0;
   a.scale_log2 = 1.4426950408889634f / sqrtf((float)dm.D);
   if (dm.D == 128) {

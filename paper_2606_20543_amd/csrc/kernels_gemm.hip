@@ -138,17 +138,24 @@ struct GemmKArgs {
 template <int NT, int KCB>
 __device__ __forceinline__ void load_a(u32x4 (&ra)[NT][KCB], const u32x4* W, int KB, int nb0, int N, int kb0,
                                        int lane) {
+  // feature tiles past N reload the last tile (no branch: a branch around the
+  // burst makes the compiler wait for all of it at the join); their results
+  // are never stored
+  const u32x4* p[NT];
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt) {
-    if ((nb0 + nt) * 16 < N) {
-      const u32x4* p = W + ((size_t)(nb0 + nt) * KB + kb0) * 64 + lane;
-#pragma unroll
-      for (int kb = 0; kb < KCB; ++kb) ra[nt][kb] = __builtin_nontemporal_load(p + kb * 64);
-    } else {
-#pragma unroll
-      for (int kb = 0; kb < KCB; ++kb) ra[nt][kb] = u32x4{0u, 0u, 0u, 0u};
-    }
+    const int nb = (nb0 + nt) * 16 < N ? nb0 + nt : N / 16 - 1;
+    p[nt] = W + ((size_t)nb * KB + kb0) * 64 + lane;
   }
+  // issued in the order the MFMAs consume them (k-block major), each waited
+  // for by its position in the queue: no scheduling across the loads
+#pragma unroll
+  for (int kb = 0; kb < KCB; ++kb)
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
+      ra[nt][kb] = __builtin_nontemporal_load(p[nt] + kb * 64);
+      __builtin_amdgcn_sched_barrier(0);
+    }
 }
 
 template <int MT, int KCB>
@@ -168,17 +175,15 @@ __device__ __forceinline__ void load_x(u32x4 (&rx)[2][NP], const uint16_t* in, s
                                        int k0) {
   using X = XStage<MT, KCB>;
   const int cg = threadIdx.x % X::CG, r0 = threadIdx.x / X::CG;
+  // token rows past M repeat row M-1: no branch around the loads (so they
+  // issue back to back); the results of those rows are never stored
 #pragma unroll
   for (int p = 0; p < NP; ++p) {
-    int r = r0 + p * X::RSTEP;
-    if (r < M && r < X::MP) {
-      const uint16_t* src = in + (size_t)r * ld_in + k0 + cg * 8;
-      rx[0][p] = *(const u32x4*)src;
-      rx[1][p] = *(const u32x4*)(src + plane);
-    } else {
-      rx[0][p] = u32x4{0u, 0u, 0u, 0u};
-      rx[1][p] = u32x4{0u, 0u, 0u, 0u};
-    }
+    const int r = r0 + p * X::RSTEP;
+    const int rc = r < M ? r : M - 1;
+    const uint16_t* src = in + (size_t)rc * ld_in + k0 + cg * 8;
+    rx[0][p] = *(const u32x4*)src;
+    rx[1][p] = *(const u32x4*)(src + plane);
   }
 }
 
@@ -189,13 +194,14 @@ __device__ __forceinline__ void store_x(const u32x4 (&rx)[2][NP], uint16_t* xs) 
 #pragma unroll
   for (int p = 0; p < NP; ++p) {
     int r = r0 + p * X::RSTEP;
-    if (r < X::MP) {
+    if (X::PASSES * X::RSTEP == X::MP || r < X::MP) {
       *(u32x4*)(xs + r * X::LD + cg * 8) = rx[0][p];
       *(u32x4*)(xs + X::PL + r * X::LD + cg * 8) = rx[1][p];
     }
   }
 }
 
+// k-block order, so the MFMAs of block kb wait only for that block's weights
 template <int MT, int NT, int KCB>
 __device__ __forceinline__ void compute_chunk(floatx4 (&acc)[NT][MT], const u32x4 (&ra)[NT][KCB], const uint16_t* xs,
                                               int lane) {
@@ -222,8 +228,56 @@ __device__ __forceinline__ void compute_chunk(floatx4 (&acc)[NT][MT], const u32x
   }
 }
 
-// per-token 1/rms(x) from the producer's partial sums, loaded in parallel
-// (parts in blocks of 16 through LDS, summed in part order)
+// ---- per-token 1/rms(x) from the producer's partial sums of x^2 ----
+// Thread (t = tid % MP, part group pg = tid / MP) loads parts pg, pg + G, ...
+// into registers before the weight burst is issued (so the wait for them does
+// not wait for the weights), sums them in part order, and the G group sums
+// meet in LDS (summed in group order: deterministic).
+template <int MP>
+struct RmsPre {
+  static constexpr int G = 256 / MP;
+  static constexpr int RQ = (GEMM_RMS_MAX_PARTS + G - 1) / G;
+};
+
+// raw loads only (no use of the values, so nothing waits for them here);
+// without partial sums (ssq == nullptr) the loads read in[0] and are ignored
+template <int MP>
+__device__ __forceinline__ void rms_issue(const EpiArgs& e, const void* dummy, int M, int t0,
+                                          float (&v)[RmsPre<MP>::RQ]) {
+  const int t = threadIdx.x % MP, pg = threadIdx.x / MP;
+  const int tc = t < M ? t : M - 1;
+  const bool has = e.ssq != nullptr;
+  const float* base = has ? e.ssq : (const float*)dummy;
+  const size_t c = has ? (size_t)e.ssq_off + (size_t)(t0 + tc) * e.ssq_step : 0;
+  const size_t ld = has ? (size_t)e.ssq_ld : 0;
+#pragma unroll
+  for (int q = 0; q < RmsPre<MP>::RQ; ++q) {
+    const int p = pg + q * RmsPre<MP>::G;
+    v[q] = base[(size_t)(p < e.ssq_parts ? p : 0) * ld + c];
+  }
+}
+
+// writes rscale[0..MP); visible after the caller's next barrier
+template <int MP>
+__device__ __forceinline__ void rms_finish(const EpiArgs& e, const float (&v)[RmsPre<MP>::RQ], float* red,
+                                           float* rscale) {
+  // branch-free in ssq (a branch here would make the compiler settle the
+  // weight loads at the join); without partial sums the scale is 1
+  const int pg = threadIdx.x / MP;
+  float s = 0.f;
+#pragma unroll
+  for (int q = 0; q < RmsPre<MP>::RQ; ++q) s += (pg + q * RmsPre<MP>::G < e.ssq_parts) ? v[q] : 0.f;
+  red[threadIdx.x] = s;  // [pg][t]
+  lds_barrier();
+  if (threadIdx.x < MP) {
+    float a = 0.f;
+#pragma unroll
+    for (int g = 0; g < RmsPre<MP>::G; ++g) a += red[g * MP + threadIdx.x];
+    rscale[threadIdx.x] = e.ssq ? 1.0f / sqrtf(a * e.inv_d + e.eps) : 1.f;
+  }
+}
+
+// per-token 1/rms(x) for large token tiles (parts in blocks of 16 through LDS)
 template <int MP>
 __device__ __forceinline__ void rms_prologue(const EpiArgs& e, int M, int t0, float (*red)[MP], float* rscale) {
   float s = 0.f;
@@ -234,23 +288,185 @@ __device__ __forceinline__ void rms_prologue(const EpiArgs& e, int M, int t0, fl
                            ? e.ssq[(size_t)p * e.ssq_ld + (size_t)e.ssq_off + (size_t)(t0 + t) * e.ssq_step]
                            : 0.f;
     }
-    __syncthreads();
+    lds_barrier();
     if (threadIdx.x < MP)
       for (int p = 0; p < 16; ++p) s += red[p][threadIdx.x];
-    __syncthreads();
+    lds_barrier();
   }
   if (threadIdx.x < MP) rscale[threadIdx.x] = 1.0f / sqrtf(s * e.inv_d + e.eps);
 }
 
+// ---- fused epilogue, bf16 path ----
+// The accumulator fragment acc[nt][mt] of a lane holds features n .. n+3
+// (n = (nb0 + nt) * 16 + 4 * (lane / 16)) of token t0 + mt * 16 + lane % 16.
+// Operands that do not depend on the accumulators (the token's raster
+// position, rotary factors, g_next, the old residual) are loaded first, in
+// one batch, and the stores follow: no load waits behind a store.
+__device__ __forceinline__ uint32_t pack2(uint16_t a, uint16_t b) { return (uint32_t)a | ((uint32_t)b << 16); }
+
+__device__ __forceinline__ void split2(float a, float b, uint32_t& hi, uint32_t& lo) {
+  const uint16_t ha = f2bf(a), hb = f2bf(b);
+  hi = pack2(ha, hb);
+  lo = pack2(f2bf(a - bf2f(ha)), f2bf(b - bf2f(hb)));
+}
+
+template <int NT, int MT>
+struct EpiOps {
+  float4 a[NT][MT];  // RESID: old x[t][n..n+3]; QKV: (cos, sin) of rotary pairs j, j+1 at the token's position
+  float4 g[NT];      // RESID: g_next[n..n+3]
+  int pos[MT];       // QKV: raster position of the token
+};
+
+// block start f[b] of each fragment token (raw load; the position is formed at the epilogue)
+template <int NT, int MT>
+__device__ __forceinline__ void epi_block_starts(const EpiArgs& e, int M, int t0, int lane, EpiOps<NT, MT>& op) {
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt) {
+    const int tl = mt * 16 + (lane & 15);
+    op.pos[mt] = e.f[(t0 + (tl < M ? tl : M - 1)) / e.Kblk];
+  }
+}
+
+// indexes are clamped into range (results of clamped lanes are never stored),
+// so the loads carry no branches and issue back to back
+template <int NT, int MT>
+__device__ __forceinline__ void epi_load(const EpiArgs& e, int nb0, int N, int M, int t0, int lane,
+                                         EpiOps<NT, MT>& op) {
+  const int nq = 4 * (lane >> 4);
+  if (e.kind == EPI_RESID) {
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
+      const int n = (nb0 + nt) * 16 < N ? (nb0 + nt) * 16 + nq : nq;
+      op.g[nt] = *(const float4*)(e.gnext + n);
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) {
+        const int tl = mt * 16 + (lane & 15);
+        op.a[nt][mt] = *(const float4*)(e.x + (size_t)(t0 + (tl < M ? tl : M - 1)) * e.ld + n);
+      }
+    }
+  } else if (e.kind == EPI_QKV) {
+    const int qN = e.Hq * e.D, half = e.D >> 1;
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) {
+      const int tl = mt * 16 + (lane & 15);
+      const int t = t0 + (tl < M ? tl : M - 1);
+      op.pos[mt] += t % e.Kblk;
+    }
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
+      const int n = (nb0 + nt) * 16 + nq;
+      const int nn = n < qN ? n : n - qN;
+      const int j = (nn % e.D) >> 1;  // even: pairs j, j+1
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) op.a[nt][mt] = *(const float4*)(e.rope + (size_t)op.pos[mt] * half + j);
+    }
+  }
+}
+
+// returns per-mt partial sums of the new residual squared (RESID)
+template <int NT, int MT>
+__device__ __forceinline__ void epi_store(const EpiArgs& e, const floatx4 (&acc)[NT][MT], const EpiOps<NT, MT>& op,
+                                          int nb0, int N, int M, int t0, int lane, const float* rscale,
+                                          float (&sq)[MT]) {
+  const int nq = 4 * (lane >> 4);
+  uint16_t* q = (uint16_t*)e.q;
+  uint16_t* kc = (uint16_t*)e.kc;
+  uint16_t* vc = (uint16_t*)e.vc;
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) {
+    const int n = (nb0 + nt) * 16 + nq;
+    if ((nb0 + nt) * 16 >= N) continue;
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) {
+      const int tl = mt * 16 + (lane & 15);
+      if (tl >= M) continue;
+      const int t = t0 + tl;
+      const float r = rscale[tl];
+      const floatx4 v = acc[nt][mt];
+      switch (e.kind) {
+        case EPI_QKV: {
+          const int b = t / e.Kblk, k = t - b * e.Kblk;
+          const int pos = op.pos[mt];
+          const int D = e.D, half = D >> 1;
+          const int qN = e.Hq * D, kN = e.Hkv * D;
+          if (n < qN + kN) {
+            // features n..n+3 = rotary pairs (j, j + D/2) and (j + 1, j + 1 + D/2)
+            const float4 cs = op.a[nt][mt];
+            const float x0 = v[0] * r, y0 = v[1] * r, x1 = v[2] * r, y1 = v[3] * r;
+            const float a0 = x0 * cs.x - y0 * cs.y, c0 = y0 * cs.x + x0 * cs.y;
+            const float a1 = x1 * cs.z - y1 * cs.w, c1 = y1 * cs.z + x1 * cs.w;
+            const bool isq = n < qN;
+            const int nn = isq ? n : n - qN;
+            const int head = nn / D, j = (nn - head * D) >> 1;
+            if (isq) {
+              const size_t base = (((size_t)b * e.Hq + head) * e.Kblk + k) * D;
+              uint32_t h0, l0, h1, l1;
+              split2(a0, a1, h0, l0);
+              split2(c0, c1, h1, l1);
+              *(uint32_t*)(q + base + j) = h0;
+              *(uint32_t*)(q + base + j + half) = h1;
+              *(uint32_t*)(q + e.q_plane + base + j) = l0;
+              *(uint32_t*)(q + e.q_plane + base + j + half) = l1;
+            } else {
+              const size_t base = (((size_t)b * e.Hkv + head) * e.Lmax + pos) * D;
+              *(uint32_t*)(kc + base + j) = pack2(f2bf(a0), f2bf(a1));
+              *(uint32_t*)(kc + base + j + half) = pack2(f2bf(c0), f2bf(c1));
+            }
+          } else {
+            const int nv = n - qN - kN;
+            const int head = nv / D, dd = nv - head * D;
+            const size_t base = (((size_t)b * e.Hkv + head) * D + dd) * e.Lmax + pos;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) vc[base + (size_t)i * e.Lmax] = f2bf(v[i] * r);
+          }
+          break;
+        }
+        case EPI_RESID: {
+          const size_t i = (size_t)t * e.ld + n;
+          const float4 xo = op.a[nt][mt];
+          const float4 g = op.g[nt];
+          const float4 xv = make_float4(xo.x + v[0], xo.y + v[1], xo.z + v[2], xo.w + v[3]);
+          *(float4*)(e.x + i) = xv;
+          uint32_t h0, l0, h1, l1;
+          split2(g.x * xv.x, g.y * xv.y, h0, l0);
+          split2(g.z * xv.z, g.w * xv.w, h1, l1);
+          uint16_t* xn = (uint16_t*)e.xn;
+          *(uint2*)(xn + i) = make_uint2(h0, h1);
+          *(uint2*)(xn + e.xn_plane + i) = make_uint2(l0, l1);
+          sq[mt] += (xv.x * xv.x + xv.y * xv.y) + (xv.z * xv.z + xv.w * xv.w);
+          break;
+        }
+        case EPI_SWIGLU: {
+          // packed rows (2j, 2j+1) = (gate j, up j)
+          const float g0 = v[0] * r, u0 = v[1] * r, g1 = v[2] * r, u1 = v[3] * r;
+          const float s0 = g0 / (1.0f + expf(-g0)), s1 = g1 / (1.0f + expf(-g1));
+          uint32_t hi, lo;
+          split2(s0 * u0, s1 * u1, hi, lo);
+          uint16_t* h = (uint16_t*)e.h;
+          const size_t i = (size_t)t * e.ld + (n >> 1);
+          *(uint32_t*)(h + i) = hi;
+          *(uint32_t*)(h + e.h_plane + i) = lo;
+          break;
+        }
+        default: {  // EPI_LOGITS
+          *(float4*)(e.logits + (size_t)t * e.ld + n) = make_float4(v[0] * r, v[1] * r, v[2] * r, v[3] * r);
+          break;
+        }
+      }
+    }
+  }
+}
+
 // NBUF = 1: the workgroup's whole K-slice is one chunk, loaded in one burst
-// (weights to registers, tokens to LDS); NBUF = 2: chunks double-buffered.
+// (tokens to LDS, weights to registers; the MFMAs of k-block kb start as soon
+// as its weights land); NBUF = 2: chunks double-buffered.
 template <int MT, int NT, int KCB, int NBUF>
 __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmKArgs a) {
   using X = XStage<MT, KCB>;
   __shared__ __attribute__((aligned(16))) uint16_t xs[NBUF][2 * X::PL];
   __shared__ float sq_red[4][X::MP];
   __shared__ float rscale[X::MP];
-  __shared__ float rms_red[16][X::MP];
+  __shared__ float rms_red[NBUF == 1 ? 256 : 16 * X::MP];
   __shared__ int is_last;
 
   int fb, s;
@@ -269,38 +485,50 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmKArgs a) {
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) acc[nt][mt] = floatx4{0.f, 0.f, 0.f, 0.f};
 
+  EpiOps<NT, MT> op;
   u32x4 ra[NBUF][NT][KCB];
   u32x4 rx[2][X::PASSES];
 
-  load_a<NT, KCB>(ra[0], a.W, a.KB, nb0, a.N, kb_split, lane);
-  load_x<MT, KCB>(rx, in, a.in_plane, a.ld_in, a.M, kb_split * 32);
-  // the per-token rms scale is fetched while the weights are in flight
-  if (e.ssq)
-    rms_prologue<X::MP>(e, a.M, a.t0, rms_red, rscale);
-  else if (threadIdx.x < X::MP)
-    rscale[threadIdx.x] = 1.f;
-  store_x<MT, KCB>(rx, xs[0]);
-  __syncthreads();
   if constexpr (NBUF == 1) {
+    // issue order: block starts, rms partial sums, tokens, then the weight
+    // burst; nothing is waited for before the whole burst is in flight
+    float rv[RmsPre<X::MP>::RQ];
+    epi_block_starts<NT, MT>(e, a.M, a.t0, lane, op);
+    rms_issue<X::MP>(e, in, a.M, a.t0, rv);
+    load_x<MT, KCB>(rx, in, a.in_plane, a.ld_in, a.M, kb_split * 32);
+    load_a<NT, KCB>(ra[0], a.W, a.KB, nb0, a.N, kb_split, lane);
+    __builtin_amdgcn_sched_barrier(0);
+    rms_finish<X::MP>(e, rv, rms_red, rscale);
+    store_x<MT, KCB>(rx, xs[0]);
+    lds_barrier();
     compute_chunk<MT, NT, KCB>(acc, ra[0], xs[0], lane);
   } else {
-  for (int c = 0; c < nc; c += 2) {
-    if (c + 1 < nc) {
-      load_x<MT, KCB>(rx, in, a.in_plane, a.ld_in, a.M, (kb_split + (c + 1) * KCB) * 32);
-      load_a<NT, KCB>(ra[1], a.W, a.KB, nb0, a.N, kb_split + (c + 1) * KCB, lane);
+    epi_block_starts<NT, MT>(e, a.M, a.t0, lane, op);
+    load_x<MT, KCB>(rx, in, a.in_plane, a.ld_in, a.M, kb_split * 32);
+    load_a<NT, KCB>(ra[0], a.W, a.KB, nb0, a.N, kb_split, lane);
+    if (e.ssq)
+      rms_prologue<X::MP>(e, a.M, a.t0, (float(*)[X::MP])rms_red, rscale);
+    else if (threadIdx.x < X::MP)
+      rscale[threadIdx.x] = 1.f;
+    store_x<MT, KCB>(rx, xs[0]);
+    lds_barrier();
+    for (int c = 0; c < nc; c += 2) {
+      if (c + 1 < nc) {
+        load_x<MT, KCB>(rx, in, a.in_plane, a.ld_in, a.M, (kb_split + (c + 1) * KCB) * 32);
+        load_a<NT, KCB>(ra[1], a.W, a.KB, nb0, a.N, kb_split + (c + 1) * KCB, lane);
+      }
+      compute_chunk<MT, NT, KCB>(acc, ra[0], xs[0], lane);
+      if (c + 1 < nc) store_x<MT, KCB>(rx, xs[1]);
+      lds_barrier();
+      if (c + 1 >= nc) break;
+      if (c + 2 < nc) {
+        load_x<MT, KCB>(rx, in, a.in_plane, a.ld_in, a.M, (kb_split + (c + 2) * KCB) * 32);
+        load_a<NT, KCB>(ra[0], a.W, a.KB, nb0, a.N, kb_split + (c + 2) * KCB, lane);
+      }
+      compute_chunk<MT, NT, KCB>(acc, ra[1], xs[1], lane);
+      if (c + 2 < nc) store_x<MT, KCB>(rx, xs[0]);
+      lds_barrier();
     }
-    compute_chunk<MT, NT, KCB>(acc, ra[0], xs[0], lane);
-    if (c + 1 < nc) store_x<MT, KCB>(rx, xs[1]);
-    __syncthreads();
-    if (c + 1 >= nc) break;
-    if (c + 2 < nc) {
-      load_x<MT, KCB>(rx, in, a.in_plane, a.ld_in, a.M, (kb_split + (c + 2) * KCB) * 32);
-      load_a<NT, KCB>(ra[0], a.W, a.KB, nb0, a.N, kb_split + (c + 2) * KCB, lane);
-    }
-    compute_chunk<MT, NT, KCB>(acc, ra[1], xs[1], lane);
-    if (c + 2 < nc) store_x<MT, KCB>(rx, xs[0]);
-    __syncthreads();
-  }
   }
 
   if (a.S > 1) {
@@ -324,17 +552,38 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmKArgs a) {
     }
     __syncthreads();
     if (!is_last) return;
+  }
+  // epilogue operands first, then (split-K) the partials, summed in split
+  // order; eight splits' loads are in flight together (indexes clamped, the
+  // surplus masked out of the sum, so no branch sits between the loads)
+  epi_load<NT, MT>(e, nb0, a.N, a.M, a.t0, lane, op);
+  if (a.S > 1) {
+    const size_t frag = (size_t)NT * MT * 64 * 4;
+    const float* P = a.part + ((size_t)fb * 4 + w) * frag + lane * 4;
+    const size_t split_stride = (size_t)a.n_fb * 4 * frag;
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt)
 #pragma unroll
-      for (int mt = 0; mt < MT; ++mt) {
-        floatx4 v = floatx4{0.f, 0.f, 0.f, 0.f};
-        for (int s2 = 0; s2 < a.S; ++s2) {
-          floatx4 pv = *(const floatx4*)(P + (size_t)s2 * split_stride + ((nt * MT + mt) * 64 + lane) * 4);
-          v += pv;
-        }
-        acc[nt][mt] = v;
+      for (int mt = 0; mt < MT; ++mt) acc[nt][mt] = floatx4{0.f, 0.f, 0.f, 0.f};
+    for (int s0 = 0; s0 < a.S; s0 += 8) {
+      floatx4 pv[8][NT][MT];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const float* Ps = P + (size_t)min(s0 + j, a.S - 1) * split_stride;
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+          for (int mt = 0; mt < MT; ++mt) pv[j][nt][mt] = *(const floatx4*)(Ps + (nt * MT + mt) * 64 * 4);
       }
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const float m = (s0 + j < a.S) ? 1.f : 0.f;
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+          for (int mt = 0; mt < MT; ++mt) acc[nt][mt] += pv[j][nt][mt] * m;
+      }
+    }
     if (threadIdx.x == 0) a.counters[fb] = 0u;
   }
 
@@ -342,21 +591,7 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmKArgs a) {
   float sq[MT];
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt) sq[mt] = 0.f;
-#pragma unroll
-  for (int nt = 0; nt < NT; ++nt) {
-    const int n = (nb0 + nt) * 16 + 4 * (lane >> 4);
-    if ((nb0 + nt) * 16 >= a.N) continue;
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt) {
-      const int tl = mt * 16 + (lane & 15);
-      if (tl < a.M) {
-        const int t = a.t0 + tl;
-        const float r = rscale[tl];
-        sq[mt] += epi_pair<true>(e, t, n, acc[nt][mt][0], acc[nt][mt][1], r);
-        sq[mt] += epi_pair<true>(e, t, n + 2, acc[nt][mt][2], acc[nt][mt][3], r);
-      }
-    }
-  }
+  epi_store<NT, MT>(e, acc, op, nb0, a.N, a.M, a.t0, lane, rscale, sq);
   if (e.kind == EPI_RESID) {
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
@@ -379,31 +614,44 @@ GemmPlan gemm_plan_bf16(int M, int N, int K, int xcd) {
   p.xcd = xcd;
   int Mc = M < 128 ? M : 128;
   p.MT = Mc <= 16 ? 1 : Mc <= 32 ? 2 : Mc <= 64 ? 4 : 8;
-  p.NT = p.MT >= 4 ? 2 : 1;
-  p.bn = 4 * p.NT * 16;
-  p.n_fb = (N + p.bn - 1) / p.bn;
   const int kb = K / 32;
   if (p.MT <= 2) {
     // one burst per workgroup: the smallest split count whose K-slice (8 or 16
-    // k-blocks) fits registers and LDS, preferring >= 256 workgroups
-    p.S = 0;
-    for (int s = 1; s <= kb; ++s) {
-      if (kb % s) continue;
-      const int kcb = kb / s;
-      if (kcb != 16 && kcb != 8) continue;
-      if (p.S == 0) p.S = s;
-      if (p.n_fb * s >= 256) {
-        p.S = s;
-        break;
+    // k-blocks) fits registers and LDS, preferring >= 256 workgroups.  Two
+    // 16-feature tiles per wave (16-block slices only) when one tile per wave
+    // would need more workgroups than two per CU hold at once.
+    auto burst = [&](int nt, int& n_fb, int& S) {
+      n_fb = (N + 64 * nt - 1) / (64 * nt);
+      S = 0;
+      for (int s = 1; s <= kb; ++s) {
+        if (kb % s) continue;
+        const int kcb = kb / s;
+        if (kcb != 16 && kcb != 8) continue;
+        if (S == 0) S = s;
+        if (n_fb * s >= 256) {
+          S = s;
+          break;
+        }
       }
-    }
-    if (p.S) {
+    };
+    int f1, s1, f2, s2;
+    burst(1, f1, s1);
+    burst(2, f2, s2);
+    const bool two = s2 && kb / s2 == 16 && (!s1 || f1 * s1 > 512);
+    if (two || s1) {
+      p.NT = two ? 2 : 1;
+      p.bn = 64 * p.NT;
+      p.n_fb = two ? f2 : f1;
+      p.S = two ? s2 : s1;
       p.KCB = kb / p.S;
       p.kchunks = 1;
       return p;
     }
   }
   // double-buffered chunks
+  p.NT = p.MT >= 4 ? 2 : 1;
+  p.bn = 4 * p.NT * 16;
+  p.n_fb = (N + p.bn - 1) / p.bn;
   p.KCB = p.MT == 1 ? 8 : p.MT == 2 ? 4 : p.MT == 4 ? 2 : 1;
   int kch = K / (p.KCB * 32);
   p.S = 1;
@@ -454,12 +702,14 @@ void gemm_bf16(const GemmPlan& p, const void* Wpacked, int N, int K, const void*
     a.epi = epi;
     switch (p.MT) {
       case 1:
-        if (p.kchunks == 1 && p.KCB == 16) launch_gemm<1, 1, 16, 1>(a, p.n_fb, p.S, st);
+        if (p.kchunks == 1 && p.KCB == 16 && p.NT == 2) launch_gemm<1, 2, 16, 1>(a, p.n_fb, p.S, st);
+        else if (p.kchunks == 1 && p.KCB == 16) launch_gemm<1, 1, 16, 1>(a, p.n_fb, p.S, st);
         else if (p.kchunks == 1 && p.KCB == 8) launch_gemm<1, 1, 8, 1>(a, p.n_fb, p.S, st);
         else launch_gemm<1, 1, 8, 2>(a, p.n_fb, p.S, st);
         break;
       case 2:
-        if (p.kchunks == 1 && p.KCB == 16) launch_gemm<2, 1, 16, 1>(a, p.n_fb, p.S, st);
+        if (p.kchunks == 1 && p.KCB == 16 && p.NT == 2) launch_gemm<2, 2, 16, 1>(a, p.n_fb, p.S, st);
+        else if (p.kchunks == 1 && p.KCB == 16) launch_gemm<2, 1, 16, 1>(a, p.n_fb, p.S, st);
         else if (p.kchunks == 1 && p.KCB == 8) launch_gemm<2, 1, 8, 1>(a, p.n_fb, p.S, st);
         else launch_gemm<2, 1, 4, 2>(a, p.n_fb, p.S, st);
         break;

@@ -93,6 +93,7 @@ ssd_status validate_config(const ssd_model_config* c) {
     if (c->d_model % 256 || (c->n_heads * c->head_dim) % 256 || c->d_ff % 256)
       return fail(SSD_E_INVAL, "bf16 models need d_model, n_heads*head_dim and d_ff multiples of 256");
     if (c->head_dim != 128 && c->head_dim != 64) return fail(SSD_E_INVAL, "bf16 models need head_dim 64 or 128");
+    if (c->d_model > 64 * GEMM_RMS_MAX_PARTS) return fail(SSD_E_INVAL, "bf16 models need d_model <= %d", 64 * GEMM_RMS_MAX_PARTS);
     if ((c->img_hi - c->img_lo) % 16) return fail(SSD_E_INVAL, "bf16 models need an image range multiple of 16");
   } else {
     if ((c->img_hi - c->img_lo) % 2 || c->d_model % 2) return fail(SSD_E_INVAL, "fp32 models need even d_model and image range");

@@ -81,6 +81,10 @@ struct LayerW {
   void* w2;    // N = d, K = dff
 };
 
+// Most partial sums of x^2 per token a GEMM's 1/rms prologue accepts (the
+// producing GEMM writes one per 64-feature block: d_model <= 8192).
+constexpr int GEMM_RMS_MAX_PARTS = 128;
+
 // GEMM launch plan for one (M, N, K) problem.
 struct GemmPlan {
   int MT, NT, KCB;  // token tiles, feature tiles per wave, 32-k blocks per chunk
@@ -109,6 +113,15 @@ __host__ __device__ inline void xcd_unmap(int w, int per_group, int X, int& grou
     group = w / per_group;
     member = w % per_group;
   }
+}
+
+// Workgroup barrier that orders LDS only: waits for this wave's LDS accesses,
+// not for its outstanding global loads (a full __syncthreads() fence waits for
+// every load in flight, which would stall a prefetched weight burst).
+__device__ __forceinline__ void lds_barrier() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
 }
 
 // ---- launchers (kernels_*.hip) ----
