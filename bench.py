@@ -12,8 +12,11 @@ heads, MLP 5632, 16384 image codes), 64-token random prompt, 24x24 grid,
 batch 1, greedy rule, r = 2, drafts planted from the backbone's own greedy
 AR image with keep-probability 0.6.  Weights N(0, 0.02) from seed 0.
 
-Prints one JSON line (rank 0).  Extra keys: `roofline` (the weight-streaming
-GEMM kernel, HIP events around every launch in the timed region),
+Prints one JSON line (rank 0).  `value` comes from the timed steps, run with
+plain launches.  The same number of steps then runs again with every GEMM and
+attention launch timed by its own dispatch-timestamp HIP events (per-launch
+timing leaves gaps between kernels, so it stays out of the timed steps).
+Extra keys: `roofline` (the weight-streaming GEMM kernel, from those events),
 `attention` (the same for the attention kernel), `cpu_baseline` (the oracle
 on the host cores on a bounded sample), AR tokens/s on the same kernels.
 """
@@ -29,6 +32,8 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
+GEMM_SRC = os.path.join(ROOT, "paper_2606_20543_amd", "csrc", "kernels_gemm.hip")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gemm_bf16_1b-24x24_traffic.md")
 
 
 def log(*a):
@@ -66,6 +71,44 @@ def gpu_greedy_ar(ssd, model, shape, prefix, n):
     return out, dt
 
 
+def gemm_source_hash():
+    import hashlib
+    with open(GEMM_SRC, "rb") as fh:
+        return hashlib.sha256(fh.read()).hexdigest()
+
+
+def measured_traffic(workload):
+    """HBM bytes per GEMM launch from the committed rocprofv3 FETCH_SIZE/WRITE_SIZE
+    summary; None when the summary is missing, for another workload, or taken
+    on a different GEMM source than the one built now."""
+    try:
+        with open(TRAFFIC_FILE) as fh:
+            kv = dict(l.split(":", 1) for l in fh.read().splitlines() if l.startswith("- ") and ":" in l)
+    except OSError:
+        return None
+    kv = {k[2:].strip(): v.strip() for k, v in kv.items()}
+    if kv.get("workload") != workload or kv.get("kernels_gemm.hip sha256") != gemm_source_hash():
+        return None
+    try:
+        return float(kv["hbm bytes per launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def copy_calibration(mib):
+    """A plain device-to-device copy of known size, for scaling the PMC byte counters."""
+    import torch
+    n = mib << 20
+    a = torch.empty(n, dtype=torch.uint8, device="cuda")
+    b = torch.empty_like(a)
+    a.fill_(1)
+    torch.cuda.synchronize()
+    for _ in range(3):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    log(f"[bench] copied {mib} MiB three times (calibration)")
+
+
 def cpu_baseline(wl, w, prefix, drafts):
     """The oracle (numpy float64) on the host cores, on prefix + the first two rows."""
     from oracle import decode as Dc
@@ -73,7 +116,7 @@ def cpu_baseline(wl, w, prefix, drafts):
     shape = wl.model
     om = M.Model(M.Config(shape.n_layers, shape.d_model, shape.n_heads, shape.n_kv_heads, shape.head_dim,
                           shape.d_ff, shape.vocab, shape.img_lo, shape.img_hi, shape.dtype), w)
-    rows = 2
+    rows = min(12, wl.grid)  # about 10-20 s of host work on the 1B workload
     t0 = time.perf_counter()
     tok, st = Dc.decode_image(om, prefix, rows, wl.grid, drafts[:, :rows, :], rule=wl.rule, seed=3,
                               top_k=wl.top_k, b=wl.rounds)
@@ -97,13 +140,19 @@ def main():
     ap.add_argument("--workload", default="1b-24x24")
     ap.add_argument("--accept-p", type=float, default=None)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--no-ar", action="store_true")
+    ap.add_argument("--ar", action="store_true", help="also time greedy AR decoding (one pass per token)")
     ap.add_argument("--no-events", action="store_true", help="time without the per-launch event hook")
+    ap.add_argument("--copy-calibration-mib", type=int, default=0,
+                    help="only run a plain device copy of this size (PMC byte-counter calibration) and exit")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this build runs on exactly one GPU (asked for {args.gpus}); the verify path "
               "shards by independent images, see DESIGN.md", file=sys.stderr)
         sys.exit(2)
+
+    if args.copy_calibration_mib:
+        copy_calibration(args.copy_calibration_mib)
+        return
 
     import torch
     import paper_2606_20543_amd as ssd
@@ -120,30 +169,35 @@ def main():
     model = ssd.ssd_init_model(cfg, w)
     prefix = synth.prompt(shape, B, P)
 
-    ar_rate = None
-    if not args.no_ar:
-        log("[bench] greedy AR on the GPU (plants the drafts)")
-        ar, ar_dt = gpu_greedy_ar(ssd, model, shape, prefix, H * W)
-        ar_rate = B * H * W / ar_dt
-        target = ar.reshape(B, H, W)
-    else:
-        target = synth.random_codes(shape, (B, H, W))
-    drafts = synth.plant(target, p_keep, shape.v_img)
-
     dev = torch.device("cuda:0")
     d_prefix = torch.from_numpy(prefix.astype(np.int32)).to(dev)
-    d_drafts = torch.from_numpy((drafts + shape.img_lo).astype(np.int32)).to(dev)
     d_out = torch.zeros((B, H, W), dtype=torch.int32, device=dev)
     sc = ssd.ssd_schedule()
     sc.grid_h, sc.grid_w, sc.k_h, sc.h_rounds, sc.k_v, sc.b_rounds, sc.i_rounds = H, W, 5, 1, 1, wl.rounds, 0
     sc.rule, sc.top_k, sc.temperature, sc.seed = wl.rule, wl.top_k, wl.temperature, synth.SEED_SAMPLING
 
+    # Target image: one decode with random drafts.  Under the greedy rule the
+    # committed image is the backbone's greedy image whatever the drafts are;
+    # under a sampling rule it is the sample this seed commits.  The timed
+    # drafts keep each target token with probability p_keep (else another code).
+    log("[bench] target decode (random drafts)")
+    d_rand = torch.from_numpy((synth.random_codes(shape, (B, H, W)) + shape.img_lo).astype(np.int32)).to(dev)
+    ssd.ssd_decode_image(model, sc, B, P, d_prefix, d_rand, d_out)
+    target = d_out.cpu().numpy().astype(np.int64) - shape.img_lo
+    drafts = synth.plant(target, p_keep, shape.v_img)
+    d_drafts = torch.from_numpy((drafts + shape.img_lo).astype(np.int32)).to(dev)
+
+    ar_rate = None
+    if args.ar:
+        log("[bench] greedy AR on the GPU (one commit pass per token)")
+        ar, ar_dt = gpu_greedy_ar(ssd, model, shape, prefix, H * W)
+        ar_rate = B * H * W / ar_dt
+
     for i in range(args.warmup):
         ssd.ssd_decode_image(model, sc, B, P, d_prefix, d_drafts, d_out)
         log(f"[bench] warmup {i + 1}/{args.warmup} done")
-    torch.cuda.synchronize()
-    ssd.ssd_profile(model, 0 if args.no_events else 1)
-    ssd.ssd_profile_read(model, reset=True)
+    # timed region: plain launches (per-launch timing adds gaps between kernels)
+    ssd.ssd_profile(model, 0)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     stats = None
@@ -151,19 +205,35 @@ def main():
         stats = ssd.ssd_decode_image(model, sc, B, P, d_prefix, d_drafts, d_out)
     torch.cuda.synchronize()
     dt = time.perf_counter() - t0
-    prof = ssd.ssd_profile_read(model, reset=True)
-    ssd.ssd_profile(model, 0)
     log(f"[bench] timed {args.steps} steps in {dt:.3f} s")
+    # profiled region: the same steps again, every GEMM / attention launch
+    # timed by its own dispatch-timestamp events (on the library's stream)
+    prof = None
+    if not args.no_events:
+        ssd.ssd_profile(model, 1)
+        ssd.ssd_profile_read(model, reset=True)
+        torch.cuda.synchronize()
+        tp = time.perf_counter()
+        for i in range(args.steps):
+            ssd.ssd_decode_image(model, sc, B, P, d_prefix, d_drafts, d_out)
+        torch.cuda.synchronize()
+        tp = time.perf_counter() - tp
+        prof = ssd.ssd_profile_read(model, reset=True)
+        ssd.ssd_profile(model, 0)
+        log(f"[bench] profiled {args.steps} steps in {tp:.3f} s")
 
     ms_step = dt * 1000.0 / args.steps
     value = B * H * W / (dt / args.steps)
-    gemm = [prof[c] for c in ("qkv", "o_proj", "gate_up", "down", "lm_head")]
+    classes = ("qkv", "o_proj", "gate_up", "down", "lm_head", "attention")
+    if prof is None:
+        prof = {c: (0.0, 0, 0.0) for c in classes}
+    gemm = [prof[c] for c in classes[:5]]
     g_ms = sum(x[0] for x in gemm)
     g_n = sum(x[1] for x in gemm)
     g_bytes = sum(x[2] for x in gemm)
-    g_gbs = g_bytes / (g_ms / 1000.0) / 1e9 if g_ms > 0 else 0.0
+    g_gbs = g_bytes / (g_ms / 1000.0) / 1e9 if g_ms > 0 else None
     a_ms, a_n, a_bytes = prof["attention"]
-    a_gbs = a_bytes / (a_ms / 1000.0) / 1e9 if a_ms > 0 else 0.0
+    a_gbs = a_bytes / (a_ms / 1000.0) / 1e9 if a_ms > 0 else None
     per_class = {c: {"ms_per_launch": prof[c][0] / max(prof[c][1], 1), "launches": prof[c][1],
                      "GB_per_s": prof[c][2] / (prof[c][0] / 1000.0) / 1e9 if prof[c][0] > 0 else None}
                  for c in prof}
@@ -186,11 +256,15 @@ def main():
                    "rounds": wl.rounds, "k_h": 5, "k_v": 1, "top_k": wl.top_k, "planted_keep_p": p_keep,
                    "passes_per_image": stats.passes, "parallelism": "single GPU"},
         "roofline": {"bound": "hbm", "kernel": "gemm_bf16_kernel (QKV/O/gate-up/down/LM-head weight streaming)",
-                     "achieved": g_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": g_gbs / HBM_PEAK_GBS,
-                     "traffic": None, "launches": g_n, "ms_per_launch": g_ms / max(g_n, 1),
-                     "bytes_per_launch": g_bytes / max(g_n, 1)},
+                     "achieved": g_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": g_gbs / HBM_PEAK_GBS if g_gbs else None,
+                     "traffic": measured_traffic(wl.name), "launches": g_n, "ms_per_launch": g_ms / max(g_n, 1),
+                     "bytes_per_launch": g_bytes / max(g_n, 1),
+                     "timing": "dispatch-timestamp events (hipExtLaunchKernelGGL) on every launch of the profiled "
+                               "region, which repeats the timed steps right after them"},
         "attention": {"bound": "hbm", "achieved": a_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                      "frac": a_gbs / HBM_PEAK_GBS, "launches": a_n, "ms_per_launch": a_ms / max(a_n, 1)},
+                      "frac": a_gbs / HBM_PEAK_GBS if a_gbs else None, "launches": a_n,
+                      "ms_per_launch": a_ms / max(a_n, 1)},
         "kernel_classes": per_class,
         "acceptance": acc,
         "verify_ms_per_pass": ms_step / stats.passes,
