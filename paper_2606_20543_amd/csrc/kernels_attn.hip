@@ -359,7 +359,7 @@ size_t attn_partials_floats(const Dims& dm, const AttnPlan& p, int B) {
 
 template <int D, int QPW>
 static void launch_attn(const AttnKArgs& a, hipStream_t st) {
-  hipLaunchKernelGGL((attn_bf16_kernel<D, QPW>), dim3(xcd_grid(a.groups, a.nchunk, a.xcd)), dim3(256), 0, st, a);
+  launch_timed(attn_bf16_kernel<D, QPW>, dim3(xcd_grid(a.groups, a.nchunk, a.xcd)), dim3(256), st, a);
 }
 
 void attention_bf16(const Dims& dm, const AttnPlan& p, int B, int K, const int* f, const void* q, size_t q_plane,

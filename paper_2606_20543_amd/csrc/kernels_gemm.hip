@@ -676,7 +676,7 @@ size_t gemm_partials_floats(const GemmPlan& p, int M) {
 
 template <int MT, int NT, int KCB, int NBUF>
 static void launch_gemm(const GemmKArgs& a, int n_fb, int S, hipStream_t st) {
-  hipLaunchKernelGGL((gemm_bf16_kernel<MT, NT, KCB, NBUF>), dim3(xcd_grid(n_fb, S, a.xcd)), dim3(256), 0, st, a);
+  launch_timed(gemm_bf16_kernel<MT, NT, KCB, NBUF>, dim3(xcd_grid(n_fb, S, a.xcd)), dim3(256), st, a);
 }
 
 void gemm_bf16(const GemmPlan& p, const void* Wpacked, int N, int K, const void* in, size_t in_plane, int ld_in,

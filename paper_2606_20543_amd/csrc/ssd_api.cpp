@@ -105,9 +105,14 @@ ssd_status validate_config(const ssd_model_config* c) {
 
 struct ssd_session;
 
+namespace ssd {
+thread_local LaunchTimer* g_launch_timer = nullptr;
+}
+
 namespace {
-// event timing of kernel classes (measurement hook)
-struct Prof {
+// Per-launch timing of kernel classes (measurement hook): the GEMM and
+// attention launches of a class run with dispatch-timestamp events.
+struct Prof : LaunchTimer {
   bool on = false;
   std::vector<hipEvent_t> pool;
   size_t used = 0;
@@ -119,6 +124,8 @@ struct Prof {
   std::vector<Mark> marks;
   double ms[6] = {0, 0, 0, 0, 0, 0}, bytes[6] = {0, 0, 0, 0, 0, 0};
   int64_t n[6] = {0, 0, 0, 0, 0, 0};
+  int cur_cls = 0;
+  double cur_bytes = 0;
   hipEvent_t get() {
     if (used == pool.size()) {
       hipEvent_t e;
@@ -127,18 +134,30 @@ struct Prof {
     }
     return pool[used++];
   }
-  // record around a launch sequence
+  void next(hipEvent_t& a, hipEvent_t& b) override {
+    a = get();
+    b = get();
+    marks.push_back(Mark{cur_cls, a, b, cur_bytes});
+    cur_bytes = 0;  // a call's algorithmic bytes go with its first launch
+  }
+  // time the launches of one call of class cls (b algorithmic bytes)
   template <typename F>
   void run(int cls, double b, hipStream_t st, F&& f) {
+    (void)st;
     if (!on) {
       f();
       return;
     }
-    hipEvent_t e0 = get(), e1 = get();
-    HIPCHK(hipEventRecord(e0, st));
-    f();
-    HIPCHK(hipEventRecord(e1, st));
-    marks.push_back(Mark{cls, e0, e1, b});
+    cur_cls = cls;
+    cur_bytes = b;
+    g_launch_timer = this;
+    try {
+      f();
+    } catch (...) {
+      g_launch_timer = nullptr;
+      throw;
+    }
+    g_launch_timer = nullptr;
   }
   // after the stream has drained
   void flush() {
@@ -152,7 +171,7 @@ struct Prof {
     marks.clear();
     used = 0;
   }
-  ~Prof() {
+  ~Prof() override {
     for (hipEvent_t e : pool) (void)hipEventDestroy(e);
   }
 };
@@ -205,6 +224,7 @@ struct ssd_session {
   size_t kv_layer_elems;
   float2* rope;
   float* gpart;
+  int ssq_parts_cap;
   size_t gpart_cap;
   unsigned* gcnt;
   size_t gcnt_cap;
@@ -268,6 +288,19 @@ void run_forward(ssd_session* s, int K, int lm_mode) {
     GemmPlan p13 = gemm_plan_bf16(M, 2 * dm.dff, d, X);
     GemmPlan p2 = gemm_plan_bf16(M, d, dm.dff, X);
     AttnPlan pa = attn_plan(dm, B, K, max_ctx_now, X);
+    // workspaces were sized at session creation for every plan the session can
+    // meet; a plan outside them is a bug, refused before any launch
+    auto need = [](bool ok, const char* what) {
+      if (!ok) throw HipError{hipErrorInvalidValue, what};
+    };
+    need(M <= s->Mmax, "token count exceeds the session's activation buffers");
+    for (const GemmPlan* gp : {&pq, &po, &p13, &p2}) {
+      need(gemm_partials_floats(*gp, M) <= s->gpart_cap && (size_t)gp->n_fb <= s->gcnt_cap,
+           "GEMM plan exceeds the split-K workspace");
+    }
+    need(po.n_fb <= s->ssq_parts_cap && p2.n_fb <= s->ssq_parts_cap, "rms partial sums exceed their buffer");
+    need(attn_partials_floats(dm, pa, B) <= s->apart_cap && (size_t)B * dm.Hkv * pa.nqg <= s->acnt_cap,
+         "attention plan exceeds its workspace");
     double attn_bytes = 2.0 * M * dm.Hq * D * A;  // q read + o written
     for (int b = 0; b < B; ++b) attn_bytes += 2.0 * (s->f[b] + K) * dm.Hkv * D * es;
     const double qkv_bytes = (double)Nqkv * d * es + (double)M * d * A + (double)M * dm.Hq * D * A +
@@ -329,6 +362,8 @@ void run_forward(ssd_session* s, int K, int lm_mode) {
     e.ld = dm.Vimg;
     if (lm_mode == 0) {
       GemmPlan pl = gemm_plan_bf16(M, dm.Vimg, d, X);
+      if (gemm_partials_floats(pl, M) > s->gpart_cap || (size_t)pl.n_fb > s->gcnt_cap)
+        throw HipError{hipErrorInvalidValue, "GEMM plan exceeds the split-K workspace"};
       m->prof.run(4, (double)dm.Vimg * d * es + (double)M * d * A + (double)M * dm.Vimg * 4, st, [&] {
         gemm_bf16(pl, m->wlm, dm.Vimg, d, s->xn, s->xn_plane, d, M, e, s->gpart, s->gcnt, st);
       });
@@ -336,6 +371,8 @@ void run_forward(ssd_session* s, int K, int lm_mode) {
       e.ssq_off = K - 1;
       e.ssq_step = K;
       GemmPlan pl = gemm_plan_bf16(B, dm.Vimg, d, X);
+      if (gemm_partials_floats(pl, B) > s->gpart_cap || (size_t)pl.n_fb > s->gcnt_cap)
+        throw HipError{hipErrorInvalidValue, "GEMM plan exceeds the split-K workspace"};
       m->prof.run(4, (double)dm.Vimg * d * es + (double)B * d * A + (double)B * dm.Vimg * 4, st, [&] {
         gemm_bf16(pl, m->wlm, dm.Vimg, d, (const uint16_t*)s->xn + (size_t)(K - 1) * d, s->xn_plane, K * d, B, e,
                   s->gpart, s->gcnt, st);
@@ -450,8 +487,8 @@ void size_workspaces(const Dims& dm, int B, int P, int Kmax, int Lmax, size_t& g
   for (int K = 1; K <= Kmax; ++K) Ks.push_back(K);
   Ks.push_back(P);
   for (int K : Ks) {
-    for (int ctx = 1; ctx <= Lmax + 63; ctx += 64) {
-      AttnPlan pc = attn_plan(dm, B, K, std::min(ctx, Lmax), 0);
+    for (int ctx = 1; ctx <= Lmax; ++ctx) {
+      AttnPlan pc = attn_plan(dm, B, K, ctx, 0);
       apart = std::max(apart, attn_partials_floats(dm, pc, B));
       acnt = std::max(acnt, (size_t)B * dm.Hkv * pc.nqg);
     }
@@ -494,6 +531,7 @@ ssd_status create_session(ssd_model* m, int B, int P, int Lmax_req, int Kmax, ss
     s->xn = s->mem.get<char>(M * dm.d * 4);
     s->ssq_rows_ld = (int)M;
     s->ssq = s->mem.get<float>((size_t)ssq_parts * M);
+    s->ssq_parts_cap = ssq_parts;
     s->q = s->mem.get<char>(M * dm.Hq * dm.D * 4);
     s->o = s->mem.get<char>(M * dm.Hq * dm.D * 4);
     s->h = s->mem.get<char>(M * dm.dff * 4);

@@ -23,6 +23,7 @@
 //   w1/w3:    packed row 2j <- gate row j, 2j+1 <- up row j (SwiGLU pair)
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -122,6 +123,28 @@ __device__ __forceinline__ void lds_barrier() {
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
   __builtin_amdgcn_s_barrier();
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
+// Measurement hook (host side).  While set, the GEMM and attention launchers
+// start each kernel through hipExtLaunchKernelGGL with a start/stop event pair
+// from the timer: the events take the dispatch's own begin/end timestamps, so
+// no marker packet sits between consecutive kernels.  Per thread; set around
+// one launch sequence.
+struct LaunchTimer {
+  virtual ~LaunchTimer() = default;
+  virtual void next(hipEvent_t& start, hipEvent_t& stop) = 0;
+};
+extern thread_local LaunchTimer* g_launch_timer;
+
+template <typename Kern, typename... Args>
+inline void launch_timed(Kern kernel, dim3 grid, dim3 block, hipStream_t st, Args... args) {
+  if (g_launch_timer) {
+    hipEvent_t a, b;
+    g_launch_timer->next(a, b);
+    hipExtLaunchKernelGGL(kernel, grid, block, 0, st, a, b, 0, args...);
+  } else {
+    hipLaunchKernelGGL(kernel, grid, block, 0, st, args...);
+  }
 }
 
 // ---- launchers (kernels_*.hip) ----

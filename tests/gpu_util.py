@@ -131,3 +131,59 @@ def flip_within_tolerance(rule, L_oracle, ref_oracle, t, u0, u1, new_gpu, acc_gp
     lo = c[new_gpu - 1] if new_gpu > 0 else 0.0
     hi = c[new_gpu]
     return lo - eps_a <= target <= hi + eps_a
+
+
+def check_round(shape, sess, os_, blk, nf, rule, rnd, top_k, ref, stats):
+    """One verify round on the GPU and in the oracle from the same state, under
+    the parity protocol above; the oracle session os_ advances with it.  Returns
+    (the GPU's new block codes, the GPU outputs)."""
+    tol = TOL[shape.dtype]
+    B, K = blk.shape
+    carry = np.zeros((B, shape.v_img), np.float32)
+    ssd.ssd_get_carry(sess, carry)
+    f_before = os_.f.copy()
+    cerr = float(np.abs(carry - os_.carry).max())
+    stats["max_logit_err"] = max(stats.get("max_logit_err", 0.0), cerr)
+    assert cerr < tol, f"carry error {cerr}"
+    out = gpu_verify(sess, shape, blk + shape.img_lo, vparams(rule, top_k=top_k, rnd=rnd, n_fixed=nf),
+                     ref=None if ref is None else np.ascontiguousarray(ref, np.float32))
+    refs = None
+    if ref is not None:
+        refs = [[ref[b, k].astype(np.float64) for k in range(K)] for b in range(B)]
+    gnew, gacc, gcnt, _ = oracle_rule_on(out["logits"], carry, blk, nf, rule, rnd, 3, f_before, 1.0, top_k, refs)
+    onew, oacc, _, ologits = Dc.verify_round(os_, blk, nf, rule, rnd, 3, 1.0, top_k,
+                                             None if refs is None else [list(r) for r in refs])
+    err = float(np.abs(out["logits"] - ologits).max())
+    stats["max_logit_err"] = max(stats["max_logit_err"], err)
+    assert err < tol, f"logit error {err}"
+    assert np.array_equal(out["tokens"] - shape.img_lo, gnew)
+    assert np.array_equal(out["accept"][:, nf:], gacc[:, nf:])
+    assert np.array_equal(out["count"], gcnt)
+    assert list(out["frontier"]) == list(f_before)
+    diff = np.argwhere((onew != gnew) | (oacc != gacc))
+    stats["flips"] = stats.get("flips", 0) + len(diff)
+    stats["positions"] = stats.get("positions", 0) + B * (K - nf)
+    for b, k in diff:
+        Lo = os_.carry[b] if k == 0 else ologits[b, k - 1]
+        Lg = carry[b] if k == 0 else out["logits"][b, k - 1]
+        delta = float(np.abs(Lg - Lo).max())
+        pos = int(f_before[b]) + int(k)
+        ok = flip_within_tolerance(rule, Lo, None if refs is None else refs[b][k], int(blk[b, k]),
+                                   R.uniform(3, b, pos, rnd, 0), R.uniform(3, b, pos, rnd, 1),
+                                   int(gnew[b, k]), bool(gacc[b, k]), delta, 1.0, top_k)
+        assert ok, f"decision at (b={b}, k={k}) differs beyond what logit error {delta:.2e} allows"
+    return gnew, out
+
+
+def check_commit(shape, sess, os_, blk, stats, want_h=False):
+    """Commit pass on both sides: logits within tolerance, same frontier."""
+    tol = TOL[shape.dtype]
+    out = gpu_verify(sess, shape, blk + shape.img_lo, vparams(commit=1), want_h=want_h)
+    ol, oh = Dc.commit(os_, blk)
+    err = float(np.abs(out["logits"] - ol).max())
+    stats["max_logit_err"] = max(stats.get("max_logit_err", 0.0), err)
+    assert err < tol, f"commit logit error {err}"
+    if want_h:
+        assert np.abs(out["h_pre"] - oh).max() < 0.05 * np.abs(oh).max()
+    assert list(out["frontier"]) == list(os_.f)
+    return out

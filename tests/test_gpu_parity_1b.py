@@ -28,39 +28,7 @@ def pair():
 
 
 def _check_round(sess, os_, blk, nf, rule, rnd, top_k, ref, stats, K):
-    B = blk.shape[0]
-    carry = np.zeros((B, SHAPE.v_img), np.float32)
-    ssd.ssd_get_carry(sess, carry)
-    f_before = os_.f.copy()
-    assert np.abs(carry - os_.carry).max() < TOL
-    out = G.gpu_verify(sess, SHAPE, blk + SHAPE.img_lo, G.vparams(rule, top_k=top_k, rnd=rnd, n_fixed=nf),
-                       ref=None if ref is None else np.ascontiguousarray(ref, np.float32))
-    refs = None
-    if ref is not None:
-        refs = [[ref[b, k].astype(np.float64) for k in range(K)] for b in range(B)]
-    gnew, gacc, gcnt, _ = G.oracle_rule_on(out["logits"], carry, blk, nf, rule, rnd, 3, f_before, 1.0, top_k, refs)
-    onew, oacc, _, ologits = Dc.verify_round(os_, blk, nf, rule, rnd, 3, 1.0, top_k,
-                                             None if refs is None else [list(r) for r in refs])
-    err = np.abs(out["logits"] - ologits).max()
-    stats["max_logit_err"] = max(stats.get("max_logit_err", 0.0), float(err))
-    assert err < TOL, f"logit error {err}"
-    assert np.array_equal(out["tokens"] - SHAPE.img_lo, gnew)
-    assert np.array_equal(out["accept"][:, nf:], gacc[:, nf:])
-    assert np.array_equal(out["count"], gcnt)
-    assert list(out["frontier"]) == list(f_before)
-    diff = np.argwhere((onew != gnew) | (oacc != gacc))
-    stats["flips"] = stats.get("flips", 0) + len(diff)
-    stats["positions"] = stats.get("positions", 0) + B * (K - nf)
-    for b, k in diff:
-        Lo = os_.carry[b] if k == 0 else ologits[b, k - 1]
-        Lg = carry[b] if k == 0 else out["logits"][b, k - 1]
-        delta = float(np.abs(Lg - Lo).max())
-        pos = int(f_before[b]) + int(k)
-        ok = G.flip_within_tolerance(rule, Lo, None if refs is None else refs[b][k], int(blk[b, k]),
-                                     R.uniform(3, b, pos, rnd, 0), R.uniform(3, b, pos, rnd, 1),
-                                     int(gnew[b, k]), bool(gacc[b, k]), delta, 1.0, top_k)
-        assert ok, f"decision at (b={b}, k={k}) differs beyond what logit error {delta:.2e} allows"
-    return gnew, out
+    return G.check_round(SHAPE, sess, os_, blk, nf, rule, rnd, top_k, ref, stats)
 
 
 def test_1b_greedy_rows(pair):
@@ -85,12 +53,7 @@ def test_1b_greedy_rows(pair):
                 gnew, _ = _check_round(sess, os_, blk, nf, R.RULE_GREEDY, rnd, 0, None, stats, K)
                 work[:, start:start + K] = gnew
                 rnd += 1
-            blk = work[:, start:start + K]
-            out = G.gpu_verify(sess, SHAPE, blk + SHAPE.img_lo, G.vparams(commit=1), want_h=True)
-            ol, oh = Dc.commit(os_, blk)
-            assert np.abs(out["logits"] - ol).max() < TOL
-            assert np.abs(out["h_pre"] - oh).max() < 0.05 * np.abs(oh).max()
-            assert list(out["frontier"]) == list(os_.f)
+            G.check_commit(SHAPE, sess, os_, work[:, start:start + K], stats, want_h=True)
         print("1b greedy parity stats", stats, flush=True)
         assert stats["flips"] <= 0.02 * stats["positions"] + 1
     finally:
