@@ -7,23 +7,28 @@
 // next raster positions.
 //
 // bf16 path: a workgroup of four waves owns one key chunk of one query group
-// (up to 32 query rows of one sequence x KV head; the K*g rows of a KV head,
+// (16 or 32 query rows of one sequence x KV head; the K*g rows of a KV head,
 // g = query heads per KV head, are tiled by 16).  Wave w streams the chunk's
-// 32-key blocks w, w+4, ... : S^T = K Q^T and O^T = V^T P^T run on
+// 32-key blocks w, w+4, ..., with the next block's K and V tiles in flight
+// while the current one is multiplied.  S^T = K Q^T and O^T = V^T P^T run on
 // v_mfma_f32_16x16x32_bf16 with queries as the MFMA columns, so the softmax
 // statistics of a query live in one lane column and need two cross-lane
 // shuffles; the P^T operand is built in registers straight from the S^T
 // accumulators (its key order is matched by reading the transposed V cache),
 // so P never touches LDS.  The four waves' (max, sum, O) triples are merged
-// through LDS.  Chunks of one query group run on workgroups of one XCD; each
-// publishes its merged triple and the last to arrive combines them in chunk
-// order, all threads loading in parallel.
+// through LDS.  A context is split into several chunks only when the chunks'
+// shorter streams outweigh the cost of merging them (few query groups, long
+// contexts) or to fill the chip (many query groups); chunks of one query group
+// run on workgroups of one XCD, and the last to arrive combines them in chunk
+// order.
 #include "ssd_internal.h"
 
 namespace ssd {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float floatx4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
 __device__ __forceinline__ uint16_t f2bf_a(float f) {
   uint32_t u = __float_as_uint(f);
@@ -31,22 +36,29 @@ __device__ __forceinline__ uint16_t f2bf_a(float f) {
   return (uint16_t)(u >> 16);
 }
 
-constexpr int ATTN_WAVES = 4;
-constexpr int ATTN_KEYS = 32;                           // keys per wave step
-constexpr int ATTN_MIN_CHUNK = ATTN_WAVES * ATTN_KEYS;  // keys per workgroup step
-constexpr int ATTN_MAX_CHUNKS = 64;
+constexpr int AT_KEYS = 32;        // keys per wave step
+constexpr int AT_STEP = 128;       // chunk granularity in keys (one workgroup step)
+constexpr int AT_MAX_CHUNKS = 64;
+// four waves per workgroup: one wave per SIMD, so a wave holds two K/V blocks
+// (the one in use and the next) beside its queries and accumulators
+template <int QPW>
+struct AtShape {
+  static constexpr int WAVES = 4;
+  static constexpr int THREADS = WAVES * 64;
+  static constexpr int STEP = WAVES * AT_KEYS;
+};
 
 struct AttnKArgs {
-  const uint16_t* q;   // [B][Hq][K][D], hi plane then lo plane (q_plane elements apart)
-  const uint16_t* kc;  // [B][Hkv][Lmax][D]
-  const uint16_t* vc;  // [B][Hkv][D][Lmax]
+  const uint16_t* q;   // [B][Hkv][qrows_pad x D tiles], hi plane then lo plane (q_plane elements apart)
+  const uint16_t* kc;  // [B][Hkv][Lmax x D tiles]
+  const uint16_t* vc;  // [B][Hkv][D x Lmax tiles, keys permuted]
   uint16_t* o;         // [B*K][Hq*D], hi plane then lo plane (o_plane elements apart)
   size_t q_plane, o_plane;
   float* opart;        // [groups][nchunk][QPW*16][D]   chunk partial O (relative to the chunk max)
   float2* spart;       // [groups][nchunk][QPW*16]      chunk (max, sum), log2 domain
   unsigned* counters;  // [groups]
   const int* f;
-  int K, Hq, Hkv, g, Lmax, rows, chunk, nchunk, nqg, groups, xcd;
+  int K, Hq, Hkv, g, Lmax, rows, qrows_pad, chunk, nchunk, nqg, groups, heads, xcd;
   float scale_log2;
 };
 
@@ -67,24 +79,131 @@ __device__ __forceinline__ void store_split4(uint16_t* p, size_t plane, floatx4 
   *(uint2*)(p + plane) = x;
 }
 
+// K and V operands of one 32-key block: K tiles (keys key0 + kt*16 + [0,16),
+// dims kd*32 + [0,32)) are the A operands of S^T, V^T tiles (dims dt*16 + [0,16),
+// keys key0 + [0,32)) those of O^T.  In the tiled caches each is 1 KiB
+// contiguous in lane order: one coalesced 16-byte load per lane.  A block past
+// the cache (a prefetch beyond the chunk) reloads the cache's last block.
+template <int D>
+struct KVTile {
+  u32x4 k[2][D / 32];
+  u32x4 v[D / 16];
+};
+
+template <int D>
+__device__ __forceinline__ void load_kv(KVTile<D>& t, const uint16_t* kbase, const uint16_t* vbase, int key0,
+                                        int Lmax, int lane) {
+  const int kb = key0 < Lmax - 32 ? key0 : Lmax - 32;
+#pragma unroll
+  for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+    for (int kd = 0; kd < D / 32; ++kd)
+      t.k[kt][kd] = *(const u32x4*)(kbase + ((size_t)((kb >> 4) + kt) * (D / 32) + kd) * 512 + lane * 8);
+#pragma unroll
+  for (int dt = 0; dt < D / 16; ++dt)
+    t.v[dt] = *(const u32x4*)(vbase + ((size_t)dt * (Lmax >> 5) + (kb >> 5)) * 512 + lane * 8);
+}
+
+// one 32-key block through the online softmax of the wave's query tiles
 template <int D, int QPW>
-__global__ __launch_bounds__(256) void attn_bf16_kernel(AttnKArgs a) {
+__device__ __forceinline__ void attend_block(const KVTile<D>& t, int key0, const bf16x8 (&qh)[QPW][D / 32],
+                                             const bf16x8 (&ql)[QPW][D / 32], const int (&qpos)[QPW],
+                                             float scale_log2, int grp, float (&m)[QPW], float (&l)[QPW],
+                                             floatx4 (&O)[QPW][D / 16]) {
+  constexpr int KD = D / 32, DT = D / 16;
+  floatx4 s[2][QPW];
+#pragma unroll
+  for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+    for (int qt = 0; qt < QPW; ++qt) {
+      floatx4 acc = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int kd = 0; kd < KD; ++kd) {
+        const bf16x8 kf = __builtin_bit_cast(bf16x8, t.k[kt][kd]);
+        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qh[qt][kd], acc, 0, 0, 0);
+        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, ql[qt][kd], acc, 0, 0, 0);
+      }
+      s[kt][qt] = acc;
+    }
+#pragma unroll
+  for (int qt = 0; qt < QPW; ++qt) {
+    float sv[8];
+    float mx = -INFINITY;
+#pragma unroll
+    for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int key = key0 + kt * 16 + 4 * grp + e;
+        float v = s[kt][qt][e] * scale_log2;
+        v = (key <= qpos[qt]) ? v : -INFINITY;
+        sv[kt * 4 + e] = v;
+        mx = fmaxf(mx, v);
+      }
+    mx = fmaxf(mx, __shfl_xor(mx, 16));
+    mx = fmaxf(mx, __shfl_xor(mx, 32));
+    const float mnew = fmaxf(m[qt], mx);
+    const bool none = (mnew == -INFINITY);
+    const float alpha = none ? 1.f : exp2f(m[qt] - mnew);
+    float ps = 0.f;
+    uint16_t pb[8], pl[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const float p = none ? 0.f : exp2f(sv[i] - mnew);
+      ps += p;
+      pb[i] = f2bf_a(p);
+      pl[i] = f2bf_a(p - __uint_as_float((uint32_t)pb[i] << 16));
+    }
+    l[qt] = l[qt] * alpha + ps;
+    m[qt] = mnew;
+    const u32x4 pv = {(uint32_t)pb[0] | ((uint32_t)pb[1] << 16), (uint32_t)pb[2] | ((uint32_t)pb[3] << 16),
+                      (uint32_t)pb[4] | ((uint32_t)pb[5] << 16), (uint32_t)pb[6] | ((uint32_t)pb[7] << 16)};
+    const u32x4 pw = {(uint32_t)pl[0] | ((uint32_t)pl[1] << 16), (uint32_t)pl[2] | ((uint32_t)pl[3] << 16),
+                      (uint32_t)pl[4] | ((uint32_t)pl[5] << 16), (uint32_t)pl[6] | ((uint32_t)pl[7] << 16)};
+    const bf16x8 pf = __builtin_bit_cast(bf16x8, pv);
+    const bf16x8 pg = __builtin_bit_cast(bf16x8, pw);
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) {
+      O[qt][dt] *= alpha;
+      const bf16x8 vf = __builtin_bit_cast(bf16x8, t.v[dt]);
+      O[qt][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf, O[qt][dt], 0, 0, 0);
+      O[qt][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pg, O[qt][dt], 0, 0, 0);
+    }
+  }
+}
+
+// PF = 1: the next block's K/V tiles are loaded while the current one is used
+template <int D, int QPW, int PF>
+// one wave per SIMD: the register file holds two K/V blocks, the queries and
+// the accumulators without the compiler sinking the prefetch loads
+__global__ __launch_bounds__(AtShape<QPW>::THREADS) __attribute__((amdgpu_waves_per_eu(1, 1)))
+void attn_bf16_kernel(AttnKArgs a) {
+  constexpr int NW = AtShape<QPW>::WAVES, NTH = AtShape<QPW>::THREADS, STEP = AtShape<QPW>::STEP;
   constexpr int KD = D / 32;   // 32-wide k steps over the head dimension
   constexpr int DT = D / 16;   // 16-row d tiles of O^T
   constexpr int ROWS = QPW * 16;
   constexpr int RS = D + 4;    // LDS row stride (floats): rows of one wave fall on different banks
-  constexpr int NV = ROWS * D / 4 / 256;  // float4 outputs per thread
-  static_assert(NV >= 1 && ROWS * D / 4 == NV * 256, "thread map");
-  static_assert(3 * ATTN_MAX_CHUNKS * ROWS <= ATTN_WAVES * ROWS * RS, "chunk statistics fit the O stage");
-  __shared__ __align__(16) float sm_o[ATTN_WAVES * ROWS * RS];
-  __shared__ float sm_m[ATTN_WAVES * ROWS], sm_l[ATTN_WAVES * ROWS];
+  constexpr int NOUT = ROWS * D / 4;                          // float4 outputs of the workgroup
+  constexpr int NV = (NOUT + NTH - 1) / NTH;    // per thread
+  static_assert(2 * AT_MAX_CHUNKS * ROWS <= NW * ROWS * RS, "chunk statistics fit the O stage");
+  __shared__ __align__(16) float sm_o[NW * ROWS * RS];
+  __shared__ float sm_m[NW * ROWS], sm_l[NW * ROWS];
   __shared__ int is_last;
 
-  // reduction group = (sequence x KV head, query group); members = key chunks, all on one XCD
-  int grp_id, c;
-  xcd_unmap(blockIdx.x, a.nchunk, a.xcd, grp_id, c);
-  if (grp_id >= a.groups) return;
-  const int qg = grp_id % a.nqg, z = grp_id / a.nqg;
+  // single chunk: the query groups of one (sequence, KV head) share an XCD
+  // (they read the same K/V); several chunks: the chunks of one query group
+  // share an XCD (their partials meet in its L2)
+  int grp_id, c, z, qg;
+  if (a.nchunk == 1) {
+    xcd_unmap(blockIdx.x, a.nqg, a.xcd, z, qg);
+    if (z >= a.heads) return;
+    grp_id = z * a.nqg + qg;
+    c = 0;
+  } else {
+    xcd_unmap(blockIdx.x, a.nchunk, a.xcd, grp_id, c);
+    if (grp_id >= a.groups) return;
+    qg = grp_id % a.nqg;
+    z = grp_id / a.nqg;
+  }
   const int b = z / a.Hkv, hkv = z - b * a.Hkv;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int col = lane & 15, grp = lane >> 4;
@@ -96,23 +215,32 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnKArgs a) {
   const int kend = min(kbeg + a.chunk, ctx);
   const int rbase = qg * ROWS;
 
+  const uint16_t* kbase = a.kc + ((size_t)b * a.Hkv + hkv) * a.Lmax * D;
+  const uint16_t* vbase = a.vc + ((size_t)b * a.Hkv + hkv) * (size_t)D * a.Lmax;
+  const int first = kbeg + wave * AT_KEYS;
+  const int nit = first < kend ? (kend - first + STEP - 1) / STEP : 0;
+
+  // first K/V block in flight together with the queries.  K/V loads are never
+  // conditional (a branch around loads makes the compiler wait for all of them
+  // at the join): rows past the cache are clamped, and a block past the chunk
+  // is loaded but never used.
+  KVTile<D> ta, tb;
+  load_kv<D>(ta, kbase, vbase, first, a.Lmax, lane);
+
   // query fragments (B operand of S^T = K Q^T): lane holds row col of tile qt, d = 8*grp.. (+32 kd);
   // q is fp32 carried as hi + lo bf16 operands
   bf16x8 qh[QPW][KD], ql[QPW][KD];
   int qpos[QPW];
+  const uint16_t* qbase = a.q + (size_t)z * a.qrows_pad * D;
 #pragma unroll
   for (int qt = 0; qt < QPW; ++qt) {
-    const int r = rbase + qt * 16 + col;
-    const bool ok = r < a.rows;
-    const int j = ok ? r / a.K : 0, k = ok ? r - (r / a.K) * a.K : 0;
-    qpos[qt] = ok ? fb + k : -1;
-    const uint16_t* qp = a.q + (((size_t)b * a.Hq + hkv * a.g + j) * a.K + k) * D + grp * 8;
+    const int r = rbase + qt * 16 + col;  // padded rows (r >= rows) exist and are masked
+    qpos[qt] = r < a.rows ? fb + r % a.K : -1;
+    const uint16_t* qp = qbase + ((size_t)((rbase >> 4) + qt) * KD) * 512 + lane * 8;
 #pragma unroll
     for (int kd = 0; kd < KD; ++kd) {
-      uint4 vh = ok ? *(const uint4*)(qp + kd * 32) : make_uint4(0, 0, 0, 0);
-      uint4 vl = ok ? *(const uint4*)(qp + a.q_plane + kd * 32) : make_uint4(0, 0, 0, 0);
-      qh[qt][kd] = __builtin_bit_cast(bf16x8, vh);
-      ql[qt][kd] = __builtin_bit_cast(bf16x8, vl);
+      qh[qt][kd] = __builtin_bit_cast(bf16x8, *(const u32x4*)(qp + kd * 512));
+      ql[qt][kd] = __builtin_bit_cast(bf16x8, *(const u32x4*)(qp + a.q_plane + kd * 512));
     }
   }
 
@@ -126,93 +254,21 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnKArgs a) {
     for (int dt = 0; dt < DT; ++dt) O[qt][dt] = floatx4{0.f, 0.f, 0.f, 0.f};
   }
 
-  const uint16_t* kbase = a.kc + ((size_t)b * a.Hkv + hkv) * a.Lmax * D;
-  const uint16_t* vbase = a.vc + ((size_t)b * a.Hkv + hkv) * (size_t)D * a.Lmax;
-
-  for (int key0 = kbeg + wave * ATTN_KEYS; key0 < kend; key0 += ATTN_MIN_CHUNK) {
-    // S^T tiles for keys key0 + [0,16) and key0 + [16,32)
-    floatx4 s[2][QPW];
-#pragma unroll
-    for (int kt = 0; kt < 2; ++kt) {
-      int krow = key0 + kt * 16 + col;
-      krow = krow < a.Lmax ? krow : a.Lmax - 1;
-      const uint16_t* kp = kbase + (size_t)krow * D + grp * 8;
-      bf16x8 kf[KD];
-#pragma unroll
-      for (int kd = 0; kd < KD; ++kd) kf[kd] = __builtin_bit_cast(bf16x8, *(const uint4*)(kp + kd * 32));
-#pragma unroll
-      for (int qt = 0; qt < QPW; ++qt) {
-        floatx4 acc = floatx4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int kd = 0; kd < KD; ++kd) {
-          acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[kd], qh[qt][kd], acc, 0, 0, 0);
-          acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[kd], ql[qt][kd], acc, 0, 0, 0);
-        }
-        s[kt][qt] = acc;
-      }
+  if constexpr (PF) {
+    // the next block is loaded before the current one is used and taken over
+    // at the end of every iteration (an unconditional use: the compiler can
+    // neither sink the loads past a loop exit nor drop the overlap)
+    for (int it = 0; it < nit; ++it) {
+      const int key0 = first + it * STEP;
+      load_kv<D>(tb, kbase, vbase, key0 + STEP, a.Lmax, lane);
+      attend_block<D, QPW>(ta, key0, qh, ql, qpos, a.scale_log2, grp, m, l, O);
+      ta = tb;
     }
-    // V^T fragments: lane row d = dt*16 + col, keys key0 + 4*grp + [0,4) and key0 + 16 + 4*grp + [0,4)
-    bf16x8 vf[DT];
-    {
-      int kA = key0 + 4 * grp, kB = key0 + 16 + 4 * grp;
-      kA = kA + 3 < a.Lmax ? kA : a.Lmax - 4;
-      kB = kB + 3 < a.Lmax ? kB : a.Lmax - 4;
-#pragma unroll
-      for (int dt = 0; dt < DT; ++dt) {
-        const uint16_t* vp = vbase + (size_t)(dt * 16 + col) * a.Lmax;
-        uint2 lo = *(const uint2*)(vp + kA);
-        uint2 hi = *(const uint2*)(vp + kB);
-        uint4 v = make_uint4(lo.x, lo.y, hi.x, hi.y);
-        vf[dt] = __builtin_bit_cast(bf16x8, v);
-      }
-    }
-#pragma unroll
-    for (int qt = 0; qt < QPW; ++qt) {
-      float sv[8];
-      float mx = -INFINITY;
-#pragma unroll
-      for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const int key = key0 + kt * 16 + 4 * grp + e;
-          float v = s[kt][qt][e] * a.scale_log2;
-          v = (key <= qpos[qt]) ? v : -INFINITY;
-          sv[kt * 4 + e] = v;
-          mx = fmaxf(mx, v);
-        }
-      mx = fmaxf(mx, __shfl_xor(mx, 16));
-      mx = fmaxf(mx, __shfl_xor(mx, 32));
-      const float mnew = fmaxf(m[qt], mx);
-      const bool none = (mnew == -INFINITY);
-      const float alpha = none ? 1.f : exp2f(m[qt] - mnew);
-      float ps = 0.f;
-      uint16_t pb[8], pl[8];
-#pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        float p = none ? 0.f : exp2f(sv[i] - mnew);
-        ps += p;
-        pb[i] = f2bf_a(p);
-        pl[i] = f2bf_a(p - __uint_as_float((uint32_t)pb[i] << 16));
-      }
-      l[qt] = l[qt] * alpha + ps;
-      m[qt] = mnew;
-      uint4 pv, pw;
-      pv.x = (uint32_t)pb[0] | ((uint32_t)pb[1] << 16);
-      pv.y = (uint32_t)pb[2] | ((uint32_t)pb[3] << 16);
-      pv.z = (uint32_t)pb[4] | ((uint32_t)pb[5] << 16);
-      pv.w = (uint32_t)pb[6] | ((uint32_t)pb[7] << 16);
-      pw.x = (uint32_t)pl[0] | ((uint32_t)pl[1] << 16);
-      pw.y = (uint32_t)pl[2] | ((uint32_t)pl[3] << 16);
-      pw.z = (uint32_t)pl[4] | ((uint32_t)pl[5] << 16);
-      pw.w = (uint32_t)pl[6] | ((uint32_t)pl[7] << 16);
-      bf16x8 pf = __builtin_bit_cast(bf16x8, pv);
-      bf16x8 pg = __builtin_bit_cast(bf16x8, pw);
-#pragma unroll
-      for (int dt = 0; dt < DT; ++dt) {
-        O[qt][dt] *= alpha;
-        O[qt][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf[dt], pf, O[qt][dt], 0, 0, 0);
-        O[qt][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf[dt], pg, O[qt][dt], 0, 0, 0);
-      }
+  } else {
+    for (int it = 0; it < nit; ++it) {
+      const int key0 = first + it * STEP;
+      attend_block<D, QPW>(ta, key0, qh, ql, qpos, a.scale_log2, grp, m, l, O);
+      load_kv<D>(ta, kbase, vbase, key0 + STEP, a.Lmax, lane);
     }
   }
 
@@ -232,20 +288,21 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnKArgs a) {
   }
   __syncthreads();
 
-  // merge the four waves: thread owns NV float4 slots (row r, dims 4*d4..)
+  // merge the waves: thread owns float4 slots idx = tid + NTH * i (row r, dims 4*d4..)
   floatx4 acc[NV];
   float Lr[NV], Mr[NV];
 #pragma unroll
   for (int i = 0; i < NV; ++i) {
-    const int idx = threadIdx.x + 256 * i;
-    const int r = idx / (D / 4), d4 = idx - r * (D / 4);
+    const int idx = threadIdx.x + NTH * i;
+    const int ic = idx < NOUT ? idx : NOUT - 1;
+    const int r = ic / (D / 4), d4 = ic - r * (D / 4);
     float M = -INFINITY;
 #pragma unroll
-    for (int w = 0; w < ATTN_WAVES; ++w) M = fmaxf(M, sm_m[w * ROWS + r]);
+    for (int w = 0; w < NW; ++w) M = fmaxf(M, sm_m[w * ROWS + r]);
     float L = 0.f;
     floatx4 v = floatx4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int w = 0; w < ATTN_WAVES; ++w) {
+    for (int w = 0; w < NW; ++w) {
       const float mw = sm_m[w * ROWS + r];
       const float ew = (mw == -INFINITY) ? 0.f : exp2f(mw - M);
       L += sm_l[w * ROWS + r] * ew;
@@ -259,7 +316,8 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnKArgs a) {
   if (nch == 1) {
 #pragma unroll
     for (int i = 0; i < NV; ++i) {
-      const int idx = threadIdx.x + 256 * i;
+      const int idx = threadIdx.x + NTH * i;
+      if (idx >= NOUT) continue;
       const int r = idx / (D / 4), d4 = idx - r * (D / 4);
       const int rg = rbase + r;
       if (rg >= a.rows) continue;
@@ -276,7 +334,8 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnKArgs a) {
     floatx4* Op = (floatx4*)(a.opart + (gbase + c) * ROWS * D);
 #pragma unroll
     for (int i = 0; i < NV; ++i) {
-      const int idx = threadIdx.x + 256 * i;
+      const int idx = threadIdx.x + NTH * i;
+      if (idx >= NOUT) continue;
       Op[idx] = acc[i];
       const int r = idx / (D / 4), d4 = idx - r * (D / 4);
       if (d4 == 0) a.spart[(gbase + c) * ROWS + r] = make_float2(Mr[i], Lr[i]);
@@ -295,9 +354,9 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnKArgs a) {
   if (!is_last) return;
 
   // last chunk: statistics of every (chunk, row) into LDS (parallel loads)
-  float* cm = sm_o;                          // [nch][ROWS] chunk max
-  float* cl = sm_o + ATTN_MAX_CHUNKS * ROWS; // [nch][ROWS] chunk sum, then weight
-  for (int i = threadIdx.x; i < nch * ROWS; i += 256) {
+  float* cm = sm_o;                           // [nch][ROWS] chunk max
+  float* cl = sm_o + AT_MAX_CHUNKS * ROWS;    // [nch][ROWS] chunk sum, then weight
+  for (int i = threadIdx.x; i < nch * ROWS; i += NTH) {
     const float2 st = a.spart[gbase * ROWS + i];
     cm[i] = st.x;
     cl[i] = st.y;
@@ -317,19 +376,31 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnKArgs a) {
     sm_l[r] = L;
   }
   __syncthreads();
+  // weighted sum of the chunk partials in chunk order; the slots' loads of
+  // four chunks are in flight together
   const floatx4* G = (const floatx4*)(a.opart + gbase * ROWS * D);
+  floatx4 v[NV];
+#pragma unroll
+  for (int i = 0; i < NV; ++i) v[i] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll 4
+  for (int cc = 0; cc < nch; ++cc) {
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+      const int idx = threadIdx.x + NTH * i;
+      const int ic = idx < NOUT ? idx : NOUT - 1;
+      v[i] += G[(size_t)cc * NOUT + ic] * cl[cc * ROWS + ic / (D / 4)];
+    }
+  }
 #pragma unroll
   for (int i = 0; i < NV; ++i) {
-    const int idx = threadIdx.x + 256 * i;
+    const int idx = threadIdx.x + NTH * i;
+    if (idx >= NOUT) continue;
     const int r = idx / (D / 4), d4 = idx - r * (D / 4);
-    floatx4 v = floatx4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll 4
-    for (int cc = 0; cc < nch; ++cc) v += G[(size_t)cc * (ROWS * D / 4) + idx] * cl[cc * ROWS + r];
     const int rg = rbase + r;
     if (rg >= a.rows) continue;
     const int j = rg / a.K, k = rg - j * a.K;
     uint16_t* op = a.o + ((size_t)b * a.K + k) * (a.Hq * D) + (hkv * a.g + j) * D + 4 * d4;
-    store_split4(op, a.o_plane, v * (1.f / sm_l[r]));
+    store_split4(op, a.o_plane, v[i] * (1.f / sm_l[r]));
   }
   if (threadIdx.x == 0) a.counters[grp_id] = 0u;
 }
@@ -340,16 +411,40 @@ AttnPlan attn_plan(const Dims& dm, int B, int K, int max_ctx_now, int xcd) {
   const int g = dm.Hq / dm.Hkv;
   p.rows = K * g;
   const int qt = (p.rows + 15) / 16;
-  p.qpw = qt >= 2 ? 2 : 1;
+  p.qpw = qt >= 4 ? 2 : 1;
   p.nqg = (qt + p.qpw - 1) / p.qpw;
-  // chunk (multiple of one workgroup step): enough workgroups to cover the
-  // chip, at most ATTN_MAX_CHUNKS chunks per query group
   const long units = (long)B * dm.Hkv * p.nqg;
-  int chunk = ATTN_MIN_CHUNK;
-  auto nchunks = [&](int ch) { return (max_ctx_now + ch - 1) / ch; };
-  while ((chunk < 4096 && units * nchunks(chunk) > 1024) || nchunks(chunk) > ATTN_MAX_CHUNKS) chunk *= 2;
-  p.chunk = chunk;
-  p.nchunk = nchunks(chunk);
+  const int ctx = max_ctx_now < 1 ? 1 : max_ctx_now;
+  auto chunk_for = [&](int n) {  // whole workgroup steps covering ctx in n chunks
+    const int per = (ctx + n - 1) / n;
+    return ((per + AT_STEP - 1) / AT_STEP) * AT_STEP;
+  };
+  int best = 1;
+  if (units >= 256) {
+    // many query groups: the chip is full, chunks only bound the per-workgroup stream
+    int chunk = AT_STEP;
+    while ((chunk < 16 * AT_STEP && units * ((ctx + chunk - 1) / chunk) > 1024) ||
+           (ctx + chunk - 1) / chunk > AT_MAX_CHUNKS)
+      chunk *= 2;
+    p.chunk = chunk;
+  } else {
+    // few query groups: a chunk costs about 0.85 us per 128-key step of its
+    // workgroup, a split adds the partial publish and the merge (about
+    // 1.6 us + 0.08 us per chunk); measured on MI355X with D = 128
+    double best_t = 1e30;
+    for (int n = 1; n <= AT_MAX_CHUNKS && units * n <= 256; ++n) {
+      const int ch = chunk_for(n);
+      const int nn = (ctx + ch - 1) / ch;
+      if (nn != n) continue;
+      const double t = 0.85 * (ch / AT_STEP) * (dm.D / 128.0) + (n > 1 ? 1.6 + 0.08 * n : 0.0);
+      if (t < best_t - 1e-9) {
+        best_t = t;
+        best = n;
+      }
+    }
+    p.chunk = chunk_for(best);
+  }
+  p.nchunk = (ctx + p.chunk - 1) / p.chunk;
   return p;
 }
 
@@ -359,7 +454,8 @@ size_t attn_partials_floats(const Dims& dm, const AttnPlan& p, int B) {
 
 template <int D, int QPW>
 static void launch_attn(const AttnKArgs& a, hipStream_t st) {
-  launch_timed(attn_bf16_kernel<D, QPW>, dim3(xcd_grid(a.groups, a.nchunk, a.xcd)), dim3(256), st, a);
+  const int grid = a.nchunk == 1 ? xcd_grid(a.heads, a.nqg, a.xcd) : xcd_grid(a.groups, a.nchunk, a.xcd);
+  launch_timed(attn_bf16_kernel<D, QPW, 1>, dim3(grid), dim3(AtShape<QPW>::THREADS), st, a);
 }
 
 void attention_bf16(const Dims& dm, const AttnPlan& p, int B, int K, const int* f, const void* q, size_t q_plane,
@@ -372,7 +468,8 @@ void attention_bf16(const Dims& dm, const AttnPlan& p, int B, int K, const int* 
   a.o = (uint16_t*)o;
   a.q_plane = q_plane;
   a.o_plane = o_plane;
-  a.groups = B * dm.Hkv * p.nqg;
+  a.heads = B * dm.Hkv;
+  a.groups = a.heads * p.nqg;
   // partial O block first, then the (max, sum) pairs (offset is a multiple of D floats: 8-byte aligned)
   a.opart = partials;
   a.spart = (float2*)(partials + (size_t)a.groups * p.nchunk * p.qpw * 16 * dm.D);
@@ -384,10 +481,11 @@ void attention_bf16(const Dims& dm, const AttnPlan& p, int B, int K, const int* 
   a.g = dm.Hq / dm.Hkv;
   a.Lmax = Lmax;
   a.rows = p.rows;
+  a.qrows_pad = q_rows_pad(K, a.g);
   a.chunk = p.chunk;
   a.nchunk = p.nchunk;
   a.nqg = p.nqg;
-  a.xcd = p.nchunk > 1 ? p.xcd : 0;
+  a.xcd = p.xcd;
   a.scale_log2 = 1.4426950408889634f / sqrtf((float)dm.D);
   if (dm.D == 128) {
     if (p.qpw == 2) launch_attn<128, 2>(a, st);

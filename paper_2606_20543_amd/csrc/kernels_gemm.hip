@@ -397,27 +397,31 @@ __device__ __forceinline__ void epi_store(const EpiArgs& e, const floatx4 (&acc)
             const float a1 = x1 * cs.z - y1 * cs.w, c1 = y1 * cs.z + x1 * cs.w;
             const bool isq = n < qN;
             const int nn = isq ? n : n - qN;
-            const int head = nn / D, j = (nn - head * D) >> 1;
+            const int head = nn / D, j = (nn - head * D) >> 1;  // j even: (j, j+1) share a tile lane
             if (isq) {
-              const size_t base = (((size_t)b * e.Hq + head) * e.Kblk + k) * D;
+              // tiled q: rows r = (head within its KV group) * K + k of the KV head's block
+              const int g = e.Hq / e.Hkv, hkv = head / g;
+              const int r = (head - hkv * g) * e.Kblk + k;
+              const size_t base = ((size_t)b * e.Hkv + hkv) * (size_t)e.qrows_pad * D;
               uint32_t h0, l0, h1, l1;
               split2(a0, a1, h0, l0);
               split2(c0, c1, h1, l1);
-              *(uint32_t*)(q + base + j) = h0;
-              *(uint32_t*)(q + base + j + half) = h1;
-              *(uint32_t*)(q + e.q_plane + base + j) = l0;
-              *(uint32_t*)(q + e.q_plane + base + j + half) = l1;
+              const size_t i0 = base + tile16x32_index(r, j, D), i1 = base + tile16x32_index(r, j + half, D);
+              *(uint32_t*)(q + i0) = h0;
+              *(uint32_t*)(q + i1) = h1;
+              *(uint32_t*)(q + e.q_plane + i0) = l0;
+              *(uint32_t*)(q + e.q_plane + i1) = l1;
             } else {
-              const size_t base = (((size_t)b * e.Hkv + head) * e.Lmax + pos) * D;
-              *(uint32_t*)(kc + base + j) = pack2(f2bf(a0), f2bf(a1));
-              *(uint32_t*)(kc + base + j + half) = pack2(f2bf(c0), f2bf(c1));
+              const size_t base = ((size_t)b * e.Hkv + head) * e.Lmax * D;
+              *(uint32_t*)(kc + base + tile16x32_index(pos, j, D)) = pack2(f2bf(a0), f2bf(a1));
+              *(uint32_t*)(kc + base + tile16x32_index(pos, j + half, D)) = pack2(f2bf(c0), f2bf(c1));
             }
           } else {
             const int nv = n - qN - kN;
             const int head = nv / D, dd = nv - head * D;
-            const size_t base = (((size_t)b * e.Hkv + head) * D + dd) * e.Lmax + pos;
+            const size_t base = ((size_t)b * e.Hkv + head) * (size_t)D * e.Lmax;
 #pragma unroll
-            for (int i = 0; i < 4; ++i) vc[base + (size_t)i * e.Lmax] = f2bf(v[i] * r);
+            for (int i = 0; i < 4; ++i) vc[base + vtile_index(dd + i, pos, e.Lmax)] = f2bf(v[i] * r);
           }
           break;
         }

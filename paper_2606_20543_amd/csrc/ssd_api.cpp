@@ -270,6 +270,7 @@ void run_forward(ssd_session* s, int K, int lm_mode) {
   base.Hq = dm.Hq;
   base.Hkv = dm.Hkv;
   base.D = D;
+  base.qrows_pad = q_rows_pad(K, dm.Hq / dm.Hkv);
   base.rope = s->rope;
   base.x = s->x;
   base.xn = s->xn;
@@ -525,14 +526,16 @@ ssd_status create_session(ssd_model* m, int B, int P, int Lmax_req, int Kmax, ss
     s->x = s->mem.get<float>(M * dm.d);
     // activations: 4 bytes per element (fp32, or hi + lo bf16 planes)
     s->xn_plane = M * dm.d;
-    s->q_plane = M * dm.Hq * dm.D;
+    // q: the tiled bf16 layout pads each KV head's K*g query rows to 32; fp32 uses M*Hq*D of it
+    const size_t qcap = (size_t)B * dm.Hkv * q_rows_pad(std::max(P, Kmax), dm.Hq / dm.Hkv) * dm.D;
+    s->q_plane = qcap;
     s->o_plane = M * dm.Hq * dm.D;
     s->h_plane = M * dm.dff;
     s->xn = s->mem.get<char>(M * dm.d * 4);
     s->ssq_rows_ld = (int)M;
     s->ssq = s->mem.get<float>((size_t)ssq_parts * M);
     s->ssq_parts_cap = ssq_parts;
-    s->q = s->mem.get<char>(M * dm.Hq * dm.D * 4);
+    s->q = s->mem.get<char>(qcap * 4);
     s->o = s->mem.get<char>(M * dm.Hq * dm.D * 4);
     s->h = s->mem.get<char>(M * dm.dff * 4);
     s->logits = s->mem.get<float>(M * dm.Vimg);
@@ -557,6 +560,7 @@ ssd_status create_session(ssd_model* m, int B, int P, int Lmax_req, int Kmax, ss
     fill_u32((unsigned*)s->kc, s->kv_layer_elems * dm.L * es / 4, 0u, st);
     fill_u32((unsigned*)s->vc, s->kv_layer_elems * dm.L * es / 4, 0u, st);
     fill_u32((unsigned*)s->ref_flag, (size_t)B * s->ring, 0u, st);
+    fill_u32((unsigned*)s->q, qcap, 0u, st);  // padded query rows are read (and masked) by attention
     fill_u32(s->gcnt, gcnt, 0u, st);
     fill_u32(s->acnt, acnt, 0u, st);
     fill_u32((unsigned*)s->d_f, B, 0u, st);

@@ -4,9 +4,15 @@
 //   residual x        fp32 [M][d]
 //   xn                act [M][d]              g * x: the GEMM input after an RMSNorm
 //   ssq               fp32 [parts][Mmax]      partial sums of x^2 per token (producer feature blocks)
-//   q                 act [B][Hq][K][D]       (query row r = head_in_group * K + k)
-//   K cache           model dtype [L][B][Hkv][Lmax][D]
-//   V cache (transp.) model dtype [L][B][Hkv][D][Lmax]
+//   q                 act [B][Hkv][rows_pad x D as 16x32 tiles]   bf16 models; query row
+//                     r = head_in_group * K + k, rows_pad = K*g rounded up to 32
+//                     (fp32 models: [B][Hq][K][D] row-major)
+//   K cache           model dtype [L][B][Hkv][Lmax x D as 16x32 tiles]   (bf16; fp32: [Lmax][D])
+//   V cache (transp.) model dtype [L][B][Hkv][D x Lmax as 16x32 tiles]   (bf16; fp32: [D][Lmax])
+// A "16x32 tile" array stores each 16-row x 32-column tile (row-major tile
+// order) as one MFMA operand: 64 lanes x 8 elements, 1 KiB in bf16, so a wave
+// reads a whole tile with one coalesced 16-byte load per lane (tile16x32_index,
+// vtile_index).
 //   o                 act [M][Hq*D]           attention output
 //   h                 act [M][d_ff]           SwiGLU product
 //   logits            fp32 [M][V_img]
@@ -55,6 +61,7 @@ struct EpiArgs {
   void* kc;
   void* vc;
   int Lmax, Hq, Hkv, D;
+  int qrows_pad;         // q_rows_pad(Kblk, Hq / Hkv): rows per KV head of the tiled q (bf16 models)
   const float2* rope;    // [Lmax][D/2] (cos, sin)
   // EPI_RESID: x += v; xn = bf16(gnext * x); ssq_out[fb][t] = sum over the block's features of x^2
   float* x;
@@ -81,6 +88,25 @@ struct LayerW {
   void* w13;   // N = 2 dff, K = d
   void* w2;    // N = d, K = dff
 };
+
+// Element (row, col) of a [rows][cols] array stored as 16x32 operand tiles:
+// lane = row%16 + 16*((col%32)/8) holds cols 8-aligned, element col%8 (the
+// A/B operand layout of v_mfma_f32_16x16x32_bf16).
+__host__ __device__ inline size_t tile16x32_index(int row, int col, int cols) {
+  return ((size_t)(row >> 4) * (cols >> 5) + (col >> 5)) * 512 + (size_t)((((col & 31) >> 3) << 4) + (row & 15)) * 8 +
+         (col & 7);
+}
+// Element (d, key) of the transposed V cache [D][Lmax] as 16x32 tiles of
+// (16 dims x 32 keys), keys of a tile permuted so that lane d%16 + 16*g holds
+// keys 4g..4g+3 and 16+4g..16+4g+3 (the A operand of O^T = V^T P^T whose
+// P^T columns come straight from the S^T accumulators).
+__host__ __device__ inline size_t vtile_index(int d, int key, int Lmax) {
+  const int kk = key & 31;
+  const int g = (kk & 15) >> 2, e = (kk & 3) + ((kk >> 4) << 2);
+  return ((size_t)(d >> 4) * (Lmax >> 5) + (key >> 5)) * 512 + (size_t)(g * 16 + (d & 15)) * 8 + e;
+}
+// query rows per KV head padded for the tiled q layout
+__host__ __device__ inline int q_rows_pad(int K, int g) { return ((K * g + 31) / 32) * 32; }
 
 // Most partial sums of x^2 per token a GEMM's 1/rms prologue accepts (the
 // producing GEMM writes one per 64-feature block: d_model <= 8192).
