@@ -7,7 +7,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 OUT = os.path.join(HERE, "libssd.so")
 BUILD = os.path.join(HERE, "_build")
-SOURCES = ["kernels_gemm.hip", "kernels_attn.hip", "kernels_misc.hip", "ssd_api.cpp"]
+SOURCES = ["kernels_gemm.hip", "kernels_attn.hip", "kernels_fwd.hip", "kernels_misc.hip", "ssd_api.cpp"]
 FLAGS = [
     "-O3", "-std=c++17", "-fPIC", "--offload-arch=gfx950",
     # packed fp32 instructions stay off ("Build")

@@ -21,388 +21,20 @@
 // contexts) or to fill the chip (many query groups); chunks of one query group
 // run on workgroups of one XCD, and the last to arrive combines them in chunk
 // order.
-#include "ssd_internal.h"
+#include "tiles.h"
 
 namespace ssd {
 
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef float floatx4 __attribute__((ext_vector_type(4)));
-typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
-
-__device__ __forceinline__ uint16_t f2bf_a(float f) {
-  uint32_t u = __float_as_uint(f);
-  u += 0x7FFFu + ((u >> 16) & 1u);
-  return (uint16_t)(u >> 16);
-}
-
-constexpr int AT_KEYS = 32;        // keys per wave step
-constexpr int AT_STEP = 128;       // chunk granularity in keys (one workgroup step)
-constexpr int AT_MAX_CHUNKS = 64;
-// four waves per workgroup: one wave per SIMD, so a wave holds two K/V blocks
-// (the one in use and the next) beside its queries and accumulators
-template <int QPW>
-struct AtShape {
-  static constexpr int WAVES = 4;
-  static constexpr int THREADS = WAVES * 64;
-  static constexpr int STEP = WAVES * AT_KEYS;
-};
-
-struct AttnKArgs {
-  const uint16_t* q;   // [B][Hkv][qrows_pad x D tiles], hi plane then lo plane (q_plane elements apart)
-  const uint16_t* kc;  // [B][Hkv][Lmax x D tiles]
-  const uint16_t* vc;  // [B][Hkv][D x Lmax tiles, keys permuted]
-  uint16_t* o;         // [B*K][Hq*D], hi plane then lo plane (o_plane elements apart)
-  size_t q_plane, o_plane;
-  float* opart;        // [groups][nchunk][QPW*16][D]   chunk partial O (relative to the chunk max)
-  float2* spart;       // [groups][nchunk][QPW*16]      chunk (max, sum), log2 domain
-  unsigned* counters;  // [groups]
-  const int* f;
-  int K, Hq, Hkv, g, Lmax, rows, qrows_pad, chunk, nchunk, nqg, groups, heads, xcd;
-  float scale_log2;
-};
-
-// hi/lo bf16 planes of four consecutive fp32 values
-__device__ __forceinline__ void store_split4(uint16_t* p, size_t plane, floatx4 v) {
-  uint16_t hi[4], lo[4];
-#pragma unroll
-  for (int e = 0; e < 4; ++e) {
-    hi[e] = f2bf_a(v[e]);
-    lo[e] = f2bf_a(v[e] - __uint_as_float((uint32_t)hi[e] << 16));
-  }
-  uint2 w, x;
-  w.x = (uint32_t)hi[0] | ((uint32_t)hi[1] << 16);
-  w.y = (uint32_t)hi[2] | ((uint32_t)hi[3] << 16);
-  x.x = (uint32_t)lo[0] | ((uint32_t)lo[1] << 16);
-  x.y = (uint32_t)lo[2] | ((uint32_t)lo[3] << 16);
-  *(uint2*)p = w;
-  *(uint2*)(p + plane) = x;
-}
-
-// K and V operands of one 32-key block: K tiles (keys key0 + kt*16 + [0,16),
-// dims kd*32 + [0,32)) are the A operands of S^T, V^T tiles (dims dt*16 + [0,16),
-// keys key0 + [0,32)) those of O^T.  In the tiled caches each is 1 KiB
-// contiguous in lane order: one coalesced 16-byte load per lane.  A block past
-// the cache (a prefetch beyond the chunk) reloads the cache's last block.
-template <int D>
-struct KVTile {
-  u32x4 k[2][D / 32];
-  u32x4 v[D / 16];
-};
-
-template <int D>
-__device__ __forceinline__ void load_kv(KVTile<D>& t, const uint16_t* kbase, const uint16_t* vbase, int key0,
-                                        int Lmax, int lane) {
-  const int kb = key0 < Lmax - 32 ? key0 : Lmax - 32;
-#pragma unroll
-  for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-    for (int kd = 0; kd < D / 32; ++kd)
-      t.k[kt][kd] = *(const u32x4*)(kbase + ((size_t)((kb >> 4) + kt) * (D / 32) + kd) * 512 + lane * 8);
-#pragma unroll
-  for (int dt = 0; dt < D / 16; ++dt)
-    t.v[dt] = *(const u32x4*)(vbase + ((size_t)dt * (Lmax >> 5) + (kb >> 5)) * 512 + lane * 8);
-}
-
-// one 32-key block through the online softmax of the wave's query tiles
-template <int D, int QPW>
-__device__ __forceinline__ void attend_block(const KVTile<D>& t, int key0, const bf16x8 (&qh)[QPW][D / 32],
-                                             const bf16x8 (&ql)[QPW][D / 32], const int (&qpos)[QPW],
-                                             float scale_log2, int grp, float (&m)[QPW], float (&l)[QPW],
-                                             floatx4 (&O)[QPW][D / 16]) {
-  constexpr int KD = D / 32, DT = D / 16;
-  floatx4 s[2][QPW];
-#pragma unroll
-  for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-    for (int qt = 0; qt < QPW; ++qt) {
-      floatx4 acc = floatx4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int kd = 0; kd < KD; ++kd) {
-        const bf16x8 kf = __builtin_bit_cast(bf16x8, t.k[kt][kd]);
-        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qh[qt][kd], acc, 0, 0, 0);
-        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, ql[qt][kd], acc, 0, 0, 0);
-      }
-      s[kt][qt] = acc;
-    }
-#pragma unroll
-  for (int qt = 0; qt < QPW; ++qt) {
-    float sv[8];
-    float mx = -INFINITY;
-#pragma unroll
-    for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int key = key0 + kt * 16 + 4 * grp + e;
-        float v = s[kt][qt][e] * scale_log2;
-        v = (key <= qpos[qt]) ? v : -INFINITY;
-        sv[kt * 4 + e] = v;
-        mx = fmaxf(mx, v);
-      }
-    mx = fmaxf(mx, __shfl_xor(mx, 16));
-    mx = fmaxf(mx, __shfl_xor(mx, 32));
-    const float mnew = fmaxf(m[qt], mx);
-    const bool none = (mnew == -INFINITY);
-    const float alpha = none ? 1.f : exp2f(m[qt] - mnew);
-    float ps = 0.f;
-    uint16_t pb[8], pl[8];
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const float p = none ? 0.f : exp2f(sv[i] - mnew);
-      ps += p;
-      pb[i] = f2bf_a(p);
-      pl[i] = f2bf_a(p - __uint_as_float((uint32_t)pb[i] << 16));
-    }
-    l[qt] = l[qt] * alpha + ps;
-    m[qt] = mnew;
-    const u32x4 pv = {(uint32_t)pb[0] | ((uint32_t)pb[1] << 16), (uint32_t)pb[2] | ((uint32_t)pb[3] << 16),
-                      (uint32_t)pb[4] | ((uint32_t)pb[5] << 16), (uint32_t)pb[6] | ((uint32_t)pb[7] << 16)};
-    const u32x4 pw = {(uint32_t)pl[0] | ((uint32_t)pl[1] << 16), (uint32_t)pl[2] | ((uint32_t)pl[3] << 16),
-                      (uint32_t)pl[4] | ((uint32_t)pl[5] << 16), (uint32_t)pl[6] | ((uint32_t)pl[7] << 16)};
-    const bf16x8 pf = __builtin_bit_cast(bf16x8, pv);
-    const bf16x8 pg = __builtin_bit_cast(bf16x8, pw);
-#pragma unroll
-    for (int dt = 0; dt < DT; ++dt) {
-      O[qt][dt] *= alpha;
-      const bf16x8 vf = __builtin_bit_cast(bf16x8, t.v[dt]);
-      O[qt][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf, O[qt][dt], 0, 0, 0);
-      O[qt][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pg, O[qt][dt], 0, 0, 0);
-    }
-  }
-}
-
-// PF = 1: the next block's K/V tiles are loaded while the current one is used
-template <int D, int QPW, int PF>
 // one wave per SIMD: the register file holds two K/V blocks, the queries and
 // the accumulators without the compiler sinking the prefetch loads
+template <int D, int QPW>
 __global__ __launch_bounds__(AtShape<QPW>::THREADS) __attribute__((amdgpu_waves_per_eu(1, 1)))
 void attn_bf16_kernel(AttnKArgs a) {
-  constexpr int NW = AtShape<QPW>::WAVES, NTH = AtShape<QPW>::THREADS, STEP = AtShape<QPW>::STEP;
-  constexpr int KD = D / 32;   // 32-wide k steps over the head dimension
-  constexpr int DT = D / 16;   // 16-row d tiles of O^T
-  constexpr int ROWS = QPW * 16;
-  constexpr int RS = D + 4;    // LDS row stride (floats): rows of one wave fall on different banks
-  constexpr int NOUT = ROWS * D / 4;                          // float4 outputs of the workgroup
-  constexpr int NV = (NOUT + NTH - 1) / NTH;    // per thread
-  static_assert(2 * AT_MAX_CHUNKS * ROWS <= NW * ROWS * RS, "chunk statistics fit the O stage");
+  constexpr int NW = AtShape<QPW>::WAVES, ROWS = QPW * 16, RS = D + 4;
   __shared__ __align__(16) float sm_o[NW * ROWS * RS];
   __shared__ float sm_m[NW * ROWS], sm_l[NW * ROWS];
   __shared__ int is_last;
-
-  // single chunk: the query groups of one (sequence, KV head) share an XCD
-  // (they read the same K/V); several chunks: the chunks of one query group
-  // share an XCD (their partials meet in its L2)
-  int grp_id, c, z, qg;
-  if (a.nchunk == 1) {
-    xcd_unmap(blockIdx.x, a.nqg, a.xcd, z, qg);
-    if (z >= a.heads) return;
-    grp_id = z * a.nqg + qg;
-    c = 0;
-  } else {
-    xcd_unmap(blockIdx.x, a.nchunk, a.xcd, grp_id, c);
-    if (grp_id >= a.groups) return;
-    qg = grp_id % a.nqg;
-    z = grp_id / a.nqg;
-  }
-  const int b = z / a.Hkv, hkv = z - b * a.Hkv;
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int col = lane & 15, grp = lane >> 4;
-  const int fb = a.f[b];
-  const int ctx = fb + a.K;
-  const int nch = (ctx + a.chunk - 1) / a.chunk;
-  if (c >= nch) return;  // whole workgroup, before any barrier
-  const int kbeg = c * a.chunk;
-  const int kend = min(kbeg + a.chunk, ctx);
-  const int rbase = qg * ROWS;
-
-  const uint16_t* kbase = a.kc + ((size_t)b * a.Hkv + hkv) * a.Lmax * D;
-  const uint16_t* vbase = a.vc + ((size_t)b * a.Hkv + hkv) * (size_t)D * a.Lmax;
-  const int first = kbeg + wave * AT_KEYS;
-  const int nit = first < kend ? (kend - first + STEP - 1) / STEP : 0;
-
-  // first K/V block in flight together with the queries.  K/V loads are never
-  // conditional (a branch around loads makes the compiler wait for all of them
-  // at the join): rows past the cache are clamped, and a block past the chunk
-  // is loaded but never used.
-  KVTile<D> ta, tb;
-  load_kv<D>(ta, kbase, vbase, first, a.Lmax, lane);
-
-  // query fragments (B operand of S^T = K Q^T): lane holds row col of tile qt, d = 8*grp.. (+32 kd);
-  // q is fp32 carried as hi + lo bf16 operands
-  bf16x8 qh[QPW][KD], ql[QPW][KD];
-  int qpos[QPW];
-  const uint16_t* qbase = a.q + (size_t)z * a.qrows_pad * D;
-#pragma unroll
-  for (int qt = 0; qt < QPW; ++qt) {
-    const int r = rbase + qt * 16 + col;  // padded rows (r >= rows) exist and are masked
-    qpos[qt] = r < a.rows ? fb + r % a.K : -1;
-    const uint16_t* qp = qbase + ((size_t)((rbase >> 4) + qt) * KD) * 512 + lane * 8;
-#pragma unroll
-    for (int kd = 0; kd < KD; ++kd) {
-      qh[qt][kd] = __builtin_bit_cast(bf16x8, *(const u32x4*)(qp + kd * 512));
-      ql[qt][kd] = __builtin_bit_cast(bf16x8, *(const u32x4*)(qp + a.q_plane + kd * 512));
-    }
-  }
-
-  float m[QPW], l[QPW];
-  floatx4 O[QPW][DT];
-#pragma unroll
-  for (int qt = 0; qt < QPW; ++qt) {
-    m[qt] = -INFINITY;
-    l[qt] = 0.f;
-#pragma unroll
-    for (int dt = 0; dt < DT; ++dt) O[qt][dt] = floatx4{0.f, 0.f, 0.f, 0.f};
-  }
-
-  if constexpr (PF) {
-    // the next block is loaded before the current one is used and taken over
-    // at the end of every iteration (an unconditional use: the compiler can
-    // neither sink the loads past a loop exit nor drop the overlap)
-    for (int it = 0; it < nit; ++it) {
-      const int key0 = first + it * STEP;
-      load_kv<D>(tb, kbase, vbase, key0 + STEP, a.Lmax, lane);
-      attend_block<D, QPW>(ta, key0, qh, ql, qpos, a.scale_log2, grp, m, l, O);
-      ta = tb;
-    }
-  } else {
-    for (int it = 0; it < nit; ++it) {
-      const int key0 = first + it * STEP;
-      attend_block<D, QPW>(ta, key0, qh, ql, qpos, a.scale_log2, grp, m, l, O);
-      load_kv<D>(ta, kbase, vbase, key0 + STEP, a.Lmax, lane);
-    }
-  }
-
-  // stage this wave's triple: O^T accumulator element e of tile (qt, dt) is row
-  // qt*16 + col, dims dt*16 + 4*grp + e
-#pragma unroll
-  for (int qt = 0; qt < QPW; ++qt) {
-    l[qt] += __shfl_xor(l[qt], 16);
-    l[qt] += __shfl_xor(l[qt], 32);
-    float* row = sm_o + (size_t)(wave * ROWS + qt * 16 + col) * RS;
-#pragma unroll
-    for (int dt = 0; dt < DT; ++dt) *(floatx4*)(row + dt * 16 + 4 * grp) = O[qt][dt];
-    if (grp == 0) {
-      sm_m[wave * ROWS + qt * 16 + col] = m[qt];
-      sm_l[wave * ROWS + qt * 16 + col] = l[qt];
-    }
-  }
-  __syncthreads();
-
-  // merge the waves: thread owns float4 slots idx = tid + NTH * i (row r, dims 4*d4..)
-  floatx4 acc[NV];
-  float Lr[NV], Mr[NV];
-#pragma unroll
-  for (int i = 0; i < NV; ++i) {
-    const int idx = threadIdx.x + NTH * i;
-    const int ic = idx < NOUT ? idx : NOUT - 1;
-    const int r = ic / (D / 4), d4 = ic - r * (D / 4);
-    float M = -INFINITY;
-#pragma unroll
-    for (int w = 0; w < NW; ++w) M = fmaxf(M, sm_m[w * ROWS + r]);
-    float L = 0.f;
-    floatx4 v = floatx4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int w = 0; w < NW; ++w) {
-      const float mw = sm_m[w * ROWS + r];
-      const float ew = (mw == -INFINITY) ? 0.f : exp2f(mw - M);
-      L += sm_l[w * ROWS + r] * ew;
-      v += *(const floatx4*)(sm_o + (size_t)(w * ROWS + r) * RS + 4 * d4) * ew;
-    }
-    acc[i] = v;
-    Lr[i] = L;
-    Mr[i] = M;
-  }
-
-  if (nch == 1) {
-#pragma unroll
-    for (int i = 0; i < NV; ++i) {
-      const int idx = threadIdx.x + NTH * i;
-      if (idx >= NOUT) continue;
-      const int r = idx / (D / 4), d4 = idx - r * (D / 4);
-      const int rg = rbase + r;
-      if (rg >= a.rows) continue;
-      const int j = rg / a.K, k = rg - j * a.K;
-      uint16_t* op = a.o + ((size_t)b * a.K + k) * (a.Hq * D) + (hkv * a.g + j) * D + 4 * d4;
-      store_split4(op, a.o_plane, acc[i] * (1.f / Lr[i]));
-    }
-    return;
-  }
-
-  // publish the chunk's triple
-  const size_t gbase = (size_t)grp_id * a.nchunk;
-  {
-    floatx4* Op = (floatx4*)(a.opart + (gbase + c) * ROWS * D);
-#pragma unroll
-    for (int i = 0; i < NV; ++i) {
-      const int idx = threadIdx.x + NTH * i;
-      if (idx >= NOUT) continue;
-      Op[idx] = acc[i];
-      const int r = idx / (D / 4), d4 = idx - r * (D / 4);
-      if (d4 == 0) a.spart[(gbase + c) * ROWS + r] = make_float2(Mr[i], Lr[i]);
-    }
-  }
-  // partial stores acknowledged by this XCD's L2, then count the arrival
-  __builtin_amdgcn_s_waitcnt(0);
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    if (!a.xcd) __threadfence();  // chunks on different XCDs: write back through L2
-    unsigned prev = atomicAdd(&a.counters[grp_id], 1u);
-    is_last = (prev == (unsigned)(nch - 1));
-    if (is_last && !a.xcd) __threadfence();
-  }
-  __syncthreads();
-  if (!is_last) return;
-
-  // last chunk: statistics of every (chunk, row) into LDS (parallel loads)
-  float* cm = sm_o;                           // [nch][ROWS] chunk max
-  float* cl = sm_o + AT_MAX_CHUNKS * ROWS;    // [nch][ROWS] chunk sum, then weight
-  for (int i = threadIdx.x; i < nch * ROWS; i += NTH) {
-    const float2 st = a.spart[gbase * ROWS + i];
-    cm[i] = st.x;
-    cl[i] = st.y;
-  }
-  __syncthreads();
-  if (threadIdx.x < ROWS) {
-    const int r = threadIdx.x;
-    float M = -INFINITY;
-    for (int cc = 0; cc < nch; ++cc) M = fmaxf(M, cm[cc * ROWS + r]);
-    float L = 0.f;
-    for (int cc = 0; cc < nch; ++cc) {
-      const float lc = cl[cc * ROWS + r];
-      const float w = (lc > 0.f) ? exp2f(cm[cc * ROWS + r] - M) : 0.f;
-      L += lc * w;
-      cl[cc * ROWS + r] = w;
-    }
-    sm_l[r] = L;
-  }
-  __syncthreads();
-  // weighted sum of the chunk partials in chunk order; the slots' loads of
-  // four chunks are in flight together
-  const floatx4* G = (const floatx4*)(a.opart + gbase * ROWS * D);
-  floatx4 v[NV];
-#pragma unroll
-  for (int i = 0; i < NV; ++i) v[i] = floatx4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll 4
-  for (int cc = 0; cc < nch; ++cc) {
-#pragma unroll
-    for (int i = 0; i < NV; ++i) {
-      const int idx = threadIdx.x + NTH * i;
-      const int ic = idx < NOUT ? idx : NOUT - 1;
-      v[i] += G[(size_t)cc * NOUT + ic] * cl[cc * ROWS + ic / (D / 4)];
-    }
-  }
-#pragma unroll
-  for (int i = 0; i < NV; ++i) {
-    const int idx = threadIdx.x + NTH * i;
-    if (idx >= NOUT) continue;
-    const int r = idx / (D / 4), d4 = idx - r * (D / 4);
-    const int rg = rbase + r;
-    if (rg >= a.rows) continue;
-    const int j = rg / a.K, k = rg - j * a.K;
-    uint16_t* op = a.o + ((size_t)b * a.K + k) * (a.Hq * D) + (hkv * a.g + j) * D + 4 * d4;
-    store_split4(op, a.o_plane, v[i] * (1.f / sm_l[r]));
-  }
-  if (threadIdx.x == 0) a.counters[grp_id] = 0u;
+  attn_unit<D, QPW>(a, blockIdx.x, sm_o, sm_m, sm_l, &is_last);
 }
 
 AttnPlan attn_plan(const Dims& dm, int B, int K, int max_ctx_now, int xcd) {
@@ -455,7 +87,7 @@ size_t attn_partials_floats(const Dims& dm, const AttnPlan& p, int B) {
 template <int D, int QPW>
 static void launch_attn(const AttnKArgs& a, hipStream_t st) {
   const int grid = a.nchunk == 1 ? xcd_grid(a.heads, a.nqg, a.xcd) : xcd_grid(a.groups, a.nchunk, a.xcd);
-  launch_timed(attn_bf16_kernel<D, QPW, 1>, dim3(grid), dim3(AtShape<QPW>::THREADS), st, a);
+  launch_timed(attn_bf16_kernel<D, QPW>, dim3(grid), dim3(AtShape<QPW>::THREADS), st, a);
 }
 
 void attention_bf16(const Dims& dm, const AttnPlan& p, int B, int K, const int* f, const void* q, size_t q_plane,

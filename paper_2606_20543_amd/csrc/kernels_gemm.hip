@@ -16,21 +16,9 @@
 // each A tile meets two B operands.  When N/64 feature blocks cannot fill
 // 256 CUs the K range is split; the last workgroup of a feature block sums
 // the partials in split order (deterministic) and runs the epilogue.
-#include "ssd_internal.h"
+#include "tiles.h"
 
 namespace ssd {
-
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef float floatx4 __attribute__((ext_vector_type(4)));
-typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-
-__device__ __forceinline__ uint16_t f2bf(float f) {
-  uint32_t u = __float_as_uint(f);
-  u += 0x7FFFu + ((u >> 16) & 1u);
-  return (uint16_t)(u >> 16);
-}
-
-__device__ __forceinline__ float bf2f(uint16_t h) { return __uint_as_float(((uint32_t)h) << 16); }
 
 // stored state: bf16 for bf16 models (KV cache)
 template <bool BF>
@@ -134,332 +122,6 @@ struct GemmKArgs {
   unsigned* counters;
   EpiArgs epi;
 };
-
-template <int NT, int KCB>
-__device__ __forceinline__ void load_a(u32x4 (&ra)[NT][KCB], const u32x4* W, int KB, int nb0, int N, int kb0,
-                                       int lane) {
-  // feature tiles past N reload the last tile (no branch: a branch around the
-  // burst makes the compiler wait for all of it at the join); their results
-  // are never stored
-  const u32x4* p[NT];
-#pragma unroll
-  for (int nt = 0; nt < NT; ++nt) {
-    const int nb = (nb0 + nt) * 16 < N ? nb0 + nt : N / 16 - 1;
-    p[nt] = W + ((size_t)nb * KB + kb0) * 64 + lane;
-  }
-  // issued in the order the MFMAs consume them (k-block major), each waited
-  // for by its position in the queue: no scheduling across the loads
-#pragma unroll
-  for (int kb = 0; kb < KCB; ++kb)
-#pragma unroll
-    for (int nt = 0; nt < NT; ++nt) {
-      ra[nt][kb] = __builtin_nontemporal_load(p[nt] + kb * 64);
-      __builtin_amdgcn_sched_barrier(0);
-    }
-}
-
-template <int MT, int KCB>
-struct XStage {
-  static constexpr int MP = MT * 16;
-  static constexpr int KC = KCB * 32;
-  static constexpr int LD = KC + 8;          // bf16 per LDS row (16-byte pad)
-  static constexpr int PL = MP * LD;         // one plane
-  static constexpr int CG = KC / 8;          // 16-byte column groups per row
-  static constexpr int RSTEP = 256 / CG;     // rows covered per pass
-  static constexpr int PASSES = (MP + RSTEP - 1) / RSTEP;
-};
-
-// x chunk (both planes) -> registers
-template <int MT, int KCB, int NP>
-__device__ __forceinline__ void load_x(u32x4 (&rx)[2][NP], const uint16_t* in, size_t plane, int ld_in, int M,
-                                       int k0) {
-  using X = XStage<MT, KCB>;
-  const int cg = threadIdx.x % X::CG, r0 = threadIdx.x / X::CG;
-  // token rows past M repeat row M-1: no branch around the loads (so they
-  // issue back to back); the results of those rows are never stored
-#pragma unroll
-  for (int p = 0; p < NP; ++p) {
-    const int r = r0 + p * X::RSTEP;
-    const int rc = r < M ? r : M - 1;
-    const uint16_t* src = in + (size_t)rc * ld_in + k0 + cg * 8;
-    rx[0][p] = *(const u32x4*)src;
-    rx[1][p] = *(const u32x4*)(src + plane);
-  }
-}
-
-template <int MT, int KCB, int NP>
-__device__ __forceinline__ void store_x(const u32x4 (&rx)[2][NP], uint16_t* xs) {
-  using X = XStage<MT, KCB>;
-  const int cg = threadIdx.x % X::CG, r0 = threadIdx.x / X::CG;
-#pragma unroll
-  for (int p = 0; p < NP; ++p) {
-    int r = r0 + p * X::RSTEP;
-    if (X::PASSES * X::RSTEP == X::MP || r < X::MP) {
-      *(u32x4*)(xs + r * X::LD + cg * 8) = rx[0][p];
-      *(u32x4*)(xs + X::PL + r * X::LD + cg * 8) = rx[1][p];
-    }
-  }
-}
-
-// k-block order, so the MFMAs of block kb wait only for that block's weights
-template <int MT, int NT, int KCB>
-__device__ __forceinline__ void compute_chunk(floatx4 (&acc)[NT][MT], const u32x4 (&ra)[NT][KCB], const uint16_t* xs,
-                                              int lane) {
-  using X = XStage<MT, KCB>;
-  const int row = lane & 15, col = (lane >> 4) * 8;
-#pragma unroll
-  for (int kb = 0; kb < KCB; ++kb) {
-    bf16x8 bhi[MT], blo[MT];
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt) {
-      const uint16_t* p = xs + (mt * 16 + row) * X::LD + kb * 32 + col;
-      bhi[mt] = __builtin_bit_cast(bf16x8, *(const u32x4*)p);
-      blo[mt] = __builtin_bit_cast(bf16x8, *(const u32x4*)(p + X::PL));
-    }
-#pragma unroll
-    for (int nt = 0; nt < NT; ++nt) {
-      bf16x8 a = __builtin_bit_cast(bf16x8, ra[nt][kb]);
-#pragma unroll
-      for (int mt = 0; mt < MT; ++mt) {
-        acc[nt][mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, bhi[mt], acc[nt][mt], 0, 0, 0);
-        acc[nt][mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, blo[mt], acc[nt][mt], 0, 0, 0);
-      }
-    }
-  }
-}
-
-// ---- per-token 1/rms(x) from the producer's partial sums of x^2 ----
-// Thread (t = tid % MP, part group pg = tid / MP) loads parts pg, pg + G, ...
-// into registers before the weight burst is issued (so the wait for them does
-// not wait for the weights), sums them in part order, and the G group sums
-// meet in LDS (summed in group order: deterministic).
-template <int MP>
-struct RmsPre {
-  static constexpr int G = 256 / MP;
-  static constexpr int RQ = (GEMM_RMS_MAX_PARTS + G - 1) / G;
-};
-
-// raw loads only (no use of the values, so nothing waits for them here);
-// without partial sums (ssq == nullptr) the loads read in[0] and are ignored
-template <int MP>
-__device__ __forceinline__ void rms_issue(const EpiArgs& e, const void* dummy, int M, int t0,
-                                          float (&v)[RmsPre<MP>::RQ]) {
-  const int t = threadIdx.x % MP, pg = threadIdx.x / MP;
-  const int tc = t < M ? t : M - 1;
-  const bool has = e.ssq != nullptr;
-  const float* base = has ? e.ssq : (const float*)dummy;
-  const size_t c = has ? (size_t)e.ssq_off + (size_t)(t0 + tc) * e.ssq_step : 0;
-  const size_t ld = has ? (size_t)e.ssq_ld : 0;
-#pragma unroll
-  for (int q = 0; q < RmsPre<MP>::RQ; ++q) {
-    const int p = pg + q * RmsPre<MP>::G;
-    v[q] = base[(size_t)(p < e.ssq_parts ? p : 0) * ld + c];
-  }
-}
-
-// writes rscale[0..MP); visible after the caller's next barrier
-template <int MP>
-__device__ __forceinline__ void rms_finish(const EpiArgs& e, const float (&v)[RmsPre<MP>::RQ], float* red,
-                                           float* rscale) {
-  // branch-free in ssq (a branch here would make the compiler settle the
-  // weight loads at the join); without partial sums the scale is 1
-  const int pg = threadIdx.x / MP;
-  float s = 0.f;
-#pragma unroll
-  for (int q = 0; q < RmsPre<MP>::RQ; ++q) s += (pg + q * RmsPre<MP>::G < e.ssq_parts) ? v[q] : 0.f;
-  red[threadIdx.x] = s;  // [pg][t]
-  lds_barrier();
-  if (threadIdx.x < MP) {
-    float a = 0.f;
-#pragma unroll
-    for (int g = 0; g < RmsPre<MP>::G; ++g) a += red[g * MP + threadIdx.x];
-    rscale[threadIdx.x] = e.ssq ? 1.0f / sqrtf(a * e.inv_d + e.eps) : 1.f;
-  }
-}
-
-// per-token 1/rms(x) for large token tiles (parts in blocks of 16 through LDS)
-template <int MP>
-__device__ __forceinline__ void rms_prologue(const EpiArgs& e, int M, int t0, float (*red)[MP], float* rscale) {
-  float s = 0.f;
-  for (int p0 = 0; p0 < e.ssq_parts; p0 += 16) {
-    for (int i = threadIdx.x; i < 16 * MP; i += 256) {
-      const int p = p0 + i / MP, t = i % MP;
-      red[i / MP][t] = (p < e.ssq_parts && t < M)
-                           ? e.ssq[(size_t)p * e.ssq_ld + (size_t)e.ssq_off + (size_t)(t0 + t) * e.ssq_step]
-                           : 0.f;
-    }
-    lds_barrier();
-    if (threadIdx.x < MP)
-      for (int p = 0; p < 16; ++p) s += red[p][threadIdx.x];
-    lds_barrier();
-  }
-  if (threadIdx.x < MP) rscale[threadIdx.x] = 1.0f / sqrtf(s * e.inv_d + e.eps);
-}
-
-// ---- fused epilogue, bf16 path ----
-// The accumulator fragment acc[nt][mt] of a lane holds features n .. n+3
-// (n = (nb0 + nt) * 16 + 4 * (lane / 16)) of token t0 + mt * 16 + lane % 16.
-// Operands that do not depend on the accumulators (the token's raster
-// position, rotary factors, g_next, the old residual) are loaded first, in
-// one batch, and the stores follow: no load waits behind a store.
-__device__ __forceinline__ uint32_t pack2(uint16_t a, uint16_t b) { return (uint32_t)a | ((uint32_t)b << 16); }
-
-__device__ __forceinline__ void split2(float a, float b, uint32_t& hi, uint32_t& lo) {
-  const uint16_t ha = f2bf(a), hb = f2bf(b);
-  hi = pack2(ha, hb);
-  lo = pack2(f2bf(a - bf2f(ha)), f2bf(b - bf2f(hb)));
-}
-
-template <int NT, int MT>
-struct EpiOps {
-  float4 a[NT][MT];  // RESID: old x[t][n..n+3]; QKV: (cos, sin) of rotary pairs j, j+1 at the token's position
-  float4 g[NT];      // RESID: g_next[n..n+3]
-  int pos[MT];       // QKV: raster position of the token
-};
-
-// block start f[b] of each fragment token (raw load; the position is formed at the epilogue)
-template <int NT, int MT>
-__device__ __forceinline__ void epi_block_starts(const EpiArgs& e, int M, int t0, int lane, EpiOps<NT, MT>& op) {
-#pragma unroll
-  for (int mt = 0; mt < MT; ++mt) {
-    const int tl = mt * 16 + (lane & 15);
-    op.pos[mt] = e.f[(t0 + (tl < M ? tl : M - 1)) / e.Kblk];
-  }
-}
-
-// indexes are clamped into range (results of clamped lanes are never stored),
-// so the loads carry no branches and issue back to back
-template <int NT, int MT>
-__device__ __forceinline__ void epi_load(const EpiArgs& e, int nb0, int N, int M, int t0, int lane,
-                                         EpiOps<NT, MT>& op) {
-  const int nq = 4 * (lane >> 4);
-  if (e.kind == EPI_RESID) {
-#pragma unroll
-    for (int nt = 0; nt < NT; ++nt) {
-      const int n = (nb0 + nt) * 16 < N ? (nb0 + nt) * 16 + nq : nq;
-      op.g[nt] = *(const float4*)(e.gnext + n);
-#pragma unroll
-      for (int mt = 0; mt < MT; ++mt) {
-        const int tl = mt * 16 + (lane & 15);
-        op.a[nt][mt] = *(const float4*)(e.x + (size_t)(t0 + (tl < M ? tl : M - 1)) * e.ld + n);
-      }
-    }
-  } else if (e.kind == EPI_QKV) {
-    const int qN = e.Hq * e.D, half = e.D >> 1;
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt) {
-      const int tl = mt * 16 + (lane & 15);
-      const int t = t0 + (tl < M ? tl : M - 1);
-      op.pos[mt] += t % e.Kblk;
-    }
-#pragma unroll
-    for (int nt = 0; nt < NT; ++nt) {
-      const int n = (nb0 + nt) * 16 + nq;
-      const int nn = n < qN ? n : n - qN;
-      const int j = (nn % e.D) >> 1;  // even: pairs j, j+1
-#pragma unroll
-      for (int mt = 0; mt < MT; ++mt) op.a[nt][mt] = *(const float4*)(e.rope + (size_t)op.pos[mt] * half + j);
-    }
-  }
-}
-
-// returns per-mt partial sums of the new residual squared (RESID)
-template <int NT, int MT>
-__device__ __forceinline__ void epi_store(const EpiArgs& e, const floatx4 (&acc)[NT][MT], const EpiOps<NT, MT>& op,
-                                          int nb0, int N, int M, int t0, int lane, const float* rscale,
-                                          float (&sq)[MT]) {
-  const int nq = 4 * (lane >> 4);
-  uint16_t* q = (uint16_t*)e.q;
-  uint16_t* kc = (uint16_t*)e.kc;
-  uint16_t* vc = (uint16_t*)e.vc;
-#pragma unroll
-  for (int nt = 0; nt < NT; ++nt) {
-    const int n = (nb0 + nt) * 16 + nq;
-    if ((nb0 + nt) * 16 >= N) continue;
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt) {
-      const int tl = mt * 16 + (lane & 15);
-      if (tl >= M) continue;
-      const int t = t0 + tl;
-      const float r = rscale[tl];
-      const floatx4 v = acc[nt][mt];
-      switch (e.kind) {
-        case EPI_QKV: {
-          const int b = t / e.Kblk, k = t - b * e.Kblk;
-          const int pos = op.pos[mt];
-          const int D = e.D, half = D >> 1;
-          const int qN = e.Hq * D, kN = e.Hkv * D;
-          if (n < qN + kN) {
-            // features n..n+3 = rotary pairs (j, j + D/2) and (j + 1, j + 1 + D/2)
-            const float4 cs = op.a[nt][mt];
-            const float x0 = v[0] * r, y0 = v[1] * r, x1 = v[2] * r, y1 = v[3] * r;
-            const float a0 = x0 * cs.x - y0 * cs.y, c0 = y0 * cs.x + x0 * cs.y;
-            const float a1 = x1 * cs.z - y1 * cs.w, c1 = y1 * cs.z + x1 * cs.w;
-            const bool isq = n < qN;
-            const int nn = isq ? n : n - qN;
-            const int head = nn / D, j = (nn - head * D) >> 1;  // j even: (j, j+1) share a tile lane
-            if (isq) {
-              // tiled q: rows r = (head within its KV group) * K + k of the KV head's block
-              const int g = e.Hq / e.Hkv, hkv = head / g;
-              const int r = (head - hkv * g) * e.Kblk + k;
-              const size_t base = ((size_t)b * e.Hkv + hkv) * (size_t)e.qrows_pad * D;
-              uint32_t h0, l0, h1, l1;
-              split2(a0, a1, h0, l0);
-              split2(c0, c1, h1, l1);
-              const size_t i0 = base + tile16x32_index(r, j, D), i1 = base + tile16x32_index(r, j + half, D);
-              *(uint32_t*)(q + i0) = h0;
-              *(uint32_t*)(q + i1) = h1;
-              *(uint32_t*)(q + e.q_plane + i0) = l0;
-              *(uint32_t*)(q + e.q_plane + i1) = l1;
-            } else {
-              const size_t base = ((size_t)b * e.Hkv + head) * e.Lmax * D;
-              *(uint32_t*)(kc + base + tile16x32_index(pos, j, D)) = pack2(f2bf(a0), f2bf(a1));
-              *(uint32_t*)(kc + base + tile16x32_index(pos, j + half, D)) = pack2(f2bf(c0), f2bf(c1));
-            }
-          } else {
-            const int nv = n - qN - kN;
-            const int head = nv / D, dd = nv - head * D;
-            const size_t base = ((size_t)b * e.Hkv + head) * (size_t)D * e.Lmax;
-#pragma unroll
-            for (int i = 0; i < 4; ++i) vc[base + vtile_index(dd + i, pos, e.Lmax)] = f2bf(v[i] * r);
-          }
-          break;
-        }
-        case EPI_RESID: {
-          const size_t i = (size_t)t * e.ld + n;
-          const float4 xo = op.a[nt][mt];
-          const float4 g = op.g[nt];
-          const float4 xv = make_float4(xo.x + v[0], xo.y + v[1], xo.z + v[2], xo.w + v[3]);
-          *(float4*)(e.x + i) = xv;
-          uint32_t h0, l0, h1, l1;
-          split2(g.x * xv.x, g.y * xv.y, h0, l0);
-          split2(g.z * xv.z, g.w * xv.w, h1, l1);
-          uint16_t* xn = (uint16_t*)e.xn;
-          *(uint2*)(xn + i) = make_uint2(h0, h1);
-          *(uint2*)(xn + e.xn_plane + i) = make_uint2(l0, l1);
-          sq[mt] += (xv.x * xv.x + xv.y * xv.y) + (xv.z * xv.z + xv.w * xv.w);
-          break;
-        }
-        case EPI_SWIGLU: {
-          // packed rows (2j, 2j+1) = (gate j, up j)
-          const float g0 = v[0] * r, u0 = v[1] * r, g1 = v[2] * r, u1 = v[3] * r;
-          const float s0 = g0 / (1.0f + expf(-g0)), s1 = g1 / (1.0f + expf(-g1));
-          uint32_t hi, lo;
-          split2(s0 * u0, s1 * u1, hi, lo);
-          uint16_t* h = (uint16_t*)e.h;
-          const size_t i = (size_t)t * e.ld + (n >> 1);
-          *(uint32_t*)(h + i) = hi;
-          *(uint32_t*)(h + e.h_plane + i) = lo;
-          break;
-        }
-        default: {  // EPI_LOGITS
-          *(float4*)(e.logits + (size_t)t * e.ld + n) = make_float4(v[0] * r, v[1] * r, v[2] * r, v[3] * r);
-          break;
-        }
-      }
-    }
-  }
-}
 
 // NBUF = 1: the workgroup's whole K-slice is one chunk, loaded in one burst
 // (tokens to LDS, weights to registers; the MFMAs of k-block kb start as soon

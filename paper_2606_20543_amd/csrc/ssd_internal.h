@@ -190,6 +190,70 @@ void embed(const Dims& dm, const void* emb, const int* tok, int M, const float* 
 // fp32 path: xn = g * x, ssq[t] = sum x^2 (one part)
 void norm_rows_f32(const float* x, int M, int d, const float* g, float* xn, float* ssq, hipStream_t st);
 
+struct AttnKArgs {
+  const uint16_t* q;   // [B][Hkv][qrows_pad x D tiles], hi plane then lo plane (q_plane elements apart)
+  const uint16_t* kc;  // [B][Hkv][Lmax x D tiles]
+  const uint16_t* vc;  // [B][Hkv][D x Lmax tiles, keys permuted]
+  uint16_t* o;         // [B*K][Hq*D], hi plane then lo plane (o_plane elements apart)
+  size_t q_plane, o_plane;
+  float* opart;        // [groups][nchunk][QPW*16][D]   chunk partial O (relative to the chunk max)
+  float2* spart;       // [groups][nchunk][QPW*16]      chunk (max, sum), log2 domain
+  unsigned* counters;  // [groups]
+  const int* f;
+  int K, Hq, Hkv, g, Lmax, rows, qrows_pad, chunk, nchunk, nqg, groups, heads, xcd;
+  float scale_log2;
+};
+
+// ---- persistent forward pass (kernels_fwd.hip) ----
+enum FwdKind { FWD_GEMM = 0, FWD_ATTN = 1 };
+// A GEMM phase: 64 output features x 512 k (16 k-blocks) per work item,
+// items = xcd_grid(n_fb, S, xcd) (item -> (feature block, split) by xcd_unmap).
+struct FwdGemm {
+  const void* W;            // packed weights
+  int N, K, KB, n_fb, S, items, M;
+  const uint16_t* in;       // split input planes [M][ld_in]
+  size_t in_plane;
+  int ld_in;
+  // K-slice s (features [s*512, (s+1)*512) of the input) needs producer units
+  // [s*512*dep_scale/dep_width, ceil((s+1)*512*dep_scale/dep_width)) of `dep`
+  const unsigned* dep;      // nullptr: input ready before launch
+  int dep_width, dep_scale, dep_layer;
+  // the epilogue's 1/rms needs all rms_units units of rms_dep
+  const unsigned* rms_dep;
+  int rms_units, rms_layer;
+  float* part;
+  unsigned* counters;
+  unsigned* out_flags;      // one per feature block (nullptr: none)
+  int out_layer;
+  EpiArgs epi;
+};
+// An attention phase (geometry in FwdArgs::att; per-layer caches here).
+struct FwdAttn {
+  const unsigned* dep;      // QKV unit flags
+  int dep_width, qN, kN, layer;
+  const void* kc;
+  const void* vc;
+  unsigned* out_flags;      // one per query group
+};
+struct FwdPhase {
+  int kind;
+  FwdGemm g;
+  FwdAttn a;
+};
+// Flag values are epoch_base + layer index + 1 (epoch_base = pass * (L + 1)).
+struct FwdArgs {
+  const FwdPhase* phases;   // device
+  int n_phases;
+  int xcd;
+  unsigned* abort_flag;
+  unsigned spin_limit;
+  unsigned epoch_base;
+  AttnKArgs att;            // attention geometry of this pass (caches per phase)
+  int att_items;
+};
+hipError_t fwd_persistent(const FwdArgs& a, int MT, int D, int grid, hipStream_t st);
+int fwd_max_grid(int MT, int D);  // co-resident workgroups of the persistent kernel (0: unsupported)
+
 struct AttnPlan {
   int chunk;      // keys per workgroup
   int nchunk;     // chunks covering max context

@@ -1,0 +1,756 @@
+// Device building blocks shared by the GEMM, attention and persistent
+// forward kernels (gfx950): MFMA operand tiles, token staging through LDS,
+// fused GEMM epilogues and the per-block attention step.  Memory accesses to
+// activations go through a policy: PlainMem (ordinary loads and stores, for
+// kernels whose producers finished in an earlier launch) or CoherentMem
+// (agent-scope accesses, sc1, which bypass the per-XCD L2 so that producers
+// and consumers on different XCDs of one running kernel see each other's
+// data without L2 write-back or invalidation).
+#pragma once
+
+#include "ssd_internal.h"
+
+namespace ssd {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ uint16_t f2bf(float f) {
+  uint32_t u = __float_as_uint(f);
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+
+__device__ __forceinline__ float bf2f(uint16_t h) { return __uint_as_float(((uint32_t)h) << 16); }
+
+struct PlainMem {
+  static __device__ __forceinline__ u32x4 ld16(const void* p) { return *(const u32x4*)p; }
+  static __device__ __forceinline__ float ld4f(const float* p) { return *p; }
+  static __device__ __forceinline__ float4 ldf4(const float* p) { return *(const float4*)p; }
+  static __device__ __forceinline__ void st2(uint16_t* p, uint16_t v) { *p = v; }
+  static __device__ __forceinline__ void st4(void* p, uint32_t v) { *(uint32_t*)p = v; }
+  static __device__ __forceinline__ void st8(void* p, uint2 v) { *(uint2*)p = v; }
+  static __device__ __forceinline__ void stf4(float* p, float4 v) { *(float4*)p = v; }
+};
+
+struct CoherentMem {
+  static __device__ __forceinline__ uint64_t ld8(const void* p) {
+    return __hip_atomic_load((const uint64_t*)p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+  static __device__ __forceinline__ void st8u(void* p, uint64_t v) {
+    __hip_atomic_store((uint64_t*)p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+  static __device__ __forceinline__ u32x4 ld16(const void* p) {
+    const uint64_t a = ld8(p), b = ld8((const char*)p + 8);
+    return u32x4{(uint32_t)a, (uint32_t)(a >> 32), (uint32_t)b, (uint32_t)(b >> 32)};
+  }
+  static __device__ __forceinline__ float ld4f(const float* p) {
+    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+  static __device__ __forceinline__ float4 ldf4(const float* p) {
+    const u32x4 v = ld16(p);
+    return make_float4(__uint_as_float(v.x), __uint_as_float(v.y), __uint_as_float(v.z), __uint_as_float(v.w));
+  }
+  static __device__ __forceinline__ void st2(uint16_t* p, uint16_t v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+  static __device__ __forceinline__ void st4(void* p, uint32_t v) {
+    __hip_atomic_store((uint32_t*)p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+  static __device__ __forceinline__ void st8(void* p, uint2 v) { st8u(p, (uint64_t)v.x | ((uint64_t)v.y << 32)); }
+  static __device__ __forceinline__ void stf4(float* p, float4 v) {
+    st8u(p, (uint64_t)__float_as_uint(v.x) | ((uint64_t)__float_as_uint(v.y) << 32));
+    st8u(p + 2, (uint64_t)__float_as_uint(v.z) | ((uint64_t)__float_as_uint(v.w) << 32));
+  }
+};
+
+template <int NT, int KCB>
+__device__ __forceinline__ void load_a(u32x4 (&ra)[NT][KCB], const u32x4* W, int KB, int nb0, int N, int kb0,
+                                       int lane) {
+  // feature tiles past N reload the last tile (no branch: a branch around the
+  // burst makes the compiler wait for all of it at the join); their results
+  // are never stored
+  const u32x4* p[NT];
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) {
+    const int nb = (nb0 + nt) * 16 < N ? nb0 + nt : N / 16 - 1;
+    p[nt] = W + ((size_t)nb * KB + kb0) * 64 + lane;
+  }
+  // issued in the order the MFMAs consume them (k-block major), each waited
+  // for by its position in the queue: no scheduling across the loads
+#pragma unroll
+  for (int kb = 0; kb < KCB; ++kb)
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
+      ra[nt][kb] = __builtin_nontemporal_load(p[nt] + kb * 64);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+}
+
+template <int MT, int KCB>
+struct XStage {
+  static constexpr int MP = MT * 16;
+  static constexpr int KC = KCB * 32;
+  static constexpr int LD = KC + 8;          // bf16 per LDS row (16-byte pad)
+  static constexpr int PL = MP * LD;         // one plane
+  static constexpr int CG = KC / 8;          // 16-byte column groups per row
+  static constexpr int RSTEP = 256 / CG;     // rows covered per pass
+  static constexpr int PASSES = (MP + RSTEP - 1) / RSTEP;
+};
+
+// x chunk (both planes) -> registers
+template <int MT, int KCB, int NP, class Mem = PlainMem>
+__device__ __forceinline__ void load_x(u32x4 (&rx)[2][NP], const uint16_t* in, size_t plane, int ld_in, int M,
+                                       int k0) {
+  using X = XStage<MT, KCB>;
+  const int cg = threadIdx.x % X::CG, r0 = threadIdx.x / X::CG;
+  // token rows past M repeat row M-1: no branch around the loads (so they
+  // issue back to back); the results of those rows are never stored
+#pragma unroll
+  for (int p = 0; p < NP; ++p) {
+    const int r = r0 + p * X::RSTEP;
+    const int rc = r < M ? r : M - 1;
+    const uint16_t* src = in + (size_t)rc * ld_in + k0 + cg * 8;
+    rx[0][p] = Mem::ld16(src);
+    rx[1][p] = Mem::ld16(src + plane);
+  }
+}
+
+template <int MT, int KCB, int NP>
+__device__ __forceinline__ void store_x(const u32x4 (&rx)[2][NP], uint16_t* xs) {
+  using X = XStage<MT, KCB>;
+  const int cg = threadIdx.x % X::CG, r0 = threadIdx.x / X::CG;
+#pragma unroll
+  for (int p = 0; p < NP; ++p) {
+    int r = r0 + p * X::RSTEP;
+    if (X::PASSES * X::RSTEP == X::MP || r < X::MP) {
+      *(u32x4*)(xs + r * X::LD + cg * 8) = rx[0][p];
+      *(u32x4*)(xs + X::PL + r * X::LD + cg * 8) = rx[1][p];
+    }
+  }
+}
+
+// k-block order, so the MFMAs of block kb wait only for that block's weights
+template <int MT, int NT, int KCB>
+__device__ __forceinline__ void compute_chunk(floatx4 (&acc)[NT][MT], const u32x4 (&ra)[NT][KCB], const uint16_t* xs,
+                                              int lane) {
+  using X = XStage<MT, KCB>;
+  const int row = lane & 15, col = (lane >> 4) * 8;
+#pragma unroll
+  for (int kb = 0; kb < KCB; ++kb) {
+    bf16x8 bhi[MT], blo[MT];
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) {
+      const uint16_t* p = xs + (mt * 16 + row) * X::LD + kb * 32 + col;
+      bhi[mt] = __builtin_bit_cast(bf16x8, *(const u32x4*)p);
+      blo[mt] = __builtin_bit_cast(bf16x8, *(const u32x4*)(p + X::PL));
+    }
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
+      bf16x8 a = __builtin_bit_cast(bf16x8, ra[nt][kb]);
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) {
+        acc[nt][mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, bhi[mt], acc[nt][mt], 0, 0, 0);
+        acc[nt][mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, blo[mt], acc[nt][mt], 0, 0, 0);
+      }
+    }
+  }
+}
+
+// ---- per-token 1/rms(x) from the producer's partial sums of x^2 ----
+// Thread (t = tid % MP, part group pg = tid / MP) loads parts pg, pg + G, ...
+// into registers before the weight burst is issued (so the wait for them does
+// not wait for the weights), sums them in part order, and the G group sums
+// meet in LDS (summed in group order: deterministic).
+template <int MP>
+struct RmsPre {
+  static constexpr int G = 256 / MP;
+  static constexpr int RQ = (GEMM_RMS_MAX_PARTS + G - 1) / G;
+};
+
+// raw loads only (no use of the values, so nothing waits for them here);
+// without partial sums (ssq == nullptr) the loads read in[0] and are ignored
+template <int MP, class Mem = PlainMem>
+__device__ __forceinline__ void rms_issue(const EpiArgs& e, const void* dummy, int M, int t0,
+                                          float (&v)[RmsPre<MP>::RQ]) {
+  const int t = threadIdx.x % MP, pg = threadIdx.x / MP;
+  const int tc = t < M ? t : M - 1;
+  const bool has = e.ssq != nullptr;
+  const float* base = has ? e.ssq : (const float*)dummy;
+  const size_t c = has ? (size_t)e.ssq_off + (size_t)(t0 + tc) * e.ssq_step : 0;
+  const size_t ld = has ? (size_t)e.ssq_ld : 0;
+#pragma unroll
+  for (int q = 0; q < RmsPre<MP>::RQ; ++q) {
+    const int p = pg + q * RmsPre<MP>::G;
+    v[q] = Mem::ld4f(base + (size_t)(p < e.ssq_parts ? p : 0) * ld + c);
+  }
+}
+
+// writes rscale[0..MP); visible after the caller's next barrier
+template <int MP>
+__device__ __forceinline__ void rms_finish(const EpiArgs& e, const float (&v)[RmsPre<MP>::RQ], float* red,
+                                           float* rscale) {
+  // branch-free in ssq (a branch here would make the compiler settle the
+  // weight loads at the join); without partial sums the scale is 1
+  const int pg = threadIdx.x / MP;
+  float s = 0.f;
+#pragma unroll
+  for (int q = 0; q < RmsPre<MP>::RQ; ++q) s += (pg + q * RmsPre<MP>::G < e.ssq_parts) ? v[q] : 0.f;
+  red[threadIdx.x] = s;  // [pg][t]
+  lds_barrier();
+  if (threadIdx.x < MP) {
+    float a = 0.f;
+#pragma unroll
+    for (int g = 0; g < RmsPre<MP>::G; ++g) a += red[g * MP + threadIdx.x];
+    rscale[threadIdx.x] = e.ssq ? 1.0f / sqrtf(a * e.inv_d + e.eps) : 1.f;
+  }
+}
+
+// per-token 1/rms(x) for large token tiles (parts in blocks of 16 through LDS)
+template <int MP>
+__device__ __forceinline__ void rms_prologue(const EpiArgs& e, int M, int t0, float (*red)[MP], float* rscale) {
+  float s = 0.f;
+  for (int p0 = 0; p0 < e.ssq_parts; p0 += 16) {
+    for (int i = threadIdx.x; i < 16 * MP; i += 256) {
+      const int p = p0 + i / MP, t = i % MP;
+      red[i / MP][t] = (p < e.ssq_parts && t < M)
+                           ? e.ssq[(size_t)p * e.ssq_ld + (size_t)e.ssq_off + (size_t)(t0 + t) * e.ssq_step]
+                           : 0.f;
+    }
+    lds_barrier();
+    if (threadIdx.x < MP)
+      for (int p = 0; p < 16; ++p) s += red[p][threadIdx.x];
+    lds_barrier();
+  }
+  if (threadIdx.x < MP) rscale[threadIdx.x] = 1.0f / sqrtf(s * e.inv_d + e.eps);
+}
+
+// ---- fused epilogue, bf16 path ----
+// The accumulator fragment acc[nt][mt] of a lane holds features n .. n+3
+// (n = (nb0 + nt) * 16 + 4 * (lane / 16)) of token t0 + mt * 16 + lane % 16.
+// Operands that do not depend on the accumulators (the token's raster
+// position, rotary factors, g_next, the old residual) are loaded first, in
+// one batch, and the stores follow: no load waits behind a store.
+__device__ __forceinline__ uint32_t pack2(uint16_t a, uint16_t b) { return (uint32_t)a | ((uint32_t)b << 16); }
+
+__device__ __forceinline__ void split2(float a, float b, uint32_t& hi, uint32_t& lo) {
+  const uint16_t ha = f2bf(a), hb = f2bf(b);
+  hi = pack2(ha, hb);
+  lo = pack2(f2bf(a - bf2f(ha)), f2bf(b - bf2f(hb)));
+}
+
+template <int NT, int MT>
+struct EpiOps {
+  float4 a[NT][MT];  // RESID: old x[t][n..n+3]; QKV: (cos, sin) of rotary pairs j, j+1 at the token's position
+  float4 g[NT];      // RESID: g_next[n..n+3]
+  int pos[MT];       // QKV: raster position of the token
+};
+
+// block start f[b] of each fragment token (raw load; the position is formed at the epilogue)
+template <int NT, int MT>
+__device__ __forceinline__ void epi_block_starts(const EpiArgs& e, int M, int t0, int lane, EpiOps<NT, MT>& op) {
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt) {
+    const int tl = mt * 16 + (lane & 15);
+    op.pos[mt] = e.f[(t0 + (tl < M ? tl : M - 1)) / e.Kblk];
+  }
+}
+
+// indexes are clamped into range (results of clamped lanes are never stored),
+// so the loads carry no branches and issue back to back
+template <int NT, int MT, class Mem = PlainMem>
+__device__ __forceinline__ void epi_load(const EpiArgs& e, int nb0, int N, int M, int t0, int lane,
+                                         EpiOps<NT, MT>& op) {
+  const int nq = 4 * (lane >> 4);
+  if (e.kind == EPI_RESID) {
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
+      const int n = (nb0 + nt) * 16 < N ? (nb0 + nt) * 16 + nq : nq;
+      op.g[nt] = *(const float4*)(e.gnext + n);
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) {
+        const int tl = mt * 16 + (lane & 15);
+        op.a[nt][mt] = Mem::ldf4(e.x + (size_t)(t0 + (tl < M ? tl : M - 1)) * e.ld + n);
+      }
+    }
+  } else if (e.kind == EPI_QKV) {
+    const int qN = e.Hq * e.D, half = e.D >> 1;
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) {
+      const int tl = mt * 16 + (lane & 15);
+      const int t = t0 + (tl < M ? tl : M - 1);
+      op.pos[mt] += t % e.Kblk;
+    }
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
+      const int n = (nb0 + nt) * 16 + nq;
+      const int nn = n < qN ? n : n - qN;
+      const int j = (nn % e.D) >> 1;  // even: pairs j, j+1
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) op.a[nt][mt] = *(const float4*)(e.rope + (size_t)op.pos[mt] * half + j);
+    }
+  }
+}
+
+// returns per-mt partial sums of the new residual squared (RESID)
+template <int NT, int MT, class Mem = PlainMem>
+__device__ __forceinline__ void epi_store(const EpiArgs& e, const floatx4 (&acc)[NT][MT], const EpiOps<NT, MT>& op,
+                                          int nb0, int N, int M, int t0, int lane, const float* rscale,
+                                          float (&sq)[MT]) {
+  const int nq = 4 * (lane >> 4);
+  uint16_t* q = (uint16_t*)e.q;
+  uint16_t* kc = (uint16_t*)e.kc;
+  uint16_t* vc = (uint16_t*)e.vc;
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) {
+    const int n = (nb0 + nt) * 16 + nq;
+    if ((nb0 + nt) * 16 >= N) continue;
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) {
+      const int tl = mt * 16 + (lane & 15);
+      if (tl >= M) continue;
+      const int t = t0 + tl;
+      const float r = rscale[tl];
+      const floatx4 v = acc[nt][mt];
+      switch (e.kind) {
+        case EPI_QKV: {
+          const int b = t / e.Kblk, k = t - b * e.Kblk;
+          const int pos = op.pos[mt];
+          const int D = e.D, half = D >> 1;
+          const int qN = e.Hq * D, kN = e.Hkv * D;
+          if (n < qN + kN) {
+            // features n..n+3 = rotary pairs (j, j + D/2) and (j + 1, j + 1 + D/2)
+            const float4 cs = op.a[nt][mt];
+            const float x0 = v[0] * r, y0 = v[1] * r, x1 = v[2] * r, y1 = v[3] * r;
+            const float a0 = x0 * cs.x - y0 * cs.y, c0 = y0 * cs.x + x0 * cs.y;
+            const float a1 = x1 * cs.z - y1 * cs.w, c1 = y1 * cs.z + x1 * cs.w;
+            const bool isq = n < qN;
+            const int nn = isq ? n : n - qN;
+            const int head = nn / D, j = (nn - head * D) >> 1;  // j even: (j, j+1) share a tile lane
+            if (isq) {
+              // tiled q: rows r = (head within its KV group) * K + k of the KV head's block
+              const int g = e.Hq / e.Hkv, hkv = head / g;
+              const int r = (head - hkv * g) * e.Kblk + k;
+              const size_t base = ((size_t)b * e.Hkv + hkv) * (size_t)e.qrows_pad * D;
+              uint32_t h0, l0, h1, l1;
+              split2(a0, a1, h0, l0);
+              split2(c0, c1, h1, l1);
+              const size_t i0 = base + tile16x32_index(r, j, D), i1 = base + tile16x32_index(r, j + half, D);
+              Mem::st4(q + i0, h0);
+              Mem::st4(q + i1, h1);
+              Mem::st4(q + e.q_plane + i0, l0);
+              Mem::st4(q + e.q_plane + i1, l1);
+            } else {
+              const size_t base = ((size_t)b * e.Hkv + head) * e.Lmax * D;
+              Mem::st4(kc + base + tile16x32_index(pos, j, D), pack2(f2bf(a0), f2bf(a1)));
+              Mem::st4(kc + base + tile16x32_index(pos, j + half, D), pack2(f2bf(c0), f2bf(c1)));
+            }
+          } else {
+            const int nv = n - qN - kN;
+            const int head = nv / D, dd = nv - head * D;
+            const size_t base = ((size_t)b * e.Hkv + head) * (size_t)D * e.Lmax;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) Mem::st2(vc + base + vtile_index(dd + i, pos, e.Lmax), f2bf(v[i] * r));
+          }
+          break;
+        }
+        case EPI_RESID: {
+          const size_t i = (size_t)t * e.ld + n;
+          const float4 xo = op.a[nt][mt];
+          const float4 g = op.g[nt];
+          const float4 xv = make_float4(xo.x + v[0], xo.y + v[1], xo.z + v[2], xo.w + v[3]);
+          Mem::stf4(e.x + i, xv);
+          uint32_t h0, l0, h1, l1;
+          split2(g.x * xv.x, g.y * xv.y, h0, l0);
+          split2(g.z * xv.z, g.w * xv.w, h1, l1);
+          uint16_t* xn = (uint16_t*)e.xn;
+          Mem::st8(xn + i, make_uint2(h0, h1));
+          Mem::st8(xn + e.xn_plane + i, make_uint2(l0, l1));
+          sq[mt] += (xv.x * xv.x + xv.y * xv.y) + (xv.z * xv.z + xv.w * xv.w);
+          break;
+        }
+        case EPI_SWIGLU: {
+          // packed rows (2j, 2j+1) = (gate j, up j)
+          const float g0 = v[0] * r, u0 = v[1] * r, g1 = v[2] * r, u1 = v[3] * r;
+          const float s0 = g0 / (1.0f + expf(-g0)), s1 = g1 / (1.0f + expf(-g1));
+          uint32_t hi, lo;
+          split2(s0 * u0, s1 * u1, hi, lo);
+          uint16_t* h = (uint16_t*)e.h;
+          const size_t i = (size_t)t * e.ld + (n >> 1);
+          Mem::st4(h + i, hi);
+          Mem::st4(h + e.h_plane + i, lo);
+          break;
+        }
+        default: {  // EPI_LOGITS
+          Mem::stf4(e.logits + (size_t)t * e.ld + n, make_float4(v[0] * r, v[1] * r, v[2] * r, v[3] * r));
+          break;
+        }
+      }
+    }
+  }
+}
+
+
+// hi/lo bf16 planes of four consecutive fp32 values
+template <class Mem = PlainMem>
+__device__ __forceinline__ void store_split4(uint16_t* p, size_t plane, floatx4 v) {
+  uint16_t hi[4], lo[4];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    hi[e] = f2bf(v[e]);
+    lo[e] = f2bf(v[e] - __uint_as_float((uint32_t)hi[e] << 16));
+  }
+  uint2 w, x;
+  w.x = (uint32_t)hi[0] | ((uint32_t)hi[1] << 16);
+  w.y = (uint32_t)hi[2] | ((uint32_t)hi[3] << 16);
+  x.x = (uint32_t)lo[0] | ((uint32_t)lo[1] << 16);
+  x.y = (uint32_t)lo[2] | ((uint32_t)lo[3] << 16);
+  Mem::st8(p, w);
+  Mem::st8(p + plane, x);
+}
+
+// K and V operands of one 32-key block: K tiles (keys key0 + kt*16 + [0,16),
+// dims kd*32 + [0,32)) are the A operands of S^T, V^T tiles (dims dt*16 + [0,16),
+// keys key0 + [0,32)) those of O^T.  In the tiled caches each is 1 KiB
+// contiguous in lane order: one coalesced 16-byte load per lane.  A block past
+// the cache (a prefetch beyond the chunk) reloads the cache's last block.
+template <int D>
+struct KVTile {
+  u32x4 k[2][D / 32];
+  u32x4 v[D / 16];
+};
+
+template <int D, class Mem = PlainMem>
+__device__ __forceinline__ void load_kv(KVTile<D>& t, const uint16_t* kbase, const uint16_t* vbase, int key0,
+                                        int Lmax, int lane) {
+  const int kb = key0 < Lmax - 32 ? key0 : Lmax - 32;
+#pragma unroll
+  for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+    for (int kd = 0; kd < D / 32; ++kd)
+      t.k[kt][kd] = Mem::ld16(kbase + ((size_t)((kb >> 4) + kt) * (D / 32) + kd) * 512 + lane * 8);
+#pragma unroll
+  for (int dt = 0; dt < D / 16; ++dt)
+    t.v[dt] = Mem::ld16(vbase + ((size_t)dt * (Lmax >> 5) + (kb >> 5)) * 512 + lane * 8);
+}
+
+// one 32-key block through the online softmax of the wave's query tiles
+template <int D, int QPW>
+__device__ __forceinline__ void attend_block(const KVTile<D>& t, int key0, const bf16x8 (&qh)[QPW][D / 32],
+                                             const bf16x8 (&ql)[QPW][D / 32], const int (&qpos)[QPW],
+                                             float scale_log2, int grp, float (&m)[QPW], float (&l)[QPW],
+                                             floatx4 (&O)[QPW][D / 16]) {
+  constexpr int KD = D / 32, DT = D / 16;
+  floatx4 s[2][QPW];
+#pragma unroll
+  for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+    for (int qt = 0; qt < QPW; ++qt) {
+      floatx4 acc = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int kd = 0; kd < KD; ++kd) {
+        const bf16x8 kf = __builtin_bit_cast(bf16x8, t.k[kt][kd]);
+        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qh[qt][kd], acc, 0, 0, 0);
+        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, ql[qt][kd], acc, 0, 0, 0);
+      }
+      s[kt][qt] = acc;
+    }
+#pragma unroll
+  for (int qt = 0; qt < QPW; ++qt) {
+    float sv[8];
+    float mx = -INFINITY;
+#pragma unroll
+    for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int key = key0 + kt * 16 + 4 * grp + e;
+        float v = s[kt][qt][e] * scale_log2;
+        v = (key <= qpos[qt]) ? v : -INFINITY;
+        sv[kt * 4 + e] = v;
+        mx = fmaxf(mx, v);
+      }
+    mx = fmaxf(mx, __shfl_xor(mx, 16));
+    mx = fmaxf(mx, __shfl_xor(mx, 32));
+    const float mnew = fmaxf(m[qt], mx);
+    const bool none = (mnew == -INFINITY);
+    const float alpha = none ? 1.f : exp2f(m[qt] - mnew);
+    float ps = 0.f;
+    uint16_t pb[8], pl[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const float p = none ? 0.f : exp2f(sv[i] - mnew);
+      ps += p;
+      pb[i] = f2bf(p);
+      pl[i] = f2bf(p - __uint_as_float((uint32_t)pb[i] << 16));
+    }
+    l[qt] = l[qt] * alpha + ps;
+    m[qt] = mnew;
+    const u32x4 pv = {(uint32_t)pb[0] | ((uint32_t)pb[1] << 16), (uint32_t)pb[2] | ((uint32_t)pb[3] << 16),
+                      (uint32_t)pb[4] | ((uint32_t)pb[5] << 16), (uint32_t)pb[6] | ((uint32_t)pb[7] << 16)};
+    const u32x4 pw = {(uint32_t)pl[0] | ((uint32_t)pl[1] << 16), (uint32_t)pl[2] | ((uint32_t)pl[3] << 16),
+                      (uint32_t)pl[4] | ((uint32_t)pl[5] << 16), (uint32_t)pl[6] | ((uint32_t)pl[7] << 16)};
+    const bf16x8 pf = __builtin_bit_cast(bf16x8, pv);
+    const bf16x8 pg = __builtin_bit_cast(bf16x8, pw);
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) {
+      O[qt][dt] *= alpha;
+      const bf16x8 vf = __builtin_bit_cast(bf16x8, t.v[dt]);
+      O[qt][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf, O[qt][dt], 0, 0, 0);
+      O[qt][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pg, O[qt][dt], 0, 0, 0);
+    }
+  }
+}
+
+
+constexpr int AT_KEYS = 32;        // keys per wave step
+constexpr int AT_STEP = 128;       // chunk granularity in keys (one workgroup step)
+constexpr int AT_MAX_CHUNKS = 64;
+// four waves per workgroup: one wave per SIMD, so a wave holds two K/V blocks
+// (the one in use and the next) beside its queries and accumulators
+template <int QPW>
+struct AtShape {
+  static constexpr int WAVES = 4;
+  static constexpr int THREADS = WAVES * 64;
+  static constexpr int STEP = WAVES * AT_KEYS;
+};
+
+
+// PF = 1: the next block's K/V tiles are loaded while the current one is used
+// Attention for one work item of a launch: item = workgroup slot (single
+// chunk: the query groups of one (sequence, KV head) share an XCD, they read
+// the same K/V; several chunks: the chunks of one query group share an XCD,
+// their partials meet in its L2).  Whole-workgroup call.  Returns the query
+// group (sequence x KV head x query group index) whose output this workgroup
+// wrote, or -1 (idle slot, or a chunk whose partial another workgroup merges).
+// LDS: sm_o[NW*QPW*16*(D+4)], sm_m/sm_l[NW*QPW*16], is_last.
+template <int D, int QPW, class Mem = PlainMem, bool PF = true>
+__device__ __forceinline__ int attn_unit(const AttnKArgs& a, int item, float* sm_o, float* sm_m, float* sm_l,
+                                         int* is_last) {
+  constexpr int NW = AtShape<QPW>::WAVES, NTH = AtShape<QPW>::THREADS, STEP = AtShape<QPW>::STEP;
+  constexpr int KD = D / 32;   // 32-wide k steps over the head dimension
+  constexpr int DT = D / 16;   // 16-row d tiles of O^T
+  constexpr int ROWS = QPW * 16;
+  constexpr int RS = D + 4;    // LDS row stride (floats): rows of one wave fall on different banks
+  constexpr int NOUT = ROWS * D / 4;                          // float4 outputs of the workgroup
+  constexpr int NV = (NOUT + NTH - 1) / NTH;    // per thread
+  static_assert(2 * AT_MAX_CHUNKS * ROWS <= NW * ROWS * RS, "chunk statistics fit the O stage");
+  // single chunk: the query groups of one (sequence, KV head) share an XCD
+  // (they read the same K/V); several chunks: the chunks of one query group
+  // share an XCD (their partials meet in its L2)
+  int grp_id, c, z, qg;
+  if (a.nchunk == 1) {
+    xcd_unmap(item, a.nqg, a.xcd, z, qg);
+    if (z >= a.heads) return -1;
+    grp_id = z * a.nqg + qg;
+    c = 0;
+  } else {
+    xcd_unmap(item, a.nchunk, a.xcd, grp_id, c);
+    if (grp_id >= a.groups) return -1;
+    qg = grp_id % a.nqg;
+    z = grp_id / a.nqg;
+  }
+  const int b = z / a.Hkv, hkv = z - b * a.Hkv;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int col = lane & 15, grp = lane >> 4;
+  const int fb = a.f[b];
+  const int ctx = fb + a.K;
+  const int nch = (ctx + a.chunk - 1) / a.chunk;
+  if (c >= nch) return -1;  // whole workgroup, before any barrier
+  const int kbeg = c * a.chunk;
+  const int kend = min(kbeg + a.chunk, ctx);
+  const int rbase = qg * ROWS;
+
+  const uint16_t* kbase = a.kc + ((size_t)b * a.Hkv + hkv) * a.Lmax * D;
+  const uint16_t* vbase = a.vc + ((size_t)b * a.Hkv + hkv) * (size_t)D * a.Lmax;
+  const int first = kbeg + wave * AT_KEYS;
+  const int nit = first < kend ? (kend - first + STEP - 1) / STEP : 0;
+
+  // first K/V block in flight together with the queries.  K/V loads are never
+  // conditional (a branch around loads makes the compiler wait for all of them
+  // at the join): rows past the cache are clamped, and a block past the chunk
+  // is loaded but never used.
+  KVTile<D> ta, tb;
+  load_kv<D, Mem>(ta, kbase, vbase, first, a.Lmax, lane);
+
+  // query fragments (B operand of S^T = K Q^T): lane holds row col of tile qt, d = 8*grp.. (+32 kd);
+  // q is fp32 carried as hi + lo bf16 operands
+  bf16x8 qh[QPW][KD], ql[QPW][KD];
+  int qpos[QPW];
+  const uint16_t* qbase = a.q + (size_t)z * a.qrows_pad * D;
+#pragma unroll
+  for (int qt = 0; qt < QPW; ++qt) {
+    const int r = rbase + qt * 16 + col;  // padded rows (r >= rows) exist and are masked
+    qpos[qt] = r < a.rows ? fb + r % a.K : -1;
+    const uint16_t* qp = qbase + ((size_t)((rbase >> 4) + qt) * KD) * 512 + lane * 8;
+#pragma unroll
+    for (int kd = 0; kd < KD; ++kd) {
+      qh[qt][kd] = __builtin_bit_cast(bf16x8, Mem::ld16(qp + kd * 512));
+      ql[qt][kd] = __builtin_bit_cast(bf16x8, Mem::ld16(qp + a.q_plane + kd * 512));
+    }
+  }
+
+  float m[QPW], l[QPW];
+  floatx4 O[QPW][DT];
+#pragma unroll
+  for (int qt = 0; qt < QPW; ++qt) {
+    m[qt] = -INFINITY;
+    l[qt] = 0.f;
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) O[qt][dt] = floatx4{0.f, 0.f, 0.f, 0.f};
+  }
+
+  if constexpr (PF) {
+    // the next block is loaded before the current one is used and taken over
+    // at the end of every iteration (an unconditional use: the compiler can
+    // neither sink the loads past a loop exit nor drop the overlap)
+    for (int it = 0; it < nit; ++it) {
+      const int key0 = first + it * STEP;
+      load_kv<D, Mem>(tb, kbase, vbase, key0 + STEP, a.Lmax, lane);
+      attend_block<D, QPW>(ta, key0, qh, ql, qpos, a.scale_log2, grp, m, l, O);
+      ta = tb;
+    }
+  } else {
+    // one block in registers (for callers that keep other data live)
+    for (int it = 0; it < nit; ++it) {
+      const int key0 = first + it * STEP;
+      attend_block<D, QPW>(ta, key0, qh, ql, qpos, a.scale_log2, grp, m, l, O);
+      if (it + 1 < nit) load_kv<D, Mem>(ta, kbase, vbase, key0 + STEP, a.Lmax, lane);
+    }
+  }
+
+  // stage this wave's triple: O^T accumulator element e of tile (qt, dt) is row
+  // qt*16 + col, dims dt*16 + 4*grp + e
+#pragma unroll
+  for (int qt = 0; qt < QPW; ++qt) {
+    l[qt] += __shfl_xor(l[qt], 16);
+    l[qt] += __shfl_xor(l[qt], 32);
+    float* row = sm_o + (size_t)(wave * ROWS + qt * 16 + col) * RS;
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) *(floatx4*)(row + dt * 16 + 4 * grp) = O[qt][dt];
+    if (grp == 0) {
+      sm_m[wave * ROWS + qt * 16 + col] = m[qt];
+      sm_l[wave * ROWS + qt * 16 + col] = l[qt];
+    }
+  }
+  __syncthreads();
+
+  // merge the waves: thread owns float4 slots idx = tid + NTH * i (row r, dims 4*d4..)
+  floatx4 acc[NV];
+  float Lr[NV], Mr[NV];
+#pragma unroll
+  for (int i = 0; i < NV; ++i) {
+    const int idx = threadIdx.x + NTH * i;
+    const int ic = idx < NOUT ? idx : NOUT - 1;
+    const int r = ic / (D / 4), d4 = ic - r * (D / 4);
+    float M = -INFINITY;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) M = fmaxf(M, sm_m[w * ROWS + r]);
+    float L = 0.f;
+    floatx4 v = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int w = 0; w < NW; ++w) {
+      const float mw = sm_m[w * ROWS + r];
+      const float ew = (mw == -INFINITY) ? 0.f : exp2f(mw - M);
+      L += sm_l[w * ROWS + r] * ew;
+      v += *(const floatx4*)(sm_o + (size_t)(w * ROWS + r) * RS + 4 * d4) * ew;
+    }
+    acc[i] = v;
+    Lr[i] = L;
+    Mr[i] = M;
+  }
+
+  if (nch == 1) {
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+      const int idx = threadIdx.x + NTH * i;
+      if (idx >= NOUT) continue;
+      const int r = idx / (D / 4), d4 = idx - r * (D / 4);
+      const int rg = rbase + r;
+      if (rg >= a.rows) continue;
+      const int j = rg / a.K, k = rg - j * a.K;
+      uint16_t* op = a.o + ((size_t)b * a.K + k) * (a.Hq * D) + (hkv * a.g + j) * D + 4 * d4;
+      store_split4<Mem>(op, a.o_plane, acc[i] * (1.f / Lr[i]));
+    }
+    return grp_id;
+  }
+
+  // publish the chunk's triple
+  const size_t gbase = (size_t)grp_id * a.nchunk;
+  {
+    floatx4* Op = (floatx4*)(a.opart + (gbase + c) * ROWS * D);
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+      const int idx = threadIdx.x + NTH * i;
+      if (idx >= NOUT) continue;
+      Op[idx] = acc[i];
+      const int r = idx / (D / 4), d4 = idx - r * (D / 4);
+      if (d4 == 0) a.spart[(gbase + c) * ROWS + r] = make_float2(Mr[i], Lr[i]);
+    }
+  }
+  // partial stores acknowledged by this XCD's L2, then count the arrival
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    if (!a.xcd) __threadfence();  // chunks on different XCDs: write back through L2
+    unsigned prev = atomicAdd(&a.counters[grp_id], 1u);
+    *is_last = (prev == (unsigned)(nch - 1));
+    if (*is_last && !a.xcd) __threadfence();
+  }
+  __syncthreads();
+  if (!*is_last) return -1;
+
+  // last chunk: statistics of every (chunk, row) into LDS (parallel loads)
+  float* cm = sm_o;                           // [nch][ROWS] chunk max
+  float* cl = sm_o + AT_MAX_CHUNKS * ROWS;    // [nch][ROWS] chunk sum, then weight
+  for (int i = threadIdx.x; i < nch * ROWS; i += NTH) {
+    const float2 st = a.spart[gbase * ROWS + i];
+    cm[i] = st.x;
+    cl[i] = st.y;
+  }
+  __syncthreads();
+  if (threadIdx.x < ROWS) {
+    const int r = threadIdx.x;
+    float M = -INFINITY;
+    for (int cc = 0; cc < nch; ++cc) M = fmaxf(M, cm[cc * ROWS + r]);
+    float L = 0.f;
+    for (int cc = 0; cc < nch; ++cc) {
+      const float lc = cl[cc * ROWS + r];
+      const float w = (lc > 0.f) ? exp2f(cm[cc * ROWS + r] - M) : 0.f;
+      L += lc * w;
+      cl[cc * ROWS + r] = w;
+    }
+    sm_l[r] = L;
+  }
+  __syncthreads();
+  // weighted sum of the chunk partials in chunk order; the slots' loads of
+  // four chunks are in flight together
+  const floatx4* G = (const floatx4*)(a.opart + gbase * ROWS * D);
+  floatx4 v[NV];
+#pragma unroll
+  for (int i = 0; i < NV; ++i) v[i] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll 4
+  for (int cc = 0; cc < nch; ++cc) {
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+      const int idx = threadIdx.x + NTH * i;
+      const int ic = idx < NOUT ? idx : NOUT - 1;
+      v[i] += G[(size_t)cc * NOUT + ic] * cl[cc * ROWS + ic / (D / 4)];
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < NV; ++i) {
+    const int idx = threadIdx.x + NTH * i;
+    if (idx >= NOUT) continue;
+    const int r = idx / (D / 4), d4 = idx - r * (D / 4);
+    const int rg = rbase + r;
+    if (rg >= a.rows) continue;
+    const int j = rg / a.K, k = rg - j * a.K;
+    uint16_t* op = a.o + ((size_t)b * a.K + k) * (a.Hq * D) + (hkv * a.g + j) * D + 4 * d4;
+    store_split4<Mem>(op, a.o_plane, v[i] * (1.f / sm_l[r]));
+  }
+  if (threadIdx.x == 0) a.counters[grp_id] = 0u;
+  return grp_id;
+}
+
+}  // namespace ssd
