@@ -44,7 +44,9 @@ typedef enum {
   SSD_E_STATE = -2,    /* call not allowed in the object's current state */
   SSD_E_CAPACITY = -3, /* block would run past the session's max context */
   SSD_E_OOM = -4,      /* device allocation failed */
-  SSD_E_DEVICE = -5    /* a HIP call failed; the object is poisoned */
+  SSD_E_DEVICE = -5    /* a HIP call failed, or a single-launch forward pass gave
+                          up a bounded dependency wait (reported by the next call
+                          that synchronizes); the object is poisoned */
 } ssd_status;
 
 typedef enum { SSD_F32 = 0, SSD_BF16 = 1 } ssd_dtype;
@@ -209,14 +211,15 @@ ssd_status ssd_decode_image(ssd_model* model, const ssd_schedule* sched, int32_t
 
 /*
  * Measurement hook.  enable = 1 starts recording a HIP event pair around every
- * projection-GEMM and attention launch of the model's forward passes (on the
- * stream they run on); enable = 0 stops.  ssd_profile_read fills
- * ms[c] = summed kernel time and launches[c] = launch count per class
- * c = 0 QKV, 1 O-proj, 2 gate/up, 3 down, 4 LM head, 5 attention, and
+ * projection-GEMM and attention launch of the model's forward passes, and
+ * around every single-launch forward pass (on the stream they run on);
+ * enable = 0 stops.  ssd_profile_read fills ms[c] = summed kernel time and
+ * launches[c] = launch count per class c = 0 QKV, 1 O-proj, 2 gate/up,
+ * 3 down, 4 LM head, 5 attention, 6 whole forward pass in one launch, and
  * bytes[c] = algorithmic HBM bytes of those launches (weights + activations
- * read + outputs written, KV read/written for attention); reset = 1 clears
- * the totals afterwards.  Arrays have 6 entries; any may be NULL.
- * Synchronizes the model's stream.
+ * read + outputs written, KV read/written for attention; class 6: the sum of
+ * classes 0-5 for that pass); reset = 1 clears the totals afterwards.
+ * Arrays have 7 entries; any may be NULL.  Synchronizes the model's stream.
  */
 ssd_status ssd_profile(ssd_model* model, int32_t enable);
 ssd_status ssd_profile_read(ssd_model* model, double* ms, int64_t* launches, double* bytes, int32_t reset);

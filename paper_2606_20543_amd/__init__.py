@@ -159,14 +159,15 @@ def ssd_profile(model, enable):
     _check(lib().ssd_profile(ctypes.c_void_p(model), int(enable)))
 
 
-PROFILE_CLASSES = ("qkv", "o_proj", "gate_up", "down", "lm_head", "attention")
+PROFILE_CLASSES = ("qkv", "o_proj", "gate_up", "down", "lm_head", "attention", "forward")
 
 
 def ssd_profile_read(model, reset=False):
-    """{class: (ms, launches, bytes)} for the six kernel classes."""
+    """{class: (ms, launches, bytes)} for the seven launch classes."""
     import numpy as np
-    ms = np.zeros(6, np.float64)
-    n = np.zeros(6, np.int64)
-    by = np.zeros(6, np.float64)
+    k = len(PROFILE_CLASSES)
+    ms = np.zeros(k, np.float64)
+    n = np.zeros(k, np.int64)
+    by = np.zeros(k, np.float64)
     _check(lib().ssd_profile_read(ctypes.c_void_p(model), _ptr(ms), _ptr(n), _ptr(by), int(reset)))
     return {c: (float(ms[i]), int(n[i]), float(by[i])) for i, c in enumerate(PROFILE_CLASSES)}

@@ -16,9 +16,15 @@ FLAGS = [
 ]
 
 
+# per-source extra flags: the persistent forward kernel keeps loop-invariant
+# address arithmetic where it is used (machine-level hoisting would keep it
+# live across the whole kernel and push registers into scratch memory)
+EXTRA = {"kernels_fwd.hip": ["-mllvm", "-disable-machine-licm"]}
+
+
 def _compile(src):
     obj = os.path.join(BUILD, os.path.basename(src) + ".o")
-    cmd = ["hipcc", *FLAGS, "-c", os.path.join(CSRC, src), "-o", obj]
+    cmd = ["hipcc", *FLAGS, *EXTRA.get(src, []), "-c", os.path.join(CSRC, src), "-o", obj]
     if src.endswith(".cpp"):
         cmd = ["hipcc", "-x", "hip", *FLAGS, "-c", os.path.join(CSRC, src), "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)

@@ -37,13 +37,13 @@ void attn_bf16_kernel(AttnKArgs a) {
   attn_unit<D, QPW>(a, blockIdx.x, sm_o, sm_m, sm_l, &is_last);
 }
 
-AttnPlan attn_plan(const Dims& dm, int B, int K, int max_ctx_now, int xcd) {
+AttnPlan attn_plan(const Dims& dm, int B, int K, int max_ctx_now, int xcd, int grid) {
   AttnPlan p;
   p.xcd = xcd;
   const int g = dm.Hq / dm.Hkv;
   p.rows = K * g;
   const int qt = (p.rows + 15) / 16;
-  p.qpw = qt >= 4 ? 2 : 1;
+  p.qpw = (qt >= 4 && grid == 0) ? 2 : 1;
   p.nqg = (qt + p.qpw - 1) / p.qpw;
   const long units = (long)B * dm.Hkv * p.nqg;
   const int ctx = max_ctx_now < 1 ? 1 : max_ctx_now;
@@ -52,7 +52,8 @@ AttnPlan attn_plan(const Dims& dm, int B, int K, int max_ctx_now, int xcd) {
     return ((per + AT_STEP - 1) / AT_STEP) * AT_STEP;
   };
   int best = 1;
-  if (units >= 256) {
+  const long slots = grid > 0 ? grid : 256;
+  if (units >= slots) {
     // many query groups: the chip is full, chunks only bound the per-workgroup stream
     int chunk = AT_STEP;
     while ((chunk < 16 * AT_STEP && units * ((ctx + chunk - 1) / chunk) > 1024) ||
@@ -64,7 +65,7 @@ AttnPlan attn_plan(const Dims& dm, int B, int K, int max_ctx_now, int xcd) {
     // workgroup, a split adds the partial publish and the merge (about
     // 1.6 us + 0.08 us per chunk); measured on MI355X with D = 128
     double best_t = 1e30;
-    for (int n = 1; n <= AT_MAX_CHUNKS && units * n <= 256; ++n) {
+    for (int n = 1; n <= AT_MAX_CHUNKS && (grid > 0 ? (long)xcd_grid((int)units, n, xcd) : units * n) <= slots; ++n) {
       const int ch = chunk_for(n);
       const int nn = (ctx + ch - 1) / ch;
       if (nn != n) continue;
@@ -86,13 +87,12 @@ size_t attn_partials_floats(const Dims& dm, const AttnPlan& p, int B) {
 
 template <int D, int QPW>
 static void launch_attn(const AttnKArgs& a, hipStream_t st) {
-  const int grid = a.nchunk == 1 ? xcd_grid(a.heads, a.nqg, a.xcd) : xcd_grid(a.groups, a.nchunk, a.xcd);
-  launch_timed(attn_bf16_kernel<D, QPW>, dim3(grid), dim3(AtShape<QPW>::THREADS), st, a);
+  launch_timed(attn_bf16_kernel<D, QPW>, dim3(attn_items(a)), dim3(AtShape<QPW>::THREADS), st, a);
 }
 
-void attention_bf16(const Dims& dm, const AttnPlan& p, int B, int K, const int* f, const void* q, size_t q_plane,
+AttnKArgs attn_args(const Dims& dm, const AttnPlan& p, int B, int K, const int* f, const void* q, size_t q_plane,
                     const void* kc, const void* vc, int Lmax, void* o, size_t o_plane, float* partials,
-                    unsigned* counters, hipStream_t st) {
+                    unsigned* counters) {
   AttnKArgs a;
   a.q = (const uint16_t*)q;
   a.kc = (const uint16_t*)kc;
@@ -119,6 +119,17 @@ void attention_bf16(const Dims& dm, const AttnPlan& p, int B, int K, const int* 
   a.nqg = p.nqg;
   a.xcd = p.xcd;
   a.scale_log2 = 1.4426950408889634f / sqrtf((float)dm.D);
+  return a;
+}
+
+int attn_items(const AttnKArgs& a) {
+  return a.nchunk == 1 ? xcd_grid(a.heads, a.nqg, a.xcd) : xcd_grid(a.groups, a.nchunk, a.xcd);
+}
+
+void attention_bf16(const Dims& dm, const AttnPlan& p, int B, int K, const int* f, const void* q, size_t q_plane,
+                    const void* kc, const void* vc, int Lmax, void* o, size_t o_plane, float* partials,
+                    unsigned* counters, hipStream_t st) {
+  const AttnKArgs a = attn_args(dm, p, B, K, f, q, q_plane, kc, vc, Lmax, o, o_plane, partials, counters);
   if (dm.D == 128) {
     if (p.qpw == 2) launch_attn<128, 2>(a, st);
     else launch_attn<128, 1>(a, st);

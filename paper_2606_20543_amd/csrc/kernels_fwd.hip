@@ -26,6 +26,7 @@ namespace {
 
 constexpr int FWD_THREADS = 256;
 constexpr int FWD_KCB = 16;  // k-blocks of 32 per GEMM item (one burst)
+constexpr int FWD_RMS_PARTS = 64;  // rms partial sums per token (d_model <= 4096)
 
 __device__ __forceinline__ unsigned ld_flag(const unsigned* p) {
   return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -79,24 +80,37 @@ struct FwdLds {
   using X = XStage<MT, FWD_KCB>;
   static constexpr int GEMM_BYTES = 2 * X::PL * 2 + (4 * X::MP + X::MP + 256) * 4;
   static constexpr int ATT_ROWS = 16;  // one query tile per workgroup
-  static constexpr int ATT_BYTES = (AtShape<1>::WAVES * ATT_ROWS * (D + 4) + 2 * AtShape<1>::WAVES * ATT_ROWS) * 4;
+  static constexpr int ATT_Q_OFF = (AtShape<1>::WAVES * ATT_ROWS * (D + 4) + 2 * AtShape<1>::WAVES * ATT_ROWS) * 4;
+  static constexpr int ATT_BYTES = ATT_Q_OFF + (D / 32) * 2 * 1024;  // + the query tiles
+  static_assert(ATT_Q_OFF % 16 == 0, "query stage 16-byte aligned");
   static constexpr int BYTES = GEMM_BYTES > ATT_BYTES ? GEMM_BYTES : ATT_BYTES;
 };
+
+// The phase table is read through the constant address space: the kernel
+// never writes it, so its fields come in through scalar loads (lgkmcnt).  A
+// generic pointer would make them vector loads, and every wait for one of
+// those would also wait for the workgroup's weight stream in flight.
+#if defined(__HIP_DEVICE_COMPILE__)
+typedef const __attribute__((address_space(4))) FwdPhase* PhaseTab;
+#else
+typedef const FwdPhase* PhaseTab;  // host pass: device code is parsed, not generated
+#endif
+__device__ __forceinline__ PhaseTab phase_tab(const FwdArgs& A) { return (PhaseTab)(uintptr_t)A.phases; }
 
 // Next GEMM item of this workgroup after item `it` of phase p (it < 0: none
 // in p), not looking past an attention phase (the prefetched weights are not
 // kept live across the attention code): (p2, it2), or p2 = -1.
 __device__ __forceinline__ void next_gemm_item(const FwdArgs& A, int p, int it, int& p2, int& it2) {
   const int G = gridDim.x;
-  if (p >= 0 && it >= 0 && A.phases[p].kind == FWD_GEMM && it + G < A.phases[p].g.items) {
+  const PhaseTab tab = phase_tab(A);
+  if (p >= 0 && it >= 0 && tab[p].kind == FWD_GEMM && it + G < tab[p].g.items) {
     p2 = p;
     it2 = it + G;
     return;
   }
   for (int q = p + 1; q < A.n_phases; ++q) {
-    const FwdPhase& ph = A.phases[q];
-    if (ph.kind != FWD_GEMM) break;
-    if ((int)blockIdx.x < ph.g.items) {
+    if (tab[q].kind != FWD_GEMM) break;
+    if ((int)blockIdx.x < tab[q].g.items) {
       p2 = q;
       it2 = blockIdx.x;
       return;
@@ -106,12 +120,13 @@ __device__ __forceinline__ void next_gemm_item(const FwdArgs& A, int p, int it, 
 }
 
 template <int MT>
-__device__ __forceinline__ void issue_weights(const FwdGemm& g, int it, int xcd, u32x4 (&ra)[1][FWD_KCB]) {
+__device__ __forceinline__ void issue_weights(PhaseTab tab, int p, int it, int xcd, u32x4 (&ra)[1][FWD_KCB]) {
+  const int S = tab[p].g.S, n_fb = tab[p].g.n_fb;
   int fb, s;
-  xcd_unmap(it, g.S, xcd, fb, s);
-  if (fb >= g.n_fb) fb = g.n_fb - 1;  // idle slot: any valid tile (never used)
+  xcd_unmap(it, S, xcd, fb, s);
+  if (fb >= n_fb) fb = n_fb - 1;  // idle slot: any valid tile (never used)
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  load_a<1, FWD_KCB>(ra, (const u32x4*)g.W, g.KB, fb * 4 + w, g.N, s * FWD_KCB, lane);
+  load_a<1, FWD_KCB>(ra, (const u32x4*)tab[p].g.W, tab[p].g.KB, fb * 4 + w, tab[p].g.N, s * FWD_KCB, lane);
 }
 
 // One GEMM work item (feature block fb, K-split s).  The weights are in ra
@@ -133,16 +148,19 @@ __device__ __forceinline__ void gemm_item(const FwdArgs& A, const FwdGemm& g, in
 
   // inputs of this K-slice: the producer units covering [s*KC, (s+1)*KC) (x dep_scale)
   const int KC = FWD_KCB * 32;
-  const int u0 = (s * KC * g.dep_scale) / g.dep_width, u1 = ((s + 1) * KC * g.dep_scale + g.dep_width - 1) / g.dep_width;
+  int u0 = 0, u1 = g.dep_units;
+  if (g.dep_units == 0) {
+    u0 = (s * KC * g.dep_scale) / g.dep_width;
+    u1 = ((s + 1) * KC * g.dep_scale + g.dep_width - 1) / g.dep_width;
+  }
   EpiOps<1, MT> op;
   epi_block_starts<1, MT>(e, g.M, 0, lane, op);
   if (!wg_wait(g.dep, u0, u1, nullptr, 0, 0, nullptr, 0, 0, val, A, sflag)) {
     last = false;
     return;
   }
-  u32x4 rx[2][X::PASSES];
-  load_x<MT, FWD_KCB, X::PASSES, CoherentMem>(rx, g.in, g.in_plane, g.ld_in, g.M, s * KC);
-  store_x<MT, FWD_KCB>(rx, xs);
+  load_x_lds<MT, FWD_KCB, CPOL_SC1>(xs, g.in, g.in_plane, g.ld_in, g.M, s * KC);
+  __builtin_amdgcn_s_waitcnt(0);  // this wave's LDS copies (and its weight loads) have landed
   lds_barrier();
   floatx4 acc[1][MT];
 #pragma unroll
@@ -150,18 +168,29 @@ __device__ __forceinline__ void gemm_item(const FwdArgs& A, const FwdGemm& g, in
   compute_chunk<MT, 1, FWD_KCB>(acc, ra, xs, lane);
 
   const size_t frag = (size_t)MT * 64 * 4;
-  float* P = g.part + ((size_t)fb * 4 + w) * frag;
+  const size_t P = ((size_t)fb * 4 + w) * frag;  // this wave's fragment (floats from g.part)
   const size_t split_stride = (size_t)g.n_fb * 4 * frag;
   if (g.S > 1) {
+    // partials stay in this XCD's L2; the reading side skips L1, which may
+    // still hold the lines from an earlier layer's reduction
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt) *(floatx4*)(P + (size_t)s * split_stride + (mt * 64 + lane) * 4) = acc[0][mt];
+    for (int mt = 0; mt < MT; ++mt) {
+      const floatx4 v = acc[0][mt];
+      XcdMem::stf4(g.part, (P + (size_t)s * split_stride + (mt * 64 + lane) * 4) * 4,
+                   make_float4(v[0], v[1], v[2], v[3]));
+    }
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
     if (threadIdx.x == 0) {
       if (!A.xcd) __threadfence();
       const unsigned prev = atomicAdd(&g.counters[fb], 1u);
-      *sflag = prev == (unsigned)(g.S - 1);
-      if (*sflag && !A.xcd) __threadfence();
+      const bool lst = prev == (unsigned)(g.S - 1);
+      if (lst) {
+        // every split has arrived: re-arm the counter for the next pass
+        __hip_atomic_store(&g.counters[fb], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (!A.xcd) __threadfence();
+      }
+      *sflag = lst;
     }
     __syncthreads();
     last = *sflag != 0;
@@ -172,34 +201,35 @@ __device__ __forceinline__ void gemm_item(const FwdArgs& A, const FwdGemm& g, in
   }
   // epilogue: the rms partial sums must be complete
   if (g.rms_dep && !wg_wait(g.rms_dep, 0, g.rms_units, nullptr, 0, 0, nullptr, 0, 0, A.epoch_base + (unsigned)g.rms_layer, A,
-                            sflag)) {
-    if (threadIdx.x == 0) g.counters[fb] = 0u;
+                            sflag))
     return;
-  }
   epi_load<1, MT, CoherentMem>(e, nb0, g.N, g.M, 0, lane, op);
-  float rv[RmsPre<X::MP>::RQ];
-  rms_issue<X::MP, CoherentMem>(e, g.in, g.M, 0, rv);
+  float rv[RmsPre<X::MP, FWD_RMS_PARTS>::RQ];
+  rms_issue<X::MP, CoherentMem, FWD_RMS_PARTS>(e, g.in, g.M, 0, rv);
   if (g.S > 1) {
-    const float* Pl = P + lane * 4;
+    const size_t Pl = P + lane * 4;
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) acc[0][mt] = floatx4{0.f, 0.f, 0.f, 0.f};
-    for (int s0 = 0; s0 < g.S; s0 += 8) {
-      floatx4 pv[8][MT];
+    for (int s0 = 0; s0 < g.S; s0 += 4) {
+      floatx4 pv[4][MT];
 #pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const float* Ps = Pl + (size_t)min(s0 + j, g.S - 1) * split_stride;
+      for (int j = 0; j < 4; ++j) {
+        const size_t Ps = Pl + (size_t)min(s0 + j, g.S - 1) * split_stride;
 #pragma unroll
-        for (int mt = 0; mt < MT; ++mt) pv[j][mt] = *(const floatx4*)(Ps + mt * 64 * 4);
+        for (int mt = 0; mt < MT; ++mt) {
+          const float4 v = XcdMem::ldf4(g.part, (Ps + mt * 64 * 4) * 4);
+          pv[j][mt] = floatx4{v.x, v.y, v.z, v.w};
+        }
       }
 #pragma unroll
-      for (int j = 0; j < 8; ++j) {
+      for (int j = 0; j < 4; ++j) {
         const float m = (s0 + j < g.S) ? 1.f : 0.f;
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt) acc[0][mt] += pv[j][mt] * m;
       }
     }
   }
-  rms_finish<X::MP>(e, rv, rms_red, rscale);
+  rms_finish<X::MP, FWD_RMS_PARTS>(e, rv, rms_red, rscale);
   lds_barrier();
   float sq[MT];
 #pragma unroll
@@ -224,7 +254,6 @@ __device__ __forceinline__ void gemm_item(const FwdArgs& A, const FwdGemm& g, in
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
   if (threadIdx.x == 0) {
-    if (g.S > 1) g.counters[fb] = 0u;
     if (g.out_flags)
       __hip_atomic_store(&g.out_flags[fb], A.epoch_base + (unsigned)g.out_layer, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
@@ -234,25 +263,28 @@ template <int MT, int D>
 __global__ __launch_bounds__(FWD_THREADS) __attribute__((amdgpu_waves_per_eu(2, 2))) void fwd_kernel(FwdArgs A) {
   __shared__ __align__(16) unsigned char smem[FwdLds<MT, D>::BYTES];
   __shared__ int sflag;
+  const PhaseTab tab = phase_tab(A);
+  if (A.probe && threadIdx.x == 0)
+    A.probe[blockIdx.x] = (int)(__builtin_amdgcn_s_getreg(20 | (0 << 6) | ((4 - 1) << 11)) & 0xF);  // XCC_ID
   u32x4 ra[1][FWD_KCB];
   int pre_p = -1, pre_it = -1;  // the item whose weights ra holds (or is loading)
   {
     int p2, it2;
     next_gemm_item(A, -1, 0, p2, it2);
     if (p2 >= 0) {
-      issue_weights<MT>(A.phases[p2].g, it2, A.xcd, ra);
+      issue_weights<MT>(tab, p2, it2, A.xcd, ra);
       pre_p = p2;
       pre_it = it2;
     }
   }
   for (int p = 0; p < A.n_phases; ++p) {
-    const FwdPhase& ph = A.phases[p];
+    const FwdPhase ph = tab[p];  // by value: the fields live in scalar registers
     if (ph.kind == FWD_GEMM) {
       const FwdGemm& g = ph.g;
       for (int it = blockIdx.x; it < g.items; it += gridDim.x) {
         int fb, s;
         xcd_unmap(it, g.S, A.xcd, fb, s);
-        if (!(pre_p == p && pre_it == it)) issue_weights<MT>(g, it, A.xcd, ra);
+        if (!(pre_p == p && pre_it == it)) issue_weights<MT>(tab, p, it, A.xcd, ra);
         pre_p = -1;
         bool last = false;
         if (fb < g.n_fb) gemm_item<MT>(A, g, it, ra, smem, &sflag, last);
@@ -262,7 +294,7 @@ __global__ __launch_bounds__(FWD_THREADS) __attribute__((amdgpu_waves_per_eu(2, 
         int p2, it2;
         next_gemm_item(A, p, it, p2, it2);
         if (p2 >= 0) {
-          issue_weights<MT>(A.phases[p2].g, it2, A.xcd, ra);
+          issue_weights<MT>(tab, p2, it2, A.xcd, ra);
           pre_p = p2;
           pre_it = it2;
         }
@@ -292,7 +324,8 @@ __global__ __launch_bounds__(FWD_THREADS) __attribute__((amdgpu_waves_per_eu(2, 
         AttnKArgs a = A.att;
         a.kc = (const uint16_t*)at.kc;
         a.vc = (const uint16_t*)at.vc;
-        const int done = attn_unit<D, 1, CoherentMem, false>(a, it, sm_o, sm_m, sm_l, &sflag);
+        const int done = attn_unit<D, 1, CoherentMem, false, XcdMem, true>(
+            a, it, sm_o, sm_m, sm_l, &sflag, (uint16_t*)(smem + FwdLds<MT, D>::ATT_Q_OFF));
         if (done >= 0) {
           __builtin_amdgcn_s_waitcnt(0);
           __syncthreads();
@@ -307,7 +340,7 @@ __global__ __launch_bounds__(FWD_THREADS) __attribute__((amdgpu_waves_per_eu(2, 
       int p2, it2;
       next_gemm_item(A, p, -1, p2, it2);
       if (p2 >= 0) {
-        issue_weights<MT>(A.phases[p2].g, it2, A.xcd, ra);
+        issue_weights<MT>(tab, p2, it2, A.xcd, ra);
         pre_p = p2;
         pre_it = it2;
       } else {
@@ -325,7 +358,17 @@ __global__ __launch_bounds__(FWD_THREADS) __attribute__((amdgpu_waves_per_eu(2, 
 template <int MT, int D>
 static hipError_t launch_fwd(const FwdArgs& a, int grid, hipStream_t st) {
   void* args[] = {(void*)&a};
-  return hipLaunchCooperativeKernel((const void*)fwd_kernel<MT, D>, dim3(grid), dim3(FWD_THREADS), args, 0, st);
+  // a cooperative launch takes no dispatch events: a timed launch is bracketed
+  // by event records (negligible next to a whole forward pass)
+  hipEvent_t t0 = nullptr, t1 = nullptr;
+  if (g_launch_timer) {
+    g_launch_timer->next(t0, t1);
+    hipError_t e = hipEventRecord(t0, st);
+    if (e != hipSuccess) return e;
+  }
+  hipError_t e = hipLaunchCooperativeKernel((const void*)fwd_kernel<MT, D>, dim3(grid), dim3(FWD_THREADS), args, 0, st);
+  if (e == hipSuccess && t1) e = hipEventRecord(t1, st);
+  return e;
 }
 
 hipError_t fwd_persistent(const FwdArgs& a, int MT, int D, int grid, hipStream_t st) {

@@ -7,7 +7,9 @@
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
+#include <map>
 #include <string>
+#include <utility>
 #include <vector>
 
 #include "ssd_internal.h"
@@ -122,8 +124,9 @@ struct Prof : LaunchTimer {
     double bytes;
   };
   std::vector<Mark> marks;
-  double ms[6] = {0, 0, 0, 0, 0, 0}, bytes[6] = {0, 0, 0, 0, 0, 0};
-  int64_t n[6] = {0, 0, 0, 0, 0, 0};
+  static constexpr int NCLS = 7;  // qkv, o, gate_up, down, lm_head, attention, persistent forward
+  double ms[NCLS] = {}, bytes[NCLS] = {};
+  int64_t n[NCLS] = {};
   int cur_cls = 0;
   double cur_bytes = 0;
   hipEvent_t get() {
@@ -190,6 +193,10 @@ struct ssd_model {
   ssd_session* dec = nullptr;  // cached decode workspace
   int dec_B = 0, dec_P = 0, dec_L = 0, dec_K = 0;
   int xcd = 0;  // XCD count when workgroups are dispatched round-robin over XCDs (see xcd_grid), else 0
+  // persistent forward pass (index MT - 1: one or two 16-token tiles): grid
+  // size (0: not available) and its XCD mapping (0: fenced reductions)
+  int fwd_grid[2] = {0, 0};
+  int fwd_xcd[2] = {0, 0};
   Prof prof;
 };
 
@@ -232,6 +239,20 @@ struct ssd_session {
   size_t apart_cap;
   unsigned* acnt;
   size_t acnt_cap;
+  // persistent forward pass state (blocks of at most FWD_MAX_M tokens)
+  struct Fwd {
+    bool on = false;
+    unsigned* flags = nullptr;  // all unit flags (zeroed at creation)
+    size_t n_flags = 0;
+    unsigned *f_qkv, *f_att, *f_o, *f_gu, *f_dn;
+    int att_cap = 0;            // attention flags
+    unsigned* abort_flag = nullptr;
+    float* part[5];             // split-K partials per projection kind (qkv, o, gate_up, down, lm)
+    unsigned* cnt[5];
+    unsigned epoch = 0;
+    unsigned abort_host = 0;    // copy of *abort_flag taken at the last synchronization
+    std::map<std::pair<int, int>, std::pair<std::vector<FwdPhase>, FwdPhase*>> tables;  // (K, lm_mode)
+  } fw;
   // decode image buffers
   int* img = nullptr;    // [B][H*W] working grid (absolute ids)
   int img_cap = 0;
@@ -241,6 +262,228 @@ struct ssd_session {
 namespace {
 
 size_t esize(const Dims& dm) { return dm.bf16 ? 2 : 4; }
+
+// ---------------- persistent forward pass ----------------
+// Blocks of up to FWD_MAX_M tokens (two 16-token tiles) run the whole backbone
+// in one cooperative launch (kernels_fwd.hip); larger token counts use one
+// launch per projection and attention.
+constexpr int FWD_MAX_M = 32;
+constexpr int FWD_MAX_GRID = 512;
+constexpr int FWD_KSLICE = 512;  // input features per GEMM work item
+constexpr int FWD_FB = 64;       // output features per GEMM work item
+constexpr unsigned FWD_SPIN_LIMIT = 1u << 21;  // polls before a wait gives up (seconds)
+
+// shapes whose projections all split into 512-wide K slices and 64-wide feature blocks
+bool fwd_shape_ok(const Dims& dm) {
+  return dm.bf16 && (dm.D == 64 || dm.D == 128) && dm.d % FWD_KSLICE == 0 && (dm.Hq * dm.D) % FWD_KSLICE == 0 &&
+         dm.dff % FWD_KSLICE == 0 && dm.Vimg % FWD_FB == 0 && dm.d / FWD_FB <= 64;  // rms parts of the kernel
+}
+
+// split-K partial floats of one projection kind for up to two token tiles
+size_t fwd_part_floats(int N, int Kd) { return (size_t)(Kd / FWD_KSLICE) * (N / FWD_FB) * 4 * (2 * 64 * 4); }
+
+// attention flags a session needs: B * Hkv * query groups of the largest persistent block
+int fwd_att_units(const Dims& dm, int B, int Kmax) {
+  const int K = std::min(Kmax, FWD_MAX_M / B);
+  return B * dm.Hkv * ((K * (dm.Hq / dm.Hkv) + 15) / 16);
+}
+
+// Grid of the persistent kernel for each tile count and the XCD mapping of a
+// cooperative launch (workgroup w on XCD w % X, checked with the kernel's
+// own probe), or grid 0 where the kernel cannot run.  The single-launch pass
+// is used when SSD_FORWARD=persistent at model creation; otherwise every pass
+// runs as one launch per projection and attention.
+void setup_fwd(ssd_model* m) {
+  const char* env = std::getenv("SSD_FORWARD");
+  if (!env || std::strcmp(env, "persistent") != 0) return;
+  if (!fwd_shape_ok(m->dm)) return;
+  for (int mt = 1; mt <= 2; ++mt) {
+    int g = std::min(fwd_max_grid(mt, m->dm.D), FWD_MAX_GRID);
+    g -= g % 8;
+    if (g < 64) continue;
+    int* d = nullptr;
+    if (hipMalloc(&d, (size_t)g * sizeof(int)) != hipSuccess) {
+      (void)hipGetLastError();
+      continue;
+    }
+    FwdArgs a{};
+    a.n_phases = 0;
+    a.probe = d;
+    std::vector<int> h(g, -1);
+    bool ok = fwd_persistent(a, mt, m->dm.D, g, m->stream) == hipSuccess &&
+              hipMemcpyAsync(h.data(), d, (size_t)g * sizeof(int), hipMemcpyDeviceToHost, m->stream) == hipSuccess &&
+              hipStreamSynchronize(m->stream) == hipSuccess;
+    (void)hipFree(d);
+    if (!ok) {
+      (void)hipGetLastError();
+      continue;
+    }
+    bool mapped = m->xcd > 0;
+    for (int w = 0; w < g && mapped; ++w) mapped = h[w] == w % m->xcd;
+    m->fwd_grid[mt - 1] = g;
+    m->fwd_xcd[mt - 1] = mapped ? m->xcd : 0;
+  }
+}
+
+// The abort flag is read where the host synchronizes anyway: fetch enqueues
+// the copy, check (after the stream has drained) turns a set flag into an error.
+void fwd_abort_fetch(ssd_session* s) {
+  if (s->fw.on)
+    HIPCHK(hipMemcpyAsync(&s->fw.abort_host, s->fw.abort_flag, sizeof(unsigned), hipMemcpyDeviceToHost, s->stream));
+}
+void fwd_abort_check(ssd_session* s) {
+  if (s->fw.on && s->fw.abort_host)
+    throw HipError{hipErrorLaunchTimeOut, "persistent forward pass abandoned a dependency wait"};
+}
+
+FwdGemm fwd_gemm(const void* W, int N, int Kd, const void* in, size_t in_plane, int ld_in, int M, int X, float* part,
+                 unsigned* cnt, unsigned* out_flags, int out_layer, const EpiArgs& e) {
+  FwdGemm g{};
+  g.W = W;
+  g.N = N;
+  g.K = Kd;
+  g.KB = Kd / 32;
+  g.n_fb = N / FWD_FB;
+  g.S = Kd / FWD_KSLICE;
+  g.items = xcd_grid(g.n_fb, g.S, X);
+  g.M = M;
+  g.in = (const uint16_t*)in;
+  g.in_plane = in_plane;
+  g.ld_in = ld_in;
+  g.dep_width = FWD_FB;
+  g.dep_scale = 1;
+  g.part = part;
+  g.counters = cnt;
+  g.out_flags = out_flags;
+  g.out_layer = out_layer;
+  g.epi = e;
+  return g;
+}
+
+// Phase table of one (K, lm_mode): per layer QKV, attention, O, gate/up, down;
+// then the output layer.  Flag values are layer + 1 (plus the pass's epoch base).
+const FwdPhase* fwd_table(ssd_session* s, int K, int lm_mode, int X, const EpiArgs& base, int att_groups) {
+  auto key = std::make_pair(K, lm_mode);
+  auto it = s->fw.tables.find(key);
+  if (it != s->fw.tables.end()) return it->second.second;
+  const Dims& dm = s->dm;
+  ssd_model* m = s->m;
+  const int B = s->B, M = B * K, d = dm.d, D = dm.D;
+  const int Nqkv = (dm.Hq + 2 * dm.Hkv) * D;
+  const int nfb_d = d / FWD_FB;
+  const size_t es = esize(dm);
+  std::vector<FwdPhase> ph;
+  for (int l = 0; l < dm.L; ++l) {
+    const LayerW& W = m->layers[l];
+    char* kc = (char*)s->kc + (size_t)l * s->kv_layer_elems * es;
+    char* vc = (char*)s->vc + (size_t)l * s->kv_layer_elems * es;
+    FwdPhase p{};
+    // QKV projection (+ rotary, KV write): input xn of the previous layer's down projection
+    EpiArgs e = base;
+    e.kind = EPI_QKV;
+    e.ssq = s->ssq;
+    e.ssq_parts = l == 0 ? 1 : nfb_d;
+    e.q = s->q;
+    e.kc = kc;
+    e.vc = vc;
+    p.kind = FWD_GEMM;
+    p.g = fwd_gemm(W.wqkv, Nqkv, d, s->xn, s->xn_plane, d, M, X, s->fw.part[0], s->fw.cnt[0], s->fw.f_qkv, l + 1, e);
+    if (l > 0) {
+      p.g.dep = s->fw.f_dn;
+      p.g.dep_layer = l;
+      p.g.rms_dep = s->fw.f_dn;
+      p.g.rms_units = nfb_d;
+      p.g.rms_layer = l;
+    }
+    ph.push_back(p);
+    // attention over the cache of layer l
+    p = FwdPhase{};
+    p.kind = FWD_ATTN;
+    p.a.dep = s->fw.f_qkv;
+    p.a.dep_width = FWD_FB;
+    p.a.qN = dm.Hq * D;
+    p.a.kN = dm.Hkv * D;
+    p.a.layer = l + 1;
+    p.a.kc = kc;
+    p.a.vc = vc;
+    p.a.out_flags = s->fw.f_att;
+    ph.push_back(p);
+    // O projection + residual: needs every attention output
+    e = base;
+    e.kind = EPI_RESID;
+    e.ssq = nullptr;
+    e.gnext = W.g2;
+    e.ld = d;
+    p = FwdPhase{};
+    p.kind = FWD_GEMM;
+    p.g = fwd_gemm(W.wo, d, dm.Hq * D, s->o, s->o_plane, dm.Hq * D, M, X, s->fw.part[1], s->fw.cnt[1], s->fw.f_o, l + 1,
+                   e);
+    p.g.dep = s->fw.f_att;
+    p.g.dep_units = att_groups;
+    p.g.dep_layer = l + 1;
+    ph.push_back(p);
+    // gate/up + SwiGLU
+    e = base;
+    e.kind = EPI_SWIGLU;
+    e.ssq = s->ssq;
+    e.ssq_parts = nfb_d;
+    e.h = s->h;
+    e.ld = dm.dff;
+    p = FwdPhase{};
+    p.kind = FWD_GEMM;
+    p.g = fwd_gemm(W.w13, 2 * dm.dff, d, s->xn, s->xn_plane, d, M, X, s->fw.part[2], s->fw.cnt[2], s->fw.f_gu, l + 1,
+                   e);
+    p.g.dep = s->fw.f_o;
+    p.g.dep_layer = l + 1;
+    p.g.rms_dep = s->fw.f_o;
+    p.g.rms_units = nfb_d;
+    p.g.rms_layer = l + 1;
+    ph.push_back(p);
+    // down projection + residual: h feature j comes from gate/up block j / 32
+    e = base;
+    e.kind = EPI_RESID;
+    e.ssq = nullptr;
+    e.gnext = (l + 1 < dm.L) ? m->layers[l + 1].g1 : m->gf;
+    e.ld = d;
+    p = FwdPhase{};
+    p.kind = FWD_GEMM;
+    p.g = fwd_gemm(W.w2, d, dm.dff, s->h, s->h_plane, dm.dff, M, X, s->fw.part[3], s->fw.cnt[3], s->fw.f_dn, l + 1, e);
+    p.g.dep = s->fw.f_gu;
+    p.g.dep_scale = 2;
+    p.g.dep_layer = l + 1;
+    ph.push_back(p);
+  }
+  // output layer over all rows (lm_mode 0) or the last row of each sequence
+  EpiArgs e = base;
+  e.kind = EPI_LOGITS;
+  e.ssq = s->ssq;
+  e.ssq_parts = nfb_d;
+  e.logits = s->logits;
+  e.ld = dm.Vimg;
+  FwdPhase p{};
+  p.kind = FWD_GEMM;
+  if (lm_mode == 0) {
+    p.g = fwd_gemm(m->wlm, dm.Vimg, d, s->xn, s->xn_plane, d, M, X, s->fw.part[4], s->fw.cnt[4], nullptr, 0, e);
+  } else {
+    e.ssq_off = K - 1;
+    e.ssq_step = K;
+    p.g = fwd_gemm(m->wlm, dm.Vimg, d, (const uint16_t*)s->xn + (size_t)(K - 1) * d, s->xn_plane, K * d, B, X,
+                   s->fw.part[4], s->fw.cnt[4], nullptr, 0, e);
+  }
+  p.g.dep = s->fw.f_dn;
+  p.g.dep_layer = dm.L;
+  p.g.rms_dep = s->fw.f_dn;
+  p.g.rms_units = nfb_d;
+  p.g.rms_layer = dm.L;
+  ph.push_back(p);
+  FwdPhase* dev = s->mem.get<FwdPhase>(ph.size());
+  auto& slot = s->fw.tables[key];
+  slot.first = std::move(ph);
+  slot.second = dev;
+  HIPCHK(hipMemcpyAsync(dev, slot.first.data(), slot.first.size() * sizeof(FwdPhase), hipMemcpyHostToDevice,
+                        s->stream));
+  return dev;
+}
 
 // ---------------- forward pass ----------------
 // lm_mode: 0 = logits for all B*K rows; 1 = logits for the last row of each sequence only
@@ -309,6 +552,39 @@ void run_forward(ssd_session* s, int K, int lm_mode) {
     const double o_bytes = (double)d * dm.Hq * D * es + (double)M * dm.Hq * D * A + (double)M * d * (8 + A);
     const double gu_bytes = 2.0 * dm.dff * d * es + (double)M * d * A + (double)M * dm.dff * A;
     const double dn_bytes = (double)d * dm.dff * es + (double)M * dm.dff * A + (double)M * d * (8 + A);
+    const int mt = M <= 16 ? 1 : 2;
+    if (s->fw.on && M <= FWD_MAX_M && m->fwd_grid[mt - 1] > 0) {
+      const int G = m->fwd_grid[mt - 1], XF = m->fwd_xcd[mt - 1];
+      AttnPlan pf = attn_plan(dm, B, K, max_ctx_now, XF, G);
+      const int groups = B * dm.Hkv * pf.nqg;
+      need(attn_partials_floats(dm, pf, B) <= s->apart_cap && (size_t)groups <= s->acnt_cap && groups <= s->fw.att_cap,
+           "attention plan exceeds its workspace");
+      need(d / FWD_FB <= s->ssq_parts_cap, "rms partial sums exceed their buffer");
+      const FwdPhase* tab = fwd_table(s, K, lm_mode, XF, base, groups);
+      FwdArgs a{};
+      a.phases = tab;
+      a.n_phases = 5 * dm.L + 1;
+      a.xcd = XF;
+      a.abort_flag = s->fw.abort_flag;
+      a.spin_limit = FWD_SPIN_LIMIT;
+      // flag values of this pass lie above every value an earlier pass stored;
+      // before they would wrap, the flags restart from zero
+      if ((uint64_t)(s->fw.epoch + 2) * (dm.L + 1) >= (1ull << 32)) {
+        fill_u32(s->fw.flags, s->fw.n_flags, 0u, st);
+        s->fw.epoch = 0;
+      }
+      ++s->fw.epoch;
+      a.epoch_base = s->fw.epoch * (unsigned)(dm.L + 1);
+      a.att = attn_args(dm, pf, B, K, s->d_f, s->q, s->q_plane, nullptr, nullptr, s->Lmax, s->o, s->o_plane, s->apart,
+                        s->acnt);
+      a.att_items = attn_items(a.att);
+      const int rows_lm = lm_mode == 0 ? M : B;
+      const double lm_bytes = (double)dm.Vimg * d * es + (double)rows_lm * d * A + (double)rows_lm * dm.Vimg * 4;
+      const double fwd_bytes = dm.L * (qkv_bytes + attn_bytes + o_bytes + gu_bytes + dn_bytes) + lm_bytes;
+      m->prof.run(6, fwd_bytes, st, [&] { HIPCHK(fwd_persistent(a, mt, D, G, st)); });
+      HIPCHK(hipGetLastError());
+      return;
+    }
     for (int l = 0; l < dm.L; ++l) {
       const LayerW& W = m->layers[l];
       char* kc = (char*)s->kc + (size_t)l * s->kv_layer_elems * es;
@@ -464,8 +740,8 @@ int detect_xcd(hipStream_t st) {
 }
 
 // workspace sizes for a session that runs blocks of up to Kmax tokens and a prefill of P
-void size_workspaces(const Dims& dm, int B, int P, int Kmax, int Lmax, size_t& gpart, size_t& gcnt, size_t& apart,
-                     size_t& acnt, int& ssq_parts_max) {
+void size_workspaces(const Dims& dm, const ssd_model* m, int B, int P, int Kmax, int Lmax, size_t& gpart, size_t& gcnt,
+                     size_t& apart, size_t& acnt, int& ssq_parts_max) {
   gpart = 0;
   gcnt = 0;
   apart = 0;
@@ -497,6 +773,22 @@ void size_workspaces(const Dims& dm, int B, int P, int Kmax, int Lmax, size_t& g
     apart = std::max(apart, attn_partials_floats(dm, pa, B));
     acnt = std::max(acnt, (size_t)B * dm.Hkv * pa.nqg);
   }
+  // the persistent forward pass: its own attention plans and one rms part per 64 features
+  for (int mt = 1; mt <= 2; ++mt) {
+    const int G = m->fwd_grid[mt - 1];
+    if (G == 0) continue;
+    ssq_parts_max = std::max(ssq_parts_max, dm.d / FWD_FB);
+    for (int K : Ks) {
+      if ((long)B * K > 16 * mt || (long)B * K <= 16 * (mt - 1)) continue;
+      for (int X : {0, m->fwd_xcd[mt - 1]}) {
+        for (int ctx = 1; ctx <= Lmax; ++ctx) {
+          AttnPlan pc = attn_plan(dm, B, K, ctx, X, G);
+          apart = std::max(apart, attn_partials_floats(dm, pc, B));
+          acnt = std::max(acnt, (size_t)B * dm.Hkv * pc.nqg);
+        }
+      }
+    }
+  }
 }
 
 ssd_status create_session(ssd_model* m, int B, int P, int Lmax_req, int Kmax, ssd_session** out) {
@@ -516,7 +808,7 @@ ssd_status create_session(ssd_model* m, int B, int P, int Lmax_req, int Kmax, ss
   try {
     size_t gpart, gcnt, apart, acnt;
     int ssq_parts;
-    size_workspaces(dm, B, P, Kmax, s->Lmax, gpart, gcnt, apart, acnt, ssq_parts);
+    size_workspaces(dm, m, B, P, Kmax, s->Lmax, gpart, gcnt, apart, acnt, ssq_parts);
     const size_t M = s->Mmax;
     s->d_f = s->mem.get<int>(B);
     s->tok = s->mem.get<int>(M);
@@ -556,6 +848,44 @@ ssd_status create_session(ssd_model* m, int B, int P, int Lmax_req, int Kmax, ss
     s->acnt_cap = acnt;
     s->acnt = s->mem.get<unsigned>(acnt);
     hipStream_t st = s->stream;
+    // the persistent kernel addresses activations and caches through buffer
+    // resources: every array must stay below 2 GiB
+    const size_t lim = (size_t)1 << 31;
+    const bool fits = s->kv_layer_elems * es < lim && M * dm.d * 4 < lim && qcap * 4 < lim &&
+                      M * dm.Hq * dm.D * 4 < lim && M * dm.dff * 4 < lim && M * dm.Vimg * 4 < lim &&
+                      (size_t)ssq_parts * M * 4 < lim;
+    if (dm.bf16 && (m->fwd_grid[0] > 0 || m->fwd_grid[1] > 0) && B <= FWD_MAX_M && fits) {
+      auto& fw = s->fw;
+      const int Nqkv = (dm.Hq + 2 * dm.Hkv) * dm.D;
+      const int nq = Nqkv / FWD_FB, nd = dm.d / FWD_FB, ng = 2 * dm.dff / FWD_FB;
+      fw.att_cap = fwd_att_units(dm, B, Kmax);
+      const int n_cnt[5] = {nq, nd, ng, nd, dm.Vimg / FWD_FB};
+      fw.n_flags = (size_t)nq + fw.att_cap + nd + ng + nd + 1;
+      for (int c : n_cnt) fw.n_flags += c;
+      fw.flags = s->mem.get<unsigned>(fw.n_flags);
+      unsigned* f = fw.flags;
+      fw.f_qkv = f;
+      f += nq;
+      fw.f_att = f;
+      f += fw.att_cap;
+      fw.f_o = f;
+      f += nd;
+      fw.f_gu = f;
+      f += ng;
+      fw.f_dn = f;
+      f += nd;
+      fw.abort_flag = f;
+      f += 1;
+      // split counters live in the same zeroed block (they re-arm themselves)
+      for (int k = 0; k < 5; ++k) {
+        fw.cnt[k] = f;
+        f += n_cnt[k];
+      }
+      const int NK[5][2] = {{Nqkv, dm.d}, {dm.d, dm.Hq * dm.D}, {2 * dm.dff, dm.d}, {dm.d, dm.dff}, {dm.Vimg, dm.d}};
+      for (int k = 0; k < 5; ++k) fw.part[k] = s->mem.get<float>(fwd_part_floats(NK[k][0], NK[k][1]));
+      fill_u32(fw.flags, fw.n_flags, 0u, st);
+      fw.on = true;
+    }
     // zero state that kernels read before writing (KV slots beyond the context are multiplied by 0)
     fill_u32((unsigned*)s->kc, s->kv_layer_elems * dm.L * es / 4, 0u, st);
     fill_u32((unsigned*)s->vc, s->kv_layer_elems * dm.L * es / 4, 0u, st);
@@ -719,7 +1049,10 @@ ssd_status ssd_init_model(const ssd_model_config* cfg, const void* weights, void
     m->gf = gain(off);
     off += d;
     m->wlm = pack(off + (size_t)dm.img_lo * d, dm.Vimg, d, d_map_id);
-    if (dm.bf16) m->xcd = detect_xcd(st);
+    if (dm.bf16) {
+      m->xcd = detect_xcd(st);
+      setup_fwd(m);
+    }
     off += (size_t)dm.V * d;
     if ((int64_t)off != numel_of(*cfg)) throw HipError{hipErrorInvalidValue, "layout size mismatch"};
     HIPCHK(hipStreamSynchronize(st));
@@ -774,7 +1107,9 @@ ssd_status ssd_prefill(ssd_model* m, int32_t B, int32_t P, const int32_t* prefix
   try {
     HIPCHK(hipMemcpyAsync(s->tok, host.data(), host.size() * 4, hipMemcpyHostToDevice, s->stream));
     prefill_pass(s);
+    fwd_abort_fetch(s);
     HIPCHK(hipStreamSynchronize(s->stream));
+    fwd_abort_check(s);
   } catch (HipError& e) {
     delete s;
     m->poisoned = true;
@@ -804,7 +1139,7 @@ ssd_status ssd_profile_read(ssd_model* m, double* ms, int64_t* launches, double*
   } catch (HipError& e) {
     return fail(SSD_E_DEVICE, "%s: %s", e.what, hipGetErrorString(e.e));
   }
-  for (int c = 0; c < 6; ++c) {
+  for (int c = 0; c < Prof::NCLS; ++c) {
     if (ms) ms[c] = m->prof.ms[c];
     if (launches) launches[c] = m->prof.n[c];
     if (bytes) bytes[c] = m->prof.bytes[c];
@@ -904,12 +1239,16 @@ ssd_status ssd_verify_step(ssd_session* s, int32_t K, int32_t* tokens, const flo
       if (accept_count) HIPCHK(hipMemcpyAsync(accept_count, s->cnt, (size_t)B * 4, hipMemcpyDefault, st));
       if (prm->truncate) {
         HIPCHK(hipMemcpyAsync(s->f.data(), s->d_f, (size_t)B * 4, hipMemcpyDeviceToHost, st));
+        fwd_abort_fetch(s);
         HIPCHK(hipStreamSynchronize(st));
+        fwd_abort_check(s);
       }
     }
     if (frontier) HIPCHK(hipMemcpyAsync(frontier, s->d_f, (size_t)B * 4, hipMemcpyDefault, st));
     if (host_out) {
+      fwd_abort_fetch(s);
       HIPCHK(hipStreamSynchronize(st));
+      fwd_abort_check(s);
       s->m->prof.flush();
     }
   } catch (HipError& e) {
@@ -1084,7 +1423,9 @@ ssd_status ssd_decode_image(ssd_model* m, const ssd_schedule* sc, int32_t B, int
     HIPCHK(hipMemcpyAsync(out_tokens, s->img, (size_t)B * N * 4, hipMemcpyDefault, st));
     std::vector<int> hc(B);
     HIPCHK(hipMemcpyAsync(hc.data(), s->cnt, (size_t)B * 4, hipMemcpyDeviceToHost, st));
+    fwd_abort_fetch(s);
     HIPCHK(hipStreamSynchronize(st));
+    fwd_abort_check(s);
     m->prof.flush();
     if (stats) {
       stats->passes = passes;

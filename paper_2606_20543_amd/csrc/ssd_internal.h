@@ -216,8 +216,9 @@ struct FwdGemm {
   int ld_in;
   // K-slice s (features [s*512, (s+1)*512) of the input) needs producer units
   // [s*512*dep_scale/dep_width, ceil((s+1)*512*dep_scale/dep_width)) of `dep`
+  // (dep_units > 0: every K-slice needs all units [0, dep_units) instead)
   const unsigned* dep;      // nullptr: input ready before launch
-  int dep_width, dep_scale, dep_layer;
+  int dep_width, dep_scale, dep_units, dep_layer;
   // the epilogue's 1/rms needs all rms_units units of rms_dep
   const unsigned* rms_dep;
   int rms_units, rms_layer;
@@ -250,6 +251,7 @@ struct FwdArgs {
   unsigned epoch_base;
   AttnKArgs att;            // attention geometry of this pass (caches per phase)
   int att_items;
+  int* probe;               // non-null: workgroup w writes its XCD index to probe[w] first
 };
 hipError_t fwd_persistent(const FwdArgs& a, int MT, int D, int grid, hipStream_t st);
 int fwd_max_grid(int MT, int D);  // co-resident workgroups of the persistent kernel (0: unsupported)
@@ -262,7 +264,13 @@ struct AttnPlan {
   int rows;       // query rows per (b, kv head) = K * g
   int xcd;        // see xcd_grid
 };
-AttnPlan attn_plan(const Dims& dm, int B, int K, int max_ctx_now, int xcd);
+// grid > 0: a plan for the persistent forward pass (one query tile per work
+// item, items fitting `grid` workgroups where possible)
+AttnPlan attn_plan(const Dims& dm, int B, int K, int max_ctx_now, int xcd, int grid = 0);
+AttnKArgs attn_args(const Dims& dm, const AttnPlan& p, int B, int K, const int* f, const void* q, size_t q_plane,
+                    const void* kc, const void* vc, int Lmax, void* o, size_t o_plane, float* partials,
+                    unsigned* counters);
+int attn_items(const AttnKArgs& a);  // work items (workgroups) of one attention call
 size_t attn_partials_floats(const Dims& dm, const AttnPlan& p, int B);
 void attention_bf16(const Dims& dm, const AttnPlan& p, int B, int K, const int* f, const void* q, size_t q_plane,
                     const void* kc, const void* vc, int Lmax, void* o, size_t o_plane, float* partials,

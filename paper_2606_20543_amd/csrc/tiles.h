@@ -24,46 +24,89 @@ __device__ __forceinline__ uint16_t f2bf(float f) {
 
 __device__ __forceinline__ float bf2f(uint16_t h) { return __uint_as_float(((uint32_t)h) << 16); }
 
+// Every access names a base pointer and a byte offset from it.  The base is
+// wave-uniform at every call site (a kernel argument or a field of one), which
+// lets CoherentMem address through a buffer resource built from it.
 struct PlainMem {
-  static __device__ __forceinline__ u32x4 ld16(const void* p) { return *(const u32x4*)p; }
-  static __device__ __forceinline__ float ld4f(const float* p) { return *p; }
-  static __device__ __forceinline__ float4 ldf4(const float* p) { return *(const float4*)p; }
-  static __device__ __forceinline__ void st2(uint16_t* p, uint16_t v) { *p = v; }
-  static __device__ __forceinline__ void st4(void* p, uint32_t v) { *(uint32_t*)p = v; }
-  static __device__ __forceinline__ void st8(void* p, uint2 v) { *(uint2*)p = v; }
-  static __device__ __forceinline__ void stf4(float* p, float4 v) { *(float4*)p = v; }
+  template <typename T>
+  static __device__ __forceinline__ const T* at(const void* b, size_t off) {
+    return (const T*)((const char*)b + off);
+  }
+  template <typename T>
+  static __device__ __forceinline__ T* at(void* b, size_t off) {
+    return (T*)((char*)b + off);
+  }
+  static __device__ __forceinline__ u32x4 ld16(const void* b, size_t off) { return *at<u32x4>(b, off); }
+  static __device__ __forceinline__ float ld4f(const void* b, size_t off) { return *at<float>(b, off); }
+  static __device__ __forceinline__ float4 ldf4(const void* b, size_t off) { return *at<float4>(b, off); }
+  static __device__ __forceinline__ float2 ldf2(const void* b, size_t off) { return *at<float2>(b, off); }
+  static __device__ __forceinline__ void st2(void* b, size_t off, uint16_t v) { *at<uint16_t>(b, off) = v; }
+  static __device__ __forceinline__ void st4(void* b, size_t off, uint32_t v) { *at<uint32_t>(b, off) = v; }
+  static __device__ __forceinline__ void st8(void* b, size_t off, uint2 v) { *at<uint2>(b, off) = v; }
+  static __device__ __forceinline__ void stf4(void* b, size_t off, float4 v) { *at<float4>(b, off) = v; }
+  static __device__ __forceinline__ void stf2(void* b, size_t off, float2 v) { *at<float2>(b, off) = v; }
+  static constexpr int LDS_AUX = 0;  // cache policy of LDS DMA reads
 };
 
-struct CoherentMem {
-  static __device__ __forceinline__ uint64_t ld8(const void* p) {
-    return __hip_atomic_load((const uint64_t*)p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+// Buffer-instruction accesses with a cache policy (raw buffer, 2 GiB range
+// from the base; callers keep offsets below that).  Unlike atomic loads these
+// are ordinary memory operations: the compiler issues them back to back.
+template <int LD_POL, int ST_POL>
+struct BufMem {
+  static constexpr int LDS_AUX = LD_POL;
+  // the base is uniform by contract; readfirstlane keeps it in scalar
+  // registers where the compiler cannot prove that (no per-lane loop)
+  static __device__ __forceinline__ __amdgpu_buffer_rsrc_t rs(const void* b) {
+    const uint64_t a = (uint64_t)b;
+    const uint64_t u = ((uint64_t)__builtin_amdgcn_readfirstlane((uint32_t)(a >> 32)) << 32) |
+                       (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)a);
+    return __builtin_amdgcn_make_buffer_rsrc((void*)u, 0, 0x7FFFFFFF, 0x00020000);
   }
-  static __device__ __forceinline__ void st8u(void* p, uint64_t v) {
-    __hip_atomic_store((uint64_t*)p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  static __device__ __forceinline__ u32x4 ld16(const void* b, size_t off) {
+    return __builtin_amdgcn_raw_buffer_load_b128(rs(b), (int)off, 0, LD_POL);
   }
-  static __device__ __forceinline__ u32x4 ld16(const void* p) {
-    const uint64_t a = ld8(p), b = ld8((const char*)p + 8);
-    return u32x4{(uint32_t)a, (uint32_t)(a >> 32), (uint32_t)b, (uint32_t)(b >> 32)};
+  static __device__ __forceinline__ float ld4f(const void* b, size_t off) {
+    return __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rs(b), (int)off, 0, LD_POL));
   }
-  static __device__ __forceinline__ float ld4f(const float* p) {
-    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  }
-  static __device__ __forceinline__ float4 ldf4(const float* p) {
-    const u32x4 v = ld16(p);
+  static __device__ __forceinline__ float4 ldf4(const void* b, size_t off) {
+    const u32x4 v = ld16(b, off);
     return make_float4(__uint_as_float(v.x), __uint_as_float(v.y), __uint_as_float(v.z), __uint_as_float(v.w));
   }
-  static __device__ __forceinline__ void st2(uint16_t* p, uint16_t v) {
-    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  static __device__ __forceinline__ float2 ldf2(const void* b, size_t off) {
+    typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+    const u32x2 v = __builtin_amdgcn_raw_buffer_load_b64(rs(b), (int)off, 0, LD_POL);
+    return make_float2(__uint_as_float(v.x), __uint_as_float(v.y));
   }
-  static __device__ __forceinline__ void st4(void* p, uint32_t v) {
-    __hip_atomic_store((uint32_t*)p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  static __device__ __forceinline__ void st2(void* b, size_t off, uint16_t v) {
+    __builtin_amdgcn_raw_buffer_store_b16(v, rs(b), (int)off, 0, ST_POL);
   }
-  static __device__ __forceinline__ void st8(void* p, uint2 v) { st8u(p, (uint64_t)v.x | ((uint64_t)v.y << 32)); }
-  static __device__ __forceinline__ void stf4(float* p, float4 v) {
-    st8u(p, (uint64_t)__float_as_uint(v.x) | ((uint64_t)__float_as_uint(v.y) << 32));
-    st8u(p + 2, (uint64_t)__float_as_uint(v.z) | ((uint64_t)__float_as_uint(v.w) << 32));
+  static __device__ __forceinline__ void st4(void* b, size_t off, uint32_t v) {
+    __builtin_amdgcn_raw_buffer_store_b32(v, rs(b), (int)off, 0, ST_POL);
+  }
+  static __device__ __forceinline__ void st8(void* b, size_t off, uint2 v) {
+    typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+    __builtin_amdgcn_raw_buffer_store_b64(u32x2{v.x, v.y}, rs(b), (int)off, 0, ST_POL);
+  }
+  static __device__ __forceinline__ void stf4(void* b, size_t off, float4 v) {
+    __builtin_amdgcn_raw_buffer_store_b128(
+        u32x4{__float_as_uint(v.x), __float_as_uint(v.y), __float_as_uint(v.z), __float_as_uint(v.w)}, rs(b),
+        (int)off, 0, ST_POL);
+  }
+  static __device__ __forceinline__ void stf2(void* b, size_t off, float2 v) {
+    typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+    __builtin_amdgcn_raw_buffer_store_b64(u32x2{__float_as_uint(v.x), __float_as_uint(v.y)}, rs(b), (int)off, 0,
+                                          ST_POL);
   }
 };
+// cache-policy bits of gfx950 vector memory instructions
+constexpr int CPOL_SC0 = 1;   // loads: miss in the CU's L1 (read from the XCD's L2)
+constexpr int CPOL_SC1 = 16;  // device scope: coherent across the XCDs' L2s (write-through stores)
+// Data exchanged between workgroups on any XCDs inside one running kernel.
+using CoherentMem = BufMem<CPOL_SC1, CPOL_SC1>;
+// Data exchanged inside one XCD (split-K and key-chunk partials): plain stores
+// land in the XCD's L2, loads skip the CU's L1 (which may still hold the lines
+// from an earlier use of the same buffer in the same kernel).
+using XcdMem = BufMem<CPOL_SC0, 0>;
 
 template <int NT, int KCB>
 __device__ __forceinline__ void load_a(u32x4 (&ra)[NT][KCB], const u32x4* W, int KB, int nb0, int N, int kb0,
@@ -111,9 +154,29 @@ __device__ __forceinline__ void load_x(u32x4 (&rx)[2][NP], const uint16_t* in, s
   for (int p = 0; p < NP; ++p) {
     const int r = r0 + p * X::RSTEP;
     const int rc = r < M ? r : M - 1;
-    const uint16_t* src = in + (size_t)rc * ld_in + k0 + cg * 8;
-    rx[0][p] = Mem::ld16(src);
-    rx[1][p] = Mem::ld16(src + plane);
+    const size_t off = ((size_t)rc * ld_in + k0 + cg * 8) * 2;
+    rx[0][p] = Mem::ld16(in, off);
+    rx[1][p] = Mem::ld16(in, off + plane * 2);
+  }
+}
+
+// The same chunk straight into LDS (gfx950 LDS DMA, 16 bytes per lane, no
+// registers): wave w copies rows w, w + 4, ... of both planes, one 1 KiB row
+// per instruction.  AUX: cache policy of the global reads.  The caller waits
+// for vmcnt(0) and then barriers before the LDS is read.
+template <int MT, int KCB, int AUX>
+__device__ __forceinline__ void load_x_lds(uint16_t* xs, const uint16_t* in, size_t plane, int ld_in, int M, int k0) {
+  using X = XStage<MT, KCB>;
+  static_assert(X::KC == 512, "one 512-input row per wave instruction");
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+#pragma unroll
+  for (int r = w; r < X::MP; r += 4) {
+    const int rc = r < M ? r : M - 1;
+    const uint16_t* src = in + (size_t)rc * ld_in + k0 + lane * 8;
+    __builtin_amdgcn_global_load_lds((const void __attribute__((address_space(1)))*)src,
+                                     (void __attribute__((address_space(3)))*)(xs + r * X::LD), 16, 0, AUX);
+    __builtin_amdgcn_global_load_lds((const void __attribute__((address_space(1)))*)(src + plane),
+                                     (void __attribute__((address_space(3)))*)(xs + X::PL + r * X::LD), 16, 0, AUX);
   }
 }
 
@@ -163,17 +226,17 @@ __device__ __forceinline__ void compute_chunk(floatx4 (&acc)[NT][MT], const u32x
 // into registers before the weight burst is issued (so the wait for them does
 // not wait for the weights), sums them in part order, and the G group sums
 // meet in LDS (summed in group order: deterministic).
-template <int MP>
+template <int MP, int PARTS = GEMM_RMS_MAX_PARTS>
 struct RmsPre {
   static constexpr int G = 256 / MP;
-  static constexpr int RQ = (GEMM_RMS_MAX_PARTS + G - 1) / G;
+  static constexpr int RQ = (PARTS + G - 1) / G;
 };
 
 // raw loads only (no use of the values, so nothing waits for them here);
 // without partial sums (ssq == nullptr) the loads read in[0] and are ignored
-template <int MP, class Mem = PlainMem>
+template <int MP, class Mem = PlainMem, int PARTS = GEMM_RMS_MAX_PARTS>
 __device__ __forceinline__ void rms_issue(const EpiArgs& e, const void* dummy, int M, int t0,
-                                          float (&v)[RmsPre<MP>::RQ]) {
+                                          float (&v)[RmsPre<MP, PARTS>::RQ]) {
   const int t = threadIdx.x % MP, pg = threadIdx.x / MP;
   const int tc = t < M ? t : M - 1;
   const bool has = e.ssq != nullptr;
@@ -181,28 +244,28 @@ __device__ __forceinline__ void rms_issue(const EpiArgs& e, const void* dummy, i
   const size_t c = has ? (size_t)e.ssq_off + (size_t)(t0 + tc) * e.ssq_step : 0;
   const size_t ld = has ? (size_t)e.ssq_ld : 0;
 #pragma unroll
-  for (int q = 0; q < RmsPre<MP>::RQ; ++q) {
-    const int p = pg + q * RmsPre<MP>::G;
-    v[q] = Mem::ld4f(base + (size_t)(p < e.ssq_parts ? p : 0) * ld + c);
+  for (int q = 0; q < RmsPre<MP, PARTS>::RQ; ++q) {
+    const int p = pg + q * RmsPre<MP, PARTS>::G;
+    v[q] = Mem::ld4f(base, ((size_t)(p < e.ssq_parts ? p : 0) * ld + c) * 4);
   }
 }
 
 // writes rscale[0..MP); visible after the caller's next barrier
-template <int MP>
-__device__ __forceinline__ void rms_finish(const EpiArgs& e, const float (&v)[RmsPre<MP>::RQ], float* red,
+template <int MP, int PARTS = GEMM_RMS_MAX_PARTS>
+__device__ __forceinline__ void rms_finish(const EpiArgs& e, const float (&v)[RmsPre<MP, PARTS>::RQ], float* red,
                                            float* rscale) {
   // branch-free in ssq (a branch here would make the compiler settle the
   // weight loads at the join); without partial sums the scale is 1
   const int pg = threadIdx.x / MP;
   float s = 0.f;
 #pragma unroll
-  for (int q = 0; q < RmsPre<MP>::RQ; ++q) s += (pg + q * RmsPre<MP>::G < e.ssq_parts) ? v[q] : 0.f;
+  for (int q = 0; q < RmsPre<MP, PARTS>::RQ; ++q) s += (pg + q * RmsPre<MP, PARTS>::G < e.ssq_parts) ? v[q] : 0.f;
   red[threadIdx.x] = s;  // [pg][t]
   lds_barrier();
   if (threadIdx.x < MP) {
     float a = 0.f;
 #pragma unroll
-    for (int g = 0; g < RmsPre<MP>::G; ++g) a += red[g * MP + threadIdx.x];
+    for (int g = 0; g < RmsPre<MP, PARTS>::G; ++g) a += red[g * MP + threadIdx.x];
     rscale[threadIdx.x] = e.ssq ? 1.0f / sqrtf(a * e.inv_d + e.eps) : 1.f;
   }
 }
@@ -271,7 +334,7 @@ __device__ __forceinline__ void epi_load(const EpiArgs& e, int nb0, int N, int M
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt) {
         const int tl = mt * 16 + (lane & 15);
-        op.a[nt][mt] = Mem::ldf4(e.x + (size_t)(t0 + (tl < M ? tl : M - 1)) * e.ld + n);
+        op.a[nt][mt] = Mem::ldf4(e.x, ((size_t)(t0 + (tl < M ? tl : M - 1)) * e.ld + n) * 4);
       }
     }
   } else if (e.kind == EPI_QKV) {
@@ -337,21 +400,21 @@ __device__ __forceinline__ void epi_store(const EpiArgs& e, const floatx4 (&acc)
               split2(a0, a1, h0, l0);
               split2(c0, c1, h1, l1);
               const size_t i0 = base + tile16x32_index(r, j, D), i1 = base + tile16x32_index(r, j + half, D);
-              Mem::st4(q + i0, h0);
-              Mem::st4(q + i1, h1);
-              Mem::st4(q + e.q_plane + i0, l0);
-              Mem::st4(q + e.q_plane + i1, l1);
+              Mem::st4(q, i0 * 2, h0);
+              Mem::st4(q, i1 * 2, h1);
+              Mem::st4(q, (e.q_plane + i0) * 2, l0);
+              Mem::st4(q, (e.q_plane + i1) * 2, l1);
             } else {
               const size_t base = ((size_t)b * e.Hkv + head) * e.Lmax * D;
-              Mem::st4(kc + base + tile16x32_index(pos, j, D), pack2(f2bf(a0), f2bf(a1)));
-              Mem::st4(kc + base + tile16x32_index(pos, j + half, D), pack2(f2bf(c0), f2bf(c1)));
+              Mem::st4(kc, (base + tile16x32_index(pos, j, D)) * 2, pack2(f2bf(a0), f2bf(a1)));
+              Mem::st4(kc, (base + tile16x32_index(pos, j + half, D)) * 2, pack2(f2bf(c0), f2bf(c1)));
             }
           } else {
             const int nv = n - qN - kN;
             const int head = nv / D, dd = nv - head * D;
             const size_t base = ((size_t)b * e.Hkv + head) * (size_t)D * e.Lmax;
 #pragma unroll
-            for (int i = 0; i < 4; ++i) Mem::st2(vc + base + vtile_index(dd + i, pos, e.Lmax), f2bf(v[i] * r));
+            for (int i = 0; i < 4; ++i) Mem::st2(vc, (base + vtile_index(dd + i, pos, e.Lmax)) * 2, f2bf(v[i] * r));
           }
           break;
         }
@@ -360,13 +423,12 @@ __device__ __forceinline__ void epi_store(const EpiArgs& e, const floatx4 (&acc)
           const float4 xo = op.a[nt][mt];
           const float4 g = op.g[nt];
           const float4 xv = make_float4(xo.x + v[0], xo.y + v[1], xo.z + v[2], xo.w + v[3]);
-          Mem::stf4(e.x + i, xv);
+          Mem::stf4(e.x, i * 4, xv);
           uint32_t h0, l0, h1, l1;
           split2(g.x * xv.x, g.y * xv.y, h0, l0);
           split2(g.z * xv.z, g.w * xv.w, h1, l1);
-          uint16_t* xn = (uint16_t*)e.xn;
-          Mem::st8(xn + i, make_uint2(h0, h1));
-          Mem::st8(xn + e.xn_plane + i, make_uint2(l0, l1));
+          Mem::st8(e.xn, i * 2, make_uint2(h0, h1));
+          Mem::st8(e.xn, (e.xn_plane + i) * 2, make_uint2(l0, l1));
           sq[mt] += (xv.x * xv.x + xv.y * xv.y) + (xv.z * xv.z + xv.w * xv.w);
           break;
         }
@@ -376,14 +438,13 @@ __device__ __forceinline__ void epi_store(const EpiArgs& e, const floatx4 (&acc)
           const float s0 = g0 / (1.0f + expf(-g0)), s1 = g1 / (1.0f + expf(-g1));
           uint32_t hi, lo;
           split2(s0 * u0, s1 * u1, hi, lo);
-          uint16_t* h = (uint16_t*)e.h;
           const size_t i = (size_t)t * e.ld + (n >> 1);
-          Mem::st4(h + i, hi);
-          Mem::st4(h + e.h_plane + i, lo);
+          Mem::st4(e.h, i * 2, hi);
+          Mem::st4(e.h, (e.h_plane + i) * 2, lo);
           break;
         }
         default: {  // EPI_LOGITS
-          Mem::stf4(e.logits + (size_t)t * e.ld + n, make_float4(v[0] * r, v[1] * r, v[2] * r, v[3] * r));
+          Mem::stf4(e.logits, ((size_t)t * e.ld + n) * 4, make_float4(v[0] * r, v[1] * r, v[2] * r, v[3] * r));
           break;
         }
       }
@@ -394,7 +455,7 @@ __device__ __forceinline__ void epi_store(const EpiArgs& e, const floatx4 (&acc)
 
 // hi/lo bf16 planes of four consecutive fp32 values
 template <class Mem = PlainMem>
-__device__ __forceinline__ void store_split4(uint16_t* p, size_t plane, floatx4 v) {
+__device__ __forceinline__ void store_split4(uint16_t* base, size_t i, size_t plane, floatx4 v) {
   uint16_t hi[4], lo[4];
 #pragma unroll
   for (int e = 0; e < 4; ++e) {
@@ -406,8 +467,8 @@ __device__ __forceinline__ void store_split4(uint16_t* p, size_t plane, floatx4 
   w.y = (uint32_t)hi[2] | ((uint32_t)hi[3] << 16);
   x.x = (uint32_t)lo[0] | ((uint32_t)lo[1] << 16);
   x.y = (uint32_t)lo[2] | ((uint32_t)lo[3] << 16);
-  Mem::st8(p, w);
-  Mem::st8(p + plane, x);
+  Mem::st8(base, i * 2, w);
+  Mem::st8(base, (i + plane) * 2, x);
 }
 
 // K and V operands of one 32-key block: K tiles (keys key0 + kt*16 + [0,16),
@@ -429,20 +490,24 @@ __device__ __forceinline__ void load_kv(KVTile<D>& t, const uint16_t* kbase, con
   for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
     for (int kd = 0; kd < D / 32; ++kd)
-      t.k[kt][kd] = Mem::ld16(kbase + ((size_t)((kb >> 4) + kt) * (D / 32) + kd) * 512 + lane * 8);
+      t.k[kt][kd] = Mem::ld16(kbase, (((size_t)((kb >> 4) + kt) * (D / 32) + kd) * 512 + lane * 8) * 2);
 #pragma unroll
   for (int dt = 0; dt < D / 16; ++dt)
-    t.v[dt] = Mem::ld16(vbase + ((size_t)dt * (Lmax >> 5) + (kb >> 5)) * 512 + lane * 8);
+    t.v[dt] = Mem::ld16(vbase, (((size_t)dt * (Lmax >> 5) + (kb >> 5)) * 512 + lane * 8) * 2);
 }
 
 // one 32-key block through the online softmax of the wave's query tiles
-template <int D, int QPW>
+// QL: the query operands come from LDS (qs: tiles (qt, kd, plane) of 1 KiB in
+// lane order) instead of registers (for callers short of registers).
+template <int D, int QPW, bool QL = false>
 __device__ __forceinline__ void attend_block(const KVTile<D>& t, int key0, const bf16x8 (&qh)[QPW][D / 32],
                                              const bf16x8 (&ql)[QPW][D / 32], const int (&qpos)[QPW],
                                              float scale_log2, int grp, float (&m)[QPW], float (&l)[QPW],
-                                             floatx4 (&O)[QPW][D / 16]) {
+                                             floatx4 (&O)[QPW][D / 16], const uint16_t* qs = nullptr) {
   constexpr int KD = D / 32, DT = D / 16;
   floatx4 s[2][QPW];
+  const uint16_t* qsl = qs + (threadIdx.x & 63) * 8;
+  if constexpr (QL) asm volatile("" : "+v"(qsl));  // re-read every block (not hoisted into registers)
 #pragma unroll
   for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
@@ -451,8 +516,14 @@ __device__ __forceinline__ void attend_block(const KVTile<D>& t, int key0, const
 #pragma unroll
       for (int kd = 0; kd < KD; ++kd) {
         const bf16x8 kf = __builtin_bit_cast(bf16x8, t.k[kt][kd]);
-        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qh[qt][kd], acc, 0, 0, 0);
-        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, ql[qt][kd], acc, 0, 0, 0);
+        bf16x8 a = qh[qt][kd], b = ql[qt][kd];
+        if constexpr (QL) {
+          const uint16_t* p = qsl + ((size_t)(qt * KD + kd) * 2) * 512;
+          a = __builtin_bit_cast(bf16x8, *(const u32x4*)p);
+          b = __builtin_bit_cast(bf16x8, *(const u32x4*)(p + 512));
+        }
+        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, a, acc, 0, 0, 0);
+        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, b, acc, 0, 0, 0);
       }
       s[kt][qt] = acc;
     }
@@ -524,9 +595,11 @@ struct AtShape {
 // group (sequence x KV head x query group index) whose output this workgroup
 // wrote, or -1 (idle slot, or a chunk whose partial another workgroup merges).
 // LDS: sm_o[NW*QPW*16*(D+4)], sm_m/sm_l[NW*QPW*16], is_last.
-template <int D, int QPW, class Mem = PlainMem, bool PF = true>
+// Mem: queries, K/V and the output; PMem: the chunk partials; QL: queries
+// staged in LDS (sm_q, QPW * D/32 * 2 KiB) instead of registers.
+template <int D, int QPW, class Mem = PlainMem, bool PF = true, class PMem = PlainMem, bool QL = false>
 __device__ __forceinline__ int attn_unit(const AttnKArgs& a, int item, float* sm_o, float* sm_m, float* sm_l,
-                                         int* is_last) {
+                                         int* is_last, uint16_t* sm_q = nullptr) {
   constexpr int NW = AtShape<QPW>::WAVES, NTH = AtShape<QPW>::THREADS, STEP = AtShape<QPW>::STEP;
   constexpr int KD = D / 32;   // 32-wide k steps over the head dimension
   constexpr int DT = D / 16;   // 16-row d tiles of O^T
@@ -582,12 +655,35 @@ __device__ __forceinline__ int attn_unit(const AttnKArgs& a, int item, float* sm
   for (int qt = 0; qt < QPW; ++qt) {
     const int r = rbase + qt * 16 + col;  // padded rows (r >= rows) exist and are masked
     qpos[qt] = r < a.rows ? fb + r % a.K : -1;
-    const uint16_t* qp = qbase + ((size_t)((rbase >> 4) + qt) * KD) * 512 + lane * 8;
+    const size_t qo = ((size_t)((rbase >> 4) + qt) * KD) * 512 + lane * 8;
 #pragma unroll
     for (int kd = 0; kd < KD; ++kd) {
-      qh[qt][kd] = __builtin_bit_cast(bf16x8, Mem::ld16(qp + kd * 512));
-      ql[qt][kd] = __builtin_bit_cast(bf16x8, Mem::ld16(qp + a.q_plane + kd * 512));
+      if constexpr (QL) {
+        qh[qt][kd] = bf16x8{};
+        ql[qt][kd] = bf16x8{};
+      } else {
+        qh[qt][kd] = __builtin_bit_cast(bf16x8, Mem::ld16(qbase, (qo + kd * 512) * 2));
+        ql[qt][kd] = __builtin_bit_cast(bf16x8, Mem::ld16(qbase, (qo + a.q_plane + kd * 512) * 2));
+      }
     }
+  }
+  if constexpr (QL) {
+    // LDS DMA of the query tiles: tile i = (qt * KD + kd) * 2 + plane, 1 KiB each,
+    // spread over the waves; every wave then reads all of them
+    constexpr int NQ = QPW * KD * 2;
+    constexpr int AUX = Mem::LDS_AUX;
+    static_assert(NQ % NW == 0, "query tiles split evenly over the waves");
+#pragma unroll
+    for (int j = 0; j < NQ / NW; ++j) {
+      const int i = wave * (NQ / NW) + j;
+      const int qt = i / (2 * KD), kd = (i / 2) % KD, pl = i & 1;
+      const uint16_t* src = qbase + ((size_t)((rbase >> 4) + qt) * KD + kd) * 512 + (pl ? a.q_plane : 0) + lane * 8;
+      __builtin_amdgcn_global_load_lds((const void __attribute__((address_space(1)))*)src,
+                                       (void __attribute__((address_space(3)))*)(sm_q + (size_t)i * 512), 16, 0,
+                                       AUX);
+    }
+    __builtin_amdgcn_s_waitcnt(0);
+    lds_barrier();
   }
 
   float m[QPW], l[QPW];
@@ -607,14 +703,14 @@ __device__ __forceinline__ int attn_unit(const AttnKArgs& a, int item, float* sm
     for (int it = 0; it < nit; ++it) {
       const int key0 = first + it * STEP;
       load_kv<D, Mem>(tb, kbase, vbase, key0 + STEP, a.Lmax, lane);
-      attend_block<D, QPW>(ta, key0, qh, ql, qpos, a.scale_log2, grp, m, l, O);
+      attend_block<D, QPW, QL>(ta, key0, qh, ql, qpos, a.scale_log2, grp, m, l, O, sm_q);
       ta = tb;
     }
   } else {
     // one block in registers (for callers that keep other data live)
     for (int it = 0; it < nit; ++it) {
       const int key0 = first + it * STEP;
-      attend_block<D, QPW>(ta, key0, qh, ql, qpos, a.scale_log2, grp, m, l, O);
+      attend_block<D, QPW, QL>(ta, key0, qh, ql, qpos, a.scale_log2, grp, m, l, O, sm_q);
       if (it + 1 < nit) load_kv<D, Mem>(ta, kbase, vbase, key0 + STEP, a.Lmax, lane);
     }
   }
@@ -669,8 +765,8 @@ __device__ __forceinline__ int attn_unit(const AttnKArgs& a, int item, float* sm
       const int rg = rbase + r;
       if (rg >= a.rows) continue;
       const int j = rg / a.K, k = rg - j * a.K;
-      uint16_t* op = a.o + ((size_t)b * a.K + k) * (a.Hq * D) + (hkv * a.g + j) * D + 4 * d4;
-      store_split4<Mem>(op, a.o_plane, acc[i] * (1.f / Lr[i]));
+      const size_t oi = ((size_t)b * a.K + k) * (a.Hq * D) + (hkv * a.g + j) * D + 4 * d4;
+      store_split4<Mem>(a.o, oi, a.o_plane, acc[i] * (1.f / Lr[i]));
     }
     return grp_id;
   }
@@ -683,9 +779,10 @@ __device__ __forceinline__ int attn_unit(const AttnKArgs& a, int item, float* sm
     for (int i = 0; i < NV; ++i) {
       const int idx = threadIdx.x + NTH * i;
       if (idx >= NOUT) continue;
-      Op[idx] = acc[i];
+      const floatx4 v = acc[i];
+      PMem::stf4(Op, (size_t)idx * 16, make_float4(v[0], v[1], v[2], v[3]));
       const int r = idx / (D / 4), d4 = idx - r * (D / 4);
-      if (d4 == 0) a.spart[(gbase + c) * ROWS + r] = make_float2(Mr[i], Lr[i]);
+      if (d4 == 0) PMem::stf2(a.spart, ((gbase + c) * ROWS + r) * 8, make_float2(Mr[i], Lr[i]));
     }
   }
   // partial stores acknowledged by this XCD's L2, then count the arrival
@@ -695,6 +792,7 @@ __device__ __forceinline__ int attn_unit(const AttnKArgs& a, int item, float* sm
     if (!a.xcd) __threadfence();  // chunks on different XCDs: write back through L2
     unsigned prev = atomicAdd(&a.counters[grp_id], 1u);
     *is_last = (prev == (unsigned)(nch - 1));
+    if (*is_last) a.counters[grp_id] = 0u;  // every chunk has arrived: re-arm for the next pass
     if (*is_last && !a.xcd) __threadfence();
   }
   __syncthreads();
@@ -704,7 +802,7 @@ __device__ __forceinline__ int attn_unit(const AttnKArgs& a, int item, float* sm
   float* cm = sm_o;                           // [nch][ROWS] chunk max
   float* cl = sm_o + AT_MAX_CHUNKS * ROWS;    // [nch][ROWS] chunk sum, then weight
   for (int i = threadIdx.x; i < nch * ROWS; i += NTH) {
-    const float2 st = a.spart[gbase * ROWS + i];
+    const float2 st = PMem::ldf2(a.spart, (gbase * ROWS + i) * 8);
     cm[i] = st.x;
     cl[i] = st.y;
   }
@@ -735,7 +833,8 @@ __device__ __forceinline__ int attn_unit(const AttnKArgs& a, int item, float* sm
     for (int i = 0; i < NV; ++i) {
       const int idx = threadIdx.x + NTH * i;
       const int ic = idx < NOUT ? idx : NOUT - 1;
-      v[i] += G[(size_t)cc * NOUT + ic] * cl[cc * ROWS + ic / (D / 4)];
+      const float4 g4 = PMem::ldf4(G, ((size_t)cc * NOUT + ic) * 16);
+      v[i] += floatx4{g4.x, g4.y, g4.z, g4.w} * cl[cc * ROWS + ic / (D / 4)];
     }
   }
 #pragma unroll
@@ -746,10 +845,9 @@ __device__ __forceinline__ int attn_unit(const AttnKArgs& a, int item, float* sm
     const int rg = rbase + r;
     if (rg >= a.rows) continue;
     const int j = rg / a.K, k = rg - j * a.K;
-    uint16_t* op = a.o + ((size_t)b * a.K + k) * (a.Hq * D) + (hkv * a.g + j) * D + 4 * d4;
-    store_split4<Mem>(op, a.o_plane, v[i] * (1.f / sm_l[r]));
+    const size_t oi = ((size_t)b * a.K + k) * (a.Hq * D) + (hkv * a.g + j) * D + 4 * d4;
+    store_split4<Mem>(a.o, oi, a.o_plane, v[i] * (1.f / sm_l[r]));
   }
-  if (threadIdx.x == 0) a.counters[grp_id] = 0u;
   return grp_id;
 }
 
