@@ -97,6 +97,12 @@ typedef const FwdPhase* PhaseTab;  // host pass: device code is parsed, not gene
 #endif
 __device__ __forceinline__ PhaseTab phase_tab(const FwdArgs& A) { return (PhaseTab)(uintptr_t)A.phases; }
 
+// this workgroup's first item of a phase rotated by rot
+__device__ __forceinline__ int first_item(int rot) {
+  const int G = gridDim.x;
+  return ((int)blockIdx.x - rot + G) % G;
+}
+
 // Next GEMM item of this workgroup after item `it` of phase p (it < 0: none
 // in p), not looking past an attention phase (the prefetched weights are not
 // kept live across the attention code): (p2, it2), or p2 = -1.
@@ -110,30 +116,35 @@ __device__ __forceinline__ void next_gemm_item(const FwdArgs& A, int p, int it, 
   }
   for (int q = p + 1; q < A.n_phases; ++q) {
     if (tab[q].kind != FWD_GEMM) break;
-    if ((int)blockIdx.x < tab[q].g.items) {
+    const int first = first_item(tab[q].rot);
+    if (first < tab[q].g.items) {
       p2 = q;
-      it2 = blockIdx.x;
+      it2 = first;
       return;
     }
   }
   p2 = -1;
 }
 
+// weights of burst b (16 k-blocks) of item `it` of phase p
 template <int MT>
-__device__ __forceinline__ void issue_weights(PhaseTab tab, int p, int it, int xcd, u32x4 (&ra)[1][FWD_KCB]) {
+__device__ __forceinline__ void issue_weights(PhaseTab tab, int p, int it, int b, int xcd, u32x4 (&ra)[1][FWD_KCB]) {
   const int S = tab[p].g.S, n_fb = tab[p].g.n_fb;
   int fb, s;
   xcd_unmap(it, S, xcd, fb, s);
   if (fb >= n_fb) fb = n_fb - 1;  // idle slot: any valid tile (never used)
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  load_a<1, FWD_KCB>(ra, (const u32x4*)tab[p].g.W, tab[p].g.KB, fb * 4 + w, tab[p].g.N, s * FWD_KCB, lane);
+  load_a<1, FWD_KCB>(ra, (const u32x4*)tab[p].g.W, tab[p].g.KB, fb * 4 + w, tab[p].g.N,
+                     (s * tab[p].g.bursts + b) * FWD_KCB, lane);
 }
 
-// One GEMM work item (feature block fb, K-split s).  The weights are in ra
-// (loaded by the caller).  Returns whether this workgroup ran the epilogue.
+// One GEMM work item (feature block fb, K-split s of g.bursts 512-wide
+// bursts).  The first burst's weights are in ra (loaded by the caller); the
+// later ones are loaded here, each after the previous burst's products.
+// Returns whether this workgroup ran the epilogue.
 template <int MT>
-__device__ __forceinline__ void gemm_item(const FwdArgs& A, const FwdGemm& g, int it, u32x4 (&ra)[1][FWD_KCB],
-                                          unsigned char* smem, int* sflag, bool& last) {
+__device__ __forceinline__ void gemm_item(const FwdArgs& A, PhaseTab tab, int p, const FwdGemm& g, int it,
+                                          u32x4 (&ra)[1][FWD_KCB], unsigned char* smem, int* sflag, bool& last) {
   using X = XStage<MT, FWD_KCB>;
   uint16_t* xs = (uint16_t*)smem;
   float* sq_red = (float*)(smem + 2 * X::PL * 2);  // [4][MP]
@@ -147,9 +158,20 @@ __device__ __forceinline__ void gemm_item(const FwdArgs& A, const FwdGemm& g, in
   const unsigned val = A.epoch_base + (unsigned)g.dep_layer;
 
   // inputs of this K-slice: the producer units covering [s*KC, (s+1)*KC) (x dep_scale)
-  const int KC = FWD_KCB * 32;
+  const int KC = FWD_KCB * 32 * g.bursts;
   int u0 = 0, u1 = g.dep_units;
-  if (g.dep_units == 0) {
+  if (g.dep_att) {
+    // attention outputs: the query groups of the KV heads whose query heads
+    // this slice covers (one sequence; several sequences wait for all groups)
+    const AttnKArgs& at = A.att;
+    if (at.heads == at.Hkv) {
+      const int h0 = (s * KC) / e.D, h1 = ((s + 1) * KC - 1) / e.D;
+      u0 = (h0 / at.g) * at.nqg;
+      u1 = (h1 / at.g + 1) * at.nqg;
+    } else {
+      u1 = at.groups;
+    }
+  } else if (g.dep_units == 0) {
     u0 = (s * KC * g.dep_scale) / g.dep_width;
     u1 = ((s + 1) * KC * g.dep_scale + g.dep_width - 1) / g.dep_width;
   }
@@ -159,13 +181,19 @@ __device__ __forceinline__ void gemm_item(const FwdArgs& A, const FwdGemm& g, in
     last = false;
     return;
   }
-  load_x_lds<MT, FWD_KCB, CPOL_SC1>(xs, g.in, g.in_plane, g.ld_in, g.M, s * KC);
-  __builtin_amdgcn_s_waitcnt(0);  // this wave's LDS copies (and its weight loads) have landed
-  lds_barrier();
   floatx4 acc[1][MT];
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt) acc[0][mt] = floatx4{0.f, 0.f, 0.f, 0.f};
-  compute_chunk<MT, 1, FWD_KCB>(acc, ra, xs, lane);
+  for (int b = 0; b < g.bursts; ++b) {
+    if (b > 0) {
+      lds_barrier();  // every wave is done reading the previous x chunk
+      issue_weights<MT>(tab, p, it, b, A.xcd, ra);
+    }
+    load_x_lds<MT, FWD_KCB, CPOL_SC1>(xs, g.in, g.in_plane, g.ld_in, g.M, s * KC + b * FWD_KCB * 32);
+    __builtin_amdgcn_s_waitcnt(0);  // this wave's LDS copies (and its weight loads) have landed
+    lds_barrier();
+    compute_chunk<MT, 1, FWD_KCB>(acc, ra, xs, lane);
+  }
 
   const size_t frag = (size_t)MT * 64 * 4;
   const size_t P = ((size_t)fb * 4 + w) * frag;  // this wave's fragment (floats from g.part)
@@ -272,7 +300,7 @@ __global__ __launch_bounds__(FWD_THREADS) __attribute__((amdgpu_waves_per_eu(2, 
     int p2, it2;
     next_gemm_item(A, -1, 0, p2, it2);
     if (p2 >= 0) {
-      issue_weights<MT>(tab, p2, it2, A.xcd, ra);
+      issue_weights<MT>(tab, p2, it2, 0, A.xcd, ra);
       pre_p = p2;
       pre_it = it2;
     }
@@ -281,20 +309,20 @@ __global__ __launch_bounds__(FWD_THREADS) __attribute__((amdgpu_waves_per_eu(2, 
     const FwdPhase ph = tab[p];  // by value: the fields live in scalar registers
     if (ph.kind == FWD_GEMM) {
       const FwdGemm& g = ph.g;
-      for (int it = blockIdx.x; it < g.items; it += gridDim.x) {
+      for (int it = first_item(ph.rot); it < g.items; it += gridDim.x) {
         int fb, s;
         xcd_unmap(it, g.S, A.xcd, fb, s);
-        if (!(pre_p == p && pre_it == it)) issue_weights<MT>(tab, p, it, A.xcd, ra);
+        if (!(pre_p == p && pre_it == it)) issue_weights<MT>(tab, p, it, 0, A.xcd, ra);
         pre_p = -1;
         bool last = false;
-        if (fb < g.n_fb) gemm_item<MT>(A, g, it, ra, smem, &sflag, last);
+        if (fb < g.n_fb) gemm_item<MT>(A, tab, p, g, it, ra, smem, &sflag, last);
         // next item's weights: right away for a workgroup that ran no
         // epilogue, after the epilogue otherwise (its loads must not queue
         // behind a weight burst)
         int p2, it2;
         next_gemm_item(A, p, it, p2, it2);
         if (p2 >= 0) {
-          issue_weights<MT>(tab, p2, it2, A.xcd, ra);
+          issue_weights<MT>(tab, p2, it2, 0, A.xcd, ra);
           pre_p = p2;
           pre_it = it2;
         }
@@ -305,7 +333,7 @@ __global__ __launch_bounds__(FWD_THREADS) __attribute__((amdgpu_waves_per_eu(2, 
       float* sm_o = (float*)smem;
       float* sm_m = sm_o + AtShape<1>::WAVES * 16 * (D + 4);
       float* sm_l = sm_m + AtShape<1>::WAVES * 16;
-      for (int it = blockIdx.x; it < A.att_items; it += gridDim.x) {
+      for (int it = first_item(ph.rot); it < A.att_items; it += gridDim.x) {
         // inputs: q of the group's query heads, k and v of its KV head
         int z, qg, grp_id, c;
         if (A.att.nchunk == 1) {
@@ -340,7 +368,7 @@ __global__ __launch_bounds__(FWD_THREADS) __attribute__((amdgpu_waves_per_eu(2, 
       int p2, it2;
       next_gemm_item(A, p, -1, p2, it2);
       if (p2 >= 0) {
-        issue_weights<MT>(tab, p2, it2, A.xcd, ra);
+        issue_weights<MT>(tab, p2, it2, 0, A.xcd, ra);
         pre_p = p2;
         pre_it = it2;
       } else {

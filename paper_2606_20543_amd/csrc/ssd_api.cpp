@@ -336,15 +336,23 @@ void fwd_abort_check(ssd_session* s) {
     throw HipError{hipErrorLaunchTimeOut, "persistent forward pass abandoned a dependency wait"};
 }
 
-FwdGemm fwd_gemm(const void* W, int N, int Kd, const void* in, size_t in_plane, int ld_in, int M, int X, float* part,
-                 unsigned* cnt, unsigned* out_flags, int out_layer, const EpiArgs& e) {
+// A projection as persistent work items: 64 features x (bursts x 512) inputs
+// each, with the fewest bursts that keep the items within one round of the
+// grid (a burst beyond the first costs its weight load's latency, a second
+// round a whole item).
+FwdGemm fwd_gemm(const void* W, int N, int Kd, const void* in, size_t in_plane, int ld_in, int M, int X, int grid,
+                 float* part, unsigned* cnt, unsigned* out_flags, int out_layer, const EpiArgs& e) {
   FwdGemm g{};
   g.W = W;
   g.N = N;
   g.K = Kd;
   g.KB = Kd / 32;
   g.n_fb = N / FWD_FB;
-  g.S = Kd / FWD_KSLICE;
+  const int slices = Kd / FWD_KSLICE;
+  g.bursts = 1;
+  for (int b = 2; b <= 4; b *= 2)
+    if (xcd_grid(g.n_fb, slices / g.bursts, X) > grid && slices % b == 0) g.bursts = b;
+  g.S = slices / g.bursts;
   g.items = xcd_grid(g.n_fb, g.S, X);
   g.M = M;
   g.in = (const uint16_t*)in;
@@ -362,7 +370,7 @@ FwdGemm fwd_gemm(const void* W, int N, int Kd, const void* in, size_t in_plane, 
 
 // Phase table of one (K, lm_mode): per layer QKV, attention, O, gate/up, down;
 // then the output layer.  Flag values are layer + 1 (plus the pass's epoch base).
-const FwdPhase* fwd_table(ssd_session* s, int K, int lm_mode, int X, const EpiArgs& base, int att_groups) {
+const FwdPhase* fwd_table(ssd_session* s, int K, int lm_mode, int X, int G, const EpiArgs& base, int att_groups) {
   auto key = std::make_pair(K, lm_mode);
   auto it = s->fw.tables.find(key);
   if (it != s->fw.tables.end()) return it->second.second;
@@ -387,7 +395,7 @@ const FwdPhase* fwd_table(ssd_session* s, int K, int lm_mode, int X, const EpiAr
     e.kc = kc;
     e.vc = vc;
     p.kind = FWD_GEMM;
-    p.g = fwd_gemm(W.wqkv, Nqkv, d, s->xn, s->xn_plane, d, M, X, s->fw.part[0], s->fw.cnt[0], s->fw.f_qkv, l + 1, e);
+    p.g = fwd_gemm(W.wqkv, Nqkv, d, s->xn, s->xn_plane, d, M, X, G, s->fw.part[0], s->fw.cnt[0], s->fw.f_qkv, l + 1, e);
     if (l > 0) {
       p.g.dep = s->fw.f_dn;
       p.g.dep_layer = l;
@@ -416,10 +424,10 @@ const FwdPhase* fwd_table(ssd_session* s, int K, int lm_mode, int X, const EpiAr
     e.ld = d;
     p = FwdPhase{};
     p.kind = FWD_GEMM;
-    p.g = fwd_gemm(W.wo, d, dm.Hq * D, s->o, s->o_plane, dm.Hq * D, M, X, s->fw.part[1], s->fw.cnt[1], s->fw.f_o, l + 1,
+    p.g = fwd_gemm(W.wo, d, dm.Hq * D, s->o, s->o_plane, dm.Hq * D, M, X, G, s->fw.part[1], s->fw.cnt[1], s->fw.f_o, l + 1,
                    e);
     p.g.dep = s->fw.f_att;
-    p.g.dep_units = att_groups;
+    p.g.dep_att = 1;
     p.g.dep_layer = l + 1;
     ph.push_back(p);
     // gate/up + SwiGLU
@@ -431,7 +439,7 @@ const FwdPhase* fwd_table(ssd_session* s, int K, int lm_mode, int X, const EpiAr
     e.ld = dm.dff;
     p = FwdPhase{};
     p.kind = FWD_GEMM;
-    p.g = fwd_gemm(W.w13, 2 * dm.dff, d, s->xn, s->xn_plane, d, M, X, s->fw.part[2], s->fw.cnt[2], s->fw.f_gu, l + 1,
+    p.g = fwd_gemm(W.w13, 2 * dm.dff, d, s->xn, s->xn_plane, d, M, X, G, s->fw.part[2], s->fw.cnt[2], s->fw.f_gu, l + 1,
                    e);
     p.g.dep = s->fw.f_o;
     p.g.dep_layer = l + 1;
@@ -447,7 +455,7 @@ const FwdPhase* fwd_table(ssd_session* s, int K, int lm_mode, int X, const EpiAr
     e.ld = d;
     p = FwdPhase{};
     p.kind = FWD_GEMM;
-    p.g = fwd_gemm(W.w2, d, dm.dff, s->h, s->h_plane, dm.dff, M, X, s->fw.part[3], s->fw.cnt[3], s->fw.f_dn, l + 1, e);
+    p.g = fwd_gemm(W.w2, d, dm.dff, s->h, s->h_plane, dm.dff, M, X, G, s->fw.part[3], s->fw.cnt[3], s->fw.f_dn, l + 1, e);
     p.g.dep = s->fw.f_gu;
     p.g.dep_scale = 2;
     p.g.dep_layer = l + 1;
@@ -463,11 +471,11 @@ const FwdPhase* fwd_table(ssd_session* s, int K, int lm_mode, int X, const EpiAr
   FwdPhase p{};
   p.kind = FWD_GEMM;
   if (lm_mode == 0) {
-    p.g = fwd_gemm(m->wlm, dm.Vimg, d, s->xn, s->xn_plane, d, M, X, s->fw.part[4], s->fw.cnt[4], nullptr, 0, e);
+    p.g = fwd_gemm(m->wlm, dm.Vimg, d, s->xn, s->xn_plane, d, M, X, G, s->fw.part[4], s->fw.cnt[4], nullptr, 0, e);
   } else {
     e.ssq_off = K - 1;
     e.ssq_step = K;
-    p.g = fwd_gemm(m->wlm, dm.Vimg, d, (const uint16_t*)s->xn + (size_t)(K - 1) * d, s->xn_plane, K * d, B, X,
+    p.g = fwd_gemm(m->wlm, dm.Vimg, d, (const uint16_t*)s->xn + (size_t)(K - 1) * d, s->xn_plane, K * d, B, X, G,
                    s->fw.part[4], s->fw.cnt[4], nullptr, 0, e);
   }
   p.g.dep = s->fw.f_dn;
@@ -476,6 +484,14 @@ const FwdPhase* fwd_table(ssd_session* s, int K, int lm_mode, int X, const EpiAr
   p.g.rms_units = nfb_d;
   p.g.rms_layer = dm.L;
   ph.push_back(p);
+  // rotations: each phase starts on the workgroups after the previous phase's
+  // items (attention counts its query groups, its fewest items)
+  int R = 0;
+  for (FwdPhase& q : ph) {
+    q.rot = R;
+    const int n = q.kind == FWD_GEMM ? q.g.items : ((att_groups + 7) / 8) * 8;
+    R = (R + n) % G;
+  }
   FwdPhase* dev = s->mem.get<FwdPhase>(ph.size());
   auto& slot = s->fw.tables[key];
   slot.first = std::move(ph);
@@ -560,7 +576,7 @@ void run_forward(ssd_session* s, int K, int lm_mode) {
       need(attn_partials_floats(dm, pf, B) <= s->apart_cap && (size_t)groups <= s->acnt_cap && groups <= s->fw.att_cap,
            "attention plan exceeds its workspace");
       need(d / FWD_FB <= s->ssq_parts_cap, "rms partial sums exceed their buffer");
-      const FwdPhase* tab = fwd_table(s, K, lm_mode, XF, base, groups);
+      const FwdPhase* tab = fwd_table(s, K, lm_mode, XF, G, base, groups);
       FwdArgs a{};
       a.phases = tab;
       a.n_phases = 5 * dm.L + 1;

@@ -206,19 +206,22 @@ struct AttnKArgs {
 
 // ---- persistent forward pass (kernels_fwd.hip) ----
 enum FwdKind { FWD_GEMM = 0, FWD_ATTN = 1 };
-// A GEMM phase: 64 output features x 512 k (16 k-blocks) per work item,
-// items = xcd_grid(n_fb, S, xcd) (item -> (feature block, split) by xcd_unmap).
+// A GEMM phase: 64 output features x (bursts x 512) k per work item,
+// items = xcd_grid(n_fb, S, xcd) (item -> (feature block, split) by xcd_unmap),
+// S = K / (bursts x 512).
 struct FwdGemm {
   const void* W;            // packed weights
-  int N, K, KB, n_fb, S, items, M;
+  int N, K, KB, n_fb, S, bursts, items, M;
   const uint16_t* in;       // split input planes [M][ld_in]
   size_t in_plane;
   int ld_in;
   // K-slice s (features [s*512, (s+1)*512) of the input) needs producer units
   // [s*512*dep_scale/dep_width, ceil((s+1)*512*dep_scale/dep_width)) of `dep`
-  // (dep_units > 0: every K-slice needs all units [0, dep_units) instead)
+  // (dep_units > 0: every K-slice needs all units [0, dep_units) instead;
+  // dep_att: the units are attention query groups, the slice needs those of
+  // its heads' KV heads)
   const unsigned* dep;      // nullptr: input ready before launch
-  int dep_width, dep_scale, dep_units, dep_layer;
+  int dep_width, dep_scale, dep_units, dep_att, dep_layer;
   // the epilogue's 1/rms needs all rms_units units of rms_dep
   const unsigned* rms_dep;
   int rms_units, rms_layer;
@@ -236,8 +239,12 @@ struct FwdAttn {
   const void* vc;
   unsigned* out_flags;      // one per query group
 };
+// Work item i of a phase runs on workgroup (i + rot) % grid (rot a multiple
+// of the XCD count): consecutive phases start on different workgroups, so the
+// workgroups still finishing one phase are not the first ones the next needs.
 struct FwdPhase {
   int kind;
+  int rot;
   FwdGemm g;
   FwdAttn a;
 };

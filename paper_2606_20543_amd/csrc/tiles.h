@@ -171,8 +171,8 @@ __device__ __forceinline__ void load_x_lds(uint16_t* xs, const uint16_t* in, siz
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
 #pragma unroll
   for (int r = w; r < X::MP; r += 4) {
-    const int rc = r < M ? r : M - 1;
-    const uint16_t* src = in + (size_t)rc * ld_in + k0 + lane * 8;
+    if (r >= M) break;  // rows past M are never stored (their LDS rows stay stale)
+    const uint16_t* src = in + (size_t)r * ld_in + k0 + lane * 8;
     __builtin_amdgcn_global_load_lds((const void __attribute__((address_space(1)))*)src,
                                      (void __attribute__((address_space(3)))*)(xs + r * X::LD), 16, 0, AUX);
     __builtin_amdgcn_global_load_lds((const void __attribute__((address_space(1)))*)(src + plane),
