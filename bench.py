@@ -16,7 +16,8 @@ Prints one JSON line (rank 0).  `value` comes from the timed steps, run with
 plain launches.  The same number of steps then runs again with every GEMM and
 attention launch timed by its own dispatch-timestamp HIP events (per-launch
 timing leaves gaps between kernels, so it stays out of the timed steps).
-Extra keys: `roofline` (the weight-streaming GEMM kernel, from those events),
+Extra keys: `roofline` (the weight-streaming GEMM kernel, from those events;
+with --forward persistent the single-launch forward kernel),
 `attention` (the same for the attention kernel), `cpu_baseline` (the oracle
 on the host cores on a bounded sample), AR tokens/s on the same kernels.
 """
@@ -32,7 +33,9 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
-GEMM_SRC = os.path.join(ROOT, "paper_2606_20543_amd", "csrc", "kernels_gemm.hip")
+# sources the GEMM kernel is compiled from (the traffic summary names their hash)
+GEMM_SRCS = [os.path.join(ROOT, "paper_2606_20543_amd", "csrc", f)
+             for f in ("kernels_gemm.hip", "tiles.h", "ssd_internal.h")]
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gemm_bf16_1b-24x24_traffic.md")
 
 
@@ -73,8 +76,11 @@ def gpu_greedy_ar(ssd, model, shape, prefix, n):
 
 def gemm_source_hash():
     import hashlib
-    with open(GEMM_SRC, "rb") as fh:
-        return hashlib.sha256(fh.read()).hexdigest()
+    h = hashlib.sha256()
+    for f in GEMM_SRCS:
+        with open(f, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
 
 
 def measured_traffic(workload):
@@ -87,7 +93,7 @@ def measured_traffic(workload):
     except OSError:
         return None
     kv = {k[2:].strip(): v.strip() for k, v in kv.items()}
-    if kv.get("workload") != workload or kv.get("kernels_gemm.hip sha256") != gemm_source_hash():
+    if kv.get("workload") != workload or kv.get("gemm sources sha256") != gemm_source_hash():
         return None
     try:
         return float(kv["hbm bytes per launch"])
@@ -116,7 +122,7 @@ def cpu_baseline(wl, w, prefix, drafts):
     shape = wl.model
     om = M.Model(M.Config(shape.n_layers, shape.d_model, shape.n_heads, shape.n_kv_heads, shape.head_dim,
                           shape.d_ff, shape.vocab, shape.img_lo, shape.img_hi, shape.dtype), w)
-    rows = min(12, wl.grid)  # about 10-20 s of host work on the 1B workload
+    rows = min(wl.grid, 24)  # the whole 24x24 image: about 10-20 s of host work on the 1B workload
     t0 = time.perf_counter()
     tok, st = Dc.decode_image(om, prefix, rows, wl.grid, drafts[:, :rows, :], rule=wl.rule, seed=3,
                               top_k=wl.top_k, b=wl.rounds)
@@ -142,6 +148,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--ar", action="store_true", help="also time greedy AR decoding (one pass per token)")
     ap.add_argument("--no-events", action="store_true", help="time without the per-launch event hook")
+    ap.add_argument("--forward", choices=("kernels", "persistent"), default="kernels",
+                    help="forward pass: one launch per projection/attention, or one cooperative launch per pass "
+                         "(blocks of up to 32 tokens)")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="only run a plain device copy of this size (PMC byte-counter calibration) and exit")
     args = ap.parse_args()
@@ -155,6 +164,7 @@ def main():
         return
 
     import torch
+    os.environ["SSD_FORWARD"] = args.forward  # read at model creation
     import paper_2606_20543_amd as ssd
     import synth
 
@@ -224,9 +234,11 @@ def main():
 
     ms_step = dt * 1000.0 / args.steps
     value = B * H * W / (dt / args.steps)
-    classes = ("qkv", "o_proj", "gate_up", "down", "lm_head", "attention")
+    classes = ("qkv", "o_proj", "gate_up", "down", "lm_head", "attention", "forward")
     if prof is None:
         prof = {c: (0.0, 0, 0.0) for c in classes}
+    f_ms, f_n, f_bytes = prof["forward"]
+    f_gbs = f_bytes / (f_ms / 1000.0) / 1e9 if f_ms > 0 else None
     gemm = [prof[c] for c in classes[:5]]
     g_ms = sum(x[0] for x in gemm)
     g_n = sum(x[1] for x in gemm)
@@ -254,7 +266,7 @@ def main():
         "data": "synthetic (random N(0,0.02) weights, random prompt ids, planted drafts)",
         "config": {"workload": wl.name, "batch": B, "prefix": P, "grid": f"{H}x{W}", "rule": wl.rule,
                    "rounds": wl.rounds, "k_h": 5, "k_v": 1, "top_k": wl.top_k, "planted_keep_p": p_keep,
-                   "passes_per_image": stats.passes, "parallelism": "single GPU"},
+                   "passes_per_image": stats.passes, "forward": args.forward, "parallelism": "single GPU"},
         "roofline": {"bound": "hbm", "kernel": "gemm_bf16_kernel (QKV/O/gate-up/down/LM-head weight streaming)",
                      "achieved": g_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": g_gbs / HBM_PEAK_GBS if g_gbs else None,
@@ -262,6 +274,10 @@ def main():
                      "bytes_per_launch": g_bytes / max(g_n, 1),
                      "timing": "dispatch-timestamp events (hipExtLaunchKernelGGL) on every launch of the profiled "
                                "region, which repeats the timed steps right after them"},
+        "forward_launch": {"bound": "hbm", "kernel": "fwd_kernel (whole backbone + output layer in one launch)",
+                           "achieved": f_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                           "frac": f_gbs / HBM_PEAK_GBS if f_gbs else None, "launches": f_n,
+                           "ms_per_launch": f_ms / max(f_n, 1), "bytes_per_launch": f_bytes / max(f_n, 1)},
         "attention": {"bound": "hbm", "achieved": a_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                       "frac": a_gbs / HBM_PEAK_GBS if a_gbs else None, "launches": a_n,
                       "ms_per_launch": a_ms / max(a_n, 1)},
@@ -271,6 +287,10 @@ def main():
         "ar_tokens_per_s_same_kernels": ar_rate,
         "speedup_vs_ar_same_kernels": (value / ar_rate) if ar_rate else None,
     }
+    if f_n > 0:
+        # the single-launch pass carries the weight stream: it is the kernel the roofline is about
+        result["roofline"] = dict(result["forward_launch"], traffic=None,
+                                  timing="event records around every cooperative launch of the profiled region")
     if not args.no_cpu_baseline:
         log("[bench] timing the oracle on the host cores")
         result["cpu_baseline"] = cpu_baseline(wl, w, prefix, drafts)
