@@ -275,6 +275,116 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmKArgs a) {
   }
 }
 
+// Wide workgroups for one-burst GEMMs: WV waves, each one 16-feature tile of
+// one 512-input K-slice, so that one workgroup per CU covers the launch.  A
+// grid of 4-wave workgroups that puts two workgroups on some CUs and one on
+// others finishes when the doubled CUs have received twice the bytes
+// (measured on a 384-workgroup QKV launch: those workgroups' weights landed
+// about 2 us after the others').  The K-slice's token rows are copied to LDS
+// by LDS DMA (no staging registers).
+template <int MT, int WV>
+__global__ __launch_bounds__(WV * 64) void gemm_wide_kernel(GemmKArgs a) {
+  constexpr int KCB = 16, NTH = WV * 64;
+  using X = XStage<MT, KCB>;
+  using RP = RmsPre<X::MP, GEMM_RMS_MAX_PARTS, NTH>;
+  __shared__ __attribute__((aligned(16))) uint16_t xs[2 * X::PL];
+  __shared__ float sq_red[WV][X::MP];
+  __shared__ float rscale[X::MP];
+  __shared__ float rms_red[NTH];
+  __shared__ int is_last;
+
+  int fb, s;
+  xcd_unmap(blockIdx.x, a.S, a.xcd, fb, s);
+  if (fb >= a.n_fb) return;
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int nb0 = fb * WV + w;
+  const int kb_split = s * KCB;
+  const EpiArgs& e = a.epi;
+
+  floatx4 acc[1][MT];
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt) acc[0][mt] = floatx4{0.f, 0.f, 0.f, 0.f};
+  EpiOps<1, MT> op;
+  u32x4 ra[1][KCB];
+  float rv[RP::RQ];
+  // issue order: block starts, rms partial sums, token rows, weights; the
+  // token rows go to LDS as soon as they land, the weights keep streaming
+  using XT = XStage<MT, KCB, NTH>;
+  u32x4 rx[2][XT::PASSES];
+  epi_block_starts<1, MT>(e, a.M, a.t0, lane, op);
+  rms_issue<X::MP, PlainMem, GEMM_RMS_MAX_PARTS, NTH>(e, a.in, a.M, a.t0, rv);
+  load_x<MT, KCB, XT::PASSES, PlainMem, NTH>(rx, a.in, a.in_plane, a.ld_in, a.M, kb_split * 32);
+  load_a<1, KCB>(ra, a.W, a.KB, nb0, a.N, kb_split, lane);
+  __builtin_amdgcn_sched_barrier(0);
+  rms_finish<X::MP, GEMM_RMS_MAX_PARTS, NTH>(e, rv, rms_red, rscale);
+  store_x<MT, KCB, XT::PASSES, NTH>(rx, xs);
+  lds_barrier();
+  compute_chunk<MT, 1, KCB>(acc, ra, xs, lane);
+
+  if (a.S > 1) {
+    const size_t frag = (size_t)MT * 64 * 4;
+    float* P = a.part + ((size_t)fb * WV + w) * frag;
+    const size_t split_stride = (size_t)a.n_fb * WV * frag;
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) *(floatx4*)(P + (size_t)s * split_stride + (mt * 64 + lane) * 4) = acc[0][mt];
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      if (!a.xcd) __threadfence();
+      unsigned prev = atomicAdd(&a.counters[fb], 1u);
+      is_last = (prev == (unsigned)(a.S - 1));
+      if (is_last && !a.xcd) __threadfence();
+    }
+    __syncthreads();
+    if (!is_last) return;
+  }
+  epi_load<1, MT>(e, nb0, a.N, a.M, a.t0, lane, op);
+  if (a.S > 1) {
+    const size_t frag = (size_t)MT * 64 * 4;
+    const float* P = a.part + ((size_t)fb * WV + w) * frag + lane * 4;
+    const size_t split_stride = (size_t)a.n_fb * WV * frag;
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) acc[0][mt] = floatx4{0.f, 0.f, 0.f, 0.f};
+    for (int s0 = 0; s0 < a.S; s0 += 8) {
+      floatx4 pv[8][MT];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const float* Ps = P + (size_t)min(s0 + j, a.S - 1) * split_stride;
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) pv[j][mt] = *(const floatx4*)(Ps + mt * 64 * 4);
+      }
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const float m = (s0 + j < a.S) ? 1.f : 0.f;
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) acc[0][mt] += pv[j][mt] * m;
+      }
+    }
+    if (threadIdx.x == 0) a.counters[fb] = 0u;
+  }
+  float sq[MT];
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt) sq[mt] = 0.f;
+  epi_store<1, MT>(e, acc, op, nb0, a.N, a.M, a.t0, lane, rscale, sq);
+  if (e.kind == EPI_RESID) {
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) {
+      float v = sq[mt];
+      v += __shfl_xor(v, 16);
+      v += __shfl_xor(v, 32);
+      if (lane < 16) sq_red[w][mt * 16 + lane] = v;
+    }
+    __syncthreads();
+    if (threadIdx.x < X::MP && threadIdx.x < a.M) {
+      const int tl = threadIdx.x;
+      float v = 0.f;
+#pragma unroll
+      for (int ww = 0; ww < WV; ++ww) v += sq_red[ww][tl];
+      e.ssq_out[(size_t)fb * e.ssq_out_ld + a.t0 + tl] = v;
+    }
+  }
+}
+
 GemmPlan gemm_plan_bf16(int M, int N, int K, int xcd) {
   GemmPlan p;
   p.xcd = xcd;
@@ -306,15 +416,44 @@ GemmPlan gemm_plan_bf16(int M, int N, int K, int xcd) {
     const bool two = s2 && kb / s2 == 16 && (!s1 || f1 * s1 > 512);
     if (two || s1) {
       p.NT = two ? 2 : 1;
+      p.WV = 4;
       p.bn = 64 * p.NT;
       p.n_fb = two ? f2 : f1;
       p.S = two ? s2 : s1;
       p.KCB = kb / p.S;
       p.kchunks = 1;
+      // Wide workgroups when two-tile waves leave the CUs unevenly loaded
+      // (grid not a multiple of the 256 CUs) and wide ones cover them exactly
+      // once each, cost = bytes through the busiest CU (weights + token rows).
+      // Measured on the 1B shapes: gate/up (352 two-tile workgroups -> 256 of
+      // 11 waves) 18.2 -> 16.4 us; one-tile grids (QKV 384 -> 256 of 6 waves,
+      // down 352 -> 176 of 8) and even grids (LM head 512) got slower.
+      auto cost = [&](int grid, int wv, int nt, int kcb) {
+        return (double)((grid + 255) / 256) * ((double)wv * nt * kcb * 1024 + (double)Mc * kcb * 32 * 4);
+      };
+      double best = cost(p.n_fb * p.S, 4, p.NT, p.KCB);
+      if (p.NT == 2 && (p.n_fb * p.S) % 256 != 0 && kb % 16 == 0 && N % 16 == 0) {
+        for (int wv : {6, 8, 11, 16}) {
+          if ((N / 16) % wv) continue;
+          const int nfb = N / 16 / wv, S = kb / 16;
+          if ((nfb * S) % 256 != 0) continue;
+          const double c = cost(nfb * S, wv, 1, 16);
+          if (c < 0.95 * best) {
+            best = c;
+            p.WV = wv;
+            p.NT = 1;
+            p.bn = 16 * wv;
+            p.n_fb = nfb;
+            p.S = S;
+            p.KCB = 16;
+          }
+        }
+      }
       return p;
     }
   }
   // double-buffered chunks
+  p.WV = 4;
   p.NT = p.MT >= 4 ? 2 : 1;
   p.bn = 4 * p.NT * 16;
   p.n_fb = (N + p.bn - 1) / p.bn;
@@ -337,7 +476,22 @@ GemmPlan gemm_plan_bf16(int M, int N, int K, int xcd) {
 size_t gemm_partials_floats(const GemmPlan& p, int M) {
   (void)M;
   if (p.S <= 1) return 0;
-  return (size_t)p.S * p.n_fb * 4 * p.NT * p.MT * 64 * 4;
+  return (size_t)p.S * p.n_fb * p.WV * p.NT * p.MT * 64 * 4;
+}
+
+template <int MT, int WV>
+static void launch_wide(const GemmKArgs& a, int n_fb, int S, hipStream_t st) {
+  launch_timed(gemm_wide_kernel<MT, WV>, dim3(xcd_grid(n_fb, S, a.xcd)), dim3(WV * 64), st, a);
+}
+
+template <int MT>
+static void launch_wide_mt(int wv, const GemmKArgs& a, int n_fb, int S, hipStream_t st) {
+  switch (wv) {
+    case 6: launch_wide<MT, 6>(a, n_fb, S, st); break;
+    case 8: launch_wide<MT, 8>(a, n_fb, S, st); break;
+    case 11: launch_wide<MT, 11>(a, n_fb, S, st); break;
+    default: launch_wide<MT, 16>(a, n_fb, S, st); break;
+  }
 }
 
 template <int MT, int NT, int KCB, int NBUF>
@@ -366,6 +520,11 @@ void gemm_bf16(const GemmPlan& p, const void* Wpacked, int N, int K, const void*
     a.part = partials;
     a.counters = counters;
     a.epi = epi;
+    if (p.WV != 4) {
+      if (p.MT == 1) launch_wide_mt<1>(p.WV, a, p.n_fb, p.S, st);
+      else launch_wide_mt<2>(p.WV, a, p.n_fb, p.S, st);
+      continue;
+    }
     switch (p.MT) {
       case 1:
         if (p.kchunks == 1 && p.KCB == 16 && p.NT == 2) launch_gemm<1, 2, 16, 1>(a, p.n_fb, p.S, st);

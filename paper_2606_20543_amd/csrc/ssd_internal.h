@@ -115,6 +115,7 @@ constexpr int GEMM_RMS_MAX_PARTS = 128;
 // GEMM launch plan for one (M, N, K) problem.
 struct GemmPlan {
   int MT, NT, KCB;  // token tiles, feature tiles per wave, 32-k blocks per chunk
+  int WV;           // waves per workgroup (4, or 6..16 for one-burst wide workgroups)
   int S;            // K splits
   int n_fb;         // feature blocks
   int kchunks;      // chunks per split

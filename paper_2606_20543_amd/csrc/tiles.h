@@ -131,22 +131,22 @@ __device__ __forceinline__ void load_a(u32x4 (&ra)[NT][KCB], const u32x4* W, int
     }
 }
 
-template <int MT, int KCB>
+template <int MT, int KCB, int NTH = 256>
 struct XStage {
   static constexpr int MP = MT * 16;
   static constexpr int KC = KCB * 32;
   static constexpr int LD = KC + 8;          // bf16 per LDS row (16-byte pad)
   static constexpr int PL = MP * LD;         // one plane
   static constexpr int CG = KC / 8;          // 16-byte column groups per row
-  static constexpr int RSTEP = 256 / CG;     // rows covered per pass
+  static constexpr int RSTEP = NTH / CG;     // rows covered per pass (NTH threads)
   static constexpr int PASSES = (MP + RSTEP - 1) / RSTEP;
 };
 
 // x chunk (both planes) -> registers
-template <int MT, int KCB, int NP, class Mem = PlainMem>
+template <int MT, int KCB, int NP, class Mem = PlainMem, int NTH = 256>
 __device__ __forceinline__ void load_x(u32x4 (&rx)[2][NP], const uint16_t* in, size_t plane, int ld_in, int M,
                                        int k0) {
-  using X = XStage<MT, KCB>;
+  using X = XStage<MT, KCB, NTH>;
   const int cg = threadIdx.x % X::CG, r0 = threadIdx.x / X::CG;
   // token rows past M repeat row M-1: no branch around the loads (so they
   // issue back to back); the results of those rows are never stored
@@ -164,13 +164,13 @@ __device__ __forceinline__ void load_x(u32x4 (&rx)[2][NP], const uint16_t* in, s
 // registers): wave w copies rows w, w + 4, ... of both planes, one 1 KiB row
 // per instruction.  AUX: cache policy of the global reads.  The caller waits
 // for vmcnt(0) and then barriers before the LDS is read.
-template <int MT, int KCB, int AUX>
+template <int MT, int KCB, int AUX, int NW = 4>
 __device__ __forceinline__ void load_x_lds(uint16_t* xs, const uint16_t* in, size_t plane, int ld_in, int M, int k0) {
   using X = XStage<MT, KCB>;
   static_assert(X::KC == 512, "one 512-input row per wave instruction");
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
 #pragma unroll
-  for (int r = w; r < X::MP; r += 4) {
+  for (int r = w; r < X::MP; r += NW) {
     if (r >= M) break;  // rows past M are never stored (their LDS rows stay stale)
     const uint16_t* src = in + (size_t)r * ld_in + k0 + lane * 8;
     __builtin_amdgcn_global_load_lds((const void __attribute__((address_space(1)))*)src,
@@ -180,9 +180,9 @@ __device__ __forceinline__ void load_x_lds(uint16_t* xs, const uint16_t* in, siz
   }
 }
 
-template <int MT, int KCB, int NP>
+template <int MT, int KCB, int NP, int NTH = 256>
 __device__ __forceinline__ void store_x(const u32x4 (&rx)[2][NP], uint16_t* xs) {
-  using X = XStage<MT, KCB>;
+  using X = XStage<MT, KCB, NTH>;
   const int cg = threadIdx.x % X::CG, r0 = threadIdx.x / X::CG;
 #pragma unroll
   for (int p = 0; p < NP; ++p) {
@@ -226,17 +226,17 @@ __device__ __forceinline__ void compute_chunk(floatx4 (&acc)[NT][MT], const u32x
 // into registers before the weight burst is issued (so the wait for them does
 // not wait for the weights), sums them in part order, and the G group sums
 // meet in LDS (summed in group order: deterministic).
-template <int MP, int PARTS = GEMM_RMS_MAX_PARTS>
+template <int MP, int PARTS = GEMM_RMS_MAX_PARTS, int NTH = 256>
 struct RmsPre {
-  static constexpr int G = 256 / MP;
+  static constexpr int G = NTH / MP;
   static constexpr int RQ = (PARTS + G - 1) / G;
 };
 
 // raw loads only (no use of the values, so nothing waits for them here);
 // without partial sums (ssq == nullptr) the loads read in[0] and are ignored
-template <int MP, class Mem = PlainMem, int PARTS = GEMM_RMS_MAX_PARTS>
+template <int MP, class Mem = PlainMem, int PARTS = GEMM_RMS_MAX_PARTS, int NTH = 256>
 __device__ __forceinline__ void rms_issue(const EpiArgs& e, const void* dummy, int M, int t0,
-                                          float (&v)[RmsPre<MP, PARTS>::RQ]) {
+                                          float (&v)[RmsPre<MP, PARTS, NTH>::RQ]) {
   const int t = threadIdx.x % MP, pg = threadIdx.x / MP;
   const int tc = t < M ? t : M - 1;
   const bool has = e.ssq != nullptr;
@@ -244,28 +244,28 @@ __device__ __forceinline__ void rms_issue(const EpiArgs& e, const void* dummy, i
   const size_t c = has ? (size_t)e.ssq_off + (size_t)(t0 + tc) * e.ssq_step : 0;
   const size_t ld = has ? (size_t)e.ssq_ld : 0;
 #pragma unroll
-  for (int q = 0; q < RmsPre<MP, PARTS>::RQ; ++q) {
-    const int p = pg + q * RmsPre<MP, PARTS>::G;
+  for (int q = 0; q < RmsPre<MP, PARTS, NTH>::RQ; ++q) {
+    const int p = pg + q * RmsPre<MP, PARTS, NTH>::G;
     v[q] = Mem::ld4f(base, ((size_t)(p < e.ssq_parts ? p : 0) * ld + c) * 4);
   }
 }
 
 // writes rscale[0..MP); visible after the caller's next barrier
-template <int MP, int PARTS = GEMM_RMS_MAX_PARTS>
-__device__ __forceinline__ void rms_finish(const EpiArgs& e, const float (&v)[RmsPre<MP, PARTS>::RQ], float* red,
+template <int MP, int PARTS = GEMM_RMS_MAX_PARTS, int NTH = 256>
+__device__ __forceinline__ void rms_finish(const EpiArgs& e, const float (&v)[RmsPre<MP, PARTS, NTH>::RQ], float* red,
                                            float* rscale) {
   // branch-free in ssq (a branch here would make the compiler settle the
   // weight loads at the join); without partial sums the scale is 1
   const int pg = threadIdx.x / MP;
   float s = 0.f;
 #pragma unroll
-  for (int q = 0; q < RmsPre<MP, PARTS>::RQ; ++q) s += (pg + q * RmsPre<MP, PARTS>::G < e.ssq_parts) ? v[q] : 0.f;
+  for (int q = 0; q < RmsPre<MP, PARTS, NTH>::RQ; ++q) s += (pg + q * RmsPre<MP, PARTS, NTH>::G < e.ssq_parts) ? v[q] : 0.f;
   red[threadIdx.x] = s;  // [pg][t]
   lds_barrier();
   if (threadIdx.x < MP) {
     float a = 0.f;
 #pragma unroll
-    for (int g = 0; g < RmsPre<MP, PARTS>::G; ++g) a += red[g * MP + threadIdx.x];
+    for (int g = 0; g < RmsPre<MP, PARTS, NTH>::G; ++g) a += red[g * MP + threadIdx.x];
     rscale[threadIdx.x] = e.ssq ? 1.0f / sqrtf(a * e.inv_d + e.eps) : 1.f;
   }
 }
