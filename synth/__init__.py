@@ -151,6 +151,30 @@ def weights(m, seed=SEED_WEIGHTS, std=0.02, gain_std=0.0):
     return buf
 
 
+SEED_HEADS = 4
+
+
+def draft_head_weights(d, m, seed=SEED_HEADS, std=0.02, gain_std=0.0):
+    """Packed bf16 bits of one spatial draft head: W0 [d][2d], gain [d], W1 [m][d],
+    W3 [m][d], W2 [d][m] (tensor j on generator stream j; gains around 1)."""
+    shapes = [("w0", (d, 2 * d)), ("g", (d,)), ("w1", (m, d)), ("w3", (m, d)), ("w2", (d, m))]
+    total = int(sum(np.prod(s) for _, s in shapes))
+    buf = np.empty(total, dtype=np.uint16)
+    off = 0
+    base = buf.ctypes.data
+    for j, (name, shape) in enumerate(shapes):
+        n = int(np.prod(shape))
+        mean, sd = (1.0, gain_std) if name == "g" else (0.0, std)
+        lib().synth_normal_bf16(seed, j, mean, sd, n, ctypes.c_void_p(base + off * 2))
+        off += n
+    return buf
+
+
+def hidden_states(R, d, seed=SEED_HEADS, stream=100, std=1.0):
+    """Synthetic pre-norm hidden states [R][d] (float32), N(0, std)."""
+    return normal(seed, stream, R * d, std=std).astype(np.float32).reshape(R, d)
+
+
 def prompt(m, B, P, seed=SEED_PROMPT):
     lo, hi = (0, m.img_lo) if m.img_lo > 0 else (0, m.vocab)
     return randint(seed, 0, lo, hi, B * P).reshape(B, P)
