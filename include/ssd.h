@@ -224,6 +224,39 @@ ssd_status ssd_decode_image(ssd_model* model, const ssd_schedule* sched, int32_t
 ssd_status ssd_profile(ssd_model* model, int32_t enable);
 ssd_status ssd_profile_read(ssd_model* model, double* ms, int64_t* launches, double* bytes, int32_t reset);
 
+/*
+ * Spatial draft head f_phi (Sec. 3.3 "Draft Prediction in Latent Space",
+ * Eq. 2).  From the last layer's pre-norm hidden state h of a decoded
+ * position and the embedding e of its token, a head predicts the state at
+ * its spatial offset,
+ *     u = W0 [h; e],   h_hat = u + W2 (silu(W1 n) * (W3 n)),   n = g * u / rms(u),
+ * and drafts argmax_v GenHead(RMSNorm(h_hat))_v through the backbone's own
+ * final norm and output layer (image codes only).  A vertical head drafts a
+ * whole row below a committed row in one call (rows are independent).
+ *
+ * ssd_draft_head_numel: element count of the packed head weights for the
+ *   model's d_model and the head's inner size m (-1 if invalid).
+ * ssd_draft_head_init: weights in the model's dtype (bf16 models only), host
+ *   or device, packed W0 [d][2d] (columns: h then e), g [d], W1 [m][d],
+ *   W3 [m][d], W2 [d][m]; m a positive multiple of 256; max_rows >= 1 bounds
+ *   R of every run.  The head is tied to the model (free it first) and runs
+ *   on the model's stream.
+ * ssd_draft_head_run: h [R][d] fp32 pre-norm states (e.g. the h_pre_out of a
+ *   commit pass), tokens [R] vocabulary ids of the same positions; writes
+ *   drafts [R] (absolute image-code ids: lowest id among equal maxima) and,
+ *   if logits_out != NULL, the draft logits [R][V_img] fp32 (their softmax is
+ *   the draft distribution q of rule C).  Synchronizes when an output is in
+ *   host memory.  Errors as for the other entry points (SSD_E_DEVICE poisons
+ *   the head).
+ */
+typedef struct ssd_draft_head ssd_draft_head;
+int64_t ssd_draft_head_numel(const ssd_model* model, int32_t m);
+ssd_status ssd_draft_head_init(ssd_model* model, int32_t m, const void* weights, int32_t max_rows,
+                               ssd_draft_head** out);
+ssd_status ssd_draft_head_run(ssd_draft_head* head, int32_t R, const float* h, const int32_t* tokens,
+                              int32_t* drafts, float* logits_out);
+void ssd_free_draft_head(ssd_draft_head* head);
+
 /* Thread-local description of the last error (empty string if none). */
 const char* ssd_last_error(void);
 

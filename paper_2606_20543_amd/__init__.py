@@ -20,6 +20,7 @@ SSD_GREEDY, SSD_SAMPLE, SSD_ACCEPT_REJECT = 0, 1, 2
 EXPORTED = [
     "ssd_init_model", "ssd_weights_numel", "ssd_free_model", "ssd_prefill", "ssd_free_session",
     "ssd_verify_step", "ssd_get_carry", "ssd_decode_image", "ssd_profile", "ssd_profile_read", "ssd_last_error",
+    "ssd_draft_head_numel", "ssd_draft_head_init", "ssd_draft_head_run", "ssd_free_draft_head",
 ]
 
 
@@ -79,10 +80,16 @@ def lib():
                                        ctypes.POINTER(ssd_stats), vp]
         L.ssd_profile.argtypes = [vp, i32]
         L.ssd_profile_read.argtypes = [vp, vp, vp, vp, i32]
+        L.ssd_draft_head_numel.argtypes = [vp, i32]
+        L.ssd_draft_head_numel.restype = i64
+        L.ssd_draft_head_init.argtypes = [vp, i32, vp, i32, ctypes.POINTER(vp)]
+        L.ssd_draft_head_run.argtypes = [vp, i32, vp, vp, vp, vp]
+        L.ssd_free_draft_head.argtypes = [vp]
+        L.ssd_free_draft_head.restype = None
         L.ssd_last_error.argtypes = []
         L.ssd_last_error.restype = ctypes.c_char_p
         for name in ("ssd_init_model", "ssd_prefill", "ssd_verify_step", "ssd_get_carry", "ssd_decode_image",
-                     "ssd_profile", "ssd_profile_read"):
+                     "ssd_profile", "ssd_profile_read", "ssd_draft_head_init", "ssd_draft_head_run"):
             getattr(L, name).restype = i32
         _lib = L
     return _lib
@@ -153,6 +160,25 @@ def ssd_decode_image(model, sched, B, P, prefix, drafts, out_tokens, draft_logit
     _check(lib().ssd_decode_image(ctypes.c_void_p(model), ctypes.byref(sched), B, P, _ptr(prefix), _ptr(drafts),
                                   _ptr(draft_logits), _ptr(out_tokens), ctypes.byref(st), _ptr(stream)))
     return st
+
+
+def ssd_draft_head_numel(model, m):
+    return int(lib().ssd_draft_head_numel(ctypes.c_void_p(model), m))
+
+
+def ssd_draft_head_init(model, m, weights, max_rows):
+    out = ctypes.c_void_p()
+    _check(lib().ssd_draft_head_init(ctypes.c_void_p(model), m, _ptr(weights), max_rows, ctypes.byref(out)))
+    return out.value
+
+
+def ssd_draft_head_run(head, R, h, tokens, drafts, logits_out=None):
+    _check(lib().ssd_draft_head_run(ctypes.c_void_p(head), R, _ptr(h), _ptr(tokens), _ptr(drafts),
+                                    _ptr(logits_out)))
+
+
+def ssd_free_draft_head(head):
+    lib().ssd_free_draft_head(ctypes.c_void_p(head))
 
 
 def ssd_profile(model, enable):

@@ -594,6 +594,30 @@ __global__ __launch_bounds__(NT_SEL) void first_token_kernel(int Vimg, int img_l
   if (threadIdx.x == 0) out_abs[(size_t)b * out_stride] = v + img_lo;
 }
 
+// Draft-head input z = [h; e] as split bf16 planes [R][2d]: h fp32 (hi/lo),
+// e the bf16 embedding row of the token (exact in the hi plane).
+__global__ __launch_bounds__(256) void draft_input_kernel(const float* h, const uint16_t* emb, const int* tok, int d,
+                                                          uint16_t* z, size_t plane) {
+  const int r = blockIdx.x;
+  const float* hr = h + (size_t)r * d;
+  const uint16_t* er = emb + (size_t)tok[r] * d;
+  uint16_t* zr = z + (size_t)r * 2 * d;
+  for (int i = threadIdx.x; i < d; i += blockDim.x) {
+    const float v = hr[i];
+    const uint16_t hi = f2bf_m(v);
+    zr[i] = hi;
+    zr[plane + i] = f2bf_m(v - __uint_as_float((uint32_t)hi << 16));
+    zr[d + i] = er[i];
+    zr[plane + d + i] = 0;
+  }
+}
+
+void draft_input(const float* h, const void* emb, const int* tok, int R, int d, void* z, size_t plane,
+                 hipStream_t st) {
+  hipLaunchKernelGGL(draft_input_kernel, dim3(R), dim3(256), 0, st, h, (const uint16_t*)emb, tok, d, (uint16_t*)z,
+                     plane);
+}
+
 void first_token(int B, int Vimg, int img_lo, const float* carry, int rule, int top_k, double temperature,
                  unsigned long long seed, const int* f, int* out_abs, int out_stride, hipStream_t st) {
   hipLaunchKernelGGL(first_token_kernel, dim3(B), dim3(NT_SEL), 0, st, Vimg, img_lo, carry, rule, top_k, temperature,

@@ -1135,6 +1135,240 @@ ssd_status ssd_prefill(ssd_model* m, int32_t B, int32_t P, const int32_t* prefix
   return SSD_OK;
 }
 
+}  // extern "C"
+
+// ---------------- spatial draft head ----------------
+struct ssd_draft_head {
+  ssd_model* m;
+  int d, mi, Rmax;
+  bool poisoned = false;
+  Allocs mem;
+  void* w0;      // packed [d][2d]
+  float* g;      // [d]
+  void* w13;     // packed [2m][d], gate/up rows interleaved
+  void* w2;      // packed [d][m]
+  int* tok;      // [Rmax]
+  int* out;      // [Rmax]
+  int* f0;       // one zero: the epilogues' block-start lookup
+  float* hin;    // [Rmax][d]
+  void* z;       // [Rmax][2d] split planes
+  size_t z_plane;
+  float* x;      // [Rmax][d] fp32: u, then h_hat
+  void* xn;      // [Rmax][d] split planes
+  size_t xn_plane;
+  float* ssq;    // [parts][Rmax]
+  int ssq_cap;
+  void* hb;      // [Rmax][m] split planes
+  size_t hb_plane;
+  float* logits; // [Rmax][V_img]
+  float* gpart;
+  size_t gpart_cap;
+  unsigned* gcnt;
+  size_t gcnt_cap;
+};
+
+extern "C" {
+
+int64_t ssd_draft_head_numel(const ssd_model* m, int32_t mi) {
+  if (!m || mi <= 0) return -1;
+  const int64_t d = m->dm.d;
+  return 2 * d * d + d + 3 * (int64_t)mi * d;
+}
+
+ssd_status ssd_draft_head_init(ssd_model* m, int32_t mi, const void* weights, int32_t max_rows,
+                               ssd_draft_head** out) {
+  g_err.clear();
+  if (!m || !weights || !out) return fail(SSD_E_INVAL, "NULL argument");
+  *out = nullptr;
+  if (m->poisoned) return fail(SSD_E_STATE, "model is poisoned by an earlier device error");
+  const Dims& dm = m->dm;
+  if (!dm.bf16) return fail(SSD_E_INVAL, "draft heads need a bf16 model");
+  if (mi <= 0 || mi % 256 != 0 || mi > (1 << 16)) return fail(SSD_E_INVAL, "m must be a positive multiple of 256");
+  if (max_rows < 1 || max_rows > (1 << 16)) return fail(SSD_E_INVAL, "max_rows must be in [1, 65536]");
+  auto* h = new ssd_draft_head();
+  h->m = m;
+  h->d = dm.d;
+  h->mi = mi;
+  h->Rmax = max_rows;
+  const int d = dm.d;
+  const size_t R = max_rows;
+  hipStream_t st = m->stream;
+  try {
+    Allocs tmp;
+    const size_t max_seg = std::max({(size_t)d * 2 * d, (size_t)2 * mi * d, (size_t)d * mi});
+    uint16_t* stage = tmp.get<uint16_t>(max_seg);
+    std::vector<int> map_id(std::max({2 * d, 2 * mi, d})), map_13(2 * mi);
+    for (size_t n = 0; n < map_id.size(); ++n) map_id[n] = (int)n;
+    for (int n = 0; n < 2 * mi; ++n) map_13[n] = (n % 2 == 0) ? n / 2 : mi + n / 2;
+    int* d_id = tmp.get<int>(map_id.size());
+    int* d_13 = tmp.get<int>(map_13.size());
+    HIPCHK(hipMemcpy(d_id, map_id.data(), map_id.size() * 4, hipMemcpyHostToDevice));
+    HIPCHK(hipMemcpy(d_13, map_13.data(), map_13.size() * 4, hipMemcpyHostToDevice));
+    const uint16_t* src = (const uint16_t*)weights;
+    auto pack = [&](size_t off, int N, int K, const int* map) -> void* {
+      HIPCHK(hipMemcpy(stage, src + off, (size_t)N * K * 2, hipMemcpyDefault));
+      void* dst = h->mem.get<char>((size_t)N * K * 2);
+      pack_bf16_tiles(stage, map, N, K, dst, st);
+      HIPCHK(hipGetLastError());
+      HIPCHK(hipStreamSynchronize(st));
+      return dst;
+    };
+    size_t off = 0;
+    h->w0 = pack(off, d, 2 * d, d_id);
+    off += (size_t)d * 2 * d;
+    {
+      std::vector<uint16_t> hb(d);
+      HIPCHK(hipMemcpy(hb.data(), src + off, (size_t)d * 2, hipMemcpyDefault));
+      std::vector<float> hf(d);
+      for (int i = 0; i < d; ++i) {
+        uint32_t u = (uint32_t)hb[i] << 16;
+        std::memcpy(&hf[i], &u, 4);
+      }
+      h->g = h->mem.get<float>(d);
+      HIPCHK(hipMemcpy(h->g, hf.data(), (size_t)d * 4, hipMemcpyHostToDevice));
+    }
+    off += d;
+    h->w13 = pack(off, 2 * mi, d, d_13);
+    off += (size_t)2 * mi * d;
+    h->w2 = pack(off, d, mi, d_id);
+    // workspaces for every plan a run of up to max_rows rows can meet
+    size_t gpart = 0, gcnt = 0;
+    int parts = 1;
+    for (int Mc : {1, 16, 17, 32, 33, 64, 65, 128}) {
+      for (auto nk : {std::make_pair(d, 2 * d), std::make_pair(2 * mi, d), std::make_pair(d, mi),
+                      std::make_pair(dm.Vimg, d)}) {
+        GemmPlan p = gemm_plan_bf16(Mc, nk.first, nk.second, 0);
+        gpart = std::max(gpart, gemm_partials_floats(p, Mc));
+        gcnt = std::max(gcnt, (size_t)p.n_fb);
+        if (nk.first == d) parts = std::max(parts, p.n_fb);
+      }
+    }
+    h->gpart_cap = gpart;
+    h->gpart = h->mem.get<float>(gpart);
+    h->gcnt_cap = gcnt;
+    h->gcnt = h->mem.get<unsigned>(gcnt);
+    h->ssq_cap = parts;
+    h->ssq = h->mem.get<float>((size_t)parts * R);
+    h->tok = h->mem.get<int>(R);
+    h->out = h->mem.get<int>(R);
+    h->f0 = h->mem.get<int>(1);
+    h->hin = h->mem.get<float>(R * d);
+    h->z_plane = R * 2 * d;
+    h->z = h->mem.get<char>(R * 2 * d * 4);
+    h->x = h->mem.get<float>(R * d);
+    h->xn_plane = R * d;
+    h->xn = h->mem.get<char>(R * d * 4);
+    h->hb_plane = R * mi;
+    h->hb = h->mem.get<char>(R * mi * 4);
+    h->logits = h->mem.get<float>(R * dm.Vimg);
+    fill_u32(h->gcnt, gcnt, 0u, st);
+    fill_u32((unsigned*)h->f0, 1, 0u, st);
+    HIPCHK(hipGetLastError());
+    HIPCHK(hipStreamSynchronize(st));
+  } catch (HipError& e) {
+    delete h;
+    if (e.e == hipErrorOutOfMemory || std::string(e.what) == "hipMalloc")
+      return fail(SSD_E_OOM, "device allocation failed (%s)", hipGetErrorString(e.e));
+    return fail(SSD_E_DEVICE, "%s: %s", e.what, hipGetErrorString(e.e));
+  }
+  *out = h;
+  return SSD_OK;
+}
+
+ssd_status ssd_draft_head_run(ssd_draft_head* h, int32_t R, const float* hs, const int32_t* tokens, int32_t* drafts,
+                              float* logits_out) {
+  g_err.clear();
+  if (!h || !hs || !tokens || !drafts) return fail(SSD_E_INVAL, "NULL argument");
+  if (h->poisoned || h->m->poisoned) return fail(SSD_E_STATE, "draft head or model is poisoned");
+  if (R < 1 || R > h->Rmax) return fail(SSD_E_INVAL, "R = %d outside [1, max_rows = %d]", R, h->Rmax);
+  ssd_model* m = h->m;
+  const Dims& dm = m->dm;
+  const int d = h->d, mi = h->mi;
+  if (!is_device_ptr(tokens)) {
+    ssd_status cs = check_tokens_host(tokens, (size_t)R, 0, dm.V, "tokens");
+    if (cs != SSD_OK) return cs;
+  }
+  const bool host_out = !is_device_ptr(drafts) || (logits_out && !is_device_ptr(logits_out));
+  hipStream_t st = m->stream;
+  try {
+    HIPCHK(hipMemcpyAsync(h->hin, hs, (size_t)R * d * 4, hipMemcpyDefault, st));
+    HIPCHK(hipMemcpyAsync(h->tok, tokens, (size_t)R * 4, hipMemcpyDefault, st));
+    draft_input(h->hin, m->emb, h->tok, R, d, h->z, h->z_plane, st);
+    fill_u32((unsigned*)h->x, (size_t)R * d, 0u, st);  // u accumulates onto zero
+    const int X = m->xcd;
+    EpiArgs base{};
+    base.Kblk = h->Rmax;  // every row is block position t of "sequence" 0
+    base.f = h->f0;
+    base.ssq_ld = h->Rmax;
+    base.ssq_step = 1;
+    base.inv_d = 1.0f / (float)d;
+    base.eps = dm.eps;
+    base.Hq = dm.Hq;
+    base.Hkv = dm.Hkv;
+    base.D = dm.D;
+    base.x = h->x;
+    base.xn = h->xn;
+    base.xn_plane = h->xn_plane;
+    base.ssq_out = h->ssq;
+    base.ssq_out_ld = h->Rmax;
+    base.h = h->hb;
+    base.h_plane = h->hb_plane;
+    base.logits = h->logits;
+    auto plan = [&](int N, int K) {
+      GemmPlan p = gemm_plan_bf16(R, N, K, X);
+      if (gemm_partials_floats(p, R) > h->gpart_cap || (size_t)p.n_fb > h->gcnt_cap ||
+          (N == d && p.n_fb > h->ssq_cap))
+        throw HipError{hipErrorInvalidValue, "GEMM plan exceeds the draft head's workspace"};
+      return p;
+    };
+    // u = W0 [h; e]; n = g * u (and the parts of sum u^2)
+    GemmPlan p0 = plan(d, 2 * d);
+    EpiArgs e = base;
+    e.kind = EPI_RESID;
+    e.gnext = h->g;
+    e.ld = d;
+    gemm_bf16(p0, h->w0, d, 2 * d, h->z, h->z_plane, 2 * d, R, e, h->gpart, h->gcnt, st);
+    // SwiGLU(n / rms(u))
+    GemmPlan p1 = plan(2 * mi, d);
+    e = base;
+    e.kind = EPI_SWIGLU;
+    e.ssq = h->ssq;
+    e.ssq_parts = p0.n_fb;
+    e.ld = mi;
+    gemm_bf16(p1, h->w13, 2 * mi, d, h->xn, h->xn_plane, d, R, e, h->gpart, h->gcnt, st);
+    // h_hat = u + W2 (...); n = g_f * h_hat for the output layer
+    GemmPlan p2 = plan(d, mi);
+    e = base;
+    e.kind = EPI_RESID;
+    e.gnext = m->gf;
+    e.ld = d;
+    gemm_bf16(p2, h->w2, d, mi, h->hb, h->hb_plane, mi, R, e, h->gpart, h->gcnt, st);
+    // GenHead(RMSNorm(h_hat)) over the image codes, then the argmax
+    GemmPlan p3 = plan(dm.Vimg, d);
+    e = base;
+    e.kind = EPI_LOGITS;
+    e.ssq = h->ssq;
+    e.ssq_parts = p2.n_fb;
+    e.ld = dm.Vimg;
+    gemm_bf16(p3, m->wlm, dm.Vimg, d, h->xn, h->xn_plane, d, R, e, h->gpart, h->gcnt, st);
+    first_token(R, dm.Vimg, dm.img_lo, h->logits, SSD_GREEDY, 0, 1.0, 0, nullptr, h->out, 1, st);
+    HIPCHK(hipGetLastError());
+    HIPCHK(hipMemcpyAsync(drafts, h->out, (size_t)R * 4, hipMemcpyDefault, st));
+    if (logits_out) HIPCHK(hipMemcpyAsync(logits_out, h->logits, (size_t)R * dm.Vimg * 4, hipMemcpyDefault, st));
+    if (host_out) HIPCHK(hipStreamSynchronize(st));
+  } catch (HipError& e) {
+    h->poisoned = true;
+    return fail(SSD_E_DEVICE, "%s: %s", e.what, hipGetErrorString(e.e));
+  }
+  return SSD_OK;
+}
+
+void ssd_free_draft_head(ssd_draft_head* h) {
+  if (!h) return;
+  (void)hipStreamSynchronize(h->m->stream);
+  delete h;
+}
+
 ssd_status ssd_profile(ssd_model* m, int32_t enable) {
   if (!m) return fail(SSD_E_INVAL, "NULL model");
   try {

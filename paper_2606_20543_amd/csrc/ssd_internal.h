@@ -317,6 +317,9 @@ void xcc_probe(int* out, int n_wg, hipStream_t st);
 // references of block positions f+k <- src rows (b * rows_per_b + k); only_new keeps existing references
 void set_ref_rows(int B, int K, int rows_per_b, int Vimg, const float* src, const int* f, float* ref, int* ref_flag,
                   int ring, int only_new, hipStream_t st);
+// z = [h; e] split planes [R][2d] (plane elements apart) for a draft head
+void draft_input(const float* h, const void* emb, const int* tok, int R, int d, void* z, size_t plane,
+                 hipStream_t st);
 void first_token(int B, int Vimg, int img_lo, const float* carry, int rule, int top_k, double temperature,
                  unsigned long long seed, const int* f, int* out_abs, int out_stride, hipStream_t st);
 

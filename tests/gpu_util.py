@@ -22,6 +22,46 @@ from oracle import select as R
 TOL = {"f32": 1e-5, "bf16": 2e-2}
 
 
+class DeviceArray:
+    """Device memory from the HIP runtime the library itself links (not torch's, which
+    ships its own runtime), for calls with device pointers."""
+
+    _hip = None
+
+    @classmethod
+    def hip(cls):
+        import ctypes
+        if cls._hip is None:
+            ssd.lib()  # the library's runtime is then already loaded under this name
+            h = ctypes.CDLL("libamdhip64.so.7")
+            h.hipMalloc.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_size_t]
+            h.hipMemcpy.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int]
+            h.hipFree.argtypes = [ctypes.c_void_p]
+            h.hipDeviceSynchronize.argtypes = []
+            cls._hip = h
+        return cls._hip
+
+    def __init__(self, host):
+        import ctypes
+        self.shape, self.dtype = host.shape, host.dtype
+        self.nbytes = host.nbytes
+        p = ctypes.c_void_p()
+        assert self.hip().hipMalloc(ctypes.byref(p), self.nbytes) == 0
+        self.ptr = p.value
+        assert self.hip().hipMemcpy(self.ptr, host.ctypes.data, self.nbytes, 1) == 0  # host to device
+
+    def numpy(self):
+        out = np.empty(self.shape, self.dtype)
+        assert self.hip().hipDeviceSynchronize() == 0
+        assert self.hip().hipMemcpy(out.ctypes.data, self.ptr, self.nbytes, 2) == 0  # device to host
+        return out
+
+    def free(self):
+        if self.ptr:
+            self.hip().hipFree(self.ptr)
+            self.ptr = None
+
+
 def cfg_of(shape):
     c = ssd.ssd_model_config()
     c.n_layers, c.d_model, c.n_heads, c.n_kv_heads = shape.n_layers, shape.d_model, shape.n_heads, shape.n_kv_heads

@@ -104,4 +104,8 @@ def test_null_arguments_rejected_before_device_work(lib):
     assert L.ssd_decode_image(None, ctypes.byref(sc), 1, 1, None, None, None, None, None, None) == ssd.SSD_E_INVAL
     assert L.ssd_get_carry(None, None) == ssd.SSD_E_INVAL
     assert L.ssd_profile(None, 1) == ssd.SSD_E_INVAL
+    assert L.ssd_draft_head_init(None, 256, None, 1, ctypes.byref(out)) == ssd.SSD_E_INVAL
+    assert L.ssd_draft_head_run(None, 1, None, None, None, None) == ssd.SSD_E_INVAL
+    assert L.ssd_draft_head_numel(None, 256) == -1
+    L.ssd_free_draft_head(None)  # a no-op
     assert "NULL" in ssd.ssd_last_error()
