@@ -18,7 +18,8 @@ attention launch timed by its own dispatch-timestamp HIP events (per-launch
 timing leaves gaps between kernels, so it stays out of the timed steps).
 Extra keys: `roofline` (the weight-streaming GEMM kernel, from those events;
 with --forward persistent the single-launch forward kernel),
-`attention` (the same for the attention kernel), `cpu_baseline` (the oracle
+`attention` (the same for the attention kernel), `draft_head` (the spatial
+draft head drafting one grid row per call, timed apart from the steps), `cpu_baseline` (the oracle
 on the host cores on a bounded sample), AR tokens/s on the same kernels.
 """
 import argparse
@@ -115,6 +116,38 @@ def copy_calibration(mib):
     log(f"[bench] copied {mib} MiB three times (calibration)")
 
 
+def draft_head_cost(ssd, model, shape, tokens, calls=50):
+    """Time the spatial draft head f_phi (Eq. 2) drafting one grid row per call:
+    inner size m = 2d (the paper's head size), seeded weights, synthetic hidden
+    states.  Not part of `value`: the timed steps verify planted drafts."""
+    import torch
+    import synth
+    d, m, R = shape.d_model, 2 * shape.d_model, tokens.shape[0]
+    head = ssd.ssd_draft_head_init(model, m, synth.draft_head_weights(d, m), R)
+    try:
+        dev = torch.device("cuda:0")
+        d_h = torch.from_numpy(synth.hidden_states(R, d)).to(dev)
+        d_tok = torch.from_numpy(tokens.astype(np.int32)).to(dev)
+        d_dr = torch.zeros(R, dtype=torch.int32, device=dev)
+        h_dr = np.zeros(R, np.int32)
+        for _ in range(3):
+            ssd.ssd_draft_head_run(head, R, d_h, d_tok, h_dr)  # host output: synchronizes
+        t0 = time.perf_counter()
+        for _ in range(calls - 1):
+            ssd.ssd_draft_head_run(head, R, d_h, d_tok, d_dr)
+        ssd.ssd_draft_head_run(head, R, d_h, d_tok, h_dr)  # the stream is in order: waits for all
+        dt = (time.perf_counter() - t0) / calls
+    finally:
+        ssd.ssd_free_draft_head(head)
+    # bf16 weights read once per call: W0, gain, W1, W3, W2, the final-norm gain and the
+    # output layer's image rows; plus the fp32 states in and the embedding rows
+    by = 2 * (2 * d * d + d + 3 * m * d + d + shape.v_img * d) + R * d * (4 + 2)
+    gbs = by / dt / 1e9
+    return {"rows": R, "m": m, "calls": calls, "ms_per_call": dt * 1e3, "bytes_per_call": by,
+            "achieved": gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": gbs / HBM_PEAK_GBS,
+            "timing": "host clock over back-to-back calls on the library's stream (launch gaps included)"}
+
+
 def cpu_baseline(wl, w, prefix, drafts):
     """The oracle (numpy float64) on the host cores, on prefix + the first two rows."""
     from oracle import decode as Dc
@@ -151,6 +184,7 @@ def main():
     ap.add_argument("--forward", choices=("kernels", "persistent"), default="kernels",
                     help="forward pass: one launch per projection/attention, or one cooperative launch per pass "
                          "(blocks of up to 32 tokens)")
+    ap.add_argument("--no-draft-head", action="store_true", help="skip the draft-head timing")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="only run a plain device copy of this size (PMC byte-counter calibration) and exit")
     args = ap.parse_args()
@@ -267,7 +301,7 @@ def main():
         "config": {"workload": wl.name, "batch": B, "prefix": P, "grid": f"{H}x{W}", "rule": wl.rule,
                    "rounds": wl.rounds, "k_h": 5, "k_v": 1, "top_k": wl.top_k, "planted_keep_p": p_keep,
                    "passes_per_image": stats.passes, "forward": args.forward, "parallelism": "single GPU"},
-        "roofline": {"bound": "hbm", "kernel": "gemm_bf16_kernel (QKV/O/gate-up/down/LM-head weight streaming)",
+        "roofline": {"bound": "hbm", "kernel": "gemm_bf16_kernel + gemm_wide_kernel (QKV/O/gate-up/down/LM-head weight streaming)",
                      "achieved": g_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": g_gbs / HBM_PEAK_GBS if g_gbs else None,
                      "traffic": measured_traffic(wl.name), "launches": g_n, "ms_per_launch": g_ms / max(g_n, 1),
@@ -287,6 +321,9 @@ def main():
         "ar_tokens_per_s_same_kernels": ar_rate,
         "speedup_vs_ar_same_kernels": (value / ar_rate) if ar_rate else None,
     }
+    if not args.no_draft_head and shape.dtype == "bf16":
+        log("[bench] draft head: one grid row per call")
+        result["draft_head"] = draft_head_cost(ssd, model, shape, target[0, 0] + shape.img_lo)
     if f_n > 0:
         # the single-launch pass carries the weight stream: it is the kernel the roofline is about
         result["roofline"] = dict(result["forward_launch"], traffic=None,
