@@ -19,7 +19,9 @@ timing leaves gaps between kernels, so it stays out of the timed steps).
 Extra keys: `roofline` (the weight-streaming GEMM kernel, from those events;
 with --forward persistent the single-launch forward kernel),
 `attention` (the same for the attention kernel), `draft_head` (the spatial
-draft head drafting one grid row per call, timed apart from the steps), `cpu_baseline` (the oracle
+draft head drafting one grid row per call, timed apart from the steps),
+`verify_pass_positions` (one drafted row verified at rows 1, H/4, H/2, H-1, 50 reps
+each, beside a one-token pass at the same place), `cpu_baseline` (the oracle
 on the host cores on a bounded sample), AR tokens/s on the same kernels.
 """
 import argparse
@@ -73,6 +75,50 @@ def gpu_greedy_ar(ssd, model, shape, prefix, n):
     dt = time.perf_counter() - t0
     ssd.ssd_free_session(sess)
     return out, dt
+
+
+def position_timing(ssd, model, shape, prefix, H, W, drafts, reps=50):
+    """Verify-pass time at four positions of the image (rows 1, H/4, H/2, H-1):
+    `reps` verify rounds of one drafted row (K = W, no commit, so the frontier and
+    the pass stay the same), each synchronized and timed by the host clock; the
+    same for a one-token pass (an AR step on the same kernels).  Median, p10, p90."""
+    B, P = prefix.shape
+    rows = sorted({1, H // 4, H // 2, H - 1})
+    sess = ssd.ssd_prefill(model, B, P, prefix, P + H * W, W)
+    prm = ssd.ssd_verify_params()
+    prm.rule, prm.temperature = ssd.SSD_GREEDY, 1.0
+    fr = np.zeros(B, np.int32)
+    out = {"rows": rows, "K": W, "reps": reps, "ms_median": [], "ms_p10": [], "ms_p90": [],
+           "ar_step_ms_median": [], "pass_over_ar_step": []}
+    try:
+        y = 0
+        for row in rows:
+            prm.commit, prm.round = 1, 0
+            while y < row:  # commit rows up to this one (frontier P + row*W)
+                tok = np.ascontiguousarray((drafts[:, y, :] + shape.img_lo).astype(np.int32))
+                ssd.ssd_verify_step(sess, W, tok, prm, frontier=fr)
+                y += 1
+            prm.commit = 0
+            for K, key in ((W, "pass"), (1, "ar")):
+                ts = []
+                for j in range(reps + 3):
+                    prm.round = j
+                    tok = np.ascontiguousarray((drafts[:, row, :K] + shape.img_lo).astype(np.int32))
+                    t0 = time.perf_counter()
+                    ssd.ssd_verify_step(sess, K, tok, prm, frontier=fr)  # host outputs: synchronizes
+                    ts.append(time.perf_counter() - t0)
+                ts = np.array(ts[3:]) * 1e3
+                if key == "pass":
+                    out["ms_median"].append(float(np.median(ts)))
+                    out["ms_p10"].append(float(np.percentile(ts, 10)))
+                    out["ms_p90"].append(float(np.percentile(ts, 90)))
+                else:
+                    out["ar_step_ms_median"].append(float(np.median(ts)))
+            out["pass_over_ar_step"].append(out["ms_median"][-1] / out["ar_step_ms_median"][-1])
+    finally:
+        ssd.ssd_free_session(sess)
+    out["timing"] = "host clock around each synchronizing ssd_verify_step call (host token buffers)"
+    return out
 
 
 def gemm_source_hash():
@@ -185,6 +231,7 @@ def main():
                     help="forward pass: one launch per projection/attention, or one cooperative launch per pass "
                          "(blocks of up to 32 tokens)")
     ap.add_argument("--no-draft-head", action="store_true", help="skip the draft-head timing")
+    ap.add_argument("--no-positions", action="store_true", help="skip the per-position verify-pass timing")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="only run a plain device copy of this size (PMC byte-counter calibration) and exit")
     args = ap.parse_args()
@@ -321,6 +368,9 @@ def main():
         "ar_tokens_per_s_same_kernels": ar_rate,
         "speedup_vs_ar_same_kernels": (value / ar_rate) if ar_rate else None,
     }
+    if not args.no_positions:
+        log("[bench] verify pass at four positions of the image")
+        result["verify_pass_positions"] = position_timing(ssd, model, shape, prefix, H, W, drafts)
     if not args.no_draft_head and shape.dtype == "bf16":
         log("[bench] draft head: one grid row per call")
         result["draft_head"] = draft_head_cost(ssd, model, shape, target[0, 0] + shape.img_lo)
