@@ -17,10 +17,21 @@ position 0 is scored by the carry -- the last logits of the previous commit
 (or of the prefill).  A block may start with one fixed position (n_fixed = 1):
 a token already chosen but not yet in the cache, which is not verified.
 
+Classifier-free guidance (the paper's backbones decode with it, Table
+"app_config": weights 5.0, 4.0, 3.0; the mix is Ho & Salimans' for logits): a
+guided session pairs B = 2*Bi sequences -- image b's conditional stream is
+sequence b, its unconditional stream sequence Bi + b (a null prompt of the
+same length).  Both streams get the image's block, and every decision scores
+with the guided logits l_u + w (l_c - l_u), the carry included.
+
 Pins: tests/test_oracle_decode.py -- truncation decoding and Jacobi-style
 greedy rounds (r >= K) both reproduce greedy AR decoding (Eq. 1 with argmax)
 token for token; the verify pass leaves the frontier unchanged and the commit
 pass advances it by K; the pass count of a decoded image equals the plan's.
+tests/test_oracle_cfg.py -- guidance against unguided sessions of the same
+streams (w = 1 and w = 0 give the conditional and unconditional decodes, equal
+prompts make w irrelevant, the guided logits are affine in w with the two
+streams' own logits, images pair with their own twins).
 """
 
 import numpy as np
@@ -39,11 +50,46 @@ class Session:
         self.f = np.zeros(B, dtype=np.int64)
         self.carry = None  # (B, V_img) float64
         self.passes = 0
+        self.guide = None  # CFG weight w, or None (unguided)
+        self.n_img = B     # images decoded: B, or B / 2 under guidance
 
 
-def prefill(model, prefix, max_ctx):
+def mix(l_c, l_u, w):
+    """Guided logits of a conditional / unconditional pair (CFG)."""
+    return l_u + w * (l_c - l_u)
+
+
+def set_guidance(sess, w):
+    """Pair the session's sequences for classifier-free guidance with weight w."""
+    assert sess.B % 2 == 0
+    sess.guide = float(w)
+    sess.n_img = sess.B // 2
+
+
+def carry_of(sess, b):
+    """Logits that score image b's position f (guided under CFG)."""
+    if sess.guide is None:
+        return sess.carry[b]
+    return mix(sess.carry[b], sess.carry[b + sess.n_img], sess.guide)
+
+
+def guided(sess, logits):
+    """Per-image logits (n_img, K, V_img) of a pass over every stream."""
+    if sess.guide is None:
+        return logits
+    return mix(logits[:sess.n_img], logits[sess.n_img:], sess.guide)
+
+
+def streams(sess, block):
+    """Block tokens of every sequence: under guidance both streams of an image get its block."""
+    return block if sess.guide is None else np.concatenate([block, block], axis=0)
+
+
+def prefill(model, prefix, max_ctx, guide=None):
     """Forward the text prefix (B, P) from position 0; the carry is the last
-    position's logits (they score the first image token)."""
+    position's logits (they score the first image token).  With a guidance
+    weight, prefix stacks the Bi conditional prompts over their Bi
+    unconditional twins."""
     prefix = np.asarray(prefix)
     B, P = prefix.shape
     s = Session(model, B, P, max_ctx)
@@ -51,26 +97,36 @@ def prefill(model, prefix, max_ctx):
     s.f[:] = P
     s.carry = logits[:, P - 1, :].copy()
     s.passes = 1
+    if guide is not None:
+        set_guidance(s, guide)
     return s
 
 
 def scoring_logits(sess, logits, b, k):
-    return sess.carry[b] if k == 0 else logits[b, k - 1]
+    """Logits that score block position k of image b (logits: the pass's, every stream)."""
+    if k == 0:
+        return carry_of(sess, b)
+    if sess.guide is None:
+        return logits[b, k - 1]
+    return mix(logits[b, k - 1], logits[b + sess.n_img, k - 1], sess.guide)
 
 
 def verify_round(sess, block, n_fixed, rule, rnd, seed=0, temperature=1.0, top_k=0, ref=None):
     """One verify-and-correct round.
 
-    block -- (B, K) image-code indices (0-based within the image range)
+    block -- (B, K) image-code indices (0-based within the image range), one
+             row per image (B = n_img)
     ref   -- list over b of lists over k of reference logits (None = point mass);
              updated in place for rule (C) rejections
-    Returns (new_block, accept (B,K) bool, count (B,), logits (B,K,V_img)).
+    Returns (new_block, accept (B,K) bool, count (B,), logits (B,K,V_img)),
+    the logits guided under CFG.
     The frontier does not move; the block's KV slots are overwritten.
     """
     cfg = sess.cfg
     block = np.asarray(block, dtype=np.int64)
     B, K = block.shape
-    logits, _ = M.forward(sess.model, sess.cache, block + cfg.img_lo, sess.f)
+    assert B == sess.n_img
+    logits, _ = M.forward(sess.model, sess.cache, streams(sess, block) + cfg.img_lo, sess.f)
     sess.passes += 1
     new = block.copy()
     acc = np.zeros((B, K), dtype=bool)
@@ -86,20 +142,22 @@ def verify_round(sess, block, n_fixed, rule, rnd, seed=0, temperature=1.0, top_k
             acc[b, k] = a
             if replaced and ref is not None:
                 ref[b][k] = np.array(L, dtype=np.float64)
-    return new, acc, acc[:, n_fixed:].sum(axis=1), logits
+    return new, acc, acc[:, n_fixed:].sum(axis=1), guided(sess, logits)
 
 
 def commit(sess, block):
     """Commit pass: forward the final block, keep its KV, advance the frontier
-    by K and take the last position's logits as the new carry."""
+    by K and take the last position's logits as the new carry (per stream).
+    Returns the per-image (guided) logits and the conditional stream's h_pre."""
     cfg = sess.cfg
     block = np.asarray(block, dtype=np.int64)
     K = block.shape[1]
-    logits, h_pre = M.forward(sess.model, sess.cache, block + cfg.img_lo, sess.f)
+    assert block.shape[0] == sess.n_img
+    logits, h_pre = M.forward(sess.model, sess.cache, streams(sess, block) + cfg.img_lo, sess.f)
     sess.passes += 1
     sess.f += K
     sess.carry = logits[:, K - 1, :].copy()
-    return logits, h_pre
+    return guided(sess, logits), h_pre[:sess.n_img]
 
 
 def truncate_step(sess, block, n_fixed):
@@ -109,6 +167,7 @@ def truncate_step(sess, block, n_fixed):
     Returns (n_accepted (B,), pending (B,)).  The frontier advances by
     n_fixed + n_accepted; the KV of those positions is already final."""
     cfg = sess.cfg
+    assert sess.guide is None, "strict truncation is not defined here for guided sessions"
     block = np.asarray(block, dtype=np.int64)
     B, K = block.shape
     logits, _ = M.forward(sess.model, sess.cache, block + cfg.img_lo, sess.f)
@@ -178,9 +237,11 @@ def decode_truncate(model, prefix, drafts, K):
 
 
 def decode_image(model, prefix, H, W, drafts, rule=R.RULE_GREEDY, seed=0, temperature=1.0, top_k=0,
-                 k_h=5, h_rounds=1, k_v=1, b=2, i=0, q_table=None, trace=None):
+                 k_h=5, h_rounds=1, k_v=1, b=2, i=0, q_table=None, trace=None, guide=None):
     """Decode one image per sequence under the SSD schedule with planted drafts.
 
+    prefix  -- (B, P) prompts; with a guidance weight `guide`, (2B, P): the B
+               conditional prompts over their unconditional twins
     drafts  -- (B, H, W) image-code indices used as the draft of every position
     q_table -- optional (B, H, W, V_img) draft logits (rule C reference for the
                first round of each position); None = point masses at the drafts
@@ -190,6 +251,8 @@ def decode_image(model, prefix, H, W, drafts, rule=R.RULE_GREEDY, seed=0, temper
     cfg = model.cfg
     prefix = np.asarray(prefix)
     B, P = prefix.shape
+    if guide is not None:
+        B //= 2
     N = H * W
     drafts = np.asarray(drafts, dtype=np.int64).reshape(B, N)
     ops = S.plan(H, W, k_h=k_h, h_rounds=h_rounds, k_v=k_v, b=b, i=i)
@@ -199,11 +262,11 @@ def decode_image(model, prefix, H, W, drafts, rule=R.RULE_GREEDY, seed=0, temper
     stats = {"accepted": 0, "proposed": 0, "verify_rounds": 0}
     for op in ops:
         if op[0] == "prefill":
-            sess = prefill(model, prefix, P + N)
+            sess = prefill(model, prefix, P + N, guide)
         elif op[0] == "first":
             for bb in range(B):
                 u1 = R.uniform(seed, bb, P, 0, 2)
-                work[bb, 0] = R.sample_first(rule, sess.carry[bb], u1, temperature, top_k)
+                work[bb, 0] = R.sample_first(rule, carry_of(sess, bb), u1, temperature, top_k)
         elif op[0] == "verify":
             _, start, K, nf, rnd = op
             assert int(sess.f[0]) == P + start
