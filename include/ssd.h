@@ -166,8 +166,29 @@ ssd_status ssd_verify_step(ssd_session* sess, int32_t K, int32_t* tokens, const 
                            const ssd_verify_params* params, uint8_t* accept_mask, int32_t* accept_count,
                            int32_t* frontier, float* logits_out, float* h_pre_out);
 
-/* Copy the current carry logits [B][V_img] (scores of position f). */
+/* Copy the current carry logits [B][V_img] (scores of position f; guided
+ * sessions: the guided carry of each of the B / 2 images). */
 ssd_status ssd_get_carry(ssd_session* sess, float* carry_out);
+
+/*
+ * Classifier-free guidance (the paper's backbones decode with it: Table
+ * "app_config" lists CFG weights 5.0, 4.0 and 3.0; the mix is that of Ho and
+ * Salimans, 2022, applied to logits).  Pairs the session's B sequences
+ * (B even): sequence b < B/2 is image b's conditional stream (its prompt),
+ * sequence B/2 + b the image's unconditional stream (a null prompt of the same
+ * length, prefilled with the session).  From this call on the session
+ * decodes B/2 images: ssd_verify_step feeds each image's block to both of its
+ * streams and scores every position with the guided logits
+ *     l = l_u + weight * (l_c - l_u)
+ * (carry included); its tokens, ref_logits, accept_mask, accept_count,
+ * frontier and logits_out (guided) arrays have B/2 rows, h_pre_out holds the
+ * conditional streams' states, and ssd_get_carry returns the guided carry.
+ * Uniforms are keyed by the image index.  A later call changes the weight.
+ * Truncate mode is refused on a guided session (SSD_E_INVAL).
+ * Errors: SSD_E_INVAL for a NULL session, odd B or a non-finite weight;
+ * SSD_E_OOM if the guided-logit buffers cannot be allocated.
+ */
+ssd_status ssd_session_set_cfg(ssd_session* sess, float weight);
 
 /*
  * SSD image schedule (Sec. 3.3; Sec. 4 "SSD Configuration"; Appendix
@@ -181,6 +202,9 @@ ssd_status ssd_get_carry(ssd_session* sess, float* carry_out);
  * followed by that row's commit.  The verify-round index grows over the whole
  * image.  Passes = 1 + 2*ceil((W-1)/k_h) + sum over groups of m rows of
  * (b + i*(m-1) + m) for h_rounds = 1.
+ * cfg = 1 decodes every image with classifier-free guidance of weight
+ * cfg_weight (see ssd_session_set_cfg): the prefix then holds 2B prompts, the
+ * B conditional ones followed by their B unconditional twins.
  */
 typedef struct {
   int32_t grid_h, grid_w;
@@ -188,6 +212,8 @@ typedef struct {
   int32_t rule, top_k;
   double temperature;
   uint64_t seed;
+  int32_t cfg;       /* 0: no guidance; 1: classifier-free guidance */
+  float cfg_weight;  /* guidance weight w (cfg = 1) */
 } ssd_schedule;
 
 typedef struct {
@@ -198,7 +224,7 @@ typedef struct {
 } ssd_stats;
 
 /*
- * Decode B images: prefix [B][P]; drafts [B][H][W] image-code ids used as
+ * Decode B images: prefix [B][P] ([2B][P] with cfg = 1); drafts [B][H][W] image-code ids used as
  * the draft of every position (planted drafts); draft_logits
  * [B][H][W][V_img] or NULL (rule C reference for a position's first round,
  * NULL = point masses); out_tokens [B][H][W].  stats may be NULL.

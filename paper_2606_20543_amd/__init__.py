@@ -19,7 +19,7 @@ SSD_GREEDY, SSD_SAMPLE, SSD_ACCEPT_REJECT = 0, 1, 2
 
 EXPORTED = [
     "ssd_init_model", "ssd_weights_numel", "ssd_free_model", "ssd_prefill", "ssd_free_session",
-    "ssd_verify_step", "ssd_get_carry", "ssd_decode_image", "ssd_profile", "ssd_profile_read", "ssd_last_error",
+    "ssd_verify_step", "ssd_get_carry", "ssd_session_set_cfg", "ssd_decode_image", "ssd_profile", "ssd_profile_read", "ssd_last_error",
     "ssd_draft_head_numel", "ssd_draft_head_init", "ssd_draft_head_run", "ssd_free_draft_head",
 ]
 
@@ -47,7 +47,8 @@ class ssd_schedule(ctypes.Structure):
     _fields_ = [("grid_h", ctypes.c_int32), ("grid_w", ctypes.c_int32), ("k_h", ctypes.c_int32),
                 ("h_rounds", ctypes.c_int32), ("k_v", ctypes.c_int32), ("b_rounds", ctypes.c_int32),
                 ("i_rounds", ctypes.c_int32), ("rule", ctypes.c_int32), ("top_k", ctypes.c_int32),
-                ("temperature", ctypes.c_double), ("seed", ctypes.c_uint64)]
+                ("temperature", ctypes.c_double), ("seed", ctypes.c_uint64), ("cfg", ctypes.c_int32),
+                ("cfg_weight", ctypes.c_float)]
 
 
 class ssd_stats(ctypes.Structure):
@@ -76,6 +77,7 @@ def lib():
         L.ssd_free_session.restype = None
         L.ssd_verify_step.argtypes = [vp, i32, vp, vp, ctypes.POINTER(ssd_verify_params), vp, vp, vp, vp, vp]
         L.ssd_get_carry.argtypes = [vp, vp]
+        L.ssd_session_set_cfg.argtypes = [vp, ctypes.c_float]
         L.ssd_decode_image.argtypes = [vp, ctypes.POINTER(ssd_schedule), i32, i32, vp, vp, vp, vp,
                                        ctypes.POINTER(ssd_stats), vp]
         L.ssd_profile.argtypes = [vp, i32]
@@ -88,8 +90,8 @@ def lib():
         L.ssd_free_draft_head.restype = None
         L.ssd_last_error.argtypes = []
         L.ssd_last_error.restype = ctypes.c_char_p
-        for name in ("ssd_init_model", "ssd_prefill", "ssd_verify_step", "ssd_get_carry", "ssd_decode_image",
-                     "ssd_profile", "ssd_profile_read", "ssd_draft_head_init", "ssd_draft_head_run"):
+        for name in ("ssd_init_model", "ssd_prefill", "ssd_verify_step", "ssd_get_carry", "ssd_session_set_cfg",
+                     "ssd_decode_image", "ssd_profile", "ssd_profile_read", "ssd_draft_head_init", "ssd_draft_head_run"):
             getattr(L, name).restype = i32
         _lib = L
     return _lib
@@ -153,6 +155,10 @@ def ssd_verify_step(sess, K, tokens, params, ref_logits=None, accept_mask=None, 
 
 def ssd_get_carry(sess, carry_out):
     _check(lib().ssd_get_carry(ctypes.c_void_p(sess), _ptr(carry_out)))
+
+
+def ssd_session_set_cfg(sess, weight):
+    _check(lib().ssd_session_set_cfg(ctypes.c_void_p(sess), float(weight)))
 
 
 def ssd_decode_image(model, sched, B, P, prefix, drafts, out_tokens, draft_logits=None, stream=None):

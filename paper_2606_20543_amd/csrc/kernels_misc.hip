@@ -534,6 +534,43 @@ void commit_update(int B, int K, int Vimg, const float* logits, float* carry, in
   hipLaunchKernelGGL(commit_kernel, dim3(B), dim3(256), 0, st, Vimg, logits, rps, last, carry, f, inc, ref_flag, ring);
 }
 
+// Classifier-free guidance: guided logits l_u + w (l_c - l_u) of each image b
+// (conditional stream b, unconditional stream Bi + b).  Workgroup (r, b): rows
+// r < K of the pass's logits [2*Bi*K][V] (row = stream * K + r), r = K the
+// carry [2*Bi][V].  K = 0 mixes the carry only.
+__global__ __launch_bounds__(256) void cfg_mix_kernel(int Bi, int K, int Vimg, float w, const float* logits,
+                                                      const float* carry, float* out_logits, float* out_carry) {
+  const int r = blockIdx.x, b = blockIdx.y;
+  const float *c, *u;
+  float* o;
+  if (r < K) {
+    c = logits + ((size_t)b * K + r) * Vimg;
+    u = logits + ((size_t)(Bi + b) * K + r) * Vimg;
+    o = out_logits + ((size_t)b * K + r) * Vimg;
+  } else {
+    c = carry + (size_t)b * Vimg;
+    u = carry + (size_t)(Bi + b) * Vimg;
+    o = out_carry + (size_t)b * Vimg;
+  }
+  if ((Vimg & 3) == 0) {
+    const float4* c4 = reinterpret_cast<const float4*>(c);
+    const float4* u4 = reinterpret_cast<const float4*>(u);
+    float4* o4 = reinterpret_cast<float4*>(o);
+    for (int v = threadIdx.x; v < Vimg / 4; v += 256) {
+      const float4 x = c4[v], y = u4[v];
+      o4[v] = make_float4(y.x + w * (x.x - y.x), y.y + w * (x.y - y.y), y.z + w * (x.z - y.z), y.w + w * (x.w - y.w));
+    }
+  } else {
+    for (int v = threadIdx.x; v < Vimg; v += 256) o[v] = u[v] + w * (c[v] - u[v]);
+  }
+}
+
+void cfg_mix(int Bi, int K, int Vimg, float w, const float* logits, const float* carry, float* out_logits,
+             float* out_carry, hipStream_t st) {
+  hipLaunchKernelGGL(cfg_mix_kernel, dim3(K + 1, Bi), dim3(256), 0, st, Bi, K, Vimg, w, logits, carry, out_logits,
+                     out_carry);
+}
+
 // Which XCD (accelerator complex die) each workgroup runs on: the XCC_ID
 // hardware register (bits [3:0]).  Used once at start-up to verify the
 // round-robin workgroup-to-XCD dispatch the split-K reductions rely on.

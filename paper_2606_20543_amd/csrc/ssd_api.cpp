@@ -253,6 +253,13 @@ struct ssd_session {
     unsigned abort_host = 0;    // copy of *abort_flag taken at the last synchronization
     std::map<std::pair<int, int>, std::pair<std::vector<FwdPhase>, FwdPhase*>> tables;  // (K, lm_mode)
   } fw;
+  // classifier-free guidance: sequences b and Bi + b are image b's conditional and
+  // unconditional streams; decisions use the guided logits
+  bool cfg = false;
+  float cfg_w = 0.f;
+  int Bi = 0;              // images (B, or B / 2 when guided)
+  float* mlog = nullptr;   // guided logits [Bi][Kmax][V_img]
+  float* mcarry = nullptr; // guided carry [Bi][V_img]
   // decode image buffers
   int* img = nullptr;    // [B][H*W] working grid (absolute ids)
   int img_cap = 0;
@@ -814,6 +821,7 @@ ssd_status create_session(ssd_model* m, int B, int P, int Lmax_req, int Kmax, ss
   s->dm = dm;
   s->stream = m->stream;
   s->B = B;
+  s->Bi = B;
   s->P = P;
   s->Lmax = ((Lmax_req + 63) / 64) * 64;
   s->Kmax = Kmax;
@@ -1405,11 +1413,39 @@ ssd_status ssd_profile_read(ssd_model* m, double* ms, int64_t* launches, double*
 ssd_status ssd_get_carry(ssd_session* s, float* carry_out) {
   if (!s || !carry_out) return fail(SSD_E_INVAL, "NULL argument");
   if (s->poisoned) return fail(SSD_E_STATE, "session is poisoned");
-  if (hipMemcpyAsync(carry_out, s->carry, (size_t)s->B * s->dm.Vimg * 4, hipMemcpyDefault, s->stream) != hipSuccess ||
+  const float* src = s->carry;
+  if (s->cfg) {
+    cfg_mix(s->Bi, 0, s->dm.Vimg, s->cfg_w, nullptr, s->carry, nullptr, s->mcarry, s->stream);
+    src = s->mcarry;
+  }
+  if (hipGetLastError() != hipSuccess ||
+      hipMemcpyAsync(carry_out, src, (size_t)s->Bi * s->dm.Vimg * 4, hipMemcpyDefault, s->stream) != hipSuccess ||
       hipStreamSynchronize(s->stream) != hipSuccess) {
     s->poisoned = true;
     return fail(SSD_E_DEVICE, "copy of the carry failed");
   }
+  return SSD_OK;
+}
+
+ssd_status ssd_session_set_cfg(ssd_session* s, float weight) {
+  g_err.clear();
+  if (!s) return fail(SSD_E_INVAL, "NULL session");
+  if (s->poisoned) return fail(SSD_E_STATE, "session is poisoned");
+  if (!std::isfinite(weight)) return fail(SSD_E_INVAL, "guidance weight must be finite");
+  if (!s->cfg) {
+    if (s->B % 2) return fail(SSD_E_INVAL, "guidance pairs sequences: B = %d is odd", s->B);
+    try {
+      if (!s->mlog) {
+        s->mlog = s->mem.get<float>((size_t)(s->B / 2) * s->Kmax * s->dm.Vimg);
+        s->mcarry = s->mem.get<float>((size_t)(s->B / 2) * s->dm.Vimg);
+      }
+    } catch (HipError& e) {
+      return fail(SSD_E_OOM, "%s: %s", e.what, hipGetErrorString(e.e));
+    }
+    s->cfg = true;
+    s->Bi = s->B / 2;
+  }
+  s->cfg_w = weight;
   return SSD_OK;
 }
 
@@ -1421,6 +1457,7 @@ ssd_status ssd_verify_step(ssd_session* s, int32_t K, int32_t* tokens, const flo
   if (s->poisoned) return fail(SSD_E_STATE, "session is poisoned by an earlier device error");
   const Dims& dm = s->dm;
   const int B = s->B;
+  const int nb = s->Bi;  // rows of every per-image argument (B, or B / 2 when guided)
   if (K < 1 || K > s->Kmax) return fail(SSD_E_INVAL, "K = %d outside [1, max_block = %d]", K, s->Kmax);
   if (prm->rule < SSD_GREEDY || prm->rule > SSD_ACCEPT_REJECT) return fail(SSD_E_INVAL, "unknown rule");
   if (!(prm->temperature > 0.0)) return fail(SSD_E_INVAL, "temperature must be > 0");
@@ -1428,13 +1465,14 @@ ssd_status ssd_verify_step(ssd_session* s, int32_t K, int32_t* tokens, const flo
   if (prm->round >= 65536u) return fail(SSD_E_INVAL, "round must be < 65536");
   if (prm->truncate && (prm->commit || prm->rule != SSD_GREEDY))
     return fail(SSD_E_INVAL, "truncate needs rule SSD_GREEDY and commit = 0");
+  if (prm->truncate && s->cfg) return fail(SSD_E_INVAL, "truncate is not available on a guided session");
   for (int b = 0; b < B; ++b)
     if (s->f[b] + K > s->Lmax || s->f[b] + K >= (1 << 24))
       return fail(SSD_E_CAPACITY, "block [%d, %d) of sequence %d exceeds max_ctx", s->f[b], s->f[b] + K, b);
   const bool tok_dev = is_device_ptr(tokens);
   std::vector<int32_t> htok;
   if (!tok_dev) {
-    ssd_status cs = check_tokens_host(tokens, (size_t)B * K, dm.img_lo, dm.img_hi, "tokens");
+    ssd_status cs = check_tokens_host(tokens, (size_t)nb * K, dm.img_lo, dm.img_hi, "tokens");
     if (cs != SSD_OK) return cs;
   }
   const bool host_out = (!tok_dev && !prm->commit) || (accept_mask && !is_device_ptr(accept_mask)) ||
@@ -1442,23 +1480,32 @@ ssd_status ssd_verify_step(ssd_session* s, int32_t K, int32_t* tokens, const flo
                         (logits_out && !is_device_ptr(logits_out)) || (h_pre_out && !is_device_ptr(h_pre_out));
   hipStream_t st = s->stream;
   try {
-    HIPCHK(hipMemcpyAsync(s->tok, tokens, (size_t)B * K * 4, hipMemcpyDefault, st));
+    HIPCHK(hipMemcpyAsync(s->tok, tokens, (size_t)nb * K * 4, hipMemcpyDefault, st));
+    // a guided image's block goes to both of its streams
+    if (s->cfg) HIPCHK(hipMemcpyAsync(s->tok + (size_t)nb * K, s->tok, (size_t)nb * K * 4, hipMemcpyDeviceToDevice, st));
     if (ref_logits && !prm->commit)
     {
       // the caller's array may be host memory: stage it on the device first
-      HIPCHK(hipMemcpyAsync(s->refstage, ref_logits, (size_t)B * K * dm.Vimg * 4, hipMemcpyDefault, st));
-      set_ref_rows(B, K, K, dm.Vimg, s->refstage, s->d_f, s->ref, s->ref_flag, s->ring, 0, st);
+      HIPCHK(hipMemcpyAsync(s->refstage, ref_logits, (size_t)nb * K * dm.Vimg * 4, hipMemcpyDefault, st));
+      set_ref_rows(nb, K, K, dm.Vimg, s->refstage, s->d_f, s->ref, s->ref_flag, s->ring, 0, st);
     }
     const bool all_rows = !prm->commit || logits_out;
     run_forward(s, K, all_rows ? 0 : 1);
-    if (logits_out)
-      HIPCHK(hipMemcpyAsync(logits_out, s->logits, (size_t)B * K * dm.Vimg * 4, hipMemcpyDefault, st));
-    if (h_pre_out) HIPCHK(hipMemcpyAsync(h_pre_out, s->x, (size_t)B * K * dm.d * 4, hipMemcpyDefault, st));
+    // per-image scores: the pass's own logits, or the guided mix of the two streams
+    const float* lg = s->logits;
+    const float* cy = s->carry;
+    if (s->cfg && all_rows) {
+      cfg_mix(nb, K, dm.Vimg, s->cfg_w, s->logits, s->carry, s->mlog, s->mcarry, st);
+      lg = s->mlog;
+      cy = s->mcarry;
+    }
+    if (logits_out) HIPCHK(hipMemcpyAsync(logits_out, lg, (size_t)nb * K * dm.Vimg * 4, hipMemcpyDefault, st));
+    if (h_pre_out) HIPCHK(hipMemcpyAsync(h_pre_out, s->x, (size_t)nb * K * dm.d * 4, hipMemcpyDefault, st));
     if (prm->commit) {
       commit_update(B, all_rows ? K : -K, dm.Vimg, s->logits, s->carry, s->d_f, s->ref_flag, s->ring, st);
       for (int b = 0; b < B; ++b) s->f[b] += K;
     } else {
-      fill_u32((unsigned*)s->cnt, B, 0u, st);
+      fill_u32((unsigned*)s->cnt, nb, 0u, st);
       SelectArgs a{};
       a.rule = prm->rule;
       a.top_k = prm->top_k;
@@ -1467,14 +1514,14 @@ ssd_status ssd_verify_step(ssd_session* s, int32_t K, int32_t* tokens, const flo
       a.round = prm->round;
       a.n_fixed = prm->n_fixed;
       a.K = K;
-      a.B = B;
+      a.B = nb;
       a.Vimg = dm.Vimg;
       a.img_lo = dm.img_lo;
       a.truncate = prm->truncate;
       a.f = s->d_f;
       a.tokens = s->tok;
-      a.logits = s->logits;
-      a.carry = s->carry;
+      a.logits = lg;
+      a.carry = cy;
       a.ref = s->ref;
       a.ref_flag = s->ref_flag;
       a.ring = s->ring;
@@ -1484,9 +1531,9 @@ ssd_status ssd_verify_step(ssd_session* s, int32_t K, int32_t* tokens, const flo
       select_tokens(a, st);
       if (prm->truncate) truncate_finalize(a, s->d_f, st);
       HIPCHK(hipGetLastError());
-      HIPCHK(hipMemcpyAsync(tokens, s->tok, (size_t)B * K * 4, hipMemcpyDefault, st));
-      if (accept_mask) HIPCHK(hipMemcpyAsync(accept_mask, s->acc, (size_t)B * K, hipMemcpyDefault, st));
-      if (accept_count) HIPCHK(hipMemcpyAsync(accept_count, s->cnt, (size_t)B * 4, hipMemcpyDefault, st));
+      HIPCHK(hipMemcpyAsync(tokens, s->tok, (size_t)nb * K * 4, hipMemcpyDefault, st));
+      if (accept_mask) HIPCHK(hipMemcpyAsync(accept_mask, s->acc, (size_t)nb * K, hipMemcpyDefault, st));
+      if (accept_count) HIPCHK(hipMemcpyAsync(accept_count, s->cnt, (size_t)nb * 4, hipMemcpyDefault, st));
       if (prm->truncate) {
         HIPCHK(hipMemcpyAsync(s->f.data(), s->d_f, (size_t)B * 4, hipMemcpyDeviceToHost, st));
         fwd_abort_fetch(s);
@@ -1494,7 +1541,7 @@ ssd_status ssd_verify_step(ssd_session* s, int32_t K, int32_t* tokens, const flo
         fwd_abort_check(s);
       }
     }
-    if (frontier) HIPCHK(hipMemcpyAsync(frontier, s->d_f, (size_t)B * 4, hipMemcpyDefault, st));
+    if (frontier) HIPCHK(hipMemcpyAsync(frontier, s->d_f, (size_t)nb * 4, hipMemcpyDefault, st));
     if (host_out) {
       fwd_abort_fetch(s);
       HIPCHK(hipStreamSynchronize(st));
@@ -1565,6 +1612,10 @@ ssd_status ssd_decode_image(ssd_model* m, const ssd_schedule* sc, int32_t B, int
     return fail(SSD_E_INVAL, "bad schedule");
   if (sc->rule < SSD_GREEDY || sc->rule > SSD_ACCEPT_REJECT || !(sc->temperature > 0.0))
     return fail(SSD_E_INVAL, "bad rule or temperature");
+  if ((sc->cfg != 0 && sc->cfg != 1) || (sc->cfg && !std::isfinite(sc->cfg_weight)))
+    return fail(SSD_E_INVAL, "cfg must be 0 or 1 with a finite weight");
+  if (sc->cfg && B >= (1 << 19)) return fail(SSD_E_INVAL, "bad batch size");
+  const int Bs = sc->cfg ? 2 * B : B;  // sequences: a guided image has two streams
   const int N = H * W;
   const int Lmax = P + N;
   if (Lmax >= (1 << 24)) return fail(SSD_E_INVAL, "image too large");
@@ -1577,7 +1628,7 @@ ssd_status ssd_decode_image(ssd_model* m, const ssd_schedule* sc, int32_t B, int
     nverify += o.kind == 0;
   }
   if (nverify >= 65536) return fail(SSD_E_INVAL, "more than 65535 verify rounds");
-  std::vector<int32_t> hpre((size_t)B * P), hdr((size_t)B * N);
+  std::vector<int32_t> hpre((size_t)Bs * P), hdr((size_t)B * N);
   if (hipMemcpy(hpre.data(), prefix, hpre.size() * 4, hipMemcpyDefault) != hipSuccess ||
       hipMemcpy(hdr.data(), drafts, hdr.size() * 4, hipMemcpyDefault) != hipSuccess) {
     (void)hipGetLastError();
@@ -1589,23 +1640,30 @@ ssd_status ssd_decode_image(ssd_model* m, const ssd_schedule* sc, int32_t B, int
   if (cs != SSD_OK) return cs;
   if (stream) m->stream = (hipStream_t)stream;
   // decode workspace, reused across calls of the same shape
-  if (!m->dec || m->dec_B != B || m->dec_P != P || m->dec_L != Lmax || m->dec_K != Kmax) {
+  if (!m->dec || m->dec_B != Bs || m->dec_P != P || m->dec_L != Lmax || m->dec_K != Kmax) {
     if (m->dec) {
       ssd_session* old = m->dec;
       m->dec = nullptr;
       delete old;
     }
     ssd_session* s = nullptr;
-    ssd_status st = create_session(m, B, P, Lmax, Kmax, &s);
+    ssd_status st = create_session(m, Bs, P, Lmax, Kmax, &s);
     if (st != SSD_OK) return st;
     m->dec = s;
-    m->dec_B = B;
+    m->dec_B = Bs;
     m->dec_P = P;
     m->dec_L = Lmax;
     m->dec_K = Kmax;
   }
   ssd_session* s = m->dec;
   s->stream = m->stream;
+  if (sc->cfg) {
+    ssd_status gs = ssd_session_set_cfg(s, (float)sc->cfg_weight);
+    if (gs != SSD_OK) return gs;
+  } else {
+    s->cfg = false;
+    s->Bi = s->B;
+  }
   hipStream_t st = s->stream;
   int64_t passes = 0, nv = 0, proposed = 0;
   try {
@@ -1617,14 +1675,18 @@ ssd_status ssd_decode_image(ssd_model* m, const ssd_schedule* sc, int32_t B, int
     HIPCHK(hipMemcpyAsync(s->img, hdr.data(), hdr.size() * 4, hipMemcpyHostToDevice, st));
     if (draft_logits)
       HIPCHK(hipMemcpyAsync(s->qtab, draft_logits, (size_t)B * N * dm.Vimg * 4, hipMemcpyDefault, st));
-    fill_u32((unsigned*)s->d_f, B, 0u, st);
-    fill_u32((unsigned*)s->ref_flag, (size_t)B * s->ring, 0u, st);
-    fill_u32((unsigned*)s->cnt, B, 0u, st);
-    for (int b = 0; b < B; ++b) s->f[b] = 0;
+    fill_u32((unsigned*)s->d_f, Bs, 0u, st);
+    fill_u32((unsigned*)s->ref_flag, (size_t)Bs * s->ring, 0u, st);
+    fill_u32((unsigned*)s->cnt, Bs, 0u, st);
+    for (int b = 0; b < Bs; ++b) s->f[b] = 0;
     HIPCHK(hipMemcpyAsync(s->tok, hpre.data(), hpre.size() * 4, hipMemcpyHostToDevice, st));
     prefill_pass(s);
     ++passes;
-    first_token(B, dm.Vimg, dm.img_lo, s->carry, sc->rule, sc->top_k, sc->temperature, sc->seed, s->d_f, s->img, N, st);
+    // per-image scores: the streams' own logits, or their guided mix
+    const float* lg = s->cfg ? s->mlog : s->logits;
+    const float* cy = s->cfg ? s->mcarry : s->carry;
+    if (s->cfg) cfg_mix(B, 0, dm.Vimg, s->cfg_w, nullptr, s->carry, nullptr, s->mcarry, st);
+    first_token(B, dm.Vimg, dm.img_lo, cy, sc->rule, sc->top_k, sc->temperature, sc->seed, s->d_f, s->img, N, st);
     SelectArgs a{};
     a.rule = sc->rule;
     a.top_k = sc->top_k;
@@ -1635,8 +1697,8 @@ ssd_status ssd_decode_image(ssd_model* m, const ssd_schedule* sc, int32_t B, int
     a.img_lo = dm.img_lo;
     a.f = s->d_f;
     a.tokens = s->tok;
-    a.logits = s->logits;
-    a.carry = s->carry;
+    a.logits = lg;
+    a.carry = cy;
     a.ref = s->ref;
     a.ref_flag = s->ref_flag;
     a.ring = s->ring;
@@ -1646,6 +1708,8 @@ ssd_status ssd_decode_image(ssd_model* m, const ssd_schedule* sc, int32_t B, int
     for (const Op& o : ops) {
       HIPCHK(hipMemcpy2DAsync(s->tok, (size_t)o.K * 4, s->img + o.start, (size_t)N * 4, (size_t)o.K * 4, B,
                               hipMemcpyDeviceToDevice, st));
+      if (s->cfg)
+        HIPCHK(hipMemcpyAsync(s->tok + (size_t)B * o.K, s->tok, (size_t)B * o.K * 4, hipMemcpyDeviceToDevice, st));
       if (o.kind == 0) {
         if (sc->rule == SSD_ACCEPT_REJECT && draft_logits) {
           // first round of a position: its reference is its draft distribution
@@ -1654,6 +1718,7 @@ ssd_status ssd_decode_image(ssd_model* m, const ssd_schedule* sc, int32_t B, int
                        1, st);
         }
         run_forward(s, o.K, 0);
+        if (s->cfg) cfg_mix(B, o.K, dm.Vimg, s->cfg_w, s->logits, s->carry, s->mlog, s->mcarry, st);
         a.K = o.K;
         a.n_fixed = o.nf;
         a.round = (unsigned)o.rnd;
@@ -1664,8 +1729,8 @@ ssd_status ssd_decode_image(ssd_model* m, const ssd_schedule* sc, int32_t B, int
         proposed += (int64_t)B * (o.K - o.nf);
       } else {
         run_forward(s, o.K, 1);
-        commit_update(B, -o.K, dm.Vimg, s->logits, s->carry, s->d_f, s->ref_flag, s->ring, st);
-        for (int b = 0; b < B; ++b) s->f[b] += o.K;
+        commit_update(Bs, -o.K, dm.Vimg, s->logits, s->carry, s->d_f, s->ref_flag, s->ring, st);
+        for (int b = 0; b < Bs; ++b) s->f[b] += o.K;
       }
       ++passes;
     }

@@ -320,6 +320,10 @@ void set_ref_rows(int B, int K, int rows_per_b, int Vimg, const float* src, cons
 // z = [h; e] split planes [R][2d] (plane elements apart) for a draft head
 void draft_input(const float* h, const void* emb, const int* tok, int R, int d, void* z, size_t plane,
                  hipStream_t st);
+// guided logits l_u + w (l_c - l_u): rows [Bi][K] from the pass's [2*Bi][K] logits
+// (K may be 0) and the carry [Bi] from [2*Bi]
+void cfg_mix(int Bi, int K, int Vimg, float w, const float* logits, const float* carry, float* out_logits,
+             float* out_carry, hipStream_t st);
 void first_token(int B, int Vimg, int img_lo, const float* carry, int rule, int top_k, double temperature,
                  unsigned long long seed, const int* f, int* out_abs, int out_stride, hipStream_t st);
 

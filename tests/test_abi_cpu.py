@@ -47,7 +47,8 @@ int main(void) {{
   printf("%zu %zu %zu %zu\\n", sizeof(ssd_model_config), sizeof(ssd_verify_params), sizeof(ssd_schedule), sizeof(ssd_stats));
   printf("%zu %zu %zu %zu\\n", offsetof(ssd_verify_params, temperature), offsetof(ssd_verify_params, seed),
          offsetof(ssd_verify_params, round), offsetof(ssd_schedule, temperature));
-  printf("%zu %zu\\n", offsetof(ssd_schedule, seed), offsetof(ssd_model_config, rope_theta));
+  printf("%zu %zu %zu %zu\\n", offsetof(ssd_schedule, seed), offsetof(ssd_model_config, rope_theta),
+         offsetof(ssd_schedule, cfg), offsetof(ssd_schedule, cfg_weight));
   return 0;
 }}
 """)
@@ -59,7 +60,8 @@ int main(void) {{
             ctypes.sizeof(ssd.ssd_schedule), ctypes.sizeof(ssd.ssd_stats),
             ssd.ssd_verify_params.temperature.offset, ssd.ssd_verify_params.seed.offset,
             ssd.ssd_verify_params.round.offset, ssd.ssd_schedule.temperature.offset,
-            ssd.ssd_schedule.seed.offset, ssd.ssd_model_config.rope_theta.offset]
+            ssd.ssd_schedule.seed.offset, ssd.ssd_model_config.rope_theta.offset,
+            ssd.ssd_schedule.cfg.offset, ssd.ssd_schedule.cfg_weight.offset]
     assert got == want
 
 
@@ -103,6 +105,7 @@ def test_null_arguments_rejected_before_device_work(lib):
     sc = ssd.ssd_schedule()
     assert L.ssd_decode_image(None, ctypes.byref(sc), 1, 1, None, None, None, None, None, None) == ssd.SSD_E_INVAL
     assert L.ssd_get_carry(None, None) == ssd.SSD_E_INVAL
+    assert L.ssd_session_set_cfg(None, 5.0) == ssd.SSD_E_INVAL
     assert L.ssd_profile(None, 1) == ssd.SSD_E_INVAL
     assert L.ssd_draft_head_init(None, 256, None, 1, ctypes.byref(out)) == ssd.SSD_E_INVAL
     assert L.ssd_draft_head_run(None, 1, None, None, None, None) == ssd.SSD_E_INVAL
