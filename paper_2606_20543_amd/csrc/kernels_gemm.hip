@@ -388,14 +388,19 @@ __global__ __launch_bounds__(WV * 64) void gemm_wide_kernel(GemmKArgs a) {
 GemmPlan gemm_plan_bf16(int M, int N, int K, int xcd) {
   GemmPlan p;
   p.xcd = xcd;
-  int Mc = M < 128 ? M : 128;
+  // up to 128 tokens: one-burst launches over row tiles of at most 64
+  // (the weights are streamed once per tile); beyond: double-buffered chunks
+  // of 128-row tiles
+  int Mc = M <= 128 ? (M < 64 ? M : 64) : 128;
   p.MT = Mc <= 16 ? 1 : Mc <= 32 ? 2 : Mc <= 64 ? 4 : 8;
   const int kb = K / 32;
-  if (p.MT <= 2) {
+  if (p.MT <= 4) {
     // one burst per workgroup: the smallest split count whose K-slice (8 or 16
-    // k-blocks) fits registers and LDS, preferring >= 256 workgroups.  Two
-    // 16-feature tiles per wave (16-block slices only) when one tile per wave
-    // would need more workgroups than two per CU hold at once.
+    // k-blocks; 8 for 64-row tiles, whose 16-block token stage would not leave
+    // LDS for two workgroups per CU) fits registers and LDS, preferring >= 256
+    // workgroups.  Two 16-feature tiles per wave when one tile per wave would
+    // need more workgroups than two per CU hold at once (not for 64-row tiles:
+    // 340 registers per lane, one wave per SIMD).
     auto burst = [&](int nt, int& n_fb, int& S) {
       n_fb = (N + 64 * nt - 1) / (64 * nt);
       S = 0;
@@ -403,6 +408,7 @@ GemmPlan gemm_plan_bf16(int M, int N, int K, int xcd) {
         if (kb % s) continue;
         const int kcb = kb / s;
         if (kcb != 16 && kcb != 8) continue;
+        if (p.MT == 4 && kcb != 8) continue;
         if (S == 0) S = s;
         if (n_fb * s >= 256) {
           S = s;
@@ -413,7 +419,7 @@ GemmPlan gemm_plan_bf16(int M, int N, int K, int xcd) {
     int f1, s1, f2, s2;
     burst(1, f1, s1);
     burst(2, f2, s2);
-    const bool two = s2 && kb / s2 == 16 && (!s1 || f1 * s1 > 512);
+    const bool two = p.MT <= 2 && s2 && kb / s2 == 16 && (!s1 || f1 * s1 > 512);
     if (two || s1) {
       p.NT = two ? 2 : 1;
       p.WV = 4;
@@ -432,7 +438,28 @@ GemmPlan gemm_plan_bf16(int M, int N, int K, int xcd) {
         return (double)((grid + 255) / 256) * ((double)wv * nt * kcb * 1024 + (double)Mc * kcb * 32 * 4);
       };
       double best = cost(p.n_fb * p.S, 4, p.NT, p.KCB);
-      if (p.NT == 2 && (p.n_fb * p.S) % 256 != 0 && kb % 16 == 0 && N % 16 == 0) {
+      if (p.MT == 4 && kb % 16 == 0 && N % 16 == 0) {
+        // 64-row tiles: the 4-wave plan needs 8-block slices, twice the splits
+        // (partial sums ~ splits x N x 64 rows); wide workgroups take 16-block
+        // slices, one workgroup per CU, wherever the cost model favours them
+        // (on the 1B shapes: all projections except the O projection).  6 or 8
+        // waves: with 11 or 16 the 64-row token stage and weight burst spill.
+        for (int wv : {6, 8}) {
+          if ((N / 16) % wv) continue;
+          const int nfb = N / 16 / wv, S = kb / 16;
+          const double c = cost(nfb * S, wv, 1, 16);
+          if (c < 0.95 * best) {
+            best = c;
+            p.WV = wv;
+            p.NT = 1;
+            p.bn = 16 * wv;
+            p.n_fb = nfb;
+            p.S = S;
+            p.KCB = 16;
+          }
+        }
+      }
+      if (p.MT <= 2 && p.NT == 2 && (p.n_fb * p.S) % 256 != 0 && kb % 16 == 0 && N % 16 == 0) {
         for (int wv : {6, 8, 11, 16}) {
           if ((N / 16) % wv) continue;
           const int nfb = N / 16 / wv, S = kb / 16;
@@ -489,8 +516,8 @@ static void launch_wide_mt(int wv, const GemmKArgs& a, int n_fb, int S, hipStrea
   switch (wv) {
     case 6: launch_wide<MT, 6>(a, n_fb, S, st); break;
     case 8: launch_wide<MT, 8>(a, n_fb, S, st); break;
-    case 11: launch_wide<MT, 11>(a, n_fb, S, st); break;
-    default: launch_wide<MT, 16>(a, n_fb, S, st); break;
+    case 11: if constexpr (MT <= 2) launch_wide<MT, 11>(a, n_fb, S, st); break;
+    default: if constexpr (MT <= 2) launch_wide<MT, 16>(a, n_fb, S, st); break;
   }
 }
 
@@ -522,7 +549,8 @@ void gemm_bf16(const GemmPlan& p, const void* Wpacked, int N, int K, const void*
     a.epi = epi;
     if (p.WV != 4) {
       if (p.MT == 1) launch_wide_mt<1>(p.WV, a, p.n_fb, p.S, st);
-      else launch_wide_mt<2>(p.WV, a, p.n_fb, p.S, st);
+      else if (p.MT == 2) launch_wide_mt<2>(p.WV, a, p.n_fb, p.S, st);
+      else launch_wide_mt<4>(p.WV, a, p.n_fb, p.S, st);
       continue;
     }
     switch (p.MT) {
@@ -538,7 +566,10 @@ void gemm_bf16(const GemmPlan& p, const void* Wpacked, int N, int K, const void*
         else if (p.kchunks == 1 && p.KCB == 8) launch_gemm<2, 1, 8, 1>(a, p.n_fb, p.S, st);
         else launch_gemm<2, 1, 4, 2>(a, p.n_fb, p.S, st);
         break;
-      case 4: launch_gemm<4, 2, 2, 2>(a, p.n_fb, p.S, st); break;
+      case 4:
+        if (p.kchunks == 1 && p.KCB == 8 && p.NT == 1) launch_gemm<4, 1, 8, 1>(a, p.n_fb, p.S, st);
+        else launch_gemm<4, 2, 2, 2>(a, p.n_fb, p.S, st);
+        break;
       default: launch_gemm<8, 2, 1, 2>(a, p.n_fb, p.S, st); break;
     }
   }

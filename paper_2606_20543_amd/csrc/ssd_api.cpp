@@ -772,8 +772,9 @@ void size_workspaces(const Dims& dm, const ssd_model* m, int B, int P, int Kmax,
   ssq_parts_max = 1;
   if (!dm.bf16) return;
   const int Nqkv = (dm.Hq + 2 * dm.Hkv) * dm.D;
-  // every token-tile class a launch chunk can fall in (plans depend on min(M, 128) only)
-  for (int Mc : {1, 16, 17, 32, 33, 64, 65, 128}) {
+  // every token-tile class a plan can fall in: up to 16, 32 and 64 tokens,
+  // 65..128 (64-token tiles), beyond 128 (128-token tiles)
+  for (int Mc : {1, 16, 17, 32, 33, 64, 65, 128, 129, 256}) {
     for (auto nk : {std::make_pair(Nqkv, dm.d), std::make_pair(dm.d, dm.Hq * dm.D), std::make_pair(2 * dm.dff, dm.d),
                     std::make_pair(dm.d, dm.dff), std::make_pair(dm.Vimg, dm.d)}) {
       GemmPlan p = gemm_plan_bf16(Mc, nk.first, nk.second, 0);  // sizes do not depend on the XCD mapping
