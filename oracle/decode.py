@@ -36,6 +36,7 @@ streams' own logits, images pair with their own twins).
 
 import numpy as np
 
+from . import draft as Dr
 from . import model as M
 from . import schedule as S
 from . import select as R
@@ -49,6 +50,7 @@ class Session:
         self.cache = M.Cache(model.cfg, B, max_ctx)
         self.f = np.zeros(B, dtype=np.int64)
         self.carry = None  # (B, V_img) float64
+        self.h_carry = None  # (B, d) pre-norm state of the last cached position (it scored the carry)
         self.passes = 0
         self.guide = None  # CFG weight w, or None (unguided)
         self.n_img = B     # images decoded: B, or B / 2 under guidance
@@ -93,9 +95,10 @@ def prefill(model, prefix, max_ctx, guide=None):
     prefix = np.asarray(prefix)
     B, P = prefix.shape
     s = Session(model, B, P, max_ctx)
-    logits, _ = M.forward(model, s.cache, prefix, s.f)
+    logits, h_pre = M.forward(model, s.cache, prefix, s.f)
     s.f[:] = P
     s.carry = logits[:, P - 1, :].copy()
+    s.h_carry = h_pre[:, P - 1, :].copy()
     s.passes = 1
     if guide is not None:
         set_guidance(s, guide)
@@ -157,6 +160,7 @@ def commit(sess, block):
     sess.passes += 1
     sess.f += K
     sess.carry = logits[:, K - 1, :].copy()
+    sess.h_carry = h_pre[:, K - 1, :].copy()
     return guided(sess, logits), h_pre[:sess.n_img]
 
 
@@ -237,12 +241,22 @@ def decode_truncate(model, prefix, drafts, K):
 
 
 def decode_image(model, prefix, H, W, drafts, rule=R.RULE_GREEDY, seed=0, temperature=1.0, top_k=0,
-                 k_h=5, h_rounds=1, k_v=1, b=2, i=0, q_table=None, trace=None, guide=None):
-    """Decode one image per sequence under the SSD schedule with planted drafts.
+                 k_h=5, h_rounds=1, k_v=1, b=2, i=0, q_table=None, trace=None, guide=None, heads=None):
+    """Decode one image per sequence under the SSD schedule, with planted drafts
+    or drafted by spatial heads (Sec. 3.3).
 
     prefix  -- (B, P) prompts; with a guidance weight `guide`, (2B, P): the B
                conditional prompts over their unconditional twins
     drafts  -- (B, H, W) image-code indices used as the draft of every position
+               (ignored when heads are given)
+    heads   -- optional (horizontal, vertical): lists of oracle.draft.Head, the
+               horizontal head for offset +j at index j-1 (k_h of them) and the
+               vertical head for +j rows at index j-1 (k_v).  Head inputs are
+               [h; e] of a chosen token: h the pre-norm state that scored it (the
+               state of the raster position before it, conditional stream under
+               guidance), e its embedding; the drafts are the argmax of the
+               backbone's output layer on the predicted states, and under rule C
+               their softmax is the draft distribution q of the first round.
     q_table -- optional (B, H, W, V_img) draft logits (rule C reference for the
                first round of each position); None = point masses at the drafts
     trace   -- optional list collecting (op, accept, count, logits) per verify
@@ -254,15 +268,42 @@ def decode_image(model, prefix, H, W, drafts, rule=R.RULE_GREEDY, seed=0, temper
     if guide is not None:
         B //= 2
     N = H * W
-    drafts = np.asarray(drafts, dtype=np.int64).reshape(B, N)
     ops = S.plan(H, W, k_h=k_h, h_rounds=h_rounds, k_v=k_v, b=b, i=i)
     sess = None
-    work = drafts.copy()
+    if heads is None:
+        work = np.asarray(drafts, dtype=np.int64).reshape(B, N).copy()
+    else:
+        work = np.zeros((B, N), dtype=np.int64)
+        hs = np.zeros((B, N, cfg.d_model))  # hs[:, p]: the state that scored image token p
+        q_table = np.zeros((B, N, cfg.img_hi - cfg.img_lo)) if rule == R.RULE_ACCEPT_REJECT else None
     refs = [dict() for _ in range(B)]  # image index -> reference logits
     stats = {"accepted": 0, "proposed": 0, "verify_rounds": 0}
     for op in ops:
         if op[0] == "prefill":
             sess = prefill(model, prefix, P + N, guide)
+            if heads is not None:
+                hs[:, 0] = sess.h_carry[:B]
+        elif op[0] in ("draft_h", "draft_v"):
+            if heads is None:
+                continue
+            if op[0] == "draft_h":
+                _, src, n = op
+                srcs = np.array([src])
+                dst = [src + j for j in range(1, n + 1)]
+                lst = heads[0]
+            else:
+                _, y0, m = op
+                srcs = y0 * W + np.arange(W)
+                dst = [srcs + j * W for j in range(1, m + 1)]
+                lst = heads[1]
+            for j, d_idx in enumerate(dst):
+                idx, lg = Dr.draft(model, lst[j], hs[:, srcs].reshape(-1, cfg.d_model),
+                                   (work[:, srcs] + cfg.img_lo).reshape(-1))
+                work[:, d_idx] = idx.reshape(B, -1) if np.ndim(d_idx) else idx
+                if q_table is not None:
+                    q_table[:, d_idx] = lg.reshape(B, -1, lg.shape[-1]) if np.ndim(d_idx) else lg
+                if trace is not None:
+                    trace.append((op, j + 1, srcs.copy(), np.atleast_1d(d_idx).copy(), work[:, d_idx].copy()))
         elif op[0] == "first":
             for bb in range(B):
                 u1 = R.uniform(seed, bb, P, 0, 2)
@@ -297,7 +338,10 @@ def decode_image(model, prefix, H, W, drafts, rule=R.RULE_GREEDY, seed=0, temper
         elif op[0] == "commit":
             _, start, K = op
             assert int(sess.f[0]) == P + start
-            commit(sess, work[:, start:start + K])
+            _, hp = commit(sess, work[:, start:start + K])
+            if heads is not None:
+                n_in = min(K, N - start - 1)
+                hs[:, start + 1:start + 1 + n_in] = hp[:, :n_in]
             for bb in range(B):
                 for k in range(K):
                     refs[bb].pop(start + k, None)

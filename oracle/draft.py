@@ -39,14 +39,17 @@ def head_numel(d, m):
 
 
 class Head:
-    """A draft head's weights unpacked to float64 (bf16 bits in, like the backbone's)."""
+    """A draft head's weights unpacked to float64 (bf16 bits or float32 in, like the
+    backbone's)."""
 
     def __init__(self, d, m, packed):
-        assert packed.dtype == np.uint16 and packed.shape[0] == head_numel(d, m)
+        assert packed.dtype in (np.uint16, np.float32) and packed.shape[0] == head_numel(d, m)
         off = 0
         for name, shape in head_layout(d, m):
             n = int(np.prod(shape))
-            setattr(self, name, M.bf16_bits_to_f64(packed[off:off + n]).reshape(shape))
+            part = packed[off:off + n]
+            v = M.bf16_bits_to_f64(part) if packed.dtype == np.uint16 else part.astype(np.float64)
+            setattr(self, name, v.reshape(shape))
             off += n
         self.d, self.m = d, m
 

@@ -20,7 +20,12 @@ Readings:
   * joint verification (all rounds on the whole group) is the staged plan
     with i = 0: the group's rows are committed one after another;
   * the verify round index that feeds the random counter increases over the
-    whole image, so no (position, round) pair repeats.
+    whole image, so no (position, round) pair repeats;
+  * drafting happens where the paper puts it: before each horizontal run the
+    horizontal heads draft the run from the last token already chosen (after
+    the prefill: the first token), and at the start of each vertical group the
+    vertical heads draft the group's rows from the completed row above.
+    Drafting is not a backbone pass.
 
 Pin: tests/test_schedule.py -- the pass count equals all 31 step counts printed
 in the paper's tables (verification rounds, vertical lookahead, Pareto sweep,
@@ -35,6 +40,9 @@ def plan(H, W, k_h=5, h_rounds=1, k_v=1, b=2, i=0):
       ("first",)                                -- pick image token 0 from the carry
       ("verify", start, K, n_fixed, round)      -- one verify-and-correct round
       ("commit", start, K)                      -- commit pass over [start, start+K)
+      ("draft_h", src, n)                       -- horizontal heads 1..n draft src+1..src+n
+      ("draft_v", y0, m)                        -- vertical heads 1..m draft rows y0+1..y0+m
+                                                   from row y0
     """
     ops = [("prefill",), ("first",)]
     rnd = 0
@@ -51,10 +59,12 @@ def plan(H, W, k_h=5, h_rounds=1, k_v=1, b=2, i=0):
     while s < W:
         e = min(s + k_h, W)
         if first:
+            ops.append(("draft_h", 0, e - 1))
             verify(0, e, 1, h_rounds)
             ops.append(("commit", 0, e))
             first = False
         else:
+            ops.append(("draft_h", s - 1, e - s))
             verify(s, e - s, 0, h_rounds)
             ops.append(("commit", s, e - s))
         s = e
@@ -64,6 +74,7 @@ def plan(H, W, k_h=5, h_rounds=1, k_v=1, b=2, i=0):
     y = 1
     while y < H:
         m = min(k_v, H - y)
+        ops.append(("draft_v", y - 1, m))
         verify(y * W, m * W, 0, b)
         ops.append(("commit", y * W, W))
         for j in range(1, m):
