@@ -262,10 +262,10 @@ ssd_status ssd_profile_read(ssd_model* model, double* ms, int64_t* launches, dou
  *
  * ssd_draft_head_numel: element count of the packed head weights for the
  *   model's d_model and the head's inner size m (-1 if invalid).
- * ssd_draft_head_init: weights in the model's dtype (bf16 models only), host
- *   or device, packed W0 [d][2d] (columns: h then e), g [d], W1 [m][d],
- *   W3 [m][d], W2 [d][m]; m a positive multiple of 256; max_rows >= 1 bounds
- *   R of every run.  The head is tied to the model (free it first) and runs
+ * ssd_draft_head_init: weights in the model's dtype (bf16 bit patterns as
+ *   uint16, or float32), host or device, packed W0 [d][2d] (columns: h then
+ *   e), g [d], W1 [m][d], W3 [m][d], W2 [d][m]; m a positive multiple of 256;
+ *   max_rows >= 1 bounds R of every run.  The head is tied to the model (free it first) and runs
  *   on the model's stream.
  * ssd_draft_head_run: h [R][d] fp32 pre-norm states (e.g. the h_pre_out of a
  *   commit pass), tokens [R] vocabulary ids of the same positions; writes
@@ -282,6 +282,29 @@ ssd_status ssd_draft_head_init(ssd_model* model, int32_t m, const void* weights,
 ssd_status ssd_draft_head_run(ssd_draft_head* head, int32_t R, const float* h, const int32_t* tokens,
                               int32_t* drafts, float* logits_out);
 void ssd_free_draft_head(ssd_draft_head* head);
+
+/*
+ * Decode B images under the SSD schedule of ssd_decode_image with drafts from
+ * spatial heads instead of a planted table (Sec. 3.3: horizontal heads draft
+ * the rest of the current row, vertical heads whole rows below).  Before each
+ * horizontal run of n tokens after the last chosen token c, horizontal head j
+ * (h_heads[j-1], j = 1..n) drafts position c + j; at the start of each group of
+ * m rows below a completed row y, vertical head j (v_heads[j-1], j = 1..m)
+ * drafts row y + j, one call per head for all W columns of all images.  A
+ * head's input for source token t is [h; e(t)], h the pre-norm last-layer
+ * state that scored t (the state of the raster position before it: the
+ * prompt's last state for the first image token, else a state of the commit
+ * pass that cached t's predecessor; conditional streams under guidance).
+ * Under rule C the softmax of a position's draft logits is its reference q for
+ * its first verify round.  n_h must cover min(k_h, W-1) heads and n_v
+ * min(k_v, H-1); horizontal heads need max_rows >= B, vertical heads
+ * max_rows >= B*W.  Heads must belong to `model`.  Other arguments, the
+ * schedule and the errors are those of ssd_decode_image.
+ */
+ssd_status ssd_decode_image_heads(ssd_model* model, const ssd_schedule* sched, int32_t B, int32_t P,
+                                  const int32_t* prefix, ssd_draft_head* const* h_heads, int32_t n_h,
+                                  ssd_draft_head* const* v_heads, int32_t n_v, int32_t* out_tokens,
+                                  ssd_stats* stats, void* stream);
 
 /* Thread-local description of the last error (empty string if none). */
 const char* ssd_last_error(void);

@@ -21,6 +21,7 @@ EXPORTED = [
     "ssd_init_model", "ssd_weights_numel", "ssd_free_model", "ssd_prefill", "ssd_free_session",
     "ssd_verify_step", "ssd_get_carry", "ssd_session_set_cfg", "ssd_decode_image", "ssd_profile", "ssd_profile_read", "ssd_last_error",
     "ssd_draft_head_numel", "ssd_draft_head_init", "ssd_draft_head_run", "ssd_free_draft_head",
+    "ssd_decode_image_heads",
 ]
 
 
@@ -87,11 +88,14 @@ def lib():
         L.ssd_draft_head_init.argtypes = [vp, i32, vp, i32, ctypes.POINTER(vp)]
         L.ssd_draft_head_run.argtypes = [vp, i32, vp, vp, vp, vp]
         L.ssd_free_draft_head.argtypes = [vp]
+        L.ssd_decode_image_heads.argtypes = [vp, ctypes.POINTER(ssd_schedule), i32, i32, vp, ctypes.POINTER(vp), i32,
+                                             ctypes.POINTER(vp), i32, vp, ctypes.POINTER(ssd_stats), vp]
         L.ssd_free_draft_head.restype = None
         L.ssd_last_error.argtypes = []
         L.ssd_last_error.restype = ctypes.c_char_p
         for name in ("ssd_init_model", "ssd_prefill", "ssd_verify_step", "ssd_get_carry", "ssd_session_set_cfg",
-                     "ssd_decode_image", "ssd_profile", "ssd_profile_read", "ssd_draft_head_init", "ssd_draft_head_run"):
+                     "ssd_decode_image", "ssd_profile", "ssd_profile_read", "ssd_draft_head_init", "ssd_draft_head_run",
+                     "ssd_decode_image_heads"):
             getattr(L, name).restype = i32
         _lib = L
     return _lib
@@ -185,6 +189,17 @@ def ssd_draft_head_run(head, R, h, tokens, drafts, logits_out=None):
 
 def ssd_free_draft_head(head):
     lib().ssd_free_draft_head(ctypes.c_void_p(head))
+
+
+def ssd_decode_image_heads(model, sched, B, P, prefix, h_heads, v_heads, out_tokens, stream=None):
+    """h_heads / v_heads: sequences of head handles (horizontal offsets +1.., vertical rows +1..)."""
+    hh = (ctypes.c_void_p * max(len(h_heads), 1))(*h_heads)
+    vh = (ctypes.c_void_p * max(len(v_heads), 1))(*v_heads)
+    st = ssd_stats()
+    _check(lib().ssd_decode_image_heads(ctypes.c_void_p(model), ctypes.byref(sched), B, P, _ptr(prefix), hh,
+                                        len(h_heads), vh, len(v_heads), _ptr(out_tokens), ctypes.byref(st),
+                                        _ptr(stream)))
+    return st
 
 
 def ssd_profile(model, enable):

@@ -655,6 +655,23 @@ void draft_input(const float* h, const void* emb, const int* tok, int R, int d, 
                      plane);
 }
 
+// fp32 models: z = [h; e] as plain fp32 rows [R][2d]
+__global__ __launch_bounds__(256) void draft_input_f32_kernel(const float* h, const float* emb, const int* tok, int d,
+                                                              float* z) {
+  const int r = blockIdx.x;
+  const float* hr = h + (size_t)r * d;
+  const float* er = emb + (size_t)tok[r] * d;
+  float* zr = z + (size_t)r * 2 * d;
+  for (int i = threadIdx.x; i < d; i += blockDim.x) {
+    zr[i] = hr[i];
+    zr[d + i] = er[i];
+  }
+}
+
+void draft_input_f32(const float* h, const float* emb, const int* tok, int R, int d, float* z, hipStream_t st) {
+  hipLaunchKernelGGL(draft_input_f32_kernel, dim3(R), dim3(256), 0, st, h, emb, tok, d, z);
+}
+
 void first_token(int B, int Vimg, int img_lo, const float* carry, int rule, int top_k, double temperature,
                  unsigned long long seed, const int* f, int* out_abs, int out_stride, hipStream_t st) {
   hipLaunchKernelGGL(first_token_kernel, dim3(B), dim3(NT_SEL), 0, st, Vimg, img_lo, carry, rule, top_k, temperature,

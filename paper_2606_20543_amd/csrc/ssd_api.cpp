@@ -263,7 +263,12 @@ struct ssd_session {
   // decode image buffers
   int* img = nullptr;    // [B][H*W] working grid (absolute ids)
   int img_cap = 0;
-  float* qtab = nullptr; // draft logits table for rule C references
+  float* qtab = nullptr; // draft logits table for rule C references [B][H*W][V_img]
+  size_t qtab_cap = 0;
+  float* hs = nullptr;   // head drafting: the state that scored each image token [B][H*W][d]
+  size_t hs_cap = 0;
+  float* hsrc = nullptr; // head inputs of one draft step [B][W][d] and their tokens [B][W]
+  int* tsrc = nullptr;
 };
 
 namespace {
@@ -1176,6 +1181,108 @@ struct ssd_draft_head {
   size_t gcnt_cap;
 };
 
+namespace {
+
+// Enqueue one head on R rows: hin [R][d] fp32 pre-norm states and tok [R]
+// vocabulary ids (device).  Leaves the drafts (absolute image-code ids, lowest
+// id among equal maxima) in h->out and the draft logits in h->logits.
+void head_forward(ssd_draft_head* h, int R, const float* hin, const int* tok, hipStream_t st) {
+  ssd_model* m = h->m;
+  const Dims& dm = m->dm;
+  const int d = h->d, mi = h->mi;
+  fill_u32((unsigned*)h->x, (size_t)R * d, 0u, st);  // u accumulates onto zero
+  EpiArgs base{};
+  base.Kblk = h->Rmax;  // every row is block position t of "sequence" 0
+  base.f = h->f0;
+  base.ssq_ld = h->Rmax;
+  base.ssq_step = 1;
+  base.inv_d = 1.0f / (float)d;
+  base.eps = dm.eps;
+  base.Hq = dm.Hq;
+  base.Hkv = dm.Hkv;
+  base.D = dm.D;
+  base.x = h->x;
+  base.xn = h->xn;
+  base.xn_plane = h->xn_plane;
+  base.ssq_out = h->ssq;
+  base.ssq_out_ld = h->Rmax;
+  base.h = h->hb;
+  base.h_plane = h->hb_plane;
+  base.logits = h->logits;
+  if (!dm.bf16) {
+    // fp32 models: plain fp32 GEMMs, one row sum of squares per norm
+    draft_input_f32(hin, (const float*)m->emb, tok, R, d, (float*)h->z, st);
+    EpiArgs e = base;
+    e.kind = EPI_RESID;  // u = W0 [h; e]; n = g * u
+    e.gnext = h->g;
+    e.ld = d;
+    gemm_f32((const float*)h->w0, d, 2 * d, (const float*)h->z, 2 * d, R, e, st);
+    norm_rows_f32(h->x, R, d, nullptr, nullptr, h->ssq, st);
+    e = base;
+    e.kind = EPI_SWIGLU;  // SwiGLU(n / rms(u))
+    e.ssq = h->ssq;
+    e.ssq_parts = 1;
+    e.ld = mi;
+    gemm_f32((const float*)h->w13, 2 * mi, d, (const float*)h->xn, d, R, e, st);
+    e = base;
+    e.kind = EPI_RESID;  // h_hat = u + W2 (...); n = g_f * h_hat
+    e.gnext = m->gf;
+    e.ld = d;
+    gemm_f32((const float*)h->w2, d, mi, (const float*)h->hb, mi, R, e, st);
+    norm_rows_f32(h->x, R, d, nullptr, nullptr, h->ssq, st);
+    e = base;
+    e.kind = EPI_LOGITS;
+    e.ssq = h->ssq;
+    e.ssq_parts = 1;
+    e.ld = dm.Vimg;
+    gemm_f32((const float*)m->wlm, dm.Vimg, d, (const float*)h->xn, d, R, e, st);
+  } else {
+    draft_input(hin, m->emb, tok, R, d, h->z, h->z_plane, st);
+    const int X = m->xcd;
+    auto plan = [&](int N, int K) {
+      GemmPlan p = gemm_plan_bf16(R, N, K, X);
+      if (gemm_partials_floats(p, R) > h->gpart_cap || (size_t)p.n_fb > h->gcnt_cap ||
+          (N == d && p.n_fb > h->ssq_cap))
+        throw HipError{hipErrorInvalidValue, "GEMM plan exceeds the draft head's workspace"};
+      return p;
+    };
+    // u = W0 [h; e]; n = g * u (and the parts of sum u^2)
+    GemmPlan p0 = plan(d, 2 * d);
+    EpiArgs e = base;
+    e.kind = EPI_RESID;
+    e.gnext = h->g;
+    e.ld = d;
+    gemm_bf16(p0, h->w0, d, 2 * d, h->z, h->z_plane, 2 * d, R, e, h->gpart, h->gcnt, st);
+    // SwiGLU(n / rms(u))
+    GemmPlan p1 = plan(2 * mi, d);
+    e = base;
+    e.kind = EPI_SWIGLU;
+    e.ssq = h->ssq;
+    e.ssq_parts = p0.n_fb;
+    e.ld = mi;
+    gemm_bf16(p1, h->w13, 2 * mi, d, h->xn, h->xn_plane, d, R, e, h->gpart, h->gcnt, st);
+    // h_hat = u + W2 (...); n = g_f * h_hat for the output layer
+    GemmPlan p2 = plan(d, mi);
+    e = base;
+    e.kind = EPI_RESID;
+    e.gnext = m->gf;
+    e.ld = d;
+    gemm_bf16(p2, h->w2, d, mi, h->hb, h->hb_plane, mi, R, e, h->gpart, h->gcnt, st);
+    // GenHead(RMSNorm(h_hat)) over the image codes
+    GemmPlan p3 = plan(dm.Vimg, d);
+    e = base;
+    e.kind = EPI_LOGITS;
+    e.ssq = h->ssq;
+    e.ssq_parts = p2.n_fb;
+    e.ld = dm.Vimg;
+    gemm_bf16(p3, m->wlm, dm.Vimg, d, h->xn, h->xn_plane, d, R, e, h->gpart, h->gcnt, st);
+  }
+  first_token(R, dm.Vimg, dm.img_lo, h->logits, SSD_GREEDY, 0, 1.0, 0, nullptr, h->out, 1, st);
+  HIPCHK(hipGetLastError());
+}
+
+}  // namespace
+
 extern "C" {
 
 int64_t ssd_draft_head_numel(const ssd_model* m, int32_t mi) {
@@ -1191,7 +1298,6 @@ ssd_status ssd_draft_head_init(ssd_model* m, int32_t mi, const void* weights, in
   *out = nullptr;
   if (m->poisoned) return fail(SSD_E_STATE, "model is poisoned by an earlier device error");
   const Dims& dm = m->dm;
-  if (!dm.bf16) return fail(SSD_E_INVAL, "draft heads need a bf16 model");
   if (mi <= 0 || mi % 256 != 0 || mi > (1 << 16)) return fail(SSD_E_INVAL, "m must be a positive multiple of 256");
   if (max_rows < 1 || max_rows > (1 << 16)) return fail(SSD_E_INVAL, "max_rows must be in [1, 65536]");
   auto* h = new ssd_draft_head();
@@ -1205,7 +1311,7 @@ ssd_status ssd_draft_head_init(ssd_model* m, int32_t mi, const void* weights, in
   try {
     Allocs tmp;
     const size_t max_seg = std::max({(size_t)d * 2 * d, (size_t)2 * mi * d, (size_t)d * mi});
-    uint16_t* stage = tmp.get<uint16_t>(max_seg);
+    uint16_t* stage = tmp.get<uint16_t>(max_seg * (dm.bf16 ? 1 : 2));
     std::vector<int> map_id(std::max({2 * d, 2 * mi, d})), map_13(2 * mi);
     for (size_t n = 0; n < map_id.size(); ++n) map_id[n] = (int)n;
     for (int n = 0; n < 2 * mi; ++n) map_13[n] = (n % 2 == 0) ? n / 2 : mi + n / 2;
@@ -1214,6 +1320,27 @@ ssd_status ssd_draft_head_init(ssd_model* m, int32_t mi, const void* weights, in
     HIPCHK(hipMemcpy(d_id, map_id.data(), map_id.size() * 4, hipMemcpyHostToDevice));
     HIPCHK(hipMemcpy(d_13, map_13.data(), map_13.size() * 4, hipMemcpyHostToDevice));
     const uint16_t* src = (const uint16_t*)weights;
+    if (!dm.bf16) {
+      // fp32 models: row-major fp32 weights, gate/up rows interleaved
+      const float* sf = (const float*)weights;
+      auto copy = [&](size_t off, size_t n) -> float* {
+        float* dst = h->mem.get<float>(n);
+        HIPCHK(hipMemcpy(dst, sf + off, n * 4, hipMemcpyDefault));
+        return dst;
+      };
+      size_t off = 0;
+      h->w0 = copy(off, (size_t)d * 2 * d);
+      off += (size_t)d * 2 * d;
+      h->g = copy(off, d);
+      off += d;
+      HIPCHK(hipMemcpy(stage, sf + off, (size_t)2 * mi * d * 4, hipMemcpyDefault));
+      h->w13 = h->mem.get<float>((size_t)2 * mi * d);
+      gather_rows_f32((const float*)stage, d_13, 2 * mi, d, (float*)h->w13, st);
+      HIPCHK(hipGetLastError());
+      HIPCHK(hipStreamSynchronize(st));
+      off += (size_t)2 * mi * d;
+      h->w2 = copy(off, (size_t)d * mi);
+    }
     auto pack = [&](size_t off, int N, int K, const int* map) -> void* {
       HIPCHK(hipMemcpy(stage, src + off, (size_t)N * K * 2, hipMemcpyDefault));
       void* dst = h->mem.get<char>((size_t)N * K * 2);
@@ -1223,9 +1350,9 @@ ssd_status ssd_draft_head_init(ssd_model* m, int32_t mi, const void* weights, in
       return dst;
     };
     size_t off = 0;
-    h->w0 = pack(off, d, 2 * d, d_id);
+    if (dm.bf16) h->w0 = pack(off, d, 2 * d, d_id);
     off += (size_t)d * 2 * d;
-    {
+    if (dm.bf16) {
       std::vector<uint16_t> hb(d);
       HIPCHK(hipMemcpy(hb.data(), src + off, (size_t)d * 2, hipMemcpyDefault));
       std::vector<float> hf(d);
@@ -1237,13 +1364,16 @@ ssd_status ssd_draft_head_init(ssd_model* m, int32_t mi, const void* weights, in
       HIPCHK(hipMemcpy(h->g, hf.data(), (size_t)d * 4, hipMemcpyHostToDevice));
     }
     off += d;
-    h->w13 = pack(off, 2 * mi, d, d_13);
-    off += (size_t)2 * mi * d;
-    h->w2 = pack(off, d, mi, d_id);
+    if (dm.bf16) {
+      h->w13 = pack(off, 2 * mi, d, d_13);
+      off += (size_t)2 * mi * d;
+      h->w2 = pack(off, d, mi, d_id);
+    }
     // workspaces for every plan a run of up to max_rows rows can meet
     size_t gpart = 0, gcnt = 0;
     int parts = 1;
-    for (int Mc : {1, 16, 17, 32, 33, 64, 65, 128}) {
+    for (int Mc : {1, 16, 17, 32, 33, 64, 65, 128, 129, 256}) {
+      if (!dm.bf16) break;
       for (auto nk : {std::make_pair(d, 2 * d), std::make_pair(2 * mi, d), std::make_pair(d, mi),
                       std::make_pair(dm.Vimg, d)}) {
         GemmPlan p = gemm_plan_bf16(Mc, nk.first, nk.second, 0);
@@ -1292,7 +1422,7 @@ ssd_status ssd_draft_head_run(ssd_draft_head* h, int32_t R, const float* hs, con
   if (R < 1 || R > h->Rmax) return fail(SSD_E_INVAL, "R = %d outside [1, max_rows = %d]", R, h->Rmax);
   ssd_model* m = h->m;
   const Dims& dm = m->dm;
-  const int d = h->d, mi = h->mi;
+  const int d = h->d;
   if (!is_device_ptr(tokens)) {
     ssd_status cs = check_tokens_host(tokens, (size_t)R, 0, dm.V, "tokens");
     if (cs != SSD_OK) return cs;
@@ -1302,66 +1432,7 @@ ssd_status ssd_draft_head_run(ssd_draft_head* h, int32_t R, const float* hs, con
   try {
     HIPCHK(hipMemcpyAsync(h->hin, hs, (size_t)R * d * 4, hipMemcpyDefault, st));
     HIPCHK(hipMemcpyAsync(h->tok, tokens, (size_t)R * 4, hipMemcpyDefault, st));
-    draft_input(h->hin, m->emb, h->tok, R, d, h->z, h->z_plane, st);
-    fill_u32((unsigned*)h->x, (size_t)R * d, 0u, st);  // u accumulates onto zero
-    const int X = m->xcd;
-    EpiArgs base{};
-    base.Kblk = h->Rmax;  // every row is block position t of "sequence" 0
-    base.f = h->f0;
-    base.ssq_ld = h->Rmax;
-    base.ssq_step = 1;
-    base.inv_d = 1.0f / (float)d;
-    base.eps = dm.eps;
-    base.Hq = dm.Hq;
-    base.Hkv = dm.Hkv;
-    base.D = dm.D;
-    base.x = h->x;
-    base.xn = h->xn;
-    base.xn_plane = h->xn_plane;
-    base.ssq_out = h->ssq;
-    base.ssq_out_ld = h->Rmax;
-    base.h = h->hb;
-    base.h_plane = h->hb_plane;
-    base.logits = h->logits;
-    auto plan = [&](int N, int K) {
-      GemmPlan p = gemm_plan_bf16(R, N, K, X);
-      if (gemm_partials_floats(p, R) > h->gpart_cap || (size_t)p.n_fb > h->gcnt_cap ||
-          (N == d && p.n_fb > h->ssq_cap))
-        throw HipError{hipErrorInvalidValue, "GEMM plan exceeds the draft head's workspace"};
-      return p;
-    };
-    // u = W0 [h; e]; n = g * u (and the parts of sum u^2)
-    GemmPlan p0 = plan(d, 2 * d);
-    EpiArgs e = base;
-    e.kind = EPI_RESID;
-    e.gnext = h->g;
-    e.ld = d;
-    gemm_bf16(p0, h->w0, d, 2 * d, h->z, h->z_plane, 2 * d, R, e, h->gpart, h->gcnt, st);
-    // SwiGLU(n / rms(u))
-    GemmPlan p1 = plan(2 * mi, d);
-    e = base;
-    e.kind = EPI_SWIGLU;
-    e.ssq = h->ssq;
-    e.ssq_parts = p0.n_fb;
-    e.ld = mi;
-    gemm_bf16(p1, h->w13, 2 * mi, d, h->xn, h->xn_plane, d, R, e, h->gpart, h->gcnt, st);
-    // h_hat = u + W2 (...); n = g_f * h_hat for the output layer
-    GemmPlan p2 = plan(d, mi);
-    e = base;
-    e.kind = EPI_RESID;
-    e.gnext = m->gf;
-    e.ld = d;
-    gemm_bf16(p2, h->w2, d, mi, h->hb, h->hb_plane, mi, R, e, h->gpart, h->gcnt, st);
-    // GenHead(RMSNorm(h_hat)) over the image codes, then the argmax
-    GemmPlan p3 = plan(dm.Vimg, d);
-    e = base;
-    e.kind = EPI_LOGITS;
-    e.ssq = h->ssq;
-    e.ssq_parts = p2.n_fb;
-    e.ld = dm.Vimg;
-    gemm_bf16(p3, m->wlm, dm.Vimg, d, h->xn, h->xn_plane, d, R, e, h->gpart, h->gcnt, st);
-    first_token(R, dm.Vimg, dm.img_lo, h->logits, SSD_GREEDY, 0, 1.0, 0, nullptr, h->out, 1, st);
-    HIPCHK(hipGetLastError());
+    head_forward(h, R, h->hin, h->tok, st);
     HIPCHK(hipMemcpyAsync(drafts, h->out, (size_t)R * 4, hipMemcpyDefault, st));
     if (logits_out) HIPCHK(hipMemcpyAsync(logits_out, h->logits, (size_t)R * dm.Vimg * 4, hipMemcpyDefault, st));
     if (host_out) HIPCHK(hipStreamSynchronize(st));
@@ -1560,7 +1631,7 @@ ssd_status ssd_verify_step(ssd_session* s, int32_t K, int32_t* tokens, const flo
 namespace {
 
 struct Op {
-  int kind;  // 0 verify, 1 commit
+  int kind;  // 0 verify, 1 commit, 2 horizontal draft (src, K heads), 3 vertical draft (row src, K rows)
   int start, K, nf, rnd;
 };
 
@@ -1575,10 +1646,12 @@ std::vector<Op> make_plan(int H, int W, int k_h, int h_rounds, int k_v, int b, i
   for (int s = 1; s < W;) {
     int e = std::min(s + k_h, W);
     if (first) {
+      ops.push_back(Op{2, 0, e - 1, 0, 0});
       verify(0, e, 1, h_rounds);
       ops.push_back(Op{1, 0, e, 0, 0});
       first = false;
     } else {
+      ops.push_back(Op{2, s - 1, e - s, 0, 0});
       verify(s, e - s, 0, h_rounds);
       ops.push_back(Op{1, s, e - s, 0, 0});
     }
@@ -1587,6 +1660,7 @@ std::vector<Op> make_plan(int H, int W, int k_h, int h_rounds, int k_v, int b, i
   if (W == 1) ops.push_back(Op{1, 0, 1, 0, 0});
   for (int y = 1; y < H;) {
     int m = std::min(k_v, H - y);
+    ops.push_back(Op{3, y - 1, m, 0, 0});
     verify(y * W, m * W, 0, b);
     ops.push_back(Op{1, y * W, W, 0, 0});
     for (int j = 1; j < m; ++j) {
@@ -1600,11 +1674,25 @@ std::vector<Op> make_plan(int H, int W, int k_h, int h_rounds, int k_v, int b, i
 
 }  // namespace
 
-ssd_status ssd_decode_image(ssd_model* m, const ssd_schedule* sc, int32_t B, int32_t P, const int32_t* prefix,
-                            const int32_t* drafts, const float* draft_logits, int32_t* out_tokens, ssd_stats* stats,
-                            void* stream) {
-  g_err.clear();
-  if (!m || !sc || !prefix || !drafts || !out_tokens) return fail(SSD_E_INVAL, "NULL argument");
+namespace {
+
+// Draft source of an image decode: a planted table (drafts, optional draft
+// logits) or spatial heads (horizontal heads for offsets +1.., vertical heads
+// for rows +1..).
+struct DraftSource {
+  const int32_t* drafts = nullptr;
+  const float* draft_logits = nullptr;
+  ssd_draft_head* const* hh = nullptr;
+  int nh = 0;
+  ssd_draft_head* const* vh = nullptr;
+  int nv = 0;
+};
+
+ssd_status decode_impl(ssd_model* m, const ssd_schedule* sc, int32_t B, int32_t P, const int32_t* prefix,
+                       const DraftSource& src, int32_t* out_tokens, ssd_stats* stats, void* stream) {
+  const int32_t* drafts = src.drafts;
+  const float* draft_logits = src.draft_logits;
+  const bool heads = src.hh != nullptr || src.vh != nullptr;
   if (m->poisoned) return fail(SSD_E_STATE, "model is poisoned by an earlier device error");
   const Dims& dm = m->dm;
   const int H = sc->grid_h, W = sc->grid_w;
@@ -1625,13 +1713,29 @@ ssd_status ssd_decode_image(ssd_model* m, const ssd_schedule* sc, int32_t B, int
   int Kmax = 1;
   int nverify = 0;
   for (const Op& o : ops) {
-    Kmax = std::max(Kmax, o.K);
+    if (o.kind <= 1) Kmax = std::max(Kmax, o.K);
     nverify += o.kind == 0;
   }
+  if (heads) {
+    // every head the plan calls must exist, belong to this model and hold its rows
+    for (const Op& o : ops) {
+      if (o.kind < 2) continue;
+      const bool hor = o.kind == 2;
+      const int need = hor ? B : B * W;
+      for (int j = 0; j < o.K; ++j) {
+        ssd_draft_head* h = j < (hor ? src.nh : src.nv) ? (hor ? src.hh : src.vh)[j] : nullptr;
+        if (!h) return fail(SSD_E_INVAL, "the schedule needs %s head %d", hor ? "horizontal" : "vertical", j + 1);
+        if (h->m != m) return fail(SSD_E_INVAL, "a draft head belongs to another model");
+        if (h->poisoned) return fail(SSD_E_STATE, "a draft head is poisoned");
+        if (h->Rmax < need) return fail(SSD_E_INVAL, "a %s head drafts %d rows per call here; its max_rows is %d",
+                                        hor ? "horizontal" : "vertical", need, h->Rmax);
+      }
+    }
+  }
   if (nverify >= 65536) return fail(SSD_E_INVAL, "more than 65535 verify rounds");
-  std::vector<int32_t> hpre((size_t)Bs * P), hdr((size_t)B * N);
+  std::vector<int32_t> hpre((size_t)Bs * P), hdr((size_t)B * N, dm.img_lo);
   if (hipMemcpy(hpre.data(), prefix, hpre.size() * 4, hipMemcpyDefault) != hipSuccess ||
-      hipMemcpy(hdr.data(), drafts, hdr.size() * 4, hipMemcpyDefault) != hipSuccess) {
+      (!heads && hipMemcpy(hdr.data(), drafts, hdr.size() * 4, hipMemcpyDefault) != hipSuccess)) {
     (void)hipGetLastError();
     return fail(SSD_E_INVAL, "prefix or drafts not readable");
   }
@@ -1672,7 +1776,17 @@ ssd_status ssd_decode_image(ssd_model* m, const ssd_schedule* sc, int32_t B, int
       s->img = s->mem.get<int>((size_t)B * N);
       s->img_cap = B * N;
     }
-    if (draft_logits && !s->qtab) s->qtab = s->mem.get<float>((size_t)B * N * dm.Vimg);
+    const bool use_q = sc->rule == SSD_ACCEPT_REJECT && (draft_logits || heads);
+    if (use_q && s->qtab_cap < (size_t)B * N * dm.Vimg) {
+      s->qtab = s->mem.get<float>((size_t)B * N * dm.Vimg);
+      s->qtab_cap = (size_t)B * N * dm.Vimg;
+    }
+    if (heads && s->hs_cap < (size_t)B * N * dm.d) {
+      s->hs = s->mem.get<float>((size_t)B * N * dm.d);
+      s->hs_cap = (size_t)B * N * dm.d;
+      s->hsrc = s->mem.get<float>((size_t)B * W * dm.d);
+      s->tsrc = s->mem.get<int>((size_t)B * W);
+    }
     HIPCHK(hipMemcpyAsync(s->img, hdr.data(), hdr.size() * 4, hipMemcpyHostToDevice, st));
     if (draft_logits)
       HIPCHK(hipMemcpyAsync(s->qtab, draft_logits, (size_t)B * N * dm.Vimg * 4, hipMemcpyDefault, st));
@@ -1683,6 +1797,10 @@ ssd_status ssd_decode_image(ssd_model* m, const ssd_schedule* sc, int32_t B, int
     HIPCHK(hipMemcpyAsync(s->tok, hpre.data(), hpre.size() * 4, hipMemcpyHostToDevice, st));
     prefill_pass(s);
     ++passes;
+    const size_t rowb = (size_t)dm.d * 4;  // bytes of one state
+    if (heads)  // the state that scores image token 0: the prompt's last (conditional streams)
+      HIPCHK(hipMemcpy2DAsync(s->hs, (size_t)N * rowb, s->x + (size_t)(P - 1) * dm.d, (size_t)P * rowb, rowb, B,
+                              hipMemcpyDeviceToDevice, st));
     // per-image scores: the streams' own logits, or their guided mix
     const float* lg = s->cfg ? s->mlog : s->logits;
     const float* cy = s->cfg ? s->mcarry : s->carry;
@@ -1707,12 +1825,36 @@ ssd_status ssd_decode_image(ssd_model* m, const ssd_schedule* sc, int32_t B, int
     a.count = s->cnt;
     a.amax = s->amax;
     for (const Op& o : ops) {
+      if (o.kind >= 2) {
+        if (!heads) continue;
+        // heads draft from chosen tokens: [h; e] with h the state that scored each
+        const bool hor = o.kind == 2;
+        const int n_src = hor ? 1 : W;                 // source positions per image
+        const int p0 = hor ? o.start : o.start * W;    // first source position
+        const int step = hor ? 1 : W;                  // offset of head j is j * step
+        HIPCHK(hipMemcpy2DAsync(s->hsrc, n_src * rowb, s->hs + (size_t)p0 * dm.d, (size_t)N * rowb, n_src * rowb, B,
+                                hipMemcpyDeviceToDevice, st));
+        HIPCHK(hipMemcpy2DAsync(s->tsrc, (size_t)n_src * 4, s->img + p0, (size_t)N * 4, (size_t)n_src * 4, B,
+                                hipMemcpyDeviceToDevice, st));
+        for (int j = 1; j <= o.K; ++j) {
+          ssd_draft_head* h = (hor ? src.hh : src.vh)[j - 1];
+          head_forward(h, B * n_src, s->hsrc, s->tsrc, st);
+          const int dst = p0 + j * step;
+          HIPCHK(hipMemcpy2DAsync(s->img + dst, (size_t)N * 4, h->out, (size_t)n_src * 4, (size_t)n_src * 4, B,
+                                  hipMemcpyDeviceToDevice, st));
+          if (use_q)
+            HIPCHK(hipMemcpy2DAsync(s->qtab + (size_t)dst * dm.Vimg, (size_t)N * dm.Vimg * 4, h->logits,
+                                    (size_t)n_src * dm.Vimg * 4, (size_t)n_src * dm.Vimg * 4, B,
+                                    hipMemcpyDeviceToDevice, st));
+        }
+        continue;
+      }
       HIPCHK(hipMemcpy2DAsync(s->tok, (size_t)o.K * 4, s->img + o.start, (size_t)N * 4, (size_t)o.K * 4, B,
                               hipMemcpyDeviceToDevice, st));
       if (s->cfg)
         HIPCHK(hipMemcpyAsync(s->tok + (size_t)B * o.K, s->tok, (size_t)B * o.K * 4, hipMemcpyDeviceToDevice, st));
       if (o.kind == 0) {
-        if (sc->rule == SSD_ACCEPT_REJECT && draft_logits) {
+        if (use_q) {
           // first round of a position: its reference is its draft distribution
           // (positions that already hold a reference keep it)
           set_ref_rows(B, o.K, N, dm.Vimg, s->qtab + (size_t)o.start * dm.Vimg, s->d_f, s->ref, s->ref_flag, s->ring,
@@ -1732,6 +1874,11 @@ ssd_status ssd_decode_image(ssd_model* m, const ssd_schedule* sc, int32_t B, int
         run_forward(s, o.K, 1);
         commit_update(Bs, -o.K, dm.Vimg, s->logits, s->carry, s->d_f, s->ref_flag, s->ring, st);
         for (int b = 0; b < Bs; ++b) s->f[b] += o.K;
+        // the committed block's states score image tokens start+1 .. start+K
+        const int n_in = std::min(o.K, N - o.start - 1);
+        if (heads && n_in > 0)
+          HIPCHK(hipMemcpy2DAsync(s->hs + (size_t)(o.start + 1) * dm.d, (size_t)N * rowb, s->x, (size_t)o.K * rowb,
+                                  (size_t)n_in * rowb, B, hipMemcpyDeviceToDevice, st));
       }
       ++passes;
     }
@@ -1756,6 +1903,35 @@ ssd_status ssd_decode_image(ssd_model* m, const ssd_schedule* sc, int32_t B, int
     return fail(SSD_E_DEVICE, "%s: %s", e.what, hipGetErrorString(e.e));
   }
   return SSD_OK;
+}
+
+}  // namespace
+
+ssd_status ssd_decode_image(ssd_model* m, const ssd_schedule* sc, int32_t B, int32_t P, const int32_t* prefix,
+                            const int32_t* drafts, const float* draft_logits, int32_t* out_tokens, ssd_stats* stats,
+                            void* stream) {
+  g_err.clear();
+  if (!m || !sc || !prefix || !drafts || !out_tokens) return fail(SSD_E_INVAL, "NULL argument");
+  DraftSource src;
+  src.drafts = drafts;
+  src.draft_logits = draft_logits;
+  return decode_impl(m, sc, B, P, prefix, src, out_tokens, stats, stream);
+}
+
+ssd_status ssd_decode_image_heads(ssd_model* m, const ssd_schedule* sc, int32_t B, int32_t P, const int32_t* prefix,
+                                  ssd_draft_head* const* h_heads, int32_t n_h, ssd_draft_head* const* v_heads,
+                                  int32_t n_v, int32_t* out_tokens, ssd_stats* stats, void* stream) {
+  g_err.clear();
+  if (!m || !sc || !prefix || !out_tokens) return fail(SSD_E_INVAL, "NULL argument");
+  if (n_h < 0 || n_v < 0 || (n_h > 0 && !h_heads) || (n_v > 0 && !v_heads))
+    return fail(SSD_E_INVAL, "bad head lists");
+  static ssd_draft_head* const none[1] = {nullptr};
+  DraftSource src;
+  src.hh = n_h > 0 ? h_heads : none;
+  src.nh = n_h;
+  src.vh = n_v > 0 ? v_heads : none;
+  src.nv = n_v;
+  return decode_impl(m, sc, B, P, prefix, src, out_tokens, stats, stream);
 }
 
 }  // extern "C"

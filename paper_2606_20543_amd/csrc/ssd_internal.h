@@ -318,6 +318,7 @@ void xcc_probe(int* out, int n_wg, hipStream_t st);
 void set_ref_rows(int B, int K, int rows_per_b, int Vimg, const float* src, const int* f, float* ref, int* ref_flag,
                   int ring, int only_new, hipStream_t st);
 // z = [h; e] split planes [R][2d] (plane elements apart) for a draft head
+void draft_input_f32(const float* h, const float* emb, const int* tok, int R, int d, float* z, hipStream_t st);
 void draft_input(const float* h, const void* emb, const int* tok, int R, int d, void* z, size_t plane,
                  hipStream_t st);
 // guided logits l_u + w (l_c - l_u): rows [Bi][K] from the pass's [2*Bi][K] logits

@@ -154,18 +154,24 @@ def weights(m, seed=SEED_WEIGHTS, std=0.02, gain_std=0.0):
 SEED_HEADS = 4
 
 
-def draft_head_weights(d, m, seed=SEED_HEADS, std=0.02, gain_std=0.0):
-    """Packed bf16 bits of one spatial draft head: W0 [d][2d], gain [d], W1 [m][d],
-    W3 [m][d], W2 [d][m] (tensor j on generator stream j; gains around 1)."""
+def draft_head_weights(d, m, seed=SEED_HEADS, std=0.02, gain_std=0.0, dtype="bf16"):
+    """Packed weights of one spatial draft head: W0 [d][2d], gain [d], W1 [m][d],
+    W3 [m][d], W2 [d][m] (tensor j on generator stream j; gains around 1), as
+    bf16 bits (uint16) or float32."""
     shapes = [("w0", (d, 2 * d)), ("g", (d,)), ("w1", (m, d)), ("w3", (m, d)), ("w2", (d, m))]
     total = int(sum(np.prod(s) for _, s in shapes))
-    buf = np.empty(total, dtype=np.uint16)
+    if dtype == "bf16":
+        buf, fn = np.empty(total, dtype=np.uint16), lib().synth_normal_bf16
+    elif dtype == "f32":
+        buf, fn = np.empty(total, dtype=np.float32), lib().synth_normal_f32
+    else:
+        raise ValueError(dtype)
     off = 0
     base = buf.ctypes.data
     for j, (name, shape) in enumerate(shapes):
         n = int(np.prod(shape))
         mean, sd = (1.0, gain_std) if name == "g" else (0.0, std)
-        lib().synth_normal_bf16(seed, j, mean, sd, n, ctypes.c_void_p(base + off * 2))
+        fn(seed, j, mean, sd, n, ctypes.c_void_p(base + off * buf.itemsize))
         off += n
     return buf
 

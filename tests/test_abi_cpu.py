@@ -111,4 +111,7 @@ def test_null_arguments_rejected_before_device_work(lib):
     assert L.ssd_draft_head_run(None, 1, None, None, None, None) == ssd.SSD_E_INVAL
     assert L.ssd_draft_head_numel(None, 256) == -1
     L.ssd_free_draft_head(None)  # a no-op
+    st = ssd.ssd_stats()
+    assert L.ssd_decode_image_heads(None, ctypes.byref(sc), 1, 1, None, None, 0, None, 0, None, ctypes.byref(st),
+                                    None) == ssd.SSD_E_INVAL
     assert "NULL" in ssd.ssd_last_error()
