@@ -21,7 +21,10 @@ with --forward persistent the single-launch forward kernel),
 `attention` (the same for the attention kernel), `draft_head` (the spatial
 draft head drafting one grid row per call, timed apart from the steps),
 `verify_pass_positions` (one drafted row verified at rows 1, H/4, H/2, H-1, 50 reps
-each, beside a one-token pass at the same place), `cpu_baseline` (the oracle
+each, beside a one-token pass at the same place), `cfg` (the same decode with
+classifier-free guidance, weight 5.0), `heads_decode` (the whole loop drafted by
+seeded spatial heads instead of planted drafts, and the drafting time per
+image), `cpu_baseline` (the oracle
 on the host cores on a bounded sample), AR tokens/s on the same kernels.
 """
 import argparse
@@ -119,6 +122,58 @@ def position_timing(ssd, model, shape, prefix, H, W, drafts, reps=50):
         ssd.ssd_free_session(sess)
     out["timing"] = "host clock around each synchronizing ssd_verify_step call (host token buffers)"
     return out
+
+
+def guided_rate(ssd, model, shape, sc, prefix, d_drafts, steps, weight=5.0):
+    """Image tokens/s of the same decode with classifier-free guidance (weight 5.0,
+    the paper's Janus-Pro setting): every image gets an unconditional twin stream
+    with a null prompt (id 0 repeated), so each pass carries twice the rows."""
+    import ctypes
+    import torch
+    B, P = prefix.shape
+    g = ssd.ssd_schedule()
+    ctypes.memmove(ctypes.addressof(g), ctypes.addressof(sc), ctypes.sizeof(sc))
+    g.cfg, g.cfg_weight = 1, weight
+    both = np.concatenate([prefix, np.zeros_like(prefix)]).astype(np.int32)
+    dev = torch.device("cuda:0")
+    d_both = torch.from_numpy(both).to(dev)
+    d_out = torch.zeros((B, sc.grid_h, sc.grid_w), dtype=torch.int32, device=dev)
+    ssd.ssd_decode_image(model, g, B, P, d_both, d_drafts, d_out)  # warmup (allocates the paired workspace)
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        st = ssd.ssd_decode_image(model, g, B, P, d_both, d_drafts, d_out)
+    dt = (time.perf_counter() - t0) / steps
+    return {"weight": weight, "value": B * sc.grid_h * sc.grid_w / dt, "unit": "image tokens/s",
+            "ms_per_image": dt * 1e3 / B, "passes_per_image": st.passes, "sequences": 2 * B,
+            "steps": steps, "unconditional_prompt": "id 0 repeated (null prompt of the same length)"}
+
+
+def heads_rate(ssd, model, shape, sc, prefix, d_prefix, steps, planted_ms):
+    """Image tokens/s of the whole SSD loop with drafts from spatial heads: k_h
+    horizontal heads and k_v vertical heads of inner size m = 2d (the paper's
+    head size), seeded random weights (no trained heads exist here, so the
+    acceptance says nothing about the method)."""
+    import torch
+    import synth
+    B, P = prefix.shape
+    d, m = shape.d_model, 2 * shape.d_model
+    n = sc.k_h + sc.k_v
+    heads = [ssd.ssd_draft_head_init(model, m, synth.draft_head_weights(d, m, seed=10 + j), B * sc.grid_w)
+             for j in range(n)]
+    try:
+        d_out = torch.zeros((B, sc.grid_h, sc.grid_w), dtype=torch.int32, device=torch.device("cuda:0"))
+        hh, vh = heads[:sc.k_h], heads[sc.k_h:]
+        ssd.ssd_decode_image_heads(model, sc, B, P, d_prefix, hh, vh, d_out)  # warmup
+        t0 = time.perf_counter()
+        for _ in range(steps):
+            st = ssd.ssd_decode_image_heads(model, sc, B, P, d_prefix, hh, vh, d_out)
+        dt = (time.perf_counter() - t0) / steps
+    finally:
+        for h in heads:
+            ssd.ssd_free_draft_head(h)
+    return {"value": B * sc.grid_h * sc.grid_w / dt, "unit": "image tokens/s", "ms_per_image": dt * 1e3 / B,
+            "draft_ms_per_image": dt * 1e3 / B - planted_ms, "heads": f"{sc.k_h} horizontal + {sc.k_v} vertical, m = 2d",
+            "passes_per_image": st.passes, "steps": steps, "acceptance_random_heads": st.accepted / max(st.proposed, 1)}
 
 
 def gemm_source_hash():
@@ -232,6 +287,8 @@ def main():
                          "(blocks of up to 32 tokens)")
     ap.add_argument("--no-draft-head", action="store_true", help="skip the draft-head timing")
     ap.add_argument("--no-positions", action="store_true", help="skip the per-position verify-pass timing")
+    ap.add_argument("--no-cfg", action="store_true", help="skip the guided (CFG) decode timing")
+    ap.add_argument("--no-heads", action="store_true", help="skip the head-drafted decode timing")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="only run a plain device copy of this size (PMC byte-counter calibration) and exit")
     args = ap.parse_args()
@@ -371,6 +428,12 @@ def main():
     if not args.no_positions:
         log("[bench] verify pass at four positions of the image")
         result["verify_pass_positions"] = position_timing(ssd, model, shape, prefix, H, W, drafts)
+    if not args.no_cfg:
+        log("[bench] the same decode with classifier-free guidance")
+        result["cfg"] = guided_rate(ssd, model, shape, sc, prefix, d_drafts, args.steps)
+    if not args.no_heads:
+        log("[bench] the whole loop with drafts from spatial heads")
+        result["heads_decode"] = heads_rate(ssd, model, shape, sc, prefix, d_prefix, args.steps, ms_step / B)
     if not args.no_draft_head and shape.dtype == "bf16":
         log("[bench] draft head: one grid row per call")
         result["draft_head"] = draft_head_cost(ssd, model, shape, target[0, 0] + shape.img_lo)
