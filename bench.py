@@ -324,10 +324,11 @@ def main():
     sc.grid_h, sc.grid_w, sc.k_h, sc.h_rounds, sc.k_v, sc.b_rounds, sc.i_rounds = H, W, 5, 1, 1, wl.rounds, 0
     sc.rule, sc.top_k, sc.temperature, sc.seed = wl.rule, wl.top_k, wl.temperature, synth.SEED_SAMPLING
 
-    # Target image: one decode with random drafts.  Under the greedy rule the
-    # committed image is the backbone's greedy image whatever the drafts are;
-    # under a sampling rule it is the sample this seed commits.  The timed
-    # drafts keep each target token with probability p_keep (else another code).
+    # Target image: the image one decode commits from random drafts (with a
+    # fixed number of rounds the committed image depends on the drafts, so
+    # the timed decode, whose drafts keep each target token with probability
+    # p_keep (else another code), need not commit it again).  Tokens/s does
+    # not depend on the drafts: the pass count is fixed by the schedule.
     log("[bench] target decode (random drafts)")
     d_rand = torch.from_numpy((synth.random_codes(shape, (B, H, W)) + shape.img_lo).astype(np.int32)).to(dev)
     ssd.ssd_decode_image(model, sc, B, P, d_prefix, d_rand, d_out)
