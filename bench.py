@@ -24,7 +24,8 @@ draft head drafting one grid row per call, timed apart from the steps),
 each, beside a one-token pass at the same place), `cfg` (the same decode with
 classifier-free guidance, weight 5.0), `heads_decode` (the whole loop drafted by
 seeded spatial heads instead of planted drafts, and the drafting time per
-image), `cpu_baseline` (the oracle
+image), `attention_at_scale` (the attention kernel on its own bytes at the 8B
+shape, batch 8, context 4352), `cpu_baseline` (the oracle
 on the host cores on a bounded sample), AR tokens/s on the same kernels.
 """
 import argparse
@@ -176,6 +177,49 @@ def heads_rate(ssd, model, shape, sc, prefix, d_prefix, steps, planted_ms):
             "passes_per_image": st.passes, "steps": steps, "acceptance_random_heads": st.accepted / max(st.proposed, 1)}
 
 
+def attention_at_scale(ssd, rounds=5):
+    """The attention kernel on its own bytes where attention is large: the 8B
+    shape (32 query / 8 KV heads of 128, GQA 4) with 8 sequences verifying
+    64-token blocks at context 4352 (the last row of a 64x64 image after a
+    256-token prompt: 4288 cached positions).  One layer of that model is
+    enough (attention does not depend on the others); per-launch events on the
+    library's stream give the kernel time, and the algorithmic bytes are the
+    KV read and the q/o traffic."""
+    import dataclasses
+    import synth
+    shape = dataclasses.replace(synth.M8B, n_layers=1)
+    B, K = 8, 64
+    P = 4352 - K
+    w = synth.weights(shape)
+    model = ssd.ssd_init_model(cfg_of(ssd, shape), w)
+    del w
+    try:
+        sess = ssd.ssd_prefill(model, B, P, synth.prompt(shape, B, P), P + K, K)
+        try:
+            prm = ssd.ssd_verify_params()
+            prm.rule, prm.temperature = ssd.SSD_GREEDY, 1.0
+            tok = (synth.random_codes(shape, (B, K)) + shape.img_lo).astype(np.int32)
+            fr = np.zeros(B, np.int32)
+            ssd.ssd_verify_step(sess, K, tok, prm, frontier=fr)  # warm
+            ssd.ssd_profile(model, 1)
+            ssd.ssd_profile_read(model, reset=True)
+            for r in range(rounds):
+                prm.round = r + 1
+                ssd.ssd_verify_step(sess, K, tok, prm, frontier=fr)
+            prof = ssd.ssd_profile_read(model, reset=True)
+            ssd.ssd_profile(model, 0)
+        finally:
+            ssd.ssd_free_session(sess)
+    finally:
+        ssd.ssd_free_model(model)
+    ms, n, by = prof["attention"]
+    gbs = by / (ms / 1e3) / 1e9
+    return {"shape": "8B: 32q/8kv heads x 128, batch 8, 64-token blocks, context 4352", "bound": "hbm",
+            "achieved": gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": gbs / HBM_PEAK_GBS, "launches": n,
+            "ms_per_launch": ms / n, "bytes_per_launch": by / n,
+            "timing": "dispatch-timestamp events around each attention launch"}
+
+
 def gemm_source_hash():
     import hashlib
     h = hashlib.sha256()
@@ -289,6 +333,7 @@ def main():
     ap.add_argument("--no-positions", action="store_true", help="skip the per-position verify-pass timing")
     ap.add_argument("--no-cfg", action="store_true", help="skip the guided (CFG) decode timing")
     ap.add_argument("--no-heads", action="store_true", help="skip the head-drafted decode timing")
+    ap.add_argument("--no-attn-scale", action="store_true", help="skip the attention timing at the 8B shape")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="only run a plain device copy of this size (PMC byte-counter calibration) and exit")
     args = ap.parse_args()
@@ -438,6 +483,11 @@ def main():
     if not args.no_draft_head and shape.dtype == "bf16":
         log("[bench] draft head: one grid row per call")
         result["draft_head"] = draft_head_cost(ssd, model, shape, target[0, 0] + shape.img_lo)
+    ssd.ssd_free_model(model)
+    model = None
+    if not args.no_attn_scale:
+        log("[bench] attention at the 8B shape, context 4352")
+        result["attention_at_scale"] = attention_at_scale(ssd)
     if f_n > 0:
         # the single-launch pass carries the weight stream: it is the kernel the roofline is about
         result["roofline"] = dict(result["forward_launch"], traffic=None,
@@ -446,7 +496,6 @@ def main():
         log("[bench] timing the oracle on the host cores")
         result["cpu_baseline"] = cpu_baseline(wl, w, prefix, drafts)
     print(json.dumps(result), flush=True)
-    ssd.ssd_free_model(model)
 
 
 if __name__ == "__main__":

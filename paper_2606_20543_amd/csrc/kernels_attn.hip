@@ -65,7 +65,8 @@ AttnPlan attn_plan(const Dims& dm, int B, int K, int max_ctx_now, int xcd, int g
     // workgroup, a split adds the partial publish and the merge (about
     // 1.6 us + 0.08 us per chunk); measured on MI355X with D = 128
     double best_t = 1e30;
-    for (int n = 1; n <= AT_MAX_CHUNKS && (grid > 0 ? (long)xcd_grid((int)units, n, xcd) : units * n) <= slots; ++n) {
+    for (int n = 1;
+         n <= AT_MAX_CHUNKS && (grid > 0 ? (long)xcd_grid(B * dm.Hkv, p.nqg * n, xcd) : units * n) <= slots; ++n) {
       const int ch = chunk_for(n);
       const int nn = (ctx + ch - 1) / ch;
       if (nn != n) continue;
@@ -123,7 +124,7 @@ AttnKArgs attn_args(const Dims& dm, const AttnPlan& p, int B, int K, const int* 
 }
 
 int attn_items(const AttnKArgs& a) {
-  return a.nchunk == 1 ? xcd_grid(a.heads, a.nqg, a.xcd) : xcd_grid(a.groups, a.nchunk, a.xcd);
+  return xcd_grid(a.heads, a.nqg * a.nchunk, a.xcd);
 }
 
 void attention_bf16(const Dims& dm, const AttnPlan& p, int B, int K, const int* f, const void* q, size_t q_plane,

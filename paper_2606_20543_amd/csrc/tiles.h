@@ -608,9 +608,8 @@ __device__ __forceinline__ int attn_unit(const AttnKArgs& a, int item, float* sm
   constexpr int NOUT = ROWS * D / 4;                          // float4 outputs of the workgroup
   constexpr int NV = (NOUT + NTH - 1) / NTH;    // per thread
   static_assert(2 * AT_MAX_CHUNKS * ROWS <= NW * ROWS * RS, "chunk statistics fit the O stage");
-  // single chunk: the query groups of one (sequence, KV head) share an XCD
-  // (they read the same K/V); several chunks: the chunks of one query group
-  // share an XCD (their partials meet in its L2)
+  // the workgroups of one (sequence, KV head) share an XCD: its query groups
+  // read the same K/V
   int grp_id, c, z, qg;
   if (a.nchunk == 1) {
     xcd_unmap(item, a.nqg, a.xcd, z, qg);
@@ -618,10 +617,15 @@ __device__ __forceinline__ int attn_unit(const AttnKArgs& a, int item, float* sm
     grp_id = z * a.nqg + qg;
     c = 0;
   } else {
-    xcd_unmap(item, a.nchunk, a.xcd, grp_id, c);
-    if (grp_id >= a.groups) return -1;
-    qg = grp_id % a.nqg;
-    z = grp_id / a.nqg;
+    // every query group and key chunk of one (sequence, KV head) on one XCD:
+    // the chunk partials meet in its L2, and the query groups' reads of the
+    // same keys and values hit it (query groups of one chunk run together)
+    int r;
+    xcd_unmap(item, a.nqg * a.nchunk, a.xcd, z, r);
+    if (z >= a.heads) return -1;
+    c = r / a.nqg;
+    qg = r - c * a.nqg;
+    grp_id = z * a.nqg + qg;
   }
   const int b = z / a.Hkv, hkv = z - b * a.Hkv;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
