@@ -27,14 +27,14 @@ namespace ssd {
 
 // one wave per SIMD: the register file holds two K/V blocks, the queries and
 // the accumulators without the compiler sinking the prefetch loads
-template <int D, int QPW>
+template <int D, int QPW, bool QS>
 __global__ __launch_bounds__(AtShape<QPW>::THREADS) __attribute__((amdgpu_waves_per_eu(1, 1)))
 void attn_bf16_kernel(AttnKArgs a) {
   constexpr int NW = AtShape<QPW>::WAVES, ROWS = QPW * 16, RS = D + 4;
   __shared__ __align__(16) float sm_o[NW * ROWS * RS];
   __shared__ float sm_m[NW * ROWS], sm_l[NW * ROWS];
   __shared__ int is_last;
-  attn_unit<D, QPW>(a, blockIdx.x, sm_o, sm_m, sm_l, &is_last);
+  attn_unit<D, QPW, PlainMem, true, PlainMem, false, QS>(a, blockIdx.x, sm_o, sm_m, sm_l, &is_last);
 }
 
 AttnPlan attn_plan(const Dims& dm, int B, int K, int max_ctx_now, int xcd, int grid) {
@@ -44,7 +44,10 @@ AttnPlan attn_plan(const Dims& dm, int B, int K, int max_ctx_now, int xcd, int g
   p.rows = K * g;
   const int qt = (p.rows + 15) / 16;
   p.qpw = (qt >= 4 && grid == 0) ? 2 : 1;
-  p.nqg = (qt + p.qpw - 1) / p.qpw;
+  // 128 or more query rows per (sequence, KV head): the waves split the rows,
+  // so a K/V block is streamed once per 128 rows instead of once per 32
+  p.qs = (qt >= 8 && grid == 0 && dm.D == 128) ? 1 : 0;  // (with D = 64 its chunk statistics outgrow the LDS stage)
+  p.nqg = (qt + (p.qs ? 4 : 1) * p.qpw - 1) / ((p.qs ? 4 : 1) * p.qpw);
   const long units = (long)B * dm.Hkv * p.nqg;
   const int ctx = max_ctx_now < 1 ? 1 : max_ctx_now;
   auto chunk_for = [&](int n) {  // whole workgroup steps covering ctx in n chunks
@@ -62,15 +65,17 @@ AttnPlan attn_plan(const Dims& dm, int B, int K, int max_ctx_now, int xcd, int g
     p.chunk = chunk;
   } else {
     // few query groups: a chunk costs about 0.85 us per 128-key step of its
-    // workgroup, a split adds the partial publish and the merge (about
-    // 1.6 us + 0.08 us per chunk); measured on MI355X with D = 128
+    // workgroup (per 32-key step when the waves split the query rows), a split
+    // adds the partial publish and the merge (about 1.6 us + 0.08 us per
+    // chunk); measured on MI355X with D = 128
+    const double keys_per_step = p.qs ? AT_KEYS : AT_STEP;
     double best_t = 1e30;
     for (int n = 1;
          n <= AT_MAX_CHUNKS && (grid > 0 ? (long)xcd_grid(B * dm.Hkv, p.nqg * n, xcd) : units * n) <= slots; ++n) {
       const int ch = chunk_for(n);
       const int nn = (ctx + ch - 1) / ch;
       if (nn != n) continue;
-      const double t = 0.85 * (ch / AT_STEP) * (dm.D / 128.0) + (n > 1 ? 1.6 + 0.08 * n : 0.0);
+      const double t = 0.85 * (ch / keys_per_step) * (dm.D / 128.0) + (n > 1 ? 1.6 + 0.08 * n : 0.0);
       if (t < best_t - 1e-9) {
         best_t = t;
         best = n;
@@ -83,12 +88,12 @@ AttnPlan attn_plan(const Dims& dm, int B, int K, int max_ctx_now, int xcd, int g
 }
 
 size_t attn_partials_floats(const Dims& dm, const AttnPlan& p, int B) {
-  return (size_t)B * dm.Hkv * p.nqg * p.nchunk * p.qpw * 16 * (dm.D + 2);
+  return (size_t)B * dm.Hkv * p.nqg * p.nchunk * p.group_rows() * (dm.D + 2);
 }
 
-template <int D, int QPW>
+template <int D, int QPW, bool QS = false>
 static void launch_attn(const AttnKArgs& a, hipStream_t st) {
-  launch_timed(attn_bf16_kernel<D, QPW>, dim3(attn_items(a)), dim3(AtShape<QPW>::THREADS), st, a);
+  launch_timed(attn_bf16_kernel<D, QPW, QS>, dim3(attn_items(a)), dim3(AtShape<QPW>::THREADS), st, a);
 }
 
 AttnKArgs attn_args(const Dims& dm, const AttnPlan& p, int B, int K, const int* f, const void* q, size_t q_plane,
@@ -105,7 +110,7 @@ AttnKArgs attn_args(const Dims& dm, const AttnPlan& p, int B, int K, const int* 
   a.groups = a.heads * p.nqg;
   // partial O block first, then the (max, sum) pairs (offset is a multiple of D floats: 8-byte aligned)
   a.opart = partials;
-  a.spart = (float2*)(partials + (size_t)a.groups * p.nchunk * p.qpw * 16 * dm.D);
+  a.spart = (float2*)(partials + (size_t)a.groups * p.nchunk * p.group_rows() * dm.D);
   a.counters = counters;
   a.f = f;
   a.K = K;
@@ -132,7 +137,8 @@ void attention_bf16(const Dims& dm, const AttnPlan& p, int B, int K, const int* 
                     unsigned* counters, hipStream_t st) {
   const AttnKArgs a = attn_args(dm, p, B, K, f, q, q_plane, kc, vc, Lmax, o, o_plane, partials, counters);
   if (dm.D == 128) {
-    if (p.qpw == 2) launch_attn<128, 2>(a, st);
+    if (p.qs) launch_attn<128, 2, true>(a, st);
+    else if (p.qpw == 2) launch_attn<128, 2>(a, st);
     else launch_attn<128, 1>(a, st);
   } else {
     if (p.qpw == 2) launch_attn<64, 2>(a, st);

@@ -499,7 +499,11 @@ __device__ __forceinline__ void load_kv(KVTile<D>& t, const uint16_t* kbase, con
 // one 32-key block through the online softmax of the wave's query tiles
 // QL: the query operands come from LDS (qs: tiles (qt, kd, plane) of 1 KiB in
 // lane order) instead of registers (for callers short of registers).
-template <int D, int QPW, bool QL = false>
+// MASK = false: every key of the block is visible to every query (the block
+// lies below the block's first position), so no causal mask is applied.
+// The O rescale runs only when some lane's running max moved (alpha != 1):
+// over long contexts the max settles and the accumulators stay untouched.
+template <int D, int QPW, bool QL = false, bool MASK = true>
 __device__ __forceinline__ void attend_block(const KVTile<D>& t, int key0, const bf16x8 (&qh)[QPW][D / 32],
                                              const bf16x8 (&ql)[QPW][D / 32], const int (&qpos)[QPW],
                                              float scale_log2, int grp, float (&m)[QPW], float (&l)[QPW],
@@ -537,7 +541,7 @@ __device__ __forceinline__ void attend_block(const KVTile<D>& t, int key0, const
       for (int e = 0; e < 4; ++e) {
         const int key = key0 + kt * 16 + 4 * grp + e;
         float v = s[kt][qt][e] * scale_log2;
-        v = (key <= qpos[qt]) ? v : -INFINITY;
+        if constexpr (MASK) v = (key <= qpos[qt]) ? v : -INFINITY;
         sv[kt * 4 + e] = v;
         mx = fmaxf(mx, v);
       }
@@ -545,12 +549,13 @@ __device__ __forceinline__ void attend_block(const KVTile<D>& t, int key0, const
     mx = fmaxf(mx, __shfl_xor(mx, 32));
     const float mnew = fmaxf(m[qt], mx);
     const bool none = (mnew == -INFINITY);
-    const float alpha = none ? 1.f : exp2f(m[qt] - mnew);
+    // exponents are <= 0 (exp2 of -inf is 0): the hardware exp2 needs no range handling
+    const float alpha = none ? 1.f : __builtin_amdgcn_exp2f(m[qt] - mnew);
     float ps = 0.f;
     uint16_t pb[8], pl[8];
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
-      const float p = none ? 0.f : exp2f(sv[i] - mnew);
+      const float p = none ? 0.f : __builtin_amdgcn_exp2f(sv[i] - mnew);
       ps += p;
       pb[i] = f2bf(p);
       pl[i] = f2bf(p - __uint_as_float((uint32_t)pb[i] << 16));
@@ -563,9 +568,12 @@ __device__ __forceinline__ void attend_block(const KVTile<D>& t, int key0, const
                       (uint32_t)pl[4] | ((uint32_t)pl[5] << 16), (uint32_t)pl[6] | ((uint32_t)pl[7] << 16)};
     const bf16x8 pf = __builtin_bit_cast(bf16x8, pv);
     const bf16x8 pg = __builtin_bit_cast(bf16x8, pw);
+    if (__builtin_amdgcn_ballot_w64(alpha != 1.f) != 0) {
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) O[qt][dt] *= alpha;
+    }
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt) {
-      O[qt][dt] *= alpha;
       const bf16x8 vf = __builtin_bit_cast(bf16x8, t.v[dt]);
       O[qt][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf, O[qt][dt], 0, 0, 0);
       O[qt][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pg, O[qt][dt], 0, 0, 0);
@@ -597,17 +605,27 @@ struct AtShape {
 // LDS: sm_o[NW*QPW*16*(D+4)], sm_m/sm_l[NW*QPW*16], is_last.
 // Mem: queries, K/V and the output; PMem: the chunk partials; QL: queries
 // staged in LDS (sm_q, QPW * D/32 * 2 KiB) instead of registers.
-template <int D, int QPW, class Mem = PlainMem, bool PF = true, class PMem = PlainMem, bool QL = false>
+// QS: the waves split the query rows instead of the keys (a query group is
+// NW * QPW * 16 rows, every wave streams every key block of the chunk, so the
+// four waves read the same K/V at about the same time and nothing is merged
+// across waves): for query groups of many rows, whose K/V would otherwise be
+// streamed once per 16-32 rows.
+template <int D, int QPW, class Mem = PlainMem, bool PF = true, class PMem = PlainMem, bool QL = false,
+          bool QS = false>
 __device__ __forceinline__ int attn_unit(const AttnKArgs& a, int item, float* sm_o, float* sm_m, float* sm_l,
                                          int* is_last, uint16_t* sm_q = nullptr) {
-  constexpr int NW = AtShape<QPW>::WAVES, NTH = AtShape<QPW>::THREADS, STEP = AtShape<QPW>::STEP;
+  static_assert(!(QS && QL), "query-split units keep the queries in registers");
+  constexpr int NW = AtShape<QPW>::WAVES, NTH = AtShape<QPW>::THREADS;
+  constexpr int STEP = QS ? AT_KEYS : AtShape<QPW>::STEP;  // keys between a wave's blocks
   constexpr int KD = D / 32;   // 32-wide k steps over the head dimension
   constexpr int DT = D / 16;   // 16-row d tiles of O^T
-  constexpr int ROWS = QPW * 16;
+  constexpr int WROWS = QPW * 16;               // query rows of one wave
+  constexpr int ROWS = QS ? NW * WROWS : WROWS;  // query rows of the workgroup
+  constexpr int NWM = QS ? 1 : NW;               // waves merged per row
   constexpr int RS = D + 4;    // LDS row stride (floats): rows of one wave fall on different banks
   constexpr int NOUT = ROWS * D / 4;                          // float4 outputs of the workgroup
   constexpr int NV = (NOUT + NTH - 1) / NTH;    // per thread
-  static_assert(2 * AT_MAX_CHUNKS * ROWS <= NW * ROWS * RS, "chunk statistics fit the O stage");
+  static_assert(2 * AT_MAX_CHUNKS * ROWS <= NW * WROWS * RS, "chunk statistics fit the O stage");
   // the workgroups of one (sequence, KV head) share an XCD: its query groups
   // read the same K/V
   int grp_id, c, z, qg;
@@ -640,8 +658,9 @@ __device__ __forceinline__ int attn_unit(const AttnKArgs& a, int item, float* sm
 
   const uint16_t* kbase = a.kc + ((size_t)b * a.Hkv + hkv) * a.Lmax * D;
   const uint16_t* vbase = a.vc + ((size_t)b * a.Hkv + hkv) * (size_t)D * a.Lmax;
-  const int first = kbeg + wave * AT_KEYS;
+  const int first = kbeg + (QS ? 0 : wave * AT_KEYS);
   const int nit = first < kend ? (kend - first + STEP - 1) / STEP : 0;
+  const int wrbase = rbase + (QS ? wave * WROWS : 0);  // this wave's first query row
 
   // first K/V block in flight together with the queries.  K/V loads are never
   // conditional (a branch around loads makes the compiler wait for all of them
@@ -657,9 +676,11 @@ __device__ __forceinline__ int attn_unit(const AttnKArgs& a, int item, float* sm
   const uint16_t* qbase = a.q + (size_t)z * a.qrows_pad * D;
 #pragma unroll
   for (int qt = 0; qt < QPW; ++qt) {
-    const int r = rbase + qt * 16 + col;  // padded rows (r >= rows) exist and are masked
+    const int r = wrbase + qt * 16 + col;  // padded rows (r >= rows) exist and are masked
     qpos[qt] = r < a.rows ? fb + r % a.K : -1;
-    const size_t qo = ((size_t)((rbase >> 4) + qt) * KD) * 512 + lane * 8;
+    // tiles past the padded rows (a 128-row query group ends past them) reload the last tile: masked rows
+    const int tq = min((wrbase >> 4) + qt, (a.qrows_pad >> 4) - 1);
+    const size_t qo = ((size_t)tq * KD) * 512 + lane * 8;
 #pragma unroll
     for (int kd = 0; kd < KD; ++kd) {
       if constexpr (QL) {
@@ -707,7 +728,10 @@ __device__ __forceinline__ int attn_unit(const AttnKArgs& a, int item, float* sm
     for (int it = 0; it < nit; ++it) {
       const int key0 = first + it * STEP;
       load_kv<D, Mem>(tb, kbase, vbase, key0 + STEP, a.Lmax, lane);
-      attend_block<D, QPW, QL>(ta, key0, qh, ql, qpos, a.scale_log2, grp, m, l, O, sm_q);
+      if (key0 + AT_KEYS <= fb)
+        attend_block<D, QPW, QL, false>(ta, key0, qh, ql, qpos, a.scale_log2, grp, m, l, O, sm_q);
+      else
+        attend_block<D, QPW, QL>(ta, key0, qh, ql, qpos, a.scale_log2, grp, m, l, O, sm_q);
       ta = tb;
     }
   } else {
@@ -725,12 +749,12 @@ __device__ __forceinline__ int attn_unit(const AttnKArgs& a, int item, float* sm
   for (int qt = 0; qt < QPW; ++qt) {
     l[qt] += __shfl_xor(l[qt], 16);
     l[qt] += __shfl_xor(l[qt], 32);
-    float* row = sm_o + (size_t)(wave * ROWS + qt * 16 + col) * RS;
+    float* row = sm_o + (size_t)(wave * WROWS + qt * 16 + col) * RS;
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt) *(floatx4*)(row + dt * 16 + 4 * grp) = O[qt][dt];
     if (grp == 0) {
-      sm_m[wave * ROWS + qt * 16 + col] = m[qt];
-      sm_l[wave * ROWS + qt * 16 + col] = l[qt];
+      sm_m[wave * WROWS + qt * 16 + col] = m[qt];
+      sm_l[wave * WROWS + qt * 16 + col] = l[qt];
     }
   }
   __syncthreads();
@@ -745,11 +769,11 @@ __device__ __forceinline__ int attn_unit(const AttnKArgs& a, int item, float* sm
     const int r = ic / (D / 4), d4 = ic - r * (D / 4);
     float M = -INFINITY;
 #pragma unroll
-    for (int w = 0; w < NW; ++w) M = fmaxf(M, sm_m[w * ROWS + r]);
+    for (int w = 0; w < NWM; ++w) M = fmaxf(M, sm_m[w * ROWS + r]);
     float L = 0.f;
     floatx4 v = floatx4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int w = 0; w < NW; ++w) {
+    for (int w = 0; w < NWM; ++w) {
       const float mw = sm_m[w * ROWS + r];
       const float ew = (mw == -INFINITY) ? 0.f : exp2f(mw - M);
       L += sm_l[w * ROWS + r] * ew;
