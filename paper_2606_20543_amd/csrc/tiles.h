@@ -507,7 +507,8 @@ template <int D, int QPW, bool QL = false, bool MASK = true>
 __device__ __forceinline__ void attend_block(const KVTile<D>& t, int key0, const bf16x8 (&qh)[QPW][D / 32],
                                              const bf16x8 (&ql)[QPW][D / 32], const int (&qpos)[QPW],
                                              float scale_log2, int grp, float (&m)[QPW], float (&l)[QPW],
-                                             floatx4 (&O)[QPW][D / 16], const uint16_t* qs = nullptr) {
+                                             floatx4 (&O)[QPW][D / 16], const uint16_t* qs = nullptr,
+                                             int klim = 0x7fffffff) {
   constexpr int KD = D / 32, DT = D / 16;
   floatx4 s[2][QPW];
   const uint16_t* qsl = qs + (threadIdx.x & 63) * 8;
@@ -541,7 +542,7 @@ __device__ __forceinline__ void attend_block(const KVTile<D>& t, int key0, const
       for (int e = 0; e < 4; ++e) {
         const int key = key0 + kt * 16 + 4 * grp + e;
         float v = s[kt][qt][e] * scale_log2;
-        if constexpr (MASK) v = (key <= qpos[qt]) ? v : -INFINITY;
+        if constexpr (MASK) v = (key <= qpos[qt] && key < klim) ? v : -INFINITY;
         sv[kt * 4 + e] = v;
         mx = fmaxf(mx, v);
       }
@@ -721,7 +722,29 @@ __device__ __forceinline__ int attn_unit(const AttnKArgs& a, int item, float* sm
     for (int dt = 0; dt < DT; ++dt) O[qt][dt] = floatx4{0.f, 0.f, 0.f, 0.f};
   }
 
-  if constexpr (PF) {
+  if constexpr (PF && QS) {
+    // long streams (query split): two tiles in turn, block it from one while
+    // the next loads into the other, with no copy between them (a tile copy
+    // per block cost about a hundred register moves).  An odd count is padded
+    // with one block past the chunk, masked entirely (keys >= kend), so every
+    // load is unconditional and stays in flight.  Blocks wholly below the
+    // frontier need no mask.  (Short streams keep the copying loop below: the
+    // padding block costs them more than the copies.)
+    auto attend = [&](const KVTile<D>& t, int itx) {
+      const int key0 = first + itx * STEP;
+      if (itx < nit && key0 + AT_KEYS <= fb)
+        attend_block<D, QPW, QL, false>(t, key0, qh, ql, qpos, a.scale_log2, grp, m, l, O, sm_q);
+      else
+        attend_block<D, QPW, QL>(t, key0, qh, ql, qpos, a.scale_log2, grp, m, l, O, sm_q, kend);
+    };
+    for (int it = 0; it < nit; it += 2) {
+      const int key0 = first + it * STEP;
+      load_kv<D, Mem>(tb, kbase, vbase, key0 + STEP, a.Lmax, lane);
+      attend(ta, it);
+      load_kv<D, Mem>(ta, kbase, vbase, key0 + 2 * STEP, a.Lmax, lane);
+      attend(tb, it + 1);
+    }
+  } else if constexpr (PF) {
     // the next block is loaded before the current one is used and taken over
     // at the end of every iteration (an unconditional use: the compiler can
     // neither sink the loads past a loop exit nor drop the overlap)
