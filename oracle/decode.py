@@ -114,7 +114,22 @@ def scoring_logits(sess, logits, b, k):
     return mix(logits[b, k - 1], logits[b + sess.n_img, k - 1], sess.guide)
 
 
-def verify_round(sess, block, n_fixed, rule, rnd, seed=0, temperature=1.0, top_k=0, ref=None):
+def block_tokens(sess, block, eol=None):
+    """Vocabulary ids of a block of image codes at the frontier, and the block
+    offsets holding an end-of-line token (eol = (id, period, base): sequence
+    position p is one when (p - base) % period == period - 1; the codes there
+    are placeholders)."""
+    toks = np.asarray(block, dtype=np.int64) + sess.cfg.img_lo
+    fixed = np.zeros(toks.shape, dtype=bool)
+    if eol is not None:
+        eid, period, base = eol
+        pos = sess.f[:toks.shape[0], None] + np.arange(toks.shape[1])[None, :]
+        fixed = (pos - base) % period == period - 1
+        toks = np.where(fixed, eid, toks)
+    return toks, fixed
+
+
+def verify_round(sess, block, n_fixed, rule, rnd, seed=0, temperature=1.0, top_k=0, ref=None, eol=None):
     """One verify-and-correct round.
 
     block -- (B, K) image-code indices (0-based within the image range), one
@@ -125,16 +140,18 @@ def verify_round(sess, block, n_fixed, rule, rnd, seed=0, temperature=1.0, top_k
     the logits guided under CFG.
     The frontier does not move; the block's KV slots are overwritten.
     """
-    cfg = sess.cfg
     block = np.asarray(block, dtype=np.int64)
     B, K = block.shape
     assert B == sess.n_img
-    logits, _ = M.forward(sess.model, sess.cache, streams(sess, block) + cfg.img_lo, sess.f)
+    toks, fixed = block_tokens(sess, block, eol)
+    logits, _ = M.forward(sess.model, sess.cache, streams(sess, toks), sess.f)
     sess.passes += 1
     new = block.copy()
     acc = np.zeros((B, K), dtype=bool)
     for b in range(B):
         for k in range(n_fixed, K):
+            if fixed[b, k]:  # end-of-line positions are not verified
+                continue
             pos = int(sess.f[b]) + k
             u0 = R.uniform(seed, b, pos, rnd, 0)
             u1 = R.uniform(seed, b, pos, rnd, 1)
@@ -148,15 +165,15 @@ def verify_round(sess, block, n_fixed, rule, rnd, seed=0, temperature=1.0, top_k
     return new, acc, acc[:, n_fixed:].sum(axis=1), guided(sess, logits)
 
 
-def commit(sess, block):
+def commit(sess, block, eol=None):
     """Commit pass: forward the final block, keep its KV, advance the frontier
     by K and take the last position's logits as the new carry (per stream).
     Returns the per-image (guided) logits and the conditional stream's h_pre."""
-    cfg = sess.cfg
     block = np.asarray(block, dtype=np.int64)
     K = block.shape[1]
     assert block.shape[0] == sess.n_img
-    logits, h_pre = M.forward(sess.model, sess.cache, streams(sess, block) + cfg.img_lo, sess.f)
+    toks, _ = block_tokens(sess, block, eol)
+    logits, h_pre = M.forward(sess.model, sess.cache, streams(sess, toks), sess.f)
     sess.passes += 1
     sess.f += K
     sess.carry = logits[:, K - 1, :].copy()
@@ -209,6 +226,31 @@ def ar_decode(model, prefix, n_tokens):
     return out
 
 
+def ar_decode_eol(model, prefix, H, W, eol_id):
+    """Greedy AR decoding of an image whose rows each end with the end-of-line
+    token eol_id (forced, one pass like any other token).  Returns (image
+    codes (B, H, W), passes): the passes are H (W + 1), one per generated token,
+    the prefill producing the first."""
+    prefix = np.asarray(prefix)
+    B, P = prefix.shape
+    s = prefill(model, prefix, P + H * (W + 1))
+    img = np.zeros((B, H, W), dtype=np.int64)
+    n = H * (W + 1)
+    for p in range(n):
+        y, x = divmod(p, W + 1)
+        if x < W:
+            img[:, y, x] = [R.argmax_lowest(s.carry[b]) for b in range(B)]
+            tok = img[:, y, x:x + 1] + model.cfg.img_lo
+        else:
+            tok = np.full((B, 1), eol_id, dtype=np.int64)
+        if p + 1 < n:
+            logits, _ = M.forward(model, s.cache, tok, s.f)
+            s.passes += 1
+            s.f += 1
+            s.carry = logits[:, 0, :].copy()
+    return img, s.passes
+
+
 def decode_truncate(model, prefix, drafts, K):
     """Exact greedy speculative decoding of len(drafts[b]) image tokens per
     sequence with blocks of K positions ([pending, K-1 drafts]); sequences are
@@ -241,7 +283,8 @@ def decode_truncate(model, prefix, drafts, K):
 
 
 def decode_image(model, prefix, H, W, drafts, rule=R.RULE_GREEDY, seed=0, temperature=1.0, top_k=0,
-                 k_h=5, h_rounds=1, k_v=1, b=2, i=0, q_table=None, trace=None, guide=None, heads=None):
+                 k_h=5, h_rounds=1, k_v=1, b=2, i=0, q_table=None, trace=None, guide=None, heads=None,
+                 eol_id=None):
     """Decode one image per sequence under the SSD schedule, with planted drafts
     or drafted by spatial heads (Sec. 3.3).
 
@@ -257,6 +300,8 @@ def decode_image(model, prefix, H, W, drafts, rule=R.RULE_GREEDY, seed=0, temper
                guidance), e its embedding; the drafts are the argmax of the
                backbone's output layer on the predicted states, and under rule C
                their softmax is the draft distribution q of the first round.
+    eol_id  -- optional end-of-line token id: every image row is followed by it
+               in the sequence (fixed, never verified; not with heads)
     q_table -- optional (B, H, W, V_img) draft logits (rule C reference for the
                first round of each position); None = point masses at the drafts
     trace   -- optional list collecting (op, accept, count, logits) per verify
@@ -268,10 +313,21 @@ def decode_image(model, prefix, H, W, drafts, rule=R.RULE_GREEDY, seed=0, temper
     if guide is not None:
         B //= 2
     N = H * W
-    ops = S.plan(H, W, k_h=k_h, h_rounds=h_rounds, k_v=k_v, b=b, i=i)
+    eol = eol_id is not None
+    assert not (eol and heads is not None), "the end-of-line layout is not combined with heads here"
+    RW = W + 1 if eol else W
+    NS = H * RW  # sequence positions of the image
+    ev = (eol_id, RW, P) if eol else None
+    ops = S.plan(H, W, k_h=k_h, h_rounds=h_rounds, k_v=k_v, b=b, i=i, eol=eol)
     sess = None
     if heads is None:
-        work = np.asarray(drafts, dtype=np.int64).reshape(B, N).copy()
+        work = np.zeros((B, H, RW), dtype=np.int64)
+        work[:, :, :W] = np.asarray(drafts, dtype=np.int64).reshape(B, H, W)
+        work = work.reshape(B, NS)
+        if eol and q_table is not None:
+            qs = np.zeros((B, H, RW, q_table.shape[-1]))
+            qs[:, :, :W] = np.asarray(q_table).reshape(B, H, W, -1)
+            q_table = qs.reshape(B, NS, -1)
     else:
         work = np.zeros((B, N), dtype=np.int64)
         hs = np.zeros((B, N, cfg.d_model))  # hs[:, p]: the state that scored image token p
@@ -280,7 +336,7 @@ def decode_image(model, prefix, H, W, drafts, rule=R.RULE_GREEDY, seed=0, temper
     stats = {"accepted": 0, "proposed": 0, "verify_rounds": 0}
     for op in ops:
         if op[0] == "prefill":
-            sess = prefill(model, prefix, P + N, guide)
+            sess = prefill(model, prefix, P + NS, guide)
             if heads is not None:
                 hs[:, 0] = sess.h_carry[:B]
         elif op[0] in ("draft_h", "draft_v"):
@@ -320,25 +376,26 @@ def decode_image(model, prefix, H, W, drafts, rule=R.RULE_GREEDY, seed=0, temper
                         idx = start + k
                         if idx not in refs[bb]:
                             refs[bb][idx] = None if q_table is None else \
-                                np.asarray(q_table[bb].reshape(N, -1)[idx], np.float64)
+                                np.asarray(q_table[bb].reshape(NS, -1)[idx], np.float64)
                         row.append(refs[bb][idx])
                     ref.append(row)
             blk = work[:, start:start + K]
-            new, acc, cnt, logits = verify_round(sess, blk, nf, rule, rnd, seed, temperature, top_k, ref)
+            new, acc, cnt, logits = verify_round(sess, blk, nf, rule, rnd, seed, temperature, top_k, ref, ev)
             if ref is not None:
                 for bb in range(B):
                     for k in range(K):
                         refs[bb][start + k] = ref[bb][k]
             work[:, start:start + K] = new
             stats["accepted"] += int(cnt.sum())
-            stats["proposed"] += B * (K - nf)
+            n_eol = sum(1 for k in range(K) if eol and (start + k) % RW == W)
+            stats["proposed"] += B * (K - nf - n_eol)
             stats["verify_rounds"] += 1
             if trace is not None:
                 trace.append((op, acc, cnt, logits, new))
         elif op[0] == "commit":
             _, start, K = op
             assert int(sess.f[0]) == P + start
-            _, hp = commit(sess, work[:, start:start + K])
+            _, hp = commit(sess, work[:, start:start + K], ev)
             if heads is not None:
                 n_in = min(K, N - start - 1)
                 hs[:, start + 1:start + 1 + n_in] = hp[:, :n_in]
@@ -347,4 +404,4 @@ def decode_image(model, prefix, H, W, drafts, rule=R.RULE_GREEDY, seed=0, temper
                     refs[bb].pop(start + k, None)
     stats["passes"] = sess.passes
     assert sess.passes == S.n_passes(ops)
-    return work.reshape(B, H, W), stats
+    return work.reshape(B, H, RW)[:, :, :W], stats

@@ -21,6 +21,13 @@ Readings:
     with i = 0: the group's rows are committed one after another;
   * the verify round index that feeds the random counter increases over the
     whole image, so no (position, round) pair repeats;
+  * end-of-line layout (the Lumina-mGPT and Emu3 backbones: their AR step
+    counts are H (W + 1), Appendix tables of the configuration sweeps): each
+    image row is followed by one fixed end-of-line token, so row y occupies
+    sequence positions y (W + 1) .. y (W + 1) + W; the end-of-line token rides
+    along with the block that completes its row (the last horizontal run, each
+    row of a vertical group) and is never verified, so the pass count is the
+    same as without it;
   * drafting happens where the paper puts it: before each horizontal run the
     horizontal heads draft the run from the last token already chosen (after
     the prefill: the first token), and at the start of each vertical group the
@@ -33,9 +40,11 @@ configuration sweeps for the three backbones, joint-vs-staged ablation).
 """
 
 
-def plan(H, W, k_h=5, h_rounds=1, k_v=1, b=2, i=0):
+def plan(H, W, k_h=5, h_rounds=1, k_v=1, b=2, i=0, eol=False):
     """List of ops for one image.  Block coordinates are image indices
-    (row-major, 0 = top-left).  Ops:
+    (row-major, 0 = top-left); with eol, verify/commit coordinates are sequence
+    positions after the prompt (row y starts at y (W + 1)) and blocks that end a
+    row include its end-of-line position (draft ops stay in image indices).  Ops:
       ("prefill",)
       ("first",)                                -- pick image token 0 from the carry
       ("verify", start, K, n_fixed, round)      -- one verify-and-correct round
@@ -46,6 +55,8 @@ def plan(H, W, k_h=5, h_rounds=1, k_v=1, b=2, i=0):
     """
     ops = [("prefill",), ("first",)]
     rnd = 0
+    RW = W + 1 if eol else W  # sequence positions per row
+    tail = 1 if eol else 0    # end-of-line position closing a row
 
     def verify(start, K, nf, count):
         nonlocal rnd
@@ -58,28 +69,29 @@ def plan(H, W, k_h=5, h_rounds=1, k_v=1, b=2, i=0):
     first = True
     while s < W:
         e = min(s + k_h, W)
+        t = tail if e == W else 0
         if first:
             ops.append(("draft_h", 0, e - 1))
-            verify(0, e, 1, h_rounds)
-            ops.append(("commit", 0, e))
+            verify(0, e + t, 1, h_rounds)
+            ops.append(("commit", 0, e + t))
             first = False
         else:
             ops.append(("draft_h", s - 1, e - s))
-            verify(s, e - s, 0, h_rounds)
-            ops.append(("commit", s, e - s))
+            verify(s, e - s + t, 0, h_rounds)
+            ops.append(("commit", s, e - s + t))
         s = e
     if W == 1:  # degenerate one-column grid: commit the first token alone
-        ops.append(("commit", 0, 1))
+        ops.append(("commit", 0, 1 + tail))
     # vertical stage, groups of up to k_v rows
     y = 1
     while y < H:
         m = min(k_v, H - y)
         ops.append(("draft_v", y - 1, m))
-        verify(y * W, m * W, 0, b)
-        ops.append(("commit", y * W, W))
+        verify(y * RW, m * RW, 0, b)
+        ops.append(("commit", y * RW, RW))
         for j in range(1, m):
-            verify((y + j) * W, (m - j) * W, 0, i)
-            ops.append(("commit", (y + j) * W, W))
+            verify((y + j) * RW, (m - j) * RW, 0, i)
+            ops.append(("commit", (y + j) * RW, RW))
         y += m
     return ops
 
