@@ -205,6 +205,13 @@ ssd_status ssd_session_set_cfg(ssd_session* sess, float weight);
  * cfg = 1 decodes every image with classifier-free guidance of weight
  * cfg_weight (see ssd_session_set_cfg): the prefix then holds 2B prompts, the
  * B conditional ones followed by their B unconditional twins.
+ * eol = 1 is the end-of-line layout of backbones that close every image row
+ * with one token (their AR step counts are H*(W+1)): row y occupies sequence
+ * positions P + y*(W+1) .. P + y*(W+1) + W, the last holding eol_id.  That
+ * position rides along with the block that completes its row (the last
+ * horizontal run, every row of a vertical group), is never verified or
+ * counted, and its logits score the next row's first token; the pass count is
+ * unchanged.  Not available with heads (ssd_decode_image_heads).
  */
 typedef struct {
   int32_t grid_h, grid_w;
@@ -214,6 +221,8 @@ typedef struct {
   uint64_t seed;
   int32_t cfg;       /* 0: no guidance; 1: classifier-free guidance */
   float cfg_weight;  /* guidance weight w (cfg = 1) */
+  int32_t eol;       /* 0: rows follow each other; 1: every row ends with the token eol_id */
+  int32_t eol_id;    /* end-of-line vocabulary id (eol = 1) */
 } ssd_schedule;
 
 typedef struct {

@@ -417,8 +417,9 @@ __global__ __launch_bounds__(NT_SEL) void select_kernel(SelectArgs a) {
   const int k = blockIdx.x, b = blockIdx.y;
   const int V = a.Vimg;
   const size_t idx = (size_t)b * a.K + k;
-  if (k < a.n_fixed) {
-    if (threadIdx.x == 0) a.accept[idx] = 0;
+  if (k < a.n_fixed ||
+      (a.eol_period > 0 && (a.f[b] + k - a.eol_base) % a.eol_period == a.eol_period - 1)) {
+    if (threadIdx.x == 0) a.accept[idx] = 0;  // fixed: already chosen, or an end-of-line token
     return;
   }
   const float* L = (k == 0) ? a.carry + (size_t)b * V : a.logits + (idx - 1) * V;

@@ -1636,36 +1636,40 @@ struct Op {
 };
 
 // pass plan of one image (mirrors the schedule documented in ssd.h)
-std::vector<Op> make_plan(int H, int W, int k_h, int h_rounds, int k_v, int b, int i) {
+// eol: verify/commit blocks are in sequence positions (row y starts at
+// y * (W + 1)) and a block that completes a row includes its end-of-line slot
+std::vector<Op> make_plan(int H, int W, int k_h, int h_rounds, int k_v, int b, int i, bool eol = false) {
   std::vector<Op> ops;
   int rnd = 0;
+  const int RW = eol ? W + 1 : W, tail = eol ? 1 : 0;
   auto verify = [&](int start, int K, int nf, int count) {
     for (int c = 0; c < count; ++c) ops.push_back(Op{0, start, K, nf, rnd++});
   };
   bool first = true;
   for (int s = 1; s < W;) {
     int e = std::min(s + k_h, W);
+    const int t = e == W ? tail : 0;
     if (first) {
       ops.push_back(Op{2, 0, e - 1, 0, 0});
-      verify(0, e, 1, h_rounds);
-      ops.push_back(Op{1, 0, e, 0, 0});
+      verify(0, e + t, 1, h_rounds);
+      ops.push_back(Op{1, 0, e + t, 0, 0});
       first = false;
     } else {
       ops.push_back(Op{2, s - 1, e - s, 0, 0});
-      verify(s, e - s, 0, h_rounds);
-      ops.push_back(Op{1, s, e - s, 0, 0});
+      verify(s, e - s + t, 0, h_rounds);
+      ops.push_back(Op{1, s, e - s + t, 0, 0});
     }
     s = e;
   }
-  if (W == 1) ops.push_back(Op{1, 0, 1, 0, 0});
+  if (W == 1) ops.push_back(Op{1, 0, 1 + tail, 0, 0});
   for (int y = 1; y < H;) {
     int m = std::min(k_v, H - y);
     ops.push_back(Op{3, y - 1, m, 0, 0});
-    verify(y * W, m * W, 0, b);
-    ops.push_back(Op{1, y * W, W, 0, 0});
+    verify(y * RW, m * RW, 0, b);
+    ops.push_back(Op{1, y * RW, RW, 0, 0});
     for (int j = 1; j < m; ++j) {
-      verify((y + j) * W, (m - j) * W, 0, i);
-      ops.push_back(Op{1, (y + j) * W, W, 0, 0});
+      verify((y + j) * RW, (m - j) * RW, 0, i);
+      ops.push_back(Op{1, (y + j) * RW, RW, 0, 0});
     }
     y += m;
   }
@@ -1705,11 +1709,17 @@ ssd_status decode_impl(ssd_model* m, const ssd_schedule* sc, int32_t B, int32_t 
     return fail(SSD_E_INVAL, "cfg must be 0 or 1 with a finite weight");
   if (sc->cfg && B >= (1 << 19)) return fail(SSD_E_INVAL, "bad batch size");
   const int Bs = sc->cfg ? 2 * B : B;  // sequences: a guided image has two streams
+  if (sc->eol != 0 && sc->eol != 1) return fail(SSD_E_INVAL, "eol must be 0 or 1");
+  const bool eol = sc->eol == 1;
+  if (eol && (sc->eol_id < 0 || sc->eol_id >= dm.V)) return fail(SSD_E_INVAL, "eol_id outside the vocabulary");
+  if (eol && heads) return fail(SSD_E_INVAL, "the end-of-line layout is not available with heads");
   const int N = H * W;
-  const int Lmax = P + N;
+  const int RW = eol ? W + 1 : W;  // sequence positions per image row
+  const int NS = H * RW;           // sequence positions of the image
+  const int Lmax = P + NS;
   if (Lmax >= (1 << 24)) return fail(SSD_E_INVAL, "image too large");
-  if (!dm.bf16 && Lmax > 4096) return fail(SSD_E_INVAL, "fp32 models support P + H*W <= 4096");
-  std::vector<Op> ops = make_plan(H, W, sc->k_h, sc->h_rounds, sc->k_v, sc->b_rounds, sc->i_rounds);
+  if (!dm.bf16 && Lmax > 4096) return fail(SSD_E_INVAL, "fp32 models support P + image positions <= 4096");
+  std::vector<Op> ops = make_plan(H, W, sc->k_h, sc->h_rounds, sc->k_v, sc->b_rounds, sc->i_rounds, eol);
   int Kmax = 1;
   int nverify = 0;
   for (const Op& o : ops) {
@@ -1743,6 +1753,11 @@ ssd_status decode_impl(ssd_model* m, const ssd_schedule* sc, int32_t B, int32_t 
   if (cs != SSD_OK) return cs;
   cs = check_tokens_host(hdr.data(), hdr.size(), dm.img_lo, dm.img_hi, "drafts");
   if (cs != SSD_OK) return cs;
+  if (eol) {  // the working table holds sequence positions: each row closed by its end-of-line token
+    std::vector<int32_t> seq((size_t)B * NS, sc->eol_id);
+    for (size_t r = 0; r < (size_t)B * H; ++r) std::memcpy(&seq[r * RW], &hdr[r * W], (size_t)W * 4);
+    hdr.swap(seq);
+  }
   if (stream) m->stream = (hipStream_t)stream;
   // decode workspace, reused across calls of the same shape
   if (!m->dec || m->dec_B != Bs || m->dec_P != P || m->dec_L != Lmax || m->dec_K != Kmax) {
@@ -1772,14 +1787,14 @@ ssd_status decode_impl(ssd_model* m, const ssd_schedule* sc, int32_t B, int32_t 
   hipStream_t st = s->stream;
   int64_t passes = 0, nv = 0, proposed = 0;
   try {
-    if (s->img_cap < B * N) {
-      s->img = s->mem.get<int>((size_t)B * N);
-      s->img_cap = B * N;
+    if (s->img_cap < B * NS) {
+      s->img = s->mem.get<int>((size_t)B * NS);
+      s->img_cap = B * NS;
     }
     const bool use_q = sc->rule == SSD_ACCEPT_REJECT && (draft_logits || heads);
-    if (use_q && s->qtab_cap < (size_t)B * N * dm.Vimg) {
-      s->qtab = s->mem.get<float>((size_t)B * N * dm.Vimg);
-      s->qtab_cap = (size_t)B * N * dm.Vimg;
+    if (use_q && s->qtab_cap < (size_t)B * NS * dm.Vimg) {
+      s->qtab = s->mem.get<float>((size_t)B * NS * dm.Vimg);
+      s->qtab_cap = (size_t)B * NS * dm.Vimg;
     }
     if (heads && s->hs_cap < (size_t)B * N * dm.d) {
       s->hs = s->mem.get<float>((size_t)B * N * dm.d);
@@ -1788,8 +1803,9 @@ ssd_status decode_impl(ssd_model* m, const ssd_schedule* sc, int32_t B, int32_t 
       s->tsrc = s->mem.get<int>((size_t)B * W);
     }
     HIPCHK(hipMemcpyAsync(s->img, hdr.data(), hdr.size() * 4, hipMemcpyHostToDevice, st));
-    if (draft_logits)
-      HIPCHK(hipMemcpyAsync(s->qtab, draft_logits, (size_t)B * N * dm.Vimg * 4, hipMemcpyDefault, st));
+    if (draft_logits)  // [B][H][W][V] into the sequence layout (end-of-line rows are never read)
+      HIPCHK(hipMemcpy2DAsync(s->qtab, (size_t)RW * dm.Vimg * 4, draft_logits, (size_t)W * dm.Vimg * 4,
+                              (size_t)W * dm.Vimg * 4, (size_t)B * H, hipMemcpyDefault, st));
     fill_u32((unsigned*)s->d_f, Bs, 0u, st);
     fill_u32((unsigned*)s->ref_flag, (size_t)Bs * s->ring, 0u, st);
     fill_u32((unsigned*)s->cnt, Bs, 0u, st);
@@ -1805,7 +1821,7 @@ ssd_status decode_impl(ssd_model* m, const ssd_schedule* sc, int32_t B, int32_t 
     const float* lg = s->cfg ? s->mlog : s->logits;
     const float* cy = s->cfg ? s->mcarry : s->carry;
     if (s->cfg) cfg_mix(B, 0, dm.Vimg, s->cfg_w, nullptr, s->carry, nullptr, s->mcarry, st);
-    first_token(B, dm.Vimg, dm.img_lo, cy, sc->rule, sc->top_k, sc->temperature, sc->seed, s->d_f, s->img, N, st);
+    first_token(B, dm.Vimg, dm.img_lo, cy, sc->rule, sc->top_k, sc->temperature, sc->seed, s->d_f, s->img, NS, st);
     SelectArgs a{};
     a.rule = sc->rule;
     a.top_k = sc->top_k;
@@ -1824,6 +1840,8 @@ ssd_status decode_impl(ssd_model* m, const ssd_schedule* sc, int32_t B, int32_t 
     a.accept = s->acc;
     a.count = s->cnt;
     a.amax = s->amax;
+    a.eol_period = eol ? RW : 0;
+    a.eol_base = P;
     for (const Op& o : ops) {
       if (o.kind >= 2) {
         if (!heads) continue;
@@ -1849,7 +1867,7 @@ ssd_status decode_impl(ssd_model* m, const ssd_schedule* sc, int32_t B, int32_t 
         }
         continue;
       }
-      HIPCHK(hipMemcpy2DAsync(s->tok, (size_t)o.K * 4, s->img + o.start, (size_t)N * 4, (size_t)o.K * 4, B,
+      HIPCHK(hipMemcpy2DAsync(s->tok, (size_t)o.K * 4, s->img + o.start, (size_t)NS * 4, (size_t)o.K * 4, B,
                               hipMemcpyDeviceToDevice, st));
       if (s->cfg)
         HIPCHK(hipMemcpyAsync(s->tok + (size_t)B * o.K, s->tok, (size_t)B * o.K * 4, hipMemcpyDeviceToDevice, st));
@@ -1857,8 +1875,8 @@ ssd_status decode_impl(ssd_model* m, const ssd_schedule* sc, int32_t B, int32_t 
         if (use_q) {
           // first round of a position: its reference is its draft distribution
           // (positions that already hold a reference keep it)
-          set_ref_rows(B, o.K, N, dm.Vimg, s->qtab + (size_t)o.start * dm.Vimg, s->d_f, s->ref, s->ref_flag, s->ring,
-                       1, st);
+          set_ref_rows(B, o.K, NS, dm.Vimg, s->qtab + (size_t)o.start * dm.Vimg, s->d_f, s->ref, s->ref_flag,
+                       s->ring, 1, st);
         }
         run_forward(s, o.K, 0);
         if (s->cfg) cfg_mix(B, o.K, dm.Vimg, s->cfg_w, s->logits, s->carry, s->mlog, s->mcarry, st);
@@ -1866,10 +1884,12 @@ ssd_status decode_impl(ssd_model* m, const ssd_schedule* sc, int32_t B, int32_t 
         a.n_fixed = o.nf;
         a.round = (unsigned)o.rnd;
         select_tokens(a, st);
-        HIPCHK(hipMemcpy2DAsync(s->img + o.start, (size_t)N * 4, s->tok, (size_t)o.K * 4, (size_t)o.K * 4, B,
+        HIPCHK(hipMemcpy2DAsync(s->img + o.start, (size_t)NS * 4, s->tok, (size_t)o.K * 4, (size_t)o.K * 4, B,
                                 hipMemcpyDeviceToDevice, st));
         ++nv;
-        proposed += (int64_t)B * (o.K - o.nf);
+        int n_eol = 0;  // end-of-line slots are not verified
+        for (int k = 0; eol && k < o.K; ++k) n_eol += (o.start + k) % RW == W;
+        proposed += (int64_t)B * (o.K - o.nf - n_eol);
       } else {
         run_forward(s, o.K, 1);
         commit_update(Bs, -o.K, dm.Vimg, s->logits, s->carry, s->d_f, s->ref_flag, s->ring, st);
@@ -1883,7 +1903,9 @@ ssd_status decode_impl(ssd_model* m, const ssd_schedule* sc, int32_t B, int32_t 
       ++passes;
     }
     HIPCHK(hipGetLastError());
-    HIPCHK(hipMemcpyAsync(out_tokens, s->img, (size_t)B * N * 4, hipMemcpyDefault, st));
+    // image positions only (rows of W out of rows of RW)
+    HIPCHK(hipMemcpy2DAsync(out_tokens, (size_t)W * 4, s->img, (size_t)RW * 4, (size_t)W * 4, (size_t)B * H,
+                            hipMemcpyDefault, st));
     std::vector<int> hc(B);
     HIPCHK(hipMemcpyAsync(hc.data(), s->cnt, (size_t)B * 4, hipMemcpyDeviceToHost, st));
     fwd_abort_fetch(s);

@@ -305,6 +305,8 @@ struct SelectArgs {
   unsigned char* accept;   // [B][K]
   int* count;              // [B]
   int* amax;               // [B][K] greedy argmax (truncate mode)
+  int eol_period = 0;      // > 0: sequence position p is a fixed end-of-line token
+  int eol_base = 0;        //   when (p - eol_base) % eol_period == eol_period - 1
 };
 void select_tokens(const SelectArgs& a, hipStream_t st);
 // truncate mode: leading accepted run, f update, pending token
