@@ -301,7 +301,8 @@ def decode_image(model, prefix, H, W, drafts, rule=R.RULE_GREEDY, seed=0, temper
                backbone's output layer on the predicted states, and under rule C
                their softmax is the draft distribution q of the first round.
     eol_id  -- optional end-of-line token id: every image row is followed by it
-               in the sequence (fixed, never verified; not with heads)
+               in the sequence (fixed, never verified); with heads, the row end's
+               state scores the next row's first token
     q_table -- optional (B, H, W, V_img) draft logits (rule C reference for the
                first round of each position); None = point masses at the drafts
     trace   -- optional list collecting (op, accept, count, logits) per verify
@@ -314,7 +315,6 @@ def decode_image(model, prefix, H, W, drafts, rule=R.RULE_GREEDY, seed=0, temper
         B //= 2
     N = H * W
     eol = eol_id is not None
-    assert not (eol and heads is not None), "the end-of-line layout is not combined with heads here"
     RW = W + 1 if eol else W
     NS = H * RW  # sequence positions of the image
     ev = (eol_id, RW, P) if eol else None
@@ -329,9 +329,12 @@ def decode_image(model, prefix, H, W, drafts, rule=R.RULE_GREEDY, seed=0, temper
             qs[:, :, :W] = np.asarray(q_table).reshape(B, H, W, -1)
             q_table = qs.reshape(B, NS, -1)
     else:
-        work = np.zeros((B, N), dtype=np.int64)
+        work = np.zeros((B, NS), dtype=np.int64)
         hs = np.zeros((B, N, cfg.d_model))  # hs[:, p]: the state that scored image token p
-        q_table = np.zeros((B, N, cfg.img_hi - cfg.img_lo)) if rule == R.RULE_ACCEPT_REJECT else None
+        q_table = np.zeros((B, NS, cfg.img_hi - cfg.img_lo)) if rule == R.RULE_ACCEPT_REJECT else None
+
+    def seq_of(p):  # sequence position (after the prompt) of image index p
+        return (np.asarray(p) // W) * RW + np.asarray(p) % W
     refs = [dict() for _ in range(B)]  # image index -> reference logits
     stats = {"accepted": 0, "proposed": 0, "verify_rounds": 0}
     for op in ops:
@@ -354,12 +357,13 @@ def decode_image(model, prefix, H, W, drafts, rule=R.RULE_GREEDY, seed=0, temper
                 lst = heads[1]
             for j, d_idx in enumerate(dst):
                 idx, lg = Dr.draft(model, lst[j], hs[:, srcs].reshape(-1, cfg.d_model),
-                                   (work[:, srcs] + cfg.img_lo).reshape(-1))
-                work[:, d_idx] = idx.reshape(B, -1) if np.ndim(d_idx) else idx
+                                   (work[:, seq_of(srcs)] + cfg.img_lo).reshape(-1))
+                dq = seq_of(d_idx)
+                work[:, dq] = idx.reshape(B, -1) if np.ndim(d_idx) else idx
                 if q_table is not None:
-                    q_table[:, d_idx] = lg.reshape(B, -1, lg.shape[-1]) if np.ndim(d_idx) else lg
+                    q_table[:, dq] = lg.reshape(B, -1, lg.shape[-1]) if np.ndim(d_idx) else lg
                 if trace is not None:
-                    trace.append((op, j + 1, srcs.copy(), np.atleast_1d(d_idx).copy(), work[:, d_idx].copy()))
+                    trace.append((op, j + 1, srcs.copy(), np.atleast_1d(d_idx).copy(), work[:, dq].copy()))
         elif op[0] == "first":
             for bb in range(B):
                 u1 = R.uniform(seed, bb, P, 0, 2)
@@ -397,8 +401,12 @@ def decode_image(model, prefix, H, W, drafts, rule=R.RULE_GREEDY, seed=0, temper
             assert int(sess.f[0]) == P + start
             _, hp = commit(sess, work[:, start:start + K], ev)
             if heads is not None:
-                n_in = min(K, N - start - 1)
-                hs[:, start + 1:start + 1 + n_in] = hp[:, :n_in]
+                # the state of block offset k scores sequence position start + k + 1:
+                # kept when that is an image position (a row end's state scores the next row)
+                for k in range(K):
+                    q1 = start + k + 1
+                    if q1 < NS and q1 % RW != W:
+                        hs[:, (q1 // RW) * W + q1 % RW] = hp[:, k]
             for bb in range(B):
                 for k in range(K):
                     refs[bb].pop(start + k, None)

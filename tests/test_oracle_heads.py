@@ -74,13 +74,14 @@ def _perm(kind, j):
     return np.eye(D)[p]
 
 
-def test_embedding_heads_draft_from_their_source_tokens():
+@pytest.mark.parametrize("eol", [None, 5])
+def test_embedding_heads_draft_from_their_source_tokens(eol):
     model = _model()
     hh = _heads(3, 2, lambda kind, j: _head(w0=np.concatenate([np.zeros((D, D)), _perm(kind, j)], axis=1),
                                             w2=np.zeros((D, MI)), seed=j))
     trace = []
     img, _ = Dc.decode_image(model, _prefix(2), H, W, None, rule=R.RULE_GREEDY, k_h=3, k_v=2, b=1, i=1,
-                             heads=hh, trace=trace)
+                             heads=hh, trace=trace, eol_id=eol)
     flat = img.reshape(2, -1)
     lm = model.lm_img
     n_ops = {"draft_h": 0, "draft_v": 0}
@@ -98,21 +99,27 @@ def test_embedding_heads_draft_from_their_source_tokens():
     assert n_ops["draft_v"] == sum(o[2] for o in ops if o[0] == "draft_v")
 
 
-def test_state_heads_draft_the_argmax_that_scored_the_source():
+@pytest.mark.parametrize("eol", [None, 5])
+def test_state_heads_draft_the_argmax_that_scored_the_source(eol):
     model = _model()
     eye = np.concatenate([np.eye(D), np.zeros((D, D))], axis=1)
     hh = _heads(2, 1, lambda kind, j: _head(w0=eye, w2=np.zeros((D, MI)), seed=j))
     trace = []
     pre = _prefix(2)
     img, _ = Dc.decode_image(model, pre, H, W, None, rule=R.RULE_SAMPLE, seed=9, k_h=2, k_v=1, b=2,
-                             heads=hh, trace=trace)
-    flat = img.reshape(2, -1)
-    # full forward over the final sequence without a cache: the state at raster
-    # position P + p - 1 scored image token p
-    seq = np.concatenate([pre, flat + SHAPE.img_lo], axis=1)
+                             heads=hh, trace=trace, eol_id=eol)
+    # full forward over the final sequence without a cache (rows closed by the
+    # end-of-line token when there is one): the state at the sequence position
+    # before image token p scored it
+    rows = img + SHAPE.img_lo
+    if eol is not None:
+        rows = np.concatenate([rows, np.full((2, H, 1), eol)], axis=2)
+    seq = np.concatenate([pre, rows.reshape(2, -1)], axis=1)
     logits, _ = M.forward(model, M.Cache(model.cfg, 2, seq.shape[1]), seq, np.zeros(2, np.int64))
+    RW = W + (eol is not None)
     for op, j, srcs, dsts, drafted in _drafts(trace):
-        want = logits[:, P + srcs - 1].argmax(axis=-1)
+        spos = (srcs // W) * RW + srcs % W
+        want = logits[:, P + spos - 1].argmax(axis=-1)
         assert np.array_equal(drafted.reshape(want.shape), want)
 
 
