@@ -211,7 +211,8 @@ ssd_status ssd_session_set_cfg(ssd_session* sess, float weight);
  * position rides along with the block that completes its row (the last
  * horizontal run, every row of a vertical group), is never verified or
  * counted, and its logits score the next row's first token; the pass count is
- * unchanged.  Not available with heads (ssd_decode_image_heads).
+ * unchanged.  With heads (ssd_decode_image_heads) a row end's state is the
+ * one that scored the next row's first token.
  */
 typedef struct {
   int32_t grid_h, grid_w;

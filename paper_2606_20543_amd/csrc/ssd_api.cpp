@@ -1712,7 +1712,6 @@ ssd_status decode_impl(ssd_model* m, const ssd_schedule* sc, int32_t B, int32_t 
   if (sc->eol != 0 && sc->eol != 1) return fail(SSD_E_INVAL, "eol must be 0 or 1");
   const bool eol = sc->eol == 1;
   if (eol && (sc->eol_id < 0 || sc->eol_id >= dm.V)) return fail(SSD_E_INVAL, "eol_id outside the vocabulary");
-  if (eol && heads) return fail(SSD_E_INVAL, "the end-of-line layout is not available with heads");
   const int N = H * W;
   const int RW = eol ? W + 1 : W;  // sequence positions per image row
   const int NS = H * RW;           // sequence positions of the image
@@ -1846,22 +1845,24 @@ ssd_status decode_impl(ssd_model* m, const ssd_schedule* sc, int32_t B, int32_t 
       if (o.kind >= 2) {
         if (!heads) continue;
         // heads draft from chosen tokens: [h; e] with h the state that scored each
+        // (image indices for the states, sequence positions for the tokens)
         const bool hor = o.kind == 2;
         const int n_src = hor ? 1 : W;                 // source positions per image
-        const int p0 = hor ? o.start : o.start * W;    // first source position
+        const int p0 = hor ? o.start : o.start * W;    // first source image index
         const int step = hor ? 1 : W;                  // offset of head j is j * step
+        auto seq_of = [&](int p) { return (p / W) * RW + p % W; };
         HIPCHK(hipMemcpy2DAsync(s->hsrc, n_src * rowb, s->hs + (size_t)p0 * dm.d, (size_t)N * rowb, n_src * rowb, B,
                                 hipMemcpyDeviceToDevice, st));
-        HIPCHK(hipMemcpy2DAsync(s->tsrc, (size_t)n_src * 4, s->img + p0, (size_t)N * 4, (size_t)n_src * 4, B,
+        HIPCHK(hipMemcpy2DAsync(s->tsrc, (size_t)n_src * 4, s->img + seq_of(p0), (size_t)NS * 4, (size_t)n_src * 4, B,
                                 hipMemcpyDeviceToDevice, st));
         for (int j = 1; j <= o.K; ++j) {
           ssd_draft_head* h = (hor ? src.hh : src.vh)[j - 1];
           head_forward(h, B * n_src, s->hsrc, s->tsrc, st);
-          const int dst = p0 + j * step;
-          HIPCHK(hipMemcpy2DAsync(s->img + dst, (size_t)N * 4, h->out, (size_t)n_src * 4, (size_t)n_src * 4, B,
+          const int dq = seq_of(p0 + j * step);  // a run or a row: contiguous in the sequence
+          HIPCHK(hipMemcpy2DAsync(s->img + dq, (size_t)NS * 4, h->out, (size_t)n_src * 4, (size_t)n_src * 4, B,
                                   hipMemcpyDeviceToDevice, st));
           if (use_q)
-            HIPCHK(hipMemcpy2DAsync(s->qtab + (size_t)dst * dm.Vimg, (size_t)N * dm.Vimg * 4, h->logits,
+            HIPCHK(hipMemcpy2DAsync(s->qtab + (size_t)dq * dm.Vimg, (size_t)NS * dm.Vimg * 4, h->logits,
                                     (size_t)n_src * dm.Vimg * 4, (size_t)n_src * dm.Vimg * 4, B,
                                     hipMemcpyDeviceToDevice, st));
         }
@@ -1894,11 +1895,22 @@ ssd_status decode_impl(ssd_model* m, const ssd_schedule* sc, int32_t B, int32_t 
         run_forward(s, o.K, 1);
         commit_update(Bs, -o.K, dm.Vimg, s->logits, s->carry, s->d_f, s->ref_flag, s->ring, st);
         for (int b = 0; b < Bs; ++b) s->f[b] += o.K;
-        // the committed block's states score image tokens start+1 .. start+K
-        const int n_in = std::min(o.K, N - o.start - 1);
-        if (heads && n_in > 0)
-          HIPCHK(hipMemcpy2DAsync(s->hs + (size_t)(o.start + 1) * dm.d, (size_t)N * rowb, s->x, (size_t)o.K * rowb,
-                                  (size_t)n_in * rowb, B, hipMemcpyDeviceToDevice, st));
+        // the state of block offset k scores sequence position start + k + 1: kept
+        // under its image index when that is an image position (a row end's state
+        // scores the next row's first token), one copy per run of such offsets
+        for (int k = 0; heads && k < o.K;) {
+          int q1 = o.start + k + 1;
+          if (q1 >= NS || q1 % RW == W) {
+            ++k;
+            continue;
+          }
+          int len = 1;
+          while (k + len < o.K && q1 + len < NS && (q1 + len) % RW != W) ++len;
+          const int p1 = (q1 / RW) * W + q1 % RW;
+          HIPCHK(hipMemcpy2DAsync(s->hs + (size_t)p1 * dm.d, (size_t)N * rowb, s->x + (size_t)k * dm.d,
+                                  (size_t)o.K * rowb, (size_t)len * rowb, B, hipMemcpyDeviceToDevice, st));
+          k += len;
+        }
       }
       ++passes;
     }

@@ -116,6 +116,24 @@ def test_guided_heads_decode_matches_oracle(tiny):
     assert st.accepted == ost["accepted"]
 
 
+def test_heads_decode_with_row_ends_matches_oracle(tiny):
+    """The end-of-line layout under head drafting: a row end's state scores the
+    next row's first token, drafts land at sequence positions."""
+    pair, hs = tiny
+    B = 2
+    pre = synth.prompt(TINY, B, P)
+    out = np.zeros((B, H, W), np.int32)
+    sc = _sched(R.RULE_ACCEPT_REJECT, 100, k_v=2, b=2, i=1)
+    sc.eol, sc.eol_id = 1, 3
+    gh, gv = hs.lists("gpu")
+    st = ssd.ssd_decode_image_heads(pair.model, sc, B, P, pre, gh, gv, out)
+    oh, ov = hs.lists("oracle")
+    otok, ost = Dc.decode_image(pair.om, pre, H, W, None, rule=R.RULE_ACCEPT_REJECT, seed=3, top_k=100, k_v=2, b=2,
+                                i=1, heads=(oh, ov), eol_id=3)
+    assert np.array_equal(out - TINY.img_lo, otok)
+    assert st.passes == ost["passes"] and st.accepted == ost["accepted"] and st.proposed == ost["proposed"]
+
+
 def test_heads_argument_errors(tiny):
     pair, hs = tiny
     pre = synth.prompt(TINY, 1, P)
