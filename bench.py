@@ -294,7 +294,10 @@ def draft_head_cost(ssd, model, shape, tokens, calls=50):
 
 
 def cpu_baseline(wl, w, prefix, drafts):
-    """The oracle (numpy float64) on the host cores, on prefix + the first two rows."""
+    """The oracle (numpy float64) on the host cores: the whole image of the
+    workload (up to 24 rows), then one verify pass of a drafted row at rows 1,
+    H/4, H/2 and H-1 (the rows before each committed first), as the GPU's
+    per-position timing does."""
     from oracle import decode as Dc
     from oracle import model as M
     shape = wl.model
@@ -311,9 +314,24 @@ def cpu_baseline(wl, w, prefix, drafts):
     except Exception:
         cores = os.cpu_count()
     n_tok = prefix.shape[0] * rows * wl.grid
+    H = W = wl.grid
+    pos_rows = sorted({1, H // 4, H // 2, H - 1})
+    pos_ms = []
+    if rows == H:
+        sess = Dc.prefill(om, prefix, prefix.shape[1] + H * W)
+        y = 0
+        for r in pos_rows:
+            while y < r:
+                Dc.commit(sess, tok[:, y, :])
+                y += 1
+            t1 = time.perf_counter()
+            Dc.verify_round(sess, drafts[:, r, :], 0, wl.rule, 0, 3, 1.0, wl.top_k)
+            pos_ms.append((time.perf_counter() - t1) * 1e3)
     return {"value": n_tok / dt, "unit": "image tokens/s", "cores": int(cores), "kind": "oracle",
             "sample": f"prefill + rows 0-{rows - 1} of the {wl.grid}x{wl.grid} image ({st['passes']} passes, "
-                      f"batch {prefix.shape[0]}, {n_tok} tokens) in {dt:.1f} s"}
+                      f"batch {prefix.shape[0]}, {n_tok} tokens) in {dt:.1f} s",
+            "verify_pass_positions": {"rows": pos_rows if pos_ms else [], "ms": pos_ms,
+                                      "note": "one verify pass of a drafted row at each position, host clock"}}
 
 
 def main():
@@ -495,6 +513,10 @@ def main():
     if not args.no_cpu_baseline:
         log("[bench] timing the oracle on the host cores")
         result["cpu_baseline"] = cpu_baseline(wl, w, prefix, drafts)
+        vp = result.get("verify_pass_positions")
+        cp = result["cpu_baseline"]["verify_pass_positions"]
+        if vp and cp["ms"] and cp["rows"] == vp["rows"]:
+            cp["gpu_speedup"] = [c / g for c, g in zip(cp["ms"], vp["ms_median"])]
     print(json.dumps(result), flush=True)
 
 
