@@ -213,6 +213,13 @@ ssd_status ssd_session_set_cfg(ssd_session* sess, float weight);
  * counted, and its logits score the next row's first token; the pass count is
  * unchanged.  With heads (ssd_decode_image_heads) a row end's state is the
  * one that scored the next row's first token.
+ * A commit pass followed by a verify round of the block right after it (no
+ * head drafting in between) runs, unless separate_commit = 1, as one pass
+ * over both blocks: the committed tokens are fixed positions whose KV becomes
+ * final, the carry is the logits of the last committed position, and the
+ * verify block is scored and corrected in the same pass (the causal mask lets
+ * it see the committed block).  Decisions are those of the separate passes;
+ * ssd_stats.passes counts the backbone passes actually run.
  */
 typedef struct {
   int32_t grid_h, grid_w;
@@ -224,6 +231,8 @@ typedef struct {
   float cfg_weight;  /* guidance weight w (cfg = 1) */
   int32_t eol;       /* 0: rows follow each other; 1: every row ends with the token eol_id */
   int32_t eol_id;    /* end-of-line vocabulary id (eol = 1) */
+  int32_t separate_commit; /* 0: a commit pass and the verify round right after it run as one pass;
+                              1: one backbone pass per plan step */
 } ssd_schedule;
 
 typedef struct {

@@ -49,7 +49,8 @@ class ssd_schedule(ctypes.Structure):
                 ("h_rounds", ctypes.c_int32), ("k_v", ctypes.c_int32), ("b_rounds", ctypes.c_int32),
                 ("i_rounds", ctypes.c_int32), ("rule", ctypes.c_int32), ("top_k", ctypes.c_int32),
                 ("temperature", ctypes.c_double), ("seed", ctypes.c_uint64), ("cfg", ctypes.c_int32),
-                ("cfg_weight", ctypes.c_float), ("eol", ctypes.c_int32), ("eol_id", ctypes.c_int32)]
+                ("cfg_weight", ctypes.c_float), ("eol", ctypes.c_int32), ("eol_id", ctypes.c_int32),
+                ("separate_commit", ctypes.c_int32)]
 
 
 class ssd_stats(ctypes.Structure):

@@ -535,6 +535,11 @@ void commit_update(int B, int K, int Vimg, const float* logits, float* carry, in
   hipLaunchKernelGGL(commit_kernel, dim3(B), dim3(256), 0, st, Vimg, logits, rps, last, carry, f, inc, ref_flag, ring);
 }
 
+void commit_prefix(int B, int rps, int Kc, int Vimg, const float* logits, float* carry, int* f, int* ref_flag,
+                   int ring, hipStream_t st) {
+  hipLaunchKernelGGL(commit_kernel, dim3(B), dim3(256), 0, st, Vimg, logits, rps, Kc - 1, carry, f, Kc, ref_flag, ring);
+}
+
 // Classifier-free guidance: guided logits l_u + w (l_c - l_u) of each image b
 // (conditional stream b, unconditional stream Bi + b).  Workgroup (r, b): rows
 // r < K of the pass's logits [2*Bi*K][V] (row = stream * K + r), r = K the

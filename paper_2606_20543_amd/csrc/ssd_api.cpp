@@ -1719,11 +1719,24 @@ ssd_status decode_impl(ssd_model* m, const ssd_schedule* sc, int32_t B, int32_t 
   if (Lmax >= (1 << 24)) return fail(SSD_E_INVAL, "image too large");
   if (!dm.bf16 && Lmax > 4096) return fail(SSD_E_INVAL, "fp32 models support P + image positions <= 4096");
   std::vector<Op> ops = make_plan(H, W, sc->k_h, sc->h_rounds, sc->k_v, sc->b_rounds, sc->i_rounds, eol);
+  if (sc->separate_commit != 0 && sc->separate_commit != 1) return fail(SSD_E_INVAL, "separate_commit must be 0 or 1");
+  // fuse[i]: commit op i runs inside the pass of the verify round right after it
+  // (adjacent block, nothing fixed at its start, no head drafting in between:
+  // drafting needs the committed states first)
+  std::vector<char> fuse(ops.size(), 0);
   int Kmax = 1;
   int nverify = 0;
-  for (const Op& o : ops) {
+  for (size_t i = 0; i < ops.size(); ++i) {
+    const Op& o = ops[i];
     if (o.kind <= 1) Kmax = std::max(Kmax, o.K);
     nverify += o.kind == 0;
+    if (o.kind != 1 || sc->separate_commit) continue;
+    size_t j = i + 1;
+    while (j < ops.size() && ops[j].kind >= 2 && !heads) ++j;
+    if (j < ops.size() && ops[j].kind == 0 && ops[j].nf == 0 && ops[j].start == o.start + o.K) {
+      fuse[i] = 1;
+      Kmax = std::max(Kmax, o.K + ops[j].K);
+    }
   }
   if (heads) {
     // every head the plan calls must exist, belong to this model and hold its rows
@@ -1841,7 +1854,28 @@ ssd_status decode_impl(ssd_model* m, const ssd_schedule* sc, int32_t B, int32_t 
     a.amax = s->amax;
     a.eol_period = eol ? RW : 0;
     a.eol_base = P;
-    for (const Op& o : ops) {
+    // the state of block offset k (pass rows of `rps` per sequence) scores sequence
+    // position start + k + 1: kept under its image index when that is an image
+    // position (a row end's state scores the next row's first token), one copy per
+    // run of such offsets
+    auto keep_states = [&](int start, int Kc, int rps) {
+      for (int k = 0; heads && k < Kc;) {
+        int q1 = start + k + 1;
+        if (q1 >= NS || q1 % RW == W) {
+          ++k;
+          continue;
+        }
+        int len = 1;
+        while (k + len < Kc && q1 + len < NS && (q1 + len) % RW != W) ++len;
+        const int p1 = (q1 / RW) * W + q1 % RW;
+        HIPCHK(hipMemcpy2DAsync(s->hs + (size_t)p1 * dm.d, (size_t)N * rowb, s->x + (size_t)k * dm.d,
+                                (size_t)rps * rowb, (size_t)len * rowb, B, hipMemcpyDeviceToDevice, st));
+        k += len;
+      }
+    };
+    const Op* pending = nullptr;  // a commit waiting for the verify round it runs with
+    for (size_t i = 0; i < ops.size(); ++i) {
+      const Op& o = ops[i];
       if (o.kind >= 2) {
         if (!heads) continue;
         // heads draft from chosen tokens: [h; e] with h the state that scored each
@@ -1868,49 +1902,48 @@ ssd_status decode_impl(ssd_model* m, const ssd_schedule* sc, int32_t B, int32_t 
         }
         continue;
       }
-      HIPCHK(hipMemcpy2DAsync(s->tok, (size_t)o.K * 4, s->img + o.start, (size_t)NS * 4, (size_t)o.K * 4, B,
+      if (o.kind == 1 && fuse[i]) {
+        pending = &o;  // runs as the fixed prefix of the next verify pass
+        continue;
+      }
+      // the pass's block: this op's, behind the pending commit's when there is one
+      const int Kc = (o.kind == 0 && pending) ? pending->K : 0;
+      const int start = o.start - Kc, K = o.K + Kc;
+      HIPCHK(hipMemcpy2DAsync(s->tok, (size_t)K * 4, s->img + start, (size_t)NS * 4, (size_t)K * 4, B,
                               hipMemcpyDeviceToDevice, st));
       if (s->cfg)
-        HIPCHK(hipMemcpyAsync(s->tok + (size_t)B * o.K, s->tok, (size_t)B * o.K * 4, hipMemcpyDeviceToDevice, st));
+        HIPCHK(hipMemcpyAsync(s->tok + (size_t)B * K, s->tok, (size_t)B * K * 4, hipMemcpyDeviceToDevice, st));
       if (o.kind == 0) {
         if (use_q) {
           // first round of a position: its reference is its draft distribution
-          // (positions that already hold a reference keep it)
-          set_ref_rows(B, o.K, NS, dm.Vimg, s->qtab + (size_t)o.start * dm.Vimg, s->d_f, s->ref, s->ref_flag,
-                       s->ring, 1, st);
+          // (positions that already hold a reference keep it; a committed prefix's
+          // are dropped by its commit below)
+          set_ref_rows(B, K, NS, dm.Vimg, s->qtab + (size_t)start * dm.Vimg, s->d_f, s->ref, s->ref_flag, s->ring,
+                       1, st);
         }
-        run_forward(s, o.K, 0);
-        if (s->cfg) cfg_mix(B, o.K, dm.Vimg, s->cfg_w, s->logits, s->carry, s->mlog, s->mcarry, st);
-        a.K = o.K;
-        a.n_fixed = o.nf;
+        run_forward(s, K, 0);
+        if (s->cfg) cfg_mix(B, K, dm.Vimg, s->cfg_w, s->logits, s->carry, s->mlog, s->mcarry, st);
+        a.K = K;
+        a.n_fixed = Kc + o.nf;  // the committed prefix is fixed
         a.round = (unsigned)o.rnd;
         select_tokens(a, st);
-        HIPCHK(hipMemcpy2DAsync(s->img + o.start, (size_t)NS * 4, s->tok, (size_t)o.K * 4, (size_t)o.K * 4, B,
+        HIPCHK(hipMemcpy2DAsync(s->img + start, (size_t)NS * 4, s->tok, (size_t)K * 4, (size_t)K * 4, B,
                                 hipMemcpyDeviceToDevice, st));
         ++nv;
         int n_eol = 0;  // end-of-line slots are not verified
         for (int k = 0; eol && k < o.K; ++k) n_eol += (o.start + k) % RW == W;
         proposed += (int64_t)B * (o.K - o.nf - n_eol);
+        if (Kc > 0) {  // the prefix's KV is final: commit it
+          commit_prefix(Bs, K, Kc, dm.Vimg, s->logits, s->carry, s->d_f, s->ref_flag, s->ring, st);
+          for (int b = 0; b < Bs; ++b) s->f[b] += Kc;
+          keep_states(start, Kc, K);
+          pending = nullptr;
+        }
       } else {
         run_forward(s, o.K, 1);
         commit_update(Bs, -o.K, dm.Vimg, s->logits, s->carry, s->d_f, s->ref_flag, s->ring, st);
         for (int b = 0; b < Bs; ++b) s->f[b] += o.K;
-        // the state of block offset k scores sequence position start + k + 1: kept
-        // under its image index when that is an image position (a row end's state
-        // scores the next row's first token), one copy per run of such offsets
-        for (int k = 0; heads && k < o.K;) {
-          int q1 = o.start + k + 1;
-          if (q1 >= NS || q1 % RW == W) {
-            ++k;
-            continue;
-          }
-          int len = 1;
-          while (k + len < o.K && q1 + len < NS && (q1 + len) % RW != W) ++len;
-          const int p1 = (q1 / RW) * W + q1 % RW;
-          HIPCHK(hipMemcpy2DAsync(s->hs + (size_t)p1 * dm.d, (size_t)N * rowb, s->x + (size_t)k * dm.d,
-                                  (size_t)o.K * rowb, (size_t)len * rowb, B, hipMemcpyDeviceToDevice, st));
-          k += len;
-        }
+        keep_states(o.start, o.K, o.K);
       }
       ++passes;
     }

@@ -314,6 +314,11 @@ void truncate_finalize(const SelectArgs& a, int* f, hipStream_t st);
 // commit bookkeeping: carry <- logits[b*K + K-1]; f += K; clear ring flags of committed positions
 void commit_update(int B, int K, int Vimg, const float* logits, float* carry, int* f, int* ref_flag, int ring,
                    hipStream_t st);
+// commit of the first Kc rows of a pass of rps rows per sequence (the rest a
+// verify block): carry <- logits row Kc-1, f += Kc, ring flags of the committed
+// positions cleared
+void commit_prefix(int B, int rps, int Kc, int Vimg, const float* logits, float* carry, int* f, int* ref_flag,
+                   int ring, hipStream_t st);
 // fill helpers (graph-capture safe)
 void fill_u32(unsigned* p, size_t n, unsigned v, hipStream_t st);
 // out[w] = XCD index workgroup w ran on

@@ -17,9 +17,29 @@ import paper_2606_20543_amd as ssd
 import synth
 from oracle import decode as Dc
 from oracle import model as M
+from oracle import schedule as S
 from oracle import select as R
 
 TOL = {"f32": 1e-5, "bf16": 2e-2}
+
+
+def executed_passes(ops, heads=False, separate=False):
+    """Backbone passes the library runs for a plan: a commit followed by a verify
+    round of the adjacent block (no head drafting in between, no fixed first
+    position) shares that round's pass unless commits are kept separate."""
+    n = S.n_passes(ops)
+    if separate:
+        return n
+    fused = 0
+    for i, o in enumerate(ops):
+        if o[0] != "commit":
+            continue
+        j = i + 1
+        while j < len(ops) and ops[j][0] in ("draft_h", "draft_v") and not heads:
+            j += 1
+        if j < len(ops) and ops[j][0] == "verify" and ops[j][3] == 0 and ops[j][1] == o[1] + o[2]:
+            fused += 1
+    return n - fused
 
 
 def tol_of(shape, os_):

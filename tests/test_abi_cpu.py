@@ -49,7 +49,8 @@ int main(void) {{
          offsetof(ssd_verify_params, round), offsetof(ssd_schedule, temperature));
   printf("%zu %zu %zu %zu\\n", offsetof(ssd_schedule, seed), offsetof(ssd_model_config, rope_theta),
          offsetof(ssd_schedule, cfg), offsetof(ssd_schedule, cfg_weight));
-  printf("%zu %zu\\n", offsetof(ssd_schedule, eol), offsetof(ssd_schedule, eol_id));
+  printf("%zu %zu %zu\\n", offsetof(ssd_schedule, eol), offsetof(ssd_schedule, eol_id),
+         offsetof(ssd_schedule, separate_commit));
   return 0;
 }}
 """)
@@ -63,7 +64,8 @@ int main(void) {{
             ssd.ssd_verify_params.round.offset, ssd.ssd_schedule.temperature.offset,
             ssd.ssd_schedule.seed.offset, ssd.ssd_model_config.rope_theta.offset,
             ssd.ssd_schedule.cfg.offset, ssd.ssd_schedule.cfg_weight.offset,
-            ssd.ssd_schedule.eol.offset, ssd.ssd_schedule.eol_id.offset]
+            ssd.ssd_schedule.eol.offset, ssd.ssd_schedule.eol_id.offset,
+            ssd.ssd_schedule.separate_commit.offset]
     assert got == want
 
 

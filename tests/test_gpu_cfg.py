@@ -91,7 +91,8 @@ def test_guided_decode_image_tiny(tiny, rule, top_k):
                               out)
     otok, ost = Dc.decode_image(tiny.om, pre, H, W, drafts, rule=rule, seed=3, top_k=top_k, b=2, guide=WEIGHT)
     assert np.array_equal(out - TINY.img_lo, otok)
-    assert st.passes == ost["passes"] == S.n_passes(S.plan(H, W, b=2))
+    ops = S.plan(H, W, b=2)
+    assert ost["passes"] == S.n_passes(ops) and st.passes == G.executed_passes(ops)
     assert st.accepted == ost["accepted"] and st.proposed == ost["proposed"]
     # the same images unguided differ (the weight matters for distinct prompts)
     out0 = np.zeros_like(out)

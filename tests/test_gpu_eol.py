@@ -52,7 +52,8 @@ def test_eol_decode_matches_oracle(pair, rule, top_k, k_v, b, i):
     otok, ost = Dc.decode_image(pair.om, pre, H, W, drafts, rule=rule, seed=3, top_k=top_k, k_v=k_v, b=b, i=i,
                                 q_table=q, eol_id=EOL)
     assert np.array_equal(out - SHAPE.img_lo, otok)
-    assert st.passes == ost["passes"] == S.n_passes(S.plan(H, W, k_v=k_v, b=b, i=i, eol=True))
+    ops = S.plan(H, W, k_v=k_v, b=b, i=i, eol=True)
+    assert ost["passes"] == S.n_passes(ops) and st.passes == G.executed_passes(ops)
     assert st.accepted == ost["accepted"] and st.proposed == ost["proposed"]
 
 
@@ -76,7 +77,8 @@ def test_eol_guided_decode_matches_oracle(pair):
                               (drafts + SHAPE.img_lo).astype(np.int32), out)
     otok, ost = Dc.decode_image(pair.om, pre, H, W, drafts, rule=R.RULE_SAMPLE, seed=3, top_k=50, guide=3.0,
                                 eol_id=EOL)
-    assert np.array_equal(out - SHAPE.img_lo, otok) and st.passes == ost["passes"]
+    assert np.array_equal(out - SHAPE.img_lo, otok)
+    assert st.passes == G.executed_passes(S.plan(H, W, b=2, eol=True)) and st.accepted == ost["accepted"]
 
 
 def test_eol_argument_errors(pair):

@@ -98,7 +98,8 @@ def test_heads_decode_matches_oracle(tiny, rule, top_k, k_v, b, i):
     otok, ost = Dc.decode_image(pair.om, pre, H, W, None, rule=rule, seed=3, top_k=top_k, k_v=k_v, b=b, i=i,
                                 heads=(oh, ov[:k_v]))
     assert np.array_equal(out - TINY.img_lo, otok)
-    assert st.passes == ost["passes"] == S.n_passes(S.plan(H, W, k_v=k_v, b=b, i=i))
+    ops = S.plan(H, W, k_v=k_v, b=b, i=i)
+    assert ost["passes"] == S.n_passes(ops) and st.passes == G.executed_passes(ops, heads=True)
     assert st.accepted == ost["accepted"] and st.proposed == ost["proposed"]
 
 
@@ -131,7 +132,8 @@ def test_heads_decode_with_row_ends_matches_oracle(tiny):
     otok, ost = Dc.decode_image(pair.om, pre, H, W, None, rule=R.RULE_ACCEPT_REJECT, seed=3, top_k=100, k_v=2, b=2,
                                 i=1, heads=(oh, ov), eol_id=3)
     assert np.array_equal(out - TINY.img_lo, otok)
-    assert st.passes == ost["passes"] and st.accepted == ost["accepted"] and st.proposed == ost["proposed"]
+    assert st.passes == G.executed_passes(S.plan(H, W, k_v=2, b=2, i=1, eol=True), heads=True)
+    assert st.accepted == ost["accepted"] and st.proposed == ost["proposed"]
 
 
 def test_heads_argument_errors(tiny):
@@ -171,7 +173,7 @@ def test_heads_decode_bf16_runs_and_repeats():
             outs.append(out)
         assert np.array_equal(outs[0], outs[1])
         assert ((outs[0] >= BF16.img_lo) & (outs[0] < BF16.img_hi)).all()
-        assert st.passes == S.n_passes(S.plan(H, W, b=2))
+        assert st.passes == G.executed_passes(S.plan(H, W, b=2), heads=True)
     finally:
         hs.close()
         pair.close()

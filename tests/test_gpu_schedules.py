@@ -58,7 +58,7 @@ def test_degenerate_schedule_matches_oracle(pair, case):
                                 h_rounds=h_rounds, k_v=k_v, b=b, i=i)
     assert np.array_equal(out - SHAPE.img_lo, otok)
     ops = S.plan(H, W, k_h=k_h, h_rounds=h_rounds, k_v=k_v, b=b, i=i)
-    assert st.passes == ost["passes"] == S.n_passes(ops)
+    assert ost["passes"] == S.n_passes(ops) and st.passes == G.executed_passes(ops)
     assert st.accepted == ost["accepted"] and st.proposed == ost["proposed"]
 
 
@@ -80,7 +80,44 @@ def test_heads_decode_with_one_head_family(pair, H, W):
         otok, ost = Dc.decode_image(pair.om, pre, H, W, None, rule=R.RULE_ACCEPT_REJECT, seed=3, k_h=max(k_h, 1),
                                     b=2, heads=(ora[:k_h], ora[k_h:]))
         assert np.array_equal(out - SHAPE.img_lo, otok)
-        assert st.passes == ost["passes"] and st.accepted == ost["accepted"]
+        ops = S.plan(H, W, k_h=max(k_h, 1), b=2)
+        assert st.passes == G.executed_passes(ops, heads=True) and st.accepted == ost["accepted"]
     finally:
         for h in heads:
             ssd.ssd_free_draft_head(h)
+
+
+FUSE_CASES = [  # rule, top_k, k_v, b, i, cfg, eol
+    (R.RULE_GREEDY, 0, 1, 2, 0, 0, 0),
+    (R.RULE_ACCEPT_REJECT, 100, 2, 2, 1, 0, 0),
+    (R.RULE_SAMPLE, 40, 1, 1, 0, 1, 0),
+    (R.RULE_ACCEPT_REJECT, 0, 1, 2, 0, 0, 1),
+]
+
+
+@pytest.mark.parametrize("case", FUSE_CASES, ids=[f"rule{c[0]}-kv{c[2]}-cfg{c[5]}-eol{c[6]}" for c in FUSE_CASES])
+def test_fused_commits_decide_like_separate_passes(pair, case):
+    """A commit run inside the next verify round's pass decides exactly what the
+    separate passes decide (fp32: bit for bit), with fewer passes."""
+    rule, top_k, k_v, b, i, cfg, eol = case
+    H, W, B = 6, 7, 2
+    pre = synth.prompt(SHAPE, B, P)
+    if cfg:
+        pre = np.concatenate([pre, synth.prompt(SHAPE, B, P, seed=7)])
+    drafts = (synth.random_codes(SHAPE, (B, H, W), stream=41) + SHAPE.img_lo).astype(np.int32)
+    q = None
+    if rule == R.RULE_ACCEPT_REJECT:
+        q = synth.normal(synth.SEED_DRAFTS, 42, B * H * W * SHAPE.v_img, std=1.5).astype(np.float32)
+        q = q.reshape(B, H, W, SHAPE.v_img)
+    outs, stats = [], []
+    for separate in (0, 1):
+        sc = _sched(H, W, 5, 1, k_v, b, i, rule, top_k)
+        sc.cfg, sc.cfg_weight, sc.eol, sc.eol_id, sc.separate_commit = cfg, 3.0, eol, 3, separate
+        out = np.zeros((B, H, W), np.int32)
+        stats.append(ssd.ssd_decode_image(pair.model, sc, B, P, pre, drafts, out, draft_logits=q))
+        outs.append(out)
+    assert np.array_equal(outs[0], outs[1])
+    assert stats[0].accepted == stats[1].accepted and stats[0].proposed == stats[1].proposed
+    ops = S.plan(H, W, k_h=5, k_v=k_v, b=b, i=i, eol=bool(eol))
+    assert stats[1].passes == S.n_passes(ops)
+    assert stats[0].passes == G.executed_passes(ops) < stats[1].passes
