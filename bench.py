@@ -4,7 +4,8 @@
 A step is one ssd_decode_image call: the whole SSD schedule of one batch of
 images (prefix prefill, horizontal runs of 5 tokens with one verify round
 each, then every row verified r times and committed), i.e. every verify
-pass of the image through the library's HIP kernels.  Inputs (prompt ids and
+pass of the image through the library's HIP kernels; a commit runs inside the
+pass of the verify round that follows it (same decisions, fewer passes).  Inputs (prompt ids and
 planted drafts) are resident in device memory before the timed region.
 
 Workload (default): the 1B-class bf16 decoder (24 layers, d=2048, 16x128
@@ -21,7 +22,8 @@ with --forward persistent the single-launch forward kernel),
 `attention` (the same for the attention kernel), `draft_head` (the spatial
 draft head drafting one grid row per call, timed apart from the steps),
 `verify_pass_positions` (one drafted row verified at rows 1, H/4, H/2, H-1, 50 reps
-each, beside a one-token pass at the same place), `cfg` (the same decode with
+each, beside a one-token pass at the same place), `separate_commit` (one pass per
+plan step, the paper's step count), `cfg` (the same decode with
 classifier-free guidance, weight 5.0), `heads_decode` (the whole loop drafted by
 seeded spatial heads instead of planted drafts, and the drafting time per
 image), `attention_at_scale` (the attention kernel on its own bytes at the 8B
@@ -125,6 +127,24 @@ def position_timing(ssd, model, shape, prefix, H, W, drafts, reps=50):
     return out
 
 
+def separate_rate(ssd, model, sc, B, P, d_prefix, d_drafts, steps):
+    """The same decode with one backbone pass per plan step (commit passes not
+    run inside the next verify round): the paper's step count."""
+    import ctypes
+    import torch
+    g = ssd.ssd_schedule()
+    ctypes.memmove(ctypes.addressof(g), ctypes.addressof(sc), ctypes.sizeof(sc))
+    g.separate_commit = 1
+    d_out = torch.zeros((B, sc.grid_h, sc.grid_w), dtype=torch.int32, device=torch.device("cuda:0"))
+    ssd.ssd_decode_image(model, g, B, P, d_prefix, d_drafts, d_out)
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        st = ssd.ssd_decode_image(model, g, B, P, d_prefix, d_drafts, d_out)
+    dt = (time.perf_counter() - t0) / steps
+    return {"value": B * sc.grid_h * sc.grid_w / dt, "unit": "image tokens/s", "ms_per_image": dt * 1e3 / B,
+            "passes_per_image": st.passes, "ms_per_pass": dt * 1e3 / st.passes, "steps": steps}
+
+
 def guided_rate(ssd, model, shape, sc, prefix, d_drafts, steps, weight=5.0):
     """Image tokens/s of the same decode with classifier-free guidance (weight 5.0,
     the paper's Janus-Pro setting): every image gets an unconditional twin stream
@@ -153,7 +173,10 @@ def heads_rate(ssd, model, shape, sc, prefix, d_prefix, steps, planted_ms):
     """Image tokens/s of the whole SSD loop with drafts from spatial heads: k_h
     horizontal heads and k_v vertical heads of inner size m = 2d (the paper's
     head size), seeded random weights (no trained heads exist here, so the
-    acceptance says nothing about the method)."""
+    acceptance says nothing about the method).  Drafting needs each committed
+    row's states before the next verify round, so no commit shares a pass here;
+    the drafting time is taken against the planted decode with the same passes
+    (planted_ms)."""
     import torch
     import synth
     B, P = prefix.shape
@@ -172,8 +195,10 @@ def heads_rate(ssd, model, shape, sc, prefix, d_prefix, steps, planted_ms):
     finally:
         for h in heads:
             ssd.ssd_free_draft_head(h)
+    draft_ms = dt * 1e3 / B - planted_ms
     return {"value": B * sc.grid_h * sc.grid_w / dt, "unit": "image tokens/s", "ms_per_image": dt * 1e3 / B,
-            "draft_ms_per_image": dt * 1e3 / B - planted_ms, "heads": f"{sc.k_h} horizontal + {sc.k_v} vertical, m = 2d",
+            "draft_ms_per_image": draft_ms if draft_ms == draft_ms else None,
+            "heads": f"{sc.k_h} horizontal + {sc.k_v} vertical, m = 2d",
             "passes_per_image": st.passes, "steps": steps, "acceptance_random_heads": st.accepted / max(st.proposed, 1)}
 
 
@@ -350,6 +375,7 @@ def main():
     ap.add_argument("--no-draft-head", action="store_true", help="skip the draft-head timing")
     ap.add_argument("--no-positions", action="store_true", help="skip the per-position verify-pass timing")
     ap.add_argument("--no-cfg", action="store_true", help="skip the guided (CFG) decode timing")
+    ap.add_argument("--no-separate", action="store_true", help="skip the one-pass-per-plan-step timing")
     ap.add_argument("--no-heads", action="store_true", help="skip the head-drafted decode timing")
     ap.add_argument("--no-attn-scale", action="store_true", help="skip the attention timing at the 8B shape")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
@@ -468,7 +494,9 @@ def main():
         "data": "synthetic (random N(0,0.02) weights, random prompt ids, planted drafts)",
         "config": {"workload": wl.name, "batch": B, "prefix": P, "grid": f"{H}x{W}", "rule": wl.rule,
                    "rounds": wl.rounds, "k_h": 5, "k_v": 1, "top_k": wl.top_k, "planted_keep_p": p_keep,
-                   "passes_per_image": stats.passes, "forward": args.forward, "parallelism": "single GPU"},
+                   "plan_steps_per_image": 1 + 2 * ((W - 1 + 4) // 5) + (H - 1) * (wl.rounds + 1),
+                   "passes_per_image": stats.passes, "commit": "run inside the next verify pass where adjacent",
+                   "forward": args.forward, "parallelism": "single GPU"},
         "roofline": {"bound": "hbm", "kernel": "gemm_bf16_kernel + gemm_wide_kernel (QKV/O/gate-up/down/LM-head weight streaming)",
                      "achieved": g_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": g_gbs / HBM_PEAK_GBS if g_gbs else None,
@@ -492,12 +520,17 @@ def main():
     if not args.no_positions:
         log("[bench] verify pass at four positions of the image")
         result["verify_pass_positions"] = position_timing(ssd, model, shape, prefix, H, W, drafts)
+    if not args.no_separate:
+        log("[bench] the same decode with one pass per plan step")
+        result["separate_commit"] = separate_rate(ssd, model, sc, B, P, d_prefix, d_drafts, args.steps)
     if not args.no_cfg:
         log("[bench] the same decode with classifier-free guidance")
         result["cfg"] = guided_rate(ssd, model, shape, sc, prefix, d_drafts, args.steps)
     if not args.no_heads:
         log("[bench] the whole loop with drafts from spatial heads")
-        result["heads_decode"] = heads_rate(ssd, model, shape, sc, prefix, d_prefix, args.steps, ms_step / B)
+        same_passes = result["separate_commit"]["ms_per_image"] if "separate_commit" in result else None
+        result["heads_decode"] = heads_rate(ssd, model, shape, sc, prefix, d_prefix, args.steps,
+                                            same_passes if same_passes is not None else float("nan"))
     if not args.no_draft_head and shape.dtype == "bf16":
         log("[bench] draft head: one grid row per call")
         result["draft_head"] = draft_head_cost(ssd, model, shape, target[0, 0] + shape.img_lo)
