@@ -280,8 +280,8 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmKArgs a) {
 // grid of 4-wave workgroups that puts two workgroups on some CUs and one on
 // others finishes when the doubled CUs have received twice the bytes
 // (measured on a 384-workgroup QKV launch: those workgroups' weights landed
-// about 2 us after the others').  The K-slice's token rows are copied to LDS
-// by LDS DMA (no staging registers).
+// about 2 us after the others').  The K-slice's token rows are staged
+// through registers into LDS, their loads issued before the weights'.
 template <int MT, int WV>
 __global__ __launch_bounds__(WV * 64) void gemm_wide_kernel(GemmKArgs a) {
   constexpr int KCB = 16, NTH = WV * 64;
@@ -345,16 +345,19 @@ __global__ __launch_bounds__(WV * 64) void gemm_wide_kernel(GemmKArgs a) {
     const size_t split_stride = (size_t)a.n_fb * WV * frag;
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) acc[0][mt] = floatx4{0.f, 0.f, 0.f, 0.f};
-    for (int s0 = 0; s0 < a.S; s0 += 8) {
-      floatx4 pv[8][MT];
+    // splits in flight: 64-row tiles keep four (64 registers) so that the
+    // 11- and 16-wave workgroups fit their register share without spilling
+    constexpr int SB = MT >= 4 ? 4 : 8;
+    for (int s0 = 0; s0 < a.S; s0 += SB) {
+      floatx4 pv[SB][MT];
 #pragma unroll
-      for (int j = 0; j < 8; ++j) {
+      for (int j = 0; j < SB; ++j) {
         const float* Ps = P + (size_t)min(s0 + j, a.S - 1) * split_stride;
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt) pv[j][mt] = *(const floatx4*)(Ps + mt * 64 * 4);
       }
 #pragma unroll
-      for (int j = 0; j < 8; ++j) {
+      for (int j = 0; j < SB; ++j) {
         const float m = (s0 + j < a.S) ? 1.f : 0.f;
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt) acc[0][mt] += pv[j][mt] * m;
@@ -442,9 +445,9 @@ GemmPlan gemm_plan_bf16(int M, int N, int K, int xcd) {
         // 64-row tiles: the 4-wave plan needs 8-block slices, twice the splits
         // (partial sums ~ splits x N x 64 rows); wide workgroups take 16-block
         // slices, one workgroup per CU, wherever the cost model favours them
-        // (on the 1B shapes: all projections except the O projection).  6 or 8
-        // waves: with 11 or 16 the 64-row token stage and weight burst spill.
-        for (int wv : {6, 8}) {
+        // (on the 1B shapes: all projections except the O projection; gate/up
+        // as 256 workgroups of 11 waves, down as 176 of 8).
+        for (int wv : {6, 8, 11, 16}) {
           if ((N / 16) % wv) continue;
           const int nfb = N / 16 / wv, S = kb / 16;
           const double c = cost(nfb * S, wv, 1, 16);
@@ -516,8 +519,8 @@ static void launch_wide_mt(int wv, const GemmKArgs& a, int n_fb, int S, hipStrea
   switch (wv) {
     case 6: launch_wide<MT, 6>(a, n_fb, S, st); break;
     case 8: launch_wide<MT, 8>(a, n_fb, S, st); break;
-    case 11: if constexpr (MT <= 2) launch_wide<MT, 11>(a, n_fb, S, st); break;
-    default: if constexpr (MT <= 2) launch_wide<MT, 16>(a, n_fb, S, st); break;
+    case 11: launch_wide<MT, 11>(a, n_fb, S, st); break;
+    default: launch_wide<MT, 16>(a, n_fb, S, st); break;
   }
 }
 
