@@ -388,9 +388,249 @@ __global__ __launch_bounds__(WV * 64) void gemm_wide_kernel(GemmKArgs a) {
   }
 }
 
+// Tiled GEMM for many token rows (prefill, large batches): there the
+// product is bound by the matrix cores, not by the weight stream, so each
+// workgroup owns a 128-row x (32 NT)-feature output tile over the whole K
+// range and every operand byte it loads feeds many MFMAs.  Four waves in a
+// 2 x 2 arrangement, each 64 rows (four 16-row tiles) x 16 NT features; K
+// advances in 64-input stages: the stage's token rows (both planes) sit in
+// LDS, double-buffered, and each wave's weight fragments (prepacked, one
+// 16-byte load per lane each) go straight to registers, the next stage's
+// loads in flight while the current stage is multiplied.  All row tiles of a
+// feature tile run on one XCD (xcd_grid with the row tiles as the group), so
+// its weights come from HBM once and from that XCD's L2 after.  When the
+// tiles cannot fill the CUs (few rows, narrow outputs) the K range is split
+// over S workgroups of the same XCD; the last of them sums the partials in
+// split order and runs the epilogue.
+constexpr int TILE_ROWS = 128, TILE_KT = 64, TILE_LD = TILE_KT + 8;  // 16-byte row pad: conflict-free 16-row reads
+constexpr int TILE_PL = TILE_ROWS * TILE_LD;                           // one plane of one stage (bf16)
+
+template <int NT>
+struct TileStage {
+  u32x4 x[8];         // token rows: 4 rows x 2 planes per thread
+  u32x4 w[NT][2];     // weight fragments: NT feature tiles x 2 k-blocks
+};
+
+// Buffer loads: a scalar base, 32-bit lane offsets and a scalar offset for
+// the stage's K position, the plane and the feature tile.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t tile_rsrc(const void* b) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(b), 0, 0x7FFFFFFF, 0x00020000);
+}
+
+template <int NT>
+__device__ __forceinline__ void tile_load(TileStage<NT>& st, __amdgpu_buffer_rsrc_t xh, __amdgpu_buffer_rsrc_t xl,
+                                          const int (&xoff)[4], __amdgpu_buffer_rsrc_t wr, int lane_b, int wtile_b,
+                                          int KB, int k0) {
+#pragma unroll
+  for (int p = 0; p < 4; ++p) {
+    st.x[2 * p] = __builtin_amdgcn_raw_buffer_load_b128(xh, xoff[p], k0 * 2, 0);
+    st.x[2 * p + 1] = __builtin_amdgcn_raw_buffer_load_b128(xl, xoff[p], k0 * 2, 0);
+  }
+  const int kb0 = k0 / 32;
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+      st.w[nt][kb] = __builtin_amdgcn_raw_buffer_load_b128(wr, lane_b, wtile_b + (nt * KB + kb0 + kb) * 1024, 0);
+}
+
+template <int NT>
+__device__ __forceinline__ void tile_store_x(const TileStage<NT>& st, uint16_t* xs, int tid) {
+  const int cg = tid & 7, rr = tid >> 3;
+#pragma unroll
+  for (int p = 0; p < 4; ++p) {
+    const int r = rr + 32 * p;
+    *(u32x4*)(xs + r * TILE_LD + cg * 8) = st.x[2 * p];
+    *(u32x4*)(xs + TILE_PL + r * TILE_LD + cg * 8) = st.x[2 * p + 1];
+  }
+}
+
+template <int NT>
+__device__ __forceinline__ void tile_mma(floatx4 (&acc)[NT][4], const TileStage<NT>& st, const uint16_t* xs, int wm,
+                                         int lane) {
+  const int row = wm * 64 + (lane & 15), col = (lane >> 4) * 8;
+#pragma unroll
+  for (int kb = 0; kb < 2; ++kb) {
+    bf16x8 bhi[4], blo[4];
+#pragma unroll
+    for (int mt = 0; mt < 4; ++mt) {
+      const uint16_t* p = xs + (row + mt * 16) * TILE_LD + kb * 32 + col;
+      bhi[mt] = __builtin_bit_cast(bf16x8, *(const u32x4*)p);
+      blo[mt] = __builtin_bit_cast(bf16x8, *(const u32x4*)(p + TILE_PL));
+    }
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
+      const bf16x8 w = __builtin_bit_cast(bf16x8, st.w[nt][kb]);
+#pragma unroll
+      for (int mt = 0; mt < 4; ++mt) {
+        acc[nt][mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w, bhi[mt], acc[nt][mt], 0, 0, 0);
+        acc[nt][mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w, blo[mt], acc[nt][mt], 0, 0, 0);
+      }
+    }
+  }
+}
+
+template <int NT>
+__global__ __launch_bounds__(256, 2) void gemm_tile_kernel(GemmKArgs a) {
+  __shared__ __attribute__((aligned(16))) uint16_t xs[2][2 * TILE_PL];
+  __shared__ float rscale[TILE_ROWS];
+  __shared__ float sq_red[2][TILE_ROWS];
+
+  __shared__ int is_last;
+  const int m_tiles = (a.M + TILE_ROWS - 1) / TILE_ROWS;
+  int fb, member;
+  xcd_unmap(blockIdx.x, m_tiles * a.S, a.xcd, fb, member);
+  if (fb >= a.n_fb) return;
+  const int mtile = member / a.S, split = member - mtile * a.S;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform: scalar addressing
+  const int wm = w & 1, wn = w >> 1;
+  const int r0 = mtile * TILE_ROWS;                 // first row of the tile
+  const int nb0 = fb * 2 * NT + wn * NT;            // first 16-feature tile of this wave
+  const int t0w = a.t0 + r0 + wm * 64;              // first row of this wave (absolute)
+  const int Mw = a.M - r0 - wm * 64 < 64 ? a.M - r0 - wm * 64 : 64;  // rows of this wave (<= 0: none)
+  const int Mt = a.M - r0 < TILE_ROWS ? a.M - r0 : TILE_ROWS;
+  const EpiArgs& e = a.epi;
+  const int nst = a.K / TILE_KT / a.S, st0 = split * nst;  // this split's stages (an even count)
+
+  floatx4 acc[NT][4];
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+    for (int mt = 0; mt < 4; ++mt) acc[nt][mt] = floatx4{0.f, 0.f, 0.f, 0.f};
+
+  // lane offsets of the token rows this thread copies (rows past M repeat
+  // row M - 1; their results are never stored) and of its weight fragments
+  const __amdgpu_buffer_rsrc_t xh = tile_rsrc(a.in), xl = tile_rsrc(a.in + a.in_plane), wr = tile_rsrc(a.W);
+  int xoff[4];
+#pragma unroll
+  for (int p = 0; p < 4; ++p) {
+    const int r = r0 + (tid >> 3) + 32 * p;
+    xoff[p] = ((r < a.M ? r : a.M - 1) * a.ld_in + (tid & 7) * 8) * 2;
+  }
+  const int lane_b = lane * 16, wtile_b = nb0 * a.KB * 1024;
+  auto load = [&](TileStage<NT>& st, int stage) {
+    tile_load<NT>(st, xh, xl, xoff, wr, lane_b, wtile_b, a.KB, (st0 + stage) * TILE_KT);
+  };
+  TileStage<NT> s0, s1;
+  load(s0, 0);
+  // 1/rms of the tile's rows (the LDS of stage buffer 1 serves as the
+  // reduction scratch; it is written only after the next barrier)
+  if (e.ssq)
+    rms_prologue<TILE_ROWS>(e, Mt, a.t0 + r0, (float(*)[TILE_ROWS])(void*)xs[1], rscale);
+  else if (tid < TILE_ROWS)
+    rscale[tid] = 1.f;
+  tile_store_x<NT>(s0, xs[0], tid);
+  lds_barrier();
+  // two stages per trip (the stage count is even), so that the register
+  // stages have fixed names and the loop body has no branch (a branch makes
+  // the compiler move the accumulators between register files every trip)
+  int c = 0;
+  for (; c + 2 < nst; c += 2) {
+    load(s1, c + 1);
+    tile_mma<NT>(acc, s0, xs[0], wm, lane);
+    tile_store_x<NT>(s1, xs[1], tid);
+    lds_barrier();
+    load(s0, c + 2);
+    tile_mma<NT>(acc, s1, xs[1], wm, lane);
+    tile_store_x<NT>(s0, xs[0], tid);
+    lds_barrier();
+  }
+  load(s1, c + 1);
+  tile_mma<NT>(acc, s0, xs[0], wm, lane);
+  tile_store_x<NT>(s1, xs[1], tid);
+  lds_barrier();
+  tile_mma<NT>(acc, s1, xs[1], wm, lane);
+
+  if (a.S > 1) {
+    // split-K: publish this split's fragments; the last arrival of the tile
+    // sums all splits in split order (deterministic)
+    const int grp = fb * m_tiles + mtile;
+    constexpr int FRAG = NT * 4 * 64 * 4;  // floats per wave
+    float* P = a.part + ((size_t)grp * a.S * 4 + w) * FRAG + lane * 4;
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+      for (int mt = 0; mt < 4; ++mt) *(floatx4*)(P + (size_t)split * 4 * FRAG + (nt * 4 + mt) * 256) = acc[nt][mt];
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    if (tid == 0) {
+      if (!a.xcd) __threadfence();  // splits on different XCDs: write back through L2
+      const unsigned prev = atomicAdd(&a.counters[grp], 1u);
+      is_last = prev == (unsigned)(a.S - 1);
+      if (is_last && !a.xcd) __threadfence();
+    }
+    __syncthreads();
+    if (!is_last) return;
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+      for (int mt = 0; mt < 4; ++mt) acc[nt][mt] = floatx4{0.f, 0.f, 0.f, 0.f};
+    for (int sp = 0; sp < a.S; ++sp) {
+      floatx4 v[NT][4];
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+        for (int mt = 0; mt < 4; ++mt) v[nt][mt] = *(const floatx4*)(P + (size_t)sp * 4 * FRAG + (nt * 4 + mt) * 256);
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+        for (int mt = 0; mt < 4; ++mt) acc[nt][mt] += v[nt][mt];
+    }
+    if (tid == 0) a.counters[grp] = 0u;
+  }
+
+  float sq[4] = {0.f, 0.f, 0.f, 0.f};
+  if (Mw > 0) {
+    EpiOps<NT, 4> op;
+    epi_block_starts<NT, 4>(e, Mw, t0w, lane, op);
+    epi_load<NT, 4>(e, nb0, a.N, Mw, t0w, lane, op);
+    epi_store<NT, 4>(e, acc, op, nb0, a.N, Mw, t0w, lane, rscale + wm * 64, sq);
+  }
+  if (e.kind == EPI_RESID) {
+    // per-row sums of x^2 over this tile's features: lanes of one row, then
+    // the two waves of one row half, in a fixed order
+#pragma unroll
+    for (int mt = 0; mt < 4; ++mt) {
+      float v = sq[mt];
+      v += __shfl_xor(v, 16);
+      v += __shfl_xor(v, 32);
+      if (lane < 16) sq_red[wn][wm * 64 + mt * 16 + lane] = v;
+    }
+    __syncthreads();
+    if (tid < Mt) e.ssq_out[(size_t)fb * e.ssq_out_ld + a.t0 + r0 + tid] = sq_red[0][tid] + sq_red[1][tid];
+  }
+}
+
 GemmPlan gemm_plan_bf16(int M, int N, int K, int xcd) {
   GemmPlan p;
   p.xcd = xcd;
+  p.tile = 0;
+  if (M > 128 && K % (2 * TILE_KT) == 0 && N % 64 == 0 && (size_t)N * K * 2 < (1ull << 31)) {
+    // tiled: 128-feature tiles unless 64-feature ones spread the work over
+    // the CUs better (cost = workgroups on the busiest CU x tile width)
+    // 128-feature tiles wherever they give at least 160 workgroups (measured
+    // on the 8B and 1B shapes: up to 35 % faster than 64-feature tiles
+    // there, slower on grids that leave CUs idle); then K splits (halving
+    // the stages per split, whose count must stay even) until the grid has
+    // 256 workgroups
+    const int mt = (M + TILE_ROWS - 1) / TILE_ROWS;
+    const long w4 = (long)(N / 128) * mt;
+    const bool four = N % 128 == 0 && w4 >= 160;
+    p.tile = 1;
+    p.NT = four ? 4 : 2;
+    p.MT = TILE_ROWS / 16;
+    p.WV = 4;
+    p.bn = 32 * p.NT;
+    p.n_fb = N / p.bn;
+    p.m_tiles = mt;
+    p.S = 1;
+    const int nst = K / TILE_KT;
+    while ((long)p.n_fb * mt * p.S < 256 && p.S < 8 && nst % (4 * p.S) == 0) p.S *= 2;
+    p.KCB = TILE_KT / 32;
+    p.kchunks = nst / p.S;
+    return p;
+  }
   // up to 128 tokens: one-burst launches over row tiles of at most 64
   // (the weights are streamed once per tile); beyond: double-buffered chunks
   // of 128-row tiles
@@ -504,8 +744,9 @@ GemmPlan gemm_plan_bf16(int M, int N, int K, int xcd) {
 }
 
 size_t gemm_partials_floats(const GemmPlan& p, int M) {
-  (void)M;
   if (p.S <= 1) return 0;
+  if (p.tile) return (size_t)p.S * p.m_tiles * TILE_ROWS * p.n_fb * p.bn;
+  (void)M;
   return (size_t)p.S * p.n_fb * p.WV * p.NT * p.MT * 64 * 4;
 }
 
@@ -531,6 +772,38 @@ static void launch_gemm(const GemmKArgs& a, int n_fb, int S, hipStream_t st) {
 
 void gemm_bf16(const GemmPlan& p, const void* Wpacked, int N, int K, const void* in, size_t in_plane, int ld_in,
                int M, const EpiArgs& epi, float* partials, unsigned* counters, hipStream_t st) {
+  if (p.tile) {
+    // buffer addressing reaches 2 GiB from each plane's base: rows beyond
+    // that go to further launches (chunks of whole row tiles)
+    const size_t row_b = (size_t)ld_in * 2;
+    int rows = (int)std::min<size_t>((size_t)M, ((1ull << 31) - (size_t)K * 2) / row_b);
+    rows = std::max(TILE_ROWS, rows / TILE_ROWS * TILE_ROWS);
+    for (int t0 = 0; t0 < M; t0 += rows) {
+      GemmKArgs a{};
+      a.W = (const u32x4*)Wpacked;
+      a.N = N;
+      a.K = K;
+      a.KB = K / 32;
+      a.S = p.S;
+      a.kchunks = p.kchunks;
+      a.n_fb = p.n_fb;
+      a.in = (const uint16_t*)in + (size_t)t0 * ld_in;
+      a.in_plane = in_plane;
+      a.ld_in = ld_in;
+      a.M = std::min(rows, M - t0);
+      a.t0 = t0;
+      a.xcd = p.xcd;
+      a.part = partials;
+      a.counters = counters;
+      a.epi = epi;
+      const dim3 grid(xcd_grid(p.n_fb, (a.M + TILE_ROWS - 1) / TILE_ROWS * p.S, p.xcd));
+      if (p.NT == 4)
+        launch_timed(gemm_tile_kernel<4>, grid, dim3(256), st, a);
+      else
+        launch_timed(gemm_tile_kernel<2>, grid, dim3(256), st, a);
+    }
+    return;
+  }
   const int MP = p.MT * 16;
   for (int t0 = 0; t0 < M; t0 += MP) {
     GemmKArgs a;

@@ -567,7 +567,7 @@ void run_forward(ssd_session* s, int K, int lm_mode) {
     };
     need(M <= s->Mmax, "token count exceeds the session's activation buffers");
     for (const GemmPlan* gp : {&pq, &po, &p13, &p2}) {
-      need(gemm_partials_floats(*gp, M) <= s->gpart_cap && (size_t)gp->n_fb <= s->gcnt_cap,
+      need(gemm_partials_floats(*gp, M) <= s->gpart_cap && (size_t)gemm_counters(*gp) <= s->gcnt_cap,
            "GEMM plan exceeds the split-K workspace");
     }
     need(po.n_fb <= s->ssq_parts_cap && p2.n_fb <= s->ssq_parts_cap, "rms partial sums exceed their buffer");
@@ -667,7 +667,7 @@ void run_forward(ssd_session* s, int K, int lm_mode) {
     e.ld = dm.Vimg;
     if (lm_mode == 0) {
       GemmPlan pl = gemm_plan_bf16(M, dm.Vimg, d, X);
-      if (gemm_partials_floats(pl, M) > s->gpart_cap || (size_t)pl.n_fb > s->gcnt_cap)
+      if (gemm_partials_floats(pl, M) > s->gpart_cap || (size_t)gemm_counters(pl) > s->gcnt_cap)
         throw HipError{hipErrorInvalidValue, "GEMM plan exceeds the split-K workspace"};
       m->prof.run(4, (double)dm.Vimg * d * es + (double)M * d * A + (double)M * dm.Vimg * 4, st, [&] {
         gemm_bf16(pl, m->wlm, dm.Vimg, d, s->xn, s->xn_plane, d, M, e, s->gpart, s->gcnt, st);
@@ -676,7 +676,7 @@ void run_forward(ssd_session* s, int K, int lm_mode) {
       e.ssq_off = K - 1;
       e.ssq_step = K;
       GemmPlan pl = gemm_plan_bf16(B, dm.Vimg, d, X);
-      if (gemm_partials_floats(pl, B) > s->gpart_cap || (size_t)pl.n_fb > s->gcnt_cap)
+      if (gemm_partials_floats(pl, B) > s->gpart_cap || (size_t)gemm_counters(pl) > s->gcnt_cap)
         throw HipError{hipErrorInvalidValue, "GEMM plan exceeds the split-K workspace"};
       m->prof.run(4, (double)dm.Vimg * d * es + (double)B * d * A + (double)B * dm.Vimg * 4, st, [&] {
         gemm_bf16(pl, m->wlm, dm.Vimg, d, (const uint16_t*)s->xn + (size_t)(K - 1) * d, s->xn_plane, K * d, B, e,
@@ -778,14 +778,15 @@ void size_workspaces(const Dims& dm, const ssd_model* m, int B, int P, int Kmax,
   if (!dm.bf16) return;
   const int Nqkv = (dm.Hq + 2 * dm.Hkv) * dm.D;
   // every token-tile class a plan can fall in: up to 16, 32 and 64 tokens,
-  // 65..128 (64-token tiles), beyond 128 (128-token tiles)
-  for (int Mc : {1, 16, 17, 32, 33, 64, 65, 128, 129, 256}) {
+  // 65..128 (64-token tiles), beyond 128 (tiled, every row-tile count up to
+  // where no plan splits K any more)
+  for (int Mc : gemm_row_classes()) {
     for (auto nk : {std::make_pair(Nqkv, dm.d), std::make_pair(dm.d, dm.Hq * dm.D), std::make_pair(2 * dm.dff, dm.d),
                     std::make_pair(dm.d, dm.dff), std::make_pair(dm.Vimg, dm.d)}) {
       GemmPlan p = gemm_plan_bf16(Mc, nk.first, nk.second, 0);  // sizes do not depend on the XCD mapping
       gpart = std::max(gpart, gemm_partials_floats(p, Mc));
-      gcnt = std::max(gcnt, (size_t)p.n_fb);
-      if (nk.first == dm.d) ssq_parts_max = std::max(ssq_parts_max, p.n_fb);
+      gcnt = std::max(gcnt, (size_t)gemm_counters(p));
+      if (nk.first == dm.d) ssq_parts_max = std::max(ssq_parts_max, std::max(p.n_fb, gemm_max_parts(dm.d)));
     }
   }
   // every block length the session can run, every context up to Lmax
@@ -1241,7 +1242,7 @@ void head_forward(ssd_draft_head* h, int R, const float* hin, const int* tok, hi
     const int X = m->xcd;
     auto plan = [&](int N, int K) {
       GemmPlan p = gemm_plan_bf16(R, N, K, X);
-      if (gemm_partials_floats(p, R) > h->gpart_cap || (size_t)p.n_fb > h->gcnt_cap ||
+      if (gemm_partials_floats(p, R) > h->gpart_cap || (size_t)gemm_counters(p) > h->gcnt_cap ||
           (N == d && p.n_fb > h->ssq_cap))
         throw HipError{hipErrorInvalidValue, "GEMM plan exceeds the draft head's workspace"};
       return p;
@@ -1372,14 +1373,14 @@ ssd_status ssd_draft_head_init(ssd_model* m, int32_t mi, const void* weights, in
     // workspaces for every plan a run of up to max_rows rows can meet
     size_t gpart = 0, gcnt = 0;
     int parts = 1;
-    for (int Mc : {1, 16, 17, 32, 33, 64, 65, 128, 129, 256}) {
+    for (int Mc : gemm_row_classes()) {
       if (!dm.bf16) break;
       for (auto nk : {std::make_pair(d, 2 * d), std::make_pair(2 * mi, d), std::make_pair(d, mi),
                       std::make_pair(dm.Vimg, d)}) {
         GemmPlan p = gemm_plan_bf16(Mc, nk.first, nk.second, 0);
         gpart = std::max(gpart, gemm_partials_floats(p, Mc));
-        gcnt = std::max(gcnt, (size_t)p.n_fb);
-        if (nk.first == d) parts = std::max(parts, p.n_fb);
+        gcnt = std::max(gcnt, (size_t)gemm_counters(p));
+        if (nk.first == d) parts = std::max(parts, std::max(p.n_fb, gemm_max_parts(d)));
       }
     }
     h->gpart_cap = gpart;

@@ -17,6 +17,10 @@ stays within seconds.  Cases:
       (split-KV attention with a cross-chunk merge)
   8B width, batch 1, a 64-token block at context 4288..4352 (the last row of
       the 64x64 image), rule (A)
+  1B width, batch 4, 64-token prompt and a 64-token block (M = 256, prefill
+      and verify): tiled GEMMs whose K range is split over workgroups to
+      fill the CUs (O and down projections in 4 splits, QKV in 2), rule (A),
+      2 rounds + commit
 """
 import dataclasses
 
@@ -51,6 +55,13 @@ def pair7():
 @pytest.fixture(scope="module")
 def pair8():
     p = _pair(W8, "8B-width GQA 2-layer model")
+    yield p
+    p.close()
+
+
+@pytest.fixture(scope="module")
+def pair1():
+    p = _pair(W1, "1B-width 2-layer model")
     yield p
     p.close()
 
@@ -103,22 +114,23 @@ def test_8b_width_context_4352(pair8):
         ssd.ssd_free_session(sess)
 
 
-def test_1b_width_b4_context_1088_rule_c():
-    pair = _pair(W1, "1B-width 2-layer model")
+def test_1b_width_b4_context_1088_rule_c(pair1):
+    pair = pair1
     B, P, K, top_k = 4, 1056, 32, 2000
+    pre = synth.prompt(W1, B, P)
+    print("oracle prefill of 4 x 1056 tokens", flush=True)
+    os_ = Dc.prefill(pair.om, pre, P + K)
+    q = synth.normal(synth.SEED_DRAFTS, 14, B * K * W1.v_img, std=1.5).reshape(B, K, W1.v_img)
+    drafts = q.argmax(axis=2).astype(np.int64)
+    sess = ssd.ssd_prefill(pair.model, B, P, pre, P + K, K)
+    stats = {}
     try:
-        pre = synth.prompt(W1, B, P)
-        print("oracle prefill of 4 x 1056 tokens", flush=True)
-        os_ = Dc.prefill(pair.om, pre, P + K)
-        q = synth.normal(synth.SEED_DRAFTS, 14, B * K * W1.v_img, std=1.5).reshape(B, K, W1.v_img)
-        drafts = q.argmax(axis=2).astype(np.int64)
-        sess = ssd.ssd_prefill(pair.model, B, P, pre, P + K, K)
-        stats = {}
-        try:
-            blk, _ = G.check_round(W1, sess, os_, drafts, 0, R.RULE_ACCEPT_REJECT, 0, top_k, q, stats)
-            G.check_commit(W1, sess, os_, blk, stats)
-            print("parity stats", stats, flush=True)
-        finally:
-            ssd.ssd_free_session(sess)
+        blk, _ = G.check_round(W1, sess, os_, drafts, 0, R.RULE_ACCEPT_REJECT, 0, top_k, q, stats)
+        G.check_commit(W1, sess, os_, blk, stats)
+        print("parity stats", stats, flush=True)
     finally:
-        pair.close()
+        ssd.ssd_free_session(sess)
+
+
+def test_1b_width_b4_block64_split_tiles(pair1):
+    _greedy_block(pair1, W1, B=4, P=64, K=64, rounds=2, keep=0.6, seed_stream=15)
