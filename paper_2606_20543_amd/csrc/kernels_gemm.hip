@@ -388,8 +388,10 @@ __global__ __launch_bounds__(WV * 64) void gemm_wide_kernel(GemmKArgs a) {
   }
 }
 
-// Tiled GEMM for many token rows (prefill, large batches): there the
-// product is bound by the matrix cores, not by the weight stream, so each
+// Tiled GEMM for more than 64 token rows (prefill, batches, guided passes):
+// there the weights are worth reusing from registers and LDS rather than
+// streaming once per 64-row tile, and from a few hundred rows on the product
+// is bound by the matrix cores, not by the weight stream.  Each
 // workgroup owns a 128-row x (32 NT)-feature output tile over the whole K
 // range and every operand byte it loads feeds many MFMAs.  Four waves in a
 // 2 x 2 arrangement, each 64 rows (four 16-row tiles) x 16 NT features; K
@@ -606,9 +608,7 @@ GemmPlan gemm_plan_bf16(int M, int N, int K, int xcd) {
   GemmPlan p;
   p.xcd = xcd;
   p.tile = 0;
-  if (M > 128 && K % (2 * TILE_KT) == 0 && N % 64 == 0 && (size_t)N * K * 2 < (1ull << 31)) {
-    // tiled: 128-feature tiles unless 64-feature ones spread the work over
-    // the CUs better (cost = workgroups on the busiest CU x tile width)
+  if (M > 64 && K % (2 * TILE_KT) == 0 && N % 64 == 0 && (size_t)N * K * 2 < (1ull << 31)) {
     // 128-feature tiles wherever they give at least 160 workgroups (measured
     // on the 8B and 1B shapes: up to 35 % faster than 64-feature tiles
     // there, slower on grids that leave CUs idle); then K splits (halving
@@ -631,9 +631,9 @@ GemmPlan gemm_plan_bf16(int M, int N, int K, int xcd) {
     p.kchunks = nst / p.S;
     return p;
   }
-  // up to 128 tokens: one-burst launches over row tiles of at most 64
-  // (the weights are streamed once per tile); beyond: double-buffered chunks
-  // of 128-row tiles
+  // up to 64 tokens (and shapes the tiled kernel does not take): one-burst
+  // launches over row tiles of at most 64 (the weights are streamed once per
+  // tile); beyond 128: double-buffered chunks of 128-row tiles
   int Mc = M <= 128 ? (M < 64 ? M : 64) : 128;
   p.MT = Mc <= 16 ? 1 : Mc <= 32 ? 2 : Mc <= 64 ? 4 : 8;
   const int kb = K / 32;

@@ -123,7 +123,7 @@ struct GemmPlan {
   int kchunks;      // chunks per split
   int bn;           // features per workgroup
   int xcd;          // >0: workgroups that reduce together share one XCD (n XCDs); 0: fenced reduction
-  int tile;         // 1: tiled kernel for many rows (128-row tiles, K split only to fill the CUs)
+  int tile;         // 1: tiled kernel for more than 64 rows (128-row tiles, K split only to fill the CUs)
   int m_tiles;      // tiled: 128-row tiles
 };
 // split-K arrival counters a plan uses (tiled plans: one per output tile, when split)
@@ -131,9 +131,10 @@ inline int gemm_counters(const GemmPlan& p) {
   return p.tile ? (p.S > 1 ? p.n_fb * p.m_tiles : 0) : p.n_fb;
 }
 // Row counts that cover every plan class: up to 16, 32 and 64 rows, 65..128
-// (64-row tiles) and, for the tiled plans, each count of 128-row tiles up to
-// 256 (a split plan has fewer than 256 output tiles).  Sizing a workspace
-// over these bounds every plan of any row count.
+// (one 128-row tile, or 64-row streaming tiles for shapes the tiled kernel
+// does not take) and each count of 128-row tiles up to 256 (a split plan has
+// fewer than 256 output tiles).  Sizing a workspace over these bounds every
+// plan of any row count.
 inline std::vector<int> gemm_row_classes() {
   std::vector<int> v = {1, 16, 17, 32, 33, 64, 65, 128};
   for (int t = 2; t <= 256; ++t) v.push_back(128 * t);
