@@ -472,7 +472,10 @@ __device__ __forceinline__ void tile_mma(floatx4 (&acc)[NT][4], const TileStage<
   }
 }
 
-template <int NT>
+// DEPTH 2: two register stages, loads one stage ahead; DEPTH 4: four
+// register stages, loads three stages ahead (64-feature tiles only, which
+// still fit two workgroups per CU with them)
+template <int NT, int DEPTH>
 __global__ __launch_bounds__(256, 2) void gemm_tile_kernel(GemmKArgs a) {
   __shared__ __attribute__((aligned(16))) uint16_t xs[2][2 * TILE_PL];
   __shared__ float rscale[TILE_ROWS];
@@ -493,7 +496,7 @@ __global__ __launch_bounds__(256, 2) void gemm_tile_kernel(GemmKArgs a) {
   const int Mw = a.M - r0 - wm * 64 < 64 ? a.M - r0 - wm * 64 : 64;  // rows of this wave (<= 0: none)
   const int Mt = a.M - r0 < TILE_ROWS ? a.M - r0 : TILE_ROWS;
   const EpiArgs& e = a.epi;
-  const int nst = a.K / TILE_KT / a.S, st0 = split * nst;  // this split's stages (an even count)
+  const int nst = a.K / TILE_KT / a.S, st0 = split * nst;  // this split's stages (a multiple of DEPTH)
 
   floatx4 acc[NT][4];
 #pragma unroll
@@ -514,35 +517,79 @@ __global__ __launch_bounds__(256, 2) void gemm_tile_kernel(GemmKArgs a) {
   auto load = [&](TileStage<NT>& st, int stage) {
     tile_load<NT>(st, xh, xl, xoff, wr, lane_b, wtile_b, a.KB, (st0 + stage) * TILE_KT);
   };
-  TileStage<NT> s0, s1;
-  load(s0, 0);
   // 1/rms of the tile's rows (the LDS of stage buffer 1 serves as the
   // reduction scratch; it is written only after the next barrier)
-  if (e.ssq)
-    rms_prologue<TILE_ROWS>(e, Mt, a.t0 + r0, (float(*)[TILE_ROWS])(void*)xs[1], rscale);
-  else if (tid < TILE_ROWS)
-    rscale[tid] = 1.f;
-  tile_store_x<NT>(s0, xs[0], tid);
-  lds_barrier();
-  // two stages per trip (the stage count is even), so that the register
-  // stages have fixed names and the loop body has no branch (a branch makes
-  // the compiler move the accumulators between register files every trip)
-  int c = 0;
-  for (; c + 2 < nst; c += 2) {
+  auto rms = [&]() {
+    if (e.ssq)
+      rms_prologue<TILE_ROWS>(e, Mt, a.t0 + r0, (float(*)[TILE_ROWS])(void*)xs[1], rscale);
+    else if (tid < TILE_ROWS)
+      rscale[tid] = 1.f;
+  };
+  // DEPTH stages per trip, so that the register stages have fixed names and
+  // the loop body has no branch (a branch makes the compiler move the
+  // accumulators between register files every trip); stage c sits in LDS
+  // buffer c % 2
+  if constexpr (DEPTH == 2) {
+    TileStage<NT> s0, s1;
+    load(s0, 0);
+    rms();
+    tile_store_x<NT>(s0, xs[0], tid);
+    lds_barrier();
+    int c = 0;
+    for (; c + 2 < nst; c += 2) {
+      load(s1, c + 1);
+      tile_mma<NT>(acc, s0, xs[0], wm, lane);
+      tile_store_x<NT>(s1, xs[1], tid);
+      lds_barrier();
+      load(s0, c + 2);
+      tile_mma<NT>(acc, s1, xs[1], wm, lane);
+      tile_store_x<NT>(s0, xs[0], tid);
+      lds_barrier();
+    }
     load(s1, c + 1);
     tile_mma<NT>(acc, s0, xs[0], wm, lane);
     tile_store_x<NT>(s1, xs[1], tid);
     lds_barrier();
-    load(s0, c + 2);
     tile_mma<NT>(acc, s1, xs[1], wm, lane);
+  } else {
+    TileStage<NT> s0, s1, s2, s3;
+    load(s0, 0);
+    load(s1, 1);
+    load(s2, 2);
+    rms();
     tile_store_x<NT>(s0, xs[0], tid);
     lds_barrier();
+    int c = 0;
+    for (; c + 4 < nst; c += 4) {
+      load(s3, c + 3);
+      tile_mma<NT>(acc, s0, xs[0], wm, lane);
+      tile_store_x<NT>(s1, xs[1], tid);
+      lds_barrier();
+      load(s0, c + 4);
+      tile_mma<NT>(acc, s1, xs[1], wm, lane);
+      tile_store_x<NT>(s2, xs[0], tid);
+      lds_barrier();
+      load(s1, c + 5);
+      tile_mma<NT>(acc, s2, xs[0], wm, lane);
+      tile_store_x<NT>(s3, xs[1], tid);
+      lds_barrier();
+      load(s2, c + 6);
+      tile_mma<NT>(acc, s3, xs[1], wm, lane);
+      tile_store_x<NT>(s0, xs[0], tid);
+      lds_barrier();
+    }
+    load(s3, c + 3);
+    tile_mma<NT>(acc, s0, xs[0], wm, lane);
+    tile_store_x<NT>(s1, xs[1], tid);
+    lds_barrier();
+    tile_mma<NT>(acc, s1, xs[1], wm, lane);
+    tile_store_x<NT>(s2, xs[0], tid);
+    lds_barrier();
+    tile_mma<NT>(acc, s2, xs[0], wm, lane);
+    tile_store_x<NT>(s3, xs[1], tid);
+    lds_barrier();
+    tile_mma<NT>(acc, s3, xs[1], wm, lane);
   }
-  load(s1, c + 1);
-  tile_mma<NT>(acc, s0, xs[0], wm, lane);
-  tile_store_x<NT>(s1, xs[1], tid);
-  lds_barrier();
-  tile_mma<NT>(acc, s1, xs[1], wm, lane);
 
   if (a.S > 1) {
     // split-K: publish this split's fragments; the last arrival of the tile
@@ -629,6 +676,10 @@ GemmPlan gemm_plan_bf16(int M, int N, int K, int xcd) {
     while ((long)p.n_fb * mt * p.S < 256 && p.S < 8 && nst % (4 * p.S) == 0) p.S *= 2;
     p.KCB = TILE_KT / 32;
     p.kchunks = nst / p.S;
+    // four-stage pipeline for 64-feature tiles (measured on the 8B shapes at
+    // 512 rows: O 75 -> 59 us, down 241 -> 177); 128-feature tiles would need
+    // one workgroup per CU for it, which measured slower
+    p.depth = (p.NT == 2 && p.kchunks % 4 == 0) ? 4 : 2;
     return p;
   }
   // up to 64 tokens (and shapes the tiled kernel does not take): one-burst
@@ -798,9 +849,11 @@ void gemm_bf16(const GemmPlan& p, const void* Wpacked, int N, int K, const void*
       a.epi = epi;
       const dim3 grid(xcd_grid(p.n_fb, (a.M + TILE_ROWS - 1) / TILE_ROWS * p.S, p.xcd));
       if (p.NT == 4)
-        launch_timed(gemm_tile_kernel<4>, grid, dim3(256), st, a);
+        launch_timed(gemm_tile_kernel<4, 2>, grid, dim3(256), st, a);
+      else if (p.depth == 4)
+        launch_timed(gemm_tile_kernel<2, 4>, grid, dim3(256), st, a);
       else
-        launch_timed(gemm_tile_kernel<2>, grid, dim3(256), st, a);
+        launch_timed(gemm_tile_kernel<2, 2>, grid, dim3(256), st, a);
     }
     return;
   }

@@ -125,6 +125,7 @@ struct GemmPlan {
   int xcd;          // >0: workgroups that reduce together share one XCD (n XCDs); 0: fenced reduction
   int tile;         // 1: tiled kernel for more than 64 rows (128-row tiles, K split only to fill the CUs)
   int m_tiles;      // tiled: 128-row tiles
+  int depth;        // tiled: register stages of the K pipeline (2 or 4)
 };
 // split-K arrival counters a plan uses (tiled plans: one per output tile, when split)
 inline int gemm_counters(const GemmPlan& p) {
