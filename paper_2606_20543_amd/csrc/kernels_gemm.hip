@@ -437,6 +437,27 @@ __device__ __forceinline__ void tile_load(TileStage<NT>& st, __amdgpu_buffer_rsr
 }
 
 template <int NT>
+__device__ __forceinline__ void tile_load_x(TileStage<NT>& st, __amdgpu_buffer_rsrc_t xh, __amdgpu_buffer_rsrc_t xl,
+                                            const int (&xoff)[4], int k0) {
+#pragma unroll
+  for (int p = 0; p < 4; ++p) {
+    st.x[2 * p] = __builtin_amdgcn_raw_buffer_load_b128(xh, xoff[p], k0 * 2, 0);
+    st.x[2 * p + 1] = __builtin_amdgcn_raw_buffer_load_b128(xl, xoff[p], k0 * 2, 0);
+  }
+}
+
+template <int NT>
+__device__ __forceinline__ void tile_load_w(TileStage<NT>& st, __amdgpu_buffer_rsrc_t wr, int lane_b, int wtile_b,
+                                            int KB, int k0) {
+  const int kb0 = k0 / 32;
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+      st.w[nt][kb] = __builtin_amdgcn_raw_buffer_load_b128(wr, lane_b, wtile_b + (nt * KB + kb0 + kb) * 1024, 0);
+}
+
+template <int NT>
 __device__ __forceinline__ void tile_store_x(const TileStage<NT>& st, uint16_t* xs, int tid) {
   const int cg = tid & 7, rr = tid >> 3;
 #pragma unroll
@@ -517,6 +538,10 @@ __global__ __launch_bounds__(256, 2) void gemm_tile_kernel(GemmKArgs a) {
   auto load = [&](TileStage<NT>& st, int stage) {
     tile_load<NT>(st, xh, xl, xoff, wr, lane_b, wtile_b, a.KB, (st0 + stage) * TILE_KT);
   };
+  auto load_x = [&](TileStage<NT>& st, int stage) { tile_load_x<NT>(st, xh, xl, xoff, (st0 + stage) * TILE_KT); };
+  auto load_w = [&](TileStage<NT>& st, int stage) {
+    tile_load_w<NT>(st, wr, lane_b, wtile_b, a.KB, (st0 + stage) * TILE_KT);
+  };
   // 1/rms of the tile's rows (the LDS of stage buffer 1 serves as the
   // reduction scratch; it is written only after the next barrier)
   auto rms = [&]() {
@@ -529,7 +554,63 @@ __global__ __launch_bounds__(256, 2) void gemm_tile_kernel(GemmKArgs a) {
   // the loop body has no branch (a branch makes the compiler move the
   // accumulators between register files every trip); stage c sits in LDS
   // buffer c % 2
-  if constexpr (DEPTH == 2) {
+  if constexpr (DEPTH == 3) {
+    // weights two stages ahead in three register slots (w0..w2), token rows
+    // one stage ahead (xr); a trip runs three stages, so the LDS buffer of
+    // its first stage alternates between trips
+    TileStage<NT> w0, w1, w2, xr;
+    load(w0, 0);
+    load_w(w1, 1);
+    rms();
+    tile_store_x<NT>(w0, xs[0], tid);
+    lds_barrier();
+    int c = 0;
+    uint16_t* xa = xs[0];  // buffer of stage c
+    uint16_t* xb = xs[1];
+    for (; c + 4 < nst; c += 3) {
+      load_x(xr, c + 1);
+      load_w(w2, c + 2);
+      tile_mma<NT>(acc, w0, xa, wm, lane);
+      tile_store_x<NT>(xr, xb, tid);
+      lds_barrier();
+      load_x(xr, c + 2);
+      load_w(w0, c + 3);
+      tile_mma<NT>(acc, w1, xb, wm, lane);
+      tile_store_x<NT>(xr, xa, tid);
+      lds_barrier();
+      load_x(xr, c + 3);
+      load_w(w1, c + 4);
+      tile_mma<NT>(acc, w2, xa, wm, lane);
+      tile_store_x<NT>(xr, xb, tid);
+      lds_barrier();
+      uint16_t* t = xa;
+      xa = xb;
+      xb = t;
+    }
+    // 2, 3 or 4 stages left: w0 holds stage c (its rows in xa), w1 stage c + 1
+    const int left = nst - c;
+    load_x(xr, c + 1);
+    if (left >= 3) load_w(w2, c + 2);
+    tile_mma<NT>(acc, w0, xa, wm, lane);
+    tile_store_x<NT>(xr, xb, tid);
+    lds_barrier();
+    if (left >= 3) {
+      load_x(xr, c + 2);
+      if (left == 4) load_w(w0, c + 3);
+    }
+    tile_mma<NT>(acc, w1, xb, wm, lane);
+    if (left >= 3) {
+      tile_store_x<NT>(xr, xa, tid);
+      lds_barrier();
+      if (left == 4) load_x(xr, c + 3);
+      tile_mma<NT>(acc, w2, xa, wm, lane);
+      if (left == 4) {
+        tile_store_x<NT>(xr, xb, tid);
+        lds_barrier();
+        tile_mma<NT>(acc, w0, xb, wm, lane);
+      }
+    }
+  } else if constexpr (DEPTH == 2) {
     TileStage<NT> s0, s1;
     load(s0, 0);
     rms();
@@ -679,7 +760,7 @@ GemmPlan gemm_plan_bf16(int M, int N, int K, int xcd) {
     // four-stage pipeline for 64-feature tiles (measured on the 8B shapes at
     // 512 rows: O 75 -> 59 us, down 241 -> 177); 128-feature tiles would need
     // one workgroup per CU for it, which measured slower
-    p.depth = (p.NT == 2 && p.kchunks % 4 == 0) ? 4 : 2;
+    p.depth = p.NT == 4 ? 3 : (p.kchunks % 4 == 0 ? 4 : 2);
     return p;
   }
   // up to 64 tokens (and shapes the tiled kernel does not take): one-burst
@@ -849,7 +930,7 @@ void gemm_bf16(const GemmPlan& p, const void* Wpacked, int N, int K, const void*
       a.epi = epi;
       const dim3 grid(xcd_grid(p.n_fb, (a.M + TILE_ROWS - 1) / TILE_ROWS * p.S, p.xcd));
       if (p.NT == 4)
-        launch_timed(gemm_tile_kernel<4, 2>, grid, dim3(256), st, a);
+        launch_timed(gemm_tile_kernel<4, 3>, grid, dim3(256), st, a);
       else if (p.depth == 4)
         launch_timed(gemm_tile_kernel<2, 4>, grid, dim3(256), st, a);
       else
