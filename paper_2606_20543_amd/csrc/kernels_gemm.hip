@@ -404,8 +404,12 @@ __global__ __launch_bounds__(WV * 64) void gemm_wide_kernel(GemmKArgs a) {
 // tiles cannot fill the CUs (few rows, narrow outputs) the K range is split
 // over S workgroups of the same XCD; the last of them sums the partials in
 // split order and runs the epilogue.
-constexpr int TILE_ROWS = 128, TILE_KT = 64, TILE_LD = TILE_KT + 8;  // 16-byte row pad: conflict-free 16-row reads
-constexpr int TILE_PL = TILE_ROWS * TILE_LD;                           // one plane of one stage (bf16)
+// LDS rows of one stage are unpadded (64 inputs, eight 16-byte chunks); chunk
+// c of row r sits at chunk c ^ ((r >> 1) & 7), so that the 16 rows an MFMA
+// operand read touches at one logical chunk hit distinct banks in groups of
+// 16 and of 32 lanes, and each row's stores stay one 128-byte span
+constexpr int TILE_ROWS = 128, TILE_KT = 64, TILE_LD = TILE_KT;
+constexpr int TILE_PL = TILE_ROWS * TILE_LD;  // one plane of one stage (bf16)
 
 template <int NT>
 struct TileStage {
@@ -463,21 +467,23 @@ __device__ __forceinline__ void tile_store_x(const TileStage<NT>& st, uint16_t* 
 #pragma unroll
   for (int p = 0; p < 4; ++p) {
     const int r = rr + 32 * p;
-    *(u32x4*)(xs + r * TILE_LD + cg * 8) = st.x[2 * p];
-    *(u32x4*)(xs + TILE_PL + r * TILE_LD + cg * 8) = st.x[2 * p + 1];
+    const int pc = cg ^ ((r >> 1) & 7);
+    *(u32x4*)(xs + r * TILE_LD + pc * 8) = st.x[2 * p];
+    *(u32x4*)(xs + TILE_PL + r * TILE_LD + pc * 8) = st.x[2 * p + 1];
   }
 }
 
 template <int NT>
 __device__ __forceinline__ void tile_mma(floatx4 (&acc)[NT][4], const TileStage<NT>& st, const uint16_t* xs, int wm,
                                          int lane) {
-  const int row = wm * 64 + (lane & 15), col = (lane >> 4) * 8;
+  const int row = wm * 64 + (lane & 15);
 #pragma unroll
   for (int kb = 0; kb < 2; ++kb) {
     bf16x8 bhi[4], blo[4];
 #pragma unroll
     for (int mt = 0; mt < 4; ++mt) {
-      const uint16_t* p = xs + (row + mt * 16) * TILE_LD + kb * 32 + col;
+      // rows row + 16 mt share (row >> 1) & 7 = ((lane & 15) >> 1)
+      const uint16_t* p = xs + (row + mt * 16) * TILE_LD + (((kb * 4 + (lane >> 4)) ^ ((lane & 15) >> 1)) * 8);
       bhi[mt] = __builtin_bit_cast(bf16x8, *(const u32x4*)p);
       blo[mt] = __builtin_bit_cast(bf16x8, *(const u32x4*)(p + TILE_PL));
     }
