@@ -27,7 +27,8 @@ plan step, the paper's step count), `cfg` (the same decode with
 classifier-free guidance, weight 5.0), `heads_decode` (the whole loop drafted by
 seeded spatial heads instead of planted drafts, and the drafting time per
 image), `attention_at_scale` (the attention kernel on its own bytes at the 8B
-shape, batch 8, context 4352), `cpu_baseline` (the oracle
+shape, batch 8, context 4352), `gemm_at_scale` (the tiled GEMM of the same
+512-row passes against the dense bf16 MFMA peak), `cpu_baseline` (the oracle
 on the host cores on a bounded sample), AR tokens/s on the same kernels.
 """
 import argparse
@@ -42,6 +43,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
+MFMA_BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16
 # sources the GEMM kernel is compiled from (the traffic summary names their hash)
 GEMM_SRCS = [os.path.join(ROOT, "paper_2606_20543_amd", "csrc", f)
              for f in ("kernels_gemm.hip", "tiles.h", "ssd_internal.h")]
@@ -202,14 +204,17 @@ def heads_rate(ssd, model, shape, sc, prefix, d_prefix, steps, planted_ms):
             "passes_per_image": st.passes, "steps": steps, "acceptance_random_heads": st.accepted / max(st.proposed, 1)}
 
 
-def attention_at_scale(ssd, rounds=5):
-    """The attention kernel on its own bytes where attention is large: the 8B
-    shape (32 query / 8 KV heads of 128, GQA 4) with 8 sequences verifying
-    64-token blocks at context 4352 (the last row of a 64x64 image after a
-    256-token prompt: 4288 cached positions).  One layer of that model is
-    enough (attention does not depend on the others); per-launch events on the
-    library's stream give the kernel time, and the algorithmic bytes are the
-    KV read and the q/o traffic."""
+def at_scale(ssd, rounds=5):
+    """Kernels at the 8B shape (32 query / 8 KV heads of 128, GQA 4, MLP 14336,
+    32768 image codes) with 8 sequences verifying 64-token blocks at context
+    4352 (the last row of a 64x64 image after a 256-token prompt: 4288 cached
+    positions).  One layer of that model is enough (no kernel depends on the
+    others); per-launch events on the library's stream give the kernel times.
+    `attention_at_scale`: the attention kernel on its own bytes (the KV read
+    and the q/o traffic).  `gemm_at_scale`: the projections of those 512-row
+    passes, which run on the tiled GEMM and are bound by the matrix cores:
+    algorithmic FLOPs 2*M*N*K against the dense bf16 peak (the two activation
+    planes double what the MFMAs issue)."""
     import dataclasses
     import synth
     shape = dataclasses.replace(synth.M8B, n_layers=1)
@@ -239,10 +244,33 @@ def attention_at_scale(ssd, rounds=5):
         ssd.ssd_free_model(model)
     ms, n, by = prof["attention"]
     gbs = by / (ms / 1e3) / 1e9
-    return {"shape": "8B: 32q/8kv heads x 128, batch 8, 64-token blocks, context 4352", "bound": "hbm",
-            "achieved": gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": gbs / HBM_PEAK_GBS, "launches": n,
-            "ms_per_launch": ms / n, "bytes_per_launch": by / n,
-            "timing": "dispatch-timestamp events around each attention launch"}
+    att = {"shape": "8B: 32q/8kv heads x 128, batch 8, 64-token blocks, context 4352", "bound": "hbm",
+           "achieved": gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": gbs / HBM_PEAK_GBS, "launches": n,
+           "ms_per_launch": ms / n, "bytes_per_launch": by / n,
+           "timing": "dispatch-timestamp events around each attention launch"}
+    d, D, M = shape.d_model, shape.head_dim, B * K
+    nk = {"qkv": ((shape.n_heads + 2 * shape.n_kv_heads) * D, d), "o_proj": (d, shape.n_heads * D),
+          "gate_up": (2 * shape.d_ff, d), "down": (d, shape.d_ff), "lm_head": (shape.v_img, d)}
+    classes, tot_f, tot_ms = {}, 0.0, 0.0
+    for c, (N, Kd) in nk.items():
+        cms, cn, _ = prof[c]
+        if not cn:
+            continue
+        f = 2.0 * M * N * Kd * cn
+        classes[c] = {"N": N, "K": Kd, "ms_per_call": cms / cn, "tflops": f / (cms / 1e3) / 1e12}
+        tot_f += f
+        tot_ms += cms
+    tf = tot_f / (tot_ms / 1e3) / 1e12
+    gemm = {"shape": "8B projections at M = 512 rows (batch 8 x 64-token blocks)", "kernel": "gemm_tile_kernel",
+            "bound": "mfma", "achieved": tf, "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+            "frac": tf / MFMA_BF16_PEAK_TFLOPS, "issued_frac": 2 * tf / MFMA_BF16_PEAK_TFLOPS, "classes": classes,
+            "timing": "dispatch-timestamp events around each GEMM launch (one per projection per pass)"}
+    return {"attention_at_scale": att, "gemm_at_scale": gemm}
+
+
+def attention_at_scale(ssd):
+    """The attention entry of at_scale alone."""
+    return at_scale(ssd)["attention_at_scale"]
 
 
 def gemm_source_hash():
@@ -537,8 +565,8 @@ def main():
     ssd.ssd_free_model(model)
     model = None
     if not args.no_attn_scale:
-        log("[bench] attention at the 8B shape, context 4352")
-        result["attention_at_scale"] = attention_at_scale(ssd)
+        log("[bench] attention and the tiled GEMMs at the 8B shape, context 4352")
+        result.update(at_scale(ssd))
     if f_n > 0:
         # the single-launch pass carries the weight stream: it is the kernel the roofline is about
         result["roofline"] = dict(result["forward_launch"], traffic=None,
