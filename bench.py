@@ -410,8 +410,9 @@ def main():
                     help="only run a plain device copy of this size (PMC byte-counter calibration) and exit")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(f"bench.py: this build runs on exactly one GPU (asked for {args.gpus}); the verify path "
-              "shards by independent images, see DESIGN.md", file=sys.stderr)
+        print(f"bench.py: measures one GPU only (asked for {args.gpus}); the verify path shards by "
+              "independent images (one process per GPU, each with a full weight replica), so a "
+              "multi-GPU figure is that many independent one-GPU runs", file=sys.stderr)
         sys.exit(2)
 
     if args.copy_calibration_mib:

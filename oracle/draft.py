@@ -13,7 +13,7 @@ and the draft token is the argmax of the backbone's own output layer on the
 predicted state, GenHead(RMSNorm(h_hat)) -- the backbone's final norm and LM
 head, restricted to the image codes as everywhere here.
 
-Readings (listed in the design doc): the head's RMSNorm has a gain vector g of its
+Readings where the paper leaves details open: the head's RMSNorm has a gain vector g of its
 own (the paper does not name the norm's parameters; the backbone's norms carry
 gains) and the backbone's epsilon; m is a free size (the paper's 134.2 M
 parameters per head at d = 4096 give m = 2d); the draft distribution a rule-(C)

@@ -10,7 +10,7 @@ last layer's pre-norm hidden state h_pre, and the GenHead output layer; the
 SwiGLU form W2(silu(W1 z) * W3 z) is the one Eq. 2 writes out.
 
 The paper does not print the backbone's equations; this is the standard
-LLaMA-style block its backbones share (readings, all listed in the design doc):
+LLaMA-style block its backbones share (these readings fill in what it leaves open):
 pre-RMSNorm (eps 1e-5), rotary embedding on raster positions (rotate-half
 pairing, theta 1e4), causal softmax attention with 1/sqrt(D) scaling and
 grouped KV heads (query head h uses KV head h // (Hq/Hkv)), SwiGLU MLP, no

@@ -2,8 +2,9 @@
 host code inside libssd.so, called here through its C++ symbols).
 
 Every plan must tile its problem exactly (feature blocks x block width = N,
-splits x chunks x chunk width = K), keep the tiled kernel's pipeline depth a
-divisor of each split's stage count, and fit the workspaces that sessions
+splits x chunks x chunk width = K), give the tiled kernel's pipeline a stage
+count it runs (a multiple of the depth for depths 2 and 4, at least two
+stages for depth 3), and fit the workspaces that sessions
 and draft heads size once, at creation, by planning a fixed set of row
 counts: a plan for any row count must need no more split-K partials,
 arrival counters or per-row x^2 parts than the largest of that set, or a
@@ -75,7 +76,12 @@ def test_plans_tile_their_problem(planner, model):
                 assert p.NT in (2, 4) and p.bn == 32 * p.NT and p.n_fb * p.bn == N, where
                 assert p.m_tiles == (M + TILE_ROWS - 1) // TILE_ROWS, where
                 assert p.kchunks * p.S * TILE_KT == K, where
-                assert p.depth in (2, 4) and p.kchunks % p.depth == 0, where
+                # depth 3 (128-feature tiles): any count of at least two stages;
+                # depths 2 and 4 run whole groups of stages per trip
+                if p.depth == 3:
+                    assert p.NT == 4 and p.kchunks >= 2, where
+                else:
+                    assert p.depth in (2, 4) and p.kchunks % p.depth == 0, where
                 if p.S > 1:
                     assert p.n_fb * p.m_tiles * p.S < 512, where  # splits stop once the grid fills the CUs
             else:
@@ -100,17 +106,18 @@ def test_workspace_classes_bound_every_row_count(planner, model):
 
 
 def test_tiled_plan_choices(planner):
-    """The measured choices: 128-feature tiles where they make at least 160
-    workgroups, 64-feature tiles with four pipeline stages otherwise, K split
-    until the grid reaches 256 workgroups, streaming launches up to 64 rows."""
+    """The measured choices: 128-feature tiles (three weight stages) where they
+    make at least 160 workgroups, 64-feature tiles with four pipeline stages
+    otherwise, K split until the grid reaches 256 workgroups, streaming
+    launches up to 64 rows."""
     plan, _ = planner
     m = synth.M8B
     gu = plan(512, 2 * m.d_ff, m.d_model)  # 224 x 4 = 896 tiles
-    assert (gu.tile, gu.NT, gu.S, gu.depth) == (1, 4, 1, 2)
+    assert (gu.tile, gu.NT, gu.S, gu.depth) == (1, 4, 1, 3)
     dn = plan(512, m.d_model, m.d_ff)  # 32 x 4 = 128 < 160: 64-feature tiles, 256 workgroups
     assert (dn.tile, dn.NT, dn.S, dn.depth) == (1, 2, 1, 4)
     qkv = plan(512, (m.n_heads + 2 * m.n_kv_heads) * m.head_dim, m.d_model)  # 48 x 4 = 192 tiles, split in 2
-    assert (qkv.tile, qkv.NT, qkv.S) == (1, 4, 2)
+    assert (qkv.tile, qkv.NT, qkv.S, qkv.depth) == (1, 4, 2, 3)
     o1 = plan(256, synth.M1B.d_model, synth.M1B.d_model)  # 32 x 2 tiles of 64 features: 4 splits
     assert (o1.tile, o1.NT, o1.S) == (1, 2, 4)
     for M in (1, 24, 48, 64):
