@@ -20,7 +20,8 @@ stays within seconds.  Cases:
   1B width, batch 4, 64-token prompt and a 64-token block (M = 256, prefill
       and verify): tiled GEMMs whose K range is split over workgroups to
       fill the CUs (O and down projections in 4 splits, QKV in 2), rule (A),
-      2 rounds + commit
+      2 rounds + commit; the same block and a 24-token one with the XCD-local
+      reductions switched off (device-scope fences)
 """
 import dataclasses
 
@@ -134,3 +135,18 @@ def test_1b_width_b4_context_1088_rule_c(pair1):
 
 def test_1b_width_b4_block64_split_tiles(pair1):
     _greedy_block(pair1, W1, B=4, P=64, K=64, rounds=2, keep=0.6, seed_stream=15)
+
+
+def test_1b_width_fenced_reductions(monkeypatch):
+    """The same 256-row block, and a 24-token one, on a model created with the
+    XCD-local workgroup mapping switched off (SSD_NO_XCD_LOCAL=1): every
+    split-K and key-chunk reduction then publishes its partials through
+    device-scope fences instead of one XCD's L2."""
+    monkeypatch.setenv("SSD_NO_XCD_LOCAL", "1")
+    pair = _pair(W1, "1B-width 2-layer model, fenced reductions")
+    monkeypatch.delenv("SSD_NO_XCD_LOCAL")
+    try:
+        _greedy_block(pair, W1, B=4, P=64, K=64, rounds=1, keep=0.6, seed_stream=16)
+        _greedy_block(pair, W1, B=1, P=64, K=24, rounds=2, keep=0.6, seed_stream=17)
+    finally:
+        pair.close()
