@@ -745,9 +745,8 @@ GemmPlan gemm_plan_bf16(int M, int N, int K, int xcd) {
   if (M > 64 && K % (2 * TILE_KT) == 0 && N % 64 == 0 && (size_t)N * K * 2 < (1ull << 31)) {
     // 128-feature tiles wherever they give at least 160 workgroups (measured
     // on the 8B and 1B shapes: up to 35 % faster than 64-feature tiles
-    // there, slower on grids that leave CUs idle); then K splits (halving
-    // the stages per split, whose count must stay even) until the grid has
-    // 256 workgroups
+    // there, slower on grids that leave CUs idle); then K splits until the
+    // grid has 256 workgroups
     const int mt = (M + TILE_ROWS - 1) / TILE_ROWS;
     const long w4 = (long)(N / 128) * mt;
     const bool four = N % 128 == 0 && w4 >= 160;
@@ -758,9 +757,14 @@ GemmPlan gemm_plan_bf16(int M, int N, int K, int xcd) {
     p.bn = 32 * p.NT;
     p.n_fb = N / p.bn;
     p.m_tiles = mt;
+    // the split: the smallest divisor of the stage count (at most 16, an
+    // even count of stages per split) that brings the grid to 256
+    // workgroups, else the largest such divisor (1B down projection at 128
+    // rows: 88 stages in 11 splits, 352 workgroups)
     p.S = 1;
     const int nst = K / TILE_KT;
-    while ((long)p.n_fb * mt * p.S < 256 && p.S < 8 && nst % (4 * p.S) == 0) p.S *= 2;
+    for (int s = 2; s <= 16 && (long)p.n_fb * mt * p.S < 256; ++s)
+      if (nst % s == 0 && (nst / s) % 2 == 0) p.S = s;
     p.KCB = TILE_KT / 32;
     p.kchunks = nst / p.S;
     // four-stage pipeline for 64-feature tiles (measured on the 8B shapes at
