@@ -162,16 +162,40 @@ __device__ int block_max_i(int v, SelShared& sh) {
 }
 
 // argmax with ties to the lowest index over row[0..V)
+// Lowest index among the maxima.  Thread t scans elements 4t + 1024 j .. +3
+// in ascending order (16-byte loads: each wave load is one contiguous 1 KiB
+// span); the reductions below keep the lower index among equal values, so
+// the result does not depend on how the elements are dealt to threads.
 __device__ int block_argmax(const float* row, int V, SelShared& sh) {
-  const int VPT = (V + NT_SEL - 1) / NT_SEL;
-  const int lo = threadIdx.x * VPT, hi = min(lo + VPT, V);
   float bv = -INFINITY;
   int bi = 0x7fffffff;
-  for (int v = lo; v < hi; ++v) {
-    float x = row[v];
-    if (x > bv || bi == 0x7fffffff) {
-      bv = x;
-      bi = v;
+  if ((V & 3) == 0 && (((uintptr_t)row) & 15) == 0) {
+    for (int v = threadIdx.x * 4; v < V; v += NT_SEL * 4) {
+      const float4 x = *(const float4*)(row + v);
+      if (x.x > bv || bi == 0x7fffffff) {
+        bv = x.x;
+        bi = v;
+      }
+      if (x.y > bv) {
+        bv = x.y;
+        bi = v + 1;
+      }
+      if (x.z > bv) {
+        bv = x.z;
+        bi = v + 2;
+      }
+      if (x.w > bv) {
+        bv = x.w;
+        bi = v + 3;
+      }
+    }
+  } else {
+    for (int v = threadIdx.x; v < V; v += NT_SEL) {
+      const float x = row[v];
+      if (x > bv || bi == 0x7fffffff) {
+        bv = x;
+        bi = v;
+      }
     }
   }
   for (int o = 32; o > 0; o >>= 1) {
