@@ -539,11 +539,21 @@ void truncate_finalize(const SelectArgs& a, int* f, hipStream_t st) {
 }
 
 // commit: carry <- logits row (b * rps + last); f += f_inc; drop the references of the committed positions
+// Workgroups (x, b): the carry row of sequence b is copied by all gridDim.x
+// workgroups of b in 16-byte vectors; workgroup 0 alone clears the reference
+// flags of the committed positions and advances the frontier.
 __global__ __launch_bounds__(256) void commit_kernel(int Vimg, const float* logits, int rps, int last, float* carry,
                                                      int* f, int f_inc, int* ref_flag, int ring) {
-  const int b = blockIdx.x;
+  const int b = blockIdx.y;
   const float* src = logits + ((size_t)b * rps + last) * Vimg;
-  for (int v = threadIdx.x; v < Vimg; v += 256) carry[(size_t)b * Vimg + v] = src[v];
+  float* dst = carry + (size_t)b * Vimg;
+  if ((Vimg & 3) == 0) {
+    for (int v = (blockIdx.x * 256 + threadIdx.x) * 4; v < Vimg; v += gridDim.x * 1024)
+      *(float4*)(dst + v) = *(const float4*)(src + v);
+  } else {
+    for (int v = blockIdx.x * 256 + threadIdx.x; v < Vimg; v += gridDim.x * 256) dst[v] = src[v];
+  }
+  if (blockIdx.x != 0) return;
   const int f0 = f[b];
   if (ref_flag)
     for (int k = threadIdx.x; k < f_inc && k < ring; k += 256) ref_flag[(size_t)b * ring + (f0 + k) % ring] = 0;
@@ -551,17 +561,22 @@ __global__ __launch_bounds__(256) void commit_kernel(int Vimg, const float* logi
   if (threadIdx.x == 0) f[b] = f0 + f_inc;
 }
 
+// workgroups per sequence: one per 1024 carry values, at most 16
+static int commit_groups(int Vimg) { return std::max(1, std::min(16, (Vimg + 1023) / 1024)); }
+
 void commit_update(int B, int K, int Vimg, const float* logits, float* carry, int* f, int* ref_flag, int ring,
                    hipStream_t st) {
   // K > 0: logits rows are [B][K], carry from row K-1, f += K.
   // K < 0: logits rows are [B][1] (last row only), f += -K.
   int rps = K > 0 ? K : 1, last = K > 0 ? K - 1 : 0, inc = K > 0 ? K : -K;
-  hipLaunchKernelGGL(commit_kernel, dim3(B), dim3(256), 0, st, Vimg, logits, rps, last, carry, f, inc, ref_flag, ring);
+  hipLaunchKernelGGL(commit_kernel, dim3(commit_groups(Vimg), B), dim3(256), 0, st, Vimg, logits, rps, last, carry, f,
+                     inc, ref_flag, ring);
 }
 
 void commit_prefix(int B, int rps, int Kc, int Vimg, const float* logits, float* carry, int* f, int* ref_flag,
                    int ring, hipStream_t st) {
-  hipLaunchKernelGGL(commit_kernel, dim3(B), dim3(256), 0, st, Vimg, logits, rps, Kc - 1, carry, f, Kc, ref_flag, ring);
+  hipLaunchKernelGGL(commit_kernel, dim3(commit_groups(Vimg), B), dim3(256), 0, st, Vimg, logits, rps, Kc - 1, carry,
+                     f, Kc, ref_flag, ring);
 }
 
 // Classifier-free guidance: guided logits l_u + w (l_c - l_u) of each image b
