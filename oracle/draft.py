@@ -58,11 +58,8 @@ def f_phi(head, h, e, eps):
     """Eq. 2 on rows: h, e (R, d) -> predicted hidden states h_hat (R, d)."""
     z = np.concatenate([h, e], axis=-1)
     u = z @ head.w0.T
-    r = M.rms_inv(u, eps)[..., None]
-    gu = head.g * u
-    a = (gu @ head.w1.T) * r
-    b = (gu @ head.w3.T) * r
-    return u + (M.silu(a) * b) @ head.w2.T
+    n = M.rms_norm(u, head.g, eps)
+    return u + (M.silu(n @ head.w1.T) * (n @ head.w3.T)) @ head.w2.T
 
 
 def argmax_lowest(x):
@@ -75,5 +72,5 @@ def draft(model, head, h, tokens):
     the same positions): (image-code indices (R,), logits (R, V_img))."""
     e = model.tok_emb[np.asarray(tokens, dtype=np.int64)]
     hh = f_phi(head, np.asarray(h, dtype=np.float64), e, model.cfg.rms_eps)
-    logits = ((model.final_norm * hh) @ model.lm_img.T) * M.rms_inv(hh, model.cfg.rms_eps)[..., None]
+    logits = M.rms_norm(hh, model.final_norm, model.cfg.rms_eps) @ model.lm_img.T
     return argmax_lowest(logits), logits

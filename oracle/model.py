@@ -22,8 +22,9 @@ fixes no arithmetic precision; its memory figures imply bf16 weights.  Here
 the stored state is bf16 and the transient activations are not rounded:
   * weights and the KV cache hold bf16 values: k is rounded after the rotary
     embedding, v after its projection (rho = round-to-nearest-even to bf16);
-  * a linear layer after an RMSNorm computes (g * x) @ W^T / rms(x), i.e. the
-    per-row 1/rms(x) scale is applied to the product;
+  * RMSNorm is the plain definition n = g * x / sqrt(mean(x^2) + eps), and a
+    linear layer after it is n @ W^T (a kernel may apply the per-row 1/rms
+    after the product instead; the two agree up to rounding);
   * everything else (residual stream, q, attention weights and output, the
     SwiGLU product, logits) stays unrounded float64.
 Rounding activations to bf16 as well would make the comparison meaningless
@@ -33,8 +34,17 @@ relative change of the input then moves the 24-layer model's logits by
 
 Pins: tests/test_oracle_model.py -- closed-form special cases (single key,
 zero residual branches, rotary rotation), causality, batched block == one
-token at a time, cached == uncached recompute, shift invariance of rotary
-attention, GQA == MHA with duplicated KV heads, batch-row independence.
+token at a time, cached == uncached recompute, relative-position property of
+the rotation, GQA == MHA with duplicated KV heads, batch-row independence;
+tests/test_oracle_attention_core.py -- attention weights of a one-head model
+in closed form (scores a trigonometric function of the query-key distance:
+rotation of q and k at their raster positions, the rotary base, 1/sqrt(D),
+the softmax), in the first block and in a later block over a cache, and the
+whole forward pass against a textbook block written with torch's own
+attention routine and complex-number rotation.
+
+This module is test infrastructure: only the tests, the smoke check and the
+benchmark's CPU baseline use it.
 """
 
 from dataclasses import dataclass
@@ -143,6 +153,11 @@ def rms_inv(x, eps):
     return 1.0 / np.sqrt(np.mean(x * x, axis=-1) + eps)
 
 
+def rms_norm(x, g, eps):
+    """RMSNorm over the last axis: g * x / sqrt(mean(x^2) + eps)."""
+    return g * x * rms_inv(x, eps)[..., None]
+
+
 def rope(x, pos, inv_freq):
     """Rotate-half rotary embedding. x: (B, K, H, D); pos: (B, K) absolute positions."""
     half = x.shape[-1] // 2
@@ -178,11 +193,10 @@ def forward(model, cache, tokens, start):
     x = model.tok_emb[tokens]  # (B, K, d)
     for l, W in enumerate(model.layers):
         # attention block
-        r1 = rms_inv(x, cfg.rms_eps)[..., None]
-        a = W["attn_norm"] * x
-        q = ((a @ W["wq"].T) * r1).reshape(B, K, Hq, D)
-        k = ((a @ W["wk"].T) * r1).reshape(B, K, Hkv, D)
-        v = ((a @ W["wv"].T) * r1).reshape(B, K, Hkv, D)
+        n1 = rms_norm(x, W["attn_norm"], cfg.rms_eps)
+        q = (n1 @ W["wq"].T).reshape(B, K, Hq, D)
+        k = (n1 @ W["wk"].T).reshape(B, K, Hkv, D)
+        v = (n1 @ W["wv"].T).reshape(B, K, Hkv, D)
         q = rope(q, pos, model.inv_freq)
         k = rho(rope(k, pos, model.inv_freq))
         v = rho(v)
@@ -206,15 +220,11 @@ def forward(model, cache, tokens, start):
         o = o.reshape(B, K, Hq * D)
         x = x + o @ W["wo"].T
         # MLP block
-        r2 = rms_inv(x, cfg.rms_eps)[..., None]
-        bb = W["mlp_norm"] * x
-        gate = (bb @ W["w1"].T) * r2
-        up = (bb @ W["w3"].T) * r2
-        hdn = silu(gate) * up
+        n2 = rms_norm(x, W["mlp_norm"], cfg.rms_eps)
+        hdn = silu(n2 @ W["w1"].T) * (n2 @ W["w3"].T)
         x = x + hdn @ W["w2"].T
     h_pre = x
-    rf = rms_inv(x, cfg.rms_eps)[..., None]
-    logits = ((model.final_norm * x) @ model.lm_img.T) * rf
+    logits = rms_norm(x, model.final_norm, cfg.rms_eps) @ model.lm_img.T
     return logits, h_pre
 
 
