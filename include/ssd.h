@@ -20,7 +20,10 @@
  *  - Pointers to arrays may be host or device memory (HIP unified addressing
  *    decides).  Work is enqueued on the object's HIP stream; when any output
  *    array is host memory the call synchronizes the stream before returning,
- *    otherwise it returns without synchronizing.
+ *    otherwise it returns without synchronizing.  A session runs on the
+ *    stream given to ssd_prefill (the model's if NULL); an image decode on the
+ *    stream of its call (the model's if NULL); the model's own stream is the
+ *    one given to ssd_init_model and is never replaced.
  *  - The caller owns every array it passes; the library owns the device
  *    weights, the KV cache and all workspaces of a model/session.
  *  - Token ids are vocabulary ids.  Image codes occupy [img_lo, img_hi);
@@ -220,6 +223,18 @@ ssd_status ssd_session_set_cfg(ssd_session* sess, float weight);
  * verify block is scored and corrected in the same pass (the causal mask lets
  * it see the committed block).  Decisions are those of the separate passes;
  * ssd_stats.passes counts the backbone passes actually run.
+ * truncate = 1 replaces the schedule by strict greedy verification, the
+ * exactness-preserving decode the paper contrasts its own with (Sec. 3.3
+ * "Verification as Auto Correction"; it equals greedy AR decoding): blocks of
+ * trunc_block raster positions, the first the pending token (the argmax of the
+ * carry, already chosen) and the rest the drafts of the next positions; the
+ * leading run of drafts equal to the argmax of their scoring logits is
+ * accepted, the frontier advances past the pending token and that run, and the
+ * argmax at the first mismatch (or after the block) is the next pending token.
+ * The pass count then depends on the acceptance.  It needs rule A, cfg = 0,
+ * eol = 0 and planted drafts; k_h, h_rounds, k_v, b/i_rounds and
+ * separate_commit are ignored.  stats->proposed counts the drafts tested (the
+ * accepted ones and the first mismatch of each pass).
  */
 typedef struct {
   int32_t grid_h, grid_w;
@@ -233,6 +248,8 @@ typedef struct {
   int32_t eol_id;    /* end-of-line vocabulary id (eol = 1) */
   int32_t separate_commit; /* 0: a commit pass and the verify round right after it run as one pass;
                               1: one backbone pass per plan step */
+  int32_t truncate;        /* 0: the schedule above; 1: strict greedy verification decode */
+  int32_t trunc_block;     /* truncate = 1: positions per block (pending token + drafts), >= 2 */
 } ssd_schedule;
 
 typedef struct {
@@ -240,6 +257,12 @@ typedef struct {
   int64_t verify_rounds; /* verify passes */
   int64_t accepted;      /* accepted positions summed over verify rounds and sequences */
   int64_t proposed;      /* verified positions summed over verify rounds and sequences */
+  /* the same split by the round of the block: index j counts the (j+1)-th verify
+     round since the positions were drafted (rounds past the 8th are added to
+     index 7); index 0 is round-1 acceptance.  Strict decodes count under 0. */
+  int64_t accepted_round[8];
+  int64_t proposed_round[8];
+  int64_t wall_ns;       /* host wall-clock time of the call, nanoseconds */
 } ssd_stats;
 
 /*
@@ -253,6 +276,34 @@ typedef struct {
 ssd_status ssd_decode_image(ssd_model* model, const ssd_schedule* sched, int32_t B, int32_t P,
                             const int32_t* prefix, const int32_t* drafts, const float* draft_logits,
                             int32_t* out_tokens, ssd_stats* stats, void* stream);
+
+/*
+ * Planted drafts at a controlled acceptance (a measurement input; the paper's
+ * trained heads are not available).  Runs the decode ssd_decode_image would
+ * run for `sched` (the same passes and decisions, the strict decode too) with
+ * drafts made on the fly: right before the first verify round of a block, its
+ * draft positions are filled left to right, position x with a_x, the greedy
+ * argmax (lowest code among equal maxima) of the backbone's logits for x given
+ * the committed context and the block's earlier drafts, if keep[b][x] != 0,
+ * else with the code repl[b][x] + (repl[b][x] >= a_x), a uniformly drawn code
+ * other than a_x when repl is uniform over [0, V_img - 1).  Each a_x comes
+ * from a single-position forward pass whose KV slot the verify pass then
+ * overwrites; under rule A a kept draft is accepted in its first round unless
+ * the block pass, which adds in another order, moves the argmax (near-equal
+ * top logits only).  Strict decodes plant only what a pass tests: the leading
+ * kept drafts and the first replaced one.
+ * keep [B][H][W] uint8, repl [B][H][W] int32 (image-code indices, not ids),
+ * host or device.  drafts_out [B][H][W] receives the planted draft of every
+ * position (vocabulary ids; positions never drafted hold repl + img_lo): given
+ * to ssd_decode_image as `drafts` with the same schedule it reproduces this
+ * call's tokens, counts and passes.  out_tokens and stats as for
+ * ssd_decode_image; stats->passes leaves the planting passes out.  Guidance,
+ * the end-of-line layout and draft logits are not available here
+ * (SSD_E_INVAL); other errors as for ssd_decode_image.
+ */
+ssd_status ssd_plant_image(ssd_model* model, const ssd_schedule* sched, int32_t B, int32_t P,
+                           const int32_t* prefix, const uint8_t* keep, const int32_t* repl, int32_t* drafts_out,
+                           int32_t* out_tokens, ssd_stats* stats, void* stream);
 
 /*
  * Measurement hook.  enable = 1 starts recording a HIP event pair around every

@@ -251,16 +251,24 @@ def ar_decode_eol(model, prefix, H, W, eol_id):
     return img, s.passes
 
 
-def decode_truncate(model, prefix, drafts, K):
+def decode_truncate(model, prefix, drafts, K, plant=None, stats=None):
     """Exact greedy speculative decoding of len(drafts[b]) image tokens per
     sequence with blocks of K positions ([pending, K-1 drafts]); sequences are
-    decoded one at a time.  Returns (tokens (B, N), passes)."""
+    decoded one at a time.  Returns (tokens (B, N), passes).
+
+    plant -- optional (keep (B, N) bool, repl (B, N) codes): before each pass the
+             drafts it tests are planted left to right (planted_draft) against
+             the committed tokens and the drafts before them, stopping after the
+             first replaced one; `drafts` is then overwritten with the planted
+             table.  stats (a dict) receives accepted / proposed (drafts tested:
+             the accepted run and the first mismatch of each pass)."""
     prefix = np.asarray(prefix)
-    drafts = np.asarray(drafts, dtype=np.int64)
+    drafts = np.array(drafts, dtype=np.int64)
     B, N = drafts.shape
     P = prefix.shape[1]
     out = np.zeros((B, N), dtype=np.int64)
     passes = 0
+    acc_tot = prop_tot = 0
     for b in range(B):
         s = prefill(model, prefix[b:b + 1], P + N + K)
         pending = R.argmax_lowest(s.carry[0])
@@ -270,21 +278,47 @@ def decode_truncate(model, prefix, drafts, K):
             if done + 1 == N:
                 break
             k_blk = min(K, N - done)
+            if plant is not None:
+                before = list(out[b, :done + 1])
+                for x in range(done + 1, done + k_blk):
+                    t, _ = planted_draft(model, prefix[b], before, plant[0][b][x], plant[1][b][x])
+                    drafts[b, x] = t
+                    before.append(t)
+                    if not plant[0][b][x]:
+                        break
             blk = np.concatenate([[pending], drafts[b, done + 1:done + k_blk]])[None, :]
             n_acc, pend = truncate_step(s, blk, 1)
             n = int(n_acc[0])
+            acc_tot += n
+            prop_tot += n + (1 if n < k_blk - 1 else 0)
             out[b, done + 1:done + 1 + n] = blk[0, 1:1 + n]
             done += 1 + n
             pending = int(pend[0])
             if done >= N:
                 break
         passes += s.passes
+    if stats is not None:
+        stats.update(accepted=acc_tot, proposed=prop_tot, planted=drafts)
     return out, passes
+
+
+def planted_draft(model, prefix_row, before, keep, repl):
+    """One planted draft (a measurement input, not the method): a = the greedy
+    argmax of the backbone's logits for the next position given the prompt and
+    the image tokens `before` (everything chosen or drafted ahead of it), from a
+    plain no-cache forward pass; the draft is a if keep, else the code
+    repl + (repl >= a) (repl uniform over [0, V_img - 1) gives a uniform other
+    code).  Returns (draft, a) as image-code indices."""
+    toks = np.concatenate([np.asarray(prefix_row, dtype=np.int64),
+                           np.asarray(before, dtype=np.int64) + model.cfg.img_lo])[None, :]
+    logits, _ = M.forward_nocache(model, toks)
+    a = R.argmax_lowest(logits[0, -1])
+    return (a if keep else int(repl) + (int(repl) >= a)), a
 
 
 def decode_image(model, prefix, H, W, drafts, rule=R.RULE_GREEDY, seed=0, temperature=1.0, top_k=0,
                  k_h=5, h_rounds=1, k_v=1, b=2, i=0, q_table=None, trace=None, guide=None, heads=None,
-                 eol_id=None):
+                 eol_id=None, plant=None):
     """Decode one image per sequence under the SSD schedule, with planted drafts
     or drafted by spatial heads (Sec. 3.3).
 
@@ -306,6 +340,10 @@ def decode_image(model, prefix, H, W, drafts, rule=R.RULE_GREEDY, seed=0, temper
     q_table -- optional (B, H, W, V_img) draft logits (rule C reference for the
                first round of each position); None = point masses at the drafts
     trace   -- optional list collecting (op, accept, count, logits) per verify
+    plant   -- optional (keep (B, H, W) bool, repl (B, H, W) codes): drafts are
+               planted at each draft op, left to right (planted_draft), against
+               the tokens chosen so far; stats["planted"] then holds the table
+               (B, H, W) of planted drafts
     Returns (tokens (B, H, W), stats dict).
     """
     cfg = model.cfg
@@ -336,13 +374,31 @@ def decode_image(model, prefix, H, W, drafts, rule=R.RULE_GREEDY, seed=0, temper
     def seq_of(p):  # sequence position (after the prompt) of image index p
         return (np.asarray(p) // W) * RW + np.asarray(p) % W
     refs = [dict() for _ in range(B)]  # image index -> reference logits
-    stats = {"accepted": 0, "proposed": 0, "verify_rounds": 0}
+    stats = {"accepted": 0, "proposed": 0, "verify_rounds": 0, "accepted_first": 0, "proposed_first": 0}
+    if plant is not None:
+        assert heads is None and not eol and guide is None
+        keep = np.asarray(plant[0]).reshape(B, N).astype(bool)
+        repl = np.asarray(plant[1]).reshape(B, N)
+        stats["planted"] = repl.copy()
+    fresh = set()  # image indexes drafted and not yet verified
     for op in ops:
         if op[0] == "prefill":
             sess = prefill(model, prefix, P + NS, guide)
             if heads is not None:
                 hs[:, 0] = sess.h_carry[:B]
         elif op[0] in ("draft_h", "draft_v"):
+            if op[0] == "draft_h":
+                new_idx = [op[1] + j for j in range(1, op[2] + 1)]
+            else:
+                new_idx = [x for r in range(op[1] + 1, op[1] + op[2] + 1) for x in range(r * W, (r + 1) * W)]
+            fresh.update(new_idx)
+            if plant is not None:
+                for x in new_idx:  # left to right: each draft sees the ones before it
+                    for bb in range(B):
+                        t, _ = planted_draft(model, prefix[bb], work[bb, :x], keep[bb, x], repl[bb, x])
+                        work[bb, x] = t
+                        stats["planted"][bb, x] = t
+                continue
             if heads is None:
                 continue
             if op[0] == "draft_h":
@@ -394,6 +450,12 @@ def decode_image(model, prefix, H, W, drafts, rule=R.RULE_GREEDY, seed=0, temper
             n_eol = sum(1 for k in range(K) if eol and (start + k) % RW == W)
             stats["proposed"] += B * (K - nf - n_eol)
             stats["verify_rounds"] += 1
+            # first round of freshly drafted positions (image indexes; eol off here)
+            first = [k for k in range(nf, K) if (start + k) in fresh]
+            if first and not eol:
+                stats["accepted_first"] += int(acc[:, first].sum())
+                stats["proposed_first"] += B * len(first)
+                fresh.difference_update(start + k for k in first)
             if trace is not None:
                 trace.append((op, acc, cnt, logits, new))
         elif op[0] == "commit":
@@ -411,5 +473,7 @@ def decode_image(model, prefix, H, W, drafts, rule=R.RULE_GREEDY, seed=0, temper
                 for k in range(K):
                     refs[bb].pop(start + k, None)
     stats["passes"] = sess.passes
+    if plant is not None:
+        stats["planted"] = stats["planted"].reshape(B, H, W)
     assert sess.passes == S.n_passes(ops)
     return work.reshape(B, H, RW)[:, :, :W], stats

@@ -21,7 +21,7 @@ EXPORTED = [
     "ssd_init_model", "ssd_weights_numel", "ssd_free_model", "ssd_prefill", "ssd_free_session",
     "ssd_verify_step", "ssd_get_carry", "ssd_session_set_cfg", "ssd_decode_image", "ssd_profile", "ssd_profile_read", "ssd_last_error",
     "ssd_draft_head_numel", "ssd_draft_head_init", "ssd_draft_head_run", "ssd_free_draft_head",
-    "ssd_decode_image_heads",
+    "ssd_decode_image_heads", "ssd_plant_image",
 ]
 
 
@@ -50,12 +50,13 @@ class ssd_schedule(ctypes.Structure):
                 ("i_rounds", ctypes.c_int32), ("rule", ctypes.c_int32), ("top_k", ctypes.c_int32),
                 ("temperature", ctypes.c_double), ("seed", ctypes.c_uint64), ("cfg", ctypes.c_int32),
                 ("cfg_weight", ctypes.c_float), ("eol", ctypes.c_int32), ("eol_id", ctypes.c_int32),
-                ("separate_commit", ctypes.c_int32)]
+                ("separate_commit", ctypes.c_int32), ("truncate", ctypes.c_int32), ("trunc_block", ctypes.c_int32)]
 
 
 class ssd_stats(ctypes.Structure):
     _fields_ = [("passes", ctypes.c_int64), ("verify_rounds", ctypes.c_int64), ("accepted", ctypes.c_int64),
-                ("proposed", ctypes.c_int64)]
+                ("proposed", ctypes.c_int64), ("accepted_round", ctypes.c_int64 * 8),
+                ("proposed_round", ctypes.c_int64 * 8), ("wall_ns", ctypes.c_int64)]
 
 
 _lib = None
@@ -89,6 +90,8 @@ def lib():
         L.ssd_draft_head_init.argtypes = [vp, i32, vp, i32, ctypes.POINTER(vp)]
         L.ssd_draft_head_run.argtypes = [vp, i32, vp, vp, vp, vp]
         L.ssd_free_draft_head.argtypes = [vp]
+        L.ssd_plant_image.argtypes = [vp, ctypes.POINTER(ssd_schedule), i32, i32, vp, vp, vp, vp, vp,
+                                      ctypes.POINTER(ssd_stats), vp]
         L.ssd_decode_image_heads.argtypes = [vp, ctypes.POINTER(ssd_schedule), i32, i32, vp, ctypes.POINTER(vp), i32,
                                              ctypes.POINTER(vp), i32, vp, ctypes.POINTER(ssd_stats), vp]
         L.ssd_free_draft_head.restype = None
@@ -96,7 +99,7 @@ def lib():
         L.ssd_last_error.restype = ctypes.c_char_p
         for name in ("ssd_init_model", "ssd_prefill", "ssd_verify_step", "ssd_get_carry", "ssd_session_set_cfg",
                      "ssd_decode_image", "ssd_profile", "ssd_profile_read", "ssd_draft_head_init", "ssd_draft_head_run",
-                     "ssd_decode_image_heads"):
+                     "ssd_decode_image_heads", "ssd_plant_image"):
             getattr(L, name).restype = i32
         _lib = L
     return _lib
@@ -170,6 +173,14 @@ def ssd_decode_image(model, sched, B, P, prefix, drafts, out_tokens, draft_logit
     st = ssd_stats()
     _check(lib().ssd_decode_image(ctypes.c_void_p(model), ctypes.byref(sched), B, P, _ptr(prefix), _ptr(drafts),
                                   _ptr(draft_logits), _ptr(out_tokens), ctypes.byref(st), _ptr(stream)))
+    return st
+
+
+def ssd_plant_image(model, sched, B, P, prefix, keep, repl, drafts_out, out_tokens, stream=None):
+    """keep [B][H][W] uint8, repl [B][H][W] int32 image-code indices; fills drafts_out and out_tokens."""
+    st = ssd_stats()
+    _check(lib().ssd_plant_image(ctypes.c_void_p(model), ctypes.byref(sched), B, P, _ptr(prefix), _ptr(keep),
+                                 _ptr(repl), _ptr(drafts_out), _ptr(out_tokens), ctypes.byref(st), _ptr(stream)))
     return st
 
 

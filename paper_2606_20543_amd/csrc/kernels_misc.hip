@@ -723,4 +723,65 @@ void first_token(int B, int Vimg, int img_lo, const float* carry, int rule, int 
                      seed, f, out_abs, out_stride);
 }
 
+// The greedy argmax a of a logits row (lowest code among equal maxima) placed
+// at image index x = f[b] - P + pos_off of sequence b: with `keep` it is a
+// planted draft (a where keep[x] is set, else the other code
+// repl[x] + (repl[x] >= a)), without it the token itself (the pending token of
+// strict verification).  `active` (optional) gates sequences: an inactive one
+// is skipped, and a planted replacement (or x outside [0, x_end)) deactivates
+// it.  One workgroup per sequence.
+__global__ __launch_bounds__(NT_SEL) void place_argmax_kernel(PlaceArgs a) {
+  __shared__ SelShared sh;
+  const int b = blockIdx.x;
+  if (a.active && a.active[b] == 0) return;
+  const int x = a.f[b] - a.P + a.pos_off;
+  if (x < 0 || x >= a.x_end) {
+    if (a.active && threadIdx.x == 0) a.active[b] = 0;
+    return;
+  }
+  const int am = block_argmax(a.logits + (size_t)b * a.row_stride, a.Vimg, sh);
+  int t = am;
+  bool kept = true;
+  if (a.keep) {
+    kept = a.keep[(size_t)b * a.x_end + x] != 0;
+    if (!kept) {
+      const int r = a.repl[(size_t)b * a.x_end + x];
+      t = r + (r >= am ? 1 : 0);
+    }
+  }
+  if (threadIdx.x == 0) {
+    const int id = t + a.img_lo;
+    a.img[(size_t)b * a.img_stride + x] = id;
+    if (a.table) a.table[(size_t)b * a.x_end + x] = id;
+    if (a.next_tok) a.next_tok[b] = id;
+    if (a.active && !kept) a.active[b] = 0;
+  }
+}
+
+void place_argmax(const PlaceArgs& a, int B, hipStream_t st) {
+  hipLaunchKernelGGL(place_argmax_kernel, dim3(B), dim3(NT_SEL), 0, st, a);
+}
+
+// tok[b][k] = img[b][f[b] - P + k], k < K (blocks at per-sequence frontiers)
+__global__ __launch_bounds__(64) void gather_block_kernel(const int* img, int img_stride, const int* f, int P, int K,
+                                                          int* tok) {
+  const int b = blockIdx.x;
+  const int* src = img + (size_t)b * img_stride + (f[b] - P);
+  for (int k = threadIdx.x; k < K; k += 64) tok[(size_t)b * K + k] = src[k];
+}
+
+void gather_block(const int* img, int img_stride, const int* f, int P, int K, int B, int* tok, hipStream_t st) {
+  hipLaunchKernelGGL(gather_block_kernel, dim3(B), dim3(64), 0, st, img, img_stride, f, P, K, tok);
+}
+
+__global__ void add_i32_kernel(int* p, int n, int delta) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) p[i] += delta;
+}
+
+void add_i32(int* p, int n, int delta, hipStream_t st) {
+  if (n <= 0 || delta == 0) return;
+  hipLaunchKernelGGL(add_i32_kernel, dim3((n + 255) / 256), dim3(256), 0, st, p, n, delta);
+}
+
 }  // namespace ssd

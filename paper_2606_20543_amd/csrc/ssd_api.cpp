@@ -6,6 +6,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstdlib>
+#include <chrono>
 #include <cstring>
 #include <map>
 #include <string>
@@ -19,6 +20,10 @@ using namespace ssd;
 namespace {
 
 thread_local std::string g_err;
+
+// per-round accept counters of an image decode: the (j+1)-th verify round of a
+// block counts under j (rounds past the last counted under NCNT_ROUNDS - 1)
+constexpr int NCNT_ROUNDS = 8;
 
 ssd_status fail(ssd_status st, const char* fmt, ...) {
   char buf[512];
@@ -269,6 +274,12 @@ struct ssd_session {
   size_t hs_cap = 0;
   float* hsrc = nullptr; // head inputs of one draft step [B][W][d] and their tokens [B][W]
   int* tsrc = nullptr;
+  // planted drafts (ssd_plant_image): keep flags, replacement codes and the table out [B][H*W]
+  unsigned char* pkeep = nullptr;
+  int* prepl = nullptr;
+  int* ptab = nullptr;
+  int* pactive = nullptr;  // [B] sequences still planting (strict decode)
+  size_t plant_cap = 0;
 };
 
 namespace {
@@ -821,12 +832,12 @@ void size_workspaces(const Dims& dm, const ssd_model* m, int B, int P, int Kmax,
   }
 }
 
-ssd_status create_session(ssd_model* m, int B, int P, int Lmax_req, int Kmax, ssd_session** out) {
+ssd_status create_session(ssd_model* m, int B, int P, int Lmax_req, int Kmax, hipStream_t stream, ssd_session** out) {
   const Dims& dm = m->dm;
   auto* s = new ssd_session();
   s->m = m;
   s->dm = dm;
-  s->stream = m->stream;
+  s->stream = stream;
   s->B = B;
   s->Bi = B;
   s->P = P;
@@ -844,7 +855,7 @@ ssd_status create_session(ssd_model* m, int B, int P, int Lmax_req, int Kmax, ss
     s->d_f = s->mem.get<int>(B);
     s->tok = s->mem.get<int>(M);
     s->acc = s->mem.get<unsigned char>(M);
-    s->cnt = s->mem.get<int>(B);
+    s->cnt = s->mem.get<int>((size_t)NCNT_ROUNDS * B);  // [round of the block][B] in image decodes
     s->amax = s->mem.get<int>(M);
     s->x = s->mem.get<float>(M * dm.d);
     // activations: 4 bytes per element (fp32, or hi + lo bf16 planes)
@@ -1131,9 +1142,8 @@ ssd_status ssd_prefill(ssd_model* m, int32_t B, int32_t P, const int32_t* prefix
   }
   ssd_status cs = check_tokens_host(host.data(), host.size(), 0, m->dm.V, "prefix");
   if (cs != SSD_OK) return cs;
-  if (stream) m->stream = (hipStream_t)stream;
   ssd_session* s = nullptr;
-  ssd_status st = create_session(m, B, P, max_ctx, max_block, &s);
+  ssd_status st = create_session(m, B, P, max_ctx, max_block, stream ? (hipStream_t)stream : m->stream, &s);
   if (st != SSD_OK) return st;
   try {
     HIPCHK(hipMemcpyAsync(s->tok, host.data(), host.size() * 4, hipMemcpyHostToDevice, s->stream));
@@ -1634,6 +1644,7 @@ namespace {
 struct Op {
   int kind;  // 0 verify, 1 commit, 2 horizontal draft (src, K heads), 3 vertical draft (row src, K rows)
   int start, K, nf, rnd;
+  int rib;   // verify: rounds of this block before this one since it was drafted
 };
 
 // pass plan of one image (mirrors the schedule documented in ssd.h)
@@ -1644,7 +1655,7 @@ std::vector<Op> make_plan(int H, int W, int k_h, int h_rounds, int k_v, int b, i
   int rnd = 0;
   const int RW = eol ? W + 1 : W, tail = eol ? 1 : 0;
   auto verify = [&](int start, int K, int nf, int count) {
-    for (int c = 0; c < count; ++c) ops.push_back(Op{0, start, K, nf, rnd++});
+    for (int c = 0; c < count; ++c) ops.push_back(Op{0, start, K, nf, rnd++, c});
   };
   bool first = true;
   for (int s = 1; s < W;) {
@@ -1691,17 +1702,24 @@ struct DraftSource {
   int nh = 0;
   ssd_draft_head* const* vh = nullptr;
   int nv = 0;
+  // planting (ssd_plant_image): drafts made left to right against the decode's own argmax
+  const uint8_t* keep = nullptr;
+  const int32_t* repl = nullptr;
+  int32_t* table = nullptr;
 };
 
 ssd_status decode_impl(ssd_model* m, const ssd_schedule* sc, int32_t B, int32_t P, const int32_t* prefix,
                        const DraftSource& src, int32_t* out_tokens, ssd_stats* stats, void* stream) {
+  const auto t_call = std::chrono::steady_clock::now();
   const int32_t* drafts = src.drafts;
   const float* draft_logits = src.draft_logits;
   const bool heads = src.hh != nullptr || src.vh != nullptr;
+  const bool plant = src.keep != nullptr;
   if (m->poisoned) return fail(SSD_E_STATE, "model is poisoned by an earlier device error");
   const Dims& dm = m->dm;
   const int H = sc->grid_h, W = sc->grid_w;
   if (H < 1 || W < 1 || B < 1 || B >= (1 << 20) || P < 1) return fail(SSD_E_INVAL, "bad grid, batch or prefix size");
+  if ((int64_t)H * W >= (1 << 24)) return fail(SSD_E_INVAL, "image too large");
   if (sc->k_h < 1 || sc->h_rounds < 0 || sc->k_v < 1 || sc->b_rounds < 0 || sc->i_rounds < 0)
     return fail(SSD_E_INVAL, "bad schedule");
   if (sc->rule < SSD_GREEDY || sc->rule > SSD_ACCEPT_REJECT || !(sc->temperature > 0.0))
@@ -1713,19 +1731,31 @@ ssd_status decode_impl(ssd_model* m, const ssd_schedule* sc, int32_t B, int32_t 
   if (sc->eol != 0 && sc->eol != 1) return fail(SSD_E_INVAL, "eol must be 0 or 1");
   const bool eol = sc->eol == 1;
   if (eol && (sc->eol_id < 0 || sc->eol_id >= dm.V)) return fail(SSD_E_INVAL, "eol_id outside the vocabulary");
+  if (sc->truncate != 0 && sc->truncate != 1) return fail(SSD_E_INVAL, "truncate must be 0 or 1");
+  const bool trunc = sc->truncate == 1;
+  if (trunc) {
+    if (sc->rule != SSD_GREEDY) return fail(SSD_E_INVAL, "the strict decode needs rule SSD_GREEDY");
+    if (sc->cfg || eol || heads) return fail(SSD_E_INVAL, "the strict decode takes no guidance, row ends or heads");
+    if (sc->trunc_block < 2 || sc->trunc_block > 4096) return fail(SSD_E_INVAL, "trunc_block must be in [2, 4096]");
+  }
+  if (plant && (sc->cfg || eol || draft_logits || heads))
+    return fail(SSD_E_INVAL, "planting takes no guidance, row ends, draft logits or heads");
   const int N = H * W;
   const int RW = eol ? W + 1 : W;  // sequence positions per image row
-  const int NS = H * RW;           // sequence positions of the image
+  // working row of an image: its sequence positions, plus one block of slack
+  // for the strict decode (blocks past the last token read it)
+  const int NS = trunc ? N + sc->trunc_block : H * RW;
   const int Lmax = P + NS;
   if (Lmax >= (1 << 24)) return fail(SSD_E_INVAL, "image too large");
   if (!dm.bf16 && Lmax > 4096) return fail(SSD_E_INVAL, "fp32 models support P + image positions <= 4096");
-  std::vector<Op> ops = make_plan(H, W, sc->k_h, sc->h_rounds, sc->k_v, sc->b_rounds, sc->i_rounds, eol);
+  std::vector<Op> ops;
+  if (!trunc) ops = make_plan(H, W, sc->k_h, sc->h_rounds, sc->k_v, sc->b_rounds, sc->i_rounds, eol);
   if (sc->separate_commit != 0 && sc->separate_commit != 1) return fail(SSD_E_INVAL, "separate_commit must be 0 or 1");
   // fuse[i]: commit op i runs inside the pass of the verify round right after it
   // (adjacent block, nothing fixed at its start, no head drafting in between:
   // drafting needs the committed states first)
   std::vector<char> fuse(ops.size(), 0);
-  int Kmax = 1;
+  int Kmax = trunc ? sc->trunc_block : 1;
   int nverify = 0;
   for (size_t i = 0; i < ops.size(); ++i) {
     const Op& o = ops[i];
@@ -1757,21 +1787,37 @@ ssd_status decode_impl(ssd_model* m, const ssd_schedule* sc, int32_t B, int32_t 
   }
   if (nverify >= 65536) return fail(SSD_E_INVAL, "more than 65535 verify rounds");
   std::vector<int32_t> hpre((size_t)Bs * P), hdr((size_t)B * N, dm.img_lo);
+  std::vector<uint8_t> hkeep;
   if (hipMemcpy(hpre.data(), prefix, hpre.size() * 4, hipMemcpyDefault) != hipSuccess ||
-      (!heads && hipMemcpy(hdr.data(), drafts, hdr.size() * 4, hipMemcpyDefault) != hipSuccess)) {
+      (!heads && !plant && hipMemcpy(hdr.data(), drafts, hdr.size() * 4, hipMemcpyDefault) != hipSuccess)) {
     (void)hipGetLastError();
     return fail(SSD_E_INVAL, "prefix or drafts not readable");
+  }
+  if (plant) {
+    hkeep.resize((size_t)B * N);
+    if (hipMemcpy(hkeep.data(), src.keep, hkeep.size(), hipMemcpyDefault) != hipSuccess ||
+        hipMemcpy(hdr.data(), src.repl, hdr.size() * 4, hipMemcpyDefault) != hipSuccess) {
+      (void)hipGetLastError();
+      return fail(SSD_E_INVAL, "keep or repl not readable");
+    }
+    ssd_status rs = check_tokens_host(hdr.data(), hdr.size(), 0, dm.Vimg - 1, "repl");
+    if (rs != SSD_OK) return rs;
+    for (auto& v : hdr) v += dm.img_lo;  // the table before planting: the replacement codes as ids
   }
   ssd_status cs = check_tokens_host(hpre.data(), hpre.size(), 0, dm.V, "prefix");
   if (cs != SSD_OK) return cs;
   cs = check_tokens_host(hdr.data(), hdr.size(), dm.img_lo, dm.img_hi, "drafts");
   if (cs != SSD_OK) return cs;
-  if (eol) {  // the working table holds sequence positions: each row closed by its end-of-line token
-    std::vector<int32_t> seq((size_t)B * NS, sc->eol_id);
-    for (size_t r = 0; r < (size_t)B * H; ++r) std::memcpy(&seq[r * RW], &hdr[r * W], (size_t)W * 4);
+  if (eol || trunc) {  // the working table holds sequence positions (row ends, or the strict decode's slack)
+    std::vector<int32_t> seq((size_t)B * NS, eol ? sc->eol_id : dm.img_lo);
+    if (eol) {
+      for (size_t r = 0; r < (size_t)B * H; ++r) std::memcpy(&seq[r * RW], &hdr[r * W], (size_t)W * 4);
+    } else {
+      for (size_t b = 0; b < (size_t)B; ++b) std::memcpy(&seq[b * NS], &hdr[b * N], (size_t)N * 4);
+    }
     hdr.swap(seq);
   }
-  if (stream) m->stream = (hipStream_t)stream;
+  const hipStream_t call_st = stream ? (hipStream_t)stream : m->stream;
   // decode workspace, reused across calls of the same shape
   if (!m->dec || m->dec_B != Bs || m->dec_P != P || m->dec_L != Lmax || m->dec_K != Kmax) {
     if (m->dec) {
@@ -1780,7 +1826,7 @@ ssd_status decode_impl(ssd_model* m, const ssd_schedule* sc, int32_t B, int32_t 
       delete old;
     }
     ssd_session* s = nullptr;
-    ssd_status st = create_session(m, Bs, P, Lmax, Kmax, &s);
+    ssd_status st = create_session(m, Bs, P, Lmax, Kmax, call_st, &s);
     if (st != SSD_OK) return st;
     m->dec = s;
     m->dec_B = Bs;
@@ -1789,7 +1835,7 @@ ssd_status decode_impl(ssd_model* m, const ssd_schedule* sc, int32_t B, int32_t 
     m->dec_K = Kmax;
   }
   ssd_session* s = m->dec;
-  s->stream = m->stream;
+  s->stream = call_st;
   if (sc->cfg) {
     ssd_status gs = ssd_session_set_cfg(s, (float)sc->cfg_weight);
     if (gs != SSD_OK) return gs;
@@ -1799,6 +1845,9 @@ ssd_status decode_impl(ssd_model* m, const ssd_schedule* sc, int32_t B, int32_t 
   }
   hipStream_t st = s->stream;
   int64_t passes = 0, nv = 0, proposed = 0;
+  int64_t prop_round[NCNT_ROUNDS] = {0};
+  std::vector<int> hc((size_t)NCNT_ROUNDS * Bs, 0);  // accept counters [round][sequence]
+  int64_t acc_trunc = 0;
   try {
     if (s->img_cap < B * NS) {
       s->img = s->mem.get<int>((size_t)B * NS);
@@ -1815,13 +1864,28 @@ ssd_status decode_impl(ssd_model* m, const ssd_schedule* sc, int32_t B, int32_t 
       s->hsrc = s->mem.get<float>((size_t)B * W * dm.d);
       s->tsrc = s->mem.get<int>((size_t)B * W);
     }
+    if (plant) {
+      if (s->plant_cap < (size_t)B * N) {
+        s->pkeep = s->mem.get<unsigned char>((size_t)B * N);
+        s->prepl = s->mem.get<int>((size_t)B * N);
+        s->ptab = s->mem.get<int>((size_t)B * N);
+        s->pactive = s->mem.get<int>((size_t)B);
+        s->plant_cap = (size_t)B * N;
+      }
+      HIPCHK(hipMemcpyAsync(s->pkeep, hkeep.data(), hkeep.size(), hipMemcpyHostToDevice, st));
+      HIPCHK(hipMemcpy2DAsync(s->ptab, (size_t)N * 4, hdr.data(), (size_t)NS * 4, (size_t)N * 4, B,
+                              hipMemcpyHostToDevice, st));
+      HIPCHK(hipMemcpy2DAsync(s->prepl, (size_t)N * 4, hdr.data(), (size_t)NS * 4, (size_t)N * 4, B,
+                              hipMemcpyHostToDevice, st));
+      add_i32(s->prepl, B * N, -dm.img_lo, st);  // back to code indices
+    }
     HIPCHK(hipMemcpyAsync(s->img, hdr.data(), hdr.size() * 4, hipMemcpyHostToDevice, st));
     if (draft_logits)  // [B][H][W][V] into the sequence layout (end-of-line rows are never read)
       HIPCHK(hipMemcpy2DAsync(s->qtab, (size_t)RW * dm.Vimg * 4, draft_logits, (size_t)W * dm.Vimg * 4,
                               (size_t)W * dm.Vimg * 4, (size_t)B * H, hipMemcpyDefault, st));
     fill_u32((unsigned*)s->d_f, Bs, 0u, st);
     fill_u32((unsigned*)s->ref_flag, (size_t)Bs * s->ring, 0u, st);
-    fill_u32((unsigned*)s->cnt, Bs, 0u, st);
+    fill_u32((unsigned*)s->cnt, (size_t)NCNT_ROUNDS * Bs, 0u, st);
     for (int b = 0; b < Bs; ++b) s->f[b] = 0;
     HIPCHK(hipMemcpyAsync(s->tok, hpre.data(), hpre.size() * 4, hipMemcpyHostToDevice, st));
     prefill_pass(s);
@@ -1855,6 +1919,115 @@ ssd_status decode_impl(ssd_model* m, const ssd_schedule* sc, int32_t B, int32_t 
     a.amax = s->amax;
     a.eol_period = eol ? RW : 0;
     a.eol_base = P;
+    // planting: the argmax of a logits row placed as a planted draft
+    PlaceArgs pa{};
+    pa.row_stride = dm.Vimg;
+    pa.Vimg = dm.Vimg;
+    pa.img_lo = dm.img_lo;
+    pa.f = s->d_f;
+    pa.P = P;
+    pa.x_end = N;
+    pa.img = s->img;
+    pa.img_stride = NS;
+    pa.keep = s->pkeep;
+    pa.repl = s->prepl;
+    pa.table = s->ptab;
+    pa.next_tok = s->tok;
+    // Move every frontier by delta (device and host mirror): the single-position
+    // planting passes run at positions past the committed context.
+    auto shift_f = [&](int delta) {
+      add_i32(s->d_f, B, delta, st);
+      for (int b = 0; b < B; ++b) s->f[b] += delta;
+    };
+    if (trunc) {
+      // ---- strict greedy verification: blocks [pending, K-1 drafts] at each sequence's frontier ----
+      const int K = sc->trunc_block;
+      // the first pending token: the argmax of the prefill's carry (first_token above)
+      std::vector<int> done(B, 0), fh(B), cnt_h(B);
+      PlaceArgs pend{};
+      pend.logits = s->carry;
+      pend.row_stride = dm.Vimg;
+      pend.Vimg = dm.Vimg;
+      pend.img_lo = dm.img_lo;
+      pend.f = s->d_f;
+      pend.P = P;
+      pend.x_end = NS;
+      pend.img = s->img;
+      pend.img_stride = NS;
+      while (true) {
+        int rem = 0;  // positions left after the pending token, over the live sequences
+        for (int b = 0; b < B; ++b)
+          if (done[b] < N - 1) rem = std::max(rem, N - done[b]);
+        if (rem == 0) break;
+        const int Kp = std::min(K, rem);
+        if (plant) {
+          // plant what this pass tests: positions after the pending token, left to
+          // right, each from a single-position pass over its predecessor, while the
+          // drafts so far are kept (the first replacement ends a sequence's planting)
+          std::vector<int> act(B);
+          for (int b = 0; b < B; ++b) act[b] = done[b] < N - 1;
+          HIPCHK(hipMemcpy(s->pactive, act.data(), (size_t)B * 4, hipMemcpyHostToDevice));
+          gather_block(s->img, NS, s->d_f, P, 1, B, s->tok, st);
+          pa.active = s->pactive;
+          pa.pos_off = 1;
+          pa.logits = s->logits;
+          int moved = 0;
+          for (int j = 0; j + 1 < Kp; ++j) {
+            if (j > 0) {
+              shift_f(1);
+              ++moved;
+            }
+            run_forward(s, 1, 1);
+            place_argmax(pa, B, st);
+            HIPCHK(hipMemcpyAsync(act.data(), s->pactive, (size_t)B * 4, hipMemcpyDeviceToHost, st));
+            HIPCHK(hipStreamSynchronize(st));
+            bool any = false;
+            for (int b = 0; b < B; ++b) any |= act[b] != 0;
+            if (!any) break;
+          }
+          shift_f(-moved);
+          pa.active = nullptr;
+        }
+        gather_block(s->img, NS, s->d_f, P, Kp, B, s->tok, st);
+        run_forward(s, Kp, 0);
+        a.K = Kp;
+        a.n_fixed = 1;
+        a.round = 0;
+        a.truncate = 1;
+        a.count = s->cnt;
+        select_tokens(a, st);
+        truncate_finalize(a, s->d_f, st);  // f += 1 + accepted run; carry <- logits scoring the next pending
+        place_argmax(pend, B, st);         // next pending token at the new frontier
+        HIPCHK(hipMemcpyAsync(fh.data(), s->d_f, (size_t)B * 4, hipMemcpyDeviceToHost, st));
+        HIPCHK(hipMemcpyAsync(cnt_h.data(), s->cnt, (size_t)B * 4, hipMemcpyDeviceToHost, st));
+        fwd_abort_fetch(s);
+        HIPCHK(hipStreamSynchronize(st));
+        fwd_abort_check(s);
+        ++passes;
+        ++nv;
+        bool freeze = false;
+        for (int b = 0; b < B; ++b) {
+          if (done[b] >= N - 1) {  // finished earlier: frozen at its last position
+            fh[b] = P + N - 1;
+            freeze = true;
+            continue;
+          }
+          const int room = N - 1 - done[b];  // drafts of this pass inside the image
+          const int n = std::min(cnt_h[b], room);
+          acc_trunc += n;
+          proposed += n + ((n < Kp - 1 && n < room) ? 1 : 0);
+          done[b] = fh[b] - P;
+          if (done[b] >= N - 1) {
+            fh[b] = P + N - 1;
+            freeze |= done[b] > N - 1;
+            done[b] = N - 1;
+          }
+        }
+        for (int b = 0; b < B; ++b) s->f[b] = fh[b];
+        if (freeze) HIPCHK(hipMemcpy(s->d_f, fh.data(), (size_t)B * 4, hipMemcpyHostToDevice));
+      }
+      a.truncate = 0;
+    }
     // the state of block offset k (pass rows of `rps` per sequence) scores sequence
     // position start + k + 1: kept under its image index when that is an image
     // position (a row end's state scores the next row's first token), one copy per
@@ -1874,10 +2047,46 @@ ssd_status decode_impl(ssd_model* m, const ssd_schedule* sc, int32_t B, int32_t 
         k += len;
       }
     };
+    // planted drafts of image indexes [q0, q0 + n), left to right: the first from
+    // the logits that score q0 (the carry, or a pass over the chosen but not yet
+    // cached tokens before q0: a commit that runs inside the next verify pass, or
+    // the first image token), each later one from a single-position pass over its
+    // predecessor.  The KV slots these passes write lie inside the next verify
+    // pass's block, which rewrites them before reading.
+    auto plant_block = [&](int q0, int n) {
+      const int x0 = s->f[0] - P;  // first image index not cached (equal for all sequences)
+      const int Kc = q0 - x0;
+      if (Kc < 0 || Kc > s->Kmax) throw HipError{hipErrorInvalidValue, "planting outside the plan"};
+      if (Kc > 0) {
+        HIPCHK(hipMemcpy2DAsync(s->tok, (size_t)Kc * 4, s->img + x0, (size_t)NS * 4, (size_t)Kc * 4, B,
+                                hipMemcpyDeviceToDevice, st));
+        run_forward(s, Kc, 1);
+      }
+      pa.logits = Kc > 0 ? s->logits : s->carry;
+      pa.pos_off = Kc;
+      place_argmax(pa, B, st);
+      pa.logits = s->logits;
+      pa.pos_off = 1;
+      int moved = 0;
+      for (int j = 1; j < n; ++j) {
+        shift_f(Kc + j - 1 - moved);  // the pass reads the draft at image index q0 + j - 1
+        moved = Kc + j - 1;
+        run_forward(s, 1, 1);
+        place_argmax(pa, B, st);
+      }
+      shift_f(-moved);
+    };
     const Op* pending = nullptr;  // a commit waiting for the verify round it runs with
     for (size_t i = 0; i < ops.size(); ++i) {
       const Op& o = ops[i];
       if (o.kind >= 2) {
+        if (plant) {
+          if (o.kind == 2)
+            plant_block(o.start + 1, o.K);
+          else
+            plant_block((o.start + 1) * W, o.K * W);
+          continue;
+        }
         if (!heads) continue;
         // heads draft from chosen tokens: [h; e] with h the state that scored each
         // (image indices for the states, sequence positions for the tokens)
@@ -1924,16 +2133,20 @@ ssd_status decode_impl(ssd_model* m, const ssd_schedule* sc, int32_t B, int32_t 
         }
         run_forward(s, K, 0);
         if (s->cfg) cfg_mix(B, K, dm.Vimg, s->cfg_w, s->logits, s->carry, s->mlog, s->mcarry, st);
+        const int rr = std::min(o.rib, NCNT_ROUNDS - 1);
         a.K = K;
         a.n_fixed = Kc + o.nf;  // the committed prefix is fixed
         a.round = (unsigned)o.rnd;
+        a.count = s->cnt + (size_t)rr * Bs;
         select_tokens(a, st);
         HIPCHK(hipMemcpy2DAsync(s->img + start, (size_t)NS * 4, s->tok, (size_t)K * 4, (size_t)K * 4, B,
                                 hipMemcpyDeviceToDevice, st));
         ++nv;
         int n_eol = 0;  // end-of-line slots are not verified
         for (int k = 0; eol && k < o.K; ++k) n_eol += (o.start + k) % RW == W;
-        proposed += (int64_t)B * (o.K - o.nf - n_eol);
+        const int64_t np = (int64_t)B * (o.K - o.nf - n_eol);
+        proposed += np;
+        prop_round[rr] += np;
         if (Kc > 0) {  // the prefix's KV is final: commit it
           commit_prefix(Bs, K, Kc, dm.Vimg, s->logits, s->carry, s->d_f, s->ref_flag, s->ring, st);
           for (int b = 0; b < Bs; ++b) s->f[b] += Kc;
@@ -1949,26 +2162,45 @@ ssd_status decode_impl(ssd_model* m, const ssd_schedule* sc, int32_t B, int32_t 
       ++passes;
     }
     HIPCHK(hipGetLastError());
-    // image positions only (rows of W out of rows of RW)
-    HIPCHK(hipMemcpy2DAsync(out_tokens, (size_t)W * 4, s->img, (size_t)RW * 4, (size_t)W * 4, (size_t)B * H,
-                            hipMemcpyDefault, st));
-    std::vector<int> hc(B);
-    HIPCHK(hipMemcpyAsync(hc.data(), s->cnt, (size_t)B * 4, hipMemcpyDeviceToHost, st));
+    // image positions only (rows of W out of rows of RW; the strict decode's slack left out)
+    if (trunc)
+      HIPCHK(hipMemcpy2DAsync(out_tokens, (size_t)N * 4, s->img, (size_t)NS * 4, (size_t)N * 4, B, hipMemcpyDefault,
+                              st));
+    else
+      HIPCHK(hipMemcpy2DAsync(out_tokens, (size_t)W * 4, s->img, (size_t)RW * 4, (size_t)W * 4, (size_t)B * H,
+                              hipMemcpyDefault, st));
+    if (plant) HIPCHK(hipMemcpyAsync(src.table, s->ptab, (size_t)B * N * 4, hipMemcpyDefault, st));
+    if (!trunc) HIPCHK(hipMemcpyAsync(hc.data(), s->cnt, hc.size() * 4, hipMemcpyDeviceToHost, st));
     fwd_abort_fetch(s);
     HIPCHK(hipStreamSynchronize(st));
     fwd_abort_check(s);
     m->prof.flush();
-    if (stats) {
-      stats->passes = passes;
-      stats->verify_rounds = nv;
-      stats->proposed = proposed;
-      int64_t acc = 0;
-      for (int v : hc) acc += v;
-      stats->accepted = acc;
-    }
   } catch (HipError& e) {
     m->poisoned = true;
     return fail(SSD_E_DEVICE, "%s: %s", e.what, hipGetErrorString(e.e));
+  }
+  if (stats) {
+    *stats = ssd_stats{};
+    stats->passes = passes;
+    stats->verify_rounds = nv;
+    stats->proposed = proposed;
+    if (trunc) {
+      stats->accepted = acc_trunc;
+      stats->accepted_round[0] = acc_trunc;
+      stats->proposed_round[0] = proposed;
+    } else {
+      int64_t acc = 0;
+      for (int r = 0; r < NCNT_ROUNDS; ++r) {
+        int64_t ar = 0;
+        for (int b = 0; b < B; ++b) ar += hc[(size_t)r * Bs + b];
+        stats->accepted_round[r] = ar;
+        stats->proposed_round[r] = prop_round[r];
+        acc += ar;
+      }
+      stats->accepted = acc;
+    }
+    stats->wall_ns = (int64_t)std::chrono::duration_cast<std::chrono::nanoseconds>(
+                         std::chrono::steady_clock::now() - t_call).count();
   }
   return SSD_OK;
 }
@@ -1983,6 +2215,18 @@ ssd_status ssd_decode_image(ssd_model* m, const ssd_schedule* sc, int32_t B, int
   DraftSource src;
   src.drafts = drafts;
   src.draft_logits = draft_logits;
+  return decode_impl(m, sc, B, P, prefix, src, out_tokens, stats, stream);
+}
+
+ssd_status ssd_plant_image(ssd_model* m, const ssd_schedule* sc, int32_t B, int32_t P, const int32_t* prefix,
+                           const uint8_t* keep, const int32_t* repl, int32_t* drafts_out, int32_t* out_tokens,
+                           ssd_stats* stats, void* stream) {
+  g_err.clear();
+  if (!m || !sc || !prefix || !keep || !repl || !drafts_out || !out_tokens) return fail(SSD_E_INVAL, "NULL argument");
+  DraftSource src;
+  src.keep = keep;
+  src.repl = repl;
+  src.table = drafts_out;
   return decode_impl(m, sc, B, P, prefix, src, out_tokens, stats, stream);
 }
 

@@ -341,6 +341,27 @@ void commit_update(int B, int K, int Vimg, const float* logits, float* carry, in
 // positions cleared
 void commit_prefix(int B, int rps, int Kc, int Vimg, const float* logits, float* carry, int* f, int* ref_flag,
                    int ring, hipStream_t st);
+// greedy argmax of a logits row placed at image index f[b] - P + pos_off: a
+// planted draft (keep/repl given) or the token itself (keep == nullptr)
+struct PlaceArgs {
+  const float* logits;        // row of sequence b at logits + b * row_stride
+  size_t row_stride;
+  int Vimg, img_lo;
+  const int* f;               // [B] frontier (sequence positions)
+  int P, pos_off, x_end;      // image index x = f[b] - P + pos_off, valid in [0, x_end)
+  int* img;                   // working grid, row b at img + b * img_stride (absolute ids)
+  size_t img_stride;
+  const unsigned char* keep;  // [B][x_end] or nullptr
+  const int* repl;            // [B][x_end] codes in [0, Vimg - 1)
+  int* table;                 // [B][x_end] planted drafts out (absolute ids) or nullptr
+  int* next_tok;              // [B] token of the next single-position pass or nullptr
+  int* active;                // [B] gate or nullptr
+};
+void place_argmax(const PlaceArgs& a, int B, hipStream_t st);
+// tok[b][k] = img[b][f[b] - P + k]
+void gather_block(const int* img, int img_stride, const int* f, int P, int K, int B, int* tok, hipStream_t st);
+// p[i] += delta
+void add_i32(int* p, int n, int delta, hipStream_t st);
 // fill helpers (graph-capture safe)
 void fill_u32(unsigned* p, size_t n, unsigned v, hipStream_t st);
 // out[w] = XCD index workgroup w ran on

@@ -51,6 +51,8 @@ int main(void) {{
          offsetof(ssd_schedule, cfg), offsetof(ssd_schedule, cfg_weight));
   printf("%zu %zu %zu\\n", offsetof(ssd_schedule, eol), offsetof(ssd_schedule, eol_id),
          offsetof(ssd_schedule, separate_commit));
+  printf("%zu %zu %zu %zu %zu\\n", offsetof(ssd_schedule, truncate), offsetof(ssd_schedule, trunc_block),
+         offsetof(ssd_stats, accepted_round), offsetof(ssd_stats, proposed_round), offsetof(ssd_stats, wall_ns));
   return 0;
 }}
 """)
@@ -65,7 +67,9 @@ int main(void) {{
             ssd.ssd_schedule.seed.offset, ssd.ssd_model_config.rope_theta.offset,
             ssd.ssd_schedule.cfg.offset, ssd.ssd_schedule.cfg_weight.offset,
             ssd.ssd_schedule.eol.offset, ssd.ssd_schedule.eol_id.offset,
-            ssd.ssd_schedule.separate_commit.offset]
+            ssd.ssd_schedule.separate_commit.offset,
+            ssd.ssd_schedule.truncate.offset, ssd.ssd_schedule.trunc_block.offset,
+            ssd.ssd_stats.accepted_round.offset, ssd.ssd_stats.proposed_round.offset, ssd.ssd_stats.wall_ns.offset]
     assert got == want
 
 
@@ -118,4 +122,7 @@ def test_null_arguments_rejected_before_device_work(lib):
     st = ssd.ssd_stats()
     assert L.ssd_decode_image_heads(None, ctypes.byref(sc), 1, 1, None, None, 0, None, 0, None, ctypes.byref(st),
                                     None) == ssd.SSD_E_INVAL
+    assert "NULL" in ssd.ssd_last_error()
+    assert L.ssd_plant_image(None, ctypes.byref(sc), 1, 1, None, None, None, None, None, ctypes.byref(st),
+                             None) == ssd.SSD_E_INVAL
     assert "NULL" in ssd.ssd_last_error()
