@@ -309,16 +309,20 @@ ssd_status ssd_plant_image(ssd_model* model, const ssd_schedule* sched, int32_t 
  * Measurement hook.  enable = 1 starts recording a HIP event pair around every
  * projection-GEMM and attention launch of the model's forward passes, and
  * around every single-launch forward pass (on the stream they run on);
- * enable = 0 stops.  ssd_profile_read fills ms[c] = summed kernel time and
- * launches[c] = launch count per class c = 0 QKV, 1 O-proj, 2 gate/up,
- * 3 down, 4 LM head, 5 attention, 6 whole forward pass in one launch, and
- * bytes[c] = algorithmic HBM bytes of those launches (weights + activations
- * read + outputs written, KV read/written for attention; class 6: the sum of
- * classes 0-5 for that pass); reset = 1 clears the totals afterwards.
- * Arrays have 7 entries; any may be NULL.  Synchronizes the model's stream.
+ * enable = 0 stops.  ssd_profile_read fills, per class c = 0 QKV, 1 O-proj,
+ * 2 gate/up, 3 down, 4 LM head, 5 attention, 6 whole forward pass in one
+ * launch, 7 the launches of classes 0-4 that ran on the tiled (many-row) GEMM
+ * kernel (counted in their own class too): ms[c] = summed kernel time,
+ * launches[c] = launch count, bytes[c] = algorithmic HBM bytes of those
+ * launches (weights + activations read + outputs written, KV read/written for
+ * attention; class 6: the sum of classes 0-5 for that pass) and flops[c] =
+ * algorithmic flops (2 M N K per GEMM; 4 D per query head and visible key for
+ * attention); reset = 1 clears the totals afterwards.  Arrays have 8 entries;
+ * any may be NULL.  Synchronizes the model's stream and every recorded launch.
  */
 ssd_status ssd_profile(ssd_model* model, int32_t enable);
-ssd_status ssd_profile_read(ssd_model* model, double* ms, int64_t* launches, double* bytes, int32_t reset);
+ssd_status ssd_profile_read(ssd_model* model, double* ms, int64_t* launches, double* bytes, double* flops,
+                            int32_t reset);
 
 /*
  * Spatial draft head f_phi (Sec. 3.3 "Draft Prediction in Latent Space",
@@ -352,6 +356,7 @@ ssd_status ssd_draft_head_init(ssd_model* model, int32_t m, const void* weights,
 ssd_status ssd_draft_head_run(ssd_draft_head* head, int32_t R, const float* h, const int32_t* tokens,
                               int32_t* drafts, float* logits_out);
 void ssd_free_draft_head(ssd_draft_head* head);
+
 
 /*
  * Decode B images under the SSD schedule of ssd_decode_image with drafts from

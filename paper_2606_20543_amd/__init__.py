@@ -84,7 +84,7 @@ def lib():
         L.ssd_decode_image.argtypes = [vp, ctypes.POINTER(ssd_schedule), i32, i32, vp, vp, vp, vp,
                                        ctypes.POINTER(ssd_stats), vp]
         L.ssd_profile.argtypes = [vp, i32]
-        L.ssd_profile_read.argtypes = [vp, vp, vp, vp, i32]
+        L.ssd_profile_read.argtypes = [vp, vp, vp, vp, vp, i32]
         L.ssd_draft_head_numel.argtypes = [vp, i32]
         L.ssd_draft_head_numel.restype = i64
         L.ssd_draft_head_init.argtypes = [vp, i32, vp, i32, ctypes.POINTER(vp)]
@@ -218,15 +218,16 @@ def ssd_profile(model, enable):
     _check(lib().ssd_profile(ctypes.c_void_p(model), int(enable)))
 
 
-PROFILE_CLASSES = ("qkv", "o_proj", "gate_up", "down", "lm_head", "attention", "forward")
+PROFILE_CLASSES = ("qkv", "o_proj", "gate_up", "down", "lm_head", "attention", "forward", "tiled_gemm")
 
 
 def ssd_profile_read(model, reset=False):
-    """{class: (ms, launches, bytes)} for the seven launch classes."""
+    """{class: (ms, launches, bytes, flops)} for the eight launch classes."""
     import numpy as np
     k = len(PROFILE_CLASSES)
     ms = np.zeros(k, np.float64)
     n = np.zeros(k, np.int64)
     by = np.zeros(k, np.float64)
-    _check(lib().ssd_profile_read(ctypes.c_void_p(model), _ptr(ms), _ptr(n), _ptr(by), int(reset)))
-    return {c: (float(ms[i]), int(n[i]), float(by[i])) for i, c in enumerate(PROFILE_CLASSES)}
+    fl = np.zeros(k, np.float64)
+    _check(lib().ssd_profile_read(ctypes.c_void_p(model), _ptr(ms), _ptr(n), _ptr(by), _ptr(fl), int(reset)))
+    return {c: (float(ms[i]), int(n[i]), float(by[i]), float(fl[i])) for i, c in enumerate(PROFILE_CLASSES)}

@@ -126,14 +126,19 @@ struct Prof : LaunchTimer {
   struct Mark {
     int cls;
     hipEvent_t a, b;
-    double bytes;
+    double bytes, flops;
+    bool tiled;
   };
   std::vector<Mark> marks;
-  static constexpr int NCLS = 7;  // qkv, o, gate_up, down, lm_head, attention, persistent forward
-  double ms[NCLS] = {}, bytes[NCLS] = {};
+  // qkv, o, gate_up, down, lm_head, attention, persistent forward; then the
+  // launches of classes 0-4 that ran on the tiled GEMM kernel, counted again
+  static constexpr int NCLS = 8;
+  static constexpr int TILED = 7;
+  double ms[NCLS] = {}, bytes[NCLS] = {}, flops[NCLS] = {};
   int64_t n[NCLS] = {};
   int cur_cls = 0;
-  double cur_bytes = 0;
+  double cur_bytes = 0, cur_flops = 0;
+  bool cur_tiled = false;
   hipEvent_t get() {
     if (used == pool.size()) {
       hipEvent_t e;
@@ -145,12 +150,14 @@ struct Prof : LaunchTimer {
   void next(hipEvent_t& a, hipEvent_t& b) override {
     a = get();
     b = get();
-    marks.push_back(Mark{cur_cls, a, b, cur_bytes});
-    cur_bytes = 0;  // a call's algorithmic bytes go with its first launch
+    marks.push_back(Mark{cur_cls, a, b, cur_bytes, cur_flops, cur_tiled});
+    cur_bytes = 0;  // a call's algorithmic bytes and flops go with its first launch
+    cur_flops = 0;
   }
-  // time the launches of one call of class cls (b algorithmic bytes)
+  // time the launches of one call of class cls (b algorithmic bytes, fl
+  // algorithmic flops; tiled: a GEMM on the tiled kernel)
   template <typename F>
-  void run(int cls, double b, hipStream_t st, F&& f) {
+  void run(int cls, double b, hipStream_t st, F&& f, double fl = 0.0, bool tiled = false) {
     (void)st;
     if (!on) {
       f();
@@ -158,6 +165,8 @@ struct Prof : LaunchTimer {
     }
     cur_cls = cls;
     cur_bytes = b;
+    cur_flops = fl;
+    cur_tiled = tiled;
     g_launch_timer = this;
     try {
       f();
@@ -171,10 +180,18 @@ struct Prof : LaunchTimer {
   void flush() {
     for (const Mark& m : marks) {
       float t = 0.f;
+      HIPCHK(hipEventSynchronize(m.b));  // launches may sit on a session's own stream
       HIPCHK(hipEventElapsedTime(&t, m.a, m.b));
       ms[m.cls] += t;
       bytes[m.cls] += m.bytes;
+      flops[m.cls] += m.flops;
       n[m.cls] += 1;
+      if (m.tiled) {
+        ms[TILED] += t;
+        bytes[TILED] += m.bytes;
+        flops[TILED] += m.flops;
+        n[TILED] += 1;
+      }
     }
     marks.clear();
     used = 0;
@@ -202,6 +219,7 @@ struct ssd_model {
   // size (0: not available) and its XCD mapping (0: fenced reductions)
   int fwd_grid[2] = {0, 0};
   int fwd_xcd[2] = {0, 0};
+  unsigned fwd_spin_limit = 0;  // polls before a dependency wait of the persistent pass gives up
   Prof prof;
 };
 
@@ -210,6 +228,7 @@ struct ssd_session {
   Dims dm;
   hipStream_t stream;
   int B, P, Lmax, Kmax, Mmax, ring;
+  int max_ctx;         // the caller's bound on P + committed and drafted positions (Lmax rounds it up)
   std::vector<int> f;  // host mirror of the frontier
   bool poisoned = false;
   Allocs mem;
@@ -319,6 +338,14 @@ int fwd_att_units(const Dims& dm, int B, int Kmax) {
 void setup_fwd(ssd_model* m) {
   const char* env = std::getenv("SSD_FORWARD");
   if (!env || std::strcmp(env, "persistent") != 0) return;
+  // SSD_FWD_SPIN_LIMIT lowers the bound of every dependency wait (tests drive
+  // the abandoned-wait path with it: the grid still drains, the host reports
+  // SSD_E_DEVICE and poisons the session)
+  m->fwd_spin_limit = FWD_SPIN_LIMIT;
+  if (const char* sl = std::getenv("SSD_FWD_SPIN_LIMIT")) {
+    const long v = std::strtol(sl, nullptr, 10);
+    if (v >= 0 && v < (long)FWD_SPIN_LIMIT) m->fwd_spin_limit = (unsigned)v;
+  }
   if (!fwd_shape_ok(m->dm)) return;
   for (int mt = 1; mt <= 2; ++mt) {
     int g = std::min(fwd_max_grid(mt, m->dm.D), FWD_MAX_GRID);
@@ -585,7 +612,11 @@ void run_forward(ssd_session* s, int K, int lm_mode) {
     need(attn_partials_floats(dm, pa, B) <= s->apart_cap && (size_t)B * dm.Hkv * pa.nqg <= s->acnt_cap,
          "attention plan exceeds its workspace");
     double attn_bytes = 2.0 * M * dm.Hq * D * A;  // q read + o written
-    for (int b = 0; b < B; ++b) attn_bytes += 2.0 * (s->f[b] + K) * dm.Hkv * D * es;
+    double attn_flops = 0.0;                       // QK^T and PV over the visible keys
+    for (int b = 0; b < B; ++b) {
+      attn_bytes += 2.0 * (s->f[b] + K) * dm.Hkv * D * es;
+      attn_flops += 4.0 * dm.Hq * D * ((double)s->f[b] * K + 0.5 * K * (K + 1));
+    }
     const double qkv_bytes = (double)Nqkv * d * es + (double)M * d * A + (double)M * dm.Hq * D * A +
                              2.0 * M * dm.Hkv * D * es;
     const double o_bytes = (double)d * dm.Hq * D * es + (double)M * dm.Hq * D * A + (double)M * d * (8 + A);
@@ -605,7 +636,7 @@ void run_forward(ssd_session* s, int K, int lm_mode) {
       a.n_phases = 5 * dm.L + 1;
       a.xcd = XF;
       a.abort_flag = s->fw.abort_flag;
-      a.spin_limit = FWD_SPIN_LIMIT;
+      a.spin_limit = m->fwd_spin_limit;
       // flag values of this pass lie above every value an earlier pass stored;
       // before they would wrap, the flags restart from zero
       if ((uint64_t)(s->fw.epoch + 2) * (dm.L + 1) >= (1ull << 32)) {
@@ -637,11 +668,11 @@ void run_forward(ssd_session* s, int K, int lm_mode) {
       e.vc = vc;
       m->prof.run(0, qkv_bytes, st, [&] {
         gemm_bf16(pq, W.wqkv, Nqkv, d, s->xn, s->xn_plane, d, M, e, s->gpart, s->gcnt, st);
-      });
+      }, 2.0 * M * Nqkv * d, pq.tile);
       m->prof.run(5, attn_bytes, st, [&] {
         attention_bf16(dm, pa, B, K, s->d_f, s->q, s->q_plane, kc, vc, s->Lmax, s->o, s->o_plane, s->apart, s->acnt,
                        st);
-      });
+      }, attn_flops);
       e = base;
       e.kind = EPI_RESID;
       e.ssq = nullptr;
@@ -649,7 +680,7 @@ void run_forward(ssd_session* s, int K, int lm_mode) {
       e.ld = d;
       m->prof.run(1, o_bytes, st, [&] {
         gemm_bf16(po, W.wo, d, dm.Hq * D, s->o, s->o_plane, dm.Hq * D, M, e, s->gpart, s->gcnt, st);
-      });
+      }, 2.0 * M * d * dm.Hq * D, po.tile);
       ssq_parts = po.n_fb;
       e = base;
       e.kind = EPI_SWIGLU;
@@ -659,7 +690,7 @@ void run_forward(ssd_session* s, int K, int lm_mode) {
       e.ld = dm.dff;
       m->prof.run(2, gu_bytes, st, [&] {
         gemm_bf16(p13, W.w13, 2 * dm.dff, d, s->xn, s->xn_plane, d, M, e, s->gpart, s->gcnt, st);
-      });
+      }, 2.0 * M * 2 * dm.dff * d, p13.tile);
       e = base;
       e.kind = EPI_RESID;
       e.ssq = nullptr;
@@ -667,7 +698,7 @@ void run_forward(ssd_session* s, int K, int lm_mode) {
       e.ld = d;
       m->prof.run(3, dn_bytes, st, [&] {
         gemm_bf16(p2, W.w2, d, dm.dff, s->h, s->h_plane, dm.dff, M, e, s->gpart, s->gcnt, st);
-      });
+      }, 2.0 * M * d * dm.dff, p2.tile);
       ssq_parts = p2.n_fb;
     }
     EpiArgs e = base;
@@ -682,7 +713,7 @@ void run_forward(ssd_session* s, int K, int lm_mode) {
         throw HipError{hipErrorInvalidValue, "GEMM plan exceeds the split-K workspace"};
       m->prof.run(4, (double)dm.Vimg * d * es + (double)M * d * A + (double)M * dm.Vimg * 4, st, [&] {
         gemm_bf16(pl, m->wlm, dm.Vimg, d, s->xn, s->xn_plane, d, M, e, s->gpart, s->gcnt, st);
-      });
+      }, 2.0 * M * dm.Vimg * d, pl.tile);
     } else {
       e.ssq_off = K - 1;
       e.ssq_step = K;
@@ -692,7 +723,7 @@ void run_forward(ssd_session* s, int K, int lm_mode) {
       m->prof.run(4, (double)dm.Vimg * d * es + (double)B * d * A + (double)B * dm.Vimg * 4, st, [&] {
         gemm_bf16(pl, m->wlm, dm.Vimg, d, (const uint16_t*)s->xn + (size_t)(K - 1) * d, s->xn_plane, K * d, B, e,
                   s->gpart, s->gcnt, st);
-      });
+      }, 2.0 * B * dm.Vimg * d, pl.tile);
     }
   } else {
     for (int l = 0; l < dm.L; ++l) {
@@ -842,6 +873,7 @@ ssd_status create_session(ssd_model* m, int B, int P, int Lmax_req, int Kmax, hi
   s->Bi = B;
   s->P = P;
   s->Lmax = ((Lmax_req + 63) / 64) * 64;
+  s->max_ctx = Lmax_req;
   s->Kmax = Kmax;
   s->Mmax = B * std::max(P, Kmax);
   s->ring = Kmax;
@@ -1163,6 +1195,30 @@ ssd_status ssd_prefill(ssd_model* m, int32_t B, int32_t P, const int32_t* prefix
 }  // extern "C"
 
 // ---------------- spatial draft head ----------------
+// Per-call device workspace of a draft head run: staging of the inputs, the
+// activations of its four GEMMs (split bf16 planes), the x^2 partial sums, the
+// draft logits, the split-K partials and their arrival counters.
+struct HeadWork {
+  int* tok = nullptr;      // [R]
+  int* out = nullptr;      // [R]
+  int* f0 = nullptr;       // one zero: the epilogues' block-start lookup
+  float* hin = nullptr;    // [R][d]
+  void* z = nullptr;       // [R][2d] split planes
+  size_t z_plane = 0;
+  float* x = nullptr;      // [R][d] fp32: u, then h_hat
+  void* xn = nullptr;      // [R][d] split planes
+  size_t xn_plane = 0;
+  float* ssq = nullptr;    // [parts][rows]
+  int ssq_cap = 0, rows = 0;
+  void* hb = nullptr;      // [R][m] split planes
+  size_t hb_plane = 0;
+  float* logits = nullptr; // [R][V_img]
+  float* gpart = nullptr;
+  size_t gpart_cap = 0;
+  unsigned* gcnt = nullptr;
+  size_t gcnt_cap = 0;
+};
+
 struct ssd_draft_head {
   ssd_model* m;
   int d, mi, Rmax;
@@ -1172,88 +1228,71 @@ struct ssd_draft_head {
   float* g;      // [d]
   void* w13;     // packed [2m][d], gate/up rows interleaved
   void* w2;      // packed [d][m]
-  int* tok;      // [Rmax]
-  int* out;      // [Rmax]
-  int* f0;       // one zero: the epilogues' block-start lookup
-  float* hin;    // [Rmax][d]
-  void* z;       // [Rmax][2d] split planes
-  size_t z_plane;
-  float* x;      // [Rmax][d] fp32: u, then h_hat
-  void* xn;      // [Rmax][d] split planes
-  size_t xn_plane;
-  float* ssq;    // [parts][Rmax]
-  int ssq_cap;
-  void* hb;      // [Rmax][m] split planes
-  size_t hb_plane;
-  float* logits; // [Rmax][V_img]
-  float* gpart;
-  size_t gpart_cap;
-  unsigned* gcnt;
-  size_t gcnt_cap;
+  HeadWork work; // the head's own workspace (max_rows rows)
 };
 
 namespace {
 
-// Enqueue one head on R rows: hin [R][d] fp32 pre-norm states and tok [R]
-// vocabulary ids (device).  Leaves the drafts (absolute image-code ids, lowest
-// id among equal maxima) in h->out and the draft logits in h->logits.
-void head_forward(ssd_draft_head* h, int R, const float* hin, const int* tok, hipStream_t st) {
+// Enqueue one head on R rows of workspace w: hin [R][d] fp32 pre-norm states
+// and tok [R] vocabulary ids (device).  Leaves the drafts (absolute image-code
+// ids, lowest id among equal maxima) in w.out and the draft logits in w.logits.
+void head_forward(ssd_draft_head* h, const HeadWork& w, int R, const float* hin, const int* tok, hipStream_t st) {
   ssd_model* m = h->m;
   const Dims& dm = m->dm;
   const int d = h->d, mi = h->mi;
-  fill_u32((unsigned*)h->x, (size_t)R * d, 0u, st);  // u accumulates onto zero
+  fill_u32((unsigned*)w.x, (size_t)R * d, 0u, st);  // u accumulates onto zero
   EpiArgs base{};
-  base.Kblk = h->Rmax;  // every row is block position t of "sequence" 0
-  base.f = h->f0;
-  base.ssq_ld = h->Rmax;
+  base.Kblk = w.rows;  // every row is block position t of "sequence" 0
+  base.f = w.f0;
+  base.ssq_ld = w.rows;
   base.ssq_step = 1;
   base.inv_d = 1.0f / (float)d;
   base.eps = dm.eps;
   base.Hq = dm.Hq;
   base.Hkv = dm.Hkv;
   base.D = dm.D;
-  base.x = h->x;
-  base.xn = h->xn;
-  base.xn_plane = h->xn_plane;
-  base.ssq_out = h->ssq;
-  base.ssq_out_ld = h->Rmax;
-  base.h = h->hb;
-  base.h_plane = h->hb_plane;
-  base.logits = h->logits;
+  base.x = w.x;
+  base.xn = w.xn;
+  base.xn_plane = w.xn_plane;
+  base.ssq_out = w.ssq;
+  base.ssq_out_ld = w.rows;
+  base.h = w.hb;
+  base.h_plane = w.hb_plane;
+  base.logits = w.logits;
   if (!dm.bf16) {
     // fp32 models: plain fp32 GEMMs, one row sum of squares per norm
-    draft_input_f32(hin, (const float*)m->emb, tok, R, d, (float*)h->z, st);
+    draft_input_f32(hin, (const float*)m->emb, tok, R, d, (float*)w.z, st);
     EpiArgs e = base;
     e.kind = EPI_RESID;  // u = W0 [h; e]; n = g * u
     e.gnext = h->g;
     e.ld = d;
-    gemm_f32((const float*)h->w0, d, 2 * d, (const float*)h->z, 2 * d, R, e, st);
-    norm_rows_f32(h->x, R, d, nullptr, nullptr, h->ssq, st);
+    gemm_f32((const float*)h->w0, d, 2 * d, (const float*)w.z, 2 * d, R, e, st);
+    norm_rows_f32(w.x, R, d, nullptr, nullptr, w.ssq, st);
     e = base;
     e.kind = EPI_SWIGLU;  // SwiGLU(n / rms(u))
-    e.ssq = h->ssq;
+    e.ssq = w.ssq;
     e.ssq_parts = 1;
     e.ld = mi;
-    gemm_f32((const float*)h->w13, 2 * mi, d, (const float*)h->xn, d, R, e, st);
+    gemm_f32((const float*)h->w13, 2 * mi, d, (const float*)w.xn, d, R, e, st);
     e = base;
     e.kind = EPI_RESID;  // h_hat = u + W2 (...); n = g_f * h_hat
     e.gnext = m->gf;
     e.ld = d;
-    gemm_f32((const float*)h->w2, d, mi, (const float*)h->hb, mi, R, e, st);
-    norm_rows_f32(h->x, R, d, nullptr, nullptr, h->ssq, st);
+    gemm_f32((const float*)h->w2, d, mi, (const float*)w.hb, mi, R, e, st);
+    norm_rows_f32(w.x, R, d, nullptr, nullptr, w.ssq, st);
     e = base;
     e.kind = EPI_LOGITS;
-    e.ssq = h->ssq;
+    e.ssq = w.ssq;
     e.ssq_parts = 1;
     e.ld = dm.Vimg;
-    gemm_f32((const float*)m->wlm, dm.Vimg, d, (const float*)h->xn, d, R, e, st);
+    gemm_f32((const float*)m->wlm, dm.Vimg, d, (const float*)w.xn, d, R, e, st);
   } else {
-    draft_input(hin, m->emb, tok, R, d, h->z, h->z_plane, st);
+    draft_input(hin, m->emb, tok, R, d, w.z, w.z_plane, st);
     const int X = m->xcd;
     auto plan = [&](int N, int K) {
       GemmPlan p = gemm_plan_bf16(R, N, K, X);
-      if (gemm_partials_floats(p, R) > h->gpart_cap || (size_t)gemm_counters(p) > h->gcnt_cap ||
-          (N == d && p.n_fb > h->ssq_cap))
+      if (gemm_partials_floats(p, R) > w.gpart_cap || (size_t)gemm_counters(p) > w.gcnt_cap ||
+          (N == d && p.n_fb > w.ssq_cap))
         throw HipError{hipErrorInvalidValue, "GEMM plan exceeds the draft head's workspace"};
       return p;
     };
@@ -1263,32 +1302,32 @@ void head_forward(ssd_draft_head* h, int R, const float* hin, const int* tok, hi
     e.kind = EPI_RESID;
     e.gnext = h->g;
     e.ld = d;
-    gemm_bf16(p0, h->w0, d, 2 * d, h->z, h->z_plane, 2 * d, R, e, h->gpart, h->gcnt, st);
+    gemm_bf16(p0, h->w0, d, 2 * d, w.z, w.z_plane, 2 * d, R, e, w.gpart, w.gcnt, st);
     // SwiGLU(n / rms(u))
     GemmPlan p1 = plan(2 * mi, d);
     e = base;
     e.kind = EPI_SWIGLU;
-    e.ssq = h->ssq;
+    e.ssq = w.ssq;
     e.ssq_parts = p0.n_fb;
     e.ld = mi;
-    gemm_bf16(p1, h->w13, 2 * mi, d, h->xn, h->xn_plane, d, R, e, h->gpart, h->gcnt, st);
+    gemm_bf16(p1, h->w13, 2 * mi, d, w.xn, w.xn_plane, d, R, e, w.gpart, w.gcnt, st);
     // h_hat = u + W2 (...); n = g_f * h_hat for the output layer
     GemmPlan p2 = plan(d, mi);
     e = base;
     e.kind = EPI_RESID;
     e.gnext = m->gf;
     e.ld = d;
-    gemm_bf16(p2, h->w2, d, mi, h->hb, h->hb_plane, mi, R, e, h->gpart, h->gcnt, st);
+    gemm_bf16(p2, h->w2, d, mi, w.hb, w.hb_plane, mi, R, e, w.gpart, w.gcnt, st);
     // GenHead(RMSNorm(h_hat)) over the image codes
     GemmPlan p3 = plan(dm.Vimg, d);
     e = base;
     e.kind = EPI_LOGITS;
-    e.ssq = h->ssq;
+    e.ssq = w.ssq;
     e.ssq_parts = p2.n_fb;
     e.ld = dm.Vimg;
-    gemm_bf16(p3, m->wlm, dm.Vimg, d, h->xn, h->xn_plane, d, R, e, h->gpart, h->gcnt, st);
+    gemm_bf16(p3, m->wlm, dm.Vimg, d, w.xn, w.xn_plane, d, R, e, w.gpart, w.gcnt, st);
   }
-  first_token(R, dm.Vimg, dm.img_lo, h->logits, SSD_GREEDY, 0, 1.0, 0, nullptr, h->out, 1, st);
+  first_token(R, dm.Vimg, dm.img_lo, w.logits, SSD_GREEDY, 0, 1.0, 0, nullptr, w.out, 1, st);
   HIPCHK(hipGetLastError());
 }
 
@@ -1393,26 +1432,28 @@ ssd_status ssd_draft_head_init(ssd_model* m, int32_t mi, const void* weights, in
         if (nk.first == d) parts = std::max(parts, std::max(p.n_fb, gemm_max_parts(d)));
       }
     }
-    h->gpart_cap = gpart;
-    h->gpart = h->mem.get<float>(gpart);
-    h->gcnt_cap = gcnt;
-    h->gcnt = h->mem.get<unsigned>(gcnt);
-    h->ssq_cap = parts;
-    h->ssq = h->mem.get<float>((size_t)parts * R);
-    h->tok = h->mem.get<int>(R);
-    h->out = h->mem.get<int>(R);
-    h->f0 = h->mem.get<int>(1);
-    h->hin = h->mem.get<float>(R * d);
-    h->z_plane = R * 2 * d;
-    h->z = h->mem.get<char>(R * 2 * d * 4);
-    h->x = h->mem.get<float>(R * d);
-    h->xn_plane = R * d;
-    h->xn = h->mem.get<char>(R * d * 4);
-    h->hb_plane = R * mi;
-    h->hb = h->mem.get<char>(R * mi * 4);
-    h->logits = h->mem.get<float>(R * dm.Vimg);
-    fill_u32(h->gcnt, gcnt, 0u, st);
-    fill_u32((unsigned*)h->f0, 1, 0u, st);
+    HeadWork& w = h->work;
+    w.rows = (int)R;
+    w.gpart_cap = gpart;
+    w.gpart = h->mem.get<float>(gpart);
+    w.gcnt_cap = gcnt;
+    w.gcnt = h->mem.get<unsigned>(gcnt);
+    w.ssq_cap = parts;
+    w.ssq = h->mem.get<float>((size_t)parts * R);
+    w.tok = h->mem.get<int>(R);
+    w.out = h->mem.get<int>(R);
+    w.f0 = h->mem.get<int>(1);
+    w.hin = h->mem.get<float>(R * d);
+    w.z_plane = R * 2 * d;
+    w.z = h->mem.get<char>(R * 2 * d * 4);
+    w.x = h->mem.get<float>(R * d);
+    w.xn_plane = R * d;
+    w.xn = h->mem.get<char>(R * d * 4);
+    w.hb_plane = R * mi;
+    w.hb = h->mem.get<char>(R * mi * 4);
+    w.logits = h->mem.get<float>(R * dm.Vimg);
+    fill_u32(w.gcnt, gcnt, 0u, st);
+    fill_u32((unsigned*)w.f0, 1, 0u, st);
     HIPCHK(hipGetLastError());
     HIPCHK(hipStreamSynchronize(st));
   } catch (HipError& e) {
@@ -1441,11 +1482,12 @@ ssd_status ssd_draft_head_run(ssd_draft_head* h, int32_t R, const float* hs, con
   const bool host_out = !is_device_ptr(drafts) || (logits_out && !is_device_ptr(logits_out));
   hipStream_t st = m->stream;
   try {
-    HIPCHK(hipMemcpyAsync(h->hin, hs, (size_t)R * d * 4, hipMemcpyDefault, st));
-    HIPCHK(hipMemcpyAsync(h->tok, tokens, (size_t)R * 4, hipMemcpyDefault, st));
-    head_forward(h, R, h->hin, h->tok, st);
-    HIPCHK(hipMemcpyAsync(drafts, h->out, (size_t)R * 4, hipMemcpyDefault, st));
-    if (logits_out) HIPCHK(hipMemcpyAsync(logits_out, h->logits, (size_t)R * dm.Vimg * 4, hipMemcpyDefault, st));
+    const HeadWork& w = h->work;
+    HIPCHK(hipMemcpyAsync(w.hin, hs, (size_t)R * d * 4, hipMemcpyDefault, st));
+    HIPCHK(hipMemcpyAsync(w.tok, tokens, (size_t)R * 4, hipMemcpyDefault, st));
+    head_forward(h, w, R, w.hin, w.tok, st);
+    HIPCHK(hipMemcpyAsync(drafts, w.out, (size_t)R * 4, hipMemcpyDefault, st));
+    if (logits_out) HIPCHK(hipMemcpyAsync(logits_out, w.logits, (size_t)R * dm.Vimg * 4, hipMemcpyDefault, st));
     if (host_out) HIPCHK(hipStreamSynchronize(st));
   } catch (HipError& e) {
     h->poisoned = true;
@@ -1472,7 +1514,8 @@ ssd_status ssd_profile(ssd_model* m, int32_t enable) {
   return SSD_OK;
 }
 
-ssd_status ssd_profile_read(ssd_model* m, double* ms, int64_t* launches, double* bytes, int32_t reset) {
+ssd_status ssd_profile_read(ssd_model* m, double* ms, int64_t* launches, double* bytes, double* flops,
+                            int32_t reset) {
   if (!m) return fail(SSD_E_INVAL, "NULL model");
   try {
     HIPCHK(hipStreamSynchronize(m->stream));
@@ -1484,10 +1527,12 @@ ssd_status ssd_profile_read(ssd_model* m, double* ms, int64_t* launches, double*
     if (ms) ms[c] = m->prof.ms[c];
     if (launches) launches[c] = m->prof.n[c];
     if (bytes) bytes[c] = m->prof.bytes[c];
+    if (flops) flops[c] = m->prof.flops[c];
     if (reset) {
       m->prof.ms[c] = 0;
       m->prof.n[c] = 0;
       m->prof.bytes[c] = 0;
+      m->prof.flops[c] = 0;
     }
   }
   return SSD_OK;
@@ -1550,7 +1595,7 @@ ssd_status ssd_verify_step(ssd_session* s, int32_t K, int32_t* tokens, const flo
     return fail(SSD_E_INVAL, "truncate needs rule SSD_GREEDY and commit = 0");
   if (prm->truncate && s->cfg) return fail(SSD_E_INVAL, "truncate is not available on a guided session");
   for (int b = 0; b < B; ++b)
-    if (s->f[b] + K > s->Lmax || s->f[b] + K >= (1 << 24))
+    if (s->f[b] + K > s->max_ctx || s->f[b] + K >= (1 << 24))
       return fail(SSD_E_CAPACITY, "block [%d, %d) of sequence %d exceeds max_ctx", s->f[b], s->f[b] + K, b);
   const bool tok_dev = is_device_ptr(tokens);
   std::vector<int32_t> htok;
@@ -1818,8 +1863,8 @@ ssd_status decode_impl(ssd_model* m, const ssd_schedule* sc, int32_t B, int32_t 
     hdr.swap(seq);
   }
   const hipStream_t call_st = stream ? (hipStream_t)stream : m->stream;
-  // decode workspace, reused across calls of the same shape
-  if (!m->dec || m->dec_B != Bs || m->dec_P != P || m->dec_L != Lmax || m->dec_K != Kmax) {
+  // decode workspace, reused across calls of the same shape (a longer block bound serves shorter blocks)
+  if (!m->dec || m->dec_B != Bs || m->dec_P != P || m->dec_L != Lmax || m->dec_K < Kmax) {
     if (m->dec) {
       ssd_session* old = m->dec;
       m->dec = nullptr;
@@ -2101,12 +2146,12 @@ ssd_status decode_impl(ssd_model* m, const ssd_schedule* sc, int32_t B, int32_t 
                                 hipMemcpyDeviceToDevice, st));
         for (int j = 1; j <= o.K; ++j) {
           ssd_draft_head* h = (hor ? src.hh : src.vh)[j - 1];
-          head_forward(h, B * n_src, s->hsrc, s->tsrc, st);
+          head_forward(h, h->work, B * n_src, s->hsrc, s->tsrc, st);
           const int dq = seq_of(p0 + j * step);  // a run or a row: contiguous in the sequence
-          HIPCHK(hipMemcpy2DAsync(s->img + dq, (size_t)NS * 4, h->out, (size_t)n_src * 4, (size_t)n_src * 4, B,
+          HIPCHK(hipMemcpy2DAsync(s->img + dq, (size_t)NS * 4, h->work.out, (size_t)n_src * 4, (size_t)n_src * 4, B,
                                   hipMemcpyDeviceToDevice, st));
           if (use_q)
-            HIPCHK(hipMemcpy2DAsync(s->qtab + (size_t)dq * dm.Vimg, (size_t)NS * dm.Vimg * 4, h->logits,
+            HIPCHK(hipMemcpy2DAsync(s->qtab + (size_t)dq * dm.Vimg, (size_t)NS * dm.Vimg * 4, h->work.logits,
                                     (size_t)n_src * dm.Vimg * 4, (size_t)n_src * dm.Vimg * 4, B,
                                     hipMemcpyDeviceToDevice, st));
         }

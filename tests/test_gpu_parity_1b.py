@@ -56,6 +56,7 @@ def test_1b_greedy_rows(pair):
             G.check_commit(SHAPE, sess, os_, work[:, start:start + K], stats, want_h=True)
         print("1b greedy parity stats", stats, flush=True)
         assert stats["flips"] <= 0.02 * stats["positions"] + 1
+        assert stats["flips"] <= G.flips_expected_bound(stats["flips_expected"])
     finally:
         ssd.ssd_free_session(sess)
 
@@ -75,6 +76,8 @@ def test_1b_b4_accept_reject_topk(pair):
         blk = drafts.copy()
         refs_state = q.astype(np.float64)
         gnew, out = _check_round(sess, os_, blk, 0, R.RULE_ACCEPT_REJECT, 0, top_k, q, stats, K)
+        # the flips of round 1 are as many as the realized logit errors make likely
+        assert stats["flips"] <= G.flips_expected_bound(stats["flips_expected"]), stats
         # second round: GPU uses its stored references; the oracle gets the same
         # (accepted: the draft q; rejected: the first round's GPU scoring logits)
         carry1 = None
@@ -106,7 +109,17 @@ def test_1b_b4_accept_reject_topk(pair):
         ol3, _ = Dc.commit(os_, g2)
         assert np.abs(out3["logits"] - ol3).max() < TOL
         assert list(out3["frontier"]) == [P + K] * B
-        # end-to-end round 2: every difference must be explained by the logit error
+        # end-to-end round 2: every difference must be explained by the logit error,
+        # and there are no more of them than the realized errors make likely
+        exp2 = 0.0
+        for b in range(B):
+            for k in range(K):
+                Lo = ol2[b, k - 1] if k > 0 else ocarry[b]
+                Lg = out2["logits"][b, k - 1] if k > 0 else carry1[b]
+                exp2 += G.flip_probability(R.RULE_ACCEPT_REJECT, Lo, Lg, refs2[b][k], int(blk2[b, k]), 1.0, top_k)
+        n2 = int(((o2 != g2) | (oa2 != a2)).sum())
+        stats["flips_expected_r2"] = exp2
+        assert n2 <= G.flips_expected_bound(exp2), (n2, exp2)
         for b, k in np.argwhere((o2 != g2) | (oa2 != a2)):
             Lo = ol2[b, k - 1] if k > 0 else ocarry[b]
             Lg = out2["logits"][b, k - 1] if k > 0 else carry1[b]

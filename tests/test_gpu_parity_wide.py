@@ -17,6 +17,13 @@ stays within seconds.  Cases:
       (split-KV attention with a cross-chunk merge)
   8B width, batch 1, a 64-token block at context 4288..4352 (the last row of
       the 64x64 image), rule (A)
+  8B width, batch 8, a 64-token block at context 4288..4352 for every
+      sequence (the shape the bench's attention_at_scale and gemm_at_scale time:
+      512-row tiled GEMMs, 4 query heads per KV head over 4352 keys); the oracle
+      recomputes two of the eight sequences (sequences are independent), the
+      rule on the GPU's own logits is checked for all eight
+  7B width, batch 1, a 32-token block at context 1120..1152 (the last row of
+      the 32x32 workload), 2 rounds + commit
   1B width, batch 4, 64-token prompt and a 64-token block (M = 256, prefill
       and verify): tiled GEMMs whose K range is split over workgroups to
       fill the CUs (O and down projections in 4 splits, QKV in 2), rule (A),
@@ -85,6 +92,7 @@ def _greedy_block(pair, shape, B, P, K, rounds, keep, seed_stream):
         G.check_commit(shape, sess, os_, blk, stats, want_h=True)
         print("parity stats", stats, flush=True)
         assert stats["flips"] <= 0.02 * stats["positions"] + 1
+        assert stats["flips"] <= G.flips_expected_bound(stats["flips_expected"])
     finally:
         ssd.ssd_free_session(sess)
 
@@ -115,6 +123,53 @@ def test_8b_width_context_4352(pair8):
         ssd.ssd_free_session(sess)
 
 
+def test_8b_width_batch8_context_4352(pair8):
+    """Every sequence of the batch verifies its last 64-token row over 4288 cached
+    positions; sequences 0 and 7 are recomputed by the oracle."""
+    B, P, K = 8, 4288, 64
+    pre = synth.prompt(W8, B, P)
+    drafts = synth.random_codes(W8, (B, K), stream=18)
+    sess = ssd.ssd_prefill(pair8.model, B, P, pre, P + K, K)
+    stats = {}
+    try:
+        carry = np.zeros((B, W8.v_img), np.float32)
+        ssd.ssd_get_carry(sess, carry)
+        out = G.gpu_verify(sess, W8, drafts + W8.img_lo, G.vparams())
+        gnew, gacc, gcnt, _ = G.oracle_rule_on(out["logits"], carry, drafts, 0, R.RULE_GREEDY, 0, 3, [P] * B)
+        assert np.array_equal(out["tokens"] - W8.img_lo, gnew)
+        assert np.array_equal(out["accept"], gacc) and np.array_equal(out["count"], gcnt)
+        com = G.gpu_verify(sess, W8, gnew + W8.img_lo, G.vparams(commit=1), want_h=True)
+        assert list(com["frontier"]) == [P + K] * B
+        for b in (0, 7):
+            print(f"oracle prefill of 4288 tokens, sequence {b}", flush=True)
+            os_ = Dc.prefill(pair8.om, pre[b:b + 1], P + K)
+            cerr = float(np.abs(carry[b] - os_.carry[0]).max())
+            onew, oacc, _, ol = Dc.verify_round(os_, drafts[b:b + 1], 0, R.RULE_GREEDY, 0, 3)
+            err = float(np.abs(out["logits"][b] - ol[0]).max())
+            stats["max_logit_err"] = max(stats.get("max_logit_err", 0.0), err, cerr)
+            assert err < G.TOL["bf16"] and cerr < G.TOL["bf16"], (b, err, cerr)
+            flips = 0
+            for k in np.nonzero(onew[0] != gnew[b])[0]:
+                Lo = os_.carry[0] if k == 0 else ol[0, k - 1]
+                assert G.greedy_gap(Lo) < 2 * G.TOL["bf16"], f"sequence {b}, position {k}"
+                flips += 1
+            stats["flips"] = stats.get("flips", 0) + flips
+            cl, ch = Dc.commit(os_, gnew[b:b + 1])
+            err = float(np.abs(com["logits"][b] - cl[0]).max())
+            stats["max_logit_err"] = max(stats["max_logit_err"], err)
+            assert err < G.TOL["bf16"]
+            G.check_h_pre(W8, com["h_pre"][b:b + 1], ch, stats)
+        print("parity stats", stats, flush=True)
+        assert stats["flips"] <= 0.02 * 2 * K + 1
+    finally:
+        ssd.ssd_free_session(sess)
+
+
+def test_7b_width_context_1152(pair7):
+    """The 32x32 workload's last row: a 32-token block over 1120 cached positions."""
+    _greedy_block(pair7, W7, B=1, P=1120, K=32, rounds=2, keep=0.6, seed_stream=19)
+
+
 def test_1b_width_b4_context_1088_rule_c(pair1):
     pair = pair1
     B, P, K, top_k = 4, 1056, 32, 2000
@@ -127,8 +182,9 @@ def test_1b_width_b4_context_1088_rule_c(pair1):
     stats = {}
     try:
         blk, _ = G.check_round(W1, sess, os_, drafts, 0, R.RULE_ACCEPT_REJECT, 0, top_k, q, stats)
-        G.check_commit(W1, sess, os_, blk, stats)
+        G.check_commit(W1, sess, os_, blk, stats, want_h=True)
         print("parity stats", stats, flush=True)
+        assert stats["flips"] <= G.flips_expected_bound(stats["flips_expected"]), stats
     finally:
         ssd.ssd_free_session(sess)
 
