@@ -295,10 +295,13 @@ def check_round(shape, sess, os_, blk, nf, rule, rnd, top_k, ref, stats):
 
 
 # h_pre (the last layer's pre-norm state, the draft heads' input) elementwise,
-# relative to its row's root mean square: the output layer sees h / rms(h), so a
-# bound of H_RTOL * rms on every element keeps the normalized state within
-# H_RTOL of the oracle's per element (fp32 models: the fp32 accumulation error)
-H_RTOL = {"f32": 1e-5, "bf16": 2e-3}
+# relative to its row's root mean square.  The output layer sees h / rms(h): an
+# error of e * rms(h) on every element of a row moves a logit by about
+# e * sqrt(d) * 0.02 (a sum of d terms of random sign against N(0, 0.02)
+# weights), i.e. by e to 1.3 e at d = 2048..4096.  The bf16 bound is half of the
+# 2e-2 logit tolerance (measured: 2.3e-3 on the 24-layer 1B model); fp32 models:
+# the fp32 accumulation error.
+H_RTOL = {"f32": 1e-5, "bf16": 1e-2}
 
 
 def check_h_pre(shape, h_gpu, h_oracle, stats):
