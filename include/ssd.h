@@ -357,6 +357,25 @@ ssd_status ssd_draft_head_run(ssd_draft_head* head, int32_t R, const float* h, c
                               int32_t* drafts, float* logits_out);
 void ssd_free_draft_head(ssd_draft_head* head);
 
+/*
+ * For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the same
+ * computation and results as ssd_draft_head_run, with the run's workspace
+ * (staged inputs, activations, x^2 partial sums, draft logits, split-K
+ * partials and their counters) taken from a static device array of 64 MiB
+ * that every GPU the library runs on holds until the process ends, instead of
+ * the head's own workspace.  Allocates nothing, never synchronizes, and takes
+ * device arrays only (h, tokens, drafts, logits_out; SSD_E_INVAL otherwise).
+ * R up to the head's max_rows, as long as its workspace fits the array
+ * (about 20 d + 4 m + 4 V_img bytes per row plus the split-K partials of the
+ * four GEMMs: a few hundred rows for d = 2048, m = 2d); larger R is refused
+ * with SSD_E_INVAL before any launch.  All calls on one GPU share that GPU's array,
+ * which keeps the last call's contents (each call clears what must start at
+ * zero): calls that overlap on one GPU race, so callers serialize them (one
+ * stream, or events between streams).
+ */
+ssd_status ssd_draft_head_run_noalloc(ssd_draft_head* head, int32_t R, const float* h, const int32_t* tokens,
+                                      int32_t* drafts, float* logits_out);
 
 /*
  * Decode B images under the SSD schedule of ssd_decode_image with drafts from

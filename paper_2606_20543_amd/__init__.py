@@ -21,7 +21,7 @@ EXPORTED = [
     "ssd_init_model", "ssd_weights_numel", "ssd_free_model", "ssd_prefill", "ssd_free_session",
     "ssd_verify_step", "ssd_get_carry", "ssd_session_set_cfg", "ssd_decode_image", "ssd_profile", "ssd_profile_read", "ssd_last_error",
     "ssd_draft_head_numel", "ssd_draft_head_init", "ssd_draft_head_run", "ssd_free_draft_head",
-    "ssd_decode_image_heads", "ssd_plant_image",
+    "ssd_decode_image_heads", "ssd_plant_image", "ssd_draft_head_run_noalloc",
 ]
 
 
@@ -89,6 +89,7 @@ def lib():
         L.ssd_draft_head_numel.restype = i64
         L.ssd_draft_head_init.argtypes = [vp, i32, vp, i32, ctypes.POINTER(vp)]
         L.ssd_draft_head_run.argtypes = [vp, i32, vp, vp, vp, vp]
+        L.ssd_draft_head_run_noalloc.argtypes = [vp, i32, vp, vp, vp, vp]
         L.ssd_free_draft_head.argtypes = [vp]
         L.ssd_plant_image.argtypes = [vp, ctypes.POINTER(ssd_schedule), i32, i32, vp, vp, vp, vp, vp,
                                       ctypes.POINTER(ssd_stats), vp]
@@ -99,7 +100,7 @@ def lib():
         L.ssd_last_error.restype = ctypes.c_char_p
         for name in ("ssd_init_model", "ssd_prefill", "ssd_verify_step", "ssd_get_carry", "ssd_session_set_cfg",
                      "ssd_decode_image", "ssd_profile", "ssd_profile_read", "ssd_draft_head_init", "ssd_draft_head_run",
-                     "ssd_decode_image_heads", "ssd_plant_image"):
+                     "ssd_decode_image_heads", "ssd_plant_image", "ssd_draft_head_run_noalloc"):
             getattr(L, name).restype = i32
         _lib = L
     return _lib
@@ -197,6 +198,12 @@ def ssd_draft_head_init(model, m, weights, max_rows):
 def ssd_draft_head_run(head, R, h, tokens, drafts, logits_out=None):
     _check(lib().ssd_draft_head_run(ctypes.c_void_p(head), R, _ptr(h), _ptr(tokens), _ptr(drafts),
                                     _ptr(logits_out)))
+
+
+def ssd_draft_head_run_noalloc(head, R, h, tokens, drafts, logits_out=None):
+    """Device arrays only; the workspace comes from the library's static array."""
+    _check(lib().ssd_draft_head_run_noalloc(ctypes.c_void_p(head), R, _ptr(h), _ptr(tokens), _ptr(drafts),
+                                            _ptr(logits_out)))
 
 
 def ssd_free_draft_head(head):

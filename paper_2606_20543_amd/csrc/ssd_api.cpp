@@ -9,6 +9,7 @@
 #include <chrono>
 #include <cstring>
 #include <map>
+#include <mutex>
 #include <string>
 #include <utility>
 #include <vector>
@@ -202,6 +203,45 @@ struct Prof : LaunchTimer {
 };
 }  // namespace
 
+namespace {
+
+// Workspace of the allocation-free draft-head run (ssd_draft_head_run_noalloc):
+// a static device array, one copy on every GPU the library runs on, held until
+// the process ends.  Host code never passes `scratch` itself to a kernel or a
+// copy: the host-side name only stands in for the symbol; the device address
+// comes from hipGetSymbolAddress, looked up once per device.
+constexpr size_t NOALLOC_SCRATCH_BYTES = (size_t)64 << 20;
+static __device__ __align__(256) unsigned char scratch[NOALLOC_SCRATCH_BYTES];
+
+constexpr int MAX_DEVICES = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[MAX_DEVICES] = {};
+bool g_scratch_done[MAX_DEVICES] = {};
+
+// The current device's copy of `scratch` (nullptr if its address is unknown);
+// the first call on a device looks it up with that device current.
+void* scratch_of_current_device() {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= MAX_DEVICES) {
+    (void)hipGetLastError();
+    return nullptr;
+  }
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch_done[dev]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) == hipSuccess && p != nullptr) {
+      g_scratch_ptr[dev] = p;
+    } else {
+      (void)hipGetLastError();
+      g_scratch_ptr[dev] = nullptr;
+    }
+    g_scratch_done[dev] = true;
+  }
+  return g_scratch_ptr[dev];
+}
+
+}  // namespace
+
 struct ssd_model {
   ssd_model_config cfg;
   Dims dm;
@@ -221,6 +261,7 @@ struct ssd_model {
   int fwd_xcd[2] = {0, 0};
   unsigned fwd_spin_limit = 0;  // polls before a dependency wait of the persistent pass gives up
   Prof prof;
+  void* scratch = nullptr;  // this model's device's copy of the static workspace (allocation-free runs)
 };
 
 struct ssd_session {
@@ -1130,6 +1171,7 @@ ssd_status ssd_init_model(const ssd_model_config* cfg, const void* weights, void
     off += (size_t)dm.V * d;
     if ((int64_t)off != numel_of(*cfg)) throw HipError{hipErrorInvalidValue, "layout size mismatch"};
     HIPCHK(hipStreamSynchronize(st));
+    m->scratch = scratch_of_current_device();  // set-up of the allocation-free head runs
   } catch (HipError& e) {
     delete m;
     if (e.e == hipErrorOutOfMemory || std::string(e.what) == "hipMalloc")
@@ -1489,6 +1531,80 @@ ssd_status ssd_draft_head_run(ssd_draft_head* h, int32_t R, const float* hs, con
     HIPCHK(hipMemcpyAsync(drafts, w.out, (size_t)R * 4, hipMemcpyDefault, st));
     if (logits_out) HIPCHK(hipMemcpyAsync(logits_out, w.logits, (size_t)R * dm.Vimg * 4, hipMemcpyDefault, st));
     if (host_out) HIPCHK(hipStreamSynchronize(st));
+  } catch (HipError& e) {
+    h->poisoned = true;
+    return fail(SSD_E_DEVICE, "%s: %s", e.what, hipGetErrorString(e.e));
+  }
+  return SSD_OK;
+}
+
+ssd_status ssd_draft_head_run_noalloc(ssd_draft_head* h, int32_t R, const float* hs, const int32_t* tokens,
+                                      int32_t* drafts, float* logits_out) {
+  g_err.clear();
+  if (!h || !hs || !tokens || !drafts) return fail(SSD_E_INVAL, "NULL argument");
+  if (h->poisoned || h->m->poisoned) return fail(SSD_E_STATE, "draft head or model is poisoned");
+  if (R < 1 || R > h->Rmax) return fail(SSD_E_INVAL, "R = %d outside [1, max_rows = %d]", R, h->Rmax);
+  if (!is_device_ptr(hs) || !is_device_ptr(tokens) || !is_device_ptr(drafts) ||
+      (logits_out && !is_device_ptr(logits_out)))
+    return fail(SSD_E_INVAL, "the allocation-free run takes device arrays only");
+  ssd_model* m = h->m;
+  if (!m->scratch) return fail(SSD_E_STATE, "the static workspace's device address is unknown");
+  const Dims& dm = m->dm;
+  const int d = h->d, mi = h->mi;
+  // carve this call's workspace out of the static array: every region 256-byte aligned
+  size_t gpart = 0, gcnt = 0;
+  int parts = 1;
+  if (dm.bf16) {
+    const std::pair<int, int> nk[4] = {{d, 2 * d}, {2 * mi, d}, {d, mi}, {dm.Vimg, d}};
+    for (const auto& p : nk) {
+      GemmPlan pl = gemm_plan_bf16(R, p.first, p.second, m->xcd);
+      gpart = std::max(gpart, gemm_partials_floats(pl, R));
+      gcnt = std::max(gcnt, (size_t)gemm_counters(pl));
+      if (p.first == d) parts = std::max(parts, pl.n_fb);
+    }
+  }
+  const size_t r = (size_t)R;
+  const size_t sz[12] = {gcnt * 4, 4, r * 4, r * 4, r * d * 4, r * 2 * d * 4, r * d * 4, r * d * 4,
+                         (size_t)parts * r * 4, r * mi * 4, r * dm.Vimg * 4, gpart * 4};
+  size_t off[12], need = 0;
+  for (int i = 0; i < 12; ++i) {
+    off[i] = need;
+    need += (sz[i] + 255) & ~(size_t)255;
+  }
+  if (need > NOALLOC_SCRATCH_BYTES)
+    return fail(SSD_E_INVAL, "R = %d rows need %zu bytes of workspace; the static workspace holds %zu", R, need,
+                NOALLOC_SCRATCH_BYTES);
+  char* base = (char*)m->scratch;
+  HeadWork w;
+  w.rows = R;
+  w.gcnt = (unsigned*)(base + off[0]);
+  w.gcnt_cap = gcnt;
+  w.f0 = (int*)(base + off[1]);
+  w.tok = (int*)(base + off[2]);
+  w.out = (int*)(base + off[3]);
+  w.hin = (float*)(base + off[4]);
+  w.z = base + off[5];
+  w.z_plane = r * 2 * d;
+  w.x = (float*)(base + off[6]);
+  w.xn = base + off[7];
+  w.xn_plane = r * d;
+  w.ssq = (float*)(base + off[8]);
+  w.ssq_cap = parts;
+  w.hb = base + off[9];
+  w.hb_plane = r * mi;
+  w.logits = (float*)(base + off[10]);
+  w.gpart = (float*)(base + off[11]);
+  w.gpart_cap = gpart;
+  hipStream_t st = m->stream;
+  try {
+    // the array keeps the last call's contents: counters and the block-start lookup start at zero
+    fill_u32(w.gcnt, gcnt, 0u, st);
+    fill_u32((unsigned*)w.f0, 1, 0u, st);
+    HIPCHK(hipMemcpyAsync(w.hin, hs, r * d * 4, hipMemcpyDeviceToDevice, st));
+    HIPCHK(hipMemcpyAsync(w.tok, tokens, r * 4, hipMemcpyDeviceToDevice, st));
+    head_forward(h, w, R, w.hin, w.tok, st);
+    HIPCHK(hipMemcpyAsync(drafts, w.out, r * 4, hipMemcpyDeviceToDevice, st));
+    if (logits_out) HIPCHK(hipMemcpyAsync(logits_out, w.logits, r * dm.Vimg * 4, hipMemcpyDeviceToDevice, st));
   } catch (HipError& e) {
     h->poisoned = true;
     return fail(SSD_E_DEVICE, "%s: %s", e.what, hipGetErrorString(e.e));

@@ -97,6 +97,7 @@ int main() {
   CHECK(ssd_decode_image_heads(nullptr, &sc, 1, 1, nullptr, nullptr, 0, nullptr, 0, nullptr, &stv, nullptr) ==
         SSD_E_INVAL);
   CHECK(ssd_draft_head_run(nullptr, 1, nullptr, nullptr, nullptr, nullptr) == SSD_E_INVAL);
+  CHECK(ssd_draft_head_run_noalloc(nullptr, 1, nullptr, nullptr, nullptr, nullptr) == SSD_E_INVAL);
   CHECK(ssd_get_carry(nullptr, nullptr) == SSD_E_INVAL);
   CHECK(ssd_session_set_cfg(nullptr, 1.f) == SSD_E_INVAL);
   CHECK(ssd_profile(nullptr, 1) == SSD_E_INVAL);
