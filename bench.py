@@ -336,7 +336,8 @@ def at_scale(ssd, rounds=5):
         ssd.ssd_free_model(model)
     ms, n, by, fl = prof["attention"]
     gbs = by / (ms / 1e3) / 1e9
-    att = {"shape": "8B: 32q/8kv heads x 128, batch 8, 64-token blocks, context 4352", "bound": "hbm",
+    att = {"shape": "8B: 32q/8kv heads x 128, batch 8, 64-token blocks, context 4352", "kernel": "attn_qs_kernel",
+           "bound": "hbm",
            "achieved": gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": gbs / HBM_PEAK_GBS, "launches": n,
            "ms_per_launch": ms / n, "bytes_per_launch": by / n, "tflops": fl / (ms / 1e3) / 1e12,
            "timing": "dispatch-timestamp events around each attention launch"}
@@ -671,7 +672,7 @@ def main():
                    "passes_per_image": stats.passes, "commit": "run inside the next verify pass where adjacent",
                    "forward": args.forward, "parallelism": "single GPU"},
         "roofline": roofline,
-        "attention": {"bound": "hbm", "kernel": "attn_bf16_kernel", "achieved": a_gbs, "peak": HBM_PEAK_GBS,
+        "attention": {"bound": "hbm", "kernel": "attn_qs_kernel + attn_bf16_kernel", "achieved": a_gbs, "peak": HBM_PEAK_GBS,
                       "unit": "GB/s", "frac": a_gbs / HBM_PEAK_GBS if a_gbs else None, "launches": a_n,
                       "ms_per_launch": a_ms / max(a_n, 1), "bytes_per_launch": a_by / max(a_n, 1),
                       "TFLOP_per_s": a_fl / (a_ms / 1e3) / 1e12 if a_ms > 0 else None},

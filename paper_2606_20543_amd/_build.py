@@ -20,7 +20,12 @@ FLAGS = [
 # per-source extra flags: the persistent forward kernel keeps loop-invariant
 # address arithmetic where it is used (machine-level hoisting would keep it
 # live across the whole kernel and push registers into scratch memory)
-EXTRA = {"kernels_fwd.hip": ["-mllvm", "-disable-machine-licm"]}
+EXTRA = {"kernels_fwd.hip": ["-mllvm", "-disable-machine-licm"],
+         # attention: MFMA accumulators in ordinary vector registers (the
+         # query-split kernel fits in 256 of them; with accumulation
+         # registers the compiler copied every output accumulator between the
+         # two register files on every key block)
+         "kernels_attn.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
 
 
 def _compile(src):

@@ -25,16 +25,32 @@
 
 namespace ssd {
 
-// one wave per SIMD: the register file holds two K/V blocks, the queries and
-// the accumulators without the compiler sinking the prefetch loads
-template <int D, int QPW, bool QS>
+// key split: one wave per SIMD, so the register file holds two K/V blocks,
+// the queries and the accumulators without the compiler sinking the prefetch
+// loads
+template <int D, int QPW>
 __global__ __launch_bounds__(AtShape<QPW>::THREADS) __attribute__((amdgpu_waves_per_eu(1, 1)))
 void attn_bf16_kernel(AttnKArgs a) {
   constexpr int NW = AtShape<QPW>::WAVES, ROWS = QPW * 16, RS = D + 4;
   __shared__ __align__(16) float sm_o[NW * ROWS * RS];
   __shared__ float sm_m[NW * ROWS], sm_l[NW * ROWS];
   __shared__ int is_last;
-  attn_unit<D, QPW, PlainMem, true, PlainMem, false, QS>(a, blockIdx.x, sm_o, sm_m, sm_l, &is_last);
+  attn_unit<D, QPW, PlainMem, true, PlainMem, false, false>(a, blockIdx.x, sm_o, sm_m, sm_l, &is_last);
+}
+
+// query split: eight waves, two per SIMD (at most 256 registers each), the
+// K/V stages and the output stage in the same LDS bytes (used one after the
+// other)
+template <int D, int QPW>
+__global__ __launch_bounds__((AtShape<QPW, true>::THREADS)) __attribute__((amdgpu_waves_per_eu(2, 2)))
+void attn_qs_kernel(AttnKArgs a) {
+  constexpr int NW = AtShape<QPW, true>::WAVES, ROWS = QPW * 16, RS = D + 4;
+  constexpr int O_BYTES = NW * ROWS * RS * 4, KV_BYTES = AT_KV_STAGES * at_kv_tiles<D>() * 1024;
+  __shared__ __align__(16) char sm_u[O_BYTES > KV_BYTES ? O_BYTES : KV_BYTES];
+  __shared__ float sm_m[NW * ROWS], sm_l[NW * ROWS];
+  __shared__ int is_last;
+  attn_unit<D, QPW, PlainMem, true, PlainMem, false, true>(a, blockIdx.x, (float*)sm_u, sm_m, sm_l, &is_last,
+                                                           nullptr, (uint16_t*)sm_u);
 }
 
 AttnPlan attn_plan(const Dims& dm, int B, int K, int max_ctx_now, int xcd, int grid) {
@@ -44,10 +60,10 @@ AttnPlan attn_plan(const Dims& dm, int B, int K, int max_ctx_now, int xcd, int g
   p.rows = K * g;
   const int qt = (p.rows + 15) / 16;
   p.qpw = (qt >= 4 && grid == 0) ? 2 : 1;
-  // 128 or more query rows per (sequence, KV head): the waves split the rows,
-  // so a K/V block is streamed once per 128 rows instead of once per 32
-  p.qs = (qt >= 8 && grid == 0 && dm.D == 128) ? 1 : 0;  // (with D = 64 its chunk statistics outgrow the LDS stage)
-  p.nqg = (qt + (p.qs ? 4 : 1) * p.qpw - 1) / ((p.qs ? 4 : 1) * p.qpw);
+  // 256 or more query rows per (sequence, KV head): the eight waves split the
+  // rows, so a K/V block is streamed once per 256 rows instead of once per 32
+  p.qs = (qt >= 16 && grid == 0 && dm.D == 128) ? 1 : 0;  // (with D = 64 its chunk statistics outgrow the LDS stage)
+  p.nqg = (qt + (p.qs ? 8 : 1) * p.qpw - 1) / ((p.qs ? 8 : 1) * p.qpw);
   const long units = (long)B * dm.Hkv * p.nqg;
   const int ctx = max_ctx_now < 1 ? 1 : max_ctx_now;
   auto chunk_for = [&](int n) {  // whole workgroup steps covering ctx in n chunks
@@ -93,7 +109,10 @@ size_t attn_partials_floats(const Dims& dm, const AttnPlan& p, int B) {
 
 template <int D, int QPW, bool QS = false>
 static void launch_attn(const AttnKArgs& a, hipStream_t st) {
-  launch_timed(attn_bf16_kernel<D, QPW, QS>, dim3(attn_items(a)), dim3(AtShape<QPW>::THREADS), st, a);
+  if constexpr (QS)
+    launch_timed(attn_qs_kernel<D, QPW>, dim3(attn_items(a)), dim3(AtShape<QPW, true>::THREADS), st, a);
+  else
+    launch_timed(attn_bf16_kernel<D, QPW>, dim3(attn_items(a)), dim3(AtShape<QPW>::THREADS), st, a);
 }
 
 AttnKArgs attn_args(const Dims& dm, const AttnPlan& p, int B, int K, const int* f, const void* q, size_t q_plane,

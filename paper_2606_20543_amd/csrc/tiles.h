@@ -8,6 +8,9 @@
 // data without L2 write-back or invalidation).
 #pragma once
 
+#include <type_traits>
+#include <utility>
+
 #include "ssd_internal.h"
 
 namespace ssd {
@@ -31,6 +34,99 @@ typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 // finite value, in one instruction instead of about six.
 __device__ __forceinline__ uint32_t cvt2bf(float a, float b) {
   return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{a, b}, bf16x2));
+}
+
+// ---- LDS DMA pipelines ----
+// s_waitcnt with only vmcnt (six bits on gfx9) counted; expcnt and lgkmcnt left alone
+template <int V>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(V >= 0 && V < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((V & 15) | (7 << 4) | (15 << 8) | ((V >> 4) << 14));
+}
+
+// Workgroup barrier of an LDS DMA pipeline.  A release fence would make the
+// compiler drain every LDS DMA copy in flight (vmcnt(0)), also those of the
+// steps copied ahead; each wave waits for its own copies of the step about to
+// be read (wait_vmcnt) and the barrier orders the rest.  The memory clobber
+// keeps LDS accesses on their side of it.
+__device__ __forceinline__ void dma_barrier() { asm volatile("s_barrier" ::: "memory"); }
+
+// 16 bytes per lane from buffer r at (voff + soff) into LDS at lds + 16 * lane
+__device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t r, uint16_t* lds, int voff, int soff) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (__attribute__((address_space(3))) void*)lds, 16, voff, soff, 0, 0);
+#else
+  (void)r, (void)lds, (void)voff, (void)soff;
+#endif
+}
+
+// raw buffer resource over 2 GiB from b
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t raw_rsrc(const void* b) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(b), 0, 0x7FFFFFFF, 0x00020000);
+}
+
+// LDS byte address of a pointer into a __shared__ array
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
+}
+
+// 16-byte LDS read at a constant byte offset from addr (the instruction's
+// offset field), issued as an instruction of its own.  The compiler would
+// make a plain LDS load wait for every LDS DMA copy in flight (it cannot tell
+// which LDS bytes a copy writes), which drains the copies of the blocks
+// fetched ahead; these reads are ordered by lgkm_wait instead, and the
+// barrier of each step keeps them clear of the copies into the same buffer.
+template <int OFF>
+__device__ __forceinline__ u32x4 ds_read16_at(uint32_t addr) {
+  static_assert(OFF >= 0 && OFF < 65536, "ds_read offset field");
+  u32x4 v;
+#if defined(__HIP_DEVICE_COMPILE__)
+  asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(v) : "v"(addr), "i"(OFF));
+#else
+  (void)addr;
+  v = u32x4{0u, 0u, 0u, 0u};
+#endif
+  return v;
+}
+
+// 1 KiB tiles FIRST .. FIRST + N - 1 of the LDS block at addr into dst[0 .. N - 1]
+template <int FIRST, int... I>
+__device__ __forceinline__ void ds_read_tiles(u32x4* dst, uint32_t addr, std::integer_sequence<int, I...>) {
+  ((dst[I] = ds_read16_at<(FIRST + I) * 1024>(addr)), ...);
+}
+
+// waits until at most min(n, MAXB) groups of PER loads of this wave are
+// outstanding (n known only at run time; vmcnt takes an immediate)
+template <int PER, int MAXB>
+__device__ __forceinline__ void wait_vm_groups(int n) {
+  if constexpr (MAXB == 0) {
+    (void)n;
+    wait_vmcnt<0>();
+  } else {
+    if (n >= MAXB)
+      wait_vmcnt<MAXB * PER>();
+    else
+      wait_vm_groups<PER, MAXB - 1>(n);
+  }
+}
+
+// waits until at most N LDS operations of this wave are outstanding; the
+// registers passed are tied to the wait, so no use of them moves above it
+template <int N, int R>
+__device__ __forceinline__ void lgkm_wait(u32x4 (&r)[R]) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  static_assert(N >= 0 && N < 16, "lgkmcnt range");
+  if constexpr (R == 4)
+    asm volatile("s_waitcnt lgkmcnt(%4)" : "+v"(r[0]), "+v"(r[1]), "+v"(r[2]), "+v"(r[3]) : "n"(N));
+  else if constexpr (R == 8)
+    asm volatile("s_waitcnt lgkmcnt(%8)"
+                 : "+v"(r[0]), "+v"(r[1]), "+v"(r[2]), "+v"(r[3]), "+v"(r[4]), "+v"(r[5]), "+v"(r[6]), "+v"(r[7])
+                 : "n"(N));
+  else
+    static_assert(R == 4 || R == 8, "register groups of 4 or 8");
+#else
+  (void)r;
+#endif
 }
 
 // Every access names a base pointer and a byte offset from it.  The base is
@@ -497,19 +593,45 @@ __device__ __forceinline__ void load_kv(KVTile<D>& t, const uint16_t* kbase, con
     t.v[dt] = Mem::ld16(vbase, (((size_t)dt * (Lmax >> 5) + (kb >> 5)) * 512 + lane * 8) * 2);
 }
 
+// max over lanes l, l ^ 16, l ^ 32 and l ^ 48 by gfx950's lane-swap
+// instructions (VALU, no LDS round trip): permlane32_swap of v with itself
+// leaves v[l] and v[l ^ 32] in the pair of every lane, permlane16_swap the
+// same for l ^ 16
+__device__ __forceinline__ float max_xor16_32(float v) {
+  const auto a = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  const float m32 = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+  const auto b = __builtin_amdgcn_permlane16_swap(__float_as_uint(m32), __float_as_uint(m32), false, false);
+  return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
+}
+
+// lazy softmax reference (log2 units; probabilities stay within 2^8), and the
+// reference before any visible key: finite, so that exp2(-inf - m) is 0, and
+// below any score of the log2 domain
+constexpr float AT_LAZY_LOG2 = 8.f;
+constexpr float AT_M_NONE = -1e30f;
+
+struct NoWait {
+  __device__ __forceinline__ void operator()() const {}
+};
+
 // one 32-key block through the online softmax of the wave's query tiles
 // QL: the query operands come from LDS (qs: tiles (qt, kd, plane) of 1 KiB in
 // lane order) instead of registers (for callers short of registers).
 // MASK = false: every key of the block is visible to every query (the block
 // lies below the block's first position), so no causal mask is applied.
-// The O rescale runs only when some lane's running max moved (alpha != 1):
-// over long contexts the max settles and the accumulators stay untouched.
-template <int D, int QPW, bool QL = false, bool MASK = true>
+// The O rescale runs only when some lane's reference max moved (alpha != 1),
+// and the reference moves only by more than AT_LAZY_LOG2: past the first
+// blocks the accumulators stay untouched.
+// after_scores: called once after the score MFMAs are issued (the V
+// fragments' reads can start there, in the registers the K fragments held);
+// before_pv: called once before the first PV product (a wait for them)
+template <int D, int QPW, bool QL = false, bool MASK = true, class AfterS = NoWait, class BeforePV = NoWait>
 __device__ __forceinline__ void attend_block(const KVTile<D>& t, int key0, const bf16x8 (&qh)[QPW][D / 32],
                                              const bf16x8 (&ql)[QPW][D / 32], const int (&qpos)[QPW],
                                              float scale_log2, int grp, float (&m)[QPW], float (&l)[QPW],
                                              floatx4 (&O)[QPW][D / 16], const uint16_t* qs = nullptr,
-                                             int klim = 0x7fffffff) {
+                                             int klim = 0x7fffffff, AfterS after_scores = AfterS{},
+                                             BeforePV before_pv = BeforePV{}) {
   constexpr int KD = D / 32, DT = D / 16;
   floatx4 s[2][QPW];
   const uint16_t* qsl = qs + (threadIdx.x & 63) * 8;
@@ -533,10 +655,11 @@ __device__ __forceinline__ void attend_block(const KVTile<D>& t, int key0, const
       }
       s[kt][qt] = acc;
     }
+  after_scores();
 #pragma unroll
   for (int qt = 0; qt < QPW; ++qt) {
     float sv[8];
-    float mx = -INFINITY;
+    float tmax = -INFINITY;  // this lane's largest score of the block
 #pragma unroll
     for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
@@ -545,20 +668,33 @@ __device__ __forceinline__ void attend_block(const KVTile<D>& t, int key0, const
         float v = s[kt][qt][e] * scale_log2;
         if constexpr (MASK) v = (key <= qpos[qt] && key < klim) ? v : -INFINITY;
         sv[kt * 4 + e] = v;
-        mx = fmaxf(mx, v);
+        tmax = fmaxf(tmax, v);
       }
-    mx = fmaxf(mx, __shfl_xor(mx, 16));
-    mx = fmaxf(mx, __shfl_xor(mx, 32));
-    const float mnew = fmaxf(m[qt], mx);
-    const bool none = (mnew == -INFINITY);
-    // exponents are <= 0 (exp2 of -inf is 0): the hardware exp2 needs no range handling
-    const float alpha = none ? 1.f : __builtin_amdgcn_exp2f(m[qt] - mnew);
+    // The reference m moves only when a score exceeds it by more than
+    // AT_LAZY_LOG2, so the probabilities lie in [0, 2^AT_LAZY_LOG2]; O and l
+    // share the reference, so O / l is the same.  Each lane tests its own
+    // scores: the row's maximum over its four lanes and the O rescale (a
+    // read-modify-write of every accumulator) are needed only when some lane
+    // of the wave exceeds -- at a chunk's first visible keys, then rarely.
+    // m starts at AT_M_NONE, below any score: exp2 of (score - m) is then 0
+    // for masked (-inf) scores, and the first visible score moves m.
+    if (__builtin_amdgcn_ballot_w64(tmax > m[qt] + AT_LAZY_LOG2) != 0) {
+      const float mx = max_xor16_32(tmax);
+      const bool move = mx > m[qt] + AT_LAZY_LOG2;
+      const float mnew = move ? mx : m[qt];
+      const float alpha = __builtin_amdgcn_exp2f(m[qt] - mnew);  // 1 where m stays, 0 from AT_M_NONE
+      l[qt] *= alpha;
+      m[qt] = mnew;
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) O[qt][dt] *= alpha;
+    }
     float ps = 0.f;
     u32x4 pv, pw;  // hi / lo planes of the probabilities, pairs packed
 #pragma unroll
     for (int i = 0; i < 8; i += 2) {
-      const float p0 = none ? 0.f : __builtin_amdgcn_exp2f(sv[i] - mnew);
-      const float p1 = none ? 0.f : __builtin_amdgcn_exp2f(sv[i + 1] - mnew);
+      // exponents are <= AT_LAZY_LOG2 (exp2 of -inf is 0): the hardware exp2 needs no range handling
+      const float p0 = __builtin_amdgcn_exp2f(sv[i] - m[qt]);
+      const float p1 = __builtin_amdgcn_exp2f(sv[i + 1] - m[qt]);
       ps += p0;
       ps += p1;
       uint32_t h, lo;
@@ -566,14 +702,10 @@ __device__ __forceinline__ void attend_block(const KVTile<D>& t, int key0, const
       pv[i / 2] = h;
       pw[i / 2] = lo;
     }
-    l[qt] = l[qt] * alpha + ps;
-    m[qt] = mnew;
+    l[qt] += ps;
     const bf16x8 pf = __builtin_bit_cast(bf16x8, pv);
     const bf16x8 pg = __builtin_bit_cast(bf16x8, pw);
-    if (__builtin_amdgcn_ballot_w64(alpha != 1.f) != 0) {
-#pragma unroll
-      for (int dt = 0; dt < DT; ++dt) O[qt][dt] *= alpha;
-    }
+    if (qt == 0) before_pv();
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt) {
       const bf16x8 vf = __builtin_bit_cast(bf16x8, t.v[dt]);
@@ -587,11 +719,18 @@ __device__ __forceinline__ void attend_block(const KVTile<D>& t, int key0, const
 constexpr int AT_KEYS = 32;        // keys per wave step
 constexpr int AT_STEP = 128;       // chunk granularity in keys (one workgroup step)
 constexpr int AT_MAX_CHUNKS = 64;
-// four waves per workgroup: one wave per SIMD, so a wave holds two K/V blocks
-// (the one in use and the next) beside its queries and accumulators
-template <int QPW>
+// query-split units stage K/V blocks in LDS: AT_KV_STAGES buffers of one
+// 32-key block each (2 D/32 key tiles + D/16 value tiles of 1 KiB)
+constexpr int AT_KV_STAGES = 8;
+template <int D>
+constexpr int at_kv_tiles() { return 2 * (D / 32) + D / 16; }
+// key-split units: four waves per workgroup, one per SIMD, so a wave holds
+// two K/V blocks (the one in use and the next) beside its queries and
+// accumulators; query-split units: eight waves, two per SIMD, reading K/V
+// from LDS
+template <int QPW, bool QS = false>
 struct AtShape {
-  static constexpr int WAVES = 4;
+  static constexpr int WAVES = QS ? 8 : 4;
   static constexpr int THREADS = WAVES * 64;
   static constexpr int STEP = WAVES * AT_KEYS;
 };
@@ -608,17 +747,17 @@ struct AtShape {
 // Mem: queries, K/V and the output; PMem: the chunk partials; QL: queries
 // staged in LDS (sm_q, QPW * D/32 * 2 KiB) instead of registers.
 // QS: the waves split the query rows instead of the keys (a query group is
-// NW * QPW * 16 rows, every wave streams every key block of the chunk, so the
-// four waves read the same K/V at about the same time and nothing is merged
-// across waves): for query groups of many rows, whose K/V would otherwise be
-// streamed once per 16-32 rows.
+// NW * QPW * 16 rows, every wave streams every key block of the chunk from
+// LDS (sm_kv; sm_o may share its bytes) and nothing is merged across waves):
+// for query groups of many rows, whose K/V would otherwise be streamed once
+// per 16-32 rows.
 template <int D, int QPW, class Mem = PlainMem, bool PF = true, class PMem = PlainMem, bool QL = false,
           bool QS = false>
 __device__ __forceinline__ int attn_unit(const AttnKArgs& a, int item, float* sm_o, float* sm_m, float* sm_l,
-                                         int* is_last, uint16_t* sm_q = nullptr) {
+                                         int* is_last, uint16_t* sm_q = nullptr, uint16_t* sm_kv = nullptr) {
   static_assert(!(QS && QL), "query-split units keep the queries in registers");
-  constexpr int NW = AtShape<QPW>::WAVES, NTH = AtShape<QPW>::THREADS;
-  constexpr int STEP = QS ? AT_KEYS : AtShape<QPW>::STEP;  // keys between a wave's blocks
+  constexpr int NW = AtShape<QPW, QS>::WAVES, NTH = AtShape<QPW, QS>::THREADS;
+  constexpr int STEP = QS ? AT_KEYS : AtShape<QPW, QS>::STEP;  // keys between a wave's blocks
   constexpr int KD = D / 32;   // 32-wide k steps over the head dimension
   constexpr int DT = D / 16;   // 16-row d tiles of O^T
   constexpr int WROWS = QPW * 16;               // query rows of one wave
@@ -669,7 +808,7 @@ __device__ __forceinline__ int attn_unit(const AttnKArgs& a, int item, float* sm
   // at the join): rows past the cache are clamped, and a block past the chunk
   // is loaded but never used.
   KVTile<D> ta, tb;
-  load_kv<D, Mem>(ta, kbase, vbase, first, a.Lmax, lane);
+  if constexpr (!QS) load_kv<D, Mem>(ta, kbase, vbase, first, a.Lmax, lane);
 
   // query fragments (B operand of S^T = K Q^T): lane holds row col of tile qt, d = 8*grp.. (+32 kd);
   // q is fp32 carried as hi + lo bf16 operands
@@ -717,34 +856,75 @@ __device__ __forceinline__ int attn_unit(const AttnKArgs& a, int item, float* sm
   floatx4 O[QPW][DT];
 #pragma unroll
   for (int qt = 0; qt < QPW; ++qt) {
-    m[qt] = -INFINITY;
+    m[qt] = AT_M_NONE;
     l[qt] = 0.f;
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt) O[qt][dt] = floatx4{0.f, 0.f, 0.f, 0.f};
   }
 
-  if constexpr (PF && QS) {
-    // long streams (query split): two tiles in turn, block it from one while
-    // the next loads into the other, with no copy between them (a tile copy
-    // per block cost about a hundred register moves).  An odd count is padded
-    // with one block past the chunk, masked entirely (keys >= kend), so every
-    // load is unconditional and stays in flight.  Blocks wholly below the
-    // frontier need no mask.  (Short streams keep the copying loop below: the
-    // padding block costs them more than the copies.)
-    auto attend = [&](const KVTile<D>& t, int itx) {
-      const int key0 = first + itx * STEP;
-      if (itx < nit && key0 + AT_KEYS <= fb)
-        attend_block<D, QPW, QL, false>(t, key0, qh, ql, qpos, a.scale_log2, grp, m, l, O, sm_q);
-      else
-        attend_block<D, QPW, QL>(t, key0, qh, ql, qpos, a.scale_log2, grp, m, l, O, sm_q, kend);
+  if constexpr (QS) {
+    // long streams (query split): every wave needs every key block of the
+    // chunk, so a block is copied once into LDS by LDS DMA (each wave copies
+    // an equal share of its 1 KiB tiles, which the caches hold in MFMA operand
+    // order) and all the waves read it from there; AT_KV_STAGES - 1 blocks
+    // are in flight while one is multiplied, and no K/V data occupies
+    // registers between blocks.  Blocks wholly below the frontier need no mask.
+    constexpr int NT = at_kv_tiles<D>(), TPW = NT / NW, NST = AT_KV_STAGES;
+    static_assert(NT % NW == 0 && TPW >= 1, "K/V tiles split evenly over the waves");
+    const __amdgpu_buffer_rsrc_t krs = raw_rsrc(kbase), vrs = raw_rsrc(vbase);
+    const int wv = __builtin_amdgcn_readfirstlane(wave);
+    auto issue = [&](int c) {
+      const int key0 = first + c * STEP;
+      const int kb = key0 < a.Lmax - AT_KEYS ? key0 : a.Lmax - AT_KEYS;  // rows past the cache: clamped, masked
+      uint16_t* st = sm_kv + (size_t)(c % NST) * NT * 512;
+#pragma unroll
+      for (int j = 0; j < TPW; ++j) {
+        const int i = wv * TPW + j;  // tile i: key tiles (kt, kd) first, then value tiles dt
+        if (i < 2 * KD)
+          dma16(krs, st + i * 512, lane * 16, (((kb >> 4) + i / KD) * KD + i % KD) * 1024);
+        else
+          dma16(vrs, st + i * 512, lane * 16, ((i - 2 * KD) * (a.Lmax >> 5) + (kb >> 5)) * 1024);
+      }
     };
-    for (int it = 0; it < nit; it += 2) {
-      const int key0 = first + it * STEP;
-      load_kv<D, Mem>(tb, kbase, vbase, key0 + STEP, a.Lmax, lane);
-      attend(ta, it);
-      load_kv<D, Mem>(ta, kbase, vbase, key0 + 2 * STEP, a.Lmax, lane);
-      attend(tb, it + 1);
-    }
+    const uint32_t kv0 = lds_addr(sm_kv) + lane * 16;
+    auto attend = [&](int c, auto mask) {
+      constexpr bool MASK = decltype(mask)::value;
+      const uint32_t st = kv0 + (uint32_t)((c % NST) * NT * 1024);
+      KVTile<D> t;
+      u32x4(&kf)[2 * KD] = *reinterpret_cast<u32x4(*)[2 * KD]>(&t.k);
+      ds_read_tiles<0>(kf, st, std::make_integer_sequence<int, 2 * KD>{});
+      lgkm_wait<0>(kf);
+      // the value tiles are read once the score MFMAs are issued, into the
+      // registers the key tiles held: K and V are never live together
+      auto read_v = [&]() {
+        __builtin_amdgcn_sched_barrier(0);
+        ds_read_tiles<2 * KD>(t.v, st, std::make_integer_sequence<int, DT>{});
+        __builtin_amdgcn_sched_barrier(0);  // the reads go out before the softmax
+      };
+      auto wait_v = [&]() {
+        __builtin_amdgcn_sched_barrier(0);  // the softmax stays above the wait
+        lgkm_wait<0>(t.v);
+      };
+      attend_block<D, QPW, false, MASK>(t, first + c * STEP, qh, ql, qpos, a.scale_log2, grp, m, l, O, nullptr,
+                                        kend, read_v, wait_v);
+    };
+    auto step = [&](int c, auto mask) {
+      // this wave's copies of block c are done (those of the up to NST - 2
+      // later blocks already issued may not be)
+      wait_vm_groups<TPW, NST - 2>(nit - 1 - c);
+      // every wave's copies of block c are visible, and every wave is done with
+      // block c - 1, whose buffer takes block c + NST - 1
+      dma_barrier();
+      if (c + NST - 1 < nit) issue(c + NST - 1);
+      attend(c, mask);
+    };
+    // the blocks wholly below the frontier come first: one loop without the
+    // mask, then the rest with it (two loops, not a branch per block, keep the
+    // register assignment of each loop fixed)
+    const int nfull = fb - first >= AT_KEYS ? min(nit, (fb - first - AT_KEYS) / STEP + 1) : 0;
+    for (int c = 0; c < NST - 1 && c < nit; ++c) issue(c);
+    for (int c = 0; c < nfull; ++c) step(c, std::false_type{});
+    for (int c = nfull; c < nit; ++c) step(c, std::true_type{});
   } else if constexpr (PF) {
     // the next block is loaded before the current one is used and taken over
     // at the end of every iteration (an unconditional use: the compiler can
@@ -769,6 +949,7 @@ __device__ __forceinline__ int attn_unit(const AttnKArgs& a, int item, float* sm
 
   // stage this wave's triple: O^T accumulator element e of tile (qt, dt) is row
   // qt*16 + col, dims dt*16 + 4*grp + e
+  if constexpr (QS) __syncthreads();  // every wave is done with the K/V stages sm_o may overlay
 #pragma unroll
   for (int qt = 0; qt < QPW; ++qt) {
     l[qt] += __shfl_xor(l[qt], 16);
