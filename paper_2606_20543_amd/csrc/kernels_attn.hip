@@ -38,13 +38,14 @@ void attn_bf16_kernel(AttnKArgs a) {
   attn_unit<D, QPW, PlainMem, true, PlainMem, false, false>(a, blockIdx.x, sm_o, sm_m, sm_l, &is_last);
 }
 
-// query split: eight waves, two per SIMD (at most 256 registers each), the
-// K/V stages and the output stage in the same LDS bytes (used one after the
-// other)
+// query split: two workgroups per CU, so each SIMD runs waves of two
+// workgroups that meet no common barrier (at most 256 registers each; the
+// K/V stages and the output stage share their LDS bytes, used one after the
+// other, 68 KB per workgroup)
 template <int D, int QPW>
-__global__ __launch_bounds__((AtShape<QPW, true>::THREADS)) __attribute__((amdgpu_waves_per_eu(2, 2)))
+__global__ __launch_bounds__(AtShape<QPW>::THREADS) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void attn_qs_kernel(AttnKArgs a) {
-  constexpr int NW = AtShape<QPW, true>::WAVES, ROWS = QPW * 16, RS = D + 4;
+  constexpr int NW = AtShape<QPW>::WAVES, ROWS = QPW * 16, RS = D + 4;
   constexpr int O_BYTES = NW * ROWS * RS * 4, KV_BYTES = AT_KV_STAGES * at_kv_tiles<D>() * 1024;
   __shared__ __align__(16) char sm_u[O_BYTES > KV_BYTES ? O_BYTES : KV_BYTES];
   __shared__ float sm_m[NW * ROWS], sm_l[NW * ROWS];
@@ -60,10 +61,10 @@ AttnPlan attn_plan(const Dims& dm, int B, int K, int max_ctx_now, int xcd, int g
   p.rows = K * g;
   const int qt = (p.rows + 15) / 16;
   p.qpw = (qt >= 4 && grid == 0) ? 2 : 1;
-  // 256 or more query rows per (sequence, KV head): the eight waves split the
-  // rows, so a K/V block is streamed once per 256 rows instead of once per 32
-  p.qs = (qt >= 16 && grid == 0 && dm.D == 128) ? 1 : 0;  // (with D = 64 its chunk statistics outgrow the LDS stage)
-  p.nqg = (qt + (p.qs ? 8 : 1) * p.qpw - 1) / ((p.qs ? 8 : 1) * p.qpw);
+  // 128 or more query rows per (sequence, KV head): the waves split the rows,
+  // so a K/V block is streamed once per 128 rows instead of once per 32
+  p.qs = (qt >= 8 && grid == 0 && dm.D == 128) ? 1 : 0;  // (with D = 64 its chunk statistics outgrow the LDS stage)
+  p.nqg = (qt + (p.qs ? 4 : 1) * p.qpw - 1) / ((p.qs ? 4 : 1) * p.qpw);
   const long units = (long)B * dm.Hkv * p.nqg;
   const int ctx = max_ctx_now < 1 ? 1 : max_ctx_now;
   auto chunk_for = [&](int n) {  // whole workgroup steps covering ctx in n chunks
@@ -71,7 +72,7 @@ AttnPlan attn_plan(const Dims& dm, int B, int K, int max_ctx_now, int xcd, int g
     return ((per + AT_STEP - 1) / AT_STEP) * AT_STEP;
   };
   int best = 1;
-  const long slots = grid > 0 ? grid : 256;
+  const long slots = grid > 0 ? grid : (p.qs ? 512 : 256);  // query split: two workgroups per CU
   if (units >= slots) {
     // many query groups: the chip is full, chunks only bound the per-workgroup stream
     int chunk = AT_STEP;
@@ -110,7 +111,7 @@ size_t attn_partials_floats(const Dims& dm, const AttnPlan& p, int B) {
 template <int D, int QPW, bool QS = false>
 static void launch_attn(const AttnKArgs& a, hipStream_t st) {
   if constexpr (QS)
-    launch_timed(attn_qs_kernel<D, QPW>, dim3(attn_items(a)), dim3(AtShape<QPW, true>::THREADS), st, a);
+    launch_timed(attn_qs_kernel<D, QPW>, dim3(attn_items(a)), dim3(AtShape<QPW>::THREADS), st, a);
   else
     launch_timed(attn_bf16_kernel<D, QPW>, dim3(attn_items(a)), dim3(AtShape<QPW>::THREADS), st, a);
 }

@@ -290,11 +290,11 @@ struct AttnPlan {
   int chunk;      // keys per workgroup
   int nchunk;     // chunks covering max context
   int qpw;        // query tiles per wave
-  int qs = 0;     // 1: the waves split the query rows (query group = 8 * qpw tiles), else the keys
+  int qs = 0;     // 1: the waves split the query rows (query group = 4 * qpw tiles), else the keys
   int nqg;        // query groups
   int rows;       // query rows per (b, kv head) = K * g
   int xcd;        // see xcd_grid
-  int group_rows() const { return (qs ? 8 : 1) * qpw * 16; }
+  int group_rows() const { return (qs ? 4 : 1) * qpw * 16; }
 };
 // grid > 0: a plan for the persistent forward pass (one query tile per work
 // item, items fitting `grid` workgroups where possible)

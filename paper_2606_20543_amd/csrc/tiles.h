@@ -639,22 +639,26 @@ __device__ __forceinline__ void attend_block(const KVTile<D>& t, int key0, const
 #pragma unroll
   for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
-    for (int qt = 0; qt < QPW; ++qt) {
-      floatx4 acc = floatx4{0.f, 0.f, 0.f, 0.f};
+    for (int qt = 0; qt < QPW; ++qt) s[kt][qt] = floatx4{0.f, 0.f, 0.f, 0.f};
+  // k steps and planes outermost: the 2 QPW accumulators take turns, so no
+  // MFMA waits on the one just issued (each accumulator still sums kd = 0,
+  // 1, ... with the hi plane before the lo plane)
 #pragma unroll
-      for (int kd = 0; kd < KD; ++kd) {
-        const bf16x8 kf = __builtin_bit_cast(bf16x8, t.k[kt][kd]);
-        bf16x8 a = qh[qt][kd], b = ql[qt][kd];
-        if constexpr (QL) {
-          const uint16_t* p = qsl + ((size_t)(qt * KD + kd) * 2) * 512;
-          a = __builtin_bit_cast(bf16x8, *(const u32x4*)p);
-          b = __builtin_bit_cast(bf16x8, *(const u32x4*)(p + 512));
+  for (int kd = 0; kd < KD; ++kd)
+#pragma unroll
+    for (int pl = 0; pl < 2; ++pl)
+#pragma unroll
+      for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+        for (int qt = 0; qt < QPW; ++qt) {
+          const bf16x8 kf = __builtin_bit_cast(bf16x8, t.k[kt][kd]);
+          bf16x8 a = pl ? ql[qt][kd] : qh[qt][kd];
+          if constexpr (QL) {
+            const uint16_t* p = qsl + ((size_t)(qt * KD + kd) * 2 + pl) * 512;
+            a = __builtin_bit_cast(bf16x8, *(const u32x4*)p);
+          }
+          s[kt][qt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, a, s[kt][qt], 0, 0, 0);
         }
-        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, a, acc, 0, 0, 0);
-        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, b, acc, 0, 0, 0);
-      }
-      s[kt][qt] = acc;
-    }
   after_scores();
 #pragma unroll
   for (int qt = 0; qt < QPW; ++qt) {
@@ -706,12 +710,14 @@ __device__ __forceinline__ void attend_block(const KVTile<D>& t, int key0, const
     const bf16x8 pf = __builtin_bit_cast(bf16x8, pv);
     const bf16x8 pg = __builtin_bit_cast(bf16x8, pw);
     if (qt == 0) before_pv();
+    // the hi plane into every accumulator, then the lo plane (each O tile
+    // still takes hi before lo, and no MFMA waits on the one just issued)
 #pragma unroll
-    for (int dt = 0; dt < DT; ++dt) {
-      const bf16x8 vf = __builtin_bit_cast(bf16x8, t.v[dt]);
-      O[qt][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf, O[qt][dt], 0, 0, 0);
-      O[qt][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pg, O[qt][dt], 0, 0, 0);
-    }
+    for (int dt = 0; dt < DT; ++dt)
+      O[qt][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, t.v[dt]), pf, O[qt][dt], 0, 0, 0);
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt)
+      O[qt][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, t.v[dt]), pg, O[qt][dt], 0, 0, 0);
   }
 }
 
@@ -721,16 +727,15 @@ constexpr int AT_STEP = 128;       // chunk granularity in keys (one workgroup s
 constexpr int AT_MAX_CHUNKS = 64;
 // query-split units stage K/V blocks in LDS: AT_KV_STAGES buffers of one
 // 32-key block each (2 D/32 key tiles + D/16 value tiles of 1 KiB)
-constexpr int AT_KV_STAGES = 8;
+constexpr int AT_KV_STAGES = 4;
 template <int D>
 constexpr int at_kv_tiles() { return 2 * (D / 32) + D / 16; }
-// key-split units: four waves per workgroup, one per SIMD, so a wave holds
-// two K/V blocks (the one in use and the next) beside its queries and
-// accumulators; query-split units: eight waves, two per SIMD, reading K/V
-// from LDS
-template <int QPW, bool QS = false>
+// four waves per workgroup (key-split units: one workgroup per CU, so a wave
+// holds two K/V blocks, the one in use and the next, beside its queries and
+// accumulators; query-split units: two workgroups per CU, K/V read from LDS)
+template <int QPW>
 struct AtShape {
-  static constexpr int WAVES = QS ? 8 : 4;
+  static constexpr int WAVES = 4;
   static constexpr int THREADS = WAVES * 64;
   static constexpr int STEP = WAVES * AT_KEYS;
 };
@@ -756,8 +761,8 @@ template <int D, int QPW, class Mem = PlainMem, bool PF = true, class PMem = Pla
 __device__ __forceinline__ int attn_unit(const AttnKArgs& a, int item, float* sm_o, float* sm_m, float* sm_l,
                                          int* is_last, uint16_t* sm_q = nullptr, uint16_t* sm_kv = nullptr) {
   static_assert(!(QS && QL), "query-split units keep the queries in registers");
-  constexpr int NW = AtShape<QPW, QS>::WAVES, NTH = AtShape<QPW, QS>::THREADS;
-  constexpr int STEP = QS ? AT_KEYS : AtShape<QPW, QS>::STEP;  // keys between a wave's blocks
+  constexpr int NW = AtShape<QPW>::WAVES, NTH = AtShape<QPW>::THREADS;
+  constexpr int STEP = QS ? AT_KEYS : AtShape<QPW>::STEP;  // keys between a wave's blocks
   constexpr int KD = D / 32;   // 32-wide k steps over the head dimension
   constexpr int DT = D / 16;   // 16-row d tiles of O^T
   constexpr int WROWS = QPW * 16;               // query rows of one wave
