@@ -24,6 +24,9 @@ stays within seconds.  Cases:
       rule on the GPU's own logits is checked for all eight
   7B width, batch 1, a 32-token block at context 1120..1152 (the last row of
       the 32x32 workload), 2 rounds + commit
+  8B width, batch 2, a 40-token block at context 600..640: 160 query rows per
+      (sequence, KV head), so the query-split attention runs one full 128-row
+      group and one of 32 rows whose other 96 are padding
   1B width, batch 4, 64-token prompt and a 64-token block (M = 256, prefill
       and verify): tiled GEMMs whose K range is split over workgroups to
       fill the CUs (O and down projections in 4 splits, QKV in 2), rule (A),
@@ -163,6 +166,12 @@ def test_8b_width_batch8_context_4352(pair8):
         assert stats["flips"] <= 0.02 * 2 * K + 1
     finally:
         ssd.ssd_free_session(sess)
+
+
+def test_8b_width_ragged_query_split(pair8):
+    """The query-split attention with a partial query group (rows past K*g masked
+    and never stored) and short key chunks."""
+    _greedy_block(pair8, W8, B=2, P=600, K=40, rounds=1, keep=0.6, seed_stream=21)
 
 
 def test_7b_width_context_1152(pair7):
