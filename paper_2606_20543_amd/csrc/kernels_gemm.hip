@@ -16,6 +16,9 @@
 // each A tile meets two B operands.  When N/64 feature blocks cannot fill
 // 256 CUs the K range is split; the last workgroup of a feature block sums
 // the partials in split order (deterministic) and runs the epilogue.
+#include <cstdlib>
+#include <cstring>
+
 #include "tiles.h"
 
 namespace ssd {
@@ -738,10 +741,284 @@ __global__ __launch_bounds__(256, 2) void gemm_tile_kernel(GemmKArgs a) {
   }
 }
 
+// ---------------- wide tiles with the token rows through an LDS DMA ring ----------------
+// Eight waves (two per SIMD, one workgroup per CU) own a 128-row x 256-feature
+// output tile: 2 (rows) x 4 (features) waves of 64 x 64, the same wave tile
+// and weight path as gemm_tile_kernel<4, 3> (each wave's packed weight
+// fragments straight to registers, two 64-input stages ahead in three
+// register slots).  The token rows of a stage (both planes) are shared by
+// all eight waves and come by LDS DMA into a ring of three stages, two stages
+// ahead of use: a DMA instruction fills eight rows x 128 bytes (whole cache
+// lines), its lanes choosing the global chunk so that LDS holds the rows in
+// the swizzled layout the operand reads expect (chunk c of row r at c ^
+// ((r >> 1) & 7)).  Against the 128 x 128 tiles at two workgroups per CU
+// the token rows cross the L2 once per 256 features instead of once per 128
+// and arrive a stage earlier, without register staging.  The operand reads
+// are issued as separate instructions with their own waits, so that the
+// compiler does not make them wait for every LDS DMA copy in flight.
+constexpr int T8_STAGES = 3, T8_THREADS = 512, T8_NT = 4;
+constexpr int T8_STAGE_BYTES = 2 * TILE_PL * 2;  // one stage: both planes, 32 KiB
+
+// the eight token operand fragments of one k-block at addr: [mt * 2 + plane],
+// row tiles 16 rows (2 KiB) apart, the planes TILE_PL elements apart
+__device__ __forceinline__ void ds_read_tiles2(u32x4 (&x)[8], uint32_t addr) {
+  constexpr int PL = TILE_PL * 2, RT = 16 * TILE_LD * 2;
+  x[0] = ds_read16_at<0>(addr);
+  x[1] = ds_read16_at<PL>(addr);
+  x[2] = ds_read16_at<RT>(addr);
+  x[3] = ds_read16_at<PL + RT>(addr);
+  x[4] = ds_read16_at<2 * RT>(addr);
+  x[5] = ds_read16_at<PL + 2 * RT>(addr);
+  x[6] = ds_read16_at<3 * RT>(addr);
+  x[7] = ds_read16_at<PL + 3 * RT>(addr);
+}
+
+struct T8W {
+  u32x4 w[T8_NT][2];  // weight fragments: 4 feature tiles x 2 k-blocks of one stage
+};
+
+__global__ __launch_bounds__(T8_THREADS) __attribute__((amdgpu_waves_per_eu(2, 2)))
+void gemm_tile8_kernel(GemmKArgs a) {
+  constexpr int NT = T8_NT;
+  __shared__ __attribute__((aligned(16))) uint16_t xs[T8_STAGES * 2 * TILE_PL];
+  __shared__ float rscale[TILE_ROWS];
+  __shared__ float sq_red[4][TILE_ROWS];
+  __shared__ int is_last;
+  const int m_tiles = (a.M + TILE_ROWS - 1) / TILE_ROWS;
+  int fb, member;
+  xcd_unmap(blockIdx.x, m_tiles * a.S, a.xcd, fb, member);
+  if (fb >= a.n_fb) return;
+  const int mtile = member / a.S, split = member - mtile * a.S;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
+  const int wm = w & 1, wn = w >> 1;
+  const int r0 = mtile * TILE_ROWS;
+  const int nb0 = fb * 4 * NT + wn * NT;  // first 16-feature tile of this wave
+  const int t0w = a.t0 + r0 + wm * 64;
+  const int Mw = a.M - r0 - wm * 64 < 64 ? a.M - r0 - wm * 64 : 64;
+  const int Mt = a.M - r0 < TILE_ROWS ? a.M - r0 : TILE_ROWS;
+  const EpiArgs& e = a.epi;
+  const int nst = a.K / TILE_KT / a.S, st0 = split * nst;
+
+  floatx4 acc[NT][4];
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+    for (int mt = 0; mt < 4; ++mt) acc[nt][mt] = floatx4{0.f, 0.f, 0.f, 0.f};
+
+  const __amdgpu_buffer_rsrc_t xh = tile_rsrc(a.in), xl = tile_rsrc(a.in + a.in_plane), wr = tile_rsrc(a.W);
+  // token DMA: a stage is 32 instructions (2 planes x 16 blocks of 8 rows),
+  // four per wave; lane l of block rb takes row rb * 8 + l / 8 and stored
+  // chunk l % 8, i.e. the logical chunk (l % 8) ^ ((row >> 1) & 7) (rows past
+  // M repeat row M - 1; their results are never stored)
+  int xoff[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int i = w * 4 + j, rb = i & 15;
+    const int row = rb * 8 + (lane >> 3);
+    const int r = r0 + row;
+    const int c = (lane & 7) ^ ((row >> 1) & 7);
+    xoff[j] = ((r < a.M ? r : a.M - 1) * a.ld_in + c * 8) * 2;
+  }
+  auto issue_x = [&](int stage) {
+    uint16_t* dst = xs + (size_t)(stage % T8_STAGES) * 2 * TILE_PL;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int i = w * 4 + j, pl = i >> 4, rb = i & 15;
+      dma16(pl ? xl : xh, dst + pl * TILE_PL + rb * 512, xoff[j], (st0 + stage) * TILE_KT * 2);
+    }
+  };
+  const int lane_b = lane * 16, wtile_b = nb0 * a.KB * 1024;
+  auto load_w = [&](T8W& s, int stage) {
+    const int kb0 = (st0 + stage) * TILE_KT / 32;
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+        s.w[nt][kb] = __builtin_amdgcn_raw_buffer_load_b128(wr, lane_b, wtile_b + (nt * a.KB + kb0 + kb) * 1024, 0);
+  };
+  // operand reads: row wm * 64 + lane % 16 (+ 16 mt), logical chunk kb * 4 +
+  // lane / 16 stored at that ^ ((row >> 1) & 7), which no mt changes
+  const uint32_t xs0 = lds_addr(xs);
+  uint32_t xrd[2];
+#pragma unroll
+  for (int kb = 0; kb < 2; ++kb)
+    xrd[kb] = xs0 + (uint32_t)(((wm * 64 + (lane & 15)) * TILE_LD +
+                                (((kb * 4 + (lane >> 4)) ^ ((lane & 15) >> 1)) * 8)) * 2);
+  auto mma = [&](const T8W& s, int stage) {
+    const uint32_t so = (uint32_t)((stage % T8_STAGES) * T8_STAGE_BYTES);
+    u32x4 x0[8], x1[8];  // [mt * 2 + plane] of k-block 0, then 1
+    ds_read_tiles2(x0, xrd[0] + so);
+    ds_read_tiles2(x1, xrd[1] + so);
+    lgkm_wait<8>(x0);
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+      for (int mt = 0; mt < 4; ++mt) {
+        const bf16x8 wf = __builtin_bit_cast(bf16x8, s.w[nt][0]);
+        acc[nt][mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf, __builtin_bit_cast(bf16x8, x0[mt * 2]), acc[nt][mt], 0, 0, 0);
+        acc[nt][mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf, __builtin_bit_cast(bf16x8, x0[mt * 2 + 1]), acc[nt][mt], 0, 0, 0);
+      }
+    __builtin_amdgcn_sched_barrier(0);  // the first k-block's MFMAs stay above the second wait
+    lgkm_wait<0>(x1);
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+      for (int mt = 0; mt < 4; ++mt) {
+        const bf16x8 wf = __builtin_bit_cast(bf16x8, s.w[nt][1]);
+        acc[nt][mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf, __builtin_bit_cast(bf16x8, x1[mt * 2]), acc[nt][mt], 0, 0, 0);
+        acc[nt][mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf, __builtin_bit_cast(bf16x8, x1[mt * 2 + 1]), acc[nt][mt], 0, 0, 0);
+      }
+  };
+
+  // prologue: stages 0 and 1 in flight (tokens and weights), then the tile's
+  // 1/rms (its scratch is the third ring buffer, first written by stage 2's
+  // copies after the first barrier below)
+  T8W w0, w1, w2;
+  issue_x(0);
+  load_w(w0, 0);
+  if (nst > 1) {
+    issue_x(1);
+    load_w(w1, 1);
+  }
+  if (e.ssq)
+    rms_prologue<TILE_ROWS, T8_THREADS>(e, Mt, a.t0 + r0, (float(*)[TILE_ROWS])(void*)(xs + 2 * 2 * TILE_PL), rscale);
+  else if (tid < TILE_ROWS)
+    rscale[tid] = 1.f;
+  // stage c: this wave's copies of stage c are done (those issued after them:
+  // its weights, and stage c + 1's copies and weights when there is one), the
+  // barrier publishes everyone's copies and tells that every wave is done with
+  // stage c - 1, whose ring buffer and weight slot then take stage c + 2
+  auto step = [&](int c, const T8W& cur, T8W& ahead2, bool more) {
+    if (more) {
+      wait_vmcnt<20>();
+      dma_barrier();
+      issue_x(c + 2);
+      load_w(ahead2, c + 2);
+    } else {
+      if (c + 1 < nst)
+        wait_vmcnt<20>();
+      else
+        wait_vmcnt<8>();
+      dma_barrier();
+    }
+    mma(cur, c);
+  };
+  int c = 0;
+  for (; c + 5 <= nst; c += 3) {
+    step(c, w0, w2, true);
+    step(c + 1, w1, w0, true);
+    step(c + 2, w2, w1, true);
+  }
+  // 1 to 4 stages left, stage c in slot w0
+  if (c < nst) step(c, w0, w2, c + 2 < nst);
+  if (c + 1 < nst) step(c + 1, w1, w0, c + 3 < nst);
+  if (c + 2 < nst) step(c + 2, w2, w1, false);
+  if (c + 3 < nst) step(c + 3, w0, w2, false);
+
+  if (a.S > 1) {
+    // split-K: publish this split's fragments; the last arrival of the tile
+    // sums all splits in split order (deterministic)
+    const int grp = fb * m_tiles + mtile;
+    constexpr int FRAG = NT * 4 * 64 * 4;  // floats per wave
+    float* P = a.part + ((size_t)grp * a.S * 8 + w) * FRAG + lane * 4;
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+      for (int mt = 0; mt < 4; ++mt) *(floatx4*)(P + (size_t)split * 8 * FRAG + (nt * 4 + mt) * 256) = acc[nt][mt];
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    if (tid == 0) {
+      if (!a.xcd) __threadfence();  // splits on different XCDs: write back through L2
+      const unsigned prev = atomicAdd(&a.counters[grp], 1u);
+      is_last = prev == (unsigned)(a.S - 1);
+      if (is_last && !a.xcd) __threadfence();
+    }
+    __syncthreads();
+    if (!is_last) return;
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+      for (int mt = 0; mt < 4; ++mt) acc[nt][mt] = floatx4{0.f, 0.f, 0.f, 0.f};
+    for (int sp = 0; sp < a.S; ++sp) {
+      floatx4 v[NT][4];
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+        for (int mt = 0; mt < 4; ++mt) v[nt][mt] = *(const floatx4*)(P + (size_t)sp * 8 * FRAG + (nt * 4 + mt) * 256);
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+        for (int mt = 0; mt < 4; ++mt) acc[nt][mt] += v[nt][mt];
+    }
+    if (tid == 0) a.counters[grp] = 0u;
+  }
+
+  float sq[4] = {0.f, 0.f, 0.f, 0.f};
+  if (Mw > 0) {
+    EpiOps<NT, 4> op;
+    epi_block_starts<NT, 4>(e, Mw, t0w, lane, op);
+    epi_load<NT, 4>(e, nb0, a.N, Mw, t0w, lane, op);
+    epi_store<NT, 4>(e, acc, op, nb0, a.N, Mw, t0w, lane, rscale + wm * 64, sq);
+  }
+  if (e.kind == EPI_RESID) {
+    // per-row sums of x^2 over this tile's features: lanes of one row, then
+    // the four waves of one row half, in a fixed order
+#pragma unroll
+    for (int mt = 0; mt < 4; ++mt) {
+      float v = sq[mt];
+      v += __shfl_xor(v, 16);
+      v += __shfl_xor(v, 32);
+      if (lane < 16) sq_red[wn][wm * 64 + mt * 16 + lane] = v;
+    }
+    __syncthreads();
+    if (tid < Mt)
+      e.ssq_out[(size_t)fb * e.ssq_out_ld + a.t0 + r0 + tid] =
+          ((sq_red[0][tid] + sq_red[1][tid]) + sq_red[2][tid]) + sq_red[3][tid];
+  }
+}
+
+// the 128 x 256 LDS-DMA tiles where they apply (SSD_GEMM_T8=0 keeps every
+// plan on the 128 x 128 tiles, for comparisons)
+static bool tile8_enabled() {
+  static const bool on = [] {
+    const char* v = std::getenv("SSD_GEMM_T8");
+    return !(v && std::strcmp(v, "0") == 0);
+  }();
+  return on;
+}
+
 GemmPlan gemm_plan_bf16(int M, int N, int K, int xcd) {
   GemmPlan p;
   p.xcd = xcd;
   p.tile = 0;
+  if (M > 64 && K % (2 * TILE_KT) == 0 && N % 256 == 0 && (size_t)N * K * 2 < (1ull << 31) && tile8_enabled()) {
+    // 128 x 256 tiles, eight waves, token rows by LDS DMA, one workgroup per
+    // CU: K split by the largest divisor of the stage count that keeps the
+    // grid within 256 workgroups, wherever each workgroup still runs at least
+    // 32 stages.  Measured on the 8B shapes at 512 rows against the 128 x 128
+    // tiles: gate/up 269 -> 236 us, down 167 -> 127, output layer 274 -> 248,
+    // QKV 82 -> 79; O (16 stages per workgroup) 55 -> 62, so it stays on them.
+    const int mt = (M + TILE_ROWS - 1) / TILE_ROWS;
+    const int nfb = N / 256, nst = K / TILE_KT;
+    int S = 1;
+    for (int s = 2; s <= 16; ++s)
+      if (nst % s == 0 && (long)nfb * mt * s <= 256) S = s;
+    if (nst / S >= 32) {
+      p.tile = 3;
+      p.NT = T8_NT;
+      p.MT = TILE_ROWS / 16;
+      p.WV = T8_THREADS / 64;
+      p.bn = 256;
+      p.n_fb = nfb;
+      p.m_tiles = mt;
+      p.S = S;
+      p.KCB = TILE_KT / 32;
+      p.kchunks = nst / S;
+      p.depth = T8_STAGES;
+      return p;
+    }
+  }
   if (M > 64 && K % (2 * TILE_KT) == 0 && N % 64 == 0 && (size_t)N * K * 2 < (1ull << 31)) {
     // 128-feature tiles wherever they give at least 160 workgroups (measured
     // on the 8B and 1B shapes: up to 35 % faster than 64-feature tiles
@@ -939,7 +1216,9 @@ void gemm_bf16(const GemmPlan& p, const void* Wpacked, int N, int K, const void*
       a.counters = counters;
       a.epi = epi;
       const dim3 grid(xcd_grid(p.n_fb, (a.M + TILE_ROWS - 1) / TILE_ROWS * p.S, p.xcd));
-      if (p.NT == 4)
+      if (p.tile == 3)
+        launch_timed(gemm_tile8_kernel, grid, dim3(T8_THREADS), st, a);
+      else if (p.NT == 4)
         launch_timed(gemm_tile_kernel<4, 3>, grid, dim3(256), st, a);
       else if (p.depth == 4)
         launch_timed(gemm_tile_kernel<2, 4>, grid, dim3(256), st, a);

@@ -376,11 +376,11 @@ __device__ __forceinline__ void rms_finish(const EpiArgs& e, const float (&v)[Rm
 }
 
 // per-token 1/rms(x) for large token tiles (parts in blocks of 16 through LDS)
-template <int MP>
+template <int MP, int NTH = 256>
 __device__ __forceinline__ void rms_prologue(const EpiArgs& e, int M, int t0, float (*red)[MP], float* rscale) {
   float s = 0.f;
   for (int p0 = 0; p0 < e.ssq_parts; p0 += 16) {
-    for (int i = threadIdx.x; i < 16 * MP; i += 256) {
+    for (int i = threadIdx.x; i < 16 * MP; i += NTH) {
       const int p = p0 + i / MP, t = i % MP;
       red[i / MP][t] = (p < e.ssq_parts && t < M)
                            ? e.ssq[(size_t)p * e.ssq_ld + (size_t)e.ssq_off + (size_t)(t0 + t) * e.ssq_step]

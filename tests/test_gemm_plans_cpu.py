@@ -71,7 +71,14 @@ def test_plans_tile_their_problem(planner, model):
             p = plan(M, N, K)
             where = f"M={M} N={N} K={K}"
             assert p.S >= 1 and p.n_fb >= 1, where
-            if p.tile:
+            if p.tile == 3:
+                # 128 x 256 tiles of eight waves: K split within 256 workgroups, >= 32 stages each
+                assert M > 64, where
+                assert p.NT == 4 and p.bn == 256 and p.n_fb * 256 == N and p.WV == 8, where
+                assert p.m_tiles == (M + TILE_ROWS - 1) // TILE_ROWS, where
+                assert p.kchunks * p.S * TILE_KT == K and p.kchunks >= 32, where
+                assert p.S == 1 or p.n_fb * p.m_tiles * p.S <= 256, where
+            elif p.tile:
                 assert M > 64, where
                 assert p.NT in (2, 4) and p.bn == 32 * p.NT and p.n_fb * p.bn == N, where
                 assert p.m_tiles == (M + TILE_ROWS - 1) // TILE_ROWS, where
@@ -106,18 +113,23 @@ def test_workspace_classes_bound_every_row_count(planner, model):
 
 
 def test_tiled_plan_choices(planner):
-    """The measured choices: 128-feature tiles (three weight stages) where they
-    make at least 160 workgroups, 64-feature tiles with four pipeline stages
-    otherwise, K split until the grid reaches 256 workgroups, streaming
-    launches up to 64 rows."""
+    """The measured choices: 128 x 256 eight-wave tiles where each workgroup
+    keeps at least 32 stages after the K split (at most 256 workgroups), else
+    128-feature tiles (three weight stages) where they make at least 160
+    workgroups, 64-feature tiles with four pipeline stages otherwise, K split
+    until the grid reaches 256 workgroups; streaming launches up to 64 rows."""
     plan, _ = planner
     m = synth.M8B
-    gu = plan(512, 2 * m.d_ff, m.d_model)  # 224 x 4 = 896 tiles
-    assert (gu.tile, gu.NT, gu.S, gu.depth) == (1, 4, 1, 3)
-    dn = plan(512, m.d_model, m.d_ff)  # 32 x 4 = 128 < 160: 64-feature tiles, 256 workgroups
-    assert (dn.tile, dn.NT, dn.S, dn.depth) == (1, 2, 1, 4)
-    qkv = plan(512, (m.n_heads + 2 * m.n_kv_heads) * m.head_dim, m.d_model)  # 48 x 4 = 192 tiles, split in 2
-    assert (qkv.tile, qkv.NT, qkv.S, qkv.depth) == (1, 4, 2, 3)
+    gu = plan(512, 2 * m.d_ff, m.d_model)  # 112 x 4 = 448 tiles of 128 x 256
+    assert (gu.tile, gu.bn, gu.S) == (3, 256, 1)
+    lm = plan(512, m.v_img, m.d_model)  # 128 x 4 = 512
+    assert (lm.tile, lm.S) == (3, 1)
+    dn = plan(512, m.d_model, m.d_ff)  # 16 x 4 tiles, 224 stages in 4 splits of 56
+    assert (dn.tile, dn.S, dn.kchunks) == (3, 4, 56)
+    qkv = plan(512, (m.n_heads + 2 * m.n_kv_heads) * m.head_dim, m.d_model)  # 24 x 4, 2 splits of 32 stages
+    assert (qkv.tile, qkv.S, qkv.kchunks) == (3, 2, 32)
+    o = plan(512, m.d_model, m.n_heads * m.head_dim)  # 16 x 4 x 4 splits would leave 16 stages: 128 x 128
+    assert (o.tile, o.NT, o.S, o.depth) == (1, 2, 1, 4)
     o1 = plan(256, synth.M1B.d_model, synth.M1B.d_model)  # 32 x 2 tiles of 64 features: 4 splits
     assert (o1.tile, o1.NT, o1.S) == (1, 2, 4)
     for M in (1, 24, 48, 64):
