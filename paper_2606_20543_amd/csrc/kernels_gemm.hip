@@ -741,23 +741,24 @@ __global__ __launch_bounds__(256, 2) void gemm_tile_kernel(GemmKArgs a) {
   }
 }
 
-// ---------------- wide tiles with the token rows through an LDS DMA ring ----------------
+// ---------------- wide tiles with both operands through an LDS DMA ring ----------------
 // Eight waves (two per SIMD, one workgroup per CU) own a 128-row x 256-feature
-// output tile: 2 (rows) x 4 (features) waves of 64 x 64, the same wave tile
-// and weight path as gemm_tile_kernel<4, 3> (each wave's packed weight
-// fragments straight to registers, two 64-input stages ahead in three
-// register slots).  The token rows of a stage (both planes) are shared by
-// all eight waves and come by LDS DMA into a ring of three stages, two stages
-// ahead of use: a DMA instruction fills eight rows x 128 bytes (whole cache
+// output tile: 2 (rows) x 4 (features) waves of 64 x 64, the wave tile of
+// gemm_tile_kernel<4, 3>.  A 64-input stage -- the token rows of both planes
+// (32 KiB) and the 32 packed 1 KiB weight tiles of the 256 features (32 KiB)
+// -- comes by LDS DMA into a ring of two stages, the next stage's copies in
+// flight while the current one is multiplied; every operand byte crosses the
+// L2 once per workgroup (with the 128 x 128 tiles the token rows crossed it
+// once per 128 features and each weight fragment once per wave that uses
+// it).  A token DMA instruction fills eight rows x 128 bytes (whole cache
 // lines), its lanes choosing the global chunk so that LDS holds the rows in
-// the swizzled layout the operand reads expect (chunk c of row r at c ^
-// ((r >> 1) & 7)).  Against the 128 x 128 tiles at two workgroups per CU
-// the token rows cross the L2 once per 256 features instead of once per 128
-// and arrive a stage earlier, without register staging.  The operand reads
-// are issued as separate instructions with their own waits, so that the
+// the swizzled layout the operand reads expect (chunk c of row r at c ^ ((r
+// >> 1) & 7)); a weight tile lands in its stored lane order, so both operand
+// reads are one conflict-free ds_read_b128 per fragment.  The reads are
+// issued as separate instructions with their own waits, so that the
 // compiler does not make them wait for every LDS DMA copy in flight.
-constexpr int T8_STAGES = 3, T8_THREADS = 512, T8_NT = 4;
-constexpr int T8_STAGE_BYTES = 2 * TILE_PL * 2;  // one stage: both planes, 32 KiB
+constexpr int T8_STAGES = 2, T8_THREADS = 512, T8_NT = 4;
+constexpr int T8_STAGE_BYTES = 2 * TILE_PL * 2 + 32 * 1024;  // one stage: both token planes, then 32 weight tiles
 
 // the eight token operand fragments of one k-block at addr: [mt * 2 + plane],
 // row tiles 16 rows (2 KiB) apart, the planes TILE_PL elements apart
@@ -773,14 +774,10 @@ __device__ __forceinline__ void ds_read_tiles2(u32x4 (&x)[8], uint32_t addr) {
   x[7] = ds_read16_at<PL + 3 * RT>(addr);
 }
 
-struct T8W {
-  u32x4 w[T8_NT][2];  // weight fragments: 4 feature tiles x 2 k-blocks of one stage
-};
-
 __global__ __launch_bounds__(T8_THREADS) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void gemm_tile8_kernel(GemmKArgs a) {
   constexpr int NT = T8_NT;
-  __shared__ __attribute__((aligned(16))) uint16_t xs[T8_STAGES * 2 * TILE_PL];
+  __shared__ __attribute__((aligned(16))) uint16_t xs[T8_STAGES * T8_STAGE_BYTES / 2];
   __shared__ float rscale[TILE_ROWS];
   __shared__ float sq_red[4][TILE_ROWS];
   __shared__ int is_last;
@@ -807,10 +804,10 @@ void gemm_tile8_kernel(GemmKArgs a) {
     for (int mt = 0; mt < 4; ++mt) acc[nt][mt] = floatx4{0.f, 0.f, 0.f, 0.f};
 
   const __amdgpu_buffer_rsrc_t xh = tile_rsrc(a.in), xl = tile_rsrc(a.in + a.in_plane), wr = tile_rsrc(a.W);
-  // token DMA: a stage is 32 instructions (2 planes x 16 blocks of 8 rows),
-  // four per wave; lane l of block rb takes row rb * 8 + l / 8 and stored
-  // chunk l % 8, i.e. the logical chunk (l % 8) ^ ((row >> 1) & 7) (rows past
-  // M repeat row M - 1; their results are never stored)
+  // token DMA: 32 instructions a stage (2 planes x 16 blocks of 8 rows), four
+  // per wave; lane l of block rb takes row rb * 8 + l / 8 and stored chunk
+  // l % 8, i.e. the logical chunk (l % 8) ^ ((row >> 1) & 7) (rows past M
+  // repeat row M - 1; their results are never stored)
   int xoff[4];
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
@@ -821,21 +818,19 @@ void gemm_tile8_kernel(GemmKArgs a) {
     xoff[j] = ((r < a.M ? r : a.M - 1) * a.ld_in + c * 8) * 2;
   }
   auto issue_x = [&](int stage) {
-    uint16_t* dst = xs + (size_t)(stage % T8_STAGES) * 2 * TILE_PL;
+    uint16_t* dst = xs + (size_t)(stage % T8_STAGES) * (T8_STAGE_BYTES / 2);
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int i = w * 4 + j, pl = i >> 4, rb = i & 15;
       dma16(pl ? xl : xh, dst + pl * TILE_PL + rb * 512, xoff[j], (st0 + stage) * TILE_KT * 2);
     }
-  };
-  const int lane_b = lane * 16, wtile_b = nb0 * a.KB * 1024;
-  auto load_w = [&](T8W& s, int stage) {
+    // the stage's 32 weight tiles (16 feature tiles x 2 k-blocks), four per wave
     const int kb0 = (st0 + stage) * TILE_KT / 32;
 #pragma unroll
-    for (int nt = 0; nt < NT; ++nt)
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-        s.w[nt][kb] = __builtin_amdgcn_raw_buffer_load_b128(wr, lane_b, wtile_b + (nt * a.KB + kb0 + kb) * 1024, 0);
+    for (int j = 0; j < 4; ++j) {
+      const int i = w * 4 + j, ft = i >> 1, kb = i & 1;
+      dma16(wr, dst + 2 * TILE_PL + i * 512, lane * 16, ((fb * 16 + ft) * a.KB + kb0 + kb) * 1024);
+    }
   };
   // operand reads: row wm * 64 + lane % 16 (+ 16 mt), logical chunk kb * 4 +
   // lane / 16 stored at that ^ ((row >> 1) & 7), which no mt changes
@@ -845,76 +840,61 @@ void gemm_tile8_kernel(GemmKArgs a) {
   for (int kb = 0; kb < 2; ++kb)
     xrd[kb] = xs0 + (uint32_t)(((wm * 64 + (lane & 15)) * TILE_LD +
                                 (((kb * 4 + (lane >> 4)) ^ ((lane & 15) >> 1)) * 8)) * 2);
-  auto mma = [&](const T8W& s, int stage) {
+  // weight tile (f, kb) of the stage sits at (2 f + kb) KiB after its token
+  // planes; this wave's feature tiles are f = 4 wn .. 4 wn + 3
+  const uint32_t wrd = xs0 + (uint32_t)(2 * TILE_PL * 2 + wn * 8 * 1024 + lane * 16);
+  auto mma = [&](int stage) {
     const uint32_t so = (uint32_t)((stage % T8_STAGES) * T8_STAGE_BYTES);
-    u32x4 x0[8], x1[8];  // [mt * 2 + plane] of k-block 0, then 1
+    u32x4 x0[8], x1[8], b0[4], b1[4];  // token [mt * 2 + plane] and weight [nt] fragments of k-blocks 0 and 1
     ds_read_tiles2(x0, xrd[0] + so);
+    b0[0] = ds_read16_at<0>(wrd + so);
+    b0[1] = ds_read16_at<2048>(wrd + so);
+    b0[2] = ds_read16_at<4096>(wrd + so);
+    b0[3] = ds_read16_at<6144>(wrd + so);
     ds_read_tiles2(x1, xrd[1] + so);
-    lgkm_wait<8>(x0);
+    b1[0] = ds_read16_at<1024>(wrd + so);
+    b1[1] = ds_read16_at<3072>(wrd + so);
+    b1[2] = ds_read16_at<5120>(wrd + so);
+    b1[3] = ds_read16_at<7168>(wrd + so);
+    lgkm_wait<12>(x0);
+    lgkm_wait<12>(b0);
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt)
 #pragma unroll
       for (int mt = 0; mt < 4; ++mt) {
-        const bf16x8 wf = __builtin_bit_cast(bf16x8, s.w[nt][0]);
+        const bf16x8 wf = __builtin_bit_cast(bf16x8, b0[nt]);
         acc[nt][mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf, __builtin_bit_cast(bf16x8, x0[mt * 2]), acc[nt][mt], 0, 0, 0);
         acc[nt][mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf, __builtin_bit_cast(bf16x8, x0[mt * 2 + 1]), acc[nt][mt], 0, 0, 0);
       }
     __builtin_amdgcn_sched_barrier(0);  // the first k-block's MFMAs stay above the second wait
     lgkm_wait<0>(x1);
+    lgkm_wait<0>(b1);
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt)
 #pragma unroll
       for (int mt = 0; mt < 4; ++mt) {
-        const bf16x8 wf = __builtin_bit_cast(bf16x8, s.w[nt][1]);
+        const bf16x8 wf = __builtin_bit_cast(bf16x8, b1[nt]);
         acc[nt][mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf, __builtin_bit_cast(bf16x8, x1[mt * 2]), acc[nt][mt], 0, 0, 0);
         acc[nt][mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf, __builtin_bit_cast(bf16x8, x1[mt * 2 + 1]), acc[nt][mt], 0, 0, 0);
       }
   };
 
-  // prologue: stages 0 and 1 in flight (tokens and weights), then the tile's
-  // 1/rms (its scratch is the third ring buffer, first written by stage 2's
-  // copies after the first barrier below)
-  T8W w0, w1, w2;
+  // stage 0 in flight, then the tile's 1/rms (its scratch is the second ring
+  // buffer, first written by stage 1's copies after the first barrier below)
   issue_x(0);
-  load_w(w0, 0);
-  if (nst > 1) {
-    issue_x(1);
-    load_w(w1, 1);
-  }
   if (e.ssq)
-    rms_prologue<TILE_ROWS, T8_THREADS>(e, Mt, a.t0 + r0, (float(*)[TILE_ROWS])(void*)(xs + 2 * 2 * TILE_PL), rscale);
+    rms_prologue<TILE_ROWS, T8_THREADS>(e, Mt, a.t0 + r0, (float(*)[TILE_ROWS])(void*)(xs + T8_STAGE_BYTES / 2), rscale);
   else if (tid < TILE_ROWS)
     rscale[tid] = 1.f;
-  // stage c: this wave's copies of stage c are done (those issued after them:
-  // its weights, and stage c + 1's copies and weights when there is one), the
-  // barrier publishes everyone's copies and tells that every wave is done with
-  // stage c - 1, whose ring buffer and weight slot then take stage c + 2
-  auto step = [&](int c, const T8W& cur, T8W& ahead2, bool more) {
-    if (more) {
-      wait_vmcnt<20>();
-      dma_barrier();
-      issue_x(c + 2);
-      load_w(ahead2, c + 2);
-    } else {
-      if (c + 1 < nst)
-        wait_vmcnt<20>();
-      else
-        wait_vmcnt<8>();
-      dma_barrier();
-    }
-    mma(cur, c);
-  };
-  int c = 0;
-  for (; c + 5 <= nst; c += 3) {
-    step(c, w0, w2, true);
-    step(c + 1, w1, w0, true);
-    step(c + 2, w2, w1, true);
+  // stage c: this wave's copies of stage c are done (none are issued after
+  // them yet), the barrier publishes everyone's copies and tells that every
+  // wave is done with stage c - 1, whose ring buffer then takes stage c + 1
+  for (int c = 0; c < nst; ++c) {
+    wait_vmcnt<0>();
+    dma_barrier();
+    if (c + 1 < nst) issue_x(c + 1);
+    mma(c);
   }
-  // 1 to 4 stages left, stage c in slot w0
-  if (c < nst) step(c, w0, w2, c + 2 < nst);
-  if (c + 1 < nst) step(c + 1, w1, w0, c + 3 < nst);
-  if (c + 2 < nst) step(c + 2, w2, w1, false);
-  if (c + 3 < nst) step(c + 3, w0, w2, false);
 
   if (a.S > 1) {
     // split-K: publish this split's fragments; the last arrival of the tile
@@ -993,12 +973,13 @@ GemmPlan gemm_plan_bf16(int M, int N, int K, int xcd) {
   p.xcd = xcd;
   p.tile = 0;
   if (M > 64 && K % (2 * TILE_KT) == 0 && N % 256 == 0 && (size_t)N * K * 2 < (1ull << 31) && tile8_enabled()) {
-    // 128 x 256 tiles, eight waves, token rows by LDS DMA, one workgroup per
-    // CU: K split by the largest divisor of the stage count that keeps the
-    // grid within 256 workgroups, wherever each workgroup still runs at least
-    // 32 stages.  Measured on the 8B shapes at 512 rows against the 128 x 128
-    // tiles: gate/up 269 -> 236 us, down 167 -> 127, output layer 274 -> 248,
-    // QKV 82 -> 79; O (16 stages per workgroup) 55 -> 62, so it stays on them.
+    // 128 x 256 tiles, eight waves, both operands by LDS DMA, one workgroup
+    // per CU: K split by the largest divisor of the stage count that keeps
+    // the grid within 256 workgroups, wherever each workgroup still runs at
+    // least 32 stages.  Measured on the 8B shapes at 512 rows against the
+    // 128 x 128 tiles: gate/up 269 -> 231 us, down 167 -> 122, output layer
+    // 274 -> 234, QKV 82 -> 77; O (16 stages per workgroup) 55 -> 62, so it
+    // stays on them.
     const int mt = (M + TILE_ROWS - 1) / TILE_ROWS;
     const int nfb = N / 256, nst = K / TILE_KT;
     int S = 1;
@@ -1015,7 +996,7 @@ GemmPlan gemm_plan_bf16(int M, int N, int K, int xcd) {
       p.S = S;
       p.KCB = TILE_KT / 32;
       p.kchunks = nst / S;
-      p.depth = T8_STAGES;
+      p.depth = T8_STAGES;  // ring stages
       return p;
     }
   }

@@ -124,7 +124,7 @@ struct GemmPlan {
   int bn;           // features per workgroup
   int xcd;          // >0: workgroups that reduce together share one XCD (n XCDs); 0: fenced reduction
   int tile;         // 1: tiled kernel for more than 64 rows (128-row tiles, K split only to fill the CUs);
-                    // 3: 128 x 256 tiles of eight waves, token rows by LDS DMA
+                    // 3: 128 x 256 tiles of eight waves, both operands by LDS DMA
   int m_tiles;      // tiled: 128-row tiles
   int depth;        // tiled: register stages of the K pipeline (2 or 4)
 };
