@@ -935,7 +935,47 @@ void gemm_tile8_kernel(GemmKArgs a) {
   }
 
   float sq[4] = {0.f, 0.f, 0.f, 0.f};
-  if (Mw > 0) {
+  if (e.kind == EPI_SWIGLU) {
+    // a lane's four features of one fragment are two gate/up pairs, i.e. two
+    // adjacent outputs (4 bytes a plane): the wave's 64 x 32 outputs go
+    // through its own 8 KiB of the ring buffer the last stage did not use
+    // (every wave was done with it at that stage's barrier and no copy
+    // targets it any more), and come back as 16 bytes of one row a lane,
+    // stored as 64 contiguous bytes per row and plane
+    if (Mw > 0) {
+      uint16_t* stg = xs + (size_t)(nst % T8_STAGES) * (T8_STAGE_BYTES / 2) + w * 4096;  // [plane][64 rows][32]
+      const int q = lane >> 4;
+#pragma unroll
+      for (int mt = 0; mt < 4; ++mt) {
+        const int row = mt * 16 + (lane & 15);
+        const float r = rscale[wm * 64 + row];
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) {
+          const floatx4 v = acc[nt][mt];
+          const float g0 = v[0] * r, u0 = v[1] * r, g1 = v[2] * r, u1 = v[3] * r;
+          const float s0 = g0 / (1.0f + expf(-g0)), s1 = g1 / (1.0f + expf(-g1));
+          uint32_t hi, lo;
+          split2(s0 * u0, s1 * u1, hi, lo);
+          *(uint32_t*)(stg + row * 32 + nt * 8 + 2 * q) = hi;
+          *(uint32_t*)(stg + 2048 + row * 32 + nt * 8 + 2 * q) = lo;
+        }
+      }
+      asm volatile("" ::: "memory");  // a wave's LDS accesses run in order: its reads see all its lanes' writes
+      uint16_t* h = (uint16_t*)e.h;
+      const int c = lane & 3;
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const int row = k * 16 + (lane >> 2);
+        const uint4 hi = *(const uint4*)(stg + row * 32 + c * 8);
+        const uint4 lo = *(const uint4*)(stg + 2048 + row * 32 + c * 8);
+        if (row < Mw) {
+          const size_t i = (size_t)(t0w + row) * e.ld + nb0 * 8 + c * 8;
+          *(uint4*)(h + i) = hi;
+          *(uint4*)(h + e.h_plane + i) = lo;
+        }
+      }
+    }
+  } else if (Mw > 0) {
     EpiOps<NT, 4> op;
     epi_block_starts<NT, 4>(e, Mw, t0w, lane, op);
     epi_load<NT, 4>(e, nb0, a.N, Mw, t0w, lane, op);
