@@ -774,30 +774,18 @@ __device__ __forceinline__ void ds_read_tiles2(u32x4 (&x)[8], uint32_t addr) {
   x[7] = ds_read16_at<PL + 3 * RT>(addr);
 }
 
-__global__ __launch_bounds__(T8_THREADS) __attribute__((amdgpu_waves_per_eu(2, 2)))
-void gemm_tile8_kernel(GemmKArgs a) {
+// K loop of one tile segment: stages st0 .. st0 + nst - 1 of the 128 token
+// rows from r0 against feature block fb, summed into acc.  pro() runs once
+// the first stage's copies are in flight (the tile's 1/rms, whose LDS
+// scratch is the ring's second buffer); on return every wave is past the
+// last stage's barrier, so the buffer of stage nst is free.
+template <class Pro>
+__device__ __forceinline__ void t8_kloop(const GemmKArgs& a, int fb, int r0, int st0, int nst, uint16_t* xs,
+                                         floatx4 (&acc)[T8_NT][4], Pro&& pro) {
   constexpr int NT = T8_NT;
-  __shared__ __attribute__((aligned(16))) uint16_t xs[T8_STAGES * T8_STAGE_BYTES / 2];
-  __shared__ float rscale[TILE_ROWS];
-  __shared__ float sq_red[4][TILE_ROWS];
-  __shared__ int is_last;
-  const int m_tiles = (a.M + TILE_ROWS - 1) / TILE_ROWS;
-  int fb, member;
-  xcd_unmap(blockIdx.x, m_tiles * a.S, a.xcd, fb, member);
-  if (fb >= a.n_fb) return;
-  const int mtile = member / a.S, split = member - mtile * a.S;
   const int tid = threadIdx.x, lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
   const int wm = w & 1, wn = w >> 1;
-  const int r0 = mtile * TILE_ROWS;
-  const int nb0 = fb * 4 * NT + wn * NT;  // first 16-feature tile of this wave
-  const int t0w = a.t0 + r0 + wm * 64;
-  const int Mw = a.M - r0 - wm * 64 < 64 ? a.M - r0 - wm * 64 : 64;
-  const int Mt = a.M - r0 < TILE_ROWS ? a.M - r0 : TILE_ROWS;
-  const EpiArgs& e = a.epi;
-  const int nst = a.K / TILE_KT / a.S, st0 = split * nst;
-
-  floatx4 acc[NT][4];
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt)
 #pragma unroll
@@ -879,13 +867,8 @@ void gemm_tile8_kernel(GemmKArgs a) {
       }
   };
 
-  // stage 0 in flight, then the tile's 1/rms (its scratch is the second ring
-  // buffer, first written by stage 1's copies after the first barrier below)
   issue_x(0);
-  if (e.ssq)
-    rms_prologue<TILE_ROWS, T8_THREADS>(e, Mt, a.t0 + r0, (float(*)[TILE_ROWS])(void*)(xs + T8_STAGE_BYTES / 2), rscale);
-  else if (tid < TILE_ROWS)
-    rscale[tid] = 1.f;
+  pro();
   // stage c: this wave's copies of stage c are done (none are issued after
   // them yet), the barrier publishes everyone's copies and tells that every
   // wave is done with stage c - 1, whose ring buffer then takes stage c + 1
@@ -895,55 +878,30 @@ void gemm_tile8_kernel(GemmKArgs a) {
     if (c + 1 < nst) issue_x(c + 1);
     mma(c);
   }
+}
 
-  if (a.S > 1) {
-    // split-K: publish this split's fragments; the last arrival of the tile
-    // sums all splits in split order (deterministic)
-    const int grp = fb * m_tiles + mtile;
-    constexpr int FRAG = NT * 4 * 64 * 4;  // floats per wave
-    float* P = a.part + ((size_t)grp * a.S * 8 + w) * FRAG + lane * 4;
-#pragma unroll
-    for (int nt = 0; nt < NT; ++nt)
-#pragma unroll
-      for (int mt = 0; mt < 4; ++mt) *(floatx4*)(P + (size_t)split * 8 * FRAG + (nt * 4 + mt) * 256) = acc[nt][mt];
-    __builtin_amdgcn_s_waitcnt(0);
-    __syncthreads();
-    if (tid == 0) {
-      if (!a.xcd) __threadfence();  // splits on different XCDs: write back through L2
-      const unsigned prev = atomicAdd(&a.counters[grp], 1u);
-      is_last = prev == (unsigned)(a.S - 1);
-      if (is_last && !a.xcd) __threadfence();
-    }
-    __syncthreads();
-    if (!is_last) return;
-#pragma unroll
-    for (int nt = 0; nt < NT; ++nt)
-#pragma unroll
-      for (int mt = 0; mt < 4; ++mt) acc[nt][mt] = floatx4{0.f, 0.f, 0.f, 0.f};
-    for (int sp = 0; sp < a.S; ++sp) {
-      floatx4 v[NT][4];
-#pragma unroll
-      for (int nt = 0; nt < NT; ++nt)
-#pragma unroll
-        for (int mt = 0; mt < 4; ++mt) v[nt][mt] = *(const floatx4*)(P + (size_t)sp * 8 * FRAG + (nt * 4 + mt) * 256);
-#pragma unroll
-      for (int nt = 0; nt < NT; ++nt)
-#pragma unroll
-        for (int mt = 0; mt < 4; ++mt) acc[nt][mt] += v[nt][mt];
-    }
-    if (tid == 0) a.counters[grp] = 0u;
-  }
-
+// Epilogue of the tile (fb, rows r0 ..) from its sums; stg: a free ring
+// buffer (64 KiB).  Every thread of the workgroup calls it (one barrier for
+// the residual's row sums).
+__device__ __forceinline__ void t8_epilogue(const GemmKArgs& a, int fb, int r0, const floatx4 (&acc)[T8_NT][4],
+                                            const float* rscale, float (*sq_red)[TILE_ROWS], uint16_t* stg_all) {
+  constexpr int NT = T8_NT;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = w & 1, wn = w >> 1;
+  const int nb0 = fb * 4 * NT + wn * NT;  // first 16-feature tile of this wave
+  const int t0w = a.t0 + r0 + wm * 64;
+  const int Mw = a.M - r0 - wm * 64 < 64 ? a.M - r0 - wm * 64 : 64;
+  const int Mt = a.M - r0 < TILE_ROWS ? a.M - r0 : TILE_ROWS;
+  const EpiArgs& e = a.epi;
   float sq[4] = {0.f, 0.f, 0.f, 0.f};
   if (e.kind == EPI_SWIGLU) {
     // a lane's four features of one fragment are two gate/up pairs, i.e. two
     // adjacent outputs (4 bytes a plane): the wave's 64 x 32 outputs go
-    // through its own 8 KiB of the ring buffer the last stage did not use
-    // (every wave was done with it at that stage's barrier and no copy
-    // targets it any more), and come back as 16 bytes of one row a lane,
-    // stored as 64 contiguous bytes per row and plane
+    // through its own 8 KiB of the free ring buffer and come back as 16
+    // bytes of one row a lane, stored as 64 contiguous bytes per row and plane
     if (Mw > 0) {
-      uint16_t* stg = xs + (size_t)(nst % T8_STAGES) * (T8_STAGE_BYTES / 2) + w * 4096;  // [plane][64 rows][32]
+      uint16_t* stg = stg_all + w * 4096;  // [plane][64 rows][32]
       const int q = lane >> 4;
 #pragma unroll
       for (int mt = 0; mt < 4; ++mt) {
@@ -996,6 +954,77 @@ void gemm_tile8_kernel(GemmKArgs a) {
       e.ssq_out[(size_t)fb * e.ssq_out_ld + a.t0 + r0 + tid] =
           ((sq_red[0][tid] + sq_red[1][tid]) + sq_red[2][tid]) + sq_red[3][tid];
   }
+}
+
+// the tile's 1/rms of its rows (1 without a norm), scratch: 8 KiB of LDS
+__device__ __forceinline__ void t8_rms(const GemmKArgs& a, int r0, float* scratch, float* rscale) {
+  const int Mt = a.M - r0 < TILE_ROWS ? a.M - r0 : TILE_ROWS;
+  if (a.epi.ssq)
+    rms_prologue<TILE_ROWS, T8_THREADS>(a.epi, Mt, a.t0 + r0, (float(*)[TILE_ROWS])(void*)scratch, rscale);
+  else if (threadIdx.x < TILE_ROWS)
+    rscale[threadIdx.x] = 1.f;
+}
+
+// One workgroup per output tile and K split (grid of xcd_grid(n_fb,
+// m_tiles * S)): the splits' sums meet in the last arrival.
+__global__ __launch_bounds__(T8_THREADS) __attribute__((amdgpu_waves_per_eu(2, 2)))
+void gemm_tile8_kernel(GemmKArgs a) {
+  constexpr int NT = T8_NT;
+  __shared__ __attribute__((aligned(16))) uint16_t xs[T8_STAGES * T8_STAGE_BYTES / 2];
+  __shared__ float rscale[TILE_ROWS];
+  __shared__ float sq_red[4][TILE_ROWS];
+  __shared__ int is_last;
+  const int m_tiles = (a.M + TILE_ROWS - 1) / TILE_ROWS;
+  int fb, member;
+  xcd_unmap(blockIdx.x, m_tiles * a.S, a.xcd, fb, member);
+  if (fb >= a.n_fb) return;
+  const int mtile = member / a.S, split = member - mtile * a.S;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
+  const int r0 = mtile * TILE_ROWS;
+  const int nst = a.K / TILE_KT / a.S;
+
+  floatx4 acc[NT][4];
+  t8_kloop(a, fb, r0, split * nst, nst, xs, acc, [&] { t8_rms(a, r0, (float*)(void*)(xs + T8_STAGE_BYTES / 2), rscale); });
+
+  if (a.S > 1) {
+    // split-K: publish this split's fragments; the last arrival of the tile
+    // sums all splits in split order (deterministic)
+    const int grp = fb * m_tiles + mtile;
+    constexpr int FRAG = NT * 4 * 64 * 4;  // floats per wave
+    float* P = a.part + ((size_t)grp * a.S * 8 + w) * FRAG + lane * 4;
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+      for (int mt = 0; mt < 4; ++mt) *(floatx4*)(P + (size_t)split * 8 * FRAG + (nt * 4 + mt) * 256) = acc[nt][mt];
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    if (tid == 0) {
+      if (!a.xcd) __threadfence();  // splits on different XCDs: write back through L2
+      const unsigned prev = atomicAdd(&a.counters[grp], 1u);
+      is_last = prev == (unsigned)(a.S - 1);
+      if (is_last && !a.xcd) __threadfence();
+    }
+    __syncthreads();
+    if (!is_last) return;
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+      for (int mt = 0; mt < 4; ++mt) acc[nt][mt] = floatx4{0.f, 0.f, 0.f, 0.f};
+    for (int sp = 0; sp < a.S; ++sp) {
+      floatx4 v[NT][4];
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+        for (int mt = 0; mt < 4; ++mt) v[nt][mt] = *(const floatx4*)(P + (size_t)sp * 8 * FRAG + (nt * 4 + mt) * 256);
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+        for (int mt = 0; mt < 4; ++mt) acc[nt][mt] += v[nt][mt];
+    }
+    if (tid == 0) a.counters[grp] = 0u;
+  }
+  t8_epilogue(a, fb, r0, acc, rscale, sq_red, xs + (size_t)(nst % T8_STAGES) * (T8_STAGE_BYTES / 2));
 }
 
 // the 128 x 256 LDS-DMA tiles where they apply (SSD_GEMM_T8=0 keeps every
