@@ -121,6 +121,7 @@ struct GemmKArgs {
   int ld_in;
   int M, t0;
   int xcd;
+  int fb0;  // eight-wave tiles: feature block of the launch's first (its partials and counters count from it)
   float* part;
   unsigned* counters;
   EpiArgs epi;
@@ -985,7 +986,8 @@ void gemm_tile8_kernel(GemmKArgs a) {
   const int nst = a.K / TILE_KT / a.S;
 
   floatx4 acc[NT][4];
-  t8_kloop(a, fb, r0, split * nst, nst, xs, acc, [&] { t8_rms(a, r0, (float*)(void*)(xs + T8_STAGE_BYTES / 2), rscale); });
+  t8_kloop(a, fb + a.fb0, r0, split * nst, nst, xs, acc,
+           [&] { t8_rms(a, r0, (float*)(void*)(xs + T8_STAGE_BYTES / 2), rscale); });
 
   if (a.S > 1) {
     // split-K: publish this split's fragments; the last arrival of the tile
@@ -1024,7 +1026,7 @@ void gemm_tile8_kernel(GemmKArgs a) {
     }
     if (tid == 0) a.counters[grp] = 0u;
   }
-  t8_epilogue(a, fb, r0, acc, rscale, sq_red, xs + (size_t)(nst % T8_STAGES) * (T8_STAGE_BYTES / 2));
+  t8_epilogue(a, fb + a.fb0, r0, acc, rscale, sq_red, xs + (size_t)(nst % T8_STAGES) * (T8_STAGE_BYTES / 2));
 }
 
 // the 128 x 256 LDS-DMA tiles where they apply (SSD_GEMM_T8=0 keeps every
@@ -1041,6 +1043,8 @@ GemmPlan gemm_plan_bf16(int M, int N, int K, int xcd) {
   GemmPlan p;
   p.xcd = xcd;
   p.tile = 0;
+  p.tail_fb = 0;
+  p.tail_S = 1;
   if (M > 64 && K % (2 * TILE_KT) == 0 && N % 256 == 0 && (size_t)N * K * 2 < (1ull << 31) && tile8_enabled()) {
     // 128 x 256 tiles, eight waves, both operands by LDS DMA, one workgroup
     // per CU: K split by the largest divisor of the stage count that keeps
@@ -1066,6 +1070,21 @@ GemmPlan gemm_plan_bf16(int M, int N, int K, int xcd) {
       p.KCB = TILE_KT / 32;
       p.kchunks = nst / S;
       p.depth = T8_STAGES;  // ring stages
+      // whole tiles in as many full rounds of 256 as there are, the feature
+      // blocks left over K-split so that they fill the last round, where
+      // that saves the busiest CU a quarter of a round and more (8B gate/up
+      // at 1024 rows: 768 tiles, then 128 in two splits of 32 stages)
+      const long tiles = (long)nfb * mt, full = tiles / 256;
+      if (S == 1 && full >= 1 && tiles % 256 && (256 * full) % mt == 0) {
+        const int fb_a = (int)(256 * full / mt), r = (nfb - fb_a) * mt;
+        int st = 1;
+        for (int s = 2; s <= 16; ++s)
+          if (nst % s == 0 && (long)r * s <= 256 && nst / s >= 16) st = s;
+        if (st > 1 && nst / st + nst / 8 <= nst * 3 / 4) {
+          p.tail_fb = fb_a;
+          p.tail_S = st;
+        }
+      }
       return p;
     }
   }
@@ -1213,6 +1232,7 @@ GemmPlan gemm_plan_bf16(int M, int N, int K, int xcd) {
 }
 
 size_t gemm_partials_floats(const GemmPlan& p, int M) {
+  if (p.tile && p.tail_fb) return (size_t)p.tail_S * (p.n_fb - p.tail_fb) * p.m_tiles * TILE_ROWS * p.bn;
   if (p.S <= 1) return 0;
   if (p.tile) return (size_t)p.S * p.m_tiles * TILE_ROWS * p.n_fb * p.bn;
   (void)M;
@@ -1266,7 +1286,17 @@ void gemm_bf16(const GemmPlan& p, const void* Wpacked, int N, int K, const void*
       a.counters = counters;
       a.epi = epi;
       const dim3 grid(xcd_grid(p.n_fb, (a.M + TILE_ROWS - 1) / TILE_ROWS * p.S, p.xcd));
-      if (p.tile == 3)
+      if (p.tile == 3 && p.tail_fb && a.M == M) {
+        // whole tiles of the first feature blocks, then the rest K-split
+        const int mt = (a.M + TILE_ROWS - 1) / TILE_ROWS;
+        a.n_fb = p.tail_fb;
+        launch_timed(gemm_tile8_kernel, dim3(xcd_grid(a.n_fb, mt, p.xcd)), dim3(T8_THREADS), st, a);
+        a.fb0 = p.tail_fb;
+        a.n_fb = p.n_fb - p.tail_fb;
+        a.S = p.tail_S;
+        a.kchunks = K / TILE_KT / p.tail_S;
+        launch_timed(gemm_tile8_kernel, dim3(xcd_grid(a.n_fb, mt * a.S, p.xcd)), dim3(T8_THREADS), st, a);
+      } else if (p.tile == 3)
         launch_timed(gemm_tile8_kernel, grid, dim3(T8_THREADS), st, a);
       else if (p.NT == 4)
         launch_timed(gemm_tile_kernel<4, 3>, grid, dim3(256), st, a);
@@ -1280,6 +1310,7 @@ void gemm_bf16(const GemmPlan& p, const void* Wpacked, int N, int K, const void*
   const int MP = p.MT * 16;
   for (int t0 = 0; t0 < M; t0 += MP) {
     GemmKArgs a;
+    a.fb0 = 0;
     a.W = (const u32x4*)Wpacked;
     a.N = N;
     a.K = K;

@@ -127,9 +127,12 @@ struct GemmPlan {
                     // 3: 128 x 256 tiles of eight waves, both operands by LDS DMA
   int m_tiles;      // tiled: 128-row tiles
   int depth;        // tiled: register stages of the K pipeline (2 or 4)
+  int tail_fb;      // tile 3, > 0: feature blocks [0, tail_fb) in one launch of whole tiles, the rest
+  int tail_S;       //   in a second launch with K split tail_S ways (a last round that would run part empty)
 };
 // split-K arrival counters a plan uses (tiled plans: one per output tile, when split)
 inline int gemm_counters(const GemmPlan& p) {
+  if (p.tile && p.tail_fb) return (p.n_fb - p.tail_fb) * p.m_tiles;
   return p.tile ? (p.S > 1 ? p.n_fb * p.m_tiles : 0) : p.n_fb;
 }
 // Row counts that cover every plan class: up to 16, 32 and 64 rows, 65..128

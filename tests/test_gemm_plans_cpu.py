@@ -21,7 +21,7 @@ import synth
 
 class GemmPlan(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int) for n in ("MT", "NT", "KCB", "WV", "S", "n_fb", "kchunks", "bn", "xcd", "tile",
-                                            "m_tiles", "depth")]
+                                            "m_tiles", "depth", "tail_fb", "tail_S")]
 
 
 TILE_ROWS, TILE_KT = 128, 64
@@ -42,6 +42,8 @@ def planner():
 
 def counters(p):
     """Arrival counters a plan uses (split-K reductions)."""
+    if p.tile and p.tail_fb:
+        return (p.n_fb - p.tail_fb) * p.m_tiles
     if p.tile:
         return p.n_fb * p.m_tiles if p.S > 1 else 0
     return p.n_fb
@@ -78,6 +80,14 @@ def test_plans_tile_their_problem(planner, model):
                 assert p.m_tiles == (M + TILE_ROWS - 1) // TILE_ROWS, where
                 assert p.kchunks * p.S * TILE_KT == K and p.kchunks >= 32, where
                 assert p.S == 1 or p.n_fb * p.m_tiles * p.S <= 256, where
+                if p.tail_fb:
+                    # whole rounds of 256 tiles, then the remaining feature blocks K-split within one more
+                    assert p.S == 1 and 0 < p.tail_fb < p.n_fb and (p.tail_fb * p.m_tiles) % 256 == 0, where
+                    r = (p.n_fb - p.tail_fb) * p.m_tiles
+                    assert 0 < r < 256 and r * p.tail_S <= 256 and p.tail_S > 1, where
+                    assert (K // TILE_KT) % p.tail_S == 0 and K // TILE_KT // p.tail_S >= 16, where
+                else:
+                    assert p.tail_S == 1, where
             elif p.tile:
                 assert M > 64, where
                 assert p.NT in (2, 4) and p.bn == 32 * p.NT and p.n_fb * p.bn == N, where
@@ -130,6 +140,9 @@ def test_tiled_plan_choices(planner):
     assert (qkv.tile, qkv.S, qkv.kchunks) == (3, 2, 32)
     o = plan(512, m.d_model, m.n_heads * m.head_dim)  # 16 x 4 x 4 splits would leave 16 stages: 128 x 128
     assert (o.tile, o.NT, o.S, o.depth) == (1, 2, 1, 4)
+    gu1k = plan(1024, 2 * m.d_ff, m.d_model)  # 896 tiles: 768 in three full rounds, 128 in two splits of 32
+    assert (gu1k.tile, gu1k.S, gu1k.tail_fb, gu1k.tail_S) == (3, 1, 96, 2)
+    assert (gu.tail_fb, lm.tail_fb) == (0, 0)  # 192 tiles left at 512 rows: no split fits them into 256
     o1 = plan(256, synth.M1B.d_model, synth.M1B.d_model)  # 32 x 2 tiles of 64 features: 4 splits
     assert (o1.tile, o1.NT, o1.S) == (1, 2, 4)
     for M in (1, 24, 48, 64):

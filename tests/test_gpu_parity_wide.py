@@ -24,6 +24,8 @@ stays within seconds.  Cases:
       rule on the GPU's own logits is checked for all eight
   7B width, batch 1, a 32-token block at context 1120..1152 (the last row of
       the 32x32 workload), 2 rounds + commit
+  8B width, batch 8, 256-token prompt, one 128-token block (M = 1024: the
+      passes that carry a commit; gate/up as whole tiles plus a K-split tail)
   8B width, batch 2, a 40-token block at context 600..640: 160 query rows per
       (sequence, KV head), so the query-split attention runs one full 128-row
       group and one of 32 rows whose other 96 are padding
@@ -106,6 +108,14 @@ def test_7b_width_row_block(pair7):
 
 def test_8b_width_gqa_batch8(pair8):
     _greedy_block(pair8, W8, B=8, P=256, K=64, rounds=1, keep=0.6, seed_stream=12)
+
+
+def test_8b_width_batch8_block128(pair8):
+    """1024 rows per pass, the size of the 64x64 workload's passes that carry a
+    commit: QKV on 192 whole tiles, O and down K-split in two, gate/up as 768
+    whole tiles in three full rounds and the last 16 feature blocks K-split in
+    a second launch, the output layer on 1024 tiles."""
+    _greedy_block(pair8, W8, B=8, P=256, K=128, rounds=1, keep=0.6, seed_stream=22)
 
 
 def test_8b_width_context_4352(pair8):
