@@ -29,6 +29,8 @@ stays within seconds.  Cases:
   8B width, batch 2, a 40-token block at context 600..640: 160 query rows per
       (sequence, KV head), so the query-split attention runs one full 128-row
       group and one of 32 rows whose other 96 are padding
+  1B width, batch 4, 64-token prompt and a 256-token block (M = 1024: gate/up
+      as whole tiles plus a K-split tail of its own shape)
   1B width, batch 4, 64-token prompt and a 64-token block (M = 256, prefill
       and verify): tiled GEMMs whose K range is split over workgroups to
       fill the CUs (O and down projections in 4 splits, QKV in 2), rule (A),
@@ -210,6 +212,13 @@ def test_1b_width_b4_context_1088_rule_c(pair1):
 
 def test_1b_width_b4_block64_split_tiles(pair1):
     _greedy_block(pair1, W1, B=4, P=64, K=64, rounds=2, keep=0.6, seed_stream=15)
+
+
+def test_1b_width_b4_block256(pair1):
+    """1024 rows at the 1B widths: gate/up as 256 whole tiles and a K-split
+    second launch of the other 12 feature blocks (a different split than at the
+    8B widths), the output layer on 512 tiles."""
+    _greedy_block(pair1, W1, B=4, P=64, K=256, rounds=1, keep=0.6, seed_stream=23)
 
 
 def test_1b_width_fenced_reductions(monkeypatch):
