@@ -934,6 +934,54 @@ __device__ __forceinline__ void t8_epilogue(const GemmKArgs& a, int fb, int r0, 
         }
       }
     }
+  } else if (e.kind == EPI_RESID) {
+    // the new residual x stored in place (16 bytes a lane); the planes of
+    // g * x (8 bytes a lane and plane) go through the wave's 8 KiB of the
+    // free ring buffer one plane at a time and come back as 16 bytes of one
+    // row a lane: 128 contiguous bytes per row and plane
+    if (Mw > 0) {
+      EpiOps<NT, 4> op;
+      epi_load<NT, 4>(e, nb0, a.N, Mw, t0w, lane, op);
+      uint16_t* stg = stg_all + w * 4096;  // [64 rows][64 features], one plane
+      const int nq = 4 * (lane >> 4);
+      uint2 lo[NT][4];
+#pragma unroll
+      for (int mt = 0; mt < 4; ++mt) {
+        const int row = mt * 16 + (lane & 15);
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) {
+          const floatx4 v = acc[nt][mt];
+          const float4 xo = op.a[nt][mt], g = op.g[nt];
+          const float4 xv = make_float4(xo.x + v[0], xo.y + v[1], xo.z + v[2], xo.w + v[3]);
+          if (row < Mw) *(float4*)(e.x + (size_t)(t0w + row) * e.ld + (nb0 + nt) * 16 + nq) = xv;
+          uint32_t h0, l0, h1, l1;
+          split2(g.x * xv.x, g.y * xv.y, h0, l0);
+          split2(g.z * xv.z, g.w * xv.w, h1, l1);
+          *(uint2*)(stg + row * 64 + nt * 16 + nq) = make_uint2(h0, h1);
+          lo[nt][mt] = make_uint2(l0, l1);
+          sq[mt] += (xv.x * xv.x + xv.y * xv.y) + (xv.z * xv.z + xv.w * xv.w);
+        }
+      }
+      uint16_t* xn = (uint16_t*)e.xn;
+      const int c = lane & 7;
+#pragma unroll
+      for (int pl = 0; pl < 2; ++pl) {
+        if (pl) {
+#pragma unroll
+          for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+            for (int nt = 0; nt < NT; ++nt) *(uint2*)(stg + (mt * 16 + (lane & 15)) * 64 + nt * 16 + nq) = lo[nt][mt];
+        }
+        asm volatile("" ::: "memory");  // a wave's LDS accesses run in order: its reads see all its lanes' writes
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+          const int row = k * 8 + (lane >> 3);
+          const uint4 v = *(const uint4*)(stg + row * 64 + c * 8);
+          if (row < Mw) *(uint4*)(xn + (pl ? e.xn_plane : 0) + (size_t)(t0w + row) * e.ld + nb0 * 16 + c * 8) = v;
+        }
+        asm volatile("" ::: "memory");  // the lo plane's writes stay behind the hi plane's reads
+      }
+    }
   } else if (Mw > 0) {
     EpiOps<NT, 4> op;
     epi_block_starts<NT, 4>(e, Mw, t0w, lane, op);
