@@ -982,6 +982,72 @@ __device__ __forceinline__ void t8_epilogue(const GemmKArgs& a, int fb, int r0, 
         asm volatile("" ::: "memory");  // the lo plane's writes stay behind the hi plane's reads
       }
     }
+  } else if (e.kind == EPI_QKV && nb0 * 16 < e.Hq * e.D && (e.D & 63) == 0) {
+    // query features (a wave's 64 features lie in one head: rotary pairs j0 ..
+    // j0 + 31 and their partners j0 + D/2 ..): the rotated values, 4 bytes a
+    // lane and plane before, go through the wave's 8 KiB of the free ring
+    // buffer one plane at a time, [64 tokens][dims j0 .. j0 + 31, then
+    // j0 + D/2 ..], and come back as the 8 dims of one tiled-q lane chunk
+    // (16 bytes) a lane
+    if (Mw > 0) {
+      EpiOps<NT, 4> op;
+      epi_block_starts<NT, 4>(e, Mw, t0w, lane, op);
+      epi_load<NT, 4>(e, nb0, a.N, Mw, t0w, lane, op);
+      const int D = e.D, half = D >> 1;
+      const int n0 = nb0 * 16, head = n0 / D, j0 = (n0 - head * D) >> 1;
+      const int g = e.Hq / e.Hkv, hkv = head / g, hg = head - hkv * g;
+      uint16_t* stg = stg_all + w * 4096;
+      const int nq = 4 * (lane >> 4);
+      uint2 lo[NT][4];  // lo planes of (j, j + 1) and (j + D/2, j + 1 + D/2), for the second pass
+#pragma unroll
+      for (int mt = 0; mt < 4; ++mt) {
+        const int row = mt * 16 + (lane & 15);
+        const float r = rscale[wm * 64 + row];
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) {
+          const floatx4 v = acc[nt][mt];
+          const float4 cs = op.a[nt][mt];
+          const float x0 = v[0] * r, y0 = v[1] * r, x1 = v[2] * r, y1 = v[3] * r;
+          const float a0 = x0 * cs.x - y0 * cs.y, c0 = y0 * cs.x + x0 * cs.y;
+          const float a1 = x1 * cs.z - y1 * cs.w, c1 = y1 * cs.z + x1 * cs.w;
+          uint32_t h0, l0, h1, l1;
+          split2(a0, a1, h0, l0);
+          split2(c0, c1, h1, l1);
+          const int jj = nt * 8 + nq / 2;  // pair offset from j0 (even)
+          *(uint32_t*)(stg + row * 64 + jj) = h0;
+          *(uint32_t*)(stg + row * 64 + 32 + jj) = h1;
+          lo[nt][mt] = make_uint2(l0, l1);
+        }
+      }
+      uint16_t* qb = (uint16_t*)e.q;
+      const int c = lane & 7;
+      const int col = c < 4 ? j0 + c * 8 : j0 + half + (c - 4) * 8;
+#pragma unroll
+      for (int pl = 0; pl < 2; ++pl) {
+        if (pl) {
+#pragma unroll
+          for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+            for (int nt = 0; nt < NT; ++nt) {
+              const int row = mt * 16 + (lane & 15), jj = nt * 8 + nq / 2;
+              *(uint32_t*)(stg + row * 64 + jj) = lo[nt][mt].x;
+              *(uint32_t*)(stg + row * 64 + 32 + jj) = lo[nt][mt].y;
+            }
+        }
+        asm volatile("" ::: "memory");  // a wave's LDS accesses run in order: its reads see all its lanes' writes
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+          const int row = k * 8 + (lane >> 3);
+          const uint4 v = *(const uint4*)(stg + row * 64 + c * 8);
+          if (row < Mw) {
+            const int t = t0w + row, b = t / e.Kblk, kk = t - b * e.Kblk;
+            const size_t base = ((size_t)b * e.Hkv + hkv) * (size_t)e.qrows_pad * D;
+            *(uint4*)(qb + (pl ? e.q_plane : 0) + base + tile16x32_index(hg * e.Kblk + kk, col, D)) = v;
+          }
+        }
+        asm volatile("" ::: "memory");  // the lo plane's writes stay behind the hi plane's reads
+      }
+    }
   } else if (Mw > 0) {
     EpiOps<NT, 4> op;
     epi_block_starts<NT, 4>(e, Mw, t0w, lane, op);
