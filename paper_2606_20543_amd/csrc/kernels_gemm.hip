@@ -721,7 +721,50 @@ __global__ __launch_bounds__(256, 2) void gemm_tile_kernel(GemmKArgs a) {
   }
 
   float sq[4] = {0.f, 0.f, 0.f, 0.f};
-  if (Mw > 0) {
+  if (NT == 2 && e.kind == EPI_RESID) {
+    // the new residual x stored in place (16 bytes a lane); both planes of
+    // g * x (8 bytes a lane and plane) go through the wave's NT x 4 KiB of the
+    // stage buffers and come back as 16 bytes of one row a lane: NT x 32
+    // contiguous bytes per row and plane (64-feature tiles only: with 128
+    // features the registers this takes spill inside the K loop)
+    __syncthreads();  // every wave is done with the stage buffers
+    if (Mw > 0) {
+      EpiOps<NT, 4> op;
+      epi_load<NT, 4>(e, nb0, a.N, Mw, t0w, lane, op);
+      constexpr int RL = NT * 16;  // features of a wave row
+      uint16_t* stg = &xs[0][0] + w * (2 * 64 * RL);  // [plane][64 rows][RL]
+      const int nq = 4 * (lane >> 4);
+#pragma unroll
+      for (int mt = 0; mt < 4; ++mt) {
+        const int row = mt * 16 + (lane & 15);
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) {
+          const floatx4 v = acc[nt][mt];
+          const float4 xo = op.a[nt][mt], g = op.g[nt];
+          const float4 xv = make_float4(xo.x + v[0], xo.y + v[1], xo.z + v[2], xo.w + v[3]);
+          if (row < Mw) *(float4*)(e.x + (size_t)(t0w + row) * e.ld + (nb0 + nt) * 16 + nq) = xv;
+          uint32_t h0, l0, h1, l1;
+          split2(g.x * xv.x, g.y * xv.y, h0, l0);
+          split2(g.z * xv.z, g.w * xv.w, h1, l1);
+          *(uint2*)(stg + row * RL + nt * 16 + nq) = make_uint2(h0, h1);
+          *(uint2*)(stg + 64 * RL + row * RL + nt * 16 + nq) = make_uint2(l0, l1);
+          sq[mt] += (xv.x * xv.x + xv.y * xv.y) + (xv.z * xv.z + xv.w * xv.w);
+        }
+      }
+      asm volatile("" ::: "memory");  // a wave's LDS accesses run in order: its reads see all its lanes' writes
+      uint16_t* xn = (uint16_t*)e.xn;
+      constexpr int CH = RL / 8, RPI = 64 / CH;  // 16-byte chunks per row, rows per instruction
+      const int c = lane % CH;
+#pragma unroll
+      for (int pl = 0; pl < 2; ++pl)
+#pragma unroll
+        for (int k = 0; k < 64 / RPI; ++k) {
+          const int row = k * RPI + lane / CH;
+          const uint4 v = *(const uint4*)(stg + pl * 64 * RL + row * RL + c * 8);
+          if (row < Mw) *(uint4*)(xn + (pl ? e.xn_plane : 0) + (size_t)(t0w + row) * e.ld + nb0 * 16 + c * 8) = v;
+        }
+    }
+  } else if (Mw > 0) {
     EpiOps<NT, 4> op;
     epi_block_starts<NT, 4>(e, Mw, t0w, lane, op);
     epi_load<NT, 4>(e, nb0, a.N, Mw, t0w, lane, op);
