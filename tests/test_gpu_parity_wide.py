@@ -26,6 +26,8 @@ stays within seconds.  Cases:
       the 32x32 workload), 2 rounds + commit
   8B width, batch 8, 256-token prompt, one 128-token block (M = 1024: the
       passes that carry a commit; gate/up as whole tiles plus a K-split tail)
+  8B width, batch 8, 40-token blocks (M = 320: blocks not aligned to the
+      16-row groups of the tiled epilogues, a half-full last row tile)
   8B width, batch 2, a 40-token block at context 600..640: 160 query rows per
       (sequence, KV head), so the query-split attention runs one full 128-row
       group and one of 32 rows whose other 96 are padding
@@ -118,6 +120,13 @@ def test_8b_width_batch8_block128(pair8):
     whole tiles in three full rounds and the last 16 feature blocks K-split in
     a second launch, the output layer on 1024 tiles."""
     _greedy_block(pair8, W8, B=8, P=256, K=128, rounds=1, keep=0.6, seed_stream=22)
+
+
+def test_8b_width_batch8_block40(pair8):
+    """320 rows of 40-token blocks: the eight-wave tiles' query and residual
+    epilogues where a block starts mid-way through a 16-row group and the
+    last 128-row tile is half full (its second row half has no rows)."""
+    _greedy_block(pair8, W8, B=8, P=256, K=40, rounds=1, keep=0.6, seed_stream=24)
 
 
 def test_8b_width_context_4352(pair8):
