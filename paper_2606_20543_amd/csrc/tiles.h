@@ -662,18 +662,19 @@ __device__ __forceinline__ void attend_block(const KVTile<D>& t, int key0, const
   after_scores();
 #pragma unroll
   for (int qt = 0; qt < QPW; ++qt) {
-    float sv[8];
-    float tmax = -INFINITY;  // this lane's largest score of the block
+    float sv[8];              // raw scores (masked ones -inf)
+    float tmax = -INFINITY;  // this lane's largest score of the block, then in log2 units
 #pragma unroll
     for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         const int key = key0 + kt * 16 + 4 * grp + e;
-        float v = s[kt][qt][e] * scale_log2;
+        float v = s[kt][qt][e];
         if constexpr (MASK) v = (key <= qpos[qt] && key < klim) ? v : -INFINITY;
         sv[kt * 4 + e] = v;
         tmax = fmaxf(tmax, v);
       }
+    tmax *= scale_log2;  // the scale is positive: the largest scaled score
     // The reference m moves only when a score exceeds it by more than
     // AT_LAZY_LOG2, so the probabilities lie in [0, 2^AT_LAZY_LOG2]; O and l
     // share the reference, so O / l is the same.  Each lane tests its own
@@ -697,8 +698,8 @@ __device__ __forceinline__ void attend_block(const KVTile<D>& t, int key0, const
 #pragma unroll
     for (int i = 0; i < 8; i += 2) {
       // exponents are <= AT_LAZY_LOG2 (exp2 of -inf is 0): the hardware exp2 needs no range handling
-      const float p0 = __builtin_amdgcn_exp2f(sv[i] - m[qt]);
-      const float p1 = __builtin_amdgcn_exp2f(sv[i + 1] - m[qt]);
+      const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(sv[i], scale_log2, -m[qt]));
+      const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(sv[i + 1], scale_log2, -m[qt]));
       ps += p0;
       ps += p1;
       uint32_t h, lo;
