@@ -924,6 +924,12 @@ __device__ __forceinline__ void t8_kloop(const GemmKArgs& a, int fb, int r0, int
   }
 }
 
+// x * sigmoid(x) from the hardware exp2 and reciprocal (each within about
+// one ulp; the limits 0 and x hold for large |x|)
+__device__ __forceinline__ float silu_hw(float x) {
+  return x * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(x * -1.44269504088896341f));
+}
+
 // Epilogue of the tile (fb, rows r0 ..) from its sums; stg: a free ring
 // buffer (64 KiB).  Every thread of the workgroup calls it (one barrier for
 // the residual's row sums).
@@ -955,9 +961,8 @@ __device__ __forceinline__ void t8_epilogue(const GemmKArgs& a, int fb, int r0, 
         for (int nt = 0; nt < NT; ++nt) {
           const floatx4 v = acc[nt][mt];
           const float g0 = v[0] * r, u0 = v[1] * r, g1 = v[2] * r, u1 = v[3] * r;
-          const float s0 = g0 / (1.0f + expf(-g0)), s1 = g1 / (1.0f + expf(-g1));
           uint32_t hi, lo;
-          split2(s0 * u0, s1 * u1, hi, lo);
+          split2(silu_hw(g0) * u0, silu_hw(g1) * u1, hi, lo);
           *(uint32_t*)(stg + row * 32 + nt * 8 + 2 * q) = hi;
           *(uint32_t*)(stg + 2048 + row * 32 + nt * 8 + 2 * q) = lo;
         }
