@@ -1060,20 +1060,33 @@ __device__ __forceinline__ int attn_unit(const AttnKArgs& a, int item, float* sm
     sm_l[r] = L;
   }
   __syncthreads();
-  // weighted sum of the chunk partials in chunk order; the slots' loads of
-  // four chunks are in flight together
+  // weighted sum of the chunk partials in chunk order: a batch of a chunk's
+  // loads is issued together, and only then weighted and summed (loads
+  // interleaved with their uses were each waited for alone, one round trip
+  // per load)
   const floatx4* G = (const floatx4*)(a.opart + gbase * ROWS * D);
   floatx4 v[NV];
 #pragma unroll
   for (int i = 0; i < NV; ++i) v[i] = floatx4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll 4
+  constexpr int NB = NV < 8 ? NV : 8;  // loads in flight together (more spill registers here)
+  static_assert(NV % NB == 0, "whole batches");
   for (int cc = 0; cc < nch; ++cc) {
 #pragma unroll
-    for (int i = 0; i < NV; ++i) {
-      const int idx = threadIdx.x + NTH * i;
-      const int ic = idx < NOUT ? idx : NOUT - 1;
-      const float4 g4 = PMem::ldf4(G, ((size_t)cc * NOUT + ic) * 16);
-      v[i] += floatx4{g4.x, g4.y, g4.z, g4.w} * cl[cc * ROWS + ic / (D / 4)];
+    for (int i0 = 0; i0 < NV; i0 += NB) {
+      float4 g4[NB];
+#pragma unroll
+      for (int j = 0; j < NB; ++j) {
+        const int idx = threadIdx.x + NTH * (i0 + j);
+        const int ic = idx < NOUT ? idx : NOUT - 1;
+        g4[j] = PMem::ldf4(G, ((size_t)cc * NOUT + ic) * 16);
+      }
+      __builtin_amdgcn_sched_barrier(0);  // the batch's loads go out before its first use
+#pragma unroll
+      for (int j = 0; j < NB; ++j) {
+        const int idx = threadIdx.x + NTH * (i0 + j);
+        const int ic = idx < NOUT ? idx : NOUT - 1;
+        v[i0 + j] += floatx4{g4[j].x, g4[j].y, g4[j].z, g4[j].w} * cl[cc * ROWS + ic / (D / 4)];
+      }
     }
   }
 #pragma unroll
