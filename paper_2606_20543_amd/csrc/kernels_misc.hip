@@ -170,8 +170,7 @@ __device__ int block_argmax(const float* row, int V, SelShared& sh) {
   float bv = -INFINITY;
   int bi = 0x7fffffff;
   if ((V & 3) == 0 && (((uintptr_t)row) & 15) == 0) {
-    for (int v = threadIdx.x * 4; v < V; v += NT_SEL * 4) {
-      const float4 x = *(const float4*)(row + v);
+    auto take = [&](const float4 x, int v) {
       if (x.x > bv || bi == 0x7fffffff) {
         bv = x.x;
         bi = v;
@@ -188,7 +187,19 @@ __device__ int block_argmax(const float* row, int V, SelShared& sh) {
         bv = x.w;
         bi = v + 3;
       }
+    };
+    // eight loads in flight, then taken in order (a load used right away is
+    // waited for alone)
+    constexpr int UB = 8, STR = NT_SEL * 4;
+    int v = threadIdx.x * 4;
+    for (; v + (UB - 1) * STR < V; v += UB * STR) {
+      float4 x[UB];
+#pragma unroll
+      for (int u = 0; u < UB; ++u) x[u] = *(const float4*)(row + v + u * STR);
+#pragma unroll
+      for (int u = 0; u < UB; ++u) take(x[u], v + u * STR);
     }
+    for (; v < V; v += STR) take(*(const float4*)(row + v), v);
   } else {
     for (int v = threadIdx.x; v < V; v += NT_SEL) {
       const float x = row[v];
