@@ -1074,19 +1074,17 @@ __device__ __forceinline__ int attn_unit(const AttnKArgs& a, int item, float* sm
 #pragma unroll
     for (int i0 = 0; i0 < NV; i0 += NB) {
       float4 g4[NB];
+      float wt[NB];
 #pragma unroll
       for (int j = 0; j < NB; ++j) {
         const int idx = threadIdx.x + NTH * (i0 + j);
         const int ic = idx < NOUT ? idx : NOUT - 1;
         g4[j] = PMem::ldf4(G, ((size_t)cc * NOUT + ic) * 16);
+        wt[j] = cl[cc * ROWS + ic / (D / 4)];
       }
-      __builtin_amdgcn_sched_barrier(0);  // the batch's loads go out before its first use
+      __builtin_amdgcn_sched_barrier(0);  // the batch's loads and weight reads go out before their first use
 #pragma unroll
-      for (int j = 0; j < NB; ++j) {
-        const int idx = threadIdx.x + NTH * (i0 + j);
-        const int ic = idx < NOUT ? idx : NOUT - 1;
-        v[i0 + j] += floatx4{g4[j].x, g4[j].y, g4[j].z, g4[j].w} * cl[cc * ROWS + ic / (D / 4)];
-      }
+      for (int j = 0; j < NB; ++j) v[i0 + j] += floatx4{g4[j].x, g4[j].y, g4[j].z, g4[j].w} * wt[j];
     }
   }
 #pragma unroll
