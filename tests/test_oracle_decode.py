@@ -93,8 +93,62 @@ def test_verify_keeps_frontier_commit_advances():
     assert np.array_equal(s.carry, logits[:, -1])
     # the carry equals a fresh forward's prediction at the last committed position
     full = np.concatenate([pre, blk + U.TINY_GQA.img_lo], axis=1)
-    lf, _ = M.forward_nocache(mod, full)
+    lf, hf = M.forward_nocache(mod, full)
     assert np.allclose(s.carry, lf[:, -1], rtol=0, atol=1e-12)
+    # and the carried state is that position's pre-norm state (the one that scored the carry)
+    assert np.allclose(s.h_carry, hf[:, -1], rtol=0, atol=1e-12)
+
+
+def test_verify_uniforms_at_absolute_positions():
+    """Rule (B) at block position k of sequence b takes the sampling uniform of
+    the counter (b, f + k, round, stream 1): the raster position, not the
+    block offset, so that blocks starting elsewhere draw other numbers."""
+    mod = _setup()
+    pre = synth.prompt(U.TINY_GQA, 2, 4)
+    s = Dc.prefill(mod, pre, 4 + 12)
+    blk0 = synth.random_codes(U.TINY_GQA, (2, 4))
+    Dc.commit(s, blk0)
+    blk = synth.random_codes(U.TINY_GQA, (2, 5))
+    seed, rnd = 11, 3
+    carry = s.carry.copy()
+    new, _, _, logits = Dc.verify_round(s, blk, 0, R.RULE_SAMPLE, rnd, seed)
+    for b in range(2):
+        for k in range(5):
+            L = carry[b] if k == 0 else logits[b, k - 1]
+            u1 = R.uniform(seed, b, 8 + k, rnd, 1)
+            assert new[b, k] == R.invcdf(R.warp(L), u1), (b, k)
+    # rule (C) against a point-mass draft keeps t exactly when the accept
+    # uniform of stream 0 at (b, f + k, round) lies below p(t); the drafts are
+    # the greedy continuation and the temperatures low, so p(t) spreads over
+    # (0, 1) and both outcomes occur
+    ar = Dc.ar_decode(mod, np.concatenate([pre, blk0 + U.TINY_GQA.img_lo], axis=1), 5)
+    seen = set()
+    for T in (0.005, 0.01, 0.02, 0.05):
+        s2 = Dc.prefill(mod, pre, 4 + 12)
+        Dc.commit(s2, blk0)
+        carry = s2.carry.copy()
+        _, acc, _, logits = Dc.verify_round(s2, ar, 0, R.RULE_ACCEPT_REJECT, rnd, seed, T)
+        for b in range(2):
+            for k in range(5):
+                L = carry[b] if k == 0 else logits[b, k - 1]
+                u0 = R.uniform(seed, b, 8 + k, rnd, 0)
+                assert acc[b, k] == (u0 < R.warp(L, T)[ar[b, k]]), (T, b, k)
+                seen.add(bool(acc[b, k]))
+    assert seen == {True, False}
+
+
+def test_first_token_uses_stream_two():
+    """The first image token (no draft) is a plain sample of the prefill's
+    last logits with the uniform of counter (b, P, round 0, stream 2)."""
+    mod = _setup()
+    P = 4
+    pre = synth.prompt(U.TINY_GQA, 2, P)
+    carry = Dc.prefill(mod, pre, P + 9).carry
+    drafts = synth.random_codes(U.TINY_GQA, (2, 3, 3))
+    seed = 5
+    out, _ = Dc.decode_image(mod, pre, 3, 3, drafts, rule=R.RULE_SAMPLE, seed=seed)
+    for b in range(2):
+        assert out[b, 0, 0] == R.invcdf(R.warp(carry[b]), R.uniform(seed, b, P, 0, 2))
 
 
 def test_rule_c_same_reference_accepts_everything():

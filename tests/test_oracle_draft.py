@@ -141,3 +141,20 @@ def test_argmax_ties_go_to_the_lowest_code():
     idx, lg = Dr.draft(model, hb, rng.normal(size=(5, d)), rng.integers(0, SHAPE.vocab, size=5))
     assert np.all(lg == lg[:, :1])
     assert np.all(idx == 0)
+
+
+def test_head_norm_epsilon_closed_form():
+    """The head's RMSNorm adds the backbone's epsilon inside the root: with
+    W0 = [I | 0], gain 1 and W1 = W3 = W2 = I, an input state of constant
+    entries c with c^2 = eps normalizes to 1/sqrt(2) in every entry, so
+    h_hat = c + silu(1/sqrt(2)) / sqrt(2)."""
+    d = m = 8
+    eps = 1e-5
+    eye = _eye_bits(d, d, 0)
+    head = Dr.Head(d, m, _head_bits(d, m, w0=_eye_bits(d, 2 * d, 0), g=np.full(d, ONE), w1=eye, w3=eye, w2=eye))
+    c = np.sqrt(eps)
+    h = np.full((1, d), c)
+    e = np.random.default_rng(0).normal(size=(1, d))
+    n = 1.0 / np.sqrt(2.0)
+    want = c + n * n / (1.0 + np.exp(-n))
+    assert np.allclose(Dr.f_phi(head, h, e, eps), want, rtol=1e-13, atol=0)

@@ -189,3 +189,34 @@ def test_first_token_sampling():
     assert R.sample_first(R.RULE_GREEDY, L, 0.9) == 1
     assert R.sample_first(R.RULE_SAMPLE, L, 0.0) == 0
     assert R.sample_first(R.RULE_ACCEPT_REJECT, L, 0.9999) == 2
+
+
+def test_accept_is_strict_on_the_uniform_grid():
+    """Keep the draft with probability alpha exactly: over the 2^24-point grid
+    of uniforms, u < alpha holds for ceil(alpha * 2^24) of them, so a draft the
+    backbone gives zero probability (alpha = 0) is never kept, even at u = 0,
+    and one it gives at least q's mass (alpha = 1) always is."""
+    L = np.array([2.0, 1.0, -1.0, 0.5])
+    # t = 2 lies outside the top 2 codes: p(t) = 0 against a point-mass draft
+    a, ok, repl = R.select_position(R.RULE_ACCEPT_REJECT, L, 2, None, 0.0, 0.25, 1.0, 2)
+    assert not ok and repl and a != 2
+    # q equal to p: alpha = 1 at the largest grid value
+    a, ok, repl = R.select_position(R.RULE_ACCEPT_REJECT, L, 0, L.copy(), 1.0 - 2.0 ** -24, 0.25)
+    assert ok and a == 0 and not repl
+
+
+def test_counter_fields_do_not_overlap():
+    """The counter packs (sequence, position, round, stream) into disjoint bit
+    fields over their whole stated ranges: changing any one field at its
+    lowest or highest value gives a different counter from changing any other."""
+    hi = {"b": (1 << 20) - 1, "pos": (1 << 24) - 1, "rnd": (1 << 16) - 1, "stream": 15}
+    seen = {}
+    for f, top in hi.items():
+        for v in (1, top, 1 << (top.bit_length() - 1)):
+            args = {"b": 0, "pos": 0, "rnd": 0, "stream": 0}
+            args[f] = v
+            c = R.counter(**args)
+            assert c not in seen, (f, v, seen.get(c))
+            seen[c] = (f, v)
+    # every field set to its highest value fills exactly 64 bits
+    assert R.counter(**hi) == (1 << 64) - 1

@@ -47,3 +47,19 @@ def test_rounds_strictly_increase():
     ops = S.plan(48, 48, k_v=2, b=5, i=4)
     rnds = [o[4] for o in ops if o[0] == "verify"]
     assert rnds == list(range(len(rnds)))
+
+
+def test_staged_plan_worked_example():
+    """A 4 x 2 grid with groups of three rows, b = 2 joint rounds and i = 1
+    incremental round (Sec. 4 "SSD Configuration"; Appendix "Multi-Row
+    Anticipation Ablations"), written out by hand: row 0's last token as one
+    horizontal run behind the fixed first token, then the b rounds over all
+    three rows of the group, the leading row committed, one round over the
+    two rows still open, the next row committed, one round over the last."""
+    assert S.plan(4, 2, k_h=5, h_rounds=1, k_v=3, b=2, i=1) == [
+        ("prefill",), ("first",),
+        ("draft_h", 0, 1), ("verify", 0, 2, 1, 0), ("commit", 0, 2),
+        ("draft_v", 0, 3), ("verify", 2, 6, 0, 1), ("verify", 2, 6, 0, 2), ("commit", 2, 2),
+        ("verify", 4, 4, 0, 3), ("commit", 4, 2),
+        ("verify", 6, 2, 0, 4), ("commit", 6, 2),
+    ]
