@@ -121,7 +121,7 @@ struct GemmKArgs {
   int ld_in;
   int M, t0;
   int xcd;
-  int fb0;  // eight-wave tiles: feature block of the launch's first (its partials and counters count from it)
+  int ft0;  // eight-wave tiles: first 16-feature tile of the launch (its partials and counters count from its first tile)
   float* part;
   unsigned* counters;
   EpiArgs epi;
@@ -801,8 +801,11 @@ __global__ __launch_bounds__(256, 2) void gemm_tile_kernel(GemmKArgs a) {
 // reads are one conflict-free ds_read_b128 per fragment.  The reads are
 // issued as separate instructions with their own waits, so that the
 // compiler does not make them wait for every LDS DMA copy in flight.
-constexpr int T8_STAGES = 2, T8_THREADS = 512, T8_NT = 4;
-constexpr int T8_STAGE_BYTES = 2 * TILE_PL * 2 + 32 * 1024;  // one stage: both token planes, then 32 weight tiles
+// A narrower variant (NT = 3: waves of 64 x 48, tiles of 128 x 192, 24 weight
+// tiles a stage in the same ring) fills grids that the 256-feature tiles
+// leave part empty.
+constexpr int T8_STAGES = 2, T8_THREADS = 512;
+constexpr int T8_STAGE_BYTES = 2 * TILE_PL * 2 + 32 * 1024;  // one stage: both token planes, then up to 32 weight tiles
 
 // the eight token operand fragments of one k-block at addr: [mt * 2 + plane],
 // row tiles 16 rows (2 KiB) apart, the planes TILE_PL elements apart
@@ -819,14 +822,15 @@ __device__ __forceinline__ void ds_read_tiles2(u32x4 (&x)[8], uint32_t addr) {
 }
 
 // K loop of one tile segment: stages st0 .. st0 + nst - 1 of the 128 token
-// rows from r0 against feature block fb, summed into acc.  pro() runs once
-// the first stage's copies are in flight (the tile's 1/rms, whose LDS
-// scratch is the ring's second buffer); on return every wave is past the
-// last stage's barrier, so the buffer of stage nst is free.
-template <class Pro>
-__device__ __forceinline__ void t8_kloop(const GemmKArgs& a, int fb, int r0, int st0, int nst, uint16_t* xs,
-                                         floatx4 (&acc)[T8_NT][4], Pro&& pro) {
-  constexpr int NT = T8_NT;
+// rows from r0 against the 64 NT features from 16-feature tile ft, summed
+// into acc.  pro() runs once the first stage's copies are in flight (the
+// tile's 1/rms, whose LDS scratch is the ring's second buffer); on return
+// every wave is past the last stage's barrier, so the buffer of stage nst is
+// free.
+template <int NT, class Pro>
+__device__ __forceinline__ void t8_kloop(const GemmKArgs& a, int ft, int r0, int st0, int nst, uint16_t* xs,
+                                         floatx4 (&acc)[NT][4], Pro&& pro) {
+  static_assert(NT == 3 || NT == 4, "waves of 48 or 64 features");
   const int tid = threadIdx.x, lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
   const int wm = w & 1, wn = w >> 1;
@@ -856,12 +860,12 @@ __device__ __forceinline__ void t8_kloop(const GemmKArgs& a, int fb, int r0, int
       const int i = w * 4 + j, pl = i >> 4, rb = i & 15;
       dma16(pl ? xl : xh, dst + pl * TILE_PL + rb * 512, xoff[j], (st0 + stage) * TILE_KT * 2);
     }
-    // the stage's 32 weight tiles (16 feature tiles x 2 k-blocks), four per wave
+    // the stage's 8 NT weight tiles (4 NT feature tiles x 2 k-blocks), NT per wave
     const int kb0 = (st0 + stage) * TILE_KT / 32;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int i = w * 4 + j, ft = i >> 1, kb = i & 1;
-      dma16(wr, dst + 2 * TILE_PL + i * 512, lane * 16, ((fb * 16 + ft) * a.KB + kb0 + kb) * 1024);
+    for (int j = 0; j < NT; ++j) {
+      const int i = w * NT + j, f = i >> 1, kb = i & 1;
+      dma16(wr, dst + 2 * TILE_PL + i * 512, lane * 16, ((ft + f) * a.KB + kb0 + kb) * 1024);
     }
   };
   // operand reads: row wm * 64 + lane % 16 (+ 16 mt), logical chunk kb * 4 +
@@ -873,23 +877,23 @@ __device__ __forceinline__ void t8_kloop(const GemmKArgs& a, int fb, int r0, int
     xrd[kb] = xs0 + (uint32_t)(((wm * 64 + (lane & 15)) * TILE_LD +
                                 (((kb * 4 + (lane >> 4)) ^ ((lane & 15) >> 1)) * 8)) * 2);
   // weight tile (f, kb) of the stage sits at (2 f + kb) KiB after its token
-  // planes; this wave's feature tiles are f = 4 wn .. 4 wn + 3
-  const uint32_t wrd = xs0 + (uint32_t)(2 * TILE_PL * 2 + wn * 8 * 1024 + lane * 16);
+  // planes; this wave's feature tiles are f = NT wn .. NT wn + NT - 1
+  const uint32_t wrd = xs0 + (uint32_t)(2 * TILE_PL * 2 + wn * NT * 2048 + lane * 16);
   auto mma = [&](int stage) {
     const uint32_t so = (uint32_t)((stage % T8_STAGES) * T8_STAGE_BYTES);
-    u32x4 x0[8], x1[8], b0[4], b1[4];  // token [mt * 2 + plane] and weight [nt] fragments of k-blocks 0 and 1
+    u32x4 x0[8], x1[8], b0[NT], b1[NT];  // token [mt * 2 + plane] and weight [nt] fragments of k-blocks 0 and 1
     ds_read_tiles2(x0, xrd[0] + so);
     b0[0] = ds_read16_at<0>(wrd + so);
     b0[1] = ds_read16_at<2048>(wrd + so);
     b0[2] = ds_read16_at<4096>(wrd + so);
-    b0[3] = ds_read16_at<6144>(wrd + so);
+    if constexpr (NT == 4) b0[NT - 1] = ds_read16_at<6144>(wrd + so);
     ds_read_tiles2(x1, xrd[1] + so);
     b1[0] = ds_read16_at<1024>(wrd + so);
     b1[1] = ds_read16_at<3072>(wrd + so);
     b1[2] = ds_read16_at<5120>(wrd + so);
-    b1[3] = ds_read16_at<7168>(wrd + so);
-    lgkm_wait<12>(x0);
-    lgkm_wait<12>(b0);
+    if constexpr (NT == 4) b1[NT - 1] = ds_read16_at<7168>(wrd + so);
+    lgkm_wait<8 + NT>(x0);  // k-block 0's reads done, k-block 1's (8 + NT) may be outstanding
+    lgkm_wait<8 + NT>(b0);
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt)
 #pragma unroll
@@ -933,13 +937,13 @@ __device__ __forceinline__ float silu_hw(float x) {
 // Epilogue of the tile (fb, rows r0 ..) from its sums; stg: a free ring
 // buffer (64 KiB).  Every thread of the workgroup calls it (one barrier for
 // the residual's row sums).
-__device__ __forceinline__ void t8_epilogue(const GemmKArgs& a, int fb, int r0, const floatx4 (&acc)[T8_NT][4],
+template <int NT>
+__device__ __forceinline__ void t8_epilogue(const GemmKArgs& a, int fb, int ft, int r0, const floatx4 (&acc)[NT][4],
                                             const float* rscale, float (*sq_red)[TILE_ROWS], uint16_t* stg_all) {
-  constexpr int NT = T8_NT;
   const int tid = threadIdx.x, lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = w & 1, wn = w >> 1;
-  const int nb0 = fb * 4 * NT + wn * NT;  // first 16-feature tile of this wave
+  const int nb0 = ft + wn * NT;  // first 16-feature tile of this wave
   const int t0w = a.t0 + r0 + wm * 64;
   const int Mw = a.M - r0 - wm * 64 < 64 ? a.M - r0 - wm * 64 : 64;
   const int Mt = a.M - r0 < TILE_ROWS ? a.M - r0 : TILE_ROWS;
@@ -975,7 +979,7 @@ __device__ __forceinline__ void t8_epilogue(const GemmKArgs& a, int fb, int r0, 
         const int row = k * 16 + (lane >> 2);
         const uint4 hi = *(const uint4*)(stg + row * 32 + c * 8);
         const uint4 lo = *(const uint4*)(stg + 2048 + row * 32 + c * 8);
-        if (row < Mw) {
+        if (row < Mw && c < NT) {  // a wave's 8 NT outputs of a row are NT chunks
           const size_t i = (size_t)(t0w + row) * e.ld + nb0 * 8 + c * 8;
           *(uint4*)(h + i) = hi;
           *(uint4*)(h + e.h_plane + i) = lo;
@@ -1025,12 +1029,13 @@ __device__ __forceinline__ void t8_epilogue(const GemmKArgs& a, int fb, int r0, 
         for (int k = 0; k < 8; ++k) {
           const int row = k * 8 + (lane >> 3);
           const uint4 v = *(const uint4*)(stg + row * 64 + c * 8);
-          if (row < Mw) *(uint4*)(xn + (pl ? e.xn_plane : 0) + (size_t)(t0w + row) * e.ld + nb0 * 16 + c * 8) = v;
+          if (row < Mw && c < 2 * NT)
+            *(uint4*)(xn + (pl ? e.xn_plane : 0) + (size_t)(t0w + row) * e.ld + nb0 * 16 + c * 8) = v;
         }
         asm volatile("" ::: "memory");  // the lo plane's writes stay behind the hi plane's reads
       }
     }
-  } else if (e.kind == EPI_QKV && nb0 * 16 < e.Hq * e.D && (e.D & 63) == 0) {
+  } else if (NT == 4 && e.kind == EPI_QKV && nb0 * 16 < e.Hq * e.D && (e.D & 63) == 0) {
     // query features (a wave's 64 features lie in one head: rotary pairs j0 ..
     // j0 + 31 and their partners j0 + D/2 ..): the rotated values, 4 bytes a
     // lane and plane before, go through the wave's 8 KiB of the free ring
@@ -1129,10 +1134,13 @@ __device__ __forceinline__ void t8_rms(const GemmKArgs& a, int r0, float* scratc
 }
 
 // One workgroup per output tile and K split (grid of xcd_grid(n_fb,
-// m_tiles * S)): the splits' sums meet in the last arrival.
+// m_tiles * S)): the splits' sums meet in the last arrival.  Feature block fb
+// of the launch covers the 4 NT 16-feature tiles from a.ft0 + 4 NT fb; its
+// per-row x^2 part (residual epilogue) is number ft / (4 NT), which counts
+// the blocks of the whole projection when every launch of it has one width.
+template <int NT>
 __global__ __launch_bounds__(T8_THREADS) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void gemm_tile8_kernel(GemmKArgs a) {
-  constexpr int NT = T8_NT;
   __shared__ __attribute__((aligned(16))) uint16_t xs[T8_STAGES * T8_STAGE_BYTES / 2];
   __shared__ float rscale[TILE_ROWS];
   __shared__ float sq_red[4][TILE_ROWS];
@@ -1147,9 +1155,10 @@ void gemm_tile8_kernel(GemmKArgs a) {
   const int r0 = mtile * TILE_ROWS;
   const int nst = a.K / TILE_KT / a.S;
 
+  const int ft = a.ft0 + fb * 4 * NT;  // the tile's first 16-feature tile
   floatx4 acc[NT][4];
-  t8_kloop(a, fb + a.fb0, r0, split * nst, nst, xs, acc,
-           [&] { t8_rms(a, r0, (float*)(void*)(xs + T8_STAGE_BYTES / 2), rscale); });
+  t8_kloop<NT>(a, ft, r0, split * nst, nst, xs, acc,
+               [&] { t8_rms(a, r0, (float*)(void*)(xs + T8_STAGE_BYTES / 2), rscale); });
 
   if (a.S > 1) {
     // split-K: publish this split's fragments; the last arrival of the tile
@@ -1188,7 +1197,7 @@ void gemm_tile8_kernel(GemmKArgs a) {
     }
     if (tid == 0) a.counters[grp] = 0u;
   }
-  t8_epilogue(a, fb + a.fb0, r0, acc, rscale, sq_red, xs + (size_t)(nst % T8_STAGES) * (T8_STAGE_BYTES / 2));
+  t8_epilogue<NT>(a, ft / (4 * NT), ft, r0, acc, rscale, sq_red, xs + (size_t)(nst % T8_STAGES) * (T8_STAGE_BYTES / 2));
 }
 
 // the 128 x 256 LDS-DMA tiles where they apply (SSD_GEMM_T8=0 keeps every
@@ -1200,6 +1209,14 @@ static bool tile8_enabled() {
   }();
   return on;
 }
+// the 128 x 192 tiles where they fill a grid better (SSD_GEMM_T8N=0: never)
+static bool tile8_narrow_enabled() {
+  static const bool on = [] {
+    const char* v = std::getenv("SSD_GEMM_T8N");
+    return !(v && std::strcmp(v, "0") == 0);
+  }();
+  return on;
+}
 
 GemmPlan gemm_plan_bf16(int M, int N, int K, int xcd) {
   GemmPlan p;
@@ -1207,6 +1224,7 @@ GemmPlan gemm_plan_bf16(int M, int N, int K, int xcd) {
   p.tile = 0;
   p.tail_fb = 0;
   p.tail_S = 1;
+  p.tail_nt = 0;
   if (M > 64 && K % (2 * TILE_KT) == 0 && N % 256 == 0 && (size_t)N * K * 2 < (1ull << 31) && tile8_enabled()) {
     // 128 x 256 tiles, eight waves, both operands by LDS DMA, one workgroup
     // per CU: K split by the largest divisor of the stage count that keeps
@@ -1222,7 +1240,7 @@ GemmPlan gemm_plan_bf16(int M, int N, int K, int xcd) {
       if (nst % s == 0 && (long)nfb * mt * s <= 256) S = s;
     if (nst / S >= 32) {
       p.tile = 3;
-      p.NT = T8_NT;
+      p.NT = 4;
       p.MT = TILE_ROWS / 16;
       p.WV = T8_THREADS / 64;
       p.bn = 256;
@@ -1232,19 +1250,47 @@ GemmPlan gemm_plan_bf16(int M, int N, int K, int xcd) {
       p.KCB = TILE_KT / 32;
       p.kchunks = nst / S;
       p.depth = T8_STAGES;  // ring stages
+      // 128 x 192 tiles (waves of 64 x 48) where the 256-feature grid leaves
+      // CUs idle and the narrower one fills more of them with no more stages
+      // per workgroup (8B QKV: 96 tiles in two splits on 192 CUs at 512 rows,
+      // 128 in two splits on all 256 instead).  Only where N > K, which keeps
+      // them off the residual projections (N = d, K >= d), whose per-row x^2
+      // parts count 256-feature blocks.
+      const bool narrow = tile8_narrow_enabled() && N > K;
+      if (narrow && N % 192 == 0) {
+        const int nfb3 = N / 192;
+        int S3 = 0;
+        for (int s = 1; s <= 16; ++s)
+          if (nst % s == 0 && (long)nfb3 * mt * s <= 256 && nst / s >= 32) S3 = s;
+        if (S3 && nst / S3 <= nst / S && (long)nfb3 * mt * S3 > (long)nfb * mt * S) {
+          p.NT = 3;
+          p.bn = 192;
+          p.n_fb = nfb3;
+          p.S = S3;
+          p.kchunks = nst / S3;
+          return p;
+        }
+      }
       // whole tiles in as many full rounds of 256 as there are, the feature
       // blocks left over K-split so that they fill the last round, where
       // that saves the busiest CU a quarter of a round and more (8B gate/up
-      // at 1024 rows: 768 tiles, then 128 in two splits of 32 stages)
+      // at 1024 rows: 768 tiles, then 128 in two splits of 32 stages); where
+      // no split fits, as 128 x 192 tiles if those fill more of the round
+      // (8B gate/up at 512 rows: 256 tiles, then 192 of 256 features as 256
+      // of 192)
       const long tiles = (long)nfb * mt, full = tiles / 256;
       if (S == 1 && full >= 1 && tiles % 256 && (256 * full) % mt == 0) {
         const int fb_a = (int)(256 * full / mt), r = (nfb - fb_a) * mt;
         int st = 1;
         for (int s = 2; s <= 16; ++s)
           if (nst % s == 0 && (long)r * s <= 256 && nst / s >= 16) st = s;
+        const int fr = (nfb - fb_a) * 256;
         if (st > 1 && nst / st + nst / 8 <= nst * 3 / 4) {
           p.tail_fb = fb_a;
           p.tail_S = st;
+        } else if (narrow && fr % 192 == 0 && (long)(fr / 192) * mt <= 256 && (long)(fr / 192) * mt > r) {
+          p.tail_fb = fb_a;
+          p.tail_nt = 3;
         }
       }
       return p;
@@ -1394,7 +1440,7 @@ GemmPlan gemm_plan_bf16(int M, int N, int K, int xcd) {
 }
 
 size_t gemm_partials_floats(const GemmPlan& p, int M) {
-  if (p.tile && p.tail_fb) return (size_t)p.tail_S * (p.n_fb - p.tail_fb) * p.m_tiles * TILE_ROWS * p.bn;
+  if (p.tile && p.tail_fb) return p.tail_nt ? 0 : (size_t)p.tail_S * (p.n_fb - p.tail_fb) * p.m_tiles * TILE_ROWS * p.bn;
   if (p.S <= 1) return 0;
   if (p.tile) return (size_t)p.S * p.m_tiles * TILE_ROWS * p.n_fb * p.bn;
   (void)M;
@@ -1452,14 +1498,21 @@ void gemm_bf16(const GemmPlan& p, const void* Wpacked, int N, int K, const void*
         // whole tiles of the first feature blocks, then the rest K-split
         const int mt = (a.M + TILE_ROWS - 1) / TILE_ROWS;
         a.n_fb = p.tail_fb;
-        launch_timed(gemm_tile8_kernel, dim3(xcd_grid(a.n_fb, mt, p.xcd)), dim3(T8_THREADS), st, a);
-        a.fb0 = p.tail_fb;
-        a.n_fb = p.n_fb - p.tail_fb;
-        a.S = p.tail_S;
-        a.kchunks = K / TILE_KT / p.tail_S;
-        launch_timed(gemm_tile8_kernel, dim3(xcd_grid(a.n_fb, mt * a.S, p.xcd)), dim3(T8_THREADS), st, a);
-      } else if (p.tile == 3)
-        launch_timed(gemm_tile8_kernel, grid, dim3(T8_THREADS), st, a);
+        launch_timed(gemm_tile8_kernel<4>, dim3(xcd_grid(a.n_fb, mt, p.xcd)), dim3(T8_THREADS), st, a);
+        a.ft0 = p.tail_fb * 16;
+        if (p.tail_nt == 3) {
+          a.n_fb = (N - p.tail_fb * 256) / 192;
+          launch_timed(gemm_tile8_kernel<3>, dim3(xcd_grid(a.n_fb, mt, p.xcd)), dim3(T8_THREADS), st, a);
+        } else {
+          a.n_fb = p.n_fb - p.tail_fb;
+          a.S = p.tail_S;
+          a.kchunks = K / TILE_KT / p.tail_S;
+          launch_timed(gemm_tile8_kernel<4>, dim3(xcd_grid(a.n_fb, mt * a.S, p.xcd)), dim3(T8_THREADS), st, a);
+        }
+      } else if (p.tile == 3 && p.NT == 3)
+        launch_timed(gemm_tile8_kernel<3>, grid, dim3(T8_THREADS), st, a);
+      else if (p.tile == 3)
+        launch_timed(gemm_tile8_kernel<4>, grid, dim3(T8_THREADS), st, a);
       else if (p.NT == 4)
         launch_timed(gemm_tile_kernel<4, 3>, grid, dim3(256), st, a);
       else if (p.depth == 4)
@@ -1472,7 +1525,7 @@ void gemm_bf16(const GemmPlan& p, const void* Wpacked, int N, int K, const void*
   const int MP = p.MT * 16;
   for (int t0 = 0; t0 < M; t0 += MP) {
     GemmKArgs a;
-    a.fb0 = 0;
+    a.ft0 = 0;
     a.W = (const u32x4*)Wpacked;
     a.N = N;
     a.K = K;

@@ -129,10 +129,11 @@ struct GemmPlan {
   int depth;        // tiled: register stages of the K pipeline (2 or 4)
   int tail_fb;      // tile 3, > 0: feature blocks [0, tail_fb) in one launch of whole tiles, the rest
   int tail_S;       //   in a second launch with K split tail_S ways (a last round that would run part empty)
+  int tail_nt;      //   3: the rest as whole 128 x 192 tiles instead (tail_S 1), else 0
 };
 // split-K arrival counters a plan uses (tiled plans: one per output tile, when split)
 inline int gemm_counters(const GemmPlan& p) {
-  if (p.tile && p.tail_fb) return (p.n_fb - p.tail_fb) * p.m_tiles;
+  if (p.tile && p.tail_fb) return p.tail_nt ? 0 : (p.n_fb - p.tail_fb) * p.m_tiles;
   return p.tile ? (p.S > 1 ? p.n_fb * p.m_tiles : 0) : p.n_fb;
 }
 // Row counts that cover every plan class: up to 16, 32 and 64 rows, 65..128

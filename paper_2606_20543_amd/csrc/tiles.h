@@ -116,14 +116,16 @@ template <int N, int R>
 __device__ __forceinline__ void lgkm_wait(u32x4 (&r)[R]) {
 #if defined(__HIP_DEVICE_COMPILE__)
   static_assert(N >= 0 && N < 16, "lgkmcnt range");
-  if constexpr (R == 4)
+  if constexpr (R == 3)
+    asm volatile("s_waitcnt lgkmcnt(%3)" : "+v"(r[0]), "+v"(r[1]), "+v"(r[2]) : "n"(N));
+  else if constexpr (R == 4)
     asm volatile("s_waitcnt lgkmcnt(%4)" : "+v"(r[0]), "+v"(r[1]), "+v"(r[2]), "+v"(r[3]) : "n"(N));
   else if constexpr (R == 8)
     asm volatile("s_waitcnt lgkmcnt(%8)"
                  : "+v"(r[0]), "+v"(r[1]), "+v"(r[2]), "+v"(r[3]), "+v"(r[4]), "+v"(r[5]), "+v"(r[6]), "+v"(r[7])
                  : "n"(N));
   else
-    static_assert(R == 4 || R == 8, "register groups of 4 or 8");
+    static_assert(R == 3 || R == 4 || R == 8, "register groups of 3, 4 or 8");
 #else
   (void)r;
 #endif

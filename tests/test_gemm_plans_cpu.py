@@ -21,7 +21,7 @@ import synth
 
 class GemmPlan(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int) for n in ("MT", "NT", "KCB", "WV", "S", "n_fb", "kchunks", "bn", "xcd", "tile",
-                                            "m_tiles", "depth", "tail_fb", "tail_S")]
+                                            "m_tiles", "depth", "tail_fb", "tail_S", "tail_nt")]
 
 
 TILE_ROWS, TILE_KT = 128, 64
@@ -43,7 +43,7 @@ def planner():
 def counters(p):
     """Arrival counters a plan uses (split-K reductions)."""
     if p.tile and p.tail_fb:
-        return (p.n_fb - p.tail_fb) * p.m_tiles
+        return 0 if p.tail_nt else (p.n_fb - p.tail_fb) * p.m_tiles
     if p.tile:
         return p.n_fb * p.m_tiles if p.S > 1 else 0
     return p.n_fb
@@ -74,20 +74,32 @@ def test_plans_tile_their_problem(planner, model):
             where = f"M={M} N={N} K={K}"
             assert p.S >= 1 and p.n_fb >= 1, where
             if p.tile == 3:
-                # 128 x 256 tiles of eight waves: K split within 256 workgroups, >= 32 stages each
+                # 128 x 256 (or 128 x 192) tiles of eight waves: K split within 256 workgroups, >= 32 stages each
                 assert M > 64, where
-                assert p.NT == 4 and p.bn == 256 and p.n_fb * 256 == N and p.WV == 8, where
+                assert p.NT in (3, 4) and p.bn == 64 * p.NT and p.n_fb * p.bn == N and p.WV == 8, where
                 assert p.m_tiles == (M + TILE_ROWS - 1) // TILE_ROWS, where
                 assert p.kchunks * p.S * TILE_KT == K and p.kchunks >= 32, where
                 assert p.S == 1 or p.n_fb * p.m_tiles * p.S <= 256, where
+                if p.NT == 3:
+                    # only where the 256-feature grid would leave CUs idle, and never on a residual projection
+                    assert N > K and p.n_fb * p.m_tiles * p.S <= 256 and not p.tail_fb, where
+                    assert (N // 256) * p.m_tiles * p.S < p.n_fb * p.m_tiles * p.S, where
                 if p.tail_fb:
-                    # whole rounds of 256 tiles, then the remaining feature blocks K-split within one more
-                    assert p.S == 1 and 0 < p.tail_fb < p.n_fb and (p.tail_fb * p.m_tiles) % 256 == 0, where
+                    # whole rounds of 256 tiles, then the remaining feature blocks K-split within one more,
+                    # or as 128 x 192 tiles in one more
+                    assert p.S == 1 and p.NT == 4 and 0 < p.tail_fb < p.n_fb, where
+                    assert (p.tail_fb * p.m_tiles) % 256 == 0, where
                     r = (p.n_fb - p.tail_fb) * p.m_tiles
-                    assert 0 < r < 256 and r * p.tail_S <= 256 and p.tail_S > 1, where
-                    assert (K // TILE_KT) % p.tail_S == 0 and K // TILE_KT // p.tail_S >= 16, where
+                    assert 0 < r < 256, where
+                    if p.tail_nt:
+                        fr = (p.n_fb - p.tail_fb) * 256
+                        assert p.tail_nt == 3 and p.tail_S == 1 and N > K and fr % 192 == 0, where
+                        assert r < (fr // 192) * p.m_tiles <= 256, where
+                    else:
+                        assert r * p.tail_S <= 256 and p.tail_S > 1, where
+                        assert (K // TILE_KT) % p.tail_S == 0 and K // TILE_KT // p.tail_S >= 16, where
                 else:
-                    assert p.tail_S == 1, where
+                    assert p.tail_S == 1 and p.tail_nt == 0, where
             elif p.tile:
                 assert M > 64, where
                 assert p.NT in (2, 4) and p.bn == 32 * p.NT and p.n_fb * p.bn == N, where
@@ -127,22 +139,26 @@ def test_tiled_plan_choices(planner):
     keeps at least 32 stages after the K split (at most 256 workgroups), else
     128-feature tiles (three weight stages) where they make at least 160
     workgroups, 64-feature tiles with four pipeline stages otherwise, K split
-    until the grid reaches 256 workgroups; streaming launches up to 64 rows."""
+    until the grid reaches 256 workgroups; 128 x 192 eight-wave tiles where
+    the 256-feature grid leaves CUs idle; streaming launches up to 64 rows."""
     plan, _ = planner
     m = synth.M8B
-    gu = plan(512, 2 * m.d_ff, m.d_model)  # 112 x 4 = 448 tiles of 128 x 256
-    assert (gu.tile, gu.bn, gu.S) == (3, 256, 1)
+    gu = plan(512, 2 * m.d_ff, m.d_model)  # 112 x 4 = 448 tiles of 128 x 256: 256, then 192 as 256 of 128 x 192
+    assert (gu.tile, gu.bn, gu.S, gu.tail_fb, gu.tail_nt, gu.tail_S) == (3, 256, 1, 64, 3, 1)
     lm = plan(512, m.v_img, m.d_model)  # 128 x 4 = 512
     assert (lm.tile, lm.S) == (3, 1)
     dn = plan(512, m.d_model, m.d_ff)  # 16 x 4 tiles, 224 stages in 4 splits of 56
     assert (dn.tile, dn.S, dn.kchunks) == (3, 4, 56)
-    qkv = plan(512, (m.n_heads + 2 * m.n_kv_heads) * m.head_dim, m.d_model)  # 24 x 4, 2 splits of 32 stages
-    assert (qkv.tile, qkv.S, qkv.kchunks) == (3, 2, 32)
+    nq = (m.n_heads + 2 * m.n_kv_heads) * m.head_dim
+    qkv = plan(512, nq, m.d_model)  # 32 x 4 tiles of 128 x 192 in 2 splits of 32 stages (24 x 4 x 2 of 256: 192 CUs)
+    assert (qkv.tile, qkv.NT, qkv.bn, qkv.S, qkv.kchunks) == (3, 3, 192, 2, 32)
+    qkv1k = plan(1024, nq, m.d_model)  # 32 x 8 tiles of 128 x 192, no split
+    assert (qkv1k.tile, qkv1k.NT, qkv1k.S) == (3, 3, 1)
     o = plan(512, m.d_model, m.n_heads * m.head_dim)  # 16 x 4 x 4 splits would leave 16 stages: 128 x 128
     assert (o.tile, o.NT, o.S, o.depth) == (1, 2, 1, 4)
     gu1k = plan(1024, 2 * m.d_ff, m.d_model)  # 896 tiles: 768 in three full rounds, 128 in two splits of 32
-    assert (gu1k.tile, gu1k.S, gu1k.tail_fb, gu1k.tail_S) == (3, 1, 96, 2)
-    assert (gu.tail_fb, lm.tail_fb) == (0, 0)  # 192 tiles left at 512 rows: no split fits them into 256
+    assert (gu1k.tile, gu1k.S, gu1k.tail_fb, gu1k.tail_S, gu1k.tail_nt) == (3, 1, 96, 2, 0)
+    assert lm.tail_fb == 0 and (lm.NT, dn.NT) == (4, 4)  # two whole rounds; a residual projection
     o1 = plan(256, synth.M1B.d_model, synth.M1B.d_model)  # 32 x 2 tiles of 64 features: 4 splits
     assert (o1.tile, o1.NT, o1.S) == (1, 2, 4)
     for M in (1, 24, 48, 64):

@@ -111,12 +111,15 @@ def test_7b_width_row_block(pair7):
 
 
 def test_8b_width_gqa_batch8(pair8):
+    """512 rows, the 64x64 workload's verify passes: QKV as 128 x 192 tiles in
+    two K splits, gate/up as 256 whole tiles of 128 x 256 and then the last
+    48 feature blocks as 256 tiles of 128 x 192, down K-split in four."""
     _greedy_block(pair8, W8, B=8, P=256, K=64, rounds=1, keep=0.6, seed_stream=12)
 
 
 def test_8b_width_batch8_block128(pair8):
     """1024 rows per pass, the size of the 64x64 workload's passes that carry a
-    commit: QKV on 192 whole tiles, O and down K-split in two, gate/up as 768
+    commit: QKV on 256 whole tiles of 128 x 192, O and down K-split in two, gate/up as 768
     whole tiles in three full rounds and the last 16 feature blocks K-split in
     a second launch, the output layer on 1024 tiles."""
     _greedy_block(pair8, W8, B=8, P=256, K=128, rounds=1, keep=0.6, seed_stream=22)
@@ -193,6 +196,12 @@ def test_8b_width_ragged_query_split(pair8):
     """The query-split attention with a partial query group (rows past K*g masked
     and never stored) and short key chunks."""
     _greedy_block(pair8, W8, B=2, P=600, K=40, rounds=1, keep=0.6, seed_stream=21)
+
+
+def test_7b_width_batch4_block64(pair7):
+    """256 rows at the 7B widths: QKV (12288 features) as 64 x 2 tiles of
+    128 x 192 in two K splits instead of 48 x 2 of 128 x 256."""
+    _greedy_block(pair7, W7, B=4, P=128, K=64, rounds=1, keep=0.6, seed_stream=25)
 
 
 def test_7b_width_context_1152(pair7):
