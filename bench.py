@@ -632,7 +632,7 @@ def main():
     if t_ms >= s_ms and t_ms > 0:
         tf = t_fl / (t_ms / 1e3) / 1e12
         roofline = {"bound": "mfma", "kernel": "gemm_tile8_kernel + gemm_tile_kernel (the tiled GEMMs of the many-row "
-                    "passes: QKV, gate/up, down and the output layer on 128 x 256 tiles, O on 128 x 64)",
+                    "passes: gate/up, down and the output layer on 128 x 256 tiles, QKV and the last part of gate/up on 128 x 192, O on 128 x 64)",
                     "achieved": tf, "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s", "frac": tf / MFMA_BF16_PEAK_TFLOPS,
                     "traffic": measured_traffic("tiled", wl.name), "traffic_unit": "HBM bytes per launch",
                     "launches": t_n, "ms_per_launch": t_ms / max(t_n, 1), "flops_per_launch": t_fl / max(t_n, 1),
