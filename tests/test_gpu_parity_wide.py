@@ -125,6 +125,12 @@ def test_8b_width_batch8_block128(pair8):
     _greedy_block(pair8, W8, B=8, P=256, K=128, rounds=1, keep=0.6, seed_stream=22)
 
 
+def test_8b_width_batch7_block64(pair8):
+    """448 rows: gate/up's second launch of 128 x 192 tiles over a last
+    row tile of 64 rows, and QKV's 128 x 192 tiles in two K splits over it."""
+    _greedy_block(pair8, W8, B=7, P=256, K=64, rounds=1, keep=0.6, seed_stream=26)
+
+
 def test_8b_width_batch8_block40(pair8):
     """320 rows of 40-token blocks: the eight-wave tiles' query and residual
     epilogues where a block starts mid-way through a 16-row group and the
