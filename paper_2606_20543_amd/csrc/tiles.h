@@ -377,23 +377,49 @@ __device__ __forceinline__ void rms_finish(const EpiArgs& e, const float (&v)[Rm
   }
 }
 
-// per-token 1/rms(x) for large token tiles (parts in blocks of 16 through LDS)
+// sum of parts p0 .. p0 + Q - 1 (those below the part count) of one row, in
+// part order, NB loads in flight at a time
+template <int NB>
+__device__ __forceinline__ float rms_part_sum(const EpiArgs& e, size_t c, int p0, int Q) {
+  float s = 0.f;
+  for (int b0 = 0; b0 < Q; b0 += NB) {
+    float v[NB];
+#pragma unroll
+    for (int j = 0; j < NB; ++j) {
+      const int p = p0 + b0 + j;
+      v[j] = e.ssq[(size_t)(p < e.ssq_parts ? p : 0) * e.ssq_ld + c];
+    }
+#pragma unroll
+    for (int j = 0; j < NB; ++j)
+      if (b0 + j < Q && p0 + b0 + j < e.ssq_parts) s += v[j];
+  }
+  return s;
+}
+
+// per-token 1/rms(x) for large token tiles: the NTH / MP thread groups each
+// take a contiguous range of the parts of every row, issue their loads
+// together (in batches of 16 where a range is longer: 64 parts over four
+// groups are one batch), sum them in part order, and the group sums meet in
+// LDS, summed in group order (deterministic).  red: NTH floats of LDS.
 template <int MP, int NTH = 256>
 __device__ __forceinline__ void rms_prologue(const EpiArgs& e, int M, int t0, float (*red)[MP], float* rscale) {
-  float s = 0.f;
-  for (int p0 = 0; p0 < e.ssq_parts; p0 += 16) {
-    for (int i = threadIdx.x; i < 16 * MP; i += NTH) {
-      const int p = p0 + i / MP, t = i % MP;
-      red[i / MP][t] = (p < e.ssq_parts && t < M)
-                           ? e.ssq[(size_t)p * e.ssq_ld + (size_t)e.ssq_off + (size_t)(t0 + t) * e.ssq_step]
-                           : 0.f;
-    }
-    lds_barrier();
-    if (threadIdx.x < MP)
-      for (int p = 0; p < 16; ++p) s += red[p][threadIdx.x];
-    lds_barrier();
+  constexpr int G = NTH / MP;
+  static_assert(G >= 1 && G * MP == NTH, "whole row groups");
+  const int t = threadIdx.x % MP, g = threadIdx.x / MP;
+  const int tc = t < M ? t : M - 1;
+  const int Q = (e.ssq_parts + G - 1) / G;
+  const size_t c = (size_t)e.ssq_off + (size_t)(t0 + tc) * e.ssq_step;
+  const float s = Q <= 4 ? rms_part_sum<4>(e, c, g * Q, Q) : Q <= 8 ? rms_part_sum<8>(e, c, g * Q, Q)
+                                                                     : rms_part_sum<16>(e, c, g * Q, Q);
+  red[g][t] = s;
+  lds_barrier();
+  if (threadIdx.x < MP) {
+    float a = 0.f;
+#pragma unroll
+    for (int q = 0; q < G; ++q) a += red[q][threadIdx.x];
+    rscale[threadIdx.x] = 1.0f / sqrtf(a * e.inv_d + e.eps);
   }
-  if (threadIdx.x < MP) rscale[threadIdx.x] = 1.0f / sqrtf(s * e.inv_d + e.eps);
+  lds_barrier();  // the scratch is free again
 }
 
 // ---- fused epilogue, bf16 path ----
