@@ -138,6 +138,18 @@ def test_8b_width_batch8_block40(pair8):
     _greedy_block(pair8, W8, B=8, P=256, K=40, rounds=1, keep=0.6, seed_stream=24)
 
 
+def test_8b_width_batch8_single_token(pair8):
+    """Eight rows of one token each, the passes of greedy AR decoding and of
+    the planting run: the weight-streaming GEMMs at the 8B widths and the
+    one-query-per-sequence attention under GQA 4."""
+    _greedy_block(pair8, W8, B=8, P=600, K=1, rounds=1, keep=0.6, seed_stream=27)
+
+
+def test_7b_width_single_token(pair7):
+    """One token at the 7B widths: the AR step of the strict decode's baseline."""
+    _greedy_block(pair7, W7, B=1, P=300, K=1, rounds=1, keep=0.6, seed_stream=28)
+
+
 def test_8b_width_context_4352(pair8):
     """The 64x64 workload's last row: keys 0..4351 in the split-KV attention."""
     B, P, K = 1, 4288, 64
