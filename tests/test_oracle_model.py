@@ -262,3 +262,24 @@ def test_bf16_round_ties_to_even():
     assert M.bf16_round(np.array([one + 1.5 * ulp]))[0] == one + 2 * ulp
     assert M.bf16_round(np.array([one + 0.51 * ulp]))[0] == one + ulp
     assert M.bf16_round(np.array([-3.0]))[0] == -3.0
+
+
+def test_batch_rows_at_different_frontiers():
+    """Rows of one batched block at different positions: each row's queries and
+    keys are rotated at its own positions and see its own context only, so
+    each row's logits and states equal a no-cache recompute of that row's own
+    sequence (here row 1's block overwrites the last two slots of its prefix)."""
+    buf, _ = _fresh()
+    mod = U.model(F32, buf)
+    rng = np.random.default_rng(9)
+    pre = rng.integers(0, F32.vocab, size=(2, 4))
+    blk = rng.integers(0, F32.vocab, size=(2, 3))
+    c = M.Cache(mod.cfg, 2, 8)
+    M.forward(mod, c, pre, np.array([0, 0]))
+    starts = np.array([4, 2])
+    l, h = M.forward(mod, c, blk, starts)
+    for b in range(2):
+        seq = np.concatenate([pre[b, :starts[b]], blk[b]])[None, :]
+        lf, hf = M.forward_nocache(mod, seq)
+        assert np.allclose(l[b], lf[0, -3:], rtol=0, atol=1e-12), b
+        assert np.allclose(h[b], hf[0, -3:], rtol=0, atol=1e-12), b
