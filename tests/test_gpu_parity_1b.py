@@ -76,7 +76,7 @@ def test_1b_b4_accept_reject_topk(pair):
         blk = drafts.copy()
         refs_state = q.astype(np.float64)
         gnew, out = _check_round(sess, os_, blk, 0, R.RULE_ACCEPT_REJECT, 0, top_k, q, stats, K)
-        # the flips of round 1 are as many as the realized logit errors make likely
+        # the flips of the first verify round are as many as the realized logit errors make likely
         assert stats["flips"] <= G.flips_expected_bound(stats["flips_expected"]), stats
         # second round: GPU uses its stored references; the oracle gets the same
         # (accepted: the draft q; rejected: the first round's GPU scoring logits)
@@ -109,7 +109,7 @@ def test_1b_b4_accept_reject_topk(pair):
         ol3, _ = Dc.commit(os_, g2)
         assert np.abs(out3["logits"] - ol3).max() < TOL
         assert list(out3["frontier"]) == [P + K] * B
-        # end-to-end round 2: every difference must be explained by the logit error,
+        # end to end, second verify round: every difference must be explained by the logit error,
         # and there are no more of them than the realized errors make likely
         exp2 = 0.0
         for b in range(B):
